@@ -1,0 +1,259 @@
+"""Pins of the oracle's tensor product, convolution and backward.
+
+Each check compares against something the oracle's own formula does not
+produce: a brute-force dense contraction, an explicit per-edge loop, float64
+autograd of the forward, central finite differences, rotation/inversion
+symmetry, and the trilinear (Euler) identity.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cg, conv, graph, irreps, sh, tp, wigner
+
+
+def _unit(rng, n):
+    g = rng.standard_normal((n, 3))
+    return g / np.linalg.norm(g, axis=1, keepdims=True)
+
+
+def _small_graph(rng, n=9, e=40, pad=-1):
+    snd = rng.integers(0, n, e)
+    rcv = rng.integers(0, n, e)
+    rcv = np.where(rcv == snd, (rcv + 1) % n, rcv)
+    vec = rng.standard_normal((e, 3)) * 1.7
+    return snd.astype(np.int32), rcv.astype(np.int32), vec
+
+
+LAYS = [("2x0e+2x1o", 2, 2), ("3x0e+3x1o+3x2e", 3, 3), ("2x0e+2x1o+2x2e+2x3o", 3, 3),
+        ("2x1e+2x0o", 2, 1)]
+
+
+@pytest.mark.parametrize("spec", LAYS)
+def test_tp_equals_dense_bruteforce(spec):
+    lay = irreps.layout(*spec)
+    rng = np.random.default_rng(10)
+    R, C = 7, lay.channels
+    x = rng.standard_normal((R, lay.d_in, C))
+    y = sh.sh_unit(lay.lmax_sh, _unit(rng, R))
+    w = rng.standard_normal((R, lay.n_paths, C))
+    T = cg.dense_tensor(lay)                                   # [D_out, D_in, D_sh]
+    i3 = np.array(lay.i3())
+    ref = np.einsum("oij,riq,rj->roq", T, x, y) * w[:, i3, :]
+    got = tp.tp(lay, x, y, w).numpy()
+    assert np.abs(got - ref).max() < 1e-13
+
+
+def test_tp_scalar_path_and_bilinearity():
+    lay = irreps.layout("2x0e+2x1o+2x2e", 3, 3)
+    rng = np.random.default_rng(11)
+    R, C = 5, 2
+    x = rng.standard_normal((R, lay.d_in, C))
+    y = sh.sh_unit(3, _unit(rng, R))
+    w = rng.standard_normal((R, lay.n_paths, C))
+    z = tp.tp(lay, x, y, w).numpy()
+    for p in lay.paths:
+        if p.l1 == 0:   # 0 x l2 -> l2 is the identity coupling: z = w x_0 Y_l2
+            ref = w[:, p.k, None, :] * x[:, p.x_off, None, :] * y[:, p.y_off:p.y_off + 2 * p.l2 + 1, None]
+            assert np.abs(z[:, p.out_off:p.out_off + 2 * p.l3 + 1] - ref).max() < 1e-14
+    x2 = rng.standard_normal(x.shape)
+    a, b = 0.7, -1.3
+    lhs = tp.tp(lay, a * x + b * x2, y, w).numpy()
+    rhs = a * z + b * tp.tp(lay, x2, y, w).numpy()
+    assert np.abs(lhs - rhs).max() < 1e-12
+
+
+def _rot_features(lay, x, R, out=False):
+    """Apply the block-diagonal Wigner-D to the feature axis."""
+    x = np.array(x, copy=True)
+    if not out:
+        for b, off in zip(lay.blocks, _x_offsets(lay)):
+            D = wigner.wigner_d(b.l, R)
+            x[:, off:off + 2 * b.l + 1] = np.einsum("ij,njq->niq", D, x[:, off:off + 2 * b.l + 1])
+    else:
+        for p in lay.paths:
+            D = wigner.wigner_d(p.l3, R)
+            sl = slice(p.out_off, p.out_off + 2 * p.l3 + 1)
+            x[:, sl] = np.einsum("ij,njq->niq", D, x[:, sl])
+    return x
+
+
+def _x_offsets(lay):
+    offs, o = [], 0
+    for b in lay.blocks:
+        offs.append(o)
+        o += 2 * b.l + 1
+    return offs
+
+
+def test_tp_equivariance():
+    lay = irreps.layout("2x0e+2x1o+2x2e+2x3o", 3, 3)
+    rng = np.random.default_rng(12)
+    R = wigner.random_rotation(rng)
+    n, C = 6, 2
+    x = rng.standard_normal((n, lay.d_in, C))
+    u = _unit(rng, n)
+    w = rng.standard_normal((n, lay.n_paths, C))
+    z = tp.tp(lay, x, sh.sh_unit(3, u), w).numpy()
+    zr = tp.tp(lay, _rot_features(lay, x, R), sh.sh_unit(3, u @ R.T), w).numpy()
+    assert np.abs(zr - _rot_features(lay, z, R, out=True)).max() < 1e-11
+
+
+def _conv_loop(lay, x, vec, s, snd, rcv, n, pad=-1):
+    """Materialise every edge message, then scatter with np.add.at."""
+    y = sh.sh_vec(lay.lmax_sh, vec)
+    T = cg.dense_tensor(lay)
+    i3 = np.array(lay.i3())
+    out = np.zeros((n, lay.d_out, x.shape[2]))
+    for e in range(snd.shape[0]):
+        if pad >= 0 and (snd[e] == pad or rcv[e] == pad):
+            continue
+        msg = np.einsum("oij,iq,j->oq", T, x[snd[e]], y[e]) * s[e][i3]
+        np.add.at(out, rcv[e], msg)
+    return out
+
+
+@pytest.mark.parametrize("pad", [-1, 3])
+def test_conv_equals_materialised_messages(pad):
+    lay = irreps.layout("2x0e+2x1o+2x2e", 2, 2)
+    rng = np.random.default_rng(13)
+    n = 9
+    snd, rcv, vec = _small_graph(rng, n, 50)
+    x = rng.standard_normal((n, lay.d_in, 2))
+    s = rng.standard_normal((50, lay.n_paths, 2))
+    ref = _conv_loop(lay, x, vec, s, snd, rcv, n, pad)
+    got = conv.conv_fwd(lay, x, vec, s, snd, rcv, n, pad_node=pad, chunk=7).numpy()
+    assert np.abs(got - ref).max() < 1e-12
+    # a subset of receivers gives the same rows
+    sub = np.array([5, 0, 8])
+    part = conv.conv_fwd(lay, x, vec, s, snd, rcv, n, pad_node=pad, receivers=sub).numpy()
+    assert np.abs(part - ref[sub]).max() < 1e-12
+    if pad >= 0:
+        assert np.abs(got[pad]).max() == 0.0
+
+
+def test_conv_one_in_edge_equals_tp_and_permutation():
+    lay = irreps.layout("2x0e+2x1o+2x2e", 3, 3)
+    rng = np.random.default_rng(14)
+    n = 6
+    snd = np.array([3, 4, 5, 0, 1, 2], dtype=np.int32)
+    rcv = np.arange(n, dtype=np.int32)
+    vec = rng.standard_normal((n, 3))
+    x = rng.standard_normal((n, lay.d_in, 2))
+    s = rng.standard_normal((n, lay.n_paths, 2))
+    m = conv.conv_fwd(lay, x, vec, s, snd, rcv, n).numpy()
+    z = tp.tp(lay, x[snd], sh.sh_vec(3, vec), s).numpy()
+    assert np.abs(m - z).max() < 1e-13
+    # permuting the edge list changes nothing (beyond rounding)
+    snd2, rcv2, vec2 = _small_graph(rng, n, 30)
+    s2 = rng.standard_normal((30, lay.n_paths, 2))
+    perm = rng.permutation(30)
+    a = conv.conv_fwd(lay, x, vec2, s2, snd2, rcv2, n).numpy()
+    b = conv.conv_fwd(lay, x, vec2[perm], s2[perm], snd2[perm], rcv2[perm], n).numpy()
+    assert np.abs(a - b).max() < 1e-12
+
+
+def test_conv_equivariance_and_inversion():
+    lay = irreps.layout("2x0e+2x1o+2x2e+2x3o", 3, 3)
+    rng = np.random.default_rng(15)
+    n = 8
+    snd, rcv, vec = _small_graph(rng, n, 40)
+    x = rng.standard_normal((n, lay.d_in, 2))
+    s = rng.standard_normal((40, lay.n_paths, 2))
+    m = conv.conv_fwd(lay, x, vec, s, snd, rcv, n).numpy()
+    R = wigner.random_rotation(rng)
+    mr = conv.conv_fwd(lay, _rot_features(lay, x, R), vec @ R.T, s, snd, rcv, n).numpy()
+    assert np.abs(mr - _rot_features(lay, m, R, out=True)).max() < 1e-11
+    # inversion: r -> -r, x block of parity p -> p x; output block -> p3 * block
+    xi = np.array(x)
+    for b, off in zip(lay.blocks, _x_offsets(lay)):
+        xi[:, off:off + 2 * b.l + 1] *= b.p
+    mi = conv.conv_fwd(lay, xi, -vec, s, snd, rcv, n).numpy()
+    for p in lay.paths:
+        sl = slice(p.out_off, p.out_off + 2 * p.l3 + 1)
+        assert np.abs(mi[:, sl] - p.p3 * m[:, sl]).max() < 1e-12
+
+
+@pytest.mark.parametrize("pad", [-1, 2])
+def test_conv_bwd_against_autograd(pad):
+    lay = irreps.layout("2x0e+2x1o+2x2e", 3, 3)
+    rng = np.random.default_rng(16)
+    n, E, C = 7, 35, 3
+    snd, rcv, vec = _small_graph(rng, n, E)
+    x = torch.tensor(rng.standard_normal((n, lay.d_in, C)), requires_grad=True)
+    v = torch.tensor(vec, requires_grad=True)
+    s = torch.tensor(rng.standard_normal((E, lay.n_paths, C)), requires_grad=True)
+    dm = torch.tensor(rng.standard_normal((n, lay.d_out, C)))
+    m = conv.conv_fwd(lay, x, v, s, snd, rcv, n, pad_node=pad)
+    gx, gv, gs = torch.autograd.grad(m, (x, v, s), grad_outputs=dm)
+    out = conv.conv_bwd(lay, x.detach(), vec, s.detach(), dm, snd, rcv, n, pad_node=pad)
+    assert torch.abs(out["dx"] - gx).max() < 1e-12
+    assert torch.abs(out["ds"] - gs).max() < 1e-12
+    assert torch.abs(out["dvec"] - gv).max() < 1e-11
+    # dy against autograd through the harmonics-given forward
+    y = sh.sh_vec(3, torch.tensor(vec)).detach().requires_grad_(True)
+    m2 = conv.conv_fwd_from_y(lay, x.detach(), y, s.detach(), snd, rcv, n, pad_node=pad)
+    gy, = torch.autograd.grad(m2, y, grad_outputs=dm)
+    assert torch.abs(out["dy"] - gy).max() < 1e-12
+    # sampled outputs equal the full ones
+    sub = conv.conv_bwd(lay, x.detach(), vec, s.detach(), dm, snd, rcv, n, pad_node=pad,
+                        senders=[4, 1], edges=[0, 9, 33])
+    assert torch.abs(sub["dx"] - out["dx"][[4, 1]]).max() < 1e-13
+    assert torch.abs(sub["ds"] - out["ds"][[0, 9, 33]]).max() < 1e-13
+    assert torch.abs(sub["dvec"] - out["dvec"][[0, 9, 33]]).max() < 1e-13
+
+
+def test_conv_bwd_finite_differences_and_trilinear_identity():
+    lay = irreps.layout("2x0e+2x1o+2x2e+2x3o", 3, 3)
+    rng = np.random.default_rng(17)
+    n, E, C = 6, 24, 2
+    snd, rcv, vec = _small_graph(rng, n, E)
+    x = rng.standard_normal((n, lay.d_in, C))
+    s = rng.standard_normal((E, lay.n_paths, C))
+    dm = rng.standard_normal((n, lay.d_out, C))
+    out = conv.conv_bwd(lay, x, vec, s, dm, snd, rcv, n)
+
+    def L(x_, vec_, s_):
+        return float((conv.conv_fwd(lay, x_, vec_, s_, snd, rcv, n).numpy() * dm).sum())
+
+    h = 1e-6
+    for (a, i, q) in [(0, 3, 1), (4, 12, 0), (5, 0, 1)]:
+        xp, xm = x.copy(), x.copy()
+        xp[a, i, q] += h
+        xm[a, i, q] -= h
+        assert abs((L(xp, vec, s) - L(xm, vec, s)) / (2 * h) - out["dx"][a, i, q].item()) < 1e-7
+    for (e, k, q) in [(0, 0, 0), (7, 20, 1), (23, 33, 0)]:
+        sp, sm = s.copy(), s.copy()
+        sp[e, k, q] += h
+        sm[e, k, q] -= h
+        assert abs((L(x, vec, sp) - L(x, vec, sm)) / (2 * h) - out["ds"][e, k, q].item()) < 1e-7
+    for (e, d) in [(1, 0), (11, 2), (19, 1)]:
+        vp, vm = vec.copy(), vec.copy()
+        vp[e, d] += h
+        vm[e, d] -= h
+        assert abs((L(x, vp, s) - L(x, vm, s)) / (2 * h) - out["dvec"][e, d].item()) < 1e-6
+    # trilinear in (x, y, s): <dm, m> = <dx, x> = <ds, s> = <dy, y>  (Euler)
+    m = conv.conv_fwd(lay, x, vec, s, snd, rcv, n).numpy()
+    y = sh.sh_vec(3, vec)
+    ref = (dm * m).sum()
+    for got in [(out["dx"].numpy() * x).sum(), (out["ds"].numpy() * s).sum(),
+                (out["dy"].numpy() * y).sum()]:
+        assert abs(got - ref) < 1e-10 * max(1.0, abs(ref))
+    # dvec is orthogonal to the edge vector (Y is homogeneous of degree 0 in r)
+    assert np.abs((out["dvec"].numpy() * vec).sum(1)).max() < 1e-11
+
+
+def test_graph_csr():
+    rng = np.random.default_rng(18)
+    n = 11
+    snd, rcv, _ = _small_graph(rng, n, 60)
+    perm_r, rowptr_r, perm_s, rowptr_s = graph.build(snd, rcv, n, pad_node=4)
+    keep = (snd != 4) & (rcv != 4)
+    assert rowptr_r[-1] == keep.sum() == perm_r.shape[0]
+    assert np.all(np.diff(rowptr_r) >= 0) and np.all(np.diff(rowptr_s) >= 0)
+    # brute force: edges of each receiver in increasing edge id
+    for b in range(n):
+        ids = [e for e in range(60) if rcv[e] == b and keep[e]]
+        assert list(perm_r[rowptr_r[b]:rowptr_r[b + 1]]) == ids
+        ids = [e for e in range(60) if snd[e] == b and keep[e]]
+        assert list(perm_s[rowptr_s[b]:rowptr_s[b + 1]]) == ids
