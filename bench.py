@@ -1,0 +1,251 @@
+"""Benchmark: fused channelwise CG convolution, forward + backward, on one MI355X.
+
+One step = conv forward + conv backward (harmonics, per-edge coefficient
+pre-contraction, channelwise contraction with path weights, receiver-segment
+reduction; backward edge sweep, sender-segment dx reduction, dvec) over the
+24,000-atom synthetic water box (8,000 rigid H2O, periodic, r_c = 5 A),
+x = 128x0e+128x1o+128x2e+128x3o, harmonics l <= 3, outputs l <= 3, fp32.
+Inputs are resident in HBM before the timed region.  The CSR graph build is
+timed separately (graph_build_ms); the standalone weighted tensor product
+(200,000 rows, 128x0e+128x1o+128x2e) is reported under "tp".
+
+Prints ONE JSON line.  Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+METRIC = "edges/sec conv fwd+bwd (fp32, lmax=3, 128ch) + achieved HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def conv_bytes(N, E, C, D_in, D_out, P):
+    """Algorithmic bytes (inputs + outputs, no scratch) per kernel, and totals."""
+    f = 4
+    idx_fwd = E * 4 * 2 + (N + 1) * 4          # edge id + sender per receiver-CSR slot, rowptr
+    k = {}
+    k["conv_fwd"] = N * D_in * C * f + E * 3 * f + E * P * C * f + N * D_out * C * f + idx_fwd
+    # backward sweep: reads x, vec, s, dm, indices; writes ds (+ scratch, not counted)
+    k["conv_bwd_edges"] = (N * D_in * C * f + E * 3 * f + E * P * C * f + N * D_out * C * f
+                           + E * P * C * f + E * 4 * 3 + (N + 1) * 4)
+    k["conv_bwd_dx"] = N * D_in * C * f + (N + 1) * 4
+    k["conv_bwd_dvec"] = E * 3 * f * 2 + E * 4
+    fwd = k["conv_fwd"]
+    bwd = (N * D_in * C * f + E * 3 * f + E * P * C * f + N * D_out * C * f      # inputs
+           + N * D_in * C * f + E * 3 * f + E * P * C * f + E * 4 * 3 + (N + 1) * 4 * 2)  # outputs + idx
+    return k, fwd, bwd
+
+
+def tp_bytes(R, C, D_in, D_sh, D_out, P):
+    return R * (D_in * C + D_sh + P * C + D_out * C) * 4
+
+
+def cpu_baseline(cfg, g, x, dm, seconds=12.0):
+    """The fp64 oracle on the host cores, on a bounded sample of the same workload:
+    forward for sampled receivers and backward for sampled senders and edges."""
+    import torch
+    from oracle import conv as oconv
+    from oracle import irreps as oirreps
+    lay = oirreps.layout(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    rng = np.random.default_rng(123)
+    W = synth.bessel_matrix(cfg)
+    edges_done, t_used, n_batches = 0, 0.0, 0
+    def compact(sel):
+        # the sub-problem on the nodes these edges touch, renumbered 0..k-1
+        nodes, inv = np.unique(np.concatenate([g.sender[sel], g.receiver[sel]]), return_inverse=True)
+        k = sel.shape[0]
+        return nodes, inv[:k].astype(np.int32), inv[k:].astype(np.int32)
+
+    while t_used < seconds and n_batches < 64:
+        b = rng.choice(g.n_nodes, 4, replace=False)
+        sel_r = np.nonzero(np.isin(g.receiver, b))[0]
+        sel_s = np.nonzero(np.isin(g.sender, b))[0]
+        s_r = synth.edge_weights_rows(cfg, g.vec, sel_r, W=W)
+        s_s = synth.edge_weights_rows(cfg, g.vec, sel_s, W=W)
+        nr, snd_r, rcv_r = compact(sel_r)
+        ns, snd_s, rcv_s = compact(sel_s)
+        br = np.searchsorted(nr, b)
+        bs = np.searchsorted(ns, b)
+        xr, xs_, dms_ = x[nr], x[ns], dm[ns]
+        t0 = time.perf_counter()
+        oconv.conv_fwd(lay, xr, g.vec[sel_r], s_r, snd_r, rcv_r, nr.shape[0], receivers=br)
+        oconv.conv_bwd(lay, xs_, g.vec[sel_s], s_s, dms_, snd_s, rcv_s, ns.shape[0], senders=bs)
+        t_used += time.perf_counter() - t0
+        edges_done += (sel_r.shape[0] + sel_s.shape[0]) / 2.0
+        n_batches += 1
+    return {"value": edges_done / t_used, "unit": "edges/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"{n_batches} batches of 4 random atoms: forward of their {int(edges_done)} in-edges "
+                      f"(avg of in/out counts) and full backward (dx of the atoms, ds/dvec of their "
+                      f"out-edges), float64, {t_used:.1f} s; rate = edges / (t_fwd + t_bwd)",
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-tp", action="store_true")
+    ap.add_argument("--only", choices=["all", "conv", "tp"], default="all")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              f"(the per-GPU kernel is the unit; see the sharding notes in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_35099_amd import e3mi
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    e3mi.lib()
+    dev = torch.device("cuda:0")
+    out = {"metric": METRIC, "unit": "edges/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic"}
+
+    # ---------------------------------------------------------------- conv
+    cfg = synth.CONFIGS[4]
+    t0 = time.perf_counter()
+    g = synth.graph(cfg)
+    x = synth.node_features(cfg, g.n_nodes)
+    dm = synth.out_cotangent(cfg, g.n_nodes)
+    plan = e3mi.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    N, E, C = g.n_nodes, g.sender.shape[0], cfg.channels
+    W = synth.bessel_matrix(cfg)
+    s = torch.empty((E, plan.P, C), dtype=torch.float32, device=dev)
+    for e0 in range(0, E, 1 << 16):
+        e1 = min(E, e0 + (1 << 16))
+        s[e0:e1].copy_(torch.from_numpy(synth.edge_weights(cfg, g.vec, e0, e1, W=W)))
+    xs = torch.from_numpy(x).to(dev)
+    dms = torch.from_numpy(dm).to(dev)
+    vs = torch.from_numpy(g.vec).to(dev)
+    snd = torch.from_numpy(g.sender).to(dev)
+    rcv = torch.from_numpy(g.receiver).to(dev)
+    log(f"inputs ready: N={N} E={E} ({time.perf_counter() - t0:.1f} s)")
+
+    torch.cuda.synchronize()
+    tg = []
+    for _ in range(3):
+        a = time.perf_counter()
+        graph = e3mi.Graph(snd, rcv, N)
+        torch.cuda.synchronize()
+        tg.append((time.perf_counter() - a) * 1e3)
+    m = torch.empty((N, plan.D_out, C), dtype=torch.float32, device=dev)
+    dx = torch.empty((N, plan.D_in, C), dtype=torch.float32, device=dev)
+    dvec = torch.empty((E, 3), dtype=torch.float32, device=dev)
+    ds = torch.empty((E, plan.P, C), dtype=torch.float32, device=dev)
+    ws = e3mi.workspace(e3mi.conv_workspace_size(plan, graph)[1])
+
+    def step():
+        e3mi.conv_fwd(plan, graph, xs, vs, s, out=m)
+        e3mi.conv_bwd(plan, graph, xs, vs, s, dms, dx=dx, dvec=dvec, ds=ds, ws=ws)
+
+    if args.only in ("all", "conv"):
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(args.steps):
+            step()
+        ev1.record()
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        per = e3mi.timing_read()
+        ms_step = ev0.elapsed_time(ev1) / args.steps
+        kb, fwd_b, bwd_b = conv_bytes(N, E, C, plan.D_in, plan.D_out, plan.P)
+        kernels = {}
+        for name, (ms_tot, cnt) in per.items():
+            ms_avg = ms_tot / cnt
+            entry = {"ms": round(ms_avg, 4), "launches": cnt}
+            if name in kb:
+                entry["alg_GBps"] = round(kb[name] / (ms_avg * 1e-3) / 1e9, 1)
+                entry["alg_bytes"] = kb[name]
+            kernels[name] = entry
+        dom = max((k for k in kernels if k in kb), key=lambda k: kernels[k]["ms"])
+        ach = kb[dom] / (kernels[dom]["ms"] * 1e-3) / 1e9
+        out.update({
+            "value": E / (ms_step * 1e-3),
+            "ms_per_step": ms_step,
+            "config": {"workload": "water box, 8,000 rigid H2O = 24,000 atoms, periodic, r_c 5 A; "
+                                   "x 128x0e+128x1o+128x2e+128x3o, harmonics l<=3, outputs l<=3, "
+                                   "forward + backward convolution",
+                       "n_nodes": N, "n_edges": E, "channels": C, "paths": plan.P,
+                       "D_in": plan.D_in, "D_out": plan.D_out},
+            "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None},
+            "step_alg_GBps": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9, 1),
+            "step_alg_frac": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "fwd_alg_bytes": fwd_b, "bwd_alg_bytes": bwd_b,
+            "kernels": kernels,
+            "graph_build_ms": round(min(tg), 3),
+        })
+        log(f"conv: {ms_step:.3f} ms/step, {E / ms_step / 1e3:.1f} M edges/s; kernels {kernels}")
+
+    del ws, ds, dvec, dx, m, s
+    torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- tp
+    if not args.no_tp and args.only in ("all", "tp"):
+        tcfg = synth.CONFIGS[2]
+        tplan = e3mi.Plan(tcfg.irreps, tcfg.lmax_sh, tcfg.lmax_out)
+        tx, tu, tw = synth.tp_inputs(tcfg)
+        txd, twd = torch.from_numpy(tx).to(dev), torch.from_numpy(tw).to(dev)
+        ty = e3mi.sh(tcfg.lmax_sh, torch.from_numpy(tu).to(dev))
+        R = tx.shape[0]
+        tz = torch.empty((R, tplan.D_out, tplan.C), dtype=torch.float32, device=dev)
+        for _ in range(args.warmup):
+            e3mi.tp_fwd(tplan, txd, ty, twd, out=tz)
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record()
+        for _ in range(args.steps):
+            e3mi.tp_fwd(tplan, txd, ty, twd, out=tz)
+        a1.record()
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        tk = e3mi.timing_read()["tp_fwd"]
+        t_ms = tk[0] / tk[1]
+        nb = tp_bytes(R, tplan.C, tplan.D_in, tplan.D_sh, tplan.D_out, tplan.P)
+        out["tp"] = {"workload": "200,000 rows, x 128x0e+128x1o+128x2e, harmonics l<=3, outputs l<=3",
+                     "ms": round(t_ms, 4), "rows_per_s": R / (t_ms * 1e-3),
+                     "alg_GBps": round(nb / (t_ms * 1e-3) / 1e9, 1),
+                     "frac": round(nb / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "alg_bytes": nb,
+                     "event_ms": round(a0.elapsed_time(a1) / args.steps, 4)}
+        log(f"tp: {t_ms:.3f} ms, {out['tp']['alg_GBps']} GB/s")
+        del tz, txd, twd, ty
+
+    # ---------------------------------------------------------------- cpu
+    if not args.no_cpu_baseline and args.only in ("all", "conv"):
+        out["cpu_baseline"] = cpu_baseline(cfg, g, x, dm)
+        log(f"cpu baseline: {out['cpu_baseline']['value']:.1f} edges/s")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

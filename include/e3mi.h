@@ -1,0 +1,181 @@
+/*
+ * e3mi -- channelwise Clebsch-Gordan tensor product and message-passing
+ * convolution on AMD Instinct MI355X (gfx950).  C ABI.
+ *
+ * The operation (App. E.1 of "E3J: An Efficient and Open-Source Backend for
+ * Euclidean Equivariant Operations on GPU and TPU"):
+ *
+ *   tensor product, eq. (tensor_product_formula) and eq. (edge_scalar_weighting):
+ *     z[r, i0, q] = w[r, i3(i0), q] * sum_{i1,i2} C[i0, i1, i2] x[r, i1, q] y[r, i2]
+ *   convolution, eq. (message_passing_convolution):
+ *     m[b, i0, q] = sum_{e : receiver(e) = b} s[e, i3(i0), q] *
+ *                   sum_{i1,i2} C[i0, i1, i2] x[sender(e), i1, q] Y(vec[e]/|vec[e]|)[i2]
+ *   backward, eq. (conv-bwd): dx, ds and dvec from dm (dvec through the
+ *     harmonics' Jacobian).
+ *
+ * Index spaces.  An irreps string "Cx l p + ..." (every block with the same
+ * multiplicity C, the channel count) defines the x feature axis D_in: block
+ * by block, rows m = -l..l.  The harmonics axis D_sh holds l2 = 0..lmax_sh,
+ * rows m = -l2..l2 (D_sh = (lmax_sh+1)^2).  Paths are enumerated x block by
+ * x block, then l2 ascending, then l3 ascending from |l1-l2| to
+ * min(l1+l2, lmax_out); each path owns 2*l3+1 consecutive rows of the output
+ * axis D_out and one scalar block (i3) of the weights.
+ *
+ * Conventions (the paper leaves them open): unitary real Clebsch-Gordan
+ * coefficients in the basis of the real harmonics below, canonical sign =
+ * first non-zero entry of each path block (row-major over (M, m1, m2))
+ * positive; harmonics Y_l(u) = S_l(u_z, u_x, u_y) with S_l the textbook real
+ * solid harmonics, sum_m Y_lm(u)^2 = 2l+1, so Y_0 = 1 and Y_1(u) = sqrt(3) u.
+ *
+ * Layouts: every tensor is float32, contiguous, row-major, channels last
+ * ("trailing channels", App. E.1):
+ *   x, dx  [N, D_in, C]      m, dm  [N, D_out, C]
+ *   s, ds  [E, P, C]         vec, dvec [E, 3]
+ *   y      [rows, D_sh]      (tensor product: x [R, D_in, C], w [R, P, C],
+ *                              z [R, D_out, C])
+ *
+ * Ownership: all data pointers are device buffers owned by the caller.  Plan
+ * and graph handles are owned by the library (create/destroy).  Calls that
+ * take a stream are asynchronous on it; the *_fwd / *_bwd / e3_sh* entry
+ * points never allocate, never synchronise, and fully overwrite their
+ * outputs.  Results are bitwise reproducible for identical inputs on one
+ * device and build: every sum runs in a fixed order (receiver-sorted or
+ * sender-sorted CSR order and a fixed reduction tree) and no atomics are used.
+ *
+ * Errors: every call returns an e3_status; nothing is thrown across the ABI.
+ * Arguments are validated before any device work is enqueued.
+ */
+#ifndef E3MI_H
+#define E3MI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  E3_OK = 0,
+  E3_ERR_INVALID_ARG = 1,          /* null/misaligned pointer, negative size, bad irreps string */
+  E3_ERR_UNSUPPORTED = 2,          /* no compiled kernel variant for these irreps, or C unsupported */
+  E3_ERR_INDEX_OUT_OF_RANGE = 3,   /* an edge index outside [0, n_nodes) */
+  E3_ERR_WORKSPACE_TOO_SMALL = 4,  /* ws_bytes below e3_conv_workspace_size */
+  E3_ERR_HIP = 5,                  /* a HIP runtime call failed; see e3_last_error() */
+  E3_ERR_ALLOC = 6                 /* a library-owned allocation failed (create calls only) */
+} e3_status;
+
+/* Opaque handles. */
+typedef struct e3_plan e3_plan;    /* paths, i3, offsets, coupling tables, kernel variant */
+typedef struct e3_graph e3_graph;  /* receiver- and sender-sorted CSR of an edge list, on device */
+
+/* hipStream_t without the HIP headers; pass 0 for the null stream. */
+typedef void* e3_stream;
+
+#define E3_PARITY_ALL 0u      /* keep every triangle-allowed path (default) */
+#define E3_PARITY_NATURAL 1u  /* keep only paths whose output parity is (-1)^l3 */
+
+typedef struct {
+  int C;            /* channels (the common multiplicity) */
+  int P;            /* number of paths == number of scalar blocks per edge */
+  int D_in, D_sh, D_out;
+  int nnz;          /* non-zero coupling records */
+  int lmax_sh, lmax_out;
+  int supported;    /* 1 if a compiled kernel variant exists for this plan */
+} e3_plan_info;
+
+/* Builds the path list and the coupling tables on the host (float64).
+ * irreps_x: e.g. "128x0e+128x1o+128x2e+128x3o".  lmax_sh in [0, 3],
+ * lmax_out >= 0.  flags: E3_PARITY_ALL or E3_PARITY_NATURAL.
+ * INVALID_ARG for a malformed string or out-of-range degree; UNSUPPORTED when
+ * the blocks have different multiplicities.  A plan without a compiled kernel
+ * variant is still created (info.supported == 0): its tables can be queried,
+ * but the compute entry points return E3_ERR_UNSUPPORTED. */
+e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsigned flags,
+                         e3_plan** out);
+e3_status e3_plan_query(const e3_plan* plan, e3_plan_info* info);
+e3_status e3_plan_destroy(e3_plan* plan);
+
+/* Host copies of the plan's tables (for inspection and tests).
+ * e3_plan_paths: per path (l1, l2, l3, p3, x_off, y_off, out_off), 7 ints each,
+ * into paths[7*P].  e3_plan_records: the non-zero records (App. E.2's unfolded
+ * COO form) sorted by (i0, i1, i2); writes at most cap records and sets *n to
+ * the total count. */
+e3_status e3_plan_paths(const e3_plan* plan, int32_t* paths);
+e3_status e3_plan_records(const e3_plan* plan, int64_t cap, int32_t* i0, int32_t* i1,
+                          int32_t* i2, double* val, int64_t* n);
+
+/* Host evaluation of the builder's harmonic polynomials (float64), rows
+ * [n, (lmax+1)^2], for unit vectors u[n, 3].  lmax in [0, 3]. */
+e3_status e3_sh_host(int lmax, const double* u, double* y, int64_t n);
+
+/* Builds the receiver- and sender-sorted CSR on the device (App. E.2.2 /
+ * App. E.3 receiver order; App. E.4 sender order for the backward).
+ * sender, receiver: device int32 [n_edges].  Edges with the same key keep
+ * their edge-id order (stable).  Edges with sender or receiver equal to
+ * pad_node (pad_node >= 0) are padding: they are skipped by every kernel and
+ * get zero cotangents; pad_node = -1 means no padding node.
+ * Validates every index (E3_ERR_INDEX_OUT_OF_RANGE) and synchronises the
+ * stream once.  n_edges may be 0.  The graph allocates its own device memory. */
+e3_status e3_graph_create(const int32_t* sender, const int32_t* receiver, int64_t n_nodes,
+                          int64_t n_edges, int32_t pad_node, e3_stream stream, e3_graph** out);
+/* Number of non-padding edges. */
+e3_status e3_graph_live_edges(const e3_graph* g, int64_t* n_live);
+/* Copies the CSR to device buffers: perm_r[n_live] (edge ids by receiver),
+ * rowptr_r[n_nodes+1], perm_s[n_live] (edge ids by sender), rowptr_s[n_nodes+1].
+ * Any pointer may be null.  Synchronous on the null stream. */
+e3_status e3_graph_export(const e3_graph* g, int32_t* perm_r, int32_t* rowptr_r, int32_t* perm_s,
+                          int32_t* rowptr_s);
+e3_status e3_graph_destroy(e3_graph* g);
+
+/* Real harmonics of edge vectors (App. A.3 "Harmonics"): y[n, (lmax+1)^2] =
+ * Y(vec/|vec|).  lmax in [0, 3].  A zero vector gives Y_0 = 1 and zeros. */
+e3_status e3_sh(int lmax, const float* vec, float* y, int64_t n, e3_stream stream);
+/* dvec[n, 3] = (dY/dvec)^T dy[n, (lmax+1)^2]; zero for a zero vector. */
+e3_status e3_sh_bwd(int lmax, const float* vec, const float* dy, float* dvec, int64_t n,
+                    e3_stream stream);
+
+/* Weighted tensor product (App. E.1, eq. tensor_product_formula with
+ * eq. edge_scalar_weighting): x [rows, D_in, C], y [rows, D_sh] (broadcast over
+ * channels), w [rows, P, C] -> z [rows, D_out, C]. */
+e3_status e3_tp_fwd(const e3_plan* plan, const float* x, const float* y, const float* w, float* z,
+                    int64_t rows, e3_stream stream);
+
+/* Device workspace the convolution needs (bytes, 256-byte aligned start).
+ * Forward: 0.  Backward: the per-edge x-cotangent partials [n_live, D_in, C]
+ * summed later in sender order, plus the per-edge harmonic cotangents. */
+e3_status e3_conv_workspace_size(const e3_plan* plan, const e3_graph* graph, size_t* fwd_bytes,
+                                 size_t* bwd_bytes);
+
+/* Forward convolution (eq. message_passing_convolution): m [n_nodes, D_out, C].
+ * Receivers with no live in-edge (and the padding node) get m = 0. */
+e3_status e3_conv_fwd(const e3_plan* plan, const e3_graph* graph, const float* x, const float* vec,
+                      const float* s, float* m, void* ws, size_t ws_bytes, e3_stream stream);
+
+/* Backward convolution (eq. conv-bwd): from dm [n_nodes, D_out, C] computes
+ * dx [n_nodes, D_in, C], dvec [E, 3] and ds [E, P, C].  Deterministic and
+ * atomics-free: edge-local cotangents in a receiver-ordered sweep, dx by a
+ * sender-ordered segment sum of per-edge partials kept in ws. */
+e3_status e3_conv_bwd(const e3_plan* plan, const e3_graph* graph, const float* x, const float* vec,
+                      const float* s, const float* dm, float* dx, float* dvec, float* ds, void* ws,
+                      size_t ws_bytes, e3_stream stream);
+
+/* Per-kernel timing (instrumentation).  While enabled, every kernel the
+ * library launches is bracketed by two HIP events on the caller's stream.
+ * e3_timing_read waits for the recorded events and returns, per kernel name
+ * (32-byte NUL-padded slots in names[cap*32]), the summed duration in ms and
+ * the number of launches since the last reset; *n is the number of names
+ * (which may exceed cap).  Not thread-safe with respect to concurrent streams
+ * of one process beyond the ordering of the calls. */
+e3_status e3_timing_enable(int on);
+e3_status e3_timing_reset(void);
+e3_status e3_timing_read(int cap, char* names, double* ms, int64_t* count, int* n);
+
+const char* e3_status_str(e3_status s);
+/* Text of the last HIP error seen by this thread (empty if none). */
+const char* e3_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* E3MI_H */

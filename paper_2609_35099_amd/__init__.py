@@ -1,0 +1,12 @@
+"""MI355X-native channelwise Clebsch-Gordan tensor product and message-passing
+convolution (forward and backward), after "E3J: An Efficient and Open-Source
+Backend for Euclidean Equivariant Operations on GPU and TPU".
+
+The compute lives in the HIP library ``libe3mi.so`` (kernels under ``csrc/``,
+C ABI in ``include/e3mi.h``); ``e3mi`` is its Python binding.
+"""
+from .e3mi import (E3Error, Graph, Plan, conv_bwd, conv_fwd, conv_workspace_size, sh, sh_bwd,
+                   sh_host, tp_fwd, workspace)
+
+__all__ = ["E3Error", "Graph", "Plan", "conv_bwd", "conv_fwd", "conv_workspace_size", "sh",
+           "sh_bwd", "sh_host", "tp_fwd", "workspace"]

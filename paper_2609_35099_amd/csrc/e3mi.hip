@@ -1,0 +1,1107 @@
+// e3mi: channelwise Clebsch-Gordan tensor product and message-passing
+// convolution for MI355X (gfx950).  Kernels and the C ABI declared in
+// include/e3mi.h.
+//
+// Execution model (the same for every kernel that touches features):
+//   * lanes = channels.  A 64-lane wave covers C channels with CPL = C/64
+//     consecutive channels per lane, so every feature row (C floats) is one
+//     coalesced vector load or store; the feature axis is walked in registers.
+//   * per edge (or tensor-product row), the channel-independent
+//     pre-contraction A[(path, M), m1] = sum_m2 C[M, m1, m2] y[m2] (records
+//     grouped by output then x coordinate, App. E.4's MessageTile grouping) is
+//     computed once with lane = edge and staged in LDS; the per-channel loop
+//     reads it back as wave-uniform broadcasts.  The coupling constants are
+//     compile-time literals (generated per irreps variant).
+//   * a wave owns one receiver and one group of paths (forward) or one group
+//     of whole x blocks (backward); its accumulators live in registers and are
+//     stored once (App. E.3 receiver-stationary aggregation).  No atomics.
+//   * workgroups are single waves; block ids are mapped so that each XCD
+//     walks a contiguous range of receivers and the groups of one receiver run
+//     back to back on the same XCD (shared L2 for the sender gathers).
+#include <hip/hip_runtime.h>
+#include <hipcub/hipcub.hpp>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/e3mi.h"
+#include "builder.h"
+#include "generated/variants.inc"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+// ------------------------------------------------------------ launch timing
+// When enabled, every kernel launch of the library is bracketed by two HIP
+// events recorded on the caller's stream; e3_timing_read() resolves them into
+// per-kernel summed durations.  Off by default (no events recorded).
+struct Timing {
+  std::mutex mu;
+  bool on = false;
+  struct Pending {
+    std::string name;
+    hipEvent_t a, b;
+  };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> pool;
+  std::map<std::string, std::pair<double, int64_t>> acc;
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Timing g_timing;
+
+struct TimedLaunch {
+  hipEvent_t a = nullptr, b = nullptr;
+  const char* name;
+  hipStream_t st;
+  TimedLaunch(const char* n, hipStream_t s) : name(n), st(s) {
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    if (!g_timing.on) return;
+    a = g_timing.get();
+    b = g_timing.get();
+    if (a && b && hipEventRecord(a, st) != hipSuccess) a = nullptr;
+  }
+  ~TimedLaunch() {
+    if (!a || !b) return;
+    if (hipEventRecord(b, st) != hipSuccess) return;
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    g_timing.pending.push_back({name, a, b});
+  }
+};
+
+#define E3_HIP(call)                                                          \
+  do {                                                                        \
+    hipError_t err_ = (call);                                                 \
+    if (err_ != hipSuccess) {                                                 \
+      g_last_error = std::string(#call) + ": " + hipGetErrorString(err_);     \
+      return E3_ERR_HIP;                                                      \
+    }                                                                         \
+  } while (0)
+
+constexpr int kWave = 64;
+constexpr int kXcd = 8;
+
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------ row load/store
+template <int CPL>
+__device__ __forceinline__ void ld_row(const float* __restrict__ p, float (&v)[CPL]) {
+  if constexpr (CPL == 1) {
+    v[0] = *p;
+  } else if constexpr (CPL == 2) {
+    f2v t = *reinterpret_cast<const f2v*>(p);
+    v[0] = t.x, v[1] = t.y;
+  } else {
+    f4v t = *reinterpret_cast<const f4v*>(p);
+    v[0] = t.x, v[1] = t.y, v[2] = t.z, v[3] = t.w;
+  }
+}
+
+// streamed once: non-temporal (does not displace the gathered node features)
+template <int CPL>
+__device__ __forceinline__ void ld_row_nt(const float* __restrict__ p, float (&v)[CPL]) {
+  if constexpr (CPL == 1) {
+    v[0] = __builtin_nontemporal_load(p);
+  } else if constexpr (CPL == 2) {
+    f2v t = __builtin_nontemporal_load(reinterpret_cast<const f2v*>(p));
+    v[0] = t.x, v[1] = t.y;
+  } else {
+    f4v t = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(p));
+    v[0] = t.x, v[1] = t.y, v[2] = t.z, v[3] = t.w;
+  }
+}
+
+template <int CPL>
+__device__ __forceinline__ void st_row_nt(float* __restrict__ p, const float (&v)[CPL]) {
+  if constexpr (CPL == 1) {
+    __builtin_nontemporal_store(v[0], p);
+  } else if constexpr (CPL == 2) {
+    f2v t = {v[0], v[1]};
+    __builtin_nontemporal_store(t, reinterpret_cast<f2v*>(p));
+  } else {
+    f4v t = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(t, reinterpret_cast<f4v*>(p));
+  }
+}
+
+template <int CPL>
+__device__ __forceinline__ void st_row(float* __restrict__ p, const float (&v)[CPL]) {
+  if constexpr (CPL == 1) {
+    *p = v[0];
+  } else if constexpr (CPL == 2) {
+    *reinterpret_cast<f2v*>(p) = f2v{v[0], v[1]};
+  } else {
+    *reinterpret_cast<f4v*>(p) = f4v{v[0], v[1], v[2], v[3]};
+  }
+}
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
+
+// Unit vector of an edge; a zero vector maps to 0 (then Y_0 = 1, all else 0).
+__device__ __forceinline__ void unit_of(const float* __restrict__ vec, int64_t e, float& ux, float& uy,
+                                        float& uz, float& inv) {
+  const float vx = vec[3 * e], vy = vec[3 * e + 1], vz = vec[3 * e + 2];
+  const float r2 = vx * vx + vy * vy + vz * vz;
+  inv = r2 > 0.0f ? rsqrtf(r2) : 0.0f;
+  ux = vx * inv, uy = vy * inv, uz = vz * inv;
+}
+
+// Sum of v[16] over the 64 lanes of the wave by a fixed tree (transposed
+// halving: each stage keeps half of the values and exchanges the other half);
+// lane l with l % 4 == 0 ends with the total of index l / 4.
+__device__ __forceinline__ float wave_reduce16(const float (&v)[16], int lane) {
+  float w8[8], w4[4], w2[2];
+  const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8, b2 = lane & 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float send = b5 ? v[i] : v[i + 8];
+    const float keep = b5 ? v[i + 8] : v[i];
+    w8[i] = keep + __shfl_xor(send, 32);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float send = b4 ? w8[i] : w8[i + 4];
+    const float keep = b4 ? w8[i + 4] : w8[i];
+    w4[i] = keep + __shfl_xor(send, 16);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float send = b3 ? w4[i] : w4[i + 2];
+    const float keep = b3 ? w4[i + 2] : w4[i];
+    w2[i] = keep + __shfl_xor(send, 8);
+  }
+  float w1 = (b2 ? w2[1] : w2[0]) + __shfl_xor(b2 ? w2[0] : w2[1], 4);
+  w1 += __shfl_xor(w1, 2);
+  w1 += __shfl_xor(w1, 1);
+  return w1;
+}
+
+// ------------------------------------------------------------ harmonics
+template <int L>
+__device__ __forceinline__ void sh_of(float x, float y, float z, float* Y) {
+  if constexpr (L == 0) e3gen::sh_l0(x, y, z, Y);
+  else if constexpr (L == 1) e3gen::sh_l1(x, y, z, Y);
+  else if constexpr (L == 2) e3gen::sh_l2(x, y, z, Y);
+  else e3gen::sh_l3(x, y, z, Y);
+}
+template <int L>
+__device__ __forceinline__ void sh_grad_of(float x, float y, float z, const float* dY, float& gx, float& gy,
+                                           float& gz) {
+  if constexpr (L == 0) e3gen::sh_grad_l0(x, y, z, dY, gx, gy, gz);
+  else if constexpr (L == 1) e3gen::sh_grad_l1(x, y, z, dY, gx, gy, gz);
+  else if constexpr (L == 2) e3gen::sh_grad_l2(x, y, z, dY, gx, gy, gz);
+  else e3gen::sh_grad_l3(x, y, z, dY, gx, gy, gz);
+}
+
+// dvec = (I - u u^T) g / |r| with g the gradient of the harmonic polynomials.
+__device__ __forceinline__ void project(float ux, float uy, float uz, float inv, float gx, float gy, float gz,
+                                        float& dx, float& dy, float& dz) {
+  const float ug = ux * gx + uy * gy + uz * gz;
+  dx = (gx - ux * ug) * inv;
+  dy = (gy - uy * ug) * inv;
+  dz = (gz - uz * ug) * inv;
+}
+
+template <int L>
+__global__ __launch_bounds__(256) void k_sh(const float* __restrict__ vec, float* __restrict__ y, int64_t n) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n) return;
+  float ux, uy, uz, inv;
+  unit_of(vec, e, ux, uy, uz, inv);
+  constexpr int D = (L + 1) * (L + 1);
+  float Y[D];
+  sh_of<L>(ux, uy, uz, Y);
+#pragma unroll
+  for (int i = 0; i < D; ++i) y[e * D + i] = Y[i];
+}
+
+template <int L>
+__global__ __launch_bounds__(256) void k_sh_bwd(const float* __restrict__ vec, const float* __restrict__ dy,
+                                                float* __restrict__ dvec, int64_t n) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n) return;
+  float ux, uy, uz, inv;
+  unit_of(vec, e, ux, uy, uz, inv);
+  constexpr int D = (L + 1) * (L + 1);
+  float dY[D];
+#pragma unroll
+  for (int i = 0; i < D; ++i) dY[i] = dy[e * D + i];
+  float gx, gy, gz, ox, oy, oz;
+  sh_grad_of<L>(ux, uy, uz, dY, gx, gy, gz);
+  project(ux, uy, uz, inv, gx, gy, gz, ox, oy, oz);
+  dvec[3 * e] = ox, dvec[3 * e + 1] = oy, dvec[3 * e + 2] = oz;
+}
+
+// ------------------------------------------------------------ tensor product
+constexpr int kTpRows = 8;  // rows whose pre-contraction is staged per LDS batch
+
+template <class V, int CPL>
+__global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const float* __restrict__ y,
+                                              const float* __restrict__ w, float* __restrict__ z, int64_t rows,
+                                              int C, int lanes) {
+  using T = typename V::TP;
+  __shared__ f4v smem[(kTpRows * T::NA + 3) / 4];
+  float* sA = reinterpret_cast<float*>(smem);
+  const int lane = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kTpRows;
+  const int n = (int)((rows - r0) < kTpRows ? (rows - r0) : kTpRows);
+  if (lane < n) {
+    float Y[V::D_SH];
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) Y[i] = y[(r0 + lane) * V::D_SH + i];
+    T::make_A(Y, sA + lane * T::NA);
+  }
+  __syncthreads();
+  if (lane >= lanes) return;
+  const int q = lane * CPL;
+  for (int j = 0; j < n; ++j) {
+    const int64_t r = r0 + j;
+    float xv[T::NXR][CPL], wv[T::NPATH][CPL];
+#pragma unroll
+    for (int i = 0; i < T::NXR; ++i) ld_row_nt<CPL>(x + (r * V::D_IN + T::XROW[i]) * C + q, xv[i]);
+#pragma unroll
+    for (int i = 0; i < T::NPATH; ++i) ld_row_nt<CPL>(w + (r * V::NP + T::PATH[i]) * C + q, wv[i]);
+    float* zr = z + r * V::D_OUT * C + q;
+    auto st = [&](int row, const float (&v)[CPL]) { st_row_nt<CPL>(zr + (int64_t)row * C, v); };
+    T::template rows<CPL>(sA + j * T::NA, xv, wv, st);
+  }
+}
+
+// ------------------------------------------------------------ convolution
+constexpr int kEdgeBatch = 16;  // edges whose pre-contraction is staged per LDS batch
+
+struct ConvArgs {
+  const float* x;
+  const float* vec;
+  const float* s;
+  const float* dm;
+  float* m;
+  float* ds;
+  float* T;       // backward: per-edge x-cotangent partials, sender-CSR order
+  float* DY;      // backward: per-edge, per-group harmonic cotangents
+  const int* rowptr;  // receiver CSR
+  const int* eid;     // edge id at each receiver-CSR position
+  const int* src;     // sender at each receiver-CSR position
+  const int* r2s;     // sender-CSR position at each receiver-CSR position
+  int n_nodes;
+  int chunk;  // receivers per XCD
+  int C;
+  int lanes;
+};
+
+// Receiver and group of this wave: XCD k = blockIdx % 8 walks receivers
+// [k*chunk, (k+1)*chunk); the groups of one receiver are consecutive.
+template <int NG>
+__device__ __forceinline__ bool task_of(const ConvArgs& a, int& b, int& g) {
+  const int bid = blockIdx.x;
+  const int xcd = bid % kXcd, slot = bid / kXcd;
+  g = slot % NG;
+  const int rl = slot / NG;
+  b = xcd * a.chunk + rl;
+  return rl < a.chunk && b < a.n_nodes;
+}
+
+template <class V, int G, int CPL>
+__device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, float* sA) {
+  using F = typename V::template FG<G>;
+  const int lane = threadIdx.x;
+  const bool act = lane < a.lanes;
+  const int C = a.C, q = lane * CPL;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  float acc[F::NROW][CPL];
+#pragma unroll
+  for (int i = 0; i < F::NROW; ++i)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) acc[i][c] = 0.0f;
+  for (int eb = e0; eb < e1; eb += kEdgeBatch) {
+    const int n = imin(kEdgeBatch, e1 - eb);
+    if (lane < n) {
+      const int e = a.eid[eb + lane];
+      float ux, uy, uz, inv;
+      unit_of(a.vec, e, ux, uy, uz, inv);
+      float Y[V::D_SH];
+      V::sh(ux, uy, uz, Y);
+      F::make_A(Y, sA + lane * F::NA);
+    }
+    __syncthreads();
+    if (act) {
+      for (int j = 0; j < n; ++j) {
+        const int64_t e = uniform(a.eid[eb + j]);
+        const int64_t snd = uniform(a.src[eb + j]);
+        float xv[F::NXR][CPL], sv[F::NPATH][CPL];
+#pragma unroll
+        for (int i = 0; i < F::NXR; ++i) ld_row<CPL>(a.x + (snd * V::D_IN + F::XROW[i]) * C + q, xv[i]);
+#pragma unroll
+        for (int i = 0; i < F::NPATH; ++i) ld_row_nt<CPL>(a.s + (e * V::NP + F::PATH[i]) * C + q, sv[i]);
+        F::template edge<CPL>(sA + j * F::NA, xv, sv, acc);
+      }
+    }
+    __syncthreads();
+  }
+  if (act) {
+    float* mb = a.m + (int64_t)b * V::D_OUT * C + q;
+#pragma unroll
+    for (int i = 0; i < F::NROW; ++i) st_row_nt<CPL>(mb + (int64_t)F::OROW[i] * C, acc[i]);
+  }
+}
+
+template <class V, int G, int CPL>
+__device__ __forceinline__ void fwd_dispatch(const ConvArgs& a, int b, int g, float* sA) {
+  if constexpr (G < V::NFG) {
+    if (g == G)
+      fwd_task<V, G, CPL>(a, b, sA);
+    else
+      fwd_dispatch<V, G + 1, CPL>(a, b, g, sA);
+  }
+}
+
+template <class V, int CPL>
+__global__ __launch_bounds__(kWave, 3) void k_conv_fwd(ConvArgs a) {
+  __shared__ f4v smem[(kEdgeBatch * V::MAX_NA_F + 3) / 4];
+  int b, g;
+  if (!task_of<V::NFG>(a, b, g)) return;
+  fwd_dispatch<V, 0, CPL>(a, b, g, reinterpret_cast<float*>(smem));
+}
+
+template <class V, int G, int CPL>
+__device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, float* sA, float* sY) {
+  using B = typename V::template BG<G>;
+  const int lane = threadIdx.x;
+  const bool act = lane < a.lanes;
+  const int C = a.C, q = lane * CPL;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  if (e0 == e1) return;
+  float dmv[B::NROW][CPL];
+  if (act) {
+    const float* db = a.dm + (int64_t)b * V::D_OUT * C + q;
+#pragma unroll
+    for (int i = 0; i < B::NROW; ++i) ld_row<CPL>(db + (int64_t)B::OROW[i] * C, dmv[i]);
+  }
+  for (int eb = e0; eb < e1; eb += kEdgeBatch) {
+    const int n = imin(kEdgeBatch, e1 - eb);
+    if (lane < n) {
+      const int e = a.eid[eb + lane];
+      float ux, uy, uz, inv;
+      unit_of(a.vec, e, ux, uy, uz, inv);
+      float Y[V::D_SH];
+      V::sh(ux, uy, uz, Y);
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) sY[lane * V::D_SH + i] = Y[i];
+      B::make_A(Y, sA + lane * B::NA);
+    }
+    __syncthreads();
+    for (int j = 0; j < n; ++j) {
+      const int pos = eb + j;
+      const int64_t e = uniform(a.eid[pos]);
+      float dy[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dy[i] = 0.0f;
+      if (act) {
+        const int64_t snd = uniform(a.src[pos]);
+        const int64_t slot = uniform(a.r2s[pos]);
+        float xv[B::NXR][CPL], sv[B::NPATH][CPL], t[B::NXR][CPL], Yv[V::D_SH];
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) {
+          ld_row<CPL>(a.x + (snd * V::D_IN + B::XROW[i]) * C + q, xv[i]);
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) t[i][c] = 0.0f;
+        }
+#pragma unroll
+        for (int i = 0; i < B::NPATH; ++i) ld_row_nt<CPL>(a.s + (e * V::NP + B::PATH[i]) * C + q, sv[i]);
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
+        float* dse = a.ds + e * V::NP * C + q;
+        auto st = [&](int pl, const float (&v)[CPL]) { st_row_nt<CPL>(dse + (int64_t)B::PATH[pl] * C, v); };
+        float dyl[V::D_SH];
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0f;
+        B::template edge<CPL>(sA + j * B::NA, Yv, xv, sv, dmv, t, dyl, st);
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
+        float* Te = a.T + slot * V::D_IN * C + q;
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) st_row<CPL>(Te + (int64_t)B::XROW[i] * C, t[i]);
+      }
+      const float tot = wave_reduce16(dy, lane);
+      if ((lane & 3) == 0) a.DY[((int64_t)pos * V::NBG + G) * 16 + (lane >> 2)] = tot;
+    }
+    __syncthreads();
+  }
+}
+
+template <class V, int G, int CPL>
+__device__ __forceinline__ void bwd_dispatch(const ConvArgs& a, int b, int g, float* sA, float* sY) {
+  if constexpr (G < V::NBG) {
+    if (g == G)
+      bwd_task<V, G, CPL>(a, b, sA, sY);
+    else
+      bwd_dispatch<V, G + 1, CPL>(a, b, g, sA, sY);
+  }
+}
+
+template <class V, int CPL>
+__global__ __launch_bounds__(kWave, 2) void k_conv_bwd_edges(ConvArgs a) {
+  __shared__ f4v smem[(kEdgeBatch * (V::MAX_NA_B + V::D_SH) + 3) / 4];
+  int b, g;
+  if (!task_of<V::NBG>(a, b, g)) return;
+  float* sA = reinterpret_cast<float*>(smem);
+  bwd_dispatch<V, 0, CPL>(a, b, g, sA, sA + kEdgeBatch * V::MAX_NA_B);
+}
+
+// dx[a] = sum of the partials of a's out-edges, in sender-CSR order.
+template <int D_IN, int CPL>
+__global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__ T, float* __restrict__ dx,
+                                                       const int* __restrict__ rowptr_s, int n_nodes, int chunk,
+                                                       int C, int lanes) {
+  const int bid = blockIdx.x;
+  const int node = (bid % kXcd) * chunk + bid / kXcd;
+  if (bid / kXcd >= chunk || node >= n_nodes) return;
+  const int lane = threadIdx.x;
+  if (lane >= lanes) return;
+  const int q = lane * CPL;
+  const int s0 = uniform(rowptr_s[node]), s1 = uniform(rowptr_s[node + 1]);
+  float acc[D_IN][CPL];
+#pragma unroll
+  for (int i = 0; i < D_IN; ++i)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) acc[i][c] = 0.0f;
+  for (int sl = s0; sl < s1; ++sl) {
+    const float* Tp = T + (int64_t)sl * D_IN * C + q;
+#pragma unroll
+    for (int i = 0; i < D_IN; ++i) {
+      float v[CPL];
+      ld_row_nt<CPL>(Tp + (int64_t)i * C, v);
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) acc[i][c] += v[c];
+    }
+  }
+  float* o = dx + (int64_t)node * D_IN * C + q;
+#pragma unroll
+  for (int i = 0; i < D_IN; ++i) st_row_nt<CPL>(o + (int64_t)i * C, acc[i]);
+}
+
+// dvec of each live edge from its harmonic cotangent (summed over groups).
+template <class V>
+__global__ __launch_bounds__(256) void k_conv_bwd_dvec(const float* __restrict__ vec, const float* __restrict__ DY,
+                                                       const int* __restrict__ eid, float* __restrict__ dvec,
+                                                       int64_t n_live) {
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (pos >= n_live) return;
+  const int64_t e = eid[pos];
+  float dY[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) dY[i] = 0.0f;
+#pragma unroll
+  for (int g = 0; g < V::NBG; ++g)
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) dY[i] += DY[(pos * V::NBG + g) * 16 + i];
+  float ux, uy, uz, inv;
+  unit_of(vec, e, ux, uy, uz, inv);
+  float gx, gy, gz, ox, oy, oz;
+  V::sh_grad(ux, uy, uz, dY, gx, gy, gz);
+  project(ux, uy, uz, inv, gx, gy, gz, ox, oy, oz);
+  dvec[3 * e] = ox, dvec[3 * e + 1] = oy, dvec[3 * e + 2] = oz;
+}
+
+// Padding edges: zero ds rows and dvec (one block per padding edge).
+__global__ __launch_bounds__(256) void k_zero_pad(const int* __restrict__ pad_eid, int64_t n_pad,
+                                                  float* __restrict__ ds, float* __restrict__ dvec, int64_t row) {
+  const int64_t i = blockIdx.x;
+  if (i >= n_pad) return;
+  const int64_t e = pad_eid[i];
+  for (int64_t k = threadIdx.x; k < row; k += blockDim.x) ds[e * row + k] = 0.0f;
+  if (threadIdx.x < 3) dvec[3 * e + threadIdx.x] = 0.0f;
+}
+
+// ------------------------------------------------------------ graph
+__global__ void k_graph_keys(const int32_t* __restrict__ snd, const int32_t* __restrict__ rcv, int64_t n_edges,
+                             int32_t n_nodes, int32_t pad, uint32_t* __restrict__ key_r, uint32_t* __restrict__ key_s,
+                             int32_t* __restrict__ ids, int* __restrict__ bad) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n_edges) return;
+  const int32_t s = snd[e], r = rcv[e];
+  if (s < 0 || s >= n_nodes || r < 0 || r >= n_nodes) *bad = 1;  // every writer stores the same value
+  const bool is_pad = pad >= 0 && (s == pad || r == pad);
+  key_r[e] = is_pad ? (uint32_t)n_nodes : (uint32_t)r;
+  key_s[e] = is_pad ? (uint32_t)n_nodes : (uint32_t)s;
+  ids[e] = (int32_t)e;
+}
+
+// rowptr[b] = first position with key >= b (binary search; keys sorted).
+__global__ void k_graph_rowptr(const uint32_t* __restrict__ keys, int64_t n_edges, int32_t n_nodes,
+                               int32_t* __restrict__ rowptr) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b > n_nodes) return;
+  int64_t lo = 0, hi = n_edges;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (keys[mid] < (uint32_t)b)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  rowptr[b] = (int32_t)lo;
+}
+
+__global__ void k_graph_finish(const int32_t* __restrict__ snd, const int32_t* __restrict__ eid_r,
+                               const int32_t* __restrict__ eid_s, int64_t n_live, int32_t* __restrict__ src_r,
+                               int32_t* __restrict__ pos_s) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_live) return;
+  src_r[i] = snd[eid_r[i]];
+  pos_s[eid_s[i]] = (int32_t)i;
+}
+
+__global__ void k_graph_r2s(const int32_t* __restrict__ eid_r, const int32_t* __restrict__ pos_s, int64_t n_live,
+                            int32_t* __restrict__ r2s) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_live) return;
+  r2s[i] = pos_s[eid_r[i]];
+}
+
+unsigned blocks_for(int64_t n, int t) { return (unsigned)std::max<int64_t>(1, (n + t - 1) / t); }
+
+}  // namespace
+
+// ============================================================ handles
+struct e3_plan {
+  e3b::Layout lay;
+  std::vector<e3b::Record> recs;
+  int variant = -1;
+  int cpl = 0, lanes = 0;
+};
+
+struct e3_graph {
+  int64_t n_nodes = 0, n_edges = 0, n_live = 0, n_pad = 0;
+  int32_t pad = -1;
+  int32_t* rowptr_r = nullptr;  // [N+1]
+  int32_t* eid_r = nullptr;     // [E] (live first, then padding edges by id)
+  int32_t* src_r = nullptr;     // [n_live]
+  int32_t* r2s = nullptr;       // [n_live]
+  int32_t* rowptr_s = nullptr;  // [N+1]
+  int32_t* eid_s = nullptr;     // [E]
+  int32_t* pos_s = nullptr;     // [E] scratch
+};
+
+namespace {
+
+size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
+
+struct Ws {
+  size_t t_bytes, dy_bytes;
+};
+
+template <class V>
+Ws bwd_ws(const e3_plan* p, const e3_graph* g) {
+  Ws w;
+  w.t_bytes = align256((size_t)g->n_live * V::D_IN * p->lay.C * sizeof(float));
+  w.dy_bytes = align256((size_t)g->n_live * V::NBG * 16 * sizeof(float));
+  return w;
+}
+
+ConvArgs base_args(const e3_plan* p, const e3_graph* g) {
+  ConvArgs a{};
+  a.rowptr = g->rowptr_r;
+  a.eid = g->eid_r;
+  a.src = g->src_r;
+  a.r2s = g->r2s;
+  a.n_nodes = (int)g->n_nodes;
+  a.chunk = (int)((g->n_nodes + kXcd - 1) / kXcd);
+  a.C = p->lay.C;
+  a.lanes = p->lanes;
+  return a;
+}
+
+template <class V, int CPL>
+e3_status run_fwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s, float* m,
+                  hipStream_t st) {
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.s = s, a.m = m;
+  if (g->n_nodes == 0) return E3_OK;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG);
+  {
+    TimedLaunch t_("conv_fwd", st);
+    hipLaunchKernelGGL((k_conv_fwd<V, CPL>), dim3(grid), dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V, int CPL>
+e3_status run_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
+                  const float* dm, float* dx, float* dvec, float* ds, void* ws, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  Ws w = bwd_ws<V>(p, g);
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.s = s, a.dm = dm, a.ds = ds;
+  a.T = reinterpret_cast<float*>(ws);
+  a.DY = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.t_bytes);
+  if (g->n_live > 0) {
+    const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG);
+    TimedLaunch t_("conv_bwd_edges", st);
+    hipLaunchKernelGGL((k_conv_bwd_edges<V, CPL>), dim3(grid), dim3(kWave), 0, st, a);
+    E3_HIP(hipGetLastError());
+  }
+  {
+    TimedLaunch t_("conv_bwd_dx", st);
+    hipLaunchKernelGGL((k_conv_bwd_dx<V::D_IN, CPL>), dim3((unsigned)(kXcd * a.chunk)), dim3(kWave), 0, st, a.T, dx,
+                       g->rowptr_s, a.n_nodes, a.chunk, a.C, a.lanes);
+  }
+  E3_HIP(hipGetLastError());
+  if (g->n_live > 0) {
+    TimedLaunch t_("conv_bwd_dvec", st);
+    hipLaunchKernelGGL((k_conv_bwd_dvec<V>), dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, vec, a.DY, g->eid_r,
+                       dvec, g->n_live);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_pad > 0) {
+    const int64_t row = (int64_t)V::NP * a.C;
+    TimedLaunch t_("conv_bwd_pad", st);
+    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, ds,
+                       dvec, row);
+    E3_HIP(hipGetLastError());
+  }
+  return E3_OK;
+}
+
+template <class V, int CPL>
+e3_status run_tp(const e3_plan* p, const float* x, const float* y, const float* w, float* z, int64_t rows,
+                 hipStream_t st) {
+  if (rows == 0) return E3_OK;
+  {
+    TimedLaunch t_("tp_fwd", st);
+    hipLaunchKernelGGL((k_tp<V, CPL>), dim3(blocks_for(rows, kTpRows)), dim3(kWave), 0, st, x, y, w, z, rows,
+                       p->lay.C, p->lanes);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+struct VariantOps {
+  const char* sig;
+  int d_in, d_sh, d_out, np, lsh, nbg;
+  e3_status (*fwd[2])(const e3_plan*, const e3_graph*, const float*, const float*, const float*, float*,
+                      hipStream_t);
+  e3_status (*bwd[2])(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*,
+                      float*, float*, float*, void*, hipStream_t);
+  e3_status (*tp[2])(const e3_plan*, const float*, const float*, const float*, float*, int64_t, hipStream_t);
+  Ws (*ws)(const e3_plan*, const e3_graph*);
+};
+
+#define E3_VARIANT(V)                                                                                    \
+  VariantOps{e3gen::V::SIG,                                                                              \
+             e3gen::V::D_IN,                                                                             \
+             e3gen::V::D_SH,                                                                             \
+             e3gen::V::D_OUT,                                                                            \
+             e3gen::V::NP,                                                                               \
+             e3gen::V::LSH,                                                                              \
+             e3gen::V::NBG,                                                                              \
+             {&run_fwd<e3gen::V, 1>, &run_fwd<e3gen::V, 2>},                                             \
+             {&run_bwd<e3gen::V, 1>, &run_bwd<e3gen::V, 2>},                                             \
+             {&run_tp<e3gen::V, 1>, &run_tp<e3gen::V, 2>},                                               \
+             &bwd_ws<e3gen::V>},
+
+const VariantOps kVariants[] = {E3GEN_FOR_EACH_VARIANT(E3_VARIANT)};
+constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int cpl_index(int cpl) { return cpl == 1 ? 0 : 1; }
+
+e3_status check_plan(const e3_plan* p) {
+  if (!p) return E3_ERR_INVALID_ARG;
+  if (p->variant < 0) return E3_ERR_UNSUPPORTED;
+  return E3_OK;
+}
+
+}  // namespace
+
+// ============================================================ C ABI
+extern "C" {
+
+const char* e3_status_str(e3_status s) {
+  switch (s) {
+    case E3_OK: return "ok";
+    case E3_ERR_INVALID_ARG: return "invalid argument";
+    case E3_ERR_UNSUPPORTED: return "unsupported configuration";
+    case E3_ERR_INDEX_OUT_OF_RANGE: return "edge index out of range";
+    case E3_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case E3_ERR_HIP: return "HIP runtime error";
+    case E3_ERR_ALLOC: return "allocation failed";
+  }
+  return "unknown status";
+}
+
+const char* e3_last_error(void) { return g_last_error.c_str(); }
+
+e3_status e3_timing_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.on = on != 0;
+  return E3_OK;
+}
+
+e3_status e3_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  for (auto& p : g_timing.pending) {
+    (void)hipEventSynchronize(p.b);
+    g_timing.pool.push_back(p.a);
+    g_timing.pool.push_back(p.b);
+  }
+  g_timing.pending.clear();
+  g_timing.acc.clear();
+  return E3_OK;
+}
+
+e3_status e3_timing_read(int cap, char* names, double* ms, int64_t* count, int* n) {
+  if (cap < 0 || !n || (cap > 0 && (!names || !ms || !count))) return E3_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  for (auto& p : g_timing.pending) {
+    E3_HIP(hipEventSynchronize(p.b));
+    float t = 0.0f;
+    E3_HIP(hipEventElapsedTime(&t, p.a, p.b));
+    auto& slot = g_timing.acc[p.name];
+    slot.first += t;
+    slot.second += 1;
+    g_timing.pool.push_back(p.a);
+    g_timing.pool.push_back(p.b);
+  }
+  g_timing.pending.clear();
+  int i = 0;
+  for (const auto& [name, v] : g_timing.acc) {
+    if (i < cap) {
+      std::memset(names + 32 * i, 0, 32);
+      std::strncpy(names + 32 * i, name.c_str(), 31);
+      ms[i] = v.first;
+      count[i] = v.second;
+    }
+    ++i;
+  }
+  *n = i;
+  return E3_OK;
+}
+
+e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsigned flags, e3_plan** out) {
+  if (!irreps_x || !out) return E3_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (lmax_sh < 0 || lmax_sh > 3 || lmax_out < 0 || lmax_out > 16 || flags > 1u) return E3_ERR_INVALID_ARG;
+  std::vector<e3b::Block> blocks;
+  std::string err;
+  if (!e3b::parse_irreps(irreps_x, blocks, err)) {
+    g_last_error = err;
+    return E3_ERR_INVALID_ARG;
+  }
+  for (const auto& b : blocks)
+    if (b.l > 16) return E3_ERR_INVALID_ARG;
+  e3_plan* p = new (std::nothrow) e3_plan();
+  if (!p) return E3_ERR_ALLOC;
+  if (!e3b::make_layout(irreps_x, lmax_sh, lmax_out, flags == E3_PARITY_NATURAL, p->lay, err)) {
+    g_last_error = err;
+    delete p;
+    return E3_ERR_UNSUPPORTED;
+  }
+  try {
+    p->recs = e3b::coo(p->lay);
+  } catch (const std::exception& ex) {
+    g_last_error = ex.what();
+    delete p;
+    return E3_ERR_UNSUPPORTED;
+  }
+  const std::string sig = e3b::path_signature(p->lay);
+  // channels per lane: a wave holds at most 64 lanes of channels
+  const int C = p->lay.C;
+  int cpl = 0;
+  if (C % 4 == 0 && C >= 4) cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 0);
+  if (cpl) {
+    for (int i = 0; i < kNumVariants; ++i)
+      if (sig == kVariants[i].sig && p->lay.d_sh == kVariants[i].d_sh) p->variant = i;
+  }
+  if (p->variant >= 0) {
+    p->cpl = cpl;
+    p->lanes = C / cpl;
+  }
+  *out = p;
+  return E3_OK;
+}
+
+e3_status e3_plan_query(const e3_plan* p, e3_plan_info* info) {
+  if (!p || !info) return E3_ERR_INVALID_ARG;
+  info->C = p->lay.C;
+  info->P = (int)p->lay.paths.size();
+  info->D_in = p->lay.d_in;
+  info->D_sh = p->lay.d_sh;
+  info->D_out = p->lay.d_out;
+  info->nnz = (int)p->recs.size();
+  info->lmax_sh = p->lay.lmax_sh;
+  info->lmax_out = p->lay.lmax_out;
+  info->supported = p->variant >= 0 ? 1 : 0;
+  return E3_OK;
+}
+
+e3_status e3_plan_destroy(e3_plan* p) {
+  delete p;
+  return E3_OK;
+}
+
+e3_status e3_plan_paths(const e3_plan* p, int32_t* out) {
+  if (!p || !out) return E3_ERR_INVALID_ARG;
+  for (size_t i = 0; i < p->lay.paths.size(); ++i) {
+    const auto& q = p->lay.paths[i];
+    const int32_t v[7] = {q.l1, q.l2, q.l3, q.p3, q.x_off, q.y_off, q.out_off};
+    std::memcpy(out + 7 * i, v, sizeof(v));
+  }
+  return E3_OK;
+}
+
+e3_status e3_plan_records(const e3_plan* p, int64_t cap, int32_t* i0, int32_t* i1, int32_t* i2, double* val,
+                          int64_t* n) {
+  if (!p || !n || cap < 0) return E3_ERR_INVALID_ARG;
+  *n = (int64_t)p->recs.size();
+  const int64_t m = std::min<int64_t>(cap, *n);
+  if (m > 0 && (!i0 || !i1 || !i2 || !val)) return E3_ERR_INVALID_ARG;
+  for (int64_t k = 0; k < m; ++k) {
+    i0[k] = p->recs[k].i0, i1[k] = p->recs[k].i1, i2[k] = p->recs[k].i2, val[k] = p->recs[k].v;
+  }
+  return E3_OK;
+}
+
+e3_status e3_sh_host(int lmax, const double* u, double* y, int64_t n) {
+  if (lmax < 0 || lmax > 3 || n < 0 || (n > 0 && (!u || !y))) return E3_ERR_INVALID_ARG;
+  e3b::ShTable t = e3b::sh_table(lmax);
+  const int d = (lmax + 1) * (lmax + 1);
+  for (int64_t i = 0; i < n; ++i) e3b::sh_eval(t, u + 3 * i, y + d * i);
+  return E3_OK;
+}
+
+e3_status e3_graph_create(const int32_t* sender, const int32_t* receiver, int64_t n_nodes, int64_t n_edges,
+                          int32_t pad_node, e3_stream stream, e3_graph** out) {
+  if (!out) return E3_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (n_nodes < 0 || n_edges < 0 || n_nodes >= INT32_MAX || n_edges >= INT32_MAX) return E3_ERR_INVALID_ARG;
+  if (n_edges > 0 && (!sender || !receiver)) return E3_ERR_INVALID_ARG;
+  if (pad_node < -1 || (pad_node >= 0 && pad_node >= n_nodes)) return E3_ERR_INVALID_ARG;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  e3_graph* g = new (std::nothrow) e3_graph();
+  if (!g) return E3_ERR_ALLOC;
+  g->n_nodes = n_nodes, g->n_edges = n_edges, g->pad = pad_node;
+  const int64_t E = n_edges, N = n_nodes;
+  auto fail = [&](e3_status s) {
+    e3_graph_destroy(g);
+    return s;
+  };
+  auto alloc = [&](void** p, size_t bytes) -> bool {
+    if (hipMalloc(p, std::max<size_t>(bytes, 4)) != hipSuccess) {
+      g_last_error = "hipMalloc failed in e3_graph_create";
+      return false;
+    }
+    return true;
+  };
+  if (!alloc((void**)&g->rowptr_r, (N + 1) * 4) || !alloc((void**)&g->rowptr_s, (N + 1) * 4) ||
+      !alloc((void**)&g->eid_r, E * 4) || !alloc((void**)&g->eid_s, E * 4) || !alloc((void**)&g->src_r, E * 4) ||
+      !alloc((void**)&g->r2s, E * 4) || !alloc((void**)&g->pos_s, E * 4))
+    return fail(E3_ERR_ALLOC);
+  uint32_t *key_r = nullptr, *key_s = nullptr, *key_sorted = nullptr;
+  int32_t* ids = nullptr;
+  int* flag = nullptr;
+  void* tmp = nullptr;
+  auto cleanup = [&]() {
+    (void)hipFree(key_r), (void)hipFree(key_s), (void)hipFree(key_sorted), (void)hipFree(ids), (void)hipFree(flag),
+        (void)hipFree(tmp);
+  };
+  if (!alloc((void**)&key_r, E * 4) || !alloc((void**)&key_s, E * 4) || !alloc((void**)&key_sorted, E * 4) ||
+      !alloc((void**)&ids, E * 4) || !alloc((void**)&flag, 2 * sizeof(int))) {
+    cleanup();
+    return fail(E3_ERR_ALLOC);
+  }
+  int end_bit = 1;
+  while (end_bit < 32 && ((int64_t)1 << end_bit) <= N) ++end_bit;
+  size_t tmp_bytes = 0;
+  hipError_t herr = hipSuccess;
+  herr = hipMemsetAsync(flag, 0, 2 * sizeof(int), st);
+  if (herr == hipSuccess && E > 0) {
+    hipLaunchKernelGGL(k_graph_keys, dim3(blocks_for(E, 256)), dim3(256), 0, st, sender, receiver, E, (int32_t)N,
+                       pad_node, key_r, key_s, ids, flag);
+    herr = hipGetLastError();
+    if (herr == hipSuccess)
+      herr = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_bytes, key_r, key_sorted, ids, g->eid_r, (int)E, 0,
+                                                end_bit, st);
+    if (herr == hipSuccess && !alloc(&tmp, tmp_bytes)) {
+      cleanup();
+      return fail(E3_ERR_ALLOC);
+    }
+    if (herr == hipSuccess)
+      herr = hipcub::DeviceRadixSort::SortPairs(tmp, tmp_bytes, key_r, key_sorted, ids, g->eid_r, (int)E, 0, end_bit,
+                                                st);
+    if (herr == hipSuccess) {
+      hipLaunchKernelGGL(k_graph_rowptr, dim3(blocks_for(N + 1, 256)), dim3(256), 0, st, key_sorted, E, (int32_t)N,
+                         g->rowptr_r);
+      herr = hipGetLastError();
+    }
+    if (herr == hipSuccess)
+      herr = hipcub::DeviceRadixSort::SortPairs(tmp, tmp_bytes, key_s, key_sorted, ids, g->eid_s, (int)E, 0, end_bit,
+                                                st);
+    if (herr == hipSuccess) {
+      hipLaunchKernelGGL(k_graph_rowptr, dim3(blocks_for(N + 1, 256)), dim3(256), 0, st, key_sorted, E, (int32_t)N,
+                         g->rowptr_s);
+      herr = hipGetLastError();
+    }
+  } else if (herr == hipSuccess) {
+    herr = hipMemsetAsync(g->rowptr_r, 0, (N + 1) * 4, st);
+    if (herr == hipSuccess) herr = hipMemsetAsync(g->rowptr_s, 0, (N + 1) * 4, st);
+  }
+  int host[2] = {0, 0};
+  if (herr == hipSuccess) herr = hipMemcpyAsync(&host[0], flag, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (herr == hipSuccess) herr = hipMemcpyAsync(&host[1], g->rowptr_r + N, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (herr == hipSuccess) herr = hipStreamSynchronize(st);
+  if (herr != hipSuccess) {
+    g_last_error = std::string("e3_graph_create: ") + hipGetErrorString(herr);
+    cleanup();
+    return fail(E3_ERR_HIP);
+  }
+  if (host[0]) {
+    cleanup();
+    return fail(E3_ERR_INDEX_OUT_OF_RANGE);
+  }
+  g->n_live = host[1];
+  g->n_pad = E - g->n_live;
+  if (g->n_live > 0) {
+    hipLaunchKernelGGL(k_graph_finish, dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, sender, g->eid_r, g->eid_s,
+                       g->n_live, g->src_r, g->pos_s);
+    herr = hipGetLastError();
+    if (herr == hipSuccess) {
+      hipLaunchKernelGGL(k_graph_r2s, dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, g->eid_r, g->pos_s,
+                         g->n_live, g->r2s);
+      herr = hipGetLastError();
+    }
+    if (herr == hipSuccess) herr = hipStreamSynchronize(st);  // temporaries are freed below
+  }
+  cleanup();
+  if (herr != hipSuccess) {
+    g_last_error = std::string("e3_graph_create: ") + hipGetErrorString(herr);
+    return fail(E3_ERR_HIP);
+  }
+  *out = g;
+  return E3_OK;
+}
+
+e3_status e3_graph_live_edges(const e3_graph* g, int64_t* n_live) {
+  if (!g || !n_live) return E3_ERR_INVALID_ARG;
+  *n_live = g->n_live;
+  return E3_OK;
+}
+
+e3_status e3_graph_export(const e3_graph* g, int32_t* perm_r, int32_t* rowptr_r, int32_t* perm_s, int32_t* rowptr_s) {
+  if (!g) return E3_ERR_INVALID_ARG;
+  const size_t nl = (size_t)g->n_live * 4, nr = (size_t)(g->n_nodes + 1) * 4;
+  if (perm_r && nl) E3_HIP(hipMemcpy(perm_r, g->eid_r, nl, hipMemcpyDeviceToDevice));
+  if (rowptr_r) E3_HIP(hipMemcpy(rowptr_r, g->rowptr_r, nr, hipMemcpyDeviceToDevice));
+  if (perm_s && nl) E3_HIP(hipMemcpy(perm_s, g->eid_s, nl, hipMemcpyDeviceToDevice));
+  if (rowptr_s) E3_HIP(hipMemcpy(rowptr_s, g->rowptr_s, nr, hipMemcpyDeviceToDevice));
+  return E3_OK;
+}
+
+e3_status e3_graph_destroy(e3_graph* g) {
+  if (!g) return E3_OK;
+  (void)hipFree(g->rowptr_r), (void)hipFree(g->eid_r), (void)hipFree(g->src_r), (void)hipFree(g->r2s);
+  (void)hipFree(g->rowptr_s), (void)hipFree(g->eid_s), (void)hipFree(g->pos_s);
+  delete g;
+  return E3_OK;
+}
+
+e3_status e3_sh(int lmax, const float* vec, float* y, int64_t n, e3_stream stream) {
+  if (lmax < 0 || lmax > 3 || n < 0 || (n > 0 && (!vec || !y))) return E3_ERR_INVALID_ARG;
+  if (n == 0) return E3_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid(blocks_for(n, 256));
+  TimedLaunch t_("sh", st);
+  switch (lmax) {
+    case 0: hipLaunchKernelGGL(k_sh<0>, grid, dim3(256), 0, st, vec, y, n); break;
+    case 1: hipLaunchKernelGGL(k_sh<1>, grid, dim3(256), 0, st, vec, y, n); break;
+    case 2: hipLaunchKernelGGL(k_sh<2>, grid, dim3(256), 0, st, vec, y, n); break;
+    default: hipLaunchKernelGGL(k_sh<3>, grid, dim3(256), 0, st, vec, y, n); break;
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+e3_status e3_sh_bwd(int lmax, const float* vec, const float* dy, float* dvec, int64_t n, e3_stream stream) {
+  if (lmax < 0 || lmax > 3 || n < 0 || (n > 0 && (!vec || !dy || !dvec))) return E3_ERR_INVALID_ARG;
+  if (n == 0) return E3_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid(blocks_for(n, 256));
+  TimedLaunch t_("sh_bwd", st);
+  switch (lmax) {
+    case 0: hipLaunchKernelGGL(k_sh_bwd<0>, grid, dim3(256), 0, st, vec, dy, dvec, n); break;
+    case 1: hipLaunchKernelGGL(k_sh_bwd<1>, grid, dim3(256), 0, st, vec, dy, dvec, n); break;
+    case 2: hipLaunchKernelGGL(k_sh_bwd<2>, grid, dim3(256), 0, st, vec, dy, dvec, n); break;
+    default: hipLaunchKernelGGL(k_sh_bwd<3>, grid, dim3(256), 0, st, vec, dy, dvec, n); break;
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+e3_status e3_tp_fwd(const e3_plan* p, const float* x, const float* y, const float* w, float* z, int64_t rows,
+                    e3_stream stream) {
+  e3_status s = check_plan(p);
+  if (s != E3_OK) return s;
+  if (rows < 0) return E3_ERR_INVALID_ARG;
+  if (rows > 0 && (!x || !y || !w || !z || !aligned16(x) || !aligned16(w) || !aligned16(z))) return E3_ERR_INVALID_ARG;
+  if (rows == 0) return E3_OK;
+  const VariantOps& v = kVariants[p->variant];
+  return v.tp[cpl_index(p->cpl)](p, x, y, w, z, rows, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_conv_workspace_size(const e3_plan* p, const e3_graph* g, size_t* fwd_bytes, size_t* bwd_bytes) {
+  e3_status s = check_plan(p);
+  if (s != E3_OK) return s;
+  if (!g) return E3_ERR_INVALID_ARG;
+  Ws w = kVariants[p->variant].ws(p, g);
+  if (fwd_bytes) *fwd_bytes = 0;
+  if (bwd_bytes) *bwd_bytes = w.t_bytes + w.dy_bytes;
+  return E3_OK;
+}
+
+e3_status e3_conv_fwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
+                      float* m, void* ws, size_t ws_bytes, e3_stream stream) {
+  (void)ws, (void)ws_bytes;
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x))) return E3_ERR_INVALID_ARG;
+  if (g->n_live > 0 && (!vec || !s || !aligned16(s))) return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  return v.fwd[cpl_index(p->cpl)](p, g, x, vec, s, m, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
+                      const float* dm, float* dx, float* dvec, float* ds, void* ws, size_t ws_bytes,
+                      e3_stream stream) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
+    return E3_ERR_INVALID_ARG;
+  if (g->n_edges > 0 && (!vec || !s || !ds || !dvec || !aligned16(s) || !aligned16(ds))) return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  Ws w = v.ws(p, g);
+  if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
+  if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
+  return v.bwd[cpl_index(p->cpl)](p, g, x, vec, s, dm, dx, dvec, ds, ws, reinterpret_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

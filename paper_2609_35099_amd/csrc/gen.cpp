@@ -1,0 +1,570 @@
+// Build-time generator of the straight-line device code for each supported
+// irreps variant.
+//
+// The coupling records depend only on the irreps descriptors, so they are
+// fixed before the kernels are compiled and written into the code as literal
+// constants (the same idea as the trace-time specialisation of the paper's
+// App. E.3, done ahead of time): no coefficient table is read at run time.
+// For each variant this emits
+//   * the real harmonics of a unit vector and the transposed gradient of the
+//     harmonic polynomials (from the builder's polynomial table, App. G.1);
+//   * per wave group of paths, the per-edge pre-contraction A = C . y
+//     (entries (path, M, m1), App. E.4's grouping of records by i0 then i1),
+//     the forward contraction z = A x with the path weight, the backward
+//     contraction (cotangents of x, s and y), and the tensor-product rows.
+//
+// usage: gen <out.inc>
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <map>
+#include <set>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "builder.h"
+
+using namespace e3b;
+
+namespace {
+
+std::string flit(double v) {
+  char buf[64];
+  std::snprintf(buf, sizeof(buf), "%.9ef", v);
+  return buf;
+}
+
+struct Rec {
+  int m2;      // global row on the D_sh axis
+  double c;
+};
+
+struct Entry {     // one non-zero A[(path, M), m1]
+  int k;           // path
+  int M;           // row within the path's output block
+  int m1;          // row within the x block
+  std::vector<Rec> recs;
+};
+
+struct VariantSpec {
+  std::vector<int> ls;  // degrees of the x blocks
+  int lmax_sh, lmax_out;
+  bool natural;
+};
+
+std::string irreps_of(const std::vector<int>& ls) {
+  std::string s;
+  for (size_t i = 0; i < ls.size(); ++i) {
+    if (i) s += "+";
+    s += "1x" + std::to_string(ls[i]) + ((ls[i] % 2) ? "o" : "e");
+  }
+  return s;
+}
+
+struct PathInfo {
+  Path p;
+  std::vector<double> blk;  // [d3][d1][d2]
+  std::vector<Entry> entries;
+  int nnz = 0;
+};
+
+std::vector<PathInfo> path_infos(const Layout& lay) {
+  std::vector<PathInfo> out;
+  for (const Path& p : lay.paths) {
+    PathInfo pi;
+    pi.p = p;
+    pi.blk = real_cg_block(p.l1, p.l2, p.l3);
+    const int d1 = 2 * p.l1 + 1, d2 = 2 * p.l2 + 1, d3 = 2 * p.l3 + 1;
+    for (int M = 0; M < d3; ++M)
+      for (int a = 0; a < d1; ++a) {
+        Entry e{p.k, M, a, {}};
+        for (int b = 0; b < d2; ++b) {
+          double v = pi.blk[((size_t)M * d1 + a) * d2 + b];
+          if (v != 0.0) e.recs.push_back(Rec{p.y_off + b, v});
+        }
+        if (!e.recs.empty()) {
+          pi.nnz += (int)e.recs.size();
+          pi.entries.push_back(e);
+        }
+      }
+    out.push_back(pi);
+  }
+  return out;
+}
+
+int fwd_cost(const PathInfo& pi) { return (int)pi.entries.size() + 2 * pi.p.l3 + 1; }
+
+int bwd_cost(const PathInfo& pi) {
+  const Path& p = pi.p;
+  return 2 * (int)pi.entries.size() + pi.nnz + 2 * (2 * p.l3 + 1) + 2 * (2 * p.l2 + 1);
+}
+
+// Contiguous partition of [0, n) into g parts minimising the largest cost,
+// each part having at most rmax output rows.
+std::vector<std::pair<int, int>> partition(const std::vector<int>& cost, const std::vector<int>& rows,
+                                           int g, int rmax) {
+  const int n = (int)cost.size();
+  const int INF = 1 << 29;
+  std::vector<std::vector<int>> best(g + 1, std::vector<int>(n + 1, INF));
+  std::vector<std::vector<int>> cut(g + 1, std::vector<int>(n + 1, -1));
+  best[0][0] = 0;
+  for (int j = 1; j <= g; ++j)
+    for (int i = 1; i <= n; ++i)
+      for (int s = i - 1; s >= 0; --s) {
+        int c = 0, r = 0;
+        for (int t = s; t < i; ++t) c += cost[t], r += rows[t];
+        if (r > rmax) break;
+        if (best[j - 1][s] >= INF) continue;
+        int v = std::max(best[j - 1][s], c);
+        if (v < best[j][i]) best[j][i] = v, cut[j][i] = s;
+      }
+  if (best[g][n] >= INF) return {};
+  std::vector<std::pair<int, int>> parts;
+  int i = n;
+  for (int j = g; j >= 1; --j) {
+    int s = cut[j][i];
+    parts.push_back({s, i});
+    i = s;
+  }
+  std::reverse(parts.begin(), parts.end());
+  return parts;
+}
+
+struct Group {
+  std::vector<int> paths;      // path indices (global)
+  std::vector<int> xrows;      // global D_in rows used, ascending
+  std::vector<int> orows;      // global D_out rows, in path order
+  std::vector<int> yrows;      // global D_sh rows touched (backward)
+  std::vector<Entry> entries;  // A entries in use order
+  int na_pad = 0;
+};
+
+Group make_group(const Layout& lay, const std::vector<PathInfo>& pis, int b, int e) {
+  Group g;
+  std::set<int> xs, ys;
+  for (int k = b; k < e; ++k) {
+    const PathInfo& pi = pis[k];
+    g.paths.push_back(k);
+    for (int a = 0; a < 2 * pi.p.l1 + 1; ++a) xs.insert(pi.p.x_off + a);
+    for (int M = 0; M < 2 * pi.p.l3 + 1; ++M) g.orows.push_back(pi.p.out_off + M);
+    for (int m2 = 0; m2 < 2 * pi.p.l2 + 1; ++m2) ys.insert(pi.p.y_off + m2);
+    for (const Entry& en : pi.entries) g.entries.push_back(en);
+  }
+  g.xrows.assign(xs.begin(), xs.end());
+  g.yrows.assign(ys.begin(), ys.end());
+  int na = (int)g.entries.size();
+  g.na_pad = (na + 3) / 4 * 4;
+  if (g.na_pad % 32 == 0) g.na_pad += 4;  // stagger LDS rows across banks
+  (void)lay;
+  return g;
+}
+
+int index_of(const std::vector<int>& v, int x) {
+  auto it = std::find(v.begin(), v.end(), x);
+  return it == v.end() ? -1 : (int)(it - v.begin());
+}
+
+std::string int_list(const std::vector<int>& v) {
+  std::string s = "{";
+  for (size_t i = 0; i < v.size(); ++i) s += (i ? ", " : "") + std::to_string(v[i]);
+  if (v.empty()) s += "0";
+  return s + "}";
+}
+
+// ------------------------------------------------------------------ harmonics
+void emit_sh(std::ostream& o, int lmax) {
+  ShTable t = sh_table(lmax);
+  const int nrow = (lmax + 1) * (lmax + 1);
+  const size_t nm = t.mono.size();
+  auto powname = [](int axis, int e) {
+    const char* a = axis == 0 ? "x" : (axis == 1 ? "y" : "z");
+    return e == 0 ? std::string("1.0f") : std::string(a) + std::to_string(e);
+  };
+  auto emit_pows = [&](int upto) {
+    for (int e = 2; e <= upto; ++e)
+      for (int a = 0; a < 3; ++a) {
+        const char* n = a == 0 ? "x" : (a == 1 ? "y" : "z");
+        o << "  const float " << n << e << " = " << n << (e - 1 == 1 ? std::string("") : std::to_string(e - 1))
+          << " * " << n << ";\n";
+      }
+    o << "  const float x1 = x, y1 = y, z1 = z; (void)x1; (void)y1; (void)z1;\n";
+  };
+  auto mono_expr = [&](const std::array<int, 3>& m) {
+    std::vector<std::string> f;
+    for (int a = 0; a < 3; ++a)
+      if (m[a]) f.push_back(powname(a, m[a]));
+    if (f.empty()) return std::string("1.0f");
+    std::string s;
+    for (size_t i = 0; i < f.size(); ++i) s += (i ? " * " : "") + f[i];
+    return s;
+  };
+  // values
+  o << "// Real harmonics l <= " << lmax << " of a unit vector (x, y, z); rows l-major, m = -l..l.\n";
+  o << "__device__ __forceinline__ void sh_l" << lmax
+    << "(const float x, const float y, const float z, float* __restrict__ Y) {\n";
+  emit_pows(lmax);
+  for (int r = 0; r < nrow; ++r) {
+    std::string acc;
+    for (size_t j = 0; j < nm; ++j) {
+      double c = t.coef[r * nm + j];
+      if (c == 0.0) continue;
+      std::string term = flit(c) + " * (" + mono_expr(t.mono[j]) + ")";
+      acc += acc.empty() ? term : " + " + term;
+    }
+    if (acc.empty()) acc = "0.0f";
+    o << "  Y[" << r << "] = " << acc << ";\n";
+  }
+  o << "}\n\n";
+  // gradient of sum_r dY[r] P_r(u) with respect to u (polynomial gradient)
+  o << "// g = sum_r dY[r] grad P_r(x, y, z), P_r the harmonic polynomials above.\n";
+  o << "__device__ __forceinline__ void sh_grad_l" << lmax
+    << "(const float x, const float y, const float z, const float* __restrict__ dY, float& gx, float& gy, float& gz) {\n";
+  emit_pows(std::max(lmax - 1, 1));
+  const char* gn[3] = {"gx", "gy", "gz"};
+  for (int a = 0; a < 3; ++a) {
+    // collect: derivative monomial -> list of (row, coef * exponent)
+    std::map<std::array<int, 3>, std::vector<std::pair<int, double>>> terms;
+    for (int r = 0; r < nrow; ++r)
+      for (size_t j = 0; j < nm; ++j) {
+        double c = t.coef[r * nm + j];
+        if (c == 0.0 || t.mono[j][a] == 0) continue;
+        std::array<int, 3> d = t.mono[j];
+        double f = c * d[a];
+        d[a] -= 1;
+        terms[d].push_back({r, f});
+      }
+    o << "  " << gn[a] << " = 0.0f;\n";
+    for (const auto& [m, lst] : terms) {
+      std::string w;
+      for (const auto& [r, f] : lst) w += (w.empty() ? "" : " + ") + flit(f) + " * dY[" + std::to_string(r) + "]";
+      o << "  " << gn[a] << " = fmaf(" << mono_expr(m) << ", " << w << ", " << gn[a] << ");\n";
+    }
+  }
+  o << "}\n\n";
+}
+
+// ------------------------------------------------------------------ groups
+void emit_make_A(std::ostream& o, const Group& g) {
+  o << "  // A[entry] = sum_m2 C[M, m1, m2] y[m2] for entries (path, M, m1) of this group\n";
+  o << "  __device__ __forceinline__ static void make_A(const float* __restrict__ y, float* __restrict__ A) {\n";
+  const int na = (int)g.entries.size();
+  for (int q = 0; q < g.na_pad / 4; ++q) {
+    o << "    { float4 v;\n";
+    const char* comp[4] = {"x", "y", "z", "w"};
+    for (int c = 0; c < 4; ++c) {
+      int i = 4 * q + c;
+      std::string expr = "0.0f";
+      if (i < na) {
+        const Entry& e = g.entries[i];
+        expr = flit(e.recs[0].c) + " * y[" + std::to_string(e.recs[0].m2) + "]";
+        for (size_t r = 1; r < e.recs.size(); ++r)
+          expr = "fmaf(" + flit(e.recs[r].c) + ", y[" + std::to_string(e.recs[r].m2) + "], " + expr + ")";
+      }
+      o << "      v." << comp[c] << " = " << expr << ";\n";
+    }
+    o << "      reinterpret_cast<float4*>(A)[" << q << "] = v; }\n";
+  }
+  o << "  }\n";
+}
+
+std::string aval(int i) {
+  const char* comp[4] = {"x", "y", "z", "w"};
+  return "a" + std::to_string(i / 4) + "." + comp[i % 4];
+}
+
+// emits loads of float4 chunks covering entries [lo, hi) that are not loaded yet
+void emit_A_loads(std::ostream& o, int lo, int hi, std::vector<bool>& loaded, const char* ind) {
+  for (int q = lo / 4; q <= (hi - 1) / 4; ++q) {
+    if (q < (int)loaded.size() && !loaded[q]) {
+      o << ind << "const float4 a" << q << " = A4[" << q << "];\n";
+      loaded[q] = true;
+    }
+  }
+}
+
+void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
+  o << "  template <int CPL>\n";
+  o << "  __device__ __forceinline__ static void edge(const float* __restrict__ A, const float (&x)[NXR][CPL],\n"
+       "      const float (&s)[NPATH][CPL], float (&acc)[NROW][CPL]) {\n";
+  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  std::vector<bool> loaded(g.na_pad / 4, false);
+  int ei = 0, orow = 0;
+  for (size_t pl = 0; pl < g.paths.size(); ++pl) {
+    const PathInfo& pi = pis[g.paths[pl]];
+    const int d3 = 2 * pi.p.l3 + 1;
+    for (int M = 0; M < d3; ++M, ++orow) {
+      int lo = ei;
+      while (ei < (int)g.entries.size() && g.entries[ei].k == pi.p.k && g.entries[ei].M == M) ++ei;
+      if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
+      o << "    {  // path " << pi.p.k << " (" << pi.p.l1 << "," << pi.p.l2 << "," << pi.p.l3 << ") row " << M << "\n";
+      o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+      if (ei == lo) {
+        o << "        (void)c;\n      }\n    }\n";
+        continue;
+      }
+      for (int i = lo; i < ei; ++i) {
+        int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
+        if (i == lo)
+          o << "        float z = " << aval(i) << " * x[" << xl << "][c];\n";
+        else
+          o << "        z = fmaf(" << aval(i) << ", x[" << xl << "][c], z);\n";
+      }
+      o << "        acc[" << orow << "][c] = fmaf(s[" << pl << "][c], z, acc[" << orow << "][c]);\n";
+      o << "      }\n    }\n";
+    }
+  }
+  o << "  }\n";
+  (void)lay;
+}
+
+void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
+  o << "  // Per edge and channel, path by path: w = s dm (the mixed cotangent), t += A^T w\n"
+       "  // (the x cotangent before the sender reduction), B[m2] = sum C dm x, ds = y . B,\n"
+       "  // dy += s B (summed over this lane's channels).\n";
+  o << "  template <int CPL, class DS>\n";
+  o << "  __device__ __forceinline__ static void edge(const float* __restrict__ A, const float (&Y)[D_SH],\n"
+       "      const float (&x)[NXR][CPL], const float (&s)[NPATH][CPL], const float (&dm)[NROW][CPL],\n"
+       "      float (&t)[NXR][CPL], float (&dy)[D_SH], DS& st_ds) {\n";
+  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  std::vector<bool> loaded(g.na_pad / 4, false);
+  int ei = 0, orow0 = 0;
+  for (size_t pl = 0; pl < g.paths.size(); ++pl) {
+    const PathInfo& pi = pis[g.paths[pl]];
+    const Path& p = pi.p;
+    const int d2 = 2 * p.l2 + 1, d3 = 2 * p.l3 + 1;
+    int lo = ei;
+    while (ei < (int)g.entries.size() && g.entries[ei].k == p.k) ++ei;
+    if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
+    o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << ")\n";
+    o << "      float dsv[CPL];\n";
+    o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+    for (int M = 0; M < d3; ++M)
+      o << "        const float w" << M << " = s[" << pl << "][c] * dm[" << orow0 + M << "][c];\n";
+    std::vector<bool> binit(d2, false);
+    std::string decl;
+    for (int b = 0; b < d2; ++b) decl += (b ? ", b" : "b") + std::to_string(b);
+    o << "        float " << decl << ";\n";
+    for (int i = lo; i < ei; ++i) {
+      const Entry& en = g.entries[i];
+      int xl = index_of(g.xrows, p.x_off + en.m1);
+      o << "        t[" << xl << "][c] = fmaf(" << aval(i) << ", w" << en.M << ", t[" << xl << "][c]);\n";
+      o << "        {\n          const float pr = dm[" << orow0 + en.M << "][c] * x[" << xl << "][c];\n";
+      for (const Rec& r : en.recs) {
+        int b = r.m2 - p.y_off;
+        if (!binit[b]) {
+          o << "          b" << b << " = " << flit(r.c) << " * pr;\n";
+          binit[b] = true;
+        } else {
+          o << "          b" << b << " = fmaf(" << flit(r.c) << ", pr, b" << b << ");\n";
+        }
+      }
+      o << "        }\n";
+    }
+    std::string ds;
+    for (int b = 0; b < d2; ++b) {
+      if (!binit[b]) continue;
+      std::string yb = "Y[" + std::to_string(p.y_off + b) + "]";
+      ds = ds.empty() ? yb + " * b" + std::to_string(b) : "fmaf(" + yb + ", b" + std::to_string(b) + ", " + ds + ")";
+    }
+    o << "        dsv[c] = " << (ds.empty() ? std::string("0.0f") : ds) << ";\n";
+    for (int b = 0; b < d2; ++b) {
+      if (!binit[b]) continue;
+      o << "        dy[" << p.y_off + b << "] = fmaf(s[" << pl << "][c], b" << b << ", dy[" << p.y_off + b << "]);\n";
+    }
+    for (int b = 0; b < d2; ++b)
+      if (!binit[b]) o << "        (void)b" << b << ";\n";
+    o << "      }\n";
+    o << "      st_ds(" << pl << ", dsv);\n";
+    o << "    }\n";
+    orow0 += d3;
+  }
+  o << "  }\n";
+  (void)lay;
+}
+
+void emit_tp_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
+  o << "  // Weighted tensor product rows: z[i0] = w[i3(i0)] * sum A x; each row handed to st.\n";
+  o << "  template <int CPL, class ST>\n";
+  o << "  __device__ __forceinline__ static void rows(const float* __restrict__ A, const float (&x)[NXR][CPL],\n"
+       "      const float (&w)[NPATH][CPL], ST& st) {\n";
+  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  std::vector<bool> loaded(g.na_pad / 4, false);
+  int ei = 0;
+  for (size_t pl = 0; pl < g.paths.size(); ++pl) {
+    const PathInfo& pi = pis[g.paths[pl]];
+    const int d3 = 2 * pi.p.l3 + 1;
+    for (int M = 0; M < d3; ++M) {
+      int lo = ei;
+      while (ei < (int)g.entries.size() && g.entries[ei].k == pi.p.k && g.entries[ei].M == M) ++ei;
+      if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
+      o << "    {  // path " << pi.p.k << " row " << M << "\n";
+      o << "      float v[CPL];\n";
+      o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+      if (ei == lo) {
+        o << "        v[c] = 0.0f;\n";
+      } else {
+        for (int i = lo; i < ei; ++i) {
+          int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
+          if (i == lo)
+            o << "        float z = " << aval(i) << " * x[" << xl << "][c];\n";
+          else
+            o << "        z = fmaf(" << aval(i) << ", x[" << xl << "][c], z);\n";
+        }
+        o << "        v[c] = w[" << pl << "][c] * z;\n";
+      }
+      o << "      }\n";
+      o << "      st(" << pi.p.out_off + M << ", v);\n";
+      o << "    }\n";
+    }
+  }
+  o << "  }\n";
+  (void)lay;
+}
+
+void emit_group_meta(std::ostream& o, const Group& g) {
+  o << "  static constexpr int NA = " << g.na_pad << ";\n";
+  o << "  static constexpr int NXR = " << g.xrows.size() << ";\n";
+  o << "  static constexpr int NPATH = " << g.paths.size() << ";\n";
+  o << "  static constexpr int NROW = " << g.orows.size() << ";\n";
+  o << "  static constexpr int XROW[" << std::max<size_t>(1, g.xrows.size()) << "] = " << int_list(g.xrows) << ";\n";
+  o << "  static constexpr int PATH[" << std::max<size_t>(1, g.paths.size()) << "] = " << int_list(g.paths) << ";\n";
+  o << "  static constexpr int OROW[" << std::max<size_t>(1, g.orows.size()) << "] = " << int_list(g.orows) << ";\n";
+}
+
+std::string tag_of(const VariantSpec& v) {
+  std::string t = "V_x";
+  for (int l : v.ls) t += std::to_string(l);
+  t += "_s" + std::to_string(v.lmax_sh) + "_o" + std::to_string(v.lmax_out);
+  if (v.natural) t += "_n";
+  return t;
+}
+
+}  // namespace
+
+int main(int argc, char** argv) {
+  if (argc != 2) {
+    std::fprintf(stderr, "usage: gen <out.inc>\n");
+    return 2;
+  }
+  // Compiled variants: x blocks of degrees ls (any parities, all paths kept),
+  // harmonics up to lmax_sh, outputs up to lmax_out.
+  const std::vector<VariantSpec> specs = {
+      {{0, 1}, 2, 2, false},
+      {{0, 1, 2}, 3, 3, false},
+      {{0, 1}, 3, 3, false},
+      {{0, 1, 2, 3}, 3, 3, false},
+  };
+  const int FWD_TARGET = 150;   // per-wave FMA budget per edge and channel (forward)
+  const int FWD_RMAX = 40;      // output rows held in registers per wave
+  const int BWD_TARGET = 640;
+  const int BWD_RMAX = 56;
+
+  std::ostringstream o;
+  o << "// GENERATED by gen.cpp from the host table builder -- do not edit.\n";
+  o << "#pragma once\n\nnamespace e3gen {\n\n";
+  for (int l = 0; l <= 3; ++l) emit_sh(o, l);
+
+  std::vector<std::string> tags;
+  for (const auto& v : specs) {
+    Layout lay;
+    std::string err;
+    if (!make_layout(irreps_of(v.ls), v.lmax_sh, v.lmax_out, v.natural, lay, err)) {
+      std::fprintf(stderr, "gen: %s\n", err.c_str());
+      return 1;
+    }
+    std::vector<PathInfo> pis = path_infos(lay);
+    const int np = (int)pis.size();
+    std::vector<int> fc(np), bc(np), rows(np);
+    int total_f = 0;
+    for (int k = 0; k < np; ++k) {
+      fc[k] = fwd_cost(pis[k]);
+      bc[k] = bwd_cost(pis[k]);
+      rows[k] = 2 * pis[k].p.l3 + 1;
+      total_f += fc[k];
+    }
+    // forward groups: contiguous paths, balanced cost
+    int gf = std::max(1, (int)std::lround((double)total_f / FWD_TARGET));
+    std::vector<std::pair<int, int>> fparts;
+    for (;; ++gf) {
+      fparts = partition(fc, rows, gf, FWD_RMAX);
+      if (!fparts.empty()) break;
+    }
+    // backward groups: whole x blocks (so the x cotangent rows of different
+    // groups never overlap), merged while small
+    std::vector<std::pair<int, int>> bparts;
+    {
+      int s = 0;
+      while (s < np) {
+        int e = s, cost = 0, r = 0;
+        while (e < np) {
+          // extent of the x block starting at path e
+          int xb = pis[e].p.xb, f = e, c2 = 0, r2 = 0;
+          while (f < np && pis[f].p.xb == xb) c2 += bc[f], r2 += rows[f], ++f;
+          if (e > s && (cost + c2 > BWD_TARGET || r + r2 > BWD_RMAX)) break;
+          cost += c2, r += r2, e = f;
+        }
+        bparts.push_back({s, e});
+        s = e;
+      }
+    }
+    std::vector<Group> fg, bg;
+    for (auto [b, e] : fparts) fg.push_back(make_group(lay, pis, b, e));
+    for (auto [b, e] : bparts) bg.push_back(make_group(lay, pis, b, e));
+    Group tpg = make_group(lay, pis, 0, np);
+
+    const std::string tag = tag_of(v);
+    tags.push_back(tag);
+    int maxf = 0, maxb = 0;
+    for (auto& g : fg) maxf = std::max(maxf, g.na_pad);
+    for (auto& g : bg) maxb = std::max(maxb, g.na_pad);
+    o << "// ============================================================ " << tag << "\n";
+    o << "// " << np << " paths, D_in " << lay.d_in << ", D_sh " << lay.d_sh << ", D_out " << lay.d_out << "\n";
+    o << "struct " << tag << " {\n";
+    o << "  static constexpr int D_IN = " << lay.d_in << ", D_SH = " << lay.d_sh << ", D_OUT = " << lay.d_out
+      << ", NP = " << np << ", LSH = " << v.lmax_sh << ";\n";
+    o << "  static constexpr const char* SIG = \"" << path_signature(lay) << "\";\n";
+    o << "  static constexpr int NFG = " << fg.size() << ", NBG = " << bg.size() << ";\n";
+    o << "  static constexpr int MAX_NA_F = " << maxf << ", MAX_NA_B = " << maxb << ", NA_TP = " << tpg.na_pad << ";\n";
+    o << "  __device__ __forceinline__ static void sh(float x, float y, float z, float* Y) { sh_l" << v.lmax_sh
+      << "(x, y, z, Y); }\n";
+    o << "  __device__ __forceinline__ static void sh_grad(float x, float y, float z, const float* dY, float& gx, float& gy, float& gz) { sh_grad_l"
+      << v.lmax_sh << "(x, y, z, dY, gx, gy, gz); }\n";
+    o << "  template <int G> struct FG;\n  template <int G> struct BG;\n  struct TP;\n};\n\n";
+    for (size_t gi = 0; gi < fg.size(); ++gi) {
+      o << "template <> struct " << tag << "::FG<" << gi << "> {\n";
+      o << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
+      emit_group_meta(o, fg[gi]);
+      emit_make_A(o, fg[gi]);
+      emit_fwd_group(o, lay, pis, fg[gi]);
+      o << "};\n\n";
+    }
+    for (size_t gi = 0; gi < bg.size(); ++gi) {
+      o << "template <> struct " << tag << "::BG<" << gi << "> {\n";
+      o << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
+      emit_group_meta(o, bg[gi]);
+      emit_make_A(o, bg[gi]);
+      emit_bwd_group(o, lay, pis, bg[gi]);
+      o << "};\n\n";
+    }
+    o << "struct " << tag << "::TP {\n";
+    o << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
+    emit_group_meta(o, tpg);
+    emit_make_A(o, tpg);
+    emit_tp_group(o, lay, pis, tpg);
+    o << "};\n\n";
+  }
+  o << "#define E3GEN_FOR_EACH_VARIANT(X)";
+  for (const auto& t : tags) o << " X(" << t << ")";
+  o << "\n\n}  // namespace e3gen\n";
+
+  FILE* f = std::fopen(argv[1], "w");
+  if (!f) {
+    std::perror("gen");
+    return 1;
+  }
+  std::string s = o.str();
+  std::fwrite(s.data(), 1, s.size(), f);
+  std::fclose(f);
+  return 0;
+}

@@ -1,0 +1,312 @@
+"""Python binding of libe3mi (ctypes): argument marshalling only.
+
+Every computation runs in the HIP library; this module checks tensor shapes,
+dtypes and devices, passes raw device pointers and the current torch stream,
+and raises E3Error on a non-OK status.  If the library has not been built the
+first call raises (there is no fallback path).
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libe3mi.so")
+
+_STATUS = {0: "E3_OK", 1: "E3_ERR_INVALID_ARG", 2: "E3_ERR_UNSUPPORTED",
+           3: "E3_ERR_INDEX_OUT_OF_RANGE", 4: "E3_ERR_WORKSPACE_TOO_SMALL",
+           5: "E3_ERR_HIP", 6: "E3_ERR_ALLOC"}
+
+E3_PARITY_ALL = 0
+E3_PARITY_NATURAL = 1
+
+
+class E3Error(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str = ""):
+        self.status = status
+        name = _STATUS.get(status, str(status))
+        super().__init__(f"{where}: {name}" + (f" ({detail})" if detail else ""))
+
+
+class PlanInfo(ct.Structure):
+    _fields_ = [("C", ct.c_int), ("P", ct.c_int), ("D_in", ct.c_int), ("D_sh", ct.c_int),
+                ("D_out", ct.c_int), ("nnz", ct.c_int), ("lmax_sh", ct.c_int),
+                ("lmax_out", ct.c_int), ("supported", ct.c_int)]
+
+
+_lib = None
+
+# name -> (restype, argtypes); mirrors include/e3mi.h
+_P, _I, _I64, _U, _D = ct.c_void_p, ct.c_int, ct.c_int64, ct.c_uint, ct.c_double
+SIGNATURES = {
+    "e3_plan_create": (_I, [ct.c_char_p, _I, _I, _U, ct.POINTER(_P)]),
+    "e3_plan_query": (_I, [_P, ct.POINTER(PlanInfo)]),
+    "e3_plan_destroy": (_I, [_P]),
+    "e3_plan_paths": (_I, [_P, _P]),
+    "e3_plan_records": (_I, [_P, _I64, _P, _P, _P, _P, ct.POINTER(_I64)]),
+    "e3_sh_host": (_I, [_I, _P, _P, _I64]),
+    "e3_graph_create": (_I, [_P, _P, _I64, _I64, ct.c_int32, _P, ct.POINTER(_P)]),
+    "e3_graph_live_edges": (_I, [_P, ct.POINTER(_I64)]),
+    "e3_graph_export": (_I, [_P, _P, _P, _P, _P]),
+    "e3_graph_destroy": (_I, [_P]),
+    "e3_sh": (_I, [_I, _P, _P, _I64, _P]),
+    "e3_sh_bwd": (_I, [_I, _P, _P, _P, _I64, _P]),
+    "e3_tp_fwd": (_I, [_P, _P, _P, _P, _P, _I64, _P]),
+    "e3_conv_workspace_size": (_I, [_P, _P, ct.POINTER(ct.c_size_t), ct.POINTER(ct.c_size_t)]),
+    "e3_conv_fwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
+    "e3_conv_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
+    "e3_timing_enable": (_I, [_I]),
+    "e3_timing_reset": (_I, []),
+    "e3_timing_read": (_I, [_I, _P, _P, _P, ct.POINTER(_I)]),
+    "e3_status_str": (ct.c_char_p, [_I]),
+    "e3_last_error": (ct.c_char_p, []),
+}
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ct.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        detail = lib().e3_last_error().decode(errors="replace")
+        raise E3Error(status, where, detail)
+
+
+# ---------------------------------------------------------------- tensors
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t, name, shape=None, dtype="float32"):
+    torch = _torch()
+    want = {"float32": torch.float32, "int32": torch.int32}[dtype]
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.dtype != want:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return ct.c_void_p(t.data_ptr()) if t.numel() else ct.c_void_p(0)
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ct.c_void_p(s.cuda_stream)
+
+
+# ---------------------------------------------------------------- plan
+class Plan:
+    """Paths, coupling tables and compiled kernel variant for an irreps layout."""
+
+    def __init__(self, irreps: str, lmax_sh: int, lmax_out: int, natural: bool = False):
+        h = ct.c_void_p()
+        _check(lib().e3_plan_create(irreps.encode(), lmax_sh, lmax_out,
+                                    E3_PARITY_NATURAL if natural else E3_PARITY_ALL,
+                                    ct.byref(h)), "e3_plan_create")
+        self._h = h
+        info = PlanInfo()
+        _check(lib().e3_plan_query(h, ct.byref(info)), "e3_plan_query")
+        self.info = info
+        self.irreps = irreps
+        self.C, self.P = info.C, info.P
+        self.D_in, self.D_sh, self.D_out = info.D_in, info.D_sh, info.D_out
+        self.supported = bool(info.supported)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def paths(self) -> np.ndarray:
+        out = np.zeros((self.P, 7), dtype=np.int32)
+        _check(lib().e3_plan_paths(self._h, out.ctypes.data_as(ct.c_void_p)), "e3_plan_paths")
+        return out
+
+    def records(self):
+        n = ct.c_int64()
+        _check(lib().e3_plan_records(self._h, 0, None, None, None, None, ct.byref(n)), "e3_plan_records")
+        m = n.value
+        i0, i1, i2 = (np.zeros(m, np.int32) for _ in range(3))
+        v = np.zeros(m, np.float64)
+        _check(lib().e3_plan_records(self._h, m, i0.ctypes.data_as(ct.c_void_p), i1.ctypes.data_as(ct.c_void_p),
+                                     i2.ctypes.data_as(ct.c_void_p), v.ctypes.data_as(ct.c_void_p),
+                                     ct.byref(n)), "e3_plan_records")
+        return i0, i1, i2, v
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib().e3_plan_destroy(self._h)
+            self._h = ct.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def sh_host(lmax: int, u: np.ndarray) -> np.ndarray:
+    """The builder's harmonic polynomials evaluated on the host (float64)."""
+    u = np.ascontiguousarray(u, dtype=np.float64)
+    y = np.zeros((u.shape[0], (lmax + 1) ** 2))
+    _check(lib().e3_sh_host(lmax, u.ctypes.data_as(ct.c_void_p), y.ctypes.data_as(ct.c_void_p), u.shape[0]),
+           "e3_sh_host")
+    return y
+
+
+# ---------------------------------------------------------------- graph
+class Graph:
+    """Receiver- and sender-sorted CSR of an edge list, built on the device."""
+
+    def __init__(self, sender, receiver, n_nodes: int, pad_node: int = -1, stream=None):
+        E = sender.shape[0]
+        ps = _ptr(sender, "sender", (E,), "int32")
+        pr = _ptr(receiver, "receiver", (E,), "int32")
+        h = ct.c_void_p()
+        _check(lib().e3_graph_create(ps, pr, n_nodes, E, pad_node, _stream(stream), ct.byref(h)),
+               "e3_graph_create")
+        self._h = h
+        self.n_nodes, self.n_edges, self.pad_node = n_nodes, E, pad_node
+        n = ct.c_int64()
+        _check(lib().e3_graph_live_edges(h, ct.byref(n)), "e3_graph_live_edges")
+        self.n_live = n.value
+
+    @property
+    def handle(self):
+        return self._h
+
+    def export(self):
+        torch = _torch()
+        dev = torch.device("cuda")
+        pr = torch.empty(self.n_live, dtype=torch.int32, device=dev)
+        rr = torch.empty(self.n_nodes + 1, dtype=torch.int32, device=dev)
+        ps = torch.empty(self.n_live, dtype=torch.int32, device=dev)
+        rs = torch.empty(self.n_nodes + 1, dtype=torch.int32, device=dev)
+        torch.cuda.synchronize()
+        _check(lib().e3_graph_export(self._h, _ptr(pr, "perm_r", dtype="int32"), _ptr(rr, "rowptr_r", dtype="int32"),
+                                     _ptr(ps, "perm_s", dtype="int32"), _ptr(rs, "rowptr_s", dtype="int32")),
+               "e3_graph_export")
+        return pr, rr, ps, rs
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib().e3_graph_destroy(self._h)
+            self._h = ct.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------- compute
+def _empty(shape, like=None):
+    torch = _torch()
+    return torch.empty(shape, dtype=torch.float32, device="cuda")
+
+
+def sh(lmax: int, vec, out=None, stream=None):
+    n = vec.shape[0]
+    out = _empty((n, (lmax + 1) ** 2)) if out is None else out
+    _check(lib().e3_sh(lmax, _ptr(vec, "vec", (n, 3)), _ptr(out, "y", (n, (lmax + 1) ** 2)), n, _stream(stream)),
+           "e3_sh")
+    return out
+
+
+def sh_bwd(lmax: int, vec, dy, out=None, stream=None):
+    n = vec.shape[0]
+    out = _empty((n, 3)) if out is None else out
+    _check(lib().e3_sh_bwd(lmax, _ptr(vec, "vec", (n, 3)), _ptr(dy, "dy", (n, (lmax + 1) ** 2)),
+                           _ptr(out, "dvec", (n, 3)), n, _stream(stream)), "e3_sh_bwd")
+    return out
+
+
+def tp_fwd(plan: Plan, x, y, w, out=None, stream=None):
+    R = x.shape[0]
+    out = _empty((R, plan.D_out, plan.C)) if out is None else out
+    _check(lib().e3_tp_fwd(plan.handle, _ptr(x, "x", (R, plan.D_in, plan.C)), _ptr(y, "y", (R, plan.D_sh)),
+                           _ptr(w, "w", (R, plan.P, plan.C)), _ptr(out, "z", (R, plan.D_out, plan.C)), R,
+                           _stream(stream)), "e3_tp_fwd")
+    return out
+
+
+def conv_workspace_size(plan: Plan, graph: Graph):
+    f, b = ct.c_size_t(), ct.c_size_t()
+    _check(lib().e3_conv_workspace_size(plan.handle, graph.handle, ct.byref(f), ct.byref(b)),
+           "e3_conv_workspace_size")
+    return f.value, b.value
+
+
+def workspace(nbytes: int):
+    torch = _torch()
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device="cuda")
+
+
+def conv_fwd(plan: Plan, graph: Graph, x, vec, s, out=None, stream=None):
+    N, E = graph.n_nodes, graph.n_edges
+    out = _empty((N, plan.D_out, plan.C)) if out is None else out
+    _check(lib().e3_conv_fwd(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                             _ptr(vec, "vec", (E, 3)), _ptr(s, "s", (E, plan.P, plan.C)),
+                             _ptr(out, "m", (N, plan.D_out, plan.C)), None, 0, _stream(stream)), "e3_conv_fwd")
+    return out
+
+
+def conv_bwd(plan: Plan, graph: Graph, x, vec, s, dm, dx=None, dvec=None, ds=None, ws=None, stream=None):
+    N, E = graph.n_nodes, graph.n_edges
+    dx = _empty((N, plan.D_in, plan.C)) if dx is None else dx
+    dvec = _empty((E, 3)) if dvec is None else dvec
+    ds = _empty((E, plan.P, plan.C)) if ds is None else ds
+    if ws is None:
+        ws = workspace(conv_workspace_size(plan, graph)[1])
+    _check(lib().e3_conv_bwd(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                             _ptr(vec, "vec", (E, 3)), _ptr(s, "s", (E, plan.P, plan.C)),
+                             _ptr(dm, "dm", (N, plan.D_out, plan.C)), _ptr(dx, "dx", (N, plan.D_in, plan.C)),
+                             _ptr(dvec, "dvec", (E, 3)), _ptr(ds, "ds", (E, plan.P, plan.C)),
+                             ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd")
+    return dx, dvec, ds
+
+
+# ---------------------------------------------------------------- timing
+def timing_enable(on: bool = True):
+    _check(lib().e3_timing_enable(1 if on else 0), "e3_timing_enable")
+
+
+def timing_reset():
+    _check(lib().e3_timing_reset(), "e3_timing_reset")
+
+
+def timing_read() -> dict:
+    """{kernel name: (summed ms, launches)} since the last reset."""
+    n = ct.c_int()
+    _check(lib().e3_timing_read(0, None, None, None, ct.byref(n)), "e3_timing_read")
+    cap = n.value
+    names = ct.create_string_buffer(32 * max(cap, 1))
+    ms = np.zeros(max(cap, 1), np.float64)
+    cnt = np.zeros(max(cap, 1), np.int64)
+    _check(lib().e3_timing_read(cap, ct.cast(names, ct.c_void_p), ms.ctypes.data_as(ct.c_void_p),
+                                cnt.ctypes.data_as(ct.c_void_p), ct.byref(n)), "e3_timing_read")
+    out = {}
+    for i in range(min(cap, n.value)):
+        nm = names.raw[32 * i:32 * (i + 1)].split(b"\0", 1)[0].decode()
+        out[nm] = (float(ms[i]), int(cnt[i]))
+    return out

@@ -1,0 +1,120 @@
+"""CPU-side checks of the HIP library: it loads, exports every symbol the
+header declares, validates arguments, and its host-built tables (the
+ladder-operator Clebsch-Gordan construction and the harmonic polynomials)
+equal the oracle's independent ones.  No device work is launched here.
+"""
+import ctypes as ct
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import cg as ocg
+from oracle import irreps as oirreps
+from oracle import sh as osh
+from paper_2609_35099_amd import e3mi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "e3mi.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(e3_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = e3mi.lib()
+    names = _declared()
+    assert len(names) >= 18
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(e3mi.SIGNATURES), "binding and header disagree"
+
+
+def test_status_strings():
+    L = e3mi.lib()
+    for s in range(7):
+        assert L.e3_status_str(s)
+
+
+LAYOUTS = [("8x0e+8x1o", 2, 2), ("128x0e+128x1o+128x2e", 3, 3), ("128x0e+128x1o", 3, 3),
+           ("128x0e+128x1o+128x2e+128x3o", 3, 3), ("64x0e+64x1o+64x2e+64x3o", 3, 3),
+           ("4x1o+4x0e+4x2o", 2, 3)]
+
+
+@pytest.mark.parametrize("spec", LAYOUTS)
+def test_plan_tables_equal_oracle(spec):
+    plan = e3mi.Plan(*spec)
+    lay = oirreps.layout(*spec)
+    assert (plan.P, plan.D_in, plan.D_sh, plan.D_out, plan.C) == \
+        (lay.n_paths, lay.d_in, lay.d_sh, lay.d_out, lay.channels)
+    paths = plan.paths()
+    for row, p in zip(paths, lay.paths):
+        assert tuple(row) == (p.l1, p.l2, p.l3, p.p3, p.x_off, p.y_off, p.out_off)
+    i0, i1, i2, v = plan.records()
+    ref = ocg.coo_records(lay)
+    assert len(ref) == len(v) == plan.info.nnz
+    assert [(a, b, c) for a, b, c, _ in ref] == list(zip(i0.tolist(), i1.tolist(), i2.tolist()))
+    assert np.abs(np.array([r[3] for r in ref]) - v).max() < 1e-12
+
+
+def test_plan_supported_variants():
+    for spec in LAYOUTS[:5]:
+        assert e3mi.Plan(*spec).supported, spec
+    # a layout without a compiled kernel is still a valid plan
+    p = e3mi.Plan("4x1o+4x0e+4x2o", 2, 3)
+    assert not p.supported
+    with pytest.raises(e3mi.E3Error) as ei:
+        e3mi.lib()  # noqa
+        st = e3mi.lib().e3_tp_fwd(p.handle, None, None, None, None, 1, None)
+        e3mi._check(st, "e3_tp_fwd")
+    assert ei.value.status == 2
+
+
+def test_natural_parity_filter():
+    p = e3mi.Plan("4x0e+4x1o", 2, 2, natural=True)
+    lay = oirreps.layout("4x0e+4x1o", 2, 2, parity="natural")
+    assert p.P == lay.n_paths < oirreps.layout("4x0e+4x1o", 2, 2).n_paths
+
+
+def test_sh_host_equals_oracle():
+    rng = np.random.default_rng(0)
+    g = rng.standard_normal((100, 3))
+    u = g / np.linalg.norm(g, axis=1, keepdims=True)
+    for l in range(4):
+        assert np.abs(e3mi.sh_host(l, u) - osh.sh_unit(l, u)).max() < 1e-13
+
+
+@pytest.mark.parametrize("args", [("", 2, 2), ("8x0e+4x1o", 2, 2), ("8x0q", 2, 2), ("8x0e", -1, 2),
+                                  ("8x0e", 4, 2), ("x0e", 2, 2), ("8x0e++8x1o", 2, 2)])
+def test_plan_create_rejects_bad_input(args):
+    with pytest.raises(e3mi.E3Error) as ei:
+        e3mi.Plan(*args)
+    assert ei.value.status in (1, 2)
+
+
+def test_null_and_negative_arguments_rejected_before_device_work():
+    L = e3mi.lib()
+    h = ct.c_void_p()
+    assert L.e3_plan_create(None, 2, 2, 0, ct.byref(h)) == 1
+    assert L.e3_plan_create(b"8x0e", 2, 2, 7, ct.byref(h)) == 1
+    assert L.e3_sh(5, None, None, 10, None) == 1
+    assert L.e3_sh(2, None, None, -1, None) == 1
+    assert L.e3_sh(2, None, None, 0, None) == 0          # empty input is a no-op
+    assert L.e3_sh_bwd(2, None, None, None, 3, None) == 1
+    assert L.e3_sh_host(2, None, None, 3) == 1
+    assert L.e3_graph_create(None, None, 10, 5, -1, None, ct.byref(h)) == 1
+    assert L.e3_graph_create(None, None, -1, 0, -1, None, ct.byref(h)) == 1
+    assert L.e3_graph_create(None, None, 10, 0, 12, None, ct.byref(h)) == 1
+    assert L.e3_conv_fwd(None, None, None, None, None, None, None, 0, None) == 1
+    assert L.e3_conv_bwd(None, None, None, None, None, None, None, None, None, None, 0, None) == 1
+    plan = e3mi.Plan("8x0e+8x1o", 2, 2)
+    assert L.e3_conv_fwd(plan.handle, None, None, None, None, None, None, 0, None) == 1
+    assert L.e3_tp_fwd(plan.handle, None, None, None, None, -1, None) == 1
+    assert L.e3_tp_fwd(plan.handle, None, None, None, None, 0, None) == 0
+    assert L.e3_tp_fwd(plan.handle, None, None, None, None, 4, None) == 1
+    # misaligned pointers are refused
+    assert L.e3_tp_fwd(plan.handle, ct.c_void_p(4), ct.c_void_p(4), ct.c_void_p(4), ct.c_void_p(4), 4, None) == 1

@@ -1,0 +1,301 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
+
+Bar: relative L2 <= 1e-5 per floating-point output, bit-exact graph arrays,
+bitwise-identical repeats.  Inputs are the seeded synthetic workloads; large
+ones are checked on sampled rows the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import conv as oconv
+from oracle import graph as ograph
+from oracle import irreps as oirreps
+from oracle import sh as osh
+from oracle import tp as otp
+
+from gpu_util import (TOL, layout_of, oracle_bwd_rows, oracle_fwd_rows, rel_l2, to_dev, to_np,
+                      upload_weights)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def e3():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2609_35099_amd import e3mi
+    e3mi.lib()
+    return e3mi
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _random_graph(rng, n, e, pad=-1):
+    snd = rng.integers(0, n, e).astype(np.int32)
+    rcv = rng.integers(0, n, e).astype(np.int32)
+    rcv = np.where(rcv == snd, (rcv + 1) % n, rcv).astype(np.int32)
+    vec = (rng.standard_normal((e, 3)) * 2.0).astype(np.float32)
+    return snd, rcv, vec
+
+
+# ---------------------------------------------------------------- graph
+@pytest.mark.parametrize("case", ["cfg1", "random_pad", "empty", "isolated"])
+def test_graph_csr_bit_exact(e3, case):
+    _say("graph", case)
+    rng = np.random.default_rng(1)
+    pad = -1
+    if case == "cfg1":
+        g = synth.graph(synth.CONFIGS[1])
+        snd, rcv, n = g.sender, g.receiver, g.n_nodes
+    elif case == "random_pad":
+        n = 300
+        snd, rcv, _ = _random_graph(rng, n, 5000)
+        pad = 17
+    elif case == "empty":
+        n = 5
+        snd = rcv = np.zeros(0, np.int32)
+    else:
+        n = 1000
+        snd, rcv, _ = _random_graph(rng, 50, 700)   # nodes 50..999 isolated
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    pr, rr, ps, rs = (to_np(t) for t in G.export())
+    ref = ograph.build(snd, rcv, n, pad)
+    for got, want in zip((pr, rr, ps, rs), ref):
+        assert np.array_equal(got.astype(np.int64), want)
+
+
+def test_graph_rejects_out_of_range(e3):
+    _say("graph out of range")
+    snd = np.array([0, 1, 7], np.int32)
+    rcv = np.array([1, 2, 0], np.int32)
+    with pytest.raises(e3.E3Error) as ei:
+        e3.Graph(to_dev(snd), to_dev(rcv), 5)
+    assert ei.value.status == 3
+    with pytest.raises(e3.E3Error):
+        e3.Graph(to_dev(np.array([0, -1], np.int32)), to_dev(np.array([1, 1], np.int32)), 5)
+
+
+# ---------------------------------------------------------------- harmonics
+@pytest.mark.parametrize("lmax", [0, 1, 2, 3])
+def test_sh_and_sh_bwd(e3, lmax):
+    _say("sh", lmax)
+    rng = np.random.default_rng(2)
+    vec = (rng.standard_normal((1037, 3)) * 3).astype(np.float32)
+    vec[5] = 0.0                                   # zero vector: Y_0 = 1, zeros, dvec = 0
+    dy = rng.standard_normal((1037, (lmax + 1) ** 2)).astype(np.float32)
+    y = to_np(e3.sh(lmax, to_dev(vec)))
+    dv = to_np(e3.sh_bwd(lmax, to_dev(vec), to_dev(dy)))
+    live = np.ones(1037, bool)
+    live[5] = False
+    ref_y = osh.sh_vec(lmax, vec[live].astype(np.float64))
+    ref_dv = osh.sh_vec_vjp(lmax, vec[live].astype(np.float64), dy[live].astype(np.float64))
+    assert rel_l2(y[live], ref_y) < TOL
+    assert y[5, 0] == 1.0 and np.all(y[5, 1:] == 0.0)
+    if lmax > 0:
+        assert rel_l2(dv[live], ref_dv) < TOL
+    assert np.all(dv[5] == 0.0)
+
+
+# ---------------------------------------------------------------- tensor product
+@pytest.mark.parametrize("irreps,lsh,lout,rows", [
+    ("128x0e+128x1o+128x2e", 3, 3, 1001),   # config 2 layout, ragged batch tail
+    ("64x0e+64x1o+64x2e", 3, 3, 77),
+    ("8x0e+8x1o", 2, 2, 5),
+    ("12x0e+12x1o+12x2e+12x3o", 3, 3, 33),    # C not a power of two
+    ("100x0e+100x1o", 3, 3, 19),              # 50 lanes x 2 channels
+])
+def test_tp_parity(e3, irreps, lsh, lout, rows):
+    _say("tp", irreps, rows)
+    plan = e3.Plan(irreps, lsh, lout)
+    lay = oirreps.layout(irreps, lsh, lout)
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((rows, lay.d_in, lay.channels)).astype(np.float32)
+    g = rng.standard_normal((rows, 3))
+    y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
+    w = rng.standard_normal((rows, lay.n_paths, lay.channels)).astype(np.float32)
+    z = to_np(e3.tp_fwd(plan, to_dev(x), to_dev(y), to_dev(w)))
+    ref = otp.tp(lay, x, y, w).numpy()
+    assert rel_l2(z, ref) < TOL
+    z2 = to_np(e3.tp_fwd(plan, to_dev(x), to_dev(y), to_dev(w)))
+    assert np.array_equal(z, z2)
+
+
+def test_tp_config2_full_size_sampled(e3):
+    """Config 2 at full size (200,000 rows), checked on sampled rows."""
+    import torch
+    _say("tp config 2 full")
+    cfg = synth.CONFIGS[2]
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    lay = layout_of(cfg)
+    x, u, w = synth.tp_inputs(cfg)
+    y = osh.sh_unit(3, u.astype(np.float64)).astype(np.float32)
+    z = e3.tp_fwd(plan, to_dev(x), to_dev(y), to_dev(w))
+    torch.cuda.synchronize()
+    rows = np.concatenate([[0, 1, 7, 8, 199_999], np.random.default_rng(4).integers(0, 200_000, 59)])
+    got = to_np(z[torch.as_tensor(rows, device="cuda")])
+    ref = otp.tp(lay, x[rows], y[rows], w[rows]).numpy()
+    assert rel_l2(got, ref) < TOL
+
+
+# ---------------------------------------------------------------- convolution
+def _run_conv(e3, plan, snd, rcv, n, vec, x, s, dm, pad=-1):
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    xs, vs, ss, ds_ = to_dev(x), to_dev(vec), to_dev(s), to_dev(dm)
+    m = e3.conv_fwd(plan, G, xs, vs, ss)
+    dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, ss, ds_)
+    return G, m, dx, dvec, ds
+
+
+def _check_full(lay, snd, rcv, n, vec, x, s, dm, m, dx, dvec, ds, pad=-1):
+    ref_m = oconv.conv_fwd(lay, x, vec, s, snd, rcv, n, pad_node=pad).numpy()
+    ref = oconv.conv_bwd(lay, x, vec, s, dm, snd, rcv, n, pad_node=pad)
+    errs = dict(m=rel_l2(to_np(m), ref_m), dx=rel_l2(to_np(dx), ref["dx"].numpy()),
+                ds=rel_l2(to_np(ds), ref["ds"].numpy()), dvec=rel_l2(to_np(dvec), ref["dvec"].numpy()))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    return ref_m, ref
+
+
+def test_conv_config1_full(e3):
+    _say("conv config 1")
+    cfg = synth.CONFIGS[1]
+    g = synth.graph(cfg)
+    x = synth.node_features(cfg, g.n_nodes)
+    s = synth.edge_weights(cfg, g.vec, 0, g.sender.shape[0])
+    dm = synth.out_cotangent(cfg, g.n_nodes)
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    G, m, dx, dvec, ds = _run_conv(e3, plan, g.sender, g.receiver, g.n_nodes, g.vec, x, s, dm)
+    _check_full(layout_of(cfg), g.sender, g.receiver, g.n_nodes, g.vec, x, s, dm, m, dx, dvec, ds)
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,n,e,pad", [
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, 120, 2500, -1),
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, 90, 1800, 7),
+    ("64x0e+64x1o+64x2e+64x3o", 3, 3, 70, 1500, -1),
+    ("128x0e+128x1o", 3, 3, 200, 4000, -1),
+    ("16x0e+16x1o+16x2e", 3, 3, 40, 600, 3),
+    ("128x0e+128x1o+128x2e", 3, 3, 50, 900, -1),
+])
+def test_conv_random_graphs_full(e3, irreps, lsh, lout, n, e, pad):
+    _say("conv random", irreps, n, e, pad)
+    rng = np.random.default_rng(5)
+    lay = oirreps.layout(irreps, lsh, lout)
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    s = rng.standard_normal((e, lay.n_paths, C)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    plan = e3.Plan(irreps, lsh, lout)
+    G, m, dx, dvec, ds = _run_conv(e3, plan, snd, rcv, n, vec, x, s, dm, pad)
+    _check_full(lay, snd, rcv, n, vec, x, s, dm, m, dx, dvec, ds, pad)
+    if pad >= 0:
+        dead = (snd == pad) | (rcv == pad)
+        assert np.all(to_np(ds)[dead] == 0) and np.all(to_np(dvec)[dead] == 0)
+        assert np.all(to_np(m)[pad] == 0) and np.all(to_np(dx)[pad] == 0)
+
+
+def test_conv_degenerate_graphs(e3):
+    """No edges; a single edge; nodes without in-edges."""
+    irreps = "128x0e+128x1o+128x2e+128x3o"
+    lay = oirreps.layout(irreps, 3, 3)
+    plan = e3.Plan(irreps, 3, 3)
+    rng = np.random.default_rng(6)
+    for snd, rcv, n in [(np.zeros(0, np.int32), np.zeros(0, np.int32), 4),
+                        (np.array([2], np.int32), np.array([0], np.int32), 3)]:
+        _say("conv degenerate", len(snd))
+        e = len(snd)
+        vec = rng.standard_normal((e, 3)).astype(np.float32)
+        x = rng.standard_normal((n, lay.d_in, 128)).astype(np.float32)
+        s = rng.standard_normal((e, lay.n_paths, 128)).astype(np.float32)
+        dm = rng.standard_normal((n, lay.d_out, 128)).astype(np.float32)
+        G, m, dx, dvec, ds = _run_conv(e3, plan, snd, rcv, n, vec, x, s, dm)
+        if e == 0:
+            assert np.all(to_np(m) == 0) and np.all(to_np(dx) == 0)
+        else:
+            _check_full(lay, snd, rcv, n, vec, x, s, dm, m, dx, dvec, ds)
+            assert np.all(to_np(m)[1:] == 0)
+
+
+def test_conv_deterministic_and_invariants(e3):
+    """Bitwise-identical repeats; trilinear identity and dvec . r = 0 on GPU outputs."""
+    import torch
+    _say("conv determinism config 3")
+    cfg = synth.CONFIGS[3]
+    g = synth.graph(cfg)
+    x = synth.node_features(cfg, g.n_nodes)
+    dm = synth.out_cotangent(cfg, g.n_nodes)
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    s = upload_weights(cfg, g.vec)
+    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), g.n_nodes)
+    xs, vs, dms = to_dev(x), to_dev(g.vec), to_dev(dm)
+    outs = []
+    for _ in range(3):
+        m = e3.conv_fwd(plan, G, xs, vs, s)
+        dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, s, dms)
+        outs.append((m.clone(), dx.clone(), dvec.clone(), ds.clone()))
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert torch.equal(a, b)
+    m, dx, dvec, ds = outs[0]
+    ym = e3.sh(3, vs)
+    t_m = float((m.double() * dms.double()).sum())
+    t_x = float((dx.double() * xs.double()).sum())
+    t_s = float((ds.double() * s.double()).sum())
+    assert abs(t_x - t_m) < 1e-5 * abs(t_m) and abs(t_s - t_m) < 1e-5 * abs(t_m)
+    radial = (dvec.double() * vs.double()).sum(1).abs()
+    scale = dvec.double().norm(dim=1) * vs.double().norm(dim=1)
+    assert float((radial / scale.clamp_min(1e-30)).max()) < 1e-4
+    # sampled oracle rows
+    lay = layout_of(cfg)
+    rng = np.random.default_rng(7)
+    rs = rng.choice(g.n_nodes, 40, replace=False)
+    es = rng.choice(g.sender.shape[0], 100, replace=False)
+    W = synth.bessel_matrix(cfg)
+    sfn = lambda rows: synth.edge_weights_rows(cfg, g.vec, rows, W=W)
+    ref_m = oracle_fwd_rows(lay, x, g.vec, sfn, g.sender, g.receiver, g.n_nodes, rs)
+    ref_dx, ref_ds, ref_dv = oracle_bwd_rows(lay, x, g.vec, sfn, dm, g.sender, g.receiver, g.n_nodes, rs, es)
+    assert rel_l2(to_np(m)[rs], ref_m) < TOL
+    assert rel_l2(to_np(dx)[rs], ref_dx) < TOL
+    assert rel_l2(to_np(ds)[es], ref_ds) < TOL
+    assert rel_l2(to_np(dvec)[es], ref_dv) < TOL
+
+
+@pytest.mark.parametrize("cid", [4])
+def test_conv_full_size_sampled(e3, cid):
+    """The benchmark workload (24,000-atom water box, l<=3, 128 channels) at full
+    size, in the launch configuration the benchmark times, on sampled rows."""
+    import torch
+    _say("conv full size config", cid)
+    cfg = synth.CONFIGS[cid]
+    g = synth.graph(cfg)
+    x = synth.node_features(cfg, g.n_nodes)
+    dm = synth.out_cotangent(cfg, g.n_nodes)
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    s = upload_weights(cfg, g.vec)
+    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), g.n_nodes)
+    xs, vs, dms = to_dev(x), to_dev(g.vec), to_dev(dm)
+    m = e3.conv_fwd(plan, G, xs, vs, s)
+    dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, s, dms)
+    torch.cuda.synchronize()
+    lay = layout_of(cfg)
+    rng = np.random.default_rng(8)
+    E = g.sender.shape[0]
+    rs = np.concatenate([[0, g.n_nodes - 1], rng.choice(g.n_nodes, 22, replace=False)])
+    es = np.concatenate([[0, E - 1], rng.choice(E, 62, replace=False)])
+    W = synth.bessel_matrix(cfg) if cfg.weights == "bessel" else None
+    sfn = lambda rows: synth.edge_weights_rows(cfg, g.vec, rows, W=W)
+    ref_m = oracle_fwd_rows(lay, x, g.vec, sfn, g.sender, g.receiver, g.n_nodes, rs)
+    ref_dx, ref_ds, ref_dv = oracle_bwd_rows(lay, x, g.vec, sfn, dm, g.sender, g.receiver, g.n_nodes, rs, es)
+    ri = torch.as_tensor(rs, device="cuda")
+    ei = torch.as_tensor(es, device="cuda")
+    errs = dict(m=rel_l2(to_np(m[ri]), ref_m), dx=rel_l2(to_np(dx[ri]), ref_dx),
+                ds=rel_l2(to_np(ds[ei]), ref_ds), dvec=rel_l2(to_np(dvec[ei]), ref_dv))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
