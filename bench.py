@@ -53,6 +53,34 @@ def conv_bytes(N, E, C, D_in, D_out, P):
     return k, fwd, bwd
 
 
+KERNEL_SOURCES = ["paper_2609_35099_amd/csrc/e3mi.hip", "paper_2609_35099_amd/csrc/gen.cpp",
+                  "paper_2609_35099_amd/csrc/builder.cpp", "paper_2609_35099_amd/csrc/builder.h"]
+COUNTERS = os.path.join(ROOT, "profiles", "conv_tp_config4_hbm_bytes.txt")
+
+
+def source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    if it is missing or was taken on a different kernel source."""
+    try:
+        lines = open(COUNTERS).read().splitlines()
+    except OSError:
+        return None
+    want = source_hash()
+    for ln in lines:
+        p = ln.split()
+        if len(p) == 4 and p[0] == "traffic" and p[1] == kernel and p[2] == want:
+            return int(p[3])
+    return None
+
+
 def tp_bytes(R, C, D_in, D_sh, D_out, P):
     return R * (D_in * C + D_sh + P * C + D_out * C) * 4
 
@@ -106,6 +134,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tp", action="store_true")
     ap.add_argument("--only", choices=["all", "conv", "tp"], default="all")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run one plain 2 GiB device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -196,7 +226,8 @@ def main():
                        "n_nodes": N, "n_edges": E, "channels": C, "paths": plan.P,
                        "D_in": plan.D_in, "D_out": plan.D_out},
             "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                         "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None},
+                         "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                         "traffic": counter_traffic(dom), "alg_bytes": kb[dom]},
             "step_alg_GBps": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9, 1),
             "step_alg_frac": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "fwd_alg_bytes": fwd_b, "bwd_alg_bytes": bwd_b,
@@ -239,6 +270,21 @@ def main():
                      "event_ms": round(a0.elapsed_time(a1) / args.steps, 4)}
         log(f"tp: {t_ms:.3f} ms, {out['tp']['alg_GBps']} GB/s")
         del tz, txd, twd, ty
+
+    if args.copy_probe:
+        n = (2 << 30) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        dst.copy_(src)
+        c1.record()
+        torch.cuda.synchronize()
+        out["copy_probe"] = {"bytes_each_way": 2 << 30, "ms": round(c0.elapsed_time(c1), 4),
+                             "GBps_rw": round(2 * (2 << 30) / (c0.elapsed_time(c1) * 1e-3) / 1e9, 1)}
+        del src, dst
 
     # ---------------------------------------------------------------- cpu
     if not args.no_cpu_baseline and args.only in ("all", "conv"):

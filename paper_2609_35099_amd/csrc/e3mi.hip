@@ -95,6 +95,23 @@ struct TimedLaunch {
 constexpr int kWave = 64;
 constexpr int kXcd = 8;
 
+// Build-time tuning knobs: minimum resident waves per SIMD requested from the
+// compiler for the forward and backward sweeps, and channels per lane of the
+// backward sweep when C > 64.
+#ifndef E3_FWD_MIN_WAVES
+#define E3_FWD_MIN_WAVES 3
+#endif
+#ifndef E3_BWD_MIN_WAVES
+#define E3_BWD_MIN_WAVES 2
+#endif
+#ifndef E3_BWD_CPL
+#define E3_BWD_CPL 1
+#endif
+#ifndef E3_FWD_CPL
+#define E3_FWD_CPL 2
+#endif
+constexpr int kMaxChannels = 1024;
+
 typedef float f2v __attribute__((ext_vector_type(2)));
 typedef float f4v __attribute__((ext_vector_type(4)));
 
@@ -150,8 +167,65 @@ __device__ __forceinline__ void st_row(float* __restrict__ p, const float (&v)[C
   }
 }
 
+// Rows of C floats addressed through a buffer resource: a wave-uniform base
+// (one edge's or one node's block of rows), a per-lane byte offset (the lane's
+// channels) and a per-row scalar offset, so no per-row vector address math.
+// Offsets outside the block read as zero and stores there are dropped.
+struct RowBuf {
+  __amdgpu_buffer_rsrc_t r;
+  int voff;      // lane's first channel, bytes
+  int rowbytes;  // C * 4
+};
+
+__device__ __forceinline__ RowBuf row_buf(const float* base, int64_t nbytes, int q, int C) {
+  RowBuf b;
+  b.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0,
+                                          (int)(nbytes < 0x7fffffff ? nbytes : 0x7fffffff), 0x00020000);
+  b.voff = q * 4;
+  b.rowbytes = C * 4;
+  return b;
+}
+
+constexpr int kNT = 2;  // non-temporal (streamed once)
+
+template <int CPL, int AUX = 0>
+__device__ __forceinline__ void bld(const RowBuf& b, int row, float (&v)[CPL]) {
+  const int so = row * b.rowbytes;
+  if constexpr (CPL == 1) {
+    v[0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b.r, b.voff, so, AUX));
+  } else if constexpr (CPL == 2) {
+    f2v t = __builtin_bit_cast(f2v, __builtin_amdgcn_raw_buffer_load_b64(b.r, b.voff, so, AUX));
+    v[0] = t.x, v[1] = t.y;
+  } else {
+    f4v t = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(b.r, b.voff, so, AUX));
+    v[0] = t.x, v[1] = t.y, v[2] = t.z, v[3] = t.w;
+  }
+}
+
+template <int CPL, int AUX = 0>
+__device__ __forceinline__ void bst(const RowBuf& b, int row, const float (&v)[CPL]) {
+  const int so = row * b.rowbytes;
+  if constexpr (CPL == 1) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v[0]), b.r, b.voff, so, AUX);
+  } else if constexpr (CPL == 2) {
+    typedef unsigned u2v __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u2v, f2v{v[0], v[1]}), b.r, b.voff, so, AUX);
+  } else {
+    typedef unsigned u4v __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, f4v{v[0], v[1], v[2], v[3]}), b.r, b.voff, so,
+                                           AUX);
+  }
+}
+
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
+
+// First channel and active lanes of a slab.
+template <int CPL>
+__device__ __forceinline__ void slab_of(int C, int sl, int& ch0, int& lanes) {
+  ch0 = sl * kWave * CPL;
+  lanes = imin(kWave, (C - ch0) / CPL);
+}
 
 // Unit vector of an edge; a zero vector maps to 0 (then Y_0 = 1, all else 0).
 __device__ __forceinline__ void unit_of(const float* __restrict__ vec, int64_t e, float& ux, float& uy,
@@ -254,12 +328,15 @@ constexpr int kTpRows = 8;  // rows whose pre-contraction is staged per LDS batc
 template <class V, int CPL>
 __global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const float* __restrict__ y,
                                               const float* __restrict__ w, float* __restrict__ z, int64_t rows,
-                                              int C, int lanes) {
+                                              int C, int nslab) {
   using T = typename V::TP;
   __shared__ f4v smem[(kTpRows * T::NA + 3) / 4];
   float* sA = reinterpret_cast<float*>(smem);
   const int lane = threadIdx.x;
-  const int64_t r0 = (int64_t)blockIdx.x * kTpRows;
+  const int sl = blockIdx.x % nslab;
+  int ch0, lanes;
+  slab_of<CPL>(C, sl, ch0, lanes);
+  const int64_t r0 = (int64_t)(blockIdx.x / nslab) * kTpRows;
   const int n = (int)((rows - r0) < kTpRows ? (rows - r0) : kTpRows);
   if (lane < n) {
     float Y[V::D_SH];
@@ -269,16 +346,18 @@ __global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const
   }
   __syncthreads();
   if (lane >= lanes) return;
-  const int q = lane * CPL;
+  const int q = ch0 + lane * CPL;
   for (int j = 0; j < n; ++j) {
     const int64_t r = r0 + j;
     float xv[T::NXR][CPL], wv[T::NPATH][CPL];
+    const RowBuf xb = row_buf(x + r * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+    const RowBuf wb = row_buf(w + r * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+    const RowBuf zb = row_buf(z + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
-    for (int i = 0; i < T::NXR; ++i) ld_row_nt<CPL>(x + (r * V::D_IN + T::XROW[i]) * C + q, xv[i]);
+    for (int i = 0; i < T::NXR; ++i) bld<CPL, kNT>(xb, T::XROW[i], xv[i]);
 #pragma unroll
-    for (int i = 0; i < T::NPATH; ++i) ld_row_nt<CPL>(w + (r * V::NP + T::PATH[i]) * C + q, wv[i]);
-    float* zr = z + r * V::D_OUT * C + q;
-    auto st = [&](int row, const float (&v)[CPL]) { st_row_nt<CPL>(zr + (int64_t)row * C, v); };
+    for (int i = 0; i < T::NPATH; ++i) bld<CPL, kNT>(wb, T::PATH[i], wv[i]);
+    auto st = [&](int row, const float (&v)[CPL]) { bst<CPL, kNT>(zb, row, v); };
     T::template rows<CPL>(sA + j * T::NA, xv, wv, st);
   }
 }
@@ -302,27 +381,34 @@ struct ConvArgs {
   int n_nodes;
   int chunk;  // receivers per XCD
   int C;
-  int lanes;
+  int nslab;  // channel slabs of 64 lanes x CPL channels
 };
 
-// Receiver and group of this wave: XCD k = blockIdx % 8 walks receivers
-// [k*chunk, (k+1)*chunk); the groups of one receiver are consecutive.
+// Receiver, group and channel slab of this wave: XCD k = blockIdx % 8 walks
+// receivers [k*chunk, (k+1)*chunk); the (group, slab) waves of one receiver are
+// consecutive on that XCD.
 template <int NG>
-__device__ __forceinline__ bool task_of(const ConvArgs& a, int& b, int& g) {
+__device__ __forceinline__ bool task_of(const ConvArgs& a, int& b, int& g, int& sl) {
   const int bid = blockIdx.x;
   const int xcd = bid % kXcd, slot = bid / kXcd;
-  g = slot % NG;
-  const int rl = slot / NG;
+  const int per = NG * a.nslab;
+  const int t = slot % per;
+  g = t / a.nslab;
+  sl = t % a.nslab;
+  const int rl = slot / per;
   b = xcd * a.chunk + rl;
   return rl < a.chunk && b < a.n_nodes;
 }
 
+
 template <class V, int G, int CPL>
-__device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, float* sA) {
+__device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float* sA) {
   using F = typename V::template FG<G>;
   const int lane = threadIdx.x;
-  const bool act = lane < a.lanes;
-  const int C = a.C, q = lane * CPL;
+  int ch0, lanes;
+  slab_of<CPL>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane * CPL;
   const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
   float acc[F::NROW][CPL];
 #pragma unroll
@@ -331,74 +417,93 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, float* sA) {
     for (int c = 0; c < CPL; ++c) acc[i][c] = 0.0f;
   for (int eb = e0; eb < e1; eb += kEdgeBatch) {
     const int n = imin(kEdgeBatch, e1 - eb);
+    // lane j < n owns edge eb+j for the batch: indices, harmonics, pre-contraction
+    int my_e = 0, my_src = 0;
     if (lane < n) {
-      const int e = a.eid[eb + lane];
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
       float ux, uy, uz, inv;
-      unit_of(a.vec, e, ux, uy, uz, inv);
+      unit_of(a.vec, my_e, ux, uy, uz, inv);
       float Y[V::D_SH];
       V::sh(ux, uy, uz, Y);
       F::make_A(Y, sA + lane * F::NA);
     }
     __syncthreads();
     if (act) {
-      for (int j = 0; j < n; ++j) {
-        const int64_t e = uniform(a.eid[eb + j]);
-        const int64_t snd = uniform(a.src[eb + j]);
-        float xv[F::NXR][CPL], sv[F::NPATH][CPL];
+      // two register buffers: the rows of edge j+1 are in flight while edge j computes
+      float xa[F::NXR][CPL], sa[F::NPATH][CPL], xb[F::NXR][CPL], sb[F::NPATH][CPL];
+      auto load = [&](int j, float (&xv)[F::NXR][CPL], float (&sv)[F::NPATH][CPL]) {
+        const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+        const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+        const RowBuf xb_ = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf sb_ = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
 #pragma unroll
-        for (int i = 0; i < F::NXR; ++i) ld_row<CPL>(a.x + (snd * V::D_IN + F::XROW[i]) * C + q, xv[i]);
+        for (int i = 0; i < F::NXR; ++i) bld<CPL>(xb_, F::XROW[i], xv[i]);
 #pragma unroll
-        for (int i = 0; i < F::NPATH; ++i) ld_row_nt<CPL>(a.s + (e * V::NP + F::PATH[i]) * C + q, sv[i]);
-        F::template edge<CPL>(sA + j * F::NA, xv, sv, acc);
+        for (int i = 0; i < F::NPATH; ++i) bld<CPL, kNT>(sb_, F::PATH[i], sv[i]);
+      };
+      load(0, xa, sa);
+      for (int j = 0; j < n; j += 2) {
+        if (j + 1 < n) load(j + 1, xb, sb);
+        F::template edge<CPL>(sA + j * F::NA, xa, sa, acc);
+        if (j + 1 < n) {
+          if (j + 2 < n) load(j + 2, xa, sa);
+          F::template edge<CPL>(sA + (j + 1) * F::NA, xb, sb, acc);
+        }
       }
     }
     __syncthreads();
   }
   if (act) {
-    float* mb = a.m + (int64_t)b * V::D_OUT * C + q;
+    const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
-    for (int i = 0; i < F::NROW; ++i) st_row_nt<CPL>(mb + (int64_t)F::OROW[i] * C, acc[i]);
+    for (int i = 0; i < F::NROW; ++i) bst<CPL, kNT>(mb, F::OROW[i], acc[i]);
   }
 }
 
 template <class V, int G, int CPL>
-__device__ __forceinline__ void fwd_dispatch(const ConvArgs& a, int b, int g, float* sA) {
+__device__ __forceinline__ void fwd_dispatch(const ConvArgs& a, int b, int g, int sl, float* sA) {
   if constexpr (G < V::NFG) {
     if (g == G)
-      fwd_task<V, G, CPL>(a, b, sA);
+      fwd_task<V, G, CPL>(a, b, sl, sA);
     else
-      fwd_dispatch<V, G + 1, CPL>(a, b, g, sA);
+      fwd_dispatch<V, G + 1, CPL>(a, b, g, sl, sA);
   }
 }
 
 template <class V, int CPL>
-__global__ __launch_bounds__(kWave, 3) void k_conv_fwd(ConvArgs a) {
+__global__ __launch_bounds__(kWave, E3_FWD_MIN_WAVES) void k_conv_fwd(ConvArgs a) {
   __shared__ f4v smem[(kEdgeBatch * V::MAX_NA_F + 3) / 4];
-  int b, g;
-  if (!task_of<V::NFG>(a, b, g)) return;
-  fwd_dispatch<V, 0, CPL>(a, b, g, reinterpret_cast<float*>(smem));
+  int b, g, sl;
+  if (!task_of<V::NFG>(a, b, g, sl)) return;
+  fwd_dispatch<V, 0, CPL>(a, b, g, sl, reinterpret_cast<float*>(smem));
 }
 
 template <class V, int G, int CPL>
-__device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, float* sA, float* sY) {
+__device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float* sA, float* sY) {
   using B = typename V::template BG<G>;
   const int lane = threadIdx.x;
-  const bool act = lane < a.lanes;
-  const int C = a.C, q = lane * CPL;
+  int ch0, lanes;
+  slab_of<CPL>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane * CPL;
   const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
   if (e0 == e1) return;
   float dmv[B::NROW][CPL];
   if (act) {
-    const float* db = a.dm + (int64_t)b * V::D_OUT * C + q;
+    const RowBuf db = row_buf(a.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
-    for (int i = 0; i < B::NROW; ++i) ld_row<CPL>(db + (int64_t)B::OROW[i] * C, dmv[i]);
+    for (int i = 0; i < B::NROW; ++i) bld<CPL>(db, B::OROW[i], dmv[i]);
   }
   for (int eb = e0; eb < e1; eb += kEdgeBatch) {
     const int n = imin(kEdgeBatch, e1 - eb);
+    int my_e = 0, my_src = 0, my_slot = 0;
     if (lane < n) {
-      const int e = a.eid[eb + lane];
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
+      my_slot = a.r2s[eb + lane];
       float ux, uy, uz, inv;
-      unit_of(a.vec, e, ux, uy, uz, inv);
+      unit_of(a.vec, my_e, ux, uy, uz, inv);
       float Y[V::D_SH];
       V::sh(ux, uy, uz, Y);
 #pragma unroll
@@ -406,111 +511,128 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, float* sA, fl
       B::make_A(Y, sA + lane * B::NA);
     }
     __syncthreads();
-    for (int j = 0; j < n; ++j) {
-      const int pos = eb + j;
-      const int64_t e = uniform(a.eid[pos]);
+    float xa[B::NXR][CPL], sa[B::NPATH][CPL], xb[B::NXR][CPL], sb[B::NPATH][CPL];
+    auto load = [&](int j, float (&xv)[B::NXR][CPL], float (&sv)[B::NPATH][CPL]) {
+      if (!act) return;
+      const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+      const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+      const RowBuf xb_ = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf sb_ = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+#pragma unroll
+      for (int i = 0; i < B::NXR; ++i) bld<CPL>(xb_, B::XROW[i], xv[i]);
+#pragma unroll
+      for (int i = 0; i < B::NPATH; ++i) bld<CPL, kNT>(sb_, B::PATH[i], sv[i]);
+    };
+    auto compute = [&](int j, const float (&xv)[B::NXR][CPL], const float (&sv)[B::NPATH][CPL]) {
+      const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+      const int64_t slot = __builtin_amdgcn_readlane(my_slot, j);
       float dy[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) dy[i] = 0.0f;
       if (act) {
-        const int64_t snd = uniform(a.src[pos]);
-        const int64_t slot = uniform(a.r2s[pos]);
-        float xv[B::NXR][CPL], sv[B::NPATH][CPL], t[B::NXR][CPL], Yv[V::D_SH];
+        float t[B::NXR][CPL], Yv[V::D_SH];
 #pragma unroll
-        for (int i = 0; i < B::NXR; ++i) {
-          ld_row<CPL>(a.x + (snd * V::D_IN + B::XROW[i]) * C + q, xv[i]);
+        for (int i = 0; i < B::NXR; ++i)
 #pragma unroll
           for (int c = 0; c < CPL; ++c) t[i][c] = 0.0f;
-        }
-#pragma unroll
-        for (int i = 0; i < B::NPATH; ++i) ld_row_nt<CPL>(a.s + (e * V::NP + B::PATH[i]) * C + q, sv[i]);
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
-        float* dse = a.ds + e * V::NP * C + q;
-        auto st = [&](int pl, const float (&v)[CPL]) { st_row_nt<CPL>(dse + (int64_t)B::PATH[pl] * C, v); };
+        const RowBuf dsb = row_buf(a.ds + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        auto st = [&](int pl, const float (&v)[CPL]) { bst<CPL, kNT>(dsb, B::PATH[pl], v); };
         float dyl[V::D_SH];
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0f;
         B::template edge<CPL>(sA + j * B::NA, Yv, xv, sv, dmv, t, dyl, st);
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
-        float* Te = a.T + slot * V::D_IN * C + q;
+        const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
-        for (int i = 0; i < B::NXR; ++i) st_row<CPL>(Te + (int64_t)B::XROW[i] * C, t[i]);
+        for (int i = 0; i < B::NXR; ++i) bst<CPL>(Tb, B::XROW[i], t[i]);
       }
       const float tot = wave_reduce16(dy, lane);
-      if ((lane & 3) == 0) a.DY[((int64_t)pos * V::NBG + G) * 16 + (lane >> 2)] = tot;
+      if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+    };
+    load(0, xa, sa);
+    for (int j = 0; j < n; j += 2) {
+      if (j + 1 < n) load(j + 1, xb, sb);
+      compute(j, xa, sa);
+      if (j + 1 < n) {
+        if (j + 2 < n) load(j + 2, xa, sa);
+        compute(j + 1, xb, sb);
+      }
     }
     __syncthreads();
   }
 }
 
 template <class V, int G, int CPL>
-__device__ __forceinline__ void bwd_dispatch(const ConvArgs& a, int b, int g, float* sA, float* sY) {
+__device__ __forceinline__ void bwd_dispatch(const ConvArgs& a, int b, int g, int sl, float* sA, float* sY) {
   if constexpr (G < V::NBG) {
     if (g == G)
-      bwd_task<V, G, CPL>(a, b, sA, sY);
+      bwd_task<V, G, CPL>(a, b, sl, sA, sY);
     else
-      bwd_dispatch<V, G + 1, CPL>(a, b, g, sA, sY);
+      bwd_dispatch<V, G + 1, CPL>(a, b, g, sl, sA, sY);
   }
 }
 
 template <class V, int CPL>
-__global__ __launch_bounds__(kWave, 2) void k_conv_bwd_edges(ConvArgs a) {
+__global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd_edges(ConvArgs a) {
   __shared__ f4v smem[(kEdgeBatch * (V::MAX_NA_B + V::D_SH) + 3) / 4];
-  int b, g;
-  if (!task_of<V::NBG>(a, b, g)) return;
+  int b, g, sl;
+  if (!task_of<V::NBG>(a, b, g, sl)) return;
   float* sA = reinterpret_cast<float*>(smem);
-  bwd_dispatch<V, 0, CPL>(a, b, g, sA, sA + kEdgeBatch * V::MAX_NA_B);
+  bwd_dispatch<V, 0, CPL>(a, b, g, sl, sA, sA + kEdgeBatch * V::MAX_NA_B);
 }
 
 // dx[a] = sum of the partials of a's out-edges, in sender-CSR order.
 template <int D_IN, int CPL>
 __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__ T, float* __restrict__ dx,
                                                        const int* __restrict__ rowptr_s, int n_nodes, int chunk,
-                                                       int C, int lanes) {
+                                                       int C, int nslab) {
   const int bid = blockIdx.x;
-  const int node = (bid % kXcd) * chunk + bid / kXcd;
-  if (bid / kXcd >= chunk || node >= n_nodes) return;
+  const int slot = bid / kXcd, sl = slot % nslab, rl = slot / nslab;
+  const int node = (bid % kXcd) * chunk + rl;
+  if (rl >= chunk || node >= n_nodes) return;
   const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<CPL>(C, sl, ch0, lanes);
   if (lane >= lanes) return;
-  const int q = lane * CPL;
+  const int q = ch0 + lane * CPL;
   const int s0 = uniform(rowptr_s[node]), s1 = uniform(rowptr_s[node + 1]);
   float acc[D_IN][CPL];
 #pragma unroll
   for (int i = 0; i < D_IN; ++i)
 #pragma unroll
     for (int c = 0; c < CPL; ++c) acc[i][c] = 0.0f;
-  for (int sl = s0; sl < s1; ++sl) {
-    const float* Tp = T + (int64_t)sl * D_IN * C + q;
+  for (int t = s0; t < s1; ++t) {
+    const RowBuf tb = row_buf(T + (int64_t)t * D_IN * C, (int64_t)D_IN * C * 4, q, C);
 #pragma unroll
     for (int i = 0; i < D_IN; ++i) {
       float v[CPL];
-      ld_row_nt<CPL>(Tp + (int64_t)i * C, v);
+      bld<CPL, kNT>(tb, i, v);
 #pragma unroll
       for (int c = 0; c < CPL; ++c) acc[i][c] += v[c];
     }
   }
-  float* o = dx + (int64_t)node * D_IN * C + q;
+  const RowBuf ob = row_buf(dx + (int64_t)node * D_IN * C, (int64_t)D_IN * C * 4, q, C);
 #pragma unroll
-  for (int i = 0; i < D_IN; ++i) st_row_nt<CPL>(o + (int64_t)i * C, acc[i]);
+  for (int i = 0; i < D_IN; ++i) bst<CPL, kNT>(ob, i, acc[i]);
 }
 
 // dvec of each live edge from its harmonic cotangent (summed over groups).
 template <class V>
 __global__ __launch_bounds__(256) void k_conv_bwd_dvec(const float* __restrict__ vec, const float* __restrict__ DY,
                                                        const int* __restrict__ eid, float* __restrict__ dvec,
-                                                       int64_t n_live) {
+                                                       int64_t n_live, int nslab) {
   const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (pos >= n_live) return;
   const int64_t e = eid[pos];
   float dY[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) dY[i] = 0.0f;
+  for (int g = 0; g < V::NBG * nslab; ++g)
 #pragma unroll
-  for (int g = 0; g < V::NBG; ++g)
-#pragma unroll
-    for (int i = 0; i < V::D_SH; ++i) dY[i] += DY[(pos * V::NBG + g) * 16 + i];
+    for (int i = 0; i < V::D_SH; ++i) dY[i] += DY[(pos * V::NBG * nslab + g) * 16 + i];
   float ux, uy, uz, inv;
   unit_of(vec, e, ux, uy, uz, inv);
   float gx, gy, gz, ox, oy, oz;
@@ -584,7 +706,9 @@ struct e3_plan {
   e3b::Layout lay;
   std::vector<e3b::Record> recs;
   int variant = -1;
-  int cpl = 0, lanes = 0;
+  // Channels per lane of the forward / tensor-product / dx kernels (the
+  // backward sweep always uses 1) and the number of 64-lane channel slabs.
+  int cpl_f = 0, cpl_b = 0, nslab_f = 0, nslab_b = 0;
 };
 
 struct e3_graph {
@@ -611,7 +735,7 @@ template <class V>
 Ws bwd_ws(const e3_plan* p, const e3_graph* g) {
   Ws w;
   w.t_bytes = align256((size_t)g->n_live * V::D_IN * p->lay.C * sizeof(float));
-  w.dy_bytes = align256((size_t)g->n_live * V::NBG * 16 * sizeof(float));
+  w.dy_bytes = align256((size_t)g->n_live * V::NBG * p->nslab_b * 16 * sizeof(float));
   return w;
 }
 
@@ -624,7 +748,6 @@ ConvArgs base_args(const e3_plan* p, const e3_graph* g) {
   a.n_nodes = (int)g->n_nodes;
   a.chunk = (int)((g->n_nodes + kXcd - 1) / kXcd);
   a.C = p->lay.C;
-  a.lanes = p->lanes;
   return a;
 }
 
@@ -633,8 +756,9 @@ e3_status run_fwd(const e3_plan* p, const e3_graph* g, const float* x, const flo
                   hipStream_t st) {
   ConvArgs a = base_args(p, g);
   a.x = x, a.vec = vec, a.s = s, a.m = m;
+  a.nslab = p->nslab_f;
   if (g->n_nodes == 0) return E3_OK;
-  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG);
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
   {
     TimedLaunch t_("conv_fwd", st);
     hipLaunchKernelGGL((k_conv_fwd<V, CPL>), dim3(grid), dim3(kWave), 0, st, a);
@@ -643,7 +767,7 @@ e3_status run_fwd(const e3_plan* p, const e3_graph* g, const float* x, const flo
   return E3_OK;
 }
 
-template <class V, int CPL>
+template <class V, int CPLX>
 e3_status run_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
                   const float* dm, float* dx, float* dvec, float* ds, void* ws, hipStream_t st) {
   if (g->n_nodes == 0) return E3_OK;
@@ -652,22 +776,26 @@ e3_status run_bwd(const e3_plan* p, const e3_graph* g, const float* x, const flo
   a.x = x, a.vec = vec, a.s = s, a.dm = dm, a.ds = ds;
   a.T = reinterpret_cast<float*>(ws);
   a.DY = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.t_bytes);
+  a.nslab = p->nslab_b;
   if (g->n_live > 0) {
-    const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG);
+    const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
     TimedLaunch t_("conv_bwd_edges", st);
-    hipLaunchKernelGGL((k_conv_bwd_edges<V, CPL>), dim3(grid), dim3(kWave), 0, st, a);
+    if (p->cpl_b == 1)
+      hipLaunchKernelGGL((k_conv_bwd_edges<V, 1>), dim3(grid), dim3(kWave), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_conv_bwd_edges<V, E3_BWD_CPL>), dim3(grid), dim3(kWave), 0, st, a);
     E3_HIP(hipGetLastError());
   }
   {
     TimedLaunch t_("conv_bwd_dx", st);
-    hipLaunchKernelGGL((k_conv_bwd_dx<V::D_IN, CPL>), dim3((unsigned)(kXcd * a.chunk)), dim3(kWave), 0, st, a.T, dx,
-                       g->rowptr_s, a.n_nodes, a.chunk, a.C, a.lanes);
+    hipLaunchKernelGGL((k_conv_bwd_dx<V::D_IN, CPLX>), dim3((unsigned)(kXcd * a.chunk * p->nslab_f)), dim3(kWave), 0,
+                       st, a.T, dx, g->rowptr_s, a.n_nodes, a.chunk, a.C, p->nslab_f);
   }
   E3_HIP(hipGetLastError());
   if (g->n_live > 0) {
     TimedLaunch t_("conv_bwd_dvec", st);
     hipLaunchKernelGGL((k_conv_bwd_dvec<V>), dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, vec, a.DY, g->eid_r,
-                       dvec, g->n_live);
+                       dvec, g->n_live, p->nslab_b);
     E3_HIP(hipGetLastError());
   }
   if (g->n_pad > 0) {
@@ -686,8 +814,9 @@ e3_status run_tp(const e3_plan* p, const float* x, const float* y, const float* 
   if (rows == 0) return E3_OK;
   {
     TimedLaunch t_("tp_fwd", st);
-    hipLaunchKernelGGL((k_tp<V, CPL>), dim3(blocks_for(rows, kTpRows)), dim3(kWave), 0, st, x, y, w, z, rows,
-                       p->lay.C, p->lanes);
+    const int64_t tiles = (rows + kTpRows - 1) / kTpRows;
+    hipLaunchKernelGGL((k_tp<V, CPL>), dim3((unsigned)(tiles * p->nslab_f)), dim3(kWave), 0, st, x, y, w, z, rows,
+                       p->lay.C, p->nslab_f);
   }
   E3_HIP(hipGetLastError());
   return E3_OK;
@@ -723,6 +852,7 @@ constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 int cpl_index(int cpl) { return cpl == 1 ? 0 : 1; }
+int cpl_of(const e3_plan* p) { return p->cpl_f; }
 
 e3_status check_plan(const e3_plan* p) {
   if (!p) return E3_ERR_INVALID_ARG;
@@ -823,17 +953,20 @@ e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsign
     return E3_ERR_UNSUPPORTED;
   }
   const std::string sig = e3b::path_signature(p->lay);
-  // channels per lane: a wave holds at most 64 lanes of channels
+  // Channels: multiples of 4 up to kMaxChannels.  The forward, tensor-product
+  // and dx kernels give each lane 2 consecutive channels when C > 64 (one lane
+  // per channel otherwise); the backward sweep gives each lane 1.  Channels
+  // beyond one wave are covered by further 64-lane slabs.
   const int C = p->lay.C;
-  int cpl = 0;
-  if (C % 4 == 0 && C >= 4) cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 0);
-  if (cpl) {
+  if (C >= 4 && C % 4 == 0 && C <= kMaxChannels) {
     for (int i = 0; i < kNumVariants; ++i)
       if (sig == kVariants[i].sig && p->lay.d_sh == kVariants[i].d_sh) p->variant = i;
   }
   if (p->variant >= 0) {
-    p->cpl = cpl;
-    p->lanes = C / cpl;
+    p->cpl_f = C <= kWave ? 1 : E3_FWD_CPL;
+    p->nslab_f = (C + kWave * p->cpl_f - 1) / (kWave * p->cpl_f);
+    p->cpl_b = C <= kWave ? 1 : E3_BWD_CPL;
+    p->nslab_b = (C + kWave * p->cpl_b - 1) / (kWave * p->cpl_b);
   }
   *out = p;
   return E3_OK;
@@ -1063,7 +1196,7 @@ e3_status e3_tp_fwd(const e3_plan* p, const float* x, const float* y, const floa
   if (rows > 0 && (!x || !y || !w || !z || !aligned16(x) || !aligned16(w) || !aligned16(z))) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
   const VariantOps& v = kVariants[p->variant];
-  return v.tp[cpl_index(p->cpl)](p, x, y, w, z, rows, reinterpret_cast<hipStream_t>(stream));
+  return v.tp[cpl_index(cpl_of(p))](p, x, y, w, z, rows, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_workspace_size(const e3_plan* p, const e3_graph* g, size_t* fwd_bytes, size_t* bwd_bytes) {
@@ -1085,7 +1218,7 @@ e3_status e3_conv_fwd(const e3_plan* p, const e3_graph* g, const float* x, const
   if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x))) return E3_ERR_INVALID_ARG;
   if (g->n_live > 0 && (!vec || !s || !aligned16(s))) return E3_ERR_INVALID_ARG;
   const VariantOps& v = kVariants[p->variant];
-  return v.fwd[cpl_index(p->cpl)](p, g, x, vec, s, m, reinterpret_cast<hipStream_t>(stream));
+  return v.fwd[cpl_index(cpl_of(p))](p, g, x, vec, s, m, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
@@ -1101,7 +1234,7 @@ e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const
   Ws w = v.ws(p, g);
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
-  return v.bwd[cpl_index(p->cpl)](p, g, x, vec, s, dm, dx, dvec, ds, ws, reinterpret_cast<hipStream_t>(stream));
+  return v.bwd[cpl_index(cpl_of(p))](p, g, x, vec, s, dm, dx, dvec, ds, ws, reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -17,6 +17,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <map>
 #include <set>
 #include <sstream>
@@ -101,9 +102,9 @@ int bwd_cost(const PathInfo& pi) {
 }
 
 // Contiguous partition of [0, n) into g parts minimising the largest cost,
-// each part having at most rmax output rows.
-std::vector<std::pair<int, int>> partition(const std::vector<int>& cost, const std::vector<int>& rows,
-                                           int g, int rmax) {
+// each part [s, i) satisfying fits(s, i).
+template <class Fits>
+std::vector<std::pair<int, int>> partition(const std::vector<int>& cost, int g, Fits fits) {
   const int n = (int)cost.size();
   const int INF = 1 << 29;
   std::vector<std::vector<int>> best(g + 1, std::vector<int>(n + 1, INF));
@@ -112,9 +113,9 @@ std::vector<std::pair<int, int>> partition(const std::vector<int>& cost, const s
   for (int j = 1; j <= g; ++j)
     for (int i = 1; i <= n; ++i)
       for (int s = i - 1; s >= 0; --s) {
-        int c = 0, r = 0;
-        for (int t = s; t < i; ++t) c += cost[t], r += rows[t];
-        if (r > rmax) break;
+        if (!fits(s, i)) continue;
+        int c = 0;
+        for (int t = s; t < i; ++t) c += cost[t];
         if (best[j - 1][s] >= INF) continue;
         int v = std::max(best[j - 1][s], c);
         if (v < best[j][i]) best[j][i] = v, cut[j][i] = s;
@@ -443,8 +444,8 @@ std::string tag_of(const VariantSpec& v) {
 }  // namespace
 
 int main(int argc, char** argv) {
-  if (argc != 2) {
-    std::fprintf(stderr, "usage: gen <out.inc>\n");
+  if (argc < 2) {
+    std::fprintf(stderr, "usage: gen <out.inc> [fwd_target fwd_regs fwd_rows]\n");
     return 2;
   }
   // Compiled variants: x blocks of degrees ls (any parities, all paths kept),
@@ -455,8 +456,12 @@ int main(int argc, char** argv) {
       {{0, 1}, 3, 3, false},
       {{0, 1, 2, 3}, 3, 3, false},
   };
-  const int FWD_TARGET = 150;   // per-wave FMA budget per edge and channel (forward)
-  const int FWD_RMAX = 40;      // output rows held in registers per wave
+  // Forward groups: contiguous paths balanced on per-channel FMA work, each
+  // within a register budget (per channel of a lane: accumulators + two
+  // buffered copies of its x rows and path weights).
+  const int FWD_TARGET = argc > 2 ? std::atoi(argv[2]) : 150;
+  const int FWD_REGS = argc > 3 ? std::atoi(argv[3]) : 1000;
+  const int FWD_RMAX = argc > 4 ? std::atoi(argv[4]) : 40;
   const int BWD_TARGET = 640;
   const int BWD_RMAX = 56;
 
@@ -484,10 +489,23 @@ int main(int argc, char** argv) {
       total_f += fc[k];
     }
     // forward groups: contiguous paths, balanced cost
+    auto fwd_regs = [&](int s, int e) {  // rows + 2 x rows + 2 path weights, per lane channel
+      std::set<int> xs;
+      int r = 0;
+      for (int k = s; k < e; ++k) {
+        r += rows[k];
+        for (int a = 0; a < 2 * pis[k].p.l1 + 1; ++a) xs.insert(pis[k].p.x_off + a);
+      }
+      return r + 2 * (int)xs.size() + 2 * (e - s);
+    };
     int gf = std::max(1, (int)std::lround((double)total_f / FWD_TARGET));
     std::vector<std::pair<int, int>> fparts;
     for (;; ++gf) {
-      fparts = partition(fc, rows, gf, FWD_RMAX);
+      fparts = partition(fc, gf, [&](int s, int e) {
+        int r = 0;
+        for (int k = s; k < e; ++k) r += rows[k];
+        return r <= FWD_RMAX && fwd_regs(s, e) <= FWD_REGS;
+      });
       if (!fparts.empty()) break;
     }
     // backward groups: whole x blocks (so the x cotangent rows of different

@@ -13,7 +13,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libe3mi.so")
+# E3MI_LIB may point at another build of the same library (side-by-side builds)
+LIB_PATH = os.environ.get("E3MI_LIB") or os.path.join(_HERE, "libe3mi.so")
 
 _STATUS = {0: "E3_OK", 1: "E3_ERR_INVALID_ARG", 2: "E3_ERR_UNSUPPORTED",
            3: "E3_ERR_INDEX_OUT_OF_RANGE", 4: "E3_ERR_WORKSPACE_TOO_SMALL",
