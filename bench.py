@@ -134,6 +134,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tp", action="store_true")
     ap.add_argument("--only", choices=["all", "conv", "tp"], default="all")
+    ap.add_argument("--order", choices=["generated", "cell"], default="generated",
+                    help="atom order of the water box: as generated (spatially random) or cell-sorted")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one plain 2 GiB device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -156,7 +158,7 @@ def main():
     # ---------------------------------------------------------------- conv
     cfg = synth.CONFIGS[4]
     t0 = time.perf_counter()
-    g = synth.graph(cfg)
+    g = synth.graph(cfg, order=args.order)
     x = synth.node_features(cfg, g.n_nodes)
     dm = synth.out_cotangent(cfg, g.n_nodes)
     plan = e3mi.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
@@ -222,7 +224,8 @@ def main():
             "ms_per_step": ms_step,
             "config": {"workload": "water box, 8,000 rigid H2O = 24,000 atoms, periodic, r_c 5 A; "
                                    "x 128x0e+128x1o+128x2e+128x3o, harmonics l<=3, outputs l<=3, "
-                                   "forward + backward convolution",
+                                   "forward + backward convolution"
+                                   + ("" if args.order == "generated" else "; atoms cell-sorted"),
                        "n_nodes": N, "n_edges": E, "channels": C, "paths": plan.P,
                        "D_in": plan.D_in, "D_out": plan.D_out},
             "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,

@@ -99,7 +99,7 @@ constexpr int kXcd = 8;
 // compiler for the forward and backward sweeps, and channels per lane of the
 // backward sweep when C > 64.
 #ifndef E3_FWD_MIN_WAVES
-#define E3_FWD_MIN_WAVES 3
+#define E3_FWD_MIN_WAVES 2
 #endif
 #ifndef E3_BWD_MIN_WAVES
 #define E3_BWD_MIN_WAVES 2
@@ -584,39 +584,41 @@ __global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd_edges(Conv
   bwd_dispatch<V, 0, CPL>(a, b, g, sl, sA, sA + kEdgeBatch * V::MAX_NA_B);
 }
 
-// dx[a] = sum of the partials of a's out-edges, in sender-CSR order.
-template <int D_IN, int CPL>
+// dx[a] = sum of the partials of a's out-edges, in sender-CSR order.  A
+// node's partials are one contiguous block of (out-degree) x D_in x C floats;
+// the wave reads each slot's D_in x C floats as float4s (lane l takes float4
+// l, l+64, ... of its slab) and keeps kDxVec float4 sums per lane.
+constexpr int kDxVec = 8;
+
 __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__ T, float* __restrict__ dx,
                                                        const int* __restrict__ rowptr_s, int n_nodes, int chunk,
-                                                       int C, int nslab) {
+                                                       int flat4, int nslab) {
   const int bid = blockIdx.x;
   const int slot = bid / kXcd, sl = slot % nslab, rl = slot / nslab;
   const int node = (bid % kXcd) * chunk + rl;
   if (rl >= chunk || node >= n_nodes) return;
   const int lane = threadIdx.x;
-  int ch0, lanes;
-  slab_of<CPL>(C, sl, ch0, lanes);
-  if (lane >= lanes) return;
-  const int q = ch0 + lane * CPL;
+  const int off = (sl * kWave * kDxVec + lane) * 16;  // bytes
   const int s0 = uniform(rowptr_s[node]), s1 = uniform(rowptr_s[node + 1]);
-  float acc[D_IN][CPL];
+  typedef unsigned u4v __attribute__((ext_vector_type(4)));
+  f4v acc[kDxVec];
 #pragma unroll
-  for (int i = 0; i < D_IN; ++i)
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) acc[i][c] = 0.0f;
+  for (int k = 0; k < kDxVec; ++k) acc[k] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  const int64_t slot_bytes = (int64_t)flat4 * 16;
+#pragma unroll 2
   for (int t = s0; t < s1; ++t) {
-    const RowBuf tb = row_buf(T + (int64_t)t * D_IN * C, (int64_t)D_IN * C * 4, q, C);
+    // out-of-range float4s (past D_in x C) read as zero
+    __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(T) + (int64_t)t * flat4 * 4, (short)0, (int)slot_bytes, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < D_IN; ++i) {
-      float v[CPL];
-      bld<CPL, kNT>(tb, i, v);
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) acc[i][c] += v[c];
-    }
+    for (int k = 0; k < kDxVec; ++k)
+      acc[k] += __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(r, off, k * kWave * 16, kNT));
   }
-  const RowBuf ob = row_buf(dx + (int64_t)node * D_IN * C, (int64_t)D_IN * C * 4, q, C);
+  __amdgpu_buffer_rsrc_t o = __builtin_amdgcn_make_buffer_rsrc(dx + (int64_t)node * flat4 * 4, (short)0,
+                                                               (int)slot_bytes, 0x00020000);
 #pragma unroll
-  for (int i = 0; i < D_IN; ++i) bst<CPL, kNT>(ob, i, acc[i]);
+  for (int k = 0; k < kDxVec; ++k)
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, acc[k]), o, off, k * kWave * 16, kNT);
 }
 
 // dvec of each live edge from its harmonic cotangent (summed over groups).
@@ -788,8 +790,10 @@ e3_status run_bwd(const e3_plan* p, const e3_graph* g, const float* x, const flo
   }
   {
     TimedLaunch t_("conv_bwd_dx", st);
-    hipLaunchKernelGGL((k_conv_bwd_dx<V::D_IN, CPLX>), dim3((unsigned)(kXcd * a.chunk * p->nslab_f)), dim3(kWave), 0,
-                       st, a.T, dx, g->rowptr_s, a.n_nodes, a.chunk, a.C, p->nslab_f);
+    const int flat4 = V::D_IN * a.C / 4;
+    const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
+    hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * a.chunk * nsl)), dim3(kWave), 0, st, a.T, dx,
+                       g->rowptr_s, a.n_nodes, a.chunk, flat4, nsl);
   }
   E3_HIP(hipGetLastError());
   if (g->n_live > 0) {

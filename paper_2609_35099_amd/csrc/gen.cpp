@@ -459,9 +459,9 @@ int main(int argc, char** argv) {
   // Forward groups: contiguous paths balanced on per-channel FMA work, each
   // within a register budget (per channel of a lane: accumulators + two
   // buffered copies of its x rows and path weights).
-  const int FWD_TARGET = argc > 2 ? std::atoi(argv[2]) : 150;
+  const int FWD_TARGET = argc > 2 ? std::atoi(argv[2]) : 200;
   const int FWD_REGS = argc > 3 ? std::atoi(argv[3]) : 1000;
-  const int FWD_RMAX = argc > 4 ? std::atoi(argv[4]) : 40;
+  const int FWD_RMAX = argc > 4 ? std::atoi(argv[4]) : 56;
   const int BWD_TARGET = 640;
   const int BWD_RMAX = 56;
 

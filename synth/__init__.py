@@ -233,7 +233,23 @@ class Graph:
     box: float | None
 
 
-def graph(cfg: Config) -> Graph:
+def cell_order(pos: np.ndarray, L: float, n_mol: int, cell: float = R_CUT) -> np.ndarray:
+    """Atom permutation that sorts whole molecules by the cell of their oxygen
+    (cells of side ~r_c, visited in Morton order), keeping O, H, H together."""
+    nc = max(int(L // cell), 1)
+    c3 = np.minimum((np.mod(pos[0::3], L) / (L / nc)).astype(np.int64), nc - 1)
+    code = np.zeros(n_mol, dtype=np.int64)
+    for bit in range(12):
+        for a in range(3):
+            code |= ((c3[:, a] >> bit) & 1) << (3 * bit + a)
+    mol = np.argsort(code, kind="stable")
+    return (3 * mol[:, None] + np.arange(3)[None, :]).reshape(-1)
+
+
+def graph(cfg: Config, order: str = "generated") -> Graph:
+    """Edge list of a configuration.  order="cell" renumbers the atoms of a water
+    box so that molecules are sorted by spatial cell (the as-generated order is
+    spatially random)."""
     if cfg.n_atoms:
         pos, L = uniform_cube(cfg.cid, cfg.n_atoms)
         i, j, d = _pairs_within(pos, None, 4.0)
@@ -241,6 +257,8 @@ def graph(cfg: Config) -> Graph:
         n = cfg.n_atoms
     else:
         pos, L = water_box(cfg.cid, cfg.n_mol)
+        if order == "cell":
+            pos = pos[cell_order(pos, L, cfg.n_mol)]
         i, j, d = _pairs_within(pos, L, R_CUT)
         box = L
         n = pos.shape[0]
@@ -334,3 +352,17 @@ def tp_inputs(cfg: Config, rows: int | None = None):
     u = (g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
     w = normal_f32(cfg.cid, _S, (R, P, C))
     return x, u, w
+
+
+def normal_device(cid: int, stream: int, shape, device, chunk_rows: int = 1 << 16):
+    """N(0,1) float32 tensor drawn on the device by torch's seeded generator
+    (Philox), chunk by chunk along the first axis; for arrays too large to
+    draw on the host.  Deterministic for a given (cid, stream, shape)."""
+    import torch
+    out = torch.empty(shape, dtype=torch.float32, device=device)
+    g = torch.Generator(device=device)
+    for i, r0 in enumerate(range(0, shape[0], chunk_rows)):
+        r1 = min(shape[0], r0 + chunk_rows)
+        g.manual_seed(((cid * 1000003 + stream) * 1000003 + i) & 0x7FFFFFFFFFFFFFFF)
+        out[r0:r1].normal_(generator=g)
+    return out

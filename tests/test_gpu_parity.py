@@ -4,6 +4,8 @@ Bar: relative L2 <= 1e-5 per floating-point output, bit-exact graph arrays,
 bitwise-identical repeats.  Inputs are the seeded synthetic workloads; large
 ones are checked on sampled rows the oracle computes one by one.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -296,6 +298,46 @@ def test_conv_full_size_sampled(e3, cid):
     ei = torch.as_tensor(es, device="cuda")
     errs = dict(m=rel_l2(to_np(m[ri]), ref_m), dx=rel_l2(to_np(dx[ri]), ref_dx),
                 ds=rel_l2(to_np(ds[ei]), ref_ds), dvec=rel_l2(to_np(dvec[ei]), ref_dv))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+
+
+@pytest.mark.skipif(os.environ.get("E3MI_STRESS") != "1",
+                    reason="capacity stress (~265 GB of HBM, several minutes): set E3MI_STRESS=1")
+def test_conv_stress_config5_sampled(e3):
+    """70,000 H2O (210,000 atoms, ~11M edges), 64 channels: forward + backward at
+    full size on one GPU, checked on sampled rows."""
+    import torch
+    _say("conv stress config 5")
+    cfg = synth.CONFIGS[5]
+    g = synth.graph(cfg)
+    N, E = g.n_nodes, g.sender.shape[0]
+    print(f"N={N} E={E}", flush=True)
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    dev = torch.device("cuda")
+    x = synth.node_features(cfg, N)
+    s = synth.normal_device(cfg.cid, 2, (E, plan.P, plan.C), dev)
+    dm = synth.normal_device(cfg.cid, 3, (N, plan.D_out, plan.C), dev)
+    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), N)
+    xs, vs = to_dev(x), to_dev(g.vec)
+    m = e3.conv_fwd(plan, G, xs, vs, s)
+    torch.cuda.synchronize()
+    lay = layout_of(cfg)
+    rng = np.random.default_rng(9)
+    rs = np.concatenate([[0, N - 1], rng.choice(N, 14, replace=False)])
+    es = np.concatenate([[0, E - 1], rng.choice(E, 30, replace=False)])
+    sfn = lambda rows: s[torch.as_tensor(rows, device=dev)].cpu().numpy()
+    ref_m = oracle_fwd_rows(lay, x, g.vec, sfn, g.sender, g.receiver, N, rs)
+    err_m = rel_l2(to_np(m[torch.as_tensor(rs, device=dev)]), ref_m)
+    del m
+    torch.cuda.empty_cache()
+    dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, s, dm)
+    torch.cuda.synchronize()
+    ref_dx, ref_ds, ref_dv = oracle_bwd_rows(lay, x, g.vec, sfn, dm, g.sender, g.receiver, N, rs, es)
+    ri, ei = torch.as_tensor(rs, device=dev), torch.as_tensor(es, device=dev)
+    errs = dict(m=err_m, dx=rel_l2(to_np(dx[ri]), ref_dx), ds=rel_l2(to_np(ds[ei]), ref_ds),
+                dvec=rel_l2(to_np(dvec[ei]), ref_dv))
     print("rel-L2", errs, flush=True)
     for k, v in errs.items():
         assert v < TOL, (k, v)
