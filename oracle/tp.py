@@ -52,3 +52,27 @@ def weight(lay, z, w) -> torch.Tensor:
 def tp(lay, x, y, w) -> torch.Tensor:
     """Weighted tensor product, float64 [R, D_out, C]."""
     return weight(lay, tp_unweighted(lay, x, y), w)
+
+
+def tp_bwd(lay, x, y, w, dz):
+    """Cotangents of the weighted tensor product (App. E.1, eq. tp-bwd, with
+    the path weight of eq. edge_scalar_weighting):
+        dw[r,k,q]  = sum_{M in k} dz[r,M,q] * (x (x) y)[r,M,q]
+        dx[r,i1,q] = sum_{i0,i2} C[i0,i1,i2] y[r,i2] w[r,i3(i0),q] dz[r,i0,q]
+        dy[r,i2]   = sum_q sum_{i0,i1} C[i0,i1,i2] x[r,i1,q] w[r,i3(i0),q] dz[r,i0,q]
+    Returns (dx, dy, dw) in float64."""
+    x, y, w, dz = t64(x), t64(y), t64(w), t64(dz)
+    R, _, C = x.shape
+    dx = torch.zeros_like(x)
+    dy = torch.zeros_like(y)
+    dw = torch.zeros_like(w)
+    for p, blk in zip(lay.paths, _blocks(lay)):
+        xb = x[:, p.x_off:p.x_off + 2 * p.l1 + 1, :]
+        yb = y[:, p.y_off:p.y_off + 2 * p.l2 + 1]
+        dzb = dz[:, p.out_off:p.out_off + 2 * p.l3 + 1, :]
+        wk = w[:, p.k, :]
+        u = torch.einsum("Mab,raq,rb->rMq", blk, xb, yb)
+        dw[:, p.k, :] = (u * dzb).sum(dim=1)
+        dx[:, p.x_off:p.x_off + 2 * p.l1 + 1, :] += torch.einsum("Mab,rb,rq,rMq->raq", blk, yb, wk, dzb)
+        dy[:, p.y_off:p.y_off + 2 * p.l2 + 1] += torch.einsum("Mab,raq,rq,rMq->rb", blk, xb, wk, dzb)
+    return dx, dy, dw

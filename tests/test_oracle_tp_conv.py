@@ -257,3 +257,38 @@ def test_graph_csr():
         assert list(perm_r[rowptr_r[b]:rowptr_r[b + 1]]) == ids
         ids = [e for e in range(60) if snd[e] == b and keep[e]]
         assert list(perm_s[rowptr_s[b]:rowptr_s[b + 1]]) == ids
+
+
+@pytest.mark.parametrize("spec", [("2x0e+2x1o+2x2e", 3, 3), ("3x0e+3x1o+3x2e+3x3o", 3, 3)])
+def test_tp_bwd_against_autograd_fd_and_euler(spec):
+    lay = irreps.layout(*spec)
+    rng = np.random.default_rng(19)
+    R, C = 6, lay.channels
+    x = torch.tensor(rng.standard_normal((R, lay.d_in, C)), requires_grad=True)
+    y = torch.tensor(sh.sh_unit(lay.lmax_sh, _unit(rng, R)), requires_grad=True)
+    w = torch.tensor(rng.standard_normal((R, lay.n_paths, C)), requires_grad=True)
+    dz = torch.tensor(rng.standard_normal((R, lay.d_out, C)))
+    z = tp.tp(lay, x, y, w)
+    gx, gy, gw = torch.autograd.grad(z, (x, y, w), grad_outputs=dz)
+    dx, dy, dw = tp.tp_bwd(lay, x.detach(), y.detach(), w.detach(), dz)
+    assert torch.abs(dx - gx).max() < 1e-12
+    assert torch.abs(dy - gy).max() < 1e-12
+    assert torch.abs(dw - gw).max() < 1e-12
+    # central differences on a few entries
+    X, Y, Wt = x.detach().numpy(), y.detach().numpy(), w.detach().numpy()
+    L = lambda a, b, c: float((tp.tp(lay, a, b, c).numpy() * dz.numpy()).sum())
+    h = 1e-6
+    for (r, i, q) in [(0, 1, 0), (5, lay.d_in - 1, C - 1)]:
+        a1, a2 = X.copy(), X.copy()
+        a1[r, i, q] += h
+        a2[r, i, q] -= h
+        assert abs((L(a1, Y, Wt) - L(a2, Y, Wt)) / (2 * h) - dx[r, i, q].item()) < 1e-7
+    for (r, i) in [(1, 0), (3, lay.d_sh - 1)]:
+        b1, b2 = Y.copy(), Y.copy()
+        b1[r, i] += h
+        b2[r, i] -= h
+        assert abs((L(X, b1, Wt) - L(X, b2, Wt)) / (2 * h) - dy[r, i].item()) < 1e-7
+    # trilinear: <dz, z> = <dx, x> = <dy, y> = <dw, w>
+    ref = float((dz * z.detach()).sum())
+    for got in [(dx * x.detach()).sum(), (dy * y.detach()).sum(), (dw * w.detach()).sum()]:
+        assert abs(float(got) - ref) < 1e-10 * max(1.0, abs(ref))
