@@ -85,6 +85,11 @@ def tp_bytes(R, C, D_in, D_sh, D_out, P):
     return R * (D_in * C + D_sh + P * C + D_out * C) * 4
 
 
+def tp_bwd_bytes(R, C, D_in, D_sh, D_out, P):
+    """x, y, w, dz read; dx, dy, dw written."""
+    return R * (2 * D_in * C + 2 * D_sh + 2 * P * C + D_out * C) * 4
+
+
 def cpu_baseline(cfg, g, x, dm, seconds=12.0):
     """The fp64 oracle on the host cores, on a bounded sample of the same workload:
     forward for sampled receivers and backward for sampled senders and edges."""
@@ -272,7 +277,33 @@ def main():
                      "frac": round(nb / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "alg_bytes": nb,
                      "event_ms": round(a0.elapsed_time(a1) / args.steps, 4)}
         log(f"tp: {t_ms:.3f} ms, {out['tp']['alg_GBps']} GB/s")
-        del tz, txd, twd, ty
+        del tz
+        tdz = synth.normal_device(tcfg.cid, synth._DM, (R, tplan.D_out, tplan.C), dev)
+        tdx, tdw = torch.empty_like(txd), torch.empty_like(twd)
+        tdy = torch.empty_like(ty)
+        tws = e3mi.workspace(e3mi.tp_workspace_size(tplan, R))
+        for _ in range(args.warmup):
+            e3mi.tp_bwd(tplan, txd, ty, twd, tdz, tdx, tdy, tdw, tws)
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        a0.record()
+        for _ in range(args.steps):
+            e3mi.tp_bwd(tplan, txd, ty, twd, tdz, tdx, tdy, tdw, tws)
+        a1.record()
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        tt = e3mi.timing_read()
+        tb_ms = tt["tp_bwd"][0] / tt["tp_bwd"][1]
+        nb = tp_bwd_bytes(R, tplan.C, tplan.D_in, tplan.D_sh, tplan.D_out, tplan.P)
+        out["tp_bwd"] = {"workload": out["tp"]["workload"], "ms": round(tb_ms, 4),
+                         "dy_sum_ms": round(tt["tp_bwd_dy"][0] / tt["tp_bwd_dy"][1], 4),
+                         "rows_per_s": R / (tb_ms * 1e-3),
+                         "alg_GBps": round(nb / (tb_ms * 1e-3) / 1e9, 1),
+                         "frac": round(nb / (tb_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "alg_bytes": nb,
+                         "event_ms": round(a0.elapsed_time(a1) / args.steps, 4)}
+        log(f"tp_bwd: {tb_ms:.3f} ms, {out['tp_bwd']['alg_GBps']} GB/s")
+        del tdz, tdx, tdw, tdy, tws, txd, twd, ty
 
     if args.copy_probe:
         n = (2 << 30) // 4

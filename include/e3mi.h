@@ -141,6 +141,15 @@ e3_status e3_sh_bwd(int lmax, const float* vec, const float* dy, float* dvec, in
 e3_status e3_tp_fwd(const e3_plan* plan, const float* x, const float* y, const float* w, float* z,
                     int64_t rows, e3_stream stream);
 
+/* Backward of the weighted tensor product (App. E.1, eq. tp-bwd with the path
+ * weight of eq. edge_scalar_weighting): from dz [rows, D_out, C] computes
+ * dx [rows, D_in, C], dy [rows, D_sh] (summed over channels) and dw [rows, P, C],
+ * streaming x, y, w and dz once.  ws: at least e3_tp_workspace_size bytes (the
+ * per-wave partial sums of dy, added in a fixed order). */
+e3_status e3_tp_workspace_size(const e3_plan* plan, int64_t rows, size_t* bwd_bytes);
+e3_status e3_tp_bwd(const e3_plan* plan, const float* x, const float* y, const float* w, const float* dz,
+                    float* dx, float* dy, float* dw, void* ws, size_t ws_bytes, int64_t rows, e3_stream stream);
+
 /* Device workspace the convolution needs (bytes, 256-byte aligned start).
  * Forward: 0.  Backward: the per-edge x-cotangent partials [n_live, D_in, C]
  * summed later in sender order, plus the per-edge harmonic cotangents. */

@@ -6,7 +6,7 @@ The compute lives in the HIP library ``libe3mi.so`` (kernels under ``csrc/``,
 C ABI in ``include/e3mi.h``); ``e3mi`` is its Python binding.
 """
 from .e3mi import (E3Error, Graph, Plan, conv_bwd, conv_fwd, conv_workspace_size, sh, sh_bwd,
-                   sh_host, tp_fwd, workspace)
+                   sh_host, tp_bwd, tp_fwd, tp_workspace_size, workspace)
 
 __all__ = ["E3Error", "Graph", "Plan", "conv_bwd", "conv_fwd", "conv_workspace_size", "sh",
-           "sh_bwd", "sh_host", "tp_fwd", "workspace"]
+           "sh_bwd", "sh_host", "tp_bwd", "tp_fwd", "tp_workspace_size", "workspace"]

@@ -110,6 +110,10 @@ constexpr int kXcd = 8;
 #ifndef E3_FWD_CPL
 #define E3_FWD_CPL 2
 #endif
+// 1: the backward sweep double-buffers the path weights as well as the x rows.
+#ifndef E3_BWD_DB_S
+#define E3_BWD_DB_S 1
+#endif
 constexpr int kMaxChannels = 1024;
 
 typedef float f2v __attribute__((ext_vector_type(2)));
@@ -362,6 +366,117 @@ __global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const
   }
 }
 
+// ------------------------------------------------------------ tensor product backward
+// One wave per (tile of kTpRows rows, group of whole x blocks, channel slab):
+// the backward group code of the convolution with the row's dz in place of the
+// receiver cotangent; dx and dw rows are stored directly, dy (summed over the
+// wave's channels) goes to a per-wave slot that k_tp_bwd_dy adds up.
+struct TpbArgs {
+  const float* x;
+  const float* y;
+  const float* w;
+  const float* dz;
+  float* dx;
+  float* dw;
+  float* DY;  // [rows, NBG * nslab, 16]
+  int64_t rows;
+  int C;
+  int nslab;
+};
+
+template <class V, int G, int CPL>
+__device__ __forceinline__ void tpb_task(const TpbArgs& a, int64_t r0, int sl, float* sA, float* sY) {
+  using B = typename V::template BG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<CPL>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane * CPL;
+  const int n = (int)((a.rows - r0) < kTpRows ? (a.rows - r0) : kTpRows);
+  if (lane < n) {
+    float Y[V::D_SH];
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) Y[i] = a.y[(r0 + lane) * V::D_SH + i];
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) sY[lane * V::D_SH + i] = Y[i];
+    B::make_A(Y, sA + lane * B::NA);
+  }
+  __syncthreads();
+  for (int j = 0; j < n; ++j) {
+    const int64_t r = r0 + j;
+    float dy[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) dy[i] = 0.0f;
+    if (act) {
+      const RowBuf xb = row_buf(a.x + r * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf wb = row_buf(a.w + r * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+      const RowBuf zb = row_buf(a.dz + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+      float xv[B::NXR][CPL], wv[B::NPATH][CPL], dzv[B::NROW][CPL], t[B::NXR][CPL], Yv[V::D_SH];
+#pragma unroll
+      for (int i = 0; i < B::NXR; ++i) {
+        bld<CPL, kNT>(xb, B::XROW[i], xv[i]);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) t[i][c] = 0.0f;
+      }
+#pragma unroll
+      for (int i = 0; i < B::NPATH; ++i) bld<CPL, kNT>(wb, B::PATH[i], wv[i]);
+#pragma unroll
+      for (int i = 0; i < B::NROW; ++i) bld<CPL, kNT>(zb, B::OROW[i], dzv[i]);
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
+      const RowBuf dwb = row_buf(a.dw + r * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+      auto st = [&](int pl, const float (&v)[CPL]) { bst<CPL, kNT>(dwb, B::PATH[pl], v); };
+      float dyl[V::D_SH];
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0f;
+      B::template edge<CPL>(sA + j * B::NA, Yv, xv, wv, dzv, t, dyl, st);
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
+      const RowBuf dxb = row_buf(a.dx + r * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+#pragma unroll
+      for (int i = 0; i < B::NXR; ++i) bst<CPL, kNT>(dxb, B::XROW[i], t[i]);
+    }
+    const float tot = wave_reduce16(dy, lane);
+    if ((lane & 3) == 0) a.DY[((r * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+  }
+}
+
+template <class V, int G, int CPL>
+__device__ __forceinline__ void tpb_dispatch(const TpbArgs& a, int64_t r0, int g, int sl, float* sA, float* sY) {
+  if constexpr (G < V::NBG) {
+    if (g == G)
+      tpb_task<V, G, CPL>(a, r0, sl, sA, sY);
+    else
+      tpb_dispatch<V, G + 1, CPL>(a, r0, g, sl, sA, sY);
+  }
+}
+
+template <class V, int CPL>
+__global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_tp_bwd(TpbArgs a) {
+  __shared__ f4v smem[(kTpRows * (V::MAX_NA_B + V::D_SH) + 3) / 4];
+  const int per = V::NBG * a.nslab;
+  const int t = blockIdx.x % per;
+  const int64_t r0 = (int64_t)(blockIdx.x / per) * kTpRows;
+  float* sA = reinterpret_cast<float*>(smem);
+  tpb_dispatch<V, 0, CPL>(a, r0, t / a.nslab, t % a.nslab, sA, sA + kTpRows * V::MAX_NA_B);
+}
+
+// dy[r] = sum over the (group, slab) waves of row r.
+template <class V>
+__global__ __launch_bounds__(256) void k_tp_bwd_dy(const float* __restrict__ DY, float* __restrict__ dy, int64_t rows,
+                                                   int nslab) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows) return;
+  float acc[V::D_SH];
+#pragma unroll
+  for (int i = 0; i < V::D_SH; ++i) acc[i] = 0.0f;
+  for (int g = 0; g < V::NBG * nslab; ++g)
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) acc[i] += DY[(r * V::NBG * nslab + g) * 16 + i];
+#pragma unroll
+  for (int i = 0; i < V::D_SH; ++i) dy[r * V::D_SH + i] = acc[i];
+}
+
 // ------------------------------------------------------------ convolution
 constexpr int kEdgeBatch = 16;  // edges whose pre-contraction is staged per LDS batch
 
@@ -511,15 +626,23 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
       B::make_A(Y, sA + lane * B::NA);
     }
     __syncthreads();
-    float xa[B::NXR][CPL], sa[B::NPATH][CPL], xb[B::NXR][CPL], sb[B::NPATH][CPL];
-    auto load = [&](int j, float (&xv)[B::NXR][CPL], float (&sv)[B::NPATH][CPL]) {
+    float xa[B::NXR][CPL], sa[B::NPATH][CPL], xb[B::NXR][CPL];
+#if E3_BWD_DB_S
+    float sb[B::NPATH][CPL];
+#else
+    float (&sb)[B::NPATH][CPL] = sa;
+#endif
+    auto load_x = [&](int j, float (&xv)[B::NXR][CPL]) {
       if (!act) return;
-      const int64_t e = __builtin_amdgcn_readlane(my_e, j);
       const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
       const RowBuf xb_ = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-      const RowBuf sb_ = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) bld<CPL>(xb_, B::XROW[i], xv[i]);
+    };
+    auto load_s = [&](int j, float (&sv)[B::NPATH][CPL]) {
+      if (!act) return;
+      const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+      const RowBuf sb_ = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < B::NPATH; ++i) bld<CPL, kNT>(sb_, B::PATH[i], sv[i]);
     };
@@ -552,12 +675,21 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
       const float tot = wave_reduce16(dy, lane);
       if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
     };
-    load(0, xa, sa);
+    load_x(0, xa);
+    if (E3_BWD_DB_S) load_s(0, sa);
     for (int j = 0; j < n; j += 2) {
-      if (j + 1 < n) load(j + 1, xb, sb);
+      if (!E3_BWD_DB_S) load_s(j, sa);
+      if (j + 1 < n) {
+        load_x(j + 1, xb);
+        if (E3_BWD_DB_S) load_s(j + 1, sb);
+      }
       compute(j, xa, sa);
       if (j + 1 < n) {
-        if (j + 2 < n) load(j + 2, xa, sa);
+        if (!E3_BWD_DB_S) load_s(j + 1, sb);
+        if (j + 2 < n) {
+          load_x(j + 2, xa);
+          if (E3_BWD_DB_S) load_s(j + 2, sa);
+        }
         compute(j + 1, xb, sb);
       }
     }
@@ -826,6 +958,35 @@ e3_status run_tp(const e3_plan* p, const float* x, const float* y, const float* 
   return E3_OK;
 }
 
+template <class V, int CPL>
+e3_status run_tp_bwd(const e3_plan* p, const float* x, const float* y, const float* w, const float* dz, float* dx,
+                     float* dy, float* dw, void* ws, int64_t rows, hipStream_t st) {
+  if (rows == 0) return E3_OK;
+  TpbArgs a{};
+  a.x = x, a.y = y, a.w = w, a.dz = dz, a.dx = dx, a.dw = dw;
+  a.DY = reinterpret_cast<float*>(ws);
+  a.rows = rows;
+  a.C = p->lay.C;
+  a.nslab = p->nslab_b;
+  const int64_t tiles = (rows + kTpRows - 1) / kTpRows;
+  {
+    TimedLaunch t_("tp_bwd", st);
+    hipLaunchKernelGGL((k_tp_bwd<V, CPL>), dim3((unsigned)(tiles * V::NBG * a.nslab)), dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  {
+    TimedLaunch t_("tp_bwd_dy", st);
+    hipLaunchKernelGGL((k_tp_bwd_dy<V>), dim3(blocks_for(rows, 256)), dim3(256), 0, st, a.DY, dy, rows, a.nslab);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+size_t tp_ws(const e3_plan* p, int64_t rows) {
+  return align256((size_t)rows * V::NBG * p->nslab_b * 16 * sizeof(float));
+}
+
 struct VariantOps {
   const char* sig;
   int d_in, d_sh, d_out, np, lsh, nbg;
@@ -835,6 +996,9 @@ struct VariantOps {
                       float*, float*, float*, void*, hipStream_t);
   e3_status (*tp[2])(const e3_plan*, const float*, const float*, const float*, float*, int64_t, hipStream_t);
   Ws (*ws)(const e3_plan*, const e3_graph*);
+  e3_status (*tpb)(const e3_plan*, const float*, const float*, const float*, const float*, float*, float*, float*,
+                   void*, int64_t, hipStream_t);
+  size_t (*tpws)(const e3_plan*, int64_t);
 };
 
 #define E3_VARIANT(V)                                                                                    \
@@ -848,7 +1012,9 @@ struct VariantOps {
              {&run_fwd<e3gen::V, 1>, &run_fwd<e3gen::V, 2>},                                             \
              {&run_bwd<e3gen::V, 1>, &run_bwd<e3gen::V, 2>},                                             \
              {&run_tp<e3gen::V, 1>, &run_tp<e3gen::V, 2>},                                               \
-             &bwd_ws<e3gen::V>},
+             &bwd_ws<e3gen::V>,                                                                          \
+             &run_tp_bwd<e3gen::V, 1>,                                                                   \
+             &tp_ws<e3gen::V>},
 
 const VariantOps kVariants[] = {E3GEN_FOR_EACH_VARIANT(E3_VARIANT)};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
@@ -1201,6 +1367,28 @@ e3_status e3_tp_fwd(const e3_plan* p, const float* x, const float* y, const floa
   if (rows == 0) return E3_OK;
   const VariantOps& v = kVariants[p->variant];
   return v.tp[cpl_index(cpl_of(p))](p, x, y, w, z, rows, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_tp_workspace_size(const e3_plan* p, int64_t rows, size_t* bwd_bytes) {
+  e3_status s = check_plan(p);
+  if (s != E3_OK) return s;
+  if (rows < 0 || !bwd_bytes) return E3_ERR_INVALID_ARG;
+  *bwd_bytes = kVariants[p->variant].tpws(p, rows);
+  return E3_OK;
+}
+
+e3_status e3_tp_bwd(const e3_plan* p, const float* x, const float* y, const float* w, const float* dz, float* dx,
+                    float* dy, float* dw, void* ws, size_t ws_bytes, int64_t rows, e3_stream stream) {
+  e3_status s = check_plan(p);
+  if (s != E3_OK) return s;
+  if (rows < 0) return E3_ERR_INVALID_ARG;
+  if (rows == 0) return E3_OK;
+  if (!x || !y || !w || !dz || !dx || !dy || !dw || !ws || !aligned16(x) || !aligned16(w) || !aligned16(dz) ||
+      !aligned16(dx) || !aligned16(dw) || !aligned16(ws))
+    return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  if (ws_bytes < v.tpws(p, rows)) return E3_ERR_WORKSPACE_TOO_SMALL;
+  return v.tpb(p, x, y, w, dz, dx, dy, dw, ws, rows, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_workspace_size(const e3_plan* p, const e3_graph* g, size_t* fwd_bytes, size_t* bwd_bytes) {

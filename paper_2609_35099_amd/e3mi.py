@@ -55,6 +55,8 @@ SIGNATURES = {
     "e3_sh": (_I, [_I, _P, _P, _I64, _P]),
     "e3_sh_bwd": (_I, [_I, _P, _P, _P, _I64, _P]),
     "e3_tp_fwd": (_I, [_P, _P, _P, _P, _P, _I64, _P]),
+    "e3_tp_workspace_size": (_I, [_P, _I64, ct.POINTER(ct.c_size_t)]),
+    "e3_tp_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, _P]),
     "e3_conv_workspace_size": (_I, [_P, _P, ct.POINTER(ct.c_size_t), ct.POINTER(ct.c_size_t)]),
     "e3_conv_fwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
@@ -249,6 +251,28 @@ def tp_fwd(plan: Plan, x, y, w, out=None, stream=None):
                            _ptr(w, "w", (R, plan.P, plan.C)), _ptr(out, "z", (R, plan.D_out, plan.C)), R,
                            _stream(stream)), "e3_tp_fwd")
     return out
+
+
+def tp_workspace_size(plan: Plan, rows: int) -> int:
+    b = ct.c_size_t()
+    _check(lib().e3_tp_workspace_size(plan.handle, rows, ct.byref(b)), "e3_tp_workspace_size")
+    return b.value
+
+
+def tp_bwd(plan: Plan, x, y, w, dz, dx=None, dy=None, dw=None, ws=None, stream=None):
+    """(dx, dy, dw) of the weighted tensor product."""
+    R = x.shape[0]
+    dx = _empty((R, plan.D_in, plan.C)) if dx is None else dx
+    dy = _empty((R, plan.D_sh)) if dy is None else dy
+    dw = _empty((R, plan.P, plan.C)) if dw is None else dw
+    if ws is None:
+        ws = workspace(tp_workspace_size(plan, R))
+    _check(lib().e3_tp_bwd(plan.handle, _ptr(x, "x", (R, plan.D_in, plan.C)), _ptr(y, "y", (R, plan.D_sh)),
+                           _ptr(w, "w", (R, plan.P, plan.C)), _ptr(dz, "dz", (R, plan.D_out, plan.C)),
+                           _ptr(dx, "dx", (R, plan.D_in, plan.C)), _ptr(dy, "dy", (R, plan.D_sh)),
+                           _ptr(dw, "dw", (R, plan.P, plan.C)), ct.c_void_p(ws.data_ptr()), ws.numel(), R,
+                           _stream(stream)), "e3_tp_bwd")
+    return dx, dy, dw
 
 
 def conv_workspace_size(plan: Plan, graph: Graph):

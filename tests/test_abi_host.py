@@ -118,3 +118,16 @@ def test_null_and_negative_arguments_rejected_before_device_work():
     assert L.e3_tp_fwd(plan.handle, None, None, None, None, 4, None) == 1
     # misaligned pointers are refused
     assert L.e3_tp_fwd(plan.handle, ct.c_void_p(4), ct.c_void_p(4), ct.c_void_p(4), ct.c_void_p(4), 4, None) == 1
+    # tensor product backward: argument checks and workspace sizing, no device work
+    n = ct.c_size_t()
+    assert L.e3_tp_workspace_size(plan.handle, -1, ct.byref(n)) == 1
+    assert L.e3_tp_workspace_size(plan.handle, 10, None) == 1
+    assert L.e3_tp_workspace_size(plan.handle, 10, ct.byref(n)) == 0 and n.value >= 10 * 16 * 4
+    assert n.value % 256 == 0
+    nul = [None] * 7
+    assert L.e3_tp_bwd(plan.handle, *nul, None, 0, -1, None) == 1
+    assert L.e3_tp_bwd(plan.handle, *nul, None, 0, 0, None) == 0
+    assert L.e3_tp_bwd(plan.handle, *nul, None, 0, 3, None) == 1
+    fake = [ct.c_void_p(256)] * 7
+    assert L.e3_tp_bwd(plan.handle, *fake, ct.c_void_p(256), 16, 10, None) == 4   # workspace too small
+    assert L.e3_tp_bwd(plan.handle, *([ct.c_void_p(4)] * 7), ct.c_void_p(256), n.value, 10, None) == 1

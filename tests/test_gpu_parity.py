@@ -143,6 +143,58 @@ def test_tp_config2_full_size_sampled(e3):
     assert rel_l2(got, ref) < TOL
 
 
+@pytest.mark.parametrize("irreps,lsh,lout,rows", [
+    ("128x0e+128x1o+128x2e", 3, 3, 1001),
+    ("64x0e+64x1o+64x2e", 3, 3, 77),
+    ("8x0e+8x1o", 2, 2, 5),
+    ("12x0e+12x1o+12x2e+12x3o", 3, 3, 33),
+    ("100x0e+100x1o", 3, 3, 19),
+    ("4x0e+4x1o", 3, 3, 1),
+])
+def test_tp_bwd_parity(e3, irreps, lsh, lout, rows):
+    _say("tp bwd", irreps, rows)
+    plan = e3.Plan(irreps, lsh, lout)
+    lay = oirreps.layout(irreps, lsh, lout)
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((rows, lay.d_in, lay.channels)).astype(np.float32)
+    g = rng.standard_normal((rows, 3))
+    y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
+    w = rng.standard_normal((rows, lay.n_paths, lay.channels)).astype(np.float32)
+    dz = rng.standard_normal((rows, lay.d_out, lay.channels)).astype(np.float32)
+    args = [to_dev(a) for a in (x, y, w, dz)]
+    dx, dy, dw = (to_np(t) for t in e3.tp_bwd(plan, *args))
+    rdx, rdy, rdw = (t.numpy() for t in otp.tp_bwd(lay, x, y, w, dz))
+    errs = dict(dx=rel_l2(dx, rdx), dy=rel_l2(dy, rdy), dw=rel_l2(dw, rdw))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    again = [to_np(t) for t in e3.tp_bwd(plan, *args)]
+    for u, v in zip((dx, dy, dw), again):
+        assert np.array_equal(u, v)
+
+
+def test_tp_bwd_config2_full_size_sampled(e3):
+    """TP backward at config 2's full size, checked on sampled rows."""
+    import torch
+    _say("tp bwd config 2 full")
+    cfg = synth.CONFIGS[2]
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    lay = layout_of(cfg)
+    x, u, w = synth.tp_inputs(cfg)
+    y = osh.sh_unit(3, u.astype(np.float64)).astype(np.float32)
+    R = x.shape[0]
+    dz = synth.normal_device(cfg.cid, synth._DM, (R, lay.d_out, lay.channels), "cuda")
+    dx, dy, dw = e3.tp_bwd(plan, to_dev(x), to_dev(y), to_dev(w), dz)
+    torch.cuda.synchronize()
+    rows = np.concatenate([[0, 1, 7, 8, R - 1], np.random.default_rng(6).integers(0, R, 59)])
+    ri = torch.as_tensor(rows, device="cuda")
+    ref = otp.tp_bwd(lay, x[rows], y[rows], w[rows], to_np(dz[ri]))
+    for name, got, r in zip(("dx", "dy", "dw"), (dx, dy, dw), ref):
+        err = rel_l2(to_np(got[ri]), r.numpy())
+        print(name, err, flush=True)
+        assert err < TOL, (name, err)
+
+
 # ---------------------------------------------------------------- convolution
 def _run_conv(e3, plan, snd, rcv, n, vec, x, s, dm, pad=-1):
     G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
