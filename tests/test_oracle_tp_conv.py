@@ -292,3 +292,54 @@ def test_tp_bwd_against_autograd_fd_and_euler(spec):
     ref = float((dz * z.detach()).sum())
     for got in [(dx * x.detach()).sum(), (dy * y.detach()).sum(), (dw * w.detach()).sum()]:
         assert abs(float(got) - ref) < 1e-10 * max(1.0, abs(ref))
+
+
+# ---------------------------------------------------------------- fused radial weights
+def test_radial_one_hot_reduces_to_plain_conv():
+    """h_e = unit vector e_j gives s_e = W[j] for every edge."""
+    from oracle import radial
+    rng = np.random.default_rng(21)
+    lay = irreps.layout("2x0e+2x1o+2x2e", 3, 3)
+    snd, rcv, vec = _small_graph(rng, n=7, e=25)
+    x = rng.standard_normal((7, lay.d_in, lay.channels))
+    K = 5
+    W = rng.standard_normal((K, lay.n_paths, lay.channels))
+    for j in (0, 3):
+        h = np.zeros((25, K))
+        h[:, j] = 1.0
+        ref = conv.conv_fwd(lay, x, vec, np.broadcast_to(W[j], (25,) + W.shape[1:]), snd, rcv, 7)
+        got = radial.conv_fwd(lay, x, vec, h, W, snd, rcv, 7)
+        assert torch.allclose(got, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("pad", [-1, 4])
+def test_radial_bwd_central_differences(pad):
+    """<dh, dH> + <dW, dW'> + <dx, dX> equals the directional derivative of
+    <dm, m(x, h, W)>, taken by central differences (the loss is trilinear in
+    (x, h, W) jointly only through products, so a small step suffices)."""
+    from oracle import radial
+    rng = np.random.default_rng(22)
+    lay = irreps.layout("2x0e+2x1o+2x2e", 2, 2)
+    n, e, K = 8, 30, 4
+    snd, rcv, vec = _small_graph(rng, n=n, e=e)
+    if pad >= 0:
+        snd[::7] = pad
+    x = rng.standard_normal((n, lay.d_in, lay.channels))
+    h = rng.standard_normal((e, K))
+    W = rng.standard_normal((K, lay.n_paths, lay.channels))
+    dm = rng.standard_normal((n, lay.d_out, lay.channels))
+    dX, dH, dW = (rng.standard_normal(a.shape) for a in (x, h, W))
+    res = radial.conv_bwd(lay, x, vec, h, W, dm, snd, rcv, n, pad_node=pad)
+
+    def loss(t):
+        m = radial.conv_fwd(lay, x + t * dX, vec, h + t * dH, W + t * dW, snd, rcv, n, pad_node=pad)
+        return float((m * torch.as_tensor(dm)).sum())
+
+    eps = 1e-3
+    fd = (loss(eps) - loss(-eps)) / (2 * eps)
+    an = float((res["dx"] * torch.as_tensor(dX)).sum() + (res["dh"] * torch.as_tensor(dH)).sum()
+               + (res["dW"] * torch.as_tensor(dW)).sum())
+    # the loss is a cubic polynomial in t: central differences carry an eps^2 term only
+    assert abs(fd - an) < 1e-5 * max(1.0, abs(an))
+    if pad >= 0:
+        assert torch.all(res["dh"][snd == pad] == 0)
