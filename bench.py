@@ -53,6 +53,18 @@ def conv_bytes(N, E, C, D_in, D_out, P):
     return k, fwd, bwd
 
 
+def radial_bytes(N, E, C, D_in, D_out, P, K):
+    """Algorithmic bytes of the convolution with fused radial weights (h [E, K]
+    and W [K, P, C] replace s); ds is scratch, not counted."""
+    f = 4
+    fwd = (N * D_in * C * f + E * 3 * f + E * K * f + K * P * C * f + N * D_out * C * f
+           + E * 4 * 2 + (N + 1) * 4)
+    bwd = (N * D_in * C * f + E * 3 * f + E * K * f + K * P * C * f + N * D_out * C * f   # inputs
+           + N * D_in * C * f + E * 3 * f + E * K * f + K * P * C * f                      # outputs
+           + E * 4 * 3 + (N + 1) * 4 * 2)
+    return fwd, bwd
+
+
 KERNEL_SOURCES = ["paper_2609_35099_amd/csrc/e3mi.hip", "paper_2609_35099_amd/csrc/gen.cpp",
                   "paper_2609_35099_amd/csrc/builder.cpp", "paper_2609_35099_amd/csrc/builder.h"]
 COUNTERS = os.path.join(ROOT, "profiles", "conv_tp_config4_hbm_bytes.txt")
@@ -138,7 +150,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tp", action="store_true")
-    ap.add_argument("--only", choices=["all", "conv", "tp"], default="all")
+    ap.add_argument("--only", choices=["all", "conv", "radial", "tp"], default="all")
     ap.add_argument("--order", choices=["generated", "cell"], default="generated",
                     help="atom order of the water box: as generated (spatially random) or cell-sorted")
     ap.add_argument("--copy-probe", action="store_true",
@@ -244,7 +256,51 @@ def main():
         })
         log(f"conv: {ms_step:.3f} ms/step, {E / ms_step / 1e3:.1f} M edges/s; kernels {kernels}")
 
-    del ws, ds, dvec, dx, m, s
+    del ws, ds, s
+    torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- fused radial weights
+    if args.only in ("all", "radial"):
+        h_np, W_np = synth.radial_inputs(cfg, g.vec)
+        hs, Wd = torch.from_numpy(h_np).to(dev), torch.from_numpy(W_np).to(dev)
+        K = W_np.shape[0]
+        dh = torch.empty((E, K), dtype=torch.float32, device=dev)
+        dW = torch.empty_like(Wd)
+        rws = e3mi.workspace(e3mi.conv_radial_workspace_size(plan, graph, K))
+
+        def rstep():
+            e3mi.conv_fwd_radial(plan, graph, xs, vs, hs, Wd, out=m)
+            e3mi.conv_bwd_radial(plan, graph, xs, vs, hs, Wd, dms, dx=dx, dvec=dvec, dh=dh, dW=dW, ws=rws)
+
+        for _ in range(args.warmup):
+            rstep()
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(args.steps):
+            rstep()
+        ev1.record()
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        per = e3mi.timing_read()
+        r_ms = ev0.elapsed_time(ev1) / args.steps
+        rf, rb = radial_bytes(N, E, C, plan.D_in, plan.D_out, plan.P, K)
+        rk = {name: {"ms": round(t / c, 4), "launches": c} for name, (t, c) in per.items()}
+        out["radial"] = {
+            "workload": "as the convolution, with s = h W fused: h = 8-function Bessel basis of |r|, "
+                        "W [8, P, C]", "K": K,
+            "ms_per_step": round(r_ms, 4), "edges_per_s": E / (r_ms * 1e-3),
+            "alg_bytes_fwd": rf, "alg_bytes_bwd": rb,
+            "step_alg_GBps": round((rf + rb) / (r_ms * 1e-3) / 1e9, 1),
+            "kernels": rk,
+            # s = h W on the matrix cores, both sweeps: 2 K P C flops per edge each
+            "radial_mfma_TFLOPs": round(2 * 2 * K * plan.P * C * E / (r_ms * 1e-3) / 1e12, 2),
+        }
+        log(f"radial: {r_ms:.3f} ms/step, {E / r_ms / 1e3:.1f} M edges/s; kernels {rk}")
+        del rws, dh, dW, hs, Wd
+    del dvec, dx, m
     torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- tp

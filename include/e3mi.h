@@ -169,6 +169,29 @@ e3_status e3_conv_bwd(const e3_plan* plan, const e3_graph* graph, const float* x
                       const float* s, const float* dm, float* dx, float* dvec, float* ds, void* ws,
                       size_t ws_bytes, e3_stream stream);
 
+/* Convolution with fused radial weights (eq. message-passing-linear, where the
+ * edge scalars come from a radial embedding followed by an MLP; App. A.3).
+ * The MLP's last linear layer is fused: with h [E, K] the per-edge features
+ * entering it (the radial basis itself for a one-layer model) and W [K, P, C]
+ * its weight, the kernels use s_e[k, q] = sum_j h[e, j] W[j, k, q], formed on
+ * the matrix cores and never written to memory.  1 <= K <= 16.
+ *
+ * e3_conv_fwd_radial: m [n_nodes, D_out, C] as e3_conv_fwd with these s.
+ * e3_conv_bwd_radial: from dm computes dx [n_nodes, D_in, C], dvec [E, 3]
+ *   (through the harmonics only: the dependence of h on the edge length is the
+ *   caller's), dh [E, K] = sum_{k,q} ds W and dW [K, P, C] = sum_e h_e ds_e,
+ *   with ds of eq. conv-bwd.  Deterministic: dW is a fixed-order sum of
+ *   fixed row-chunk partials.  Padding edges get dh = 0 and dvec = 0.
+ *   ws: at least e3_conv_radial_workspace_size bytes (ds of the live edges,
+ *   the partials of dW and dh, and the plain backward's scratch).
+ * x, W, m, dx, dm and ws must be 16-byte aligned; h, dh, dW need 4. */
+e3_status e3_conv_radial_workspace_size(const e3_plan* plan, const e3_graph* graph, int K, size_t* bwd_bytes);
+e3_status e3_conv_fwd_radial(const e3_plan* plan, const e3_graph* graph, const float* x, const float* vec,
+                             const float* h, const float* W, int K, float* m, e3_stream stream);
+e3_status e3_conv_bwd_radial(const e3_plan* plan, const e3_graph* graph, const float* x, const float* vec,
+                             const float* h, const float* W, int K, const float* dm, float* dx, float* dvec,
+                             float* dh, float* dW, void* ws, size_t ws_bytes, e3_stream stream);
+
 /* Per-kernel timing (instrumentation).  While enabled, every kernel the
  * library launches is bracketed by two HIP events on the caller's stream.
  * e3_timing_read waits for the recorded events and returns, per kernel name

@@ -111,6 +111,9 @@ constexpr int kXcd = 8;
 #define E3_FWD_CPL 2
 #endif
 // 1: the backward sweep double-buffers the path weights as well as the x rows.
+#ifndef E3_RAD_WREG
+#define E3_RAD_WREG 1
+#endif
 #ifndef E3_BWD_DB_S
 #define E3_BWD_DB_S 1
 #endif
@@ -497,6 +500,10 @@ struct ConvArgs {
   int chunk;  // receivers per XCD
   int C;
   int nslab;  // channel slabs of 64 lanes x CPL channels
+  // fused radial weights: s[e, k, q] = sum_j h[e, j] W[j, k, q]
+  const float* h;  // [E, K]
+  const float* W;  // [K, P, C]
+  int K;
 };
 
 // Receiver, group and channel slab of this wave: XCD k = blockIdx % 8 walks
@@ -785,6 +792,435 @@ __global__ __launch_bounds__(256) void k_zero_pad(const int* __restrict__ pad_ei
   if (threadIdx.x < 3) dvec[3 * e + threadIdx.x] = 0.0f;
 }
 
+
+// ------------------------------------------------------------ fused radial weights
+// The per-edge weights s_e = h_e W (K radial features times a K x (P C)
+// matrix) are formed in the sweep kernels on the matrix cores and never
+// stored.  One v_mfma_f32_4x4x1f32 (16 blocks of 4x4, K = 1) takes h[edge i][j]
+// from lane 4b + i and W[j][k][channel] from every lane; lane 4b + c then holds
+// s[edge i][k][its channel] in accumulator register i, i.e. four edges of the
+// lane-per-channel layout the contraction code consumes.  K steps of that per
+// path give s for four edges.  Both sweeps use one channel per lane.
+constexpr int kRadKMax = 16;
+
+// W held in registers (KR = 8, for K <= 8): wr[j][p] = W[j][path p][channel].
+template <class V, int NPATH, int KR>
+__device__ __forceinline__ void radial_quad_reg(const float (&wr)[KR][NPATH], const float* sH, int q4,
+                                                f4v (&s4)[NPATH]) {
+  const int lane = threadIdx.x;
+#pragma unroll
+  for (int p = 0; p < NPATH; ++p) s4[p] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int j = 0; j < KR; ++j) {
+    const float hv = sH[(q4 + (lane & 3)) * kRadKMax + j];
+#pragma unroll
+    for (int p = 0; p < NPATH; ++p) s4[p] = __builtin_amdgcn_mfma_f32_4x4x1f32(hv, wr[j][p], s4[p], 0, 0, 0);
+  }
+}
+
+template <class V, int NPATH>
+__device__ __forceinline__ void radial_quad(const RowBuf& wb, const float* sH, int q4, int K, const int (&path)[NPATH],
+                                            f4v (&s4)[NPATH]) {
+  const int lane = threadIdx.x;
+#pragma unroll
+  for (int p = 0; p < NPATH; ++p) s4[p] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int j = 0; j < K; ++j) {
+    const float hv = sH[(q4 + (lane & 3)) * kRadKMax + j];
+    float wv[NPATH][1];
+#pragma unroll
+    for (int p = 0; p < NPATH; ++p) bld<1>(wb, j * V::NP + path[p], wv[p]);
+#pragma unroll
+    for (int p = 0; p < NPATH; ++p) s4[p] = __builtin_amdgcn_mfma_f32_4x4x1f32(hv, wv[p][0], s4[p], 0, 0, 0);
+  }
+}
+
+// Lane j < n of the batch stages h of its edge (rows past n read as zero).
+__device__ __forceinline__ void stage_h(const ConvArgs& a, int lane, int n, int my_e, float* sH) {
+  if (lane < kEdgeBatch)
+    for (int j = 0; j < a.K; ++j) sH[lane * kRadKMax + j] = lane < n ? a.h[(int64_t)my_e * a.K + j] : 0.0f;
+}
+
+template <class V, int G, int KR>
+__device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, float* sA, float* sH) {
+  using F = typename V::template FG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<1>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  float acc[F::NROW][1];
+#pragma unroll
+  for (int i = 0; i < F::NROW; ++i) acc[i][0] = 0.0f;
+  const RowBuf wb = row_buf(a.W, (int64_t)a.K * V::NP * C * 4, q, C);
+  float wr[KR > 0 ? KR : 1][F::NPATH];
+  if constexpr (KR > 0) {
+#pragma unroll
+    for (int j = 0; j < KR; ++j)
+#pragma unroll
+      for (int p = 0; p < F::NPATH; ++p) {
+        float v[1] = {0.0f};
+        if (j < a.K) bld<1>(wb, j * V::NP + F::PATH[p], v);
+        wr[j][p] = v[0];
+      }
+  }
+  for (int eb = e0; eb < e1; eb += kEdgeBatch) {
+    const int n = imin(kEdgeBatch, e1 - eb);
+    int my_e = 0, my_src = 0;
+    if (lane < n) {
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
+      float ux, uy, uz, inv;
+      unit_of(a.vec, my_e, ux, uy, uz, inv);
+      float Y[V::D_SH];
+      V::sh(ux, uy, uz, Y);
+      F::make_A(Y, sA + lane * F::NA);
+    }
+    stage_h(a, lane, n, my_e, sH);
+    __syncthreads();
+    float xa[F::NXR][1], xb[F::NXR][1];
+    auto load_x = [&](int j, float (&xv)[F::NXR][1]) {
+      if (!act) return;
+      const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+      const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+#pragma unroll
+      for (int i = 0; i < F::NXR; ++i) bld<1>(xr, F::XROW[i], xv[i]);
+    };
+    load_x(0, xa);
+    for (int q4 = 0; q4 < n; q4 += 4) {
+      f4v s4[F::NPATH];
+      if constexpr (KR > 0)
+        radial_quad_reg<V, F::NPATH, (KR > 0 ? KR : 1)>(wr, sH, q4, s4);
+      else
+        radial_quad<V, F::NPATH>(wb, sH, q4, a.K, F::PATH, s4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = q4 + i;
+        if (j < n) {
+          float se[F::NPATH][1];
+#pragma unroll
+          for (int p = 0; p < F::NPATH; ++p) se[p][0] = s4[p][i];
+          if (i & 1) {
+            if (j + 1 < n) load_x(j + 1, xa);
+            if (act) F::template edge<1>(sA + j * F::NA, xb, se, acc);
+          } else {
+            if (j + 1 < n) load_x(j + 1, xb);
+            if (act) F::template edge<1>(sA + j * F::NA, xa, se, acc);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (act) {
+    const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+#pragma unroll
+    for (int i = 0; i < F::NROW; ++i) bst<1, kNT>(mb, F::OROW[i], acc[i]);
+  }
+}
+
+template <class V, int G, int KR>
+__device__ __forceinline__ void fwd_rad_dispatch(const ConvArgs& a, int b, int g, int sl, float* sA, float* sH) {
+  if constexpr (G < V::NFG) {
+    if (g == G)
+      fwd_rad_task<V, G, KR>(a, b, sl, sA, sH);
+    else
+      fwd_rad_dispatch<V, G + 1, KR>(a, b, g, sl, sA, sH);
+  }
+}
+
+// KR = 8: W in registers (K <= 8); KR = 0: W re-read from cache per 4 edges.
+template <class V, int KR>
+__global__ __launch_bounds__(kWave, E3_FWD_MIN_WAVES) void k_conv_fwd_rad(ConvArgs a) {
+  __shared__ f4v smem[(kEdgeBatch * (V::MAX_NA_F + kRadKMax) + 3) / 4];
+  int b, g, sl;
+  if (!task_of<V::NFG>(a, b, g, sl)) return;
+  float* sA = reinterpret_cast<float*>(smem);
+  fwd_rad_dispatch<V, 0, KR>(a, b, g, sl, sA, sA + kEdgeBatch * V::MAX_NA_F);
+}
+
+// Backward sweep with radial weights: as k_conv_bwd_edges, but s comes from
+// the matrix cores and ds goes to scratch (row = edge id), where the gradient
+// kernel below reads it.
+template <class V, int G>
+__device__ __forceinline__ void bwd_rad_task(const ConvArgs& a, int b, int sl, float* sA, float* sY, float* sH) {
+  using B = typename V::template BG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<1>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  if (e0 == e1) return;
+  float dmv[B::NROW][1];
+  if (act) {
+    const RowBuf db = row_buf(a.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+#pragma unroll
+    for (int i = 0; i < B::NROW; ++i) bld<1>(db, B::OROW[i], dmv[i]);
+  }
+  const RowBuf wb = row_buf(a.W, (int64_t)a.K * V::NP * C * 4, q, C);
+  for (int eb = e0; eb < e1; eb += kEdgeBatch) {
+    const int n = imin(kEdgeBatch, e1 - eb);
+    int my_e = 0, my_src = 0, my_slot = 0;
+    if (lane < n) {
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
+      my_slot = a.r2s[eb + lane];
+      float ux, uy, uz, inv;
+      unit_of(a.vec, my_e, ux, uy, uz, inv);
+      float Y[V::D_SH];
+      V::sh(ux, uy, uz, Y);
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) sY[lane * V::D_SH + i] = Y[i];
+      B::make_A(Y, sA + lane * B::NA);
+    }
+    stage_h(a, lane, n, my_e, sH);
+    __syncthreads();
+    float xa[B::NXR][1], xb[B::NXR][1];
+    auto load_x = [&](int j, float (&xv)[B::NXR][1]) {
+      if (!act) return;
+      const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+      const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+#pragma unroll
+      for (int i = 0; i < B::NXR; ++i) bld<1>(xr, B::XROW[i], xv[i]);
+    };
+    auto compute = [&](int j, const float (&xv)[B::NXR][1], const float (&sv)[B::NPATH][1]) {
+      const int64_t slot = __builtin_amdgcn_readlane(my_slot, j);
+      float dy[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dy[i] = 0.0f;
+      if (act) {
+        float t[B::NXR][1], Yv[V::D_SH];
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) t[i][0] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
+        const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+        const RowBuf dsb = row_buf(a.ds + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        auto st = [&](int pl, const float (&v)[1]) { bst<1, kNT>(dsb, B::PATH[pl], v); };
+        float dyl[V::D_SH];
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0f;
+        B::template edge<1>(sA + j * B::NA, Yv, xv, sv, dmv, t, dyl, st);
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
+        const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) bst<1>(Tb, B::XROW[i], t[i]);
+      }
+      const float tot = wave_reduce16(dy, lane);
+      if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+    };
+    load_x(0, xa);
+    for (int q4 = 0; q4 < n; q4 += 4) {
+      f4v s4[B::NPATH];
+      radial_quad<V, B::NPATH>(wb, sH, q4, a.K, B::PATH, s4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = q4 + i;
+        if (j < n) {
+          float se[B::NPATH][1];
+#pragma unroll
+          for (int p = 0; p < B::NPATH; ++p) se[p][0] = s4[p][i];
+          if (i & 1) {
+            if (j + 1 < n) load_x(j + 1, xa);
+            compute(j, xb, se);
+          } else {
+            if (j + 1 < n) load_x(j + 1, xb);
+            compute(j, xa, se);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <class V, int G>
+__device__ __forceinline__ void bwd_rad_dispatch(const ConvArgs& a, int b, int g, int sl, float* sA, float* sY,
+                                                 float* sH) {
+  if constexpr (G < V::NBG) {
+    if (g == G)
+      bwd_rad_task<V, G>(a, b, sl, sA, sY, sH);
+    else
+      bwd_rad_dispatch<V, G + 1>(a, b, g, sl, sA, sY, sH);
+  }
+}
+
+template <class V>
+__global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd_rad(ConvArgs a) {
+  __shared__ f4v smem[(kEdgeBatch * (V::MAX_NA_B + V::D_SH + kRadKMax) + 3) / 4];
+  int b, g, sl;
+  if (!task_of<V::NBG>(a, b, g, sl)) return;
+  float* sA = reinterpret_cast<float*>(smem);
+  float* sY = sA + kEdgeBatch * V::MAX_NA_B;
+  bwd_rad_dispatch<V, 0>(a, b, g, sl, sA, sY, sY + kEdgeBatch * V::D_SH);
+}
+
+// Sum of v[8] over the wave by the same fixed tree as wave_reduce16; lane l
+// with l % 8 == 0 ends with the total of index l / 8.
+__device__ __forceinline__ float wave_reduce8(const float (&v)[8], int lane) {
+  float w4[4], w2[2];
+  const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float send = b5 ? v[i] : v[i + 4];
+    const float keep = b5 ? v[i + 4] : v[i];
+    w4[i] = keep + __shfl_xor(send, 32);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float send = b4 ? w4[i] : w4[i + 2];
+    const float keep = b4 ? w4[i + 2] : w4[i];
+    w2[i] = keep + __shfl_xor(send, 16);
+  }
+  float w1 = (b3 ? w2[1] : w2[0]) + __shfl_xor(b3 ? w2[0] : w2[1], 8);
+  w1 += __shfl_xor(w1, 4);
+  w1 += __shfl_xor(w1, 2);
+  w1 += __shfl_xor(w1, 1);
+  return w1;
+}
+
+// Radial gradients from ds (row = edge id, E rows of PC = P*C floats, padding
+// edges' rows zero):
+//   dW[j][col] = sum_e h[e][j] ds[e][col]   (split over fixed chunks of rows),
+//   dh[e][j]   = sum_col ds[e][col] W[j][col] (split over column slabs).
+// One wave per (row chunk, column slab); a slab is kGradF float4s per lane,
+// lane l owning float4 columns (kGradF sl + f) 64 + l.  The dW outer products
+// run on the matrix cores: h[e][4 kq + i] from lane 4b + i times ds[e][col]
+// gives dW[4 kq + i][col] in accumulator register i of the lane owning col.
+// Both partial sets are added up afterwards in a fixed order, so the result
+// does not depend on scheduling.
+constexpr int kGradF = 1;
+constexpr int kGradRows = 4;  // rows whose loads are issued before their arithmetic
+
+template <int KQ>
+__global__ __launch_bounds__(kWave) void k_rad_grad(const float* __restrict__ DS, const float* __restrict__ h,
+                                                    const float* __restrict__ W, float* __restrict__ dWp,
+                                                    float* __restrict__ DHp, int64_t n_rows, int PC4, int K,
+                                                    int nsl4, int rows_per) {
+  static_assert(KQ == 2 || KQ == 4, "K <= 8 or K <= 16");
+  constexpr int NV = 4 * KQ;
+  const int lane = threadIdx.x;
+  const int c = blockIdx.x / nsl4, sl = blockIdx.x % nsl4;
+  int col4[kGradF];
+#pragma unroll
+  for (int f = 0; f < kGradF; ++f) col4[f] = (sl * kGradF + f) * kWave + lane;
+  const int64_t r0 = (int64_t)c * rows_per;
+  const int64_t r1 = r0 + rows_per < n_rows ? r0 + rows_per : n_rows;
+  f4v wv[kGradF][NV];
+  {
+    const __amdgpu_buffer_rsrc_t wr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(W), (short)0, K * PC4 * 16, 0x00020000);
+#pragma unroll
+    for (int f = 0; f < kGradF; ++f)
+#pragma unroll
+      for (int j = 0; j < NV; ++j)
+        wv[f][j] = (j < K && col4[f] < PC4)
+                       ? __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(wr, col4[f] * 16,
+                                                                                        j * PC4 * 16, 0))
+                       : f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+  f4v acc[kGradF][4][KQ];
+#pragma unroll
+  for (int f = 0; f < kGradF; ++f)
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int k = 0; k < KQ; ++k) acc[f][u][k] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int64_t rb = r0; rb < r1; rb += kGradRows) {
+    const int nr = (int)(r1 - rb < kGradRows ? r1 - rb : kGradRows);
+    f4v d[kGradRows][kGradF];
+    float hA[kGradRows][KQ];
+#pragma unroll
+    for (int u = 0; u < kGradRows; ++u) {
+#pragma unroll
+      for (int f = 0; f < kGradF; ++f) d[u][f] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int k = 0; k < KQ; ++k) hA[u][k] = 0.0f;
+      if (u < nr) {
+        const int64_t r = rb + u;
+        const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(DS) + r * PC4 * 4, (short)0, PC4 * 16, 0x00020000);
+#pragma unroll
+        for (int f = 0; f < kGradF; ++f)
+          if (col4[f] < PC4)
+            d[u][f] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(rr, col4[f] * 16, 0, kNT));
+#pragma unroll
+        for (int k = 0; k < KQ; ++k) {
+          const int j = 4 * k + (lane & 3);
+          hA[u][k] = j < K ? h[r * K + j] : 0.0f;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kGradRows; ++u) {
+      if (u < nr) {
+        float dh[NV];
+#pragma unroll
+        for (int j = 0; j < NV; ++j) dh[j] = 0.0f;
+#pragma unroll
+        for (int f = 0; f < kGradF; ++f) {
+#pragma unroll
+          for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+            for (int k = 0; k < KQ; ++k)
+              acc[f][c4][k] = __builtin_amdgcn_mfma_f32_4x4x1f32(hA[u][k], d[u][f][c4], acc[f][c4][k], 0, 0, 0);
+#pragma unroll
+          for (int j = 0; j < NV; ++j)
+            dh[j] += d[u][f][0] * wv[f][j][0] + d[u][f][1] * wv[f][j][1] + d[u][f][2] * wv[f][j][2] +
+                     d[u][f][3] * wv[f][j][3];
+        }
+        float tot;
+        if constexpr (NV == 8)
+          tot = wave_reduce8(dh, lane);
+        else
+          tot = wave_reduce16(dh, lane);
+        if ((lane & (kWave / NV - 1)) == 0)
+          DHp[((int64_t)sl * n_rows + rb + u) * NV + lane / (kWave / NV)] = tot;
+      }
+    }
+  }
+  // dWp[c][j][col]: register i of acc[f][c4][k] is j = 4k + i, column 4 col4[f] + c4
+  float* out = dWp + (int64_t)c * K * PC4 * 4;
+#pragma unroll
+  for (int f = 0; f < kGradF; ++f)
+    if (col4[f] < PC4)
+#pragma unroll
+      for (int k = 0; k < KQ; ++k)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int j = 4 * k + i;
+          if (j < K) {
+            f4v v{acc[f][0][k][i], acc[f][1][k][i], acc[f][2][k][i], acc[f][3][k][i]};
+            *reinterpret_cast<f4v*>(out + ((int64_t)j * PC4 + col4[f]) * 4) = v;
+          }
+        }
+}
+
+// dW = sum over row chunks of the partials, in chunk order.
+__global__ __launch_bounds__(256) void k_rad_dw_sum(const float* __restrict__ dWp, float* __restrict__ dW,
+                                                     int64_t n, int nchunk) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.0f;
+  for (int c = 0; c < nchunk; ++c) s += dWp[(int64_t)c * n + i];
+  dW[i] = s;
+}
+
+// dh[e] = sum over column slabs of the partials (laid out [slab][edge][NV]),
+// in slab order; one thread per (edge, j).
+__global__ __launch_bounds__(256) void k_rad_dh_sum(const float* __restrict__ DHp, float* __restrict__ dh,
+                                                     int64_t n_rows, int K, int nsl4, int NV) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = i / NV;
+  const int j = (int)(i % NV);
+  if (r >= n_rows) return;
+  float s = 0.0f;
+  for (int sl = 0; sl < nsl4; ++sl) s += DHp[((int64_t)sl * n_rows + r) * NV + j];
+  if (j < K) dh[r * K + j] = s;
+}
+
 // ------------------------------------------------------------ graph
 __global__ void k_graph_keys(const int32_t* __restrict__ snd, const int32_t* __restrict__ rcv, int64_t n_edges,
                              int32_t n_nodes, int32_t pad, uint32_t* __restrict__ key_r, uint32_t* __restrict__ key_s,
@@ -982,6 +1418,130 @@ e3_status run_tp_bwd(const e3_plan* p, const float* x, const float* y, const flo
   return E3_OK;
 }
 
+// Scratch of the radial backward: T and DY as in the plain backward, then ds
+// by edge id (all E rows when any edge is live), the dW partials of each row
+// chunk and the dh partials of each column slab.
+struct RadWs {
+  size_t t, dy, ds, dwp, dhp;
+  int nchunk, rows_per, nsl4, nv, pc4;
+  size_t total() const { return t + dy + ds + dwp + dhp; }
+};
+
+template <class V>
+RadWs rad_ws(const e3_plan* p, const e3_graph* g, int K) {
+  RadWs w{};
+  const Ws b = bwd_ws<V>(p, g);
+  w.t = b.t_bytes, w.dy = b.dy_bytes;
+  const int64_t pc = (int64_t)V::NP * p->lay.C, nl = g->n_live > 0 ? g->n_edges : 0;
+  w.pc4 = (int)(pc / 4);
+  w.nsl4 = (w.pc4 + kWave * kGradF - 1) / (kWave * kGradF);
+  w.nv = K <= 8 ? 8 : 16;
+  // about 8k waves in the gradient kernel, at least 256 rows each
+  const int64_t want = std::max<int64_t>(1, 8192 / w.nsl4);
+  const int64_t nch = std::min<int64_t>(want, std::max<int64_t>(1, (nl + 255) / 256));
+  w.rows_per = (int)std::max<int64_t>(1, (nl + nch - 1) / nch);
+  w.nchunk = (int)((nl + w.rows_per - 1) / w.rows_per);
+  w.ds = align256((size_t)nl * pc * sizeof(float));
+  w.dwp = align256((size_t)w.nchunk * K * pc * sizeof(float));
+  w.dhp = align256((size_t)nl * w.nsl4 * w.nv * sizeof(float));
+  return w;
+}
+
+template <class V>
+e3_status run_fwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                      const float* W, int K, float* m, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.h = h, a.W = W, a.K = K, a.m = m;
+  a.nslab = p->nslab_b;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
+  {
+    TimedLaunch t_("conv_fwd_rad", st);
+    if (K <= 8 && E3_RAD_WREG)
+      hipLaunchKernelGGL((k_conv_fwd_rad<V, 8>), dim3(grid), dim3(kWave), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_conv_fwd_rad<V, 0>), dim3(grid), dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status run_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                      const float* W, int K, const float* dm, float* dx, float* dvec, float* dh, float* dW, void* ws,
+                      hipStream_t st) {
+  const RadWs w = rad_ws<V>(p, g, K);
+  char* base = reinterpret_cast<char*>(ws);
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.h = h, a.W = W, a.K = K, a.dm = dm;
+  a.T = reinterpret_cast<float*>(base);
+  a.DY = reinterpret_cast<float*>(base + w.t);
+  a.ds = reinterpret_cast<float*>(base + w.t + w.dy);
+  float* dWp = reinterpret_cast<float*>(base + w.t + w.dy + w.ds);
+  float* DHp = reinterpret_cast<float*>(base + w.t + w.dy + w.ds + w.dwp);
+  a.nslab = p->nslab_b;
+  if (g->n_live > 0) {
+    const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
+    TimedLaunch t_("conv_bwd_rad_edges", st);
+    hipLaunchKernelGGL((k_conv_bwd_rad<V>), dim3(grid), dim3(kWave), 0, st, a);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_nodes > 0) {
+    TimedLaunch t_("conv_bwd_dx", st);
+    const int flat4 = V::D_IN * a.C / 4;
+    const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
+    hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * a.chunk * nsl)), dim3(kWave), 0, st, a.T, dx,
+                       g->rowptr_s, a.n_nodes, a.chunk, flat4, nsl);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_live > 0) {
+    {
+      TimedLaunch t_("conv_bwd_dvec", st);
+      hipLaunchKernelGGL((k_conv_bwd_dvec<V>), dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, vec, a.DY,
+                         g->eid_r, dvec, g->n_live, p->nslab_b);
+      E3_HIP(hipGetLastError());
+    }
+    if (g->n_pad > 0) {
+      // the ds rows of padding edges enter the gradient sums: clear them
+      TimedLaunch t_("rad_pad_ds", st);
+      hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad,
+                         a.ds, dvec, (int64_t)w.pc4 * 4);
+      E3_HIP(hipGetLastError());
+    }
+    const int64_t E = g->n_edges;
+    {
+      TimedLaunch t_("rad_grad", st);
+      const dim3 grid((unsigned)((int64_t)w.nchunk * w.nsl4));
+      if (K <= 8)
+        hipLaunchKernelGGL(k_rad_grad<2>, grid, dim3(kWave), 0, st, a.ds, h, W, dWp, DHp, E, w.pc4, K, w.nsl4,
+                           w.rows_per);
+      else
+        hipLaunchKernelGGL(k_rad_grad<4>, grid, dim3(kWave), 0, st, a.ds, h, W, dWp, DHp, E, w.pc4, K, w.nsl4,
+                           w.rows_per);
+      E3_HIP(hipGetLastError());
+    }
+    {
+      TimedLaunch t_("rad_dh_sum", st);
+      hipLaunchKernelGGL(k_rad_dh_sum, dim3(blocks_for(E * w.nv, 256)), dim3(256), 0, st, DHp, dh, E, K, w.nsl4,
+                         w.nv);
+      E3_HIP(hipGetLastError());
+    }
+  }
+  {
+    const int64_t n = (int64_t)K * w.pc4 * 4;
+    TimedLaunch t_("rad_dw_sum", st);
+    hipLaunchKernelGGL(k_rad_dw_sum, dim3(blocks_for(n, 256)), dim3(256), 0, st, dWp, dW, n, w.nchunk);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_pad > 0) {
+    TimedLaunch t_("conv_bwd_pad", st);
+    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, dh,
+                       dvec, (int64_t)K);
+    E3_HIP(hipGetLastError());
+  }
+  return E3_OK;
+}
+
 template <class V>
 size_t tp_ws(const e3_plan* p, int64_t rows) {
   return align256((size_t)rows * V::NBG * p->nslab_b * 16 * sizeof(float));
@@ -999,6 +1559,11 @@ struct VariantOps {
   e3_status (*tpb)(const e3_plan*, const float*, const float*, const float*, const float*, float*, float*, float*,
                    void*, int64_t, hipStream_t);
   size_t (*tpws)(const e3_plan*, int64_t);
+  e3_status (*rfwd)(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*, int,
+                    float*, hipStream_t);
+  e3_status (*rbwd)(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*, int,
+                    const float*, float*, float*, float*, float*, void*, hipStream_t);
+  RadWs (*rws)(const e3_plan*, const e3_graph*, int);
 };
 
 #define E3_VARIANT(V)                                                                                    \
@@ -1014,7 +1579,10 @@ struct VariantOps {
              {&run_tp<e3gen::V, 1>, &run_tp<e3gen::V, 2>},                                               \
              &bwd_ws<e3gen::V>,                                                                          \
              &run_tp_bwd<e3gen::V, 1>,                                                                   \
-             &tp_ws<e3gen::V>},
+             &tp_ws<e3gen::V>,                                                                           \
+             &run_fwd_rad<e3gen::V>,                                                                     \
+             &run_bwd_rad<e3gen::V>,                                                                     \
+             &rad_ws<e3gen::V>},
 
 const VariantOps kVariants[] = {E3GEN_FOR_EACH_VARIANT(E3_VARIANT)};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
@@ -1427,6 +1995,40 @@ e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
   return v.bwd[cpl_index(cpl_of(p))](p, g, x, vec, s, dm, dx, dvec, ds, ws, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_conv_radial_workspace_size(const e3_plan* p, const e3_graph* g, int K, size_t* bwd_bytes) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g || !bwd_bytes || K < 1 || K > kRadKMax) return E3_ERR_INVALID_ARG;
+  *bwd_bytes = kVariants[p->variant].rws(p, g, K).total();
+  return E3_OK;
+}
+
+e3_status e3_conv_fwd_radial(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                             const float* W, int K, float* m, e3_stream stream) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g || K < 1 || K > kRadKMax) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x) || !W || !aligned16(W))) return E3_ERR_INVALID_ARG;
+  if (g->n_live > 0 && (!vec || !h)) return E3_ERR_INVALID_ARG;
+  return kVariants[p->variant].rfwd(p, g, x, vec, h, W, K, m, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_conv_bwd_radial(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                             const float* W, int K, const float* dm, float* dx, float* dvec, float* dh, float* dW,
+                             void* ws, size_t ws_bytes, e3_stream stream) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g || K < 1 || K > kRadKMax || !W || !aligned16(W) || !dW) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
+    return E3_ERR_INVALID_ARG;
+  if (g->n_edges > 0 && (!vec || !h || !dh || !dvec)) return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  const RadWs w = v.rws(p, g, K);
+  if (w.total() > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
+  if (ws_bytes < w.total()) return E3_ERR_WORKSPACE_TOO_SMALL;
+  return v.rbwd(p, g, x, vec, h, W, K, dm, dx, dvec, dh, dW, ws, reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

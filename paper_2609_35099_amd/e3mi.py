@@ -58,6 +58,9 @@ SIGNATURES = {
     "e3_tp_workspace_size": (_I, [_P, _I64, ct.POINTER(ct.c_size_t)]),
     "e3_tp_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, _P]),
     "e3_conv_workspace_size": (_I, [_P, _P, ct.POINTER(ct.c_size_t), ct.POINTER(ct.c_size_t)]),
+    "e3_conv_radial_workspace_size": (_I, [_P, _P, ct.c_int, ct.POINTER(ct.c_size_t)]),
+    "e3_conv_fwd_radial": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P, _P]),
+    "e3_conv_bwd_radial": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_fwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_timing_enable": (_I, [_I]),
@@ -309,6 +312,47 @@ def conv_bwd(plan: Plan, graph: Graph, x, vec, s, dm, dx=None, dvec=None, ds=Non
                              _ptr(dvec, "dvec", (E, 3)), _ptr(ds, "ds", (E, plan.P, plan.C)),
                              ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd")
     return dx, dvec, ds
+
+
+def conv_radial_workspace_size(plan: Plan, graph: Graph, K: int) -> int:
+    b = ct.c_size_t()
+    _check(lib().e3_conv_radial_workspace_size(plan.handle, graph.handle, K, ct.byref(b)),
+           "e3_conv_radial_workspace_size")
+    return b.value
+
+
+def conv_fwd_radial(plan: Plan, graph: Graph, x, vec, h, W, out=None, stream=None):
+    """m with per-edge weights s_e = h_e W formed inside the kernel (h [E, K], W [K, P, C])."""
+    N, E = graph.n_nodes, graph.n_edges
+    K = W.shape[0]
+    out = _empty((N, plan.D_out, plan.C)) if out is None else out
+    _check(lib().e3_conv_fwd_radial(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                                    _ptr(vec, "vec", (E, 3)), _ptr(h, "h", (E, K)),
+                                    _ptr(W, "W", (K, plan.P, plan.C)), K,
+                                    _ptr(out, "m", (N, plan.D_out, plan.C)), _stream(stream)),
+           "e3_conv_fwd_radial")
+    return out
+
+
+def conv_bwd_radial(plan: Plan, graph: Graph, x, vec, h, W, dm, dx=None, dvec=None, dh=None, dW=None, ws=None,
+                    stream=None):
+    """(dx, dvec, dh, dW) of the convolution with fused radial weights."""
+    N, E = graph.n_nodes, graph.n_edges
+    K = W.shape[0]
+    dx = _empty((N, plan.D_in, plan.C)) if dx is None else dx
+    dvec = _empty((E, 3)) if dvec is None else dvec
+    dh = _empty((E, K)) if dh is None else dh
+    dW = _empty((K, plan.P, plan.C)) if dW is None else dW
+    if ws is None:
+        ws = workspace(conv_radial_workspace_size(plan, graph, K))
+    _check(lib().e3_conv_bwd_radial(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                                    _ptr(vec, "vec", (E, 3)), _ptr(h, "h", (E, K)),
+                                    _ptr(W, "W", (K, plan.P, plan.C)), K,
+                                    _ptr(dm, "dm", (N, plan.D_out, plan.C)), _ptr(dx, "dx", (N, plan.D_in, plan.C)),
+                                    _ptr(dvec, "dvec", (E, 3)), _ptr(dh, "dh", (E, K)),
+                                    _ptr(dW, "dW", (K, plan.P, plan.C)), ct.c_void_p(ws.data_ptr()), ws.numel(),
+                                    _stream(stream)), "e3_conv_bwd_radial")
+    return dx, dvec, dh, dW
 
 
 # ---------------------------------------------------------------- timing

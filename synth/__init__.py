@@ -342,6 +342,16 @@ def edge_weights_rows(cfg: Config, vec: np.ndarray, rows: np.ndarray, W=None) ->
     return out
 
 
+def radial_inputs(cfg: Config, vec: np.ndarray):
+    """(h [E, 8], W [8, P, C]) float32 with h = the Bessel basis of |r| and W the
+    config's fixed random matrix: h @ W is the config's per-edge weight recipe."""
+    P, _ = n_paths_dout(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    r = np.linalg.norm(vec.astype(np.float64), axis=1)
+    h = bessel_basis(r).astype(np.float32)
+    W = bessel_matrix(cfg).astype(np.float32).reshape(N_BESSEL, P, cfg.channels)
+    return h, W
+
+
 def tp_inputs(cfg: Config, rows: int | None = None):
     """(x [R, D_in, C], unit vectors u [R, 3], w [R, P, C]) for the tensor product."""
     R = cfg.rows if rows is None else rows

@@ -131,3 +131,9 @@ def test_null_and_negative_arguments_rejected_before_device_work():
     fake = [ct.c_void_p(256)] * 7
     assert L.e3_tp_bwd(plan.handle, *fake, ct.c_void_p(256), 16, 10, None) == 4   # workspace too small
     assert L.e3_tp_bwd(plan.handle, *([ct.c_void_p(4)] * 7), ct.c_void_p(256), n.value, 10, None) == 1
+    # fused radial weights: a graph is required, K must lie in [1, 16]
+    assert L.e3_conv_radial_workspace_size(plan.handle, None, 8, ct.byref(n)) == 1
+    assert L.e3_conv_fwd_radial(plan.handle, None, None, None, None, None, 8, None, None) == 1
+    assert L.e3_conv_bwd_radial(plan.handle, None, None, None, None, None, 8, None, None, None, None, None,
+                                None, 0, None) == 1
+    assert L.e3_conv_fwd_radial(None, None, None, None, None, None, 8, None, None) == 1

@@ -13,6 +13,7 @@ import synth
 from oracle import conv as oconv
 from oracle import graph as ograph
 from oracle import irreps as oirreps
+from oracle import radial as oradial
 from oracle import sh as osh
 from oracle import tp as otp
 
@@ -390,6 +391,135 @@ def test_conv_stress_config5_sampled(e3):
     ri, ei = torch.as_tensor(rs, device=dev), torch.as_tensor(es, device=dev)
     errs = dict(m=err_m, dx=rel_l2(to_np(dx[ri]), ref_dx), ds=rel_l2(to_np(ds[ei]), ref_ds),
                 dvec=rel_l2(to_np(dvec[ei]), ref_dv))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+
+
+# ---------------------------------------------------------------- fused radial weights
+def _radial_full(e3, plan, lay, snd, rcv, n, vec, x, h, W, dm, pad=-1, repeat=2):
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    xs, vs, hs, Ws, dms = (to_dev(a) for a in (x, vec, h, W, dm))
+    outs = []
+    for _ in range(repeat):
+        m = e3.conv_fwd_radial(plan, G, xs, vs, hs, Ws)
+        outs.append((m,) + e3.conv_bwd_radial(plan, G, xs, vs, hs, Ws, dms))
+    outs = [[to_np(t) for t in o] for o in outs]
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert np.array_equal(a, b), "not deterministic"
+    m, dx, dvec, dh, dW = outs[0]
+    ref_m = oradial.conv_fwd(lay, x, vec, h, W, snd, rcv, n, pad_node=pad).numpy()
+    ref = oradial.conv_bwd(lay, x, vec, h, W, dm, snd, rcv, n, pad_node=pad)
+    errs = dict(m=rel_l2(m, ref_m), dx=rel_l2(dx, ref["dx"].numpy()), dvec=rel_l2(dvec, ref["dvec"].numpy()),
+                dh=rel_l2(dh, ref["dh"].numpy()), dW=rel_l2(dW, ref["dW"].numpy()))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    return m, dx, dvec, dh, dW
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,n,e,K,pad", [
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, 100, 2000, 8, -1),
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, 60, 1200, 16, 5),
+    ("64x0e+64x1o+64x2e+64x3o", 3, 3, 50, 900, 5, -1),
+    ("16x0e+16x1o+16x2e", 3, 3, 40, 600, 1, 3),
+    ("8x0e+8x1o", 2, 2, 30, 300, 12, -1),
+    ("100x0e+100x1o", 3, 3, 40, 700, 8, -1),   # 64 + 36 channel lanes
+])
+def test_conv_radial_random_graphs_full(e3, irreps, lsh, lout, n, e, K, pad):
+    _say("conv radial", irreps, n, e, K, pad)
+    rng = np.random.default_rng(11)
+    lay = oirreps.layout(irreps, lsh, lout)
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    h = rng.standard_normal((e, K)).astype(np.float32)
+    W = (rng.standard_normal((K, lay.n_paths, C)) / np.sqrt(K)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    plan = e3.Plan(irreps, lsh, lout)
+    m, dx, dvec, dh, dW = _radial_full(e3, plan, lay, snd, rcv, n, vec, x, h, W, dm, pad)
+    if pad >= 0:
+        dead = (snd == pad) | (rcv == pad)
+        assert np.all(dh[dead] == 0) and np.all(dvec[dead] == 0)
+        assert np.all(m[pad] == 0) and np.all(dx[pad] == 0)
+
+
+def test_conv_radial_degenerate_graphs(e3):
+    """No edges (dW = 0, m = 0); a single edge."""
+    irreps = "128x0e+128x1o+128x2e+128x3o"
+    lay = oirreps.layout(irreps, 3, 3)
+    plan = e3.Plan(irreps, 3, 3)
+    rng = np.random.default_rng(12)
+    K = 8
+    W = rng.standard_normal((K, lay.n_paths, 128)).astype(np.float32)
+    for snd, rcv, n in [(np.zeros(0, np.int32), np.zeros(0, np.int32), 4),
+                        (np.array([2], np.int32), np.array([0], np.int32), 3)]:
+        _say("conv radial degenerate", len(snd))
+        e = len(snd)
+        vec = rng.standard_normal((e, 3)).astype(np.float32)
+        x = rng.standard_normal((n, lay.d_in, 128)).astype(np.float32)
+        h = rng.standard_normal((e, K)).astype(np.float32)
+        dm = rng.standard_normal((n, lay.d_out, 128)).astype(np.float32)
+        if e == 0:
+            G = e3.Graph(to_dev(snd), to_dev(rcv), n)
+            xs, Ws = to_dev(x), to_dev(W)
+            vs = to_dev(vec.reshape(0, 3))
+            hs = to_dev(h.reshape(0, K))
+            m = e3.conv_fwd_radial(plan, G, xs, vs, hs, Ws)
+            dx, dvec, dh, dW = e3.conv_bwd_radial(plan, G, xs, vs, hs, Ws, to_dev(dm))
+            assert np.all(to_np(m) == 0) and np.all(to_np(dx) == 0) and np.all(to_np(dW) == 0)
+        else:
+            m = _radial_full(e3, plan, lay, snd, rcv, n, vec, x, h, W, dm, repeat=1)[0]
+            assert np.all(m[1:] == 0)
+
+
+def test_conv_radial_config4_sampled(e3):
+    """Config 4 (24,000-atom water box) with its own radial recipe fused: h = the
+    8-function Bessel basis of |r|, W = the config's fixed matrix.  m, dx, dvec
+    and dh are checked against the oracle on sampled rows.  dW sums over all
+    1.27M edges, which the oracle cannot do in seconds: it is checked against a
+    float64 sum of h_e ds_e with ds from the plain backward (itself checked
+    against the oracle in test_conv_full_size_sampled)."""
+    import torch
+    _say("conv radial config 4 full")
+    cfg = synth.CONFIGS[4]
+    g = synth.graph(cfg)
+    x = synth.node_features(cfg, g.n_nodes)
+    dm = synth.out_cotangent(cfg, g.n_nodes)
+    h, W = synth.radial_inputs(cfg, g.vec)
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), g.n_nodes)
+    xs, vs, hs, Ws, dms = (to_dev(a) for a in (x, g.vec, h, W, dm))
+    m = e3.conv_fwd_radial(plan, G, xs, vs, hs, Ws)
+    dx, dvec, dh, dW = e3.conv_bwd_radial(plan, G, xs, vs, hs, Ws, dms)
+    torch.cuda.synchronize()
+    lay = layout_of(cfg)
+    rng = np.random.default_rng(13)
+    E = g.sender.shape[0]
+    rs = np.concatenate([[0, g.n_nodes - 1], rng.choice(g.n_nodes, 22, replace=False)])
+    es = np.concatenate([[0, E - 1], rng.choice(E, 62, replace=False)])
+    sfn = lambda rows: oradial.weights(h[rows], W).numpy()
+    ref_m = oracle_fwd_rows(lay, x, g.vec, sfn, g.sender, g.receiver, g.n_nodes, rs)
+    ref_dx, ref_ds, ref_dv = oracle_bwd_rows(lay, x, g.vec, sfn, dm, g.sender, g.receiver, g.n_nodes, rs, es)
+    ref_dh = np.einsum("ekq,jkq->ej", ref_ds, W.astype(np.float64))
+    ri, ei = torch.as_tensor(rs, device="cuda"), torch.as_tensor(es, device="cuda")
+    errs = dict(m=rel_l2(to_np(m[ri]), ref_m), dx=rel_l2(to_np(dx[ri]), ref_dx),
+                dvec=rel_l2(to_np(dvec[ei]), ref_dv), dh=rel_l2(to_np(dh[ei]), ref_dh))
+    del m
+    # dW against a float64 sum over the plain backward's ds
+    s = torch.empty((E, plan.P, plan.C), dtype=torch.float32, device="cuda")
+    W64 = Ws.double().reshape(W.shape[0], -1)
+    for e0 in range(0, E, 1 << 16):
+        e1 = min(E, e0 + (1 << 16))
+        s[e0:e1] = (hs[e0:e1].double() @ W64).float().reshape(e1 - e0, plan.P, plan.C)
+    ds = e3.conv_bwd(plan, G, xs, vs, s, dms)[2]
+    del s
+    acc = torch.zeros_like(W64)
+    for e0 in range(0, E, 1 << 16):
+        e1 = min(E, e0 + (1 << 16))
+        acc += hs[e0:e1].double().T @ ds[e0:e1].double().reshape(e1 - e0, -1)
+    errs["dW"] = rel_l2(to_np(dW).reshape(acc.shape), acc.cpu().numpy())
     print("rel-L2", errs, flush=True)
     for k, v in errs.items():
         assert v < TOL, (k, v)
