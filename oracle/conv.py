@@ -85,15 +85,14 @@ def conv_fwd(lay, x, vec, s, sender, receiver, n_nodes, pad_node=-1, receivers=N
                            receivers, chunk)
 
 
-def conv_bwd(lay, x, vec, s, dm, sender, receiver, n_nodes, pad_node=-1,
-             senders=None, edges=None, chunk=1024):
-    """Cotangents of eq. (conv-bwd).
+def conv_bwd_from_y(lay, x, y, s, dm, sender, receiver, n_nodes, pad_node=-1,
+                    senders=None, edges=None, chunk=1024):
+    """Cotangents of eq. (conv-bwd) with the harmonics y [E, D_sh] given.
 
     Returns dict(dx=[len(senders) or N, D_in, C], ds=[len(edges) or E, P, C],
-    dvec=[len(edges) or E, 3], dy=[len(edges) or E, D_sh]), all float64.
+    dy=[len(edges) or E, D_sh]), all float64; differentiable in x, y, s, dm.
     """
-    x, s, dm = t64(x), t64(s), t64(dm)
-    vec = t64(vec)
+    x, y, s, dm = t64(x), t64(y), t64(s), t64(dm)
     snd = _np(sender).astype(np.int64)
     rcv = _np(receiver).astype(np.int64)
     E = snd.shape[0]
@@ -111,28 +110,27 @@ def conv_bwd(lay, x, vec, s, dm, sender, receiver, n_nodes, pad_node=-1,
     dx = x.new_zeros((srows.shape[0], lay.d_in, C))
     for c0 in range(0, eids.shape[0], chunk):
         e = eids[c0:c0 + chunk]
-        y = _sh.sh_vec(lay.lmax_sh, vec[torch.as_tensor(e)])
+        ye = y[torch.as_tensor(e)]
         se = s[torch.as_tensor(e)]
         dmb = dm[torch.as_tensor(rcv[e])]
         t = x.new_zeros((e.shape[0], lay.d_in, C))
         for p, blk in zip(lay.paths, blocks):
-            yb = y[:, p.y_off:p.y_off + 2 * p.l2 + 1]
+            yb = ye[:, p.y_off:p.y_off + 2 * p.l2 + 1]
             dmk = dmb[:, p.out_off:p.out_off + 2 * p.l3 + 1, :]
             t[:, p.x_off:p.x_off + 2 * p.l1 + 1, :] += torch.einsum(
                 "Mab,eb,eq,eMq->eaq", blk, yb, se[:, p.k, :], dmk)
         dx = dx.index_add(0, torch.as_tensor(where[snd[e]]), t)
 
-    # --- ds, dy, dvec: edge-local ------------------------------------------
+    # --- ds, dy: edge-local ------------------------------------------------
     erows = np.arange(E, dtype=np.int64) if edges is None else np.asarray(edges, np.int64)
     ds = x.new_zeros((erows.shape[0], lay.n_paths, C))
     dy = x.new_zeros((erows.shape[0], lay.d_sh))
-    dvec = x.new_zeros((erows.shape[0], 3))
     live = np.nonzero(keep[erows])[0]
     for c0 in range(0, live.shape[0], chunk):
         pos = live[c0:c0 + chunk]
         e = erows[pos]
         et = torch.as_tensor(e)
-        y = _sh.sh_vec(lay.lmax_sh, vec[et])
+        ye = y[et]
         xa = x[torch.as_tensor(snd[e])]
         se = s[et]
         dmb = dm[torch.as_tensor(rcv[e])]
@@ -140,13 +138,58 @@ def conv_bwd(lay, x, vec, s, dm, sender, receiver, n_nodes, pad_node=-1,
         dyc = x.new_zeros((e.shape[0], lay.d_sh))
         for p, blk in zip(lay.paths, blocks):
             xb = xa[:, p.x_off:p.x_off + 2 * p.l1 + 1, :]
-            yb = y[:, p.y_off:p.y_off + 2 * p.l2 + 1]
+            yb = ye[:, p.y_off:p.y_off + 2 * p.l2 + 1]
             dmk = dmb[:, p.out_off:p.out_off + 2 * p.l3 + 1, :]
             z = torch.einsum("Mab,eaq,eb->eMq", blk, xb, yb)
             dsc[:, p.k, :] = (z * dmk).sum(dim=1)
             dyc[:, p.y_off:p.y_off + 2 * p.l2 + 1] += torch.einsum(
                 "Mab,eaq,eMq,eq->eb", blk, xb, dmk, se[:, p.k, :])
-        ds[torch.as_tensor(pos)] = dsc
-        dy[torch.as_tensor(pos)] = dyc
-        dvec[torch.as_tensor(pos)] = _sh.sh_vec_vjp(lay.lmax_sh, vec[et], dyc)
-    return dict(dx=dx, ds=ds, dy=dy, dvec=dvec)
+        ds = ds.index_put((torch.as_tensor(pos),), dsc)
+        dy = dy.index_put((torch.as_tensor(pos),), dyc)
+    return dict(dx=dx, ds=ds, dy=dy)
+
+
+def conv_bwd(lay, x, vec, s, dm, sender, receiver, n_nodes, pad_node=-1,
+             senders=None, edges=None, chunk=1024):
+    """Cotangents of eq. (conv-bwd) for y = Y(vec), plus dvec = J^T dy.
+
+    Returns dict(dx=[len(senders) or N, D_in, C], ds=[len(edges) or E, P, C],
+    dvec=[len(edges) or E, 3], dy=[len(edges) or E, D_sh]), all float64.
+    """
+    vec = t64(vec)
+    y = _sh.sh_vec(lay.lmax_sh, vec)
+    res = conv_bwd_from_y(lay, x, y, s, dm, sender, receiver, n_nodes, pad_node, senders, edges, chunk)
+    erows = np.arange(vec.shape[0], dtype=np.int64) if edges is None else np.asarray(edges, np.int64)
+    snd = _np(sender).astype(np.int64)
+    rcv = _np(receiver).astype(np.int64)
+    live = np.ones(erows.shape[0], dtype=bool)
+    if pad_node >= 0:
+        live &= (snd[erows] != pad_node) & (rcv[erows] != pad_node)
+    dvec = vec.new_zeros((erows.shape[0], 3))
+    idx = np.nonzero(live)[0]
+    if idx.shape[0]:
+        dvec[torch.as_tensor(idx)] = _sh.sh_vec_vjp(lay.lmax_sh, vec[torch.as_tensor(erows[idx])],
+                                                    res["dy"][torch.as_tensor(idx)])
+    res["dvec"] = dvec
+    return res
+
+
+def conv_bwd2(lay, x, y, s, dm, ddx, ddy, dds, sender, receiver, n_nodes, pad_node=-1):
+    """Second-order rule of eq. (conv-bwd-bwd-ddm) and eq. (conv-bwd2-xys).
+
+    (ddx, ddy, dds) are variations of the backward's outputs (dx, dy, ds); the
+    result holds the variations of its inputs: dict(dx, dy, ds, ddm), with
+        ddm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds)
+        dx  = dx of conv_bwd(x, ddy, s, dm) + dx of conv_bwd(x, y, dds, dm)
+        dy  = dy of conv_bwd(ddx, y, s, dm) + dy of conv_bwd(x, y, dds, dm)
+        ds  = ds of conv_bwd(ddx, y, s, dm) + ds of conv_bwd(x, ddy, s, dm).
+    """
+    def f(a, b, c):
+        return conv_fwd_from_y(lay, a, b, c, sender, receiver, n_nodes, pad_node)
+
+    def b(a, yy, c):
+        return conv_bwd_from_y(lay, a, yy, c, dm, sender, receiver, n_nodes, pad_node)
+
+    ddm = f(ddx, y, s) + f(x, ddy, s) + f(x, y, dds)
+    bx, by, bs = b(ddx, y, s), b(x, ddy, s), b(x, y, dds)
+    return dict(dx=by["dx"] + bs["dx"], dy=bx["dy"] + bs["dy"], ds=bx["ds"] + by["ds"], ddm=ddm)

@@ -343,3 +343,49 @@ def test_radial_bwd_central_differences(pad):
     assert abs(fd - an) < 1e-5 * max(1.0, abs(an))
     if pad >= 0:
         assert torch.all(res["dh"][snd == pad] == 0)
+
+
+# ---------------------------------------------------------------- double backward
+@pytest.mark.parametrize("spec,pad", [(("2x0e+2x1o+2x2e", 3, 3), -1), (("2x0e+2x1o", 2, 2), 3)])
+def test_conv_bwd2_against_autograd_and_central_differences(spec, pad):
+    """The composed second-order rule equals (a) float64 autograd of the first
+    backward and (b) a five-point difference of L = <ddx, dx> + <ddy, dy> + <dds, ds>
+    along a random direction of (x, y, s, dm)."""
+    rng = np.random.default_rng(31)
+    lay = irreps.layout(*spec)
+    n, e = 7, 26
+    snd, rcv, vec = _small_graph(rng, n=n, e=e)
+    if pad >= 0:
+        rcv[::5] = pad
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C))
+    y = rng.standard_normal((e, lay.d_sh))          # any y, not only harmonics
+    s = rng.standard_normal((e, lay.n_paths, C))
+    dm = rng.standard_normal((n, lay.d_out, C))
+    ddx = rng.standard_normal(x.shape)
+    ddy = rng.standard_normal(y.shape)
+    dds = rng.standard_normal(s.shape)
+    got = conv.conv_bwd2(lay, x, y, s, dm, ddx, ddy, dds, snd, rcv, n, pad_node=pad)
+
+    def L(xx, yy, ss, mm):
+        r = conv.conv_bwd_from_y(lay, xx, yy, ss, mm, snd, rcv, n, pad_node=pad)
+        return ((r["dx"] * torch.as_tensor(ddx)).sum() + (r["dy"] * torch.as_tensor(ddy)).sum()
+                + (r["ds"] * torch.as_tensor(dds)).sum())
+
+    leaves = [torch.tensor(a, dtype=torch.float64, requires_grad=True) for a in (x, y, s, dm)]
+    grads = torch.autograd.grad(L(*leaves), leaves)
+    for name, g in zip(("dx", "dy", "ds", "ddm"), grads):
+        assert torch.allclose(got[name], g, rtol=1e-11, atol=1e-11), name
+    u = [rng.standard_normal(a.shape) for a in (x, y, s, dm)]
+
+    def Lt(t):
+        return float(L(*[a + t * d for a, d in zip((x, y, s, dm), u)]))
+
+    # L(t) is a cubic in t: the five-point stencil is exact for it up to rounding
+    h = 0.1
+    fd = (8 * (Lt(h) - Lt(-h)) - (Lt(2 * h) - Lt(-2 * h))) / (12 * h)
+    an = sum(float((got[k] * torch.as_tensor(d)).sum()) for k, d in zip(("dx", "dy", "ds", "ddm"), u))
+    assert abs(fd - an) < 1e-9 * max(1.0, abs(an))
+    if pad >= 0:
+        dead = (snd == pad) | (rcv == pad)
+        assert torch.all(got["dy"][dead] == 0) and torch.all(got["ds"][dead] == 0)
