@@ -150,7 +150,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tp", action="store_true")
-    ap.add_argument("--only", choices=["all", "conv", "radial", "tp"], default="all")
+    ap.add_argument("--only", choices=["all", "conv", "radial", "bwd2", "tp"], default="all")
     ap.add_argument("--order", choices=["generated", "cell"], default="generated",
                     help="atom order of the water box: as generated (spatially random) or cell-sorted")
     ap.add_argument("--copy-probe", action="store_true",
@@ -302,6 +302,41 @@ def main():
         del rws, dh, dW, hs, Wd
     del dvec, dx, m
     torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- double backward
+    if args.only in ("all", "bwd2"):
+        ys = e3mi.sh(cfg.lmax_sh, vs)
+        s2 = synth.normal_device(cfg.cid, 2, (E, plan.P, C), dev)
+        dds = synth.normal_device(cfg.cid, 9, (E, plan.P, C), dev)
+        ddx = synth.normal_device(cfg.cid, 10, (N, plan.D_in, C), dev)
+        ddy = synth.normal_device(cfg.cid, 11, (E, plan.D_sh), dev)
+        ws2 = e3mi.workspace(e3mi.conv_workspace_size(plan, graph)[1])
+        for _ in range(args.warmup):
+            outs = e3mi.conv_bwd2(plan, graph, xs, ys, s2, dms, ddx, ddy, dds, ws=ws2)
+        del outs
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(args.steps):
+            outs = e3mi.conv_bwd2(plan, graph, xs, ys, s2, dms, ddx, ddy, dds, ws=ws2)
+        ev1.record()
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        per = e3mi.timing_read()
+        b2_ms = ev0.elapsed_time(ev1) / args.steps
+        f = 4
+        nb = (N * (2 * plan.D_in + plan.D_out) * C * f + E * (2 * plan.D_sh + 2 * plan.P * C) * f   # inputs
+              + N * (plan.D_in + plan.D_out) * C * f + E * (plan.D_sh + plan.P * C) * f)             # outputs
+        out["bwd2"] = {"workload": "double backward of the convolution, same water box; ddx, ddy, dds N(0,1)",
+                       "ms": round(b2_ms, 4), "edges_per_s": E / (b2_ms * 1e-3), "alg_bytes": nb,
+                       "alg_GBps": round(nb / (b2_ms * 1e-3) / 1e9, 1),
+                       "kernels": {k: {"ms_total_per_call": round(t / args.steps, 4), "launches": c}
+                                   for k, (t, c) in per.items()}}
+        log(f"bwd2: {b2_ms:.3f} ms, {out['bwd2']['alg_GBps']} GB/s; kernels {out['bwd2']['kernels']}")
+        del outs, ws2, s2, dds, ddx, ddy, ys
+        torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- tp
     if not args.no_tp and args.only in ("all", "tp"):

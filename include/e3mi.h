@@ -169,6 +169,35 @@ e3_status e3_conv_bwd(const e3_plan* plan, const e3_graph* graph, const float* x
                       const float* s, const float* dm, float* dx, float* dvec, float* ds, void* ws,
                       size_t ws_bytes, e3_stream stream);
 
+/* The convolution with the harmonics y [E, D_sh] given by the caller instead of
+ * computed from edge vectors: eq. message_passing_convolution and eq. conv-bwd
+ * exactly as stated (y is an input of both, dy an output of the backward).
+ * e3_conv_fwd_y:  m = conv(x, y, s).
+ * e3_conv_bwd_y:  dx [n_nodes, D_in, C], dy [E, D_sh], ds [E, P, C]; any of the
+ *   three may be NULL (not stored; dx == NULL also skips its segment sum).
+ * accumulate != 0: results are added to the outputs' contents (padding edges'
+ *   rows are then left unchanged) instead of overwriting them.
+ * ws as for e3_conv_bwd. */
+e3_status e3_conv_fwd_y(const e3_plan* plan, const e3_graph* graph, const float* x, const float* y,
+                        const float* s, float* m, int accumulate, e3_stream stream);
+e3_status e3_conv_bwd_y(const e3_plan* plan, const e3_graph* graph, const float* x, const float* y,
+                        const float* s, const float* dm, float* dx, float* dy, float* ds, int accumulate,
+                        void* ws, size_t ws_bytes, e3_stream stream);
+
+/* Double backward of the convolution (eq. conv-bwd-bwd-ddm and eq.
+ * conv-bwd2-xys): given the primals (x, y, s, dm) of a backward call and
+ * variations (ddx [n_nodes, D_in, C], ddy [E, D_sh], dds [E, P, C]) of its
+ * outputs, computes the variations of its inputs:
+ *   gdm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds)      [n_nodes, D_out, C]
+ *   gx  = dx of conv_bwd(x, ddy, s, dm) + dx of conv_bwd(x, y, dds, dm)
+ *   gy  = dy of conv_bwd(ddx, y, s, dm) + dy of conv_bwd(x, y, dds, dm)
+ *   gs  = ds of conv_bwd(ddx, y, s, dm) + ds of conv_bwd(x, ddy, s, dm)
+ * by three forward and three backward sweeps that store only the cotangents
+ * used and add in place.  Deterministic.  ws as for e3_conv_bwd. */
+e3_status e3_conv_bwd2(const e3_plan* plan, const e3_graph* graph, const float* x, const float* y,
+                       const float* s, const float* dm, const float* ddx, const float* ddy, const float* dds,
+                       float* gx, float* gy, float* gs, float* gdm, void* ws, size_t ws_bytes, e3_stream stream);
+
 /* Convolution with fused radial weights (eq. message-passing-linear, where the
  * edge scalars come from a radial embedding followed by an MLP; App. A.3).
  * The MLP's last linear layer is fused: with h [E, K] the per-edge features

@@ -500,6 +500,11 @@ struct ConvArgs {
   int chunk;  // receivers per XCD
   int C;
   int nslab;  // channel slabs of 64 lanes x CPL channels
+  const float* y;  // harmonics [E, D_sh] given by the caller, or null: from vec
+  int accum;       // add to m (forward) / ds (backward) instead of overwriting it
+  // backward: bytes of one ds / T row, or 0 when that output is not wanted (the
+  // pointer then refers to valid memory that is never written)
+  int64_t ds_row, t_row;
   // fused radial weights: s[e, k, q] = sum_j h[e, j] W[j, k, q]
   const float* h;  // [E, K]
   const float* W;  // [K, P, C]
@@ -523,7 +528,20 @@ __device__ __forceinline__ bool task_of(const ConvArgs& a, int& b, int& g, int& 
 }
 
 
-template <class V, int G, int CPL>
+// Harmonics of edge e: from the caller's y when given, else Y(vec_e / |vec_e|).
+template <class V>
+__device__ __forceinline__ void edge_harmonics(const ConvArgs& a, int64_t e, float (&Y)[V::D_SH]) {
+  if (a.y) {
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) Y[i] = a.y[e * V::D_SH + i];
+  } else {
+    float ux, uy, uz, inv;
+    unit_of(a.vec, e, ux, uy, uz, inv);
+    V::sh(ux, uy, uz, Y);
+  }
+}
+
+template <class V, int G, int CPL, bool ACC>
 __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float* sA) {
   using F = typename V::template FG<G>;
   const int lane = threadIdx.x;
@@ -544,10 +562,8 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
     if (lane < n) {
       my_e = a.eid[eb + lane];
       my_src = a.src[eb + lane];
-      float ux, uy, uz, inv;
-      unit_of(a.vec, my_e, ux, uy, uz, inv);
       float Y[V::D_SH];
-      V::sh(ux, uy, uz, Y);
+      edge_harmonics<V>(a, my_e, Y);
       F::make_A(Y, sA + lane * F::NA);
     }
     __syncthreads();
@@ -578,30 +594,40 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
   }
   if (act) {
     const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+    if constexpr (ACC) {
+#pragma unroll
+      for (int i = 0; i < F::NROW; ++i) {
+        float o[CPL];
+        bld<CPL>(mb, F::OROW[i], o);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) acc[i][c] += o[c];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < F::NROW; ++i) bst<CPL, kNT>(mb, F::OROW[i], acc[i]);
   }
 }
 
-template <class V, int G, int CPL>
+template <class V, int G, int CPL, bool ACC>
 __device__ __forceinline__ void fwd_dispatch(const ConvArgs& a, int b, int g, int sl, float* sA) {
   if constexpr (G < V::NFG) {
     if (g == G)
-      fwd_task<V, G, CPL>(a, b, sl, sA);
+      fwd_task<V, G, CPL, ACC>(a, b, sl, sA);
     else
-      fwd_dispatch<V, G + 1, CPL>(a, b, g, sl, sA);
+      fwd_dispatch<V, G + 1, CPL, ACC>(a, b, g, sl, sA);
   }
 }
 
-template <class V, int CPL>
+// ACC: m += the result (the double backward's sums) instead of m = result.
+template <class V, int CPL, bool ACC>
 __global__ __launch_bounds__(kWave, E3_FWD_MIN_WAVES) void k_conv_fwd(ConvArgs a) {
   __shared__ f4v smem[(kEdgeBatch * V::MAX_NA_F + 3) / 4];
   int b, g, sl;
   if (!task_of<V::NFG>(a, b, g, sl)) return;
-  fwd_dispatch<V, 0, CPL>(a, b, g, sl, reinterpret_cast<float*>(smem));
+  fwd_dispatch<V, 0, CPL, ACC>(a, b, g, sl, reinterpret_cast<float*>(smem));
 }
 
-template <class V, int G, int CPL>
+template <class V, int G, int CPL, bool ACC>
 __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float* sA, float* sY) {
   using B = typename V::template BG<G>;
   const int lane = threadIdx.x;
@@ -624,10 +650,8 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
       my_e = a.eid[eb + lane];
       my_src = a.src[eb + lane];
       my_slot = a.r2s[eb + lane];
-      float ux, uy, uz, inv;
-      unit_of(a.vec, my_e, ux, uy, uz, inv);
       float Y[V::D_SH];
-      V::sh(ux, uy, uz, Y);
+      edge_harmonics<V>(a, my_e, Y);
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) sY[lane * V::D_SH + i] = Y[i];
       B::make_A(Y, sA + lane * B::NA);
@@ -667,17 +691,31 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
           for (int c = 0; c < CPL; ++c) t[i][c] = 0.0f;
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
-        const RowBuf dsb = row_buf(a.ds + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
-        auto st = [&](int pl, const float (&v)[CPL]) { bst<CPL, kNT>(dsb, B::PATH[pl], v); };
+        // an absent output has row size 0: its stores are dropped by the
+        // buffer range check, with no branch in the contraction code
+        const RowBuf dsb = row_buf(a.ds + e * V::NP * C, a.ds_row, q, C);
+        auto st = [&](int pl, const float (&v)[CPL]) {
+          if constexpr (ACC) {
+            float o[CPL];
+            bld<CPL>(dsb, B::PATH[pl], o);
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) o[c] += v[c];
+            bst<CPL, kNT>(dsb, B::PATH[pl], o);
+          } else {
+            bst<CPL, kNT>(dsb, B::PATH[pl], v);
+          }
+        };
         float dyl[V::D_SH];
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0f;
         B::template edge<CPL>(sA + j * B::NA, Yv, xv, sv, dmv, t, dyl, st);
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
-        const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+        {
+          const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, a.t_row, q, C);
 #pragma unroll
-        for (int i = 0; i < B::NXR; ++i) bst<CPL>(Tb, B::XROW[i], t[i]);
+          for (int i = 0; i < B::NXR; ++i) bst<CPL>(Tb, B::XROW[i], t[i]);
+        }
       }
       const float tot = wave_reduce16(dy, lane);
       if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
@@ -704,23 +742,24 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
   }
 }
 
-template <class V, int G, int CPL>
+template <class V, int G, int CPL, bool ACC>
 __device__ __forceinline__ void bwd_dispatch(const ConvArgs& a, int b, int g, int sl, float* sA, float* sY) {
   if constexpr (G < V::NBG) {
     if (g == G)
-      bwd_task<V, G, CPL>(a, b, sl, sA, sY);
+      bwd_task<V, G, CPL, ACC>(a, b, sl, sA, sY);
     else
-      bwd_dispatch<V, G + 1, CPL>(a, b, g, sl, sA, sY);
+      bwd_dispatch<V, G + 1, CPL, ACC>(a, b, g, sl, sA, sY);
   }
 }
 
-template <class V, int CPL>
+// ACC: ds += the result (the double backward's sums) instead of ds = result.
+template <class V, int CPL, bool ACC>
 __global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd_edges(ConvArgs a) {
   __shared__ f4v smem[(kEdgeBatch * (V::MAX_NA_B + V::D_SH) + 3) / 4];
   int b, g, sl;
   if (!task_of<V::NBG>(a, b, g, sl)) return;
   float* sA = reinterpret_cast<float*>(smem);
-  bwd_dispatch<V, 0, CPL>(a, b, g, sl, sA, sA + kEdgeBatch * V::MAX_NA_B);
+  bwd_dispatch<V, 0, CPL, ACC>(a, b, g, sl, sA, sA + kEdgeBatch * V::MAX_NA_B);
 }
 
 // dx[a] = sum of the partials of a's out-edges, in sender-CSR order.  A
@@ -731,7 +770,7 @@ constexpr int kDxVec = 8;
 
 __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__ T, float* __restrict__ dx,
                                                        const int* __restrict__ rowptr_s, int n_nodes, int chunk,
-                                                       int flat4, int nslab) {
+                                                       int flat4, int nslab, int accum) {
   const int bid = blockIdx.x;
   const int slot = bid / kXcd, sl = slot % nslab, rl = slot / nslab;
   const int node = (bid % kXcd) * chunk + rl;
@@ -744,6 +783,8 @@ __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__
 #pragma unroll
   for (int k = 0; k < kDxVec; ++k) acc[k] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
   const int64_t slot_bytes = (int64_t)flat4 * 16;
+  __amdgpu_buffer_rsrc_t o = __builtin_amdgcn_make_buffer_rsrc(dx + (int64_t)node * flat4 * 4, (short)0,
+                                                               (int)slot_bytes, 0x00020000);
 #pragma unroll 2
   for (int t = s0; t < s1; ++t) {
     // out-of-range float4s (past D_in x C) read as zero
@@ -753,8 +794,11 @@ __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__
     for (int k = 0; k < kDxVec; ++k)
       acc[k] += __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(r, off, k * kWave * 16, kNT));
   }
-  __amdgpu_buffer_rsrc_t o = __builtin_amdgcn_make_buffer_rsrc(dx + (int64_t)node * flat4 * 4, (short)0,
-                                                               (int)slot_bytes, 0x00020000);
+  if (accum) {  // old + this sum, so that accumulating equals adding a separate result
+#pragma unroll
+    for (int k = 0; k < kDxVec; ++k)
+      acc[k] += __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(o, off, k * kWave * 16, 0));
+  }
 #pragma unroll
   for (int k = 0; k < kDxVec; ++k)
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, acc[k]), o, off, k * kWave * 16, kNT);
@@ -783,13 +827,31 @@ __global__ __launch_bounds__(256) void k_conv_bwd_dvec(const float* __restrict__
 }
 
 // Padding edges: zero ds rows and dvec (one block per padding edge).
+// Zero the rows of padding edges in up to two per-edge arrays (null: skipped).
 __global__ __launch_bounds__(256) void k_zero_pad(const int* __restrict__ pad_eid, int64_t n_pad,
-                                                  float* __restrict__ ds, float* __restrict__ dvec, int64_t row) {
+                                                  float* __restrict__ p0, int64_t w0, float* __restrict__ p1,
+                                                  int64_t w1) {
   const int64_t i = blockIdx.x;
   if (i >= n_pad) return;
   const int64_t e = pad_eid[i];
-  for (int64_t k = threadIdx.x; k < row; k += blockDim.x) ds[e * row + k] = 0.0f;
-  if (threadIdx.x < 3) dvec[3 * e + threadIdx.x] = 0.0f;
+  if (p0)
+    for (int64_t k = threadIdx.x; k < w0; k += blockDim.x) p0[e * w0 + k] = 0.0f;
+  if (p1)
+    for (int64_t k = threadIdx.x; k < w1; k += blockDim.x) p1[e * w1 + k] = 0.0f;
+}
+
+// dy of each live edge: the sum of its per-(group, slab) partials, in order.
+template <class V>
+__global__ __launch_bounds__(256) void k_conv_bwd_dy(const float* __restrict__ DY, const int* __restrict__ eid,
+                                                     float* __restrict__ dy, int64_t n_live, int nslab, int accum) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = i / V::D_SH;
+  const int c = (int)(i % V::D_SH);
+  if (r >= n_live) return;
+  float v = 0.0f;
+  for (int g = 0; g < V::NBG * nslab; ++g) v += DY[(r * V::NBG * nslab + g) * 16 + c];
+  const int64_t o = (int64_t)eid[r] * V::D_SH + c;
+  dy[o] = accum ? dy[o] + v : v;
 }
 
 
@@ -1321,60 +1383,92 @@ ConvArgs base_args(const e3_plan* p, const e3_graph* g) {
   return a;
 }
 
+// One forward convolution.  y: caller's harmonics or null (from vec);
+// accum: m += instead of m =.
 template <class V, int CPL>
-e3_status run_fwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s, float* m,
-                  hipStream_t st) {
+e3_status run_fwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* y,
+                  const float* s, float* m, int accum, hipStream_t st) {
   ConvArgs a = base_args(p, g);
-  a.x = x, a.vec = vec, a.s = s, a.m = m;
+  a.x = x, a.vec = vec, a.y = y, a.s = s, a.m = m, a.accum = accum;
   a.nslab = p->nslab_f;
   if (g->n_nodes == 0) return E3_OK;
   const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
   {
     TimedLaunch t_("conv_fwd", st);
-    hipLaunchKernelGGL((k_conv_fwd<V, CPL>), dim3(grid), dim3(kWave), 0, st, a);
+    if (accum)
+      hipLaunchKernelGGL((k_conv_fwd<V, CPL, true>), dim3(grid), dim3(kWave), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_conv_fwd<V, CPL, false>), dim3(grid), dim3(kWave), 0, st, a);
   }
   E3_HIP(hipGetLastError());
   return E3_OK;
 }
 
+// One backward convolution.  Harmonics from y when given (then dy is the
+// harmonic cotangent output), else from vec (then dvec = J^T dy).  Any of
+// dx, dvec/dy, ds may be null: that cotangent is not stored.  accum is a mask
+// of kAccDx / kAccDy / kAccDs: those cotangents are added to the outputs'
+// contents instead of overwriting them.
+constexpr int kAccDx = 1, kAccDy = 2, kAccDs = 4;
+
 template <class V, int CPLX>
-e3_status run_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
-                  const float* dm, float* dx, float* dvec, float* ds, void* ws, hipStream_t st) {
+e3_status run_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* y,
+                  const float* s, const float* dm, float* dx, float* dvec, float* dy, float* ds, int accum, void* ws,
+                  hipStream_t st) {
   if (g->n_nodes == 0) return E3_OK;
   Ws w = bwd_ws<V>(p, g);
   ConvArgs a = base_args(p, g);
-  a.x = x, a.vec = vec, a.s = s, a.dm = dm, a.ds = ds;
+  a.x = x, a.vec = vec, a.y = y, a.s = s, a.dm = dm, a.accum = (accum & kAccDs) != 0;
   a.T = reinterpret_cast<float*>(ws);
-  a.DY = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.t_bytes);
+  a.DY = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.t_bytes);  // always written
+  a.ds = ds ? ds : a.DY;
+  a.ds_row = ds ? (int64_t)V::NP * a.C * 4 : 0;
+  a.t_row = dx ? (int64_t)V::D_IN * a.C * 4 : 0;
   a.nslab = p->nslab_b;
   if (g->n_live > 0) {
     const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
     TimedLaunch t_("conv_bwd_edges", st);
-    if (p->cpl_b == 1)
-      hipLaunchKernelGGL((k_conv_bwd_edges<V, 1>), dim3(grid), dim3(kWave), 0, st, a);
-    else
-      hipLaunchKernelGGL((k_conv_bwd_edges<V, E3_BWD_CPL>), dim3(grid), dim3(kWave), 0, st, a);
+    if (p->cpl_b == 1) {
+      if (a.accum)
+        hipLaunchKernelGGL((k_conv_bwd_edges<V, 1, true>), dim3(grid), dim3(kWave), 0, st, a);
+      else
+        hipLaunchKernelGGL((k_conv_bwd_edges<V, 1, false>), dim3(grid), dim3(kWave), 0, st, a);
+    } else {
+      if (a.accum)
+        hipLaunchKernelGGL((k_conv_bwd_edges<V, E3_BWD_CPL, true>), dim3(grid), dim3(kWave), 0, st, a);
+      else
+        hipLaunchKernelGGL((k_conv_bwd_edges<V, E3_BWD_CPL, false>), dim3(grid), dim3(kWave), 0, st, a);
+    }
     E3_HIP(hipGetLastError());
   }
-  {
+  if (dx) {
     TimedLaunch t_("conv_bwd_dx", st);
     const int flat4 = V::D_IN * a.C / 4;
     const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
     hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * a.chunk * nsl)), dim3(kWave), 0, st, a.T, dx,
-                       g->rowptr_s, a.n_nodes, a.chunk, flat4, nsl);
+                       g->rowptr_s, a.n_nodes, a.chunk, flat4, nsl, (accum & kAccDx) != 0);
+    E3_HIP(hipGetLastError());
   }
-  E3_HIP(hipGetLastError());
-  if (g->n_live > 0) {
+  if (g->n_live > 0 && dvec) {
     TimedLaunch t_("conv_bwd_dvec", st);
     hipLaunchKernelGGL((k_conv_bwd_dvec<V>), dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, vec, a.DY, g->eid_r,
                        dvec, g->n_live, p->nslab_b);
     E3_HIP(hipGetLastError());
   }
-  if (g->n_pad > 0) {
-    const int64_t row = (int64_t)V::NP * a.C;
+  if (g->n_live > 0 && dy) {
+    TimedLaunch t_("conv_bwd_dy", st);
+    hipLaunchKernelGGL((k_conv_bwd_dy<V>), dim3(blocks_for(g->n_live * V::D_SH, 256)), dim3(256), 0, st, a.DY,
+                       g->eid_r, dy, g->n_live, p->nslab_b, (accum & kAccDy) != 0);
+    E3_HIP(hipGetLastError());
+  }
+  // padding edges: zero cotangents (left unchanged when accumulating)
+  float* z0 = (accum & kAccDs) ? nullptr : ds;
+  float* z1 = dvec ? dvec : ((accum & kAccDy) ? nullptr : dy);
+  const int64_t w1 = dvec ? 3 : V::D_SH;
+  if (g->n_pad > 0 && (z0 || z1)) {
     TimedLaunch t_("conv_bwd_pad", st);
-    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, ds,
-                       dvec, row);
+    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, z0,
+                       (int64_t)V::NP * a.C, z1, w1);
     E3_HIP(hipGetLastError());
   }
   return E3_OK;
@@ -1491,7 +1585,7 @@ e3_status run_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const
     const int flat4 = V::D_IN * a.C / 4;
     const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
     hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * a.chunk * nsl)), dim3(kWave), 0, st, a.T, dx,
-                       g->rowptr_s, a.n_nodes, a.chunk, flat4, nsl);
+                       g->rowptr_s, a.n_nodes, a.chunk, flat4, nsl, 0);
     E3_HIP(hipGetLastError());
   }
   if (g->n_live > 0) {
@@ -1505,7 +1599,7 @@ e3_status run_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const
       // the ds rows of padding edges enter the gradient sums: clear them
       TimedLaunch t_("rad_pad_ds", st);
       hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad,
-                         a.ds, dvec, (int64_t)w.pc4 * 4);
+                         a.ds, (int64_t)w.pc4 * 4, dvec, (int64_t)3);
       E3_HIP(hipGetLastError());
     }
     const int64_t E = g->n_edges;
@@ -1536,7 +1630,7 @@ e3_status run_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const
   if (g->n_pad > 0) {
     TimedLaunch t_("conv_bwd_pad", st);
     hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, dh,
-                       dvec, (int64_t)K);
+                       (int64_t)K, dvec, (int64_t)3);
     E3_HIP(hipGetLastError());
   }
   return E3_OK;
@@ -1550,10 +1644,10 @@ size_t tp_ws(const e3_plan* p, int64_t rows) {
 struct VariantOps {
   const char* sig;
   int d_in, d_sh, d_out, np, lsh, nbg;
-  e3_status (*fwd[2])(const e3_plan*, const e3_graph*, const float*, const float*, const float*, float*,
-                      hipStream_t);
+  e3_status (*fwd[2])(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*,
+                      float*, int, hipStream_t);
   e3_status (*bwd[2])(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*,
-                      float*, float*, float*, void*, hipStream_t);
+                      const float*, float*, float*, float*, float*, int, void*, hipStream_t);
   e3_status (*tp[2])(const e3_plan*, const float*, const float*, const float*, float*, int64_t, hipStream_t);
   Ws (*ws)(const e3_plan*, const e3_graph*);
   e3_status (*tpb)(const e3_plan*, const float*, const float*, const float*, const float*, float*, float*, float*,
@@ -1978,7 +2072,7 @@ e3_status e3_conv_fwd(const e3_plan* p, const e3_graph* g, const float* x, const
   if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x))) return E3_ERR_INVALID_ARG;
   if (g->n_live > 0 && (!vec || !s || !aligned16(s))) return E3_ERR_INVALID_ARG;
   const VariantOps& v = kVariants[p->variant];
-  return v.fwd[cpl_index(cpl_of(p))](p, g, x, vec, s, m, reinterpret_cast<hipStream_t>(stream));
+  return v.fwd[cpl_index(cpl_of(p))](p, g, x, vec, nullptr, s, m, 0, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
@@ -1994,7 +2088,8 @@ e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const
   Ws w = v.ws(p, g);
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
-  return v.bwd[cpl_index(cpl_of(p))](p, g, x, vec, s, dm, dx, dvec, ds, ws, reinterpret_cast<hipStream_t>(stream));
+  return v.bwd[cpl_index(cpl_of(p))](p, g, x, vec, nullptr, s, dm, dx, dvec, nullptr, ds, 0, ws,
+                                     reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_radial_workspace_size(const e3_plan* p, const e3_graph* g, int K, size_t* bwd_bytes) {
@@ -2029,6 +2124,66 @@ e3_status e3_conv_bwd_radial(const e3_plan* p, const e3_graph* g, const float* x
   if (w.total() > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.total()) return E3_ERR_WORKSPACE_TOO_SMALL;
   return v.rbwd(p, g, x, vec, h, W, K, dm, dx, dvec, dh, dW, ws, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_conv_fwd_y(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
+                        float* m, int accumulate, e3_stream stream) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x))) return E3_ERR_INVALID_ARG;
+  if (g->n_live > 0 && (!y || !s || !aligned16(s))) return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  return v.fwd[cpl_index(cpl_of(p))](p, g, x, nullptr, y, s, m, accumulate != 0,
+                                     reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_conv_bwd_y(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
+                        const float* dm, float* dx, float* dy, float* ds, int accumulate, void* ws, size_t ws_bytes,
+                        e3_stream stream) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!x || !dm || !aligned16(x) || !aligned16(dm) || (dx && !aligned16(dx))))
+    return E3_ERR_INVALID_ARG;
+  if (g->n_edges > 0 && (!y || !s || !aligned16(s) || (ds && !aligned16(ds)))) return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  Ws w = v.ws(p, g);
+  if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
+  if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
+  return v.bwd[cpl_index(cpl_of(p))](p, g, x, nullptr, y, s, dm, dx, nullptr, dy, ds,
+                                     accumulate ? (kAccDx | kAccDy | kAccDs) : 0, ws,
+                                     reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_conv_bwd2(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
+                       const float* dm, const float* ddx, const float* ddy, const float* dds, float* gx, float* gy,
+                       float* gs, float* gdm, void* ws, size_t ws_bytes, e3_stream stream) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!x || !dm || !ddx || !gx || !gdm || !aligned16(x) || !aligned16(dm) || !aligned16(ddx) ||
+                         !aligned16(gx) || !aligned16(gdm)))
+    return E3_ERR_INVALID_ARG;
+  if (g->n_edges > 0 && (!y || !s || !ddy || !dds || !gy || !gs || !aligned16(s) || !aligned16(dds) ||
+                         !aligned16(gs)))
+    return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  Ws w = v.ws(p, g);
+  if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
+  if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
+  const int ci = cpl_index(cpl_of(p));
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  // ddm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds)
+  if ((st = v.fwd[ci](p, g, ddx, nullptr, y, s, gdm, 0, hs)) != E3_OK) return st;
+  if ((st = v.fwd[ci](p, g, x, nullptr, ddy, s, gdm, 1, hs)) != E3_OK) return st;
+  if ((st = v.fwd[ci](p, g, x, nullptr, y, dds, gdm, 1, hs)) != E3_OK) return st;
+  // (-, d_x y, d_x s) = conv_bwd(ddx, y, s, dm)
+  if ((st = v.bwd[ci](p, g, ddx, nullptr, y, s, dm, nullptr, nullptr, gy, gs, 0, ws, hs)) != E3_OK) return st;
+  // (d_y x, -, d_y s) = conv_bwd(x, ddy, s, dm)
+  if ((st = v.bwd[ci](p, g, x, nullptr, ddy, s, dm, gx, nullptr, nullptr, gs, kAccDs, ws, hs)) != E3_OK) return st;
+  // (d_s x, d_s y, -) = conv_bwd(x, y, dds, dm)
+  return v.bwd[ci](p, g, x, nullptr, y, dds, dm, gx, nullptr, gy, nullptr, kAccDx | kAccDy, ws, hs);
 }
 
 }  // extern "C"

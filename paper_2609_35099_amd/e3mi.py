@@ -58,6 +58,9 @@ SIGNATURES = {
     "e3_tp_workspace_size": (_I, [_P, _I64, ct.POINTER(ct.c_size_t)]),
     "e3_tp_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, _P]),
     "e3_conv_workspace_size": (_I, [_P, _P, ct.POINTER(ct.c_size_t), ct.POINTER(ct.c_size_t)]),
+    "e3_conv_fwd_y": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P]),
+    "e3_conv_bwd_y": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_int, _P, ct.c_size_t, _P]),
+    "e3_conv_bwd2": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_radial_workspace_size": (_I, [_P, _P, ct.c_int, ct.POINTER(ct.c_size_t)]),
     "e3_conv_fwd_radial": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P, _P]),
     "e3_conv_bwd_radial": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
@@ -312,6 +315,61 @@ def conv_bwd(plan: Plan, graph: Graph, x, vec, s, dm, dx=None, dvec=None, ds=Non
                              _ptr(dvec, "dvec", (E, 3)), _ptr(ds, "ds", (E, plan.P, plan.C)),
                              ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd")
     return dx, dvec, ds
+
+
+def _optr(t, name, shape):
+    return None if t is None else _ptr(t, name, shape)
+
+
+def conv_fwd_y(plan: Plan, graph: Graph, x, y, s, out=None, accumulate=False, stream=None):
+    """m = conv(x, y, s) with the harmonics y [E, D_sh] given (m += ... when accumulate)."""
+    N, E = graph.n_nodes, graph.n_edges
+    out = _empty((N, plan.D_out, plan.C)) if out is None else out
+    _check(lib().e3_conv_fwd_y(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                               _ptr(y, "y", (E, plan.D_sh)), _ptr(s, "s", (E, plan.P, plan.C)),
+                               _ptr(out, "m", (N, plan.D_out, plan.C)), 1 if accumulate else 0, _stream(stream)),
+           "e3_conv_fwd_y")
+    return out
+
+
+def conv_bwd_y(plan: Plan, graph: Graph, x, y, s, dm, dx=None, dy=None, ds=None, want=("dx", "dy", "ds"),
+               accumulate=False, ws=None, stream=None):
+    """(dx, dy, ds) of eq. (conv-bwd) with y given; cotangents not in `want` are neither
+    computed into memory nor returned (None)."""
+    N, E = graph.n_nodes, graph.n_edges
+    if "dx" in want and dx is None:
+        dx = _empty((N, plan.D_in, plan.C))
+    if "dy" in want and dy is None:
+        dy = _empty((E, plan.D_sh))
+    if "ds" in want and ds is None:
+        ds = _empty((E, plan.P, plan.C))
+    if ws is None:
+        ws = workspace(conv_workspace_size(plan, graph)[1])
+    _check(lib().e3_conv_bwd_y(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                               _ptr(y, "y", (E, plan.D_sh)), _ptr(s, "s", (E, plan.P, plan.C)),
+                               _ptr(dm, "dm", (N, plan.D_out, plan.C)), _optr(dx, "dx", (N, plan.D_in, plan.C)),
+                               _optr(dy, "dy", (E, plan.D_sh)), _optr(ds, "ds", (E, plan.P, plan.C)),
+                               1 if accumulate else 0, ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)),
+           "e3_conv_bwd_y")
+    return dx, dy, ds
+
+
+def conv_bwd2(plan: Plan, graph: Graph, x, y, s, dm, ddx, ddy, dds, ws=None, stream=None):
+    """Double backward: (gx, gy, gs, gdm), the variations of (x, y, s, dm) for
+    variations (ddx, ddy, dds) of the backward's outputs."""
+    N, E = graph.n_nodes, graph.n_edges
+    gx, gdm = _empty((N, plan.D_in, plan.C)), _empty((N, plan.D_out, plan.C))
+    gy, gs = _empty((E, plan.D_sh)), _empty((E, plan.P, plan.C))
+    if ws is None:
+        ws = workspace(conv_workspace_size(plan, graph)[1])
+    _check(lib().e3_conv_bwd2(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                              _ptr(y, "y", (E, plan.D_sh)), _ptr(s, "s", (E, plan.P, plan.C)),
+                              _ptr(dm, "dm", (N, plan.D_out, plan.C)), _ptr(ddx, "ddx", (N, plan.D_in, plan.C)),
+                              _ptr(ddy, "ddy", (E, plan.D_sh)), _ptr(dds, "dds", (E, plan.P, plan.C)),
+                              _ptr(gx, "gx", (N, plan.D_in, plan.C)), _ptr(gy, "gy", (E, plan.D_sh)),
+                              _ptr(gs, "gs", (E, plan.P, plan.C)), _ptr(gdm, "gdm", (N, plan.D_out, plan.C)),
+                              ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd2")
+    return gx, gy, gs, gdm
 
 
 def conv_radial_workspace_size(plan: Plan, graph: Graph, K: int) -> int:

@@ -523,3 +523,130 @@ def test_conv_radial_config4_sampled(e3):
     print("rel-L2", errs, flush=True)
     for k, v in errs.items():
         assert v < TOL, (k, v)
+
+
+# ---------------------------------------------------------------- harmonics as input; double backward
+@pytest.mark.parametrize("irreps,lsh,lout,n,e,pad", [
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, 80, 1500, -1),
+    ("64x0e+64x1o+64x2e", 3, 3, 50, 800, 4),
+    ("8x0e+8x1o", 2, 2, 20, 150, -1),
+])
+def test_conv_y_input_accumulate_and_optional_outputs(e3, irreps, lsh, lout, n, e, pad):
+    """conv and conv_bwd with an arbitrary y (not harmonics) against the oracle;
+    accumulate adds; an omitted cotangent leaves the others unchanged."""
+    import torch
+    _say("conv y-input", irreps, n, e, pad)
+    rng = np.random.default_rng(14)
+    lay = oirreps.layout(irreps, lsh, lout)
+    snd, rcv, _ = _random_graph(rng, n, e)
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    y = rng.standard_normal((e, lay.d_sh)).astype(np.float32)
+    s = rng.standard_normal((e, lay.n_paths, C)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    plan = e3.Plan(irreps, lsh, lout)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    xs, ys, ss, dms = (to_dev(a) for a in (x, y, s, dm))
+    m = e3.conv_fwd_y(plan, G, xs, ys, ss)
+    dx, dy, ds = e3.conv_bwd_y(plan, G, xs, ys, ss, dms)
+    ref_m = oconv.conv_fwd_from_y(lay, x, y, s, snd, rcv, n, pad_node=pad).numpy()
+    ref = oconv.conv_bwd_from_y(lay, x, y, s, dm, snd, rcv, n, pad_node=pad)
+    errs = dict(m=rel_l2(to_np(m), ref_m), dx=rel_l2(to_np(dx), ref["dx"].numpy()),
+                dy=rel_l2(to_np(dy), ref["dy"].numpy()), ds=rel_l2(to_np(ds), ref["ds"].numpy()))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    # accumulate: a second call adds the same values (x + x is exact in binary)
+    m2 = m.clone()
+    e3.conv_fwd_y(plan, G, xs, ys, ss, out=m2, accumulate=True)
+    d2 = [t.clone() for t in (dx, dy, ds)]
+    e3.conv_bwd_y(plan, G, xs, ys, ss, dms, dx=d2[0], dy=d2[1], ds=d2[2], accumulate=True)
+    assert torch.equal(m2, 2 * m)
+    for a, b in zip(d2, (dx, dy, ds)):
+        assert torch.equal(a, 2 * b)
+    # omitted cotangents: the stored ones are bit-identical
+    for want in (("dx",), ("dy",), ("ds",), ("dy", "ds")):
+        got = e3.conv_bwd_y(plan, G, xs, ys, ss, dms, want=want)
+        for name, full, part in zip(("dx", "dy", "ds"), (dx, dy, ds), got):
+            if name in want:
+                assert torch.equal(full, part), (want, name)
+            else:
+                assert part is None
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,n,e,pad", [
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, 60, 1000, -1),
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, 40, 700, 6),
+    ("16x0e+16x1o+16x2e", 3, 3, 30, 400, -1),
+    ("8x0e+8x1o", 2, 2, 20, 150, 2),
+])
+def test_conv_bwd2_random_graphs_full(e3, irreps, lsh, lout, n, e, pad):
+    import torch
+    _say("conv bwd2", irreps, n, e, pad)
+    rng = np.random.default_rng(15)
+    lay = oirreps.layout(irreps, lsh, lout)
+    snd, rcv, _ = _random_graph(rng, n, e)
+    C = lay.channels
+    arrs = dict(x=(n, lay.d_in, C), y=(e, lay.d_sh), s=(e, lay.n_paths, C), dm=(n, lay.d_out, C),
+                ddx=(n, lay.d_in, C), ddy=(e, lay.d_sh), dds=(e, lay.n_paths, C))
+    a = {k: rng.standard_normal(v).astype(np.float32) for k, v in arrs.items()}
+    plan = e3.Plan(irreps, lsh, lout)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    d = {k: to_dev(v) for k, v in a.items()}
+    outs = [e3.conv_bwd2(plan, G, d["x"], d["y"], d["s"], d["dm"], d["ddx"], d["ddy"], d["dds"]) for _ in range(2)]
+    for u, v in zip(*outs):
+        assert torch.equal(u, v)
+    ref = oconv.conv_bwd2(lay, a["x"], a["y"], a["s"], a["dm"], a["ddx"], a["ddy"], a["dds"], snd, rcv, n,
+                          pad_node=pad)
+    errs = {k: rel_l2(to_np(g), ref[k].numpy()) for k, g in zip(("dx", "dy", "ds", "ddm"), outs[0])}
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    if pad >= 0:
+        dead = (snd == pad) | (rcv == pad)
+        assert np.all(to_np(outs[0][1])[dead] == 0) and np.all(to_np(outs[0][2])[dead] == 0)
+
+
+def test_conv_bwd2_config4_sampled(e3):
+    """Double backward on config 4 (24,000-atom water box, y its harmonics) at full
+    size; checked on a compact sub-problem holding every in-edge of the sampled
+    receivers, every out-edge of the sampled senders and the sampled edges."""
+    import torch
+    _say("conv bwd2 config 4 full")
+    cfg = synth.CONFIGS[4]
+    g = synth.graph(cfg)
+    N, E = g.n_nodes, g.sender.shape[0]
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    lay = layout_of(cfg)
+    dev = torch.device("cuda")
+    x = synth.node_features(cfg, N)
+    dm = synth.out_cotangent(cfg, N)
+    rng = np.random.default_rng(16)
+    ddx = rng.standard_normal(x.shape).astype(np.float32)
+    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), N)
+    vs = to_dev(g.vec)
+    ys = e3.sh(cfg.lmax_sh, vs)
+    ddy = torch.randn((E, plan.D_sh), device=dev, generator=torch.Generator(device=dev).manual_seed(17))
+    s = upload_weights(cfg, g.vec)
+    dds = synth.normal_device(cfg.cid, 9, (E, plan.P, plan.C), dev)
+    xs, dms, ddxs = to_dev(x), to_dev(dm), to_dev(ddx)
+    gx, gy, gs, gdm = e3.conv_bwd2(plan, G, xs, ys, s, dms, ddxs, ddy, dds)
+    torch.cuda.synchronize()
+    rs = np.concatenate([[0, N - 1], rng.choice(N, 10, replace=False)])
+    es = np.concatenate([[0, E - 1], rng.choice(E, 30, replace=False)])
+    sel = np.unique(np.concatenate([np.nonzero(np.isin(g.receiver, rs))[0],
+                                    np.nonzero(np.isin(g.sender, rs))[0], es]))
+    nodes, inv = np.unique(np.concatenate([g.sender[sel], g.receiver[sel]]), return_inverse=True)
+    sc, rc = inv[:sel.shape[0]], inv[sel.shape[0]:]
+    ed = torch.as_tensor(sel, device=dev)
+    take = lambda t: t[ed].cpu().numpy()
+    ref = oconv.conv_bwd2(lay, x[nodes], take(ys), take(s), dm[nodes], ddx[nodes], take(ddy), take(dds),
+                          sc, rc, nodes.shape[0])
+    ni = np.searchsorted(nodes, rs)
+    ep = np.searchsorted(sel, es)
+    ri, ei = torch.as_tensor(rs, device=dev), torch.as_tensor(es, device=dev)
+    errs = dict(dx=rel_l2(to_np(gx[ri]), ref["dx"].numpy()[ni]), ddm=rel_l2(to_np(gdm[ri]), ref["ddm"].numpy()[ni]),
+                dy=rel_l2(to_np(gy[ei]), ref["dy"].numpy()[ep]), ds=rel_l2(to_np(gs[ei]), ref["ds"].numpy()[ep]))
+    print("rel-L2", errs, f"(sub-problem: {sel.shape[0]} edges, {nodes.shape[0]} nodes)", flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
