@@ -389,3 +389,65 @@ def test_conv_bwd2_against_autograd_and_central_differences(spec, pad):
     if pad >= 0:
         dead = (snd == pad) | (rcv == pad)
         assert torch.all(got["dy"][dead] == 0) and torch.all(got["ds"][dead] == 0)
+
+
+# ---------------------------------------------------------------- linear mixing
+def test_linear_identity_permutation_and_zero_blocks():
+    """W_o = identity copies the (single) input block; a permutation matrix
+    permutes channels; an output type with no input is zero; two input blocks
+    of one type add."""
+    from oracle import linear
+    rng = np.random.default_rng(41)
+    ins, outs = "3x0e+3x1o+3x1o+3x2e", "3x0e+3x1o+3x1e+3x2e"
+    jobs, d_in, d_out, c_in, c_out, nw = linear.plan(ins, outs)
+    x = rng.standard_normal((5, d_in, 3))
+    W = np.zeros(nw)
+    perm = np.eye(3)[[2, 0, 1]]
+    for l, orow, src, off, n in jobs:
+        if l == 0:
+            W[off:off + n] = np.eye(3).reshape(-1)
+        if l == 1 and src:
+            W[off:off + n] = np.concatenate([perm, np.eye(3)]).reshape(-1)
+        if l == 2:
+            W[off:off + n] = perm.reshape(-1)
+    y = linear.forward(ins, outs, x, W).numpy()
+    assert np.array_equal(y[:, 0:1], x[:, 0:1])                                   # 0e copied
+    assert np.allclose(y[:, 1:4], x[:, 1:4] @ perm + x[:, 4:7], atol=1e-14)        # two 1o blocks
+    assert np.all(y[:, 4:7] == 0)                                                  # 1e: no input
+    assert np.allclose(y[:, 7:12], x[:, 7:12] @ perm, atol=1e-14)
+
+
+def test_linear_equivariance_and_backward():
+    """Rotating every block by its Wigner matrix commutes with the mixing; the
+    backward equals float64 autograd of the forward and a central difference."""
+    from oracle import linear
+    rng = np.random.default_rng(42)
+    ins, outs = "4x0e+4x1o+4x2e+4x1o+4x3o", "5x0e+5x1o+5x2e+5x3o"
+    jobs, d_in, d_out, c_in, c_out, nw = linear.plan(ins, outs)
+    x = rng.standard_normal((6, d_in, c_in))
+    W = rng.standard_normal(nw)
+    R = wigner.random_rotation(rng)
+
+    def rot(a, spec):
+        a = a.copy()
+        for (l, p, r, _) in linear.blocks(spec)[0]:
+            D = wigner.wigner_d(l, R)
+            a[:, r:r + 2 * l + 1] = np.einsum("ab,nbk->nak", D, a[:, r:r + 2 * l + 1])
+        return a
+
+    y = linear.forward(ins, outs, x, W).numpy()
+    yr = linear.forward(ins, outs, rot(x, ins), W).numpy()
+    assert np.allclose(yr, rot(y, outs), atol=1e-12)
+    dout = rng.standard_normal((6, d_out, c_out))
+    dx, dW = linear.backward(ins, outs, x, W, dout)
+    xt = torch.tensor(x, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    L = (linear.forward(ins, outs, xt, Wt) * torch.as_tensor(dout)).sum()
+    gx, gW = torch.autograd.grad(L, [xt, Wt])
+    assert torch.allclose(dx, gx, atol=1e-12) and torch.allclose(dW, gW, atol=1e-12)
+    u, v = rng.standard_normal(x.shape), rng.standard_normal(W.shape)
+    f = lambda t: float((linear.forward(ins, outs, x + t * u, W + t * v) * torch.as_tensor(dout)).sum())
+    h = 1e-3
+    fd = (f(h) - f(-h)) / (2 * h)     # the loss is quadratic in t: exact up to rounding
+    an = float((dx * torch.as_tensor(u)).sum() + (dW * torch.as_tensor(v)).sum())
+    assert abs(fd - an) < 1e-8 * max(1.0, abs(an))
