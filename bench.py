@@ -150,7 +150,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tp", action="store_true")
-    ap.add_argument("--only", choices=["all", "conv", "radial", "bwd2", "tp"], default="all")
+    ap.add_argument("--only", choices=["all", "conv", "radial", "bwd2", "linear", "tp"], default="all")
     ap.add_argument("--order", choices=["generated", "cell"], default="generated",
                     help="atom order of the water box: as generated (spatially random) or cell-sorted")
     ap.add_argument("--copy-probe", action="store_true",
@@ -336,6 +336,50 @@ def main():
                                    for k, (t, c) in per.items()}}
         log(f"bwd2: {b2_ms:.3f} ms, {out['bwd2']['alg_GBps']} GB/s; kernels {out['bwd2']['kernels']}")
         del outs, ws2, s2, dds, ddx, ddy, ys
+        torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- linear mixing
+    if args.only in ("all", "linear"):
+        names = [f"{C}x{l3}{'e' if p3 > 0 else 'o'}" for (_, _, l3, p3, _, _, _) in plan.paths()]
+        lin_in = "+".join(names)
+        lin_out = "+".join(f"{C}x{l}{p}" for l in range(4) for p in "eo")
+        L = e3mi.Linear(lin_in, lin_out)
+        lx = synth.normal_device(4, 20, (N, L.D_in, L.C_in), dev)
+        lW = synth.normal_device(4, 21, (L.n_weights,), dev) / 16
+        ld = synth.normal_device(4, 22, (N, L.D_out, L.C_out), dev)
+        ly = torch.empty((N, L.D_out, L.C_out), dtype=torch.float32, device=dev)
+        ldx = torch.empty_like(lx)
+        ldW = torch.empty_like(lW)
+        lws = e3mi.workspace(L.workspace_size())
+        for _ in range(args.warmup):
+            L.forward(lx, lW, out=ly)
+            L.backward(lx, lW, ld, dx=ldx, dW=ldW, ws=lws)
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        for _ in range(args.steps):
+            L.forward(lx, lW, out=ly)
+            L.backward(lx, lW, ld, dx=ldx, dW=ldW, ws=lws)
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        per = e3mi.timing_read()
+        # multiply-adds: every input row meets C_in x C_out weights (forward, dx and dW alike)
+        flops = 2.0 * N * L.D_in * L.C_in * L.C_out
+        lk = {}
+        for name in ("linear_fwd", "linear_bwd_dx", "linear_bwd_dw", "linear_bwd_dw_sum"):
+            if name in per:
+                ms = per[name][0] / per[name][1]
+                lk[name] = {"ms": round(ms, 4)}
+                if name != "linear_bwd_dw_sum":
+                    lk[name]["TFLOPs"] = round(flops / (ms * 1e-3) / 1e12, 2)
+                    lk[name]["frac_fp32_mfma"] = round(flops / (ms * 1e-3) / 1e12 / 157.3, 4)
+        out["linear"] = {"workload": f"equivariant mixing of the convolution output, {N} nodes: 34 path blocks "
+                                     f"(D {L.D_in}) -> 8 irreps (D {L.D_out}), {C} -> {C} channels, fp32 MFMA",
+                         "gflop_per_pass": round(flops / 1e9, 2),
+                         "bound": "mfma", "peak_TFLOPs": 157.3, "kernels": lk}
+        log(f"linear: {lk}")
+        L.close()
+        del lx, lW, ld, ly, ldx, ldW, lws
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- tp

@@ -221,6 +221,30 @@ e3_status e3_conv_bwd_radial(const e3_plan* plan, const e3_graph* graph, const f
                              const float* h, const float* W, int K, const float* dm, float* dx, float* dvec,
                              float* dh, float* dW, void* ws, size_t ws_bytes, e3_stream stream);
 
+/* Equivariant linear mixing (App. A.3, linear mixing between features of the
+ * same degree, with the weight shared over the 2l+1 components so that it
+ * commutes with rotations).  An output block of type (l, p) receives every
+ * input block of the same (l, p), in input order, multiplicities concatenated:
+ *   out[n, o + m, j] = sum_t sum_k x[n, in_t + m, k] W_o[t * C_in + k, j].
+ * An output type with no input is zero.  W is the concatenation over output
+ * blocks, in order, of W_o [n_in(o) * C_in, C_out] row-major; e3_linear_query
+ * gives its length.  irreps_in / irreps_out: irreps strings with one
+ * multiplicity each (C_in, C_out multiples of 16; at most 64 blocks a side).
+ * Layouts: x [n, D_in, C_in], out [n, D_out, C_out], both 16-byte aligned.
+ * fp32 on the matrix cores.  The descriptor uploads its small block tables
+ * to the current device on first use.
+ * e3_linear_bwd: dx [n, D_in, C_in] and dW (same layout as W) from dout; dW is
+ *   a fixed-order sum of fixed row-chunk partials kept in ws (at least
+ *   e3_linear_workspace_size bytes), so it is deterministic. */
+typedef struct e3_linear e3_linear;
+e3_status e3_linear_create(const char* irreps_in, const char* irreps_out, e3_linear** out);
+e3_status e3_linear_query(const e3_linear* lin, int64_t* n_weights, int* d_in, int* d_out, int* c_in, int* c_out);
+e3_status e3_linear_destroy(e3_linear* lin);
+e3_status e3_linear_fwd(e3_linear* lin, const float* x, const float* W, float* out, int64_t n, e3_stream stream);
+e3_status e3_linear_workspace_size(const e3_linear* lin, size_t* bwd_bytes);
+e3_status e3_linear_bwd(e3_linear* lin, const float* x, const float* W, const float* dout, float* dx, float* dW,
+                        void* ws, size_t ws_bytes, int64_t n, e3_stream stream);
+
 /* Per-kernel timing (instrumentation).  While enabled, every kernel the
  * library launches is bracketed by two HIP events on the caller's stream.
  * e3_timing_read waits for the recorded events and returns, per kernel name

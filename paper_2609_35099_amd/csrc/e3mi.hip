@@ -1283,6 +1283,205 @@ __global__ __launch_bounds__(256) void k_rad_dh_sum(const float* __restrict__ DH
   if (j < K) dh[r * K + j] = s;
 }
 
+
+// ------------------------------------------------------------ linear mixing
+// Dense per-irrep channel mixing on the matrix cores (v_mfma_f32_16x16x4f32,
+// fp32 in and out).  A destination block of 2l+1 rows per node receives, for
+// each of its sources, src[n, src_row + m, k] B[k, col] summed over k and the
+// sources, B[k, col] = W[w_off + k ldk + col ldc].  The forward has one job per
+// output block (its sources: the input blocks of the same degree and parity);
+// dx has one job per input block (its sources: the output blocks it feeds,
+// with W read transposed).
+//
+// One wave per (job, tile of 32 rows, slab of 64 columns).  Operand layout of
+// the 16x16x4 instruction: A[i][kk] from lane i + 16 kk, B[kk][j] from lane
+// j + 16 kk, D[4 (l / 16) + r][l % 16] in register r of lane l.  Lane l loads
+// one float4 of its row (row l % 16 of a 16-row subtile) at columns
+// k0 + 4 (l / 16) .. +3; instruction c then uses component c, so the four kk
+// of instruction c are k0 + 4 kk + c, and B is read at the same k.  No
+// transpose of the rows is needed.
+constexpr int kLinMaxJobs = 64;
+constexpr int kLinChunks = 64;  // row chunks of the dW reduction (fixed: deterministic)
+constexpr int kLinRT = 4;       // 16-row subtiles per wave in the gather-GEMM
+
+struct LinJob {
+  int R, dst_row, src_first, nsrc;
+};
+struct LinSrc {
+  int row, pad;
+  int64_t w_off;
+};
+struct LinPair {  // dW slice: input block row, output block row, W offset
+  int R, src_row, dst_row, pad;
+  int64_t w_off;
+};
+
+struct LinArgs {
+  const float* src;
+  const float* W;
+  float* dst;
+  const LinJob* jobs;
+  const LinSrc* srcs;
+  int64_t n;
+  int D_src, C_src, D_dst, C_dst, ldk, ldc, njobs, slabs;
+  int first[kLinMaxJobs + 1];
+};
+
+template <int RT>  // RT subtiles of 16 rows per wave
+__global__ __launch_bounds__(kWave) void k_lin_gemm(LinArgs a) {
+  const int unit = blockIdx.x;
+  int lo = 0, hi = a.njobs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.first[mid] <= unit) lo = mid; else hi = mid - 1;
+  }
+  const LinJob jb = a.jobs[lo];
+  const int u = unit - a.first[lo];
+  const int col0 = (u % a.slabs) * kWave;
+  const int64_t r0 = (int64_t)(u / a.slabs) * (16 * RT);
+  const int64_t NR = a.n * jb.R;
+  const int lane = threadIdx.x, g = lane >> 4, li = lane & 15;
+  f4v acc[RT][4];
+#pragma unroll
+  for (int s = 0; s < RT; ++s)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[s][cb] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  int64_t abase[RT];
+  bool aval[RT];
+#pragma unroll
+  for (int s = 0; s < RT; ++s) {
+    const int64_t r = r0 + 16 * s + li;
+    aval[s] = r < NR;
+    const int64_t nd = aval[s] ? r / jb.R : 0, m = aval[s] ? r % jb.R : 0;
+    abase[s] = (nd * a.D_src + m) * a.C_src + 4 * g;
+  }
+  // B[k][col] = W[w_off + k ldk + col ldc]: per-lane part in the vector offset,
+  // the k step and column block in the (uniform) scalar offset; columns past
+  // C_dst read zero through the range check of a per-source descriptor.
+  const int col = col0 + li;
+  const int bvoff = ((4 * g) * a.ldk + col * a.ldc) * 4;
+  const int ncols_valid = a.C_dst - col0;  // uniform
+  for (int t = 0; t < jb.nsrc; ++t) {
+    const LinSrc sr = a.srcs[jb.src_first + t];
+    const float* sp = a.src + (int64_t)sr.row * a.C_src;
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.W + sr.w_off), (short)0, a.C_src * a.C_dst * 4, 0x00020000);
+    for (int k0 = 0; k0 < a.C_src; k0 += 16) {
+      f4v av[RT];
+#pragma unroll
+      for (int s = 0; s < RT; ++s)
+        av[s] = aval[s] ? *reinterpret_cast<const f4v*>(sp + abase[s] + k0) : f4v{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          float bv = __builtin_bit_cast(
+              float, __builtin_amdgcn_raw_buffer_load_b32(wr, bvoff, ((k0 + c) * a.ldk + 16 * cb * a.ldc) * 4, 0));
+          if (16 * cb + li >= ncols_valid) bv = 0.0f;
+#pragma unroll
+          for (int s = 0; s < RT; ++s)
+            acc[s][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s][c], bv, acc[s][cb], 0, 0, 0);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < RT; ++s)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = r0 + 16 * s + 4 * g + r;
+      if (row >= NR) continue;
+      const int64_t nd = row / jb.R, m = row % jb.R;
+      float* dp = a.dst + (nd * a.D_dst + jb.dst_row + m) * a.C_dst;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        if (16 * cb + li < ncols_valid) dp[col0 + 16 * cb + li] = acc[s][cb][r];
+    }
+}
+
+// Wt[pair][j][k] = W[w_off(pair) + k C_out + j]: each dW-sized slice
+// transposed, so that dx reads B along rows.
+__global__ __launch_bounds__(256) void k_lin_transpose(const float* __restrict__ W, const LinPair* __restrict__ pairs,
+                                                        float* __restrict__ Wt, int npairs, int C_in, int C_out) {
+  const int64_t per = (int64_t)C_in * C_out;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= per * npairs) return;
+  const int p = (int)(i / per);
+  const int64_t e = i % per;
+  const int j = (int)(e / C_in), k = (int)(e % C_in);
+  Wt[i] = W[pairs[p].w_off + (int64_t)k * C_out + j];
+}
+
+// dW partials: one wave per (pair, row chunk, 64 x 64 tile of W).  Per four
+// rows, lane l loads one float4 of x (columns k-tile + 4 (l % 16) .. +3) and
+// one of dout (j-tile + 4 (l % 16) .. +3) of row + l / 16; instruction (a, b)
+// takes component a as A and b as B (the 16x16x4 reduction index kk is the
+// row), so D[a][b][i][j] accumulates x^T dout at k = k-tile + 4 i + a,
+// j = j-tile + 4 j + b.
+struct LinDwArgs {
+  const float* x;
+  const float* dout;
+  float* dWp;  // [npairs][kLinChunks][C_in][C_out]
+  const LinPair* pairs;
+  int64_t n;
+  int D_in, C_in, D_out, C_out, ktiles, jtiles;
+};
+
+__global__ __launch_bounds__(kWave) void k_lin_dw(LinDwArgs a) {
+  const int per = kLinChunks * a.ktiles * a.jtiles;
+  const int p = blockIdx.x / per, u = blockIdx.x % per;
+  const int chunk = u / (a.ktiles * a.jtiles), kt = (u / a.jtiles) % a.ktiles, jt = u % a.jtiles;
+  const LinPair pr = a.pairs[p];
+  const int64_t NR = a.n * pr.R;
+  const int64_t rpc = (NR + kLinChunks - 1) / kLinChunks;
+  const int64_t rb = chunk * rpc, re = rb + rpc < NR ? rb + rpc : NR;
+  const int lane = threadIdx.x, g = lane >> 4, li = lane & 15;
+  f4v acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  const int kc = kt * 64 + 4 * li, jc = jt * 64 + 4 * li;  // multiples of 4; C_in, C_out are of 16
+  const bool kv = kc < a.C_in, jv = jc < a.C_out;
+  for (int64_t r = rb; r < re; r += 4) {
+    const int64_t row = r + g;
+    const bool ok = row < re;
+    const int64_t nd = ok ? row / pr.R : 0, m = ok ? row % pr.R : 0;
+    const f4v xa = ok && kv ? *reinterpret_cast<const f4v*>(a.x + (nd * a.D_in + pr.src_row + m) * a.C_in + kc)
+                            : f4v{0.0f, 0.0f, 0.0f, 0.0f};
+    const f4v db = ok && jv ? *reinterpret_cast<const f4v*>(a.dout + (nd * a.D_out + pr.dst_row + m) * a.C_out + jc)
+                            : f4v{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i], db[j], acc[i][j], 0, 0, 0);
+  }
+  // register r of acc[a][b] in lane l: k = k-tile + 4 (4 (l / 16) + r) + a, j = j-tile + 4 (l % 16) + b
+  float* out = a.dWp + ((int64_t)p * kLinChunks + chunk) * a.C_in * a.C_out;
+  if (!jv) return;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int k = kt * 64 + 4 * (4 * g + r) + i;
+      if (k >= a.C_in) continue;
+      f4v v{acc[i][0][r], acc[i][1][r], acc[i][2][r], acc[i][3][r]};
+      *reinterpret_cast<f4v*>(out + (int64_t)k * a.C_out + jc) = v;
+    }
+}
+
+// dW[w_off(p) + e] = sum over the row chunks of pair p, in chunk order.
+__global__ __launch_bounds__(256) void k_lin_dw_sum(const float* __restrict__ dWp, const LinPair* __restrict__ pairs,
+                                                     float* __restrict__ dW, int npairs, int64_t per) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)npairs * per) return;
+  const int p = (int)(i / per);
+  const int64_t e = i % per;
+  float s = 0.0f;
+  for (int c = 0; c < kLinChunks; ++c) s += dWp[((int64_t)p * kLinChunks + c) * per + e];
+  dW[pairs[p].w_off + e] = s;
+}
+
 // ------------------------------------------------------------ graph
 __global__ void k_graph_keys(const int32_t* __restrict__ snd, const int32_t* __restrict__ rcv, int64_t n_edges,
                              int32_t n_nodes, int32_t pad, uint32_t* __restrict__ key_r, uint32_t* __restrict__ key_s,
@@ -2184,6 +2383,218 @@ e3_status e3_conv_bwd2(const e3_plan* p, const e3_graph* g, const float* x, cons
   if ((st = v.bwd[ci](p, g, x, nullptr, ddy, s, dm, gx, nullptr, nullptr, gs, kAccDs, ws, hs)) != E3_OK) return st;
   // (d_s x, d_s y, -) = conv_bwd(x, y, dds, dm)
   return v.bwd[ci](p, g, x, nullptr, y, dds, dm, gx, nullptr, gy, nullptr, kAccDx | kAccDy, ws, hs);
+}
+
+}  // extern "C"
+
+// ============================================================ linear mixing (host)
+struct e3_linear {
+  int d_in = 0, d_out = 0, c_in = 0, c_out = 0;
+  int64_t nw = 0;
+  std::vector<LinJob> fj, bj;   // forward jobs (output blocks), dx jobs (input blocks)
+  std::vector<LinSrc> fs, bs;
+  std::vector<LinPair> pairs;
+  std::mutex mu;
+  char* dev = nullptr;  // device copy of the tables (uploaded on first use)
+  size_t off_fj = 0, off_fs = 0, off_bj = 0, off_bs = 0, off_pairs = 0;
+};
+
+namespace {
+e3_status lin_upload(e3_linear* L, hipStream_t st) {
+  std::lock_guard<std::mutex> lk(L->mu);
+  if (L->dev) return E3_OK;
+  size_t off = 0;
+  auto place = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
+  L->off_fj = place(L->fj.size() * sizeof(LinJob) + 1);
+  L->off_fs = place(L->fs.size() * sizeof(LinSrc) + 1);
+  L->off_bj = place(L->bj.size() * sizeof(LinJob) + 1);
+  L->off_bs = place(L->bs.size() * sizeof(LinSrc) + 1);
+  L->off_pairs = place(L->pairs.size() * sizeof(LinPair) + 1);
+  std::vector<char> host(off, 0);
+  auto put = [&](size_t o, const void* p, size_t b) { if (b) std::memcpy(host.data() + o, p, b); };
+  put(L->off_fj, L->fj.data(), L->fj.size() * sizeof(LinJob));
+  put(L->off_fs, L->fs.data(), L->fs.size() * sizeof(LinSrc));
+  put(L->off_bj, L->bj.data(), L->bj.size() * sizeof(LinJob));
+  put(L->off_bs, L->bs.data(), L->bs.size() * sizeof(LinSrc));
+  put(L->off_pairs, L->pairs.data(), L->pairs.size() * sizeof(LinPair));
+  char* d = nullptr;
+  E3_HIP(hipMalloc(&d, off));
+  hipError_t e = hipMemcpyAsync(d, host.data(), off, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    g_last_error = std::string("linear tables upload: ") + hipGetErrorString(e);
+    (void)hipFree(d);
+    return E3_ERR_HIP;
+  }
+  L->dev = d;
+  return E3_OK;
+}
+
+e3_status lin_gemm(const std::vector<LinJob>& jobs, const LinJob* djobs, const LinSrc* dsrcs, const float* src,
+                   const float* W, float* dst, int64_t n, int D_src, int C_src, int D_dst, int C_dst, int ldk, int ldc,
+                   const char* name, hipStream_t st) {
+  LinArgs a{};
+  a.src = src, a.W = W, a.dst = dst, a.jobs = djobs, a.srcs = dsrcs, a.n = n;
+  a.D_src = D_src, a.C_src = C_src, a.D_dst = D_dst, a.C_dst = C_dst, a.ldk = ldk, a.ldc = ldc;
+  a.njobs = (int)jobs.size();
+  a.slabs = (C_dst + kWave - 1) / kWave;
+  int64_t u = 0;
+  for (size_t j = 0; j < jobs.size(); ++j) {
+    a.first[j] = (int)u;
+    u += (n * jobs[j].R + 16 * kLinRT - 1) / (16 * kLinRT) * a.slabs;
+  }
+  a.first[jobs.size()] = (int)u;
+  if (u == 0) return E3_OK;
+  if (u > 0x7fffffff) return E3_ERR_INVALID_ARG;
+  TimedLaunch t_(name, st);
+  hipLaunchKernelGGL(k_lin_gemm<kLinRT>, dim3((unsigned)u), dim3(kWave), 0, st, a);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+// dW partials, then W transposed slice by slice (read by dx along rows)
+size_t lin_ws_dwp(const e3_linear* L) {
+  return align256((size_t)L->pairs.size() * kLinChunks * L->c_in * L->c_out * sizeof(float));
+}
+size_t lin_ws(const e3_linear* L) { return lin_ws_dwp(L) + align256((size_t)L->nw * sizeof(float)); }
+}  // namespace
+
+extern "C" {
+
+e3_status e3_linear_create(const char* irreps_in, const char* irreps_out, e3_linear** out) {
+  if (!irreps_in || !irreps_out || !out) return E3_ERR_INVALID_ARG;
+  *out = nullptr;
+  std::vector<e3b::Block> bi, bo;
+  std::string err;
+  if (!e3b::parse_irreps(irreps_in, bi, err) || !e3b::parse_irreps(irreps_out, bo, err)) {
+    g_last_error = err;
+    return E3_ERR_INVALID_ARG;
+  }
+  const int c_in = bi[0].mul, c_out = bo[0].mul;
+  for (const auto& b : bi)
+    if (b.mul != c_in) return E3_ERR_INVALID_ARG;
+  for (const auto& b : bo)
+    if (b.mul != c_out) return E3_ERR_INVALID_ARG;
+  if (c_in % 16 || c_out % 16 || c_in > 4096 || c_out > 4096) {
+    g_last_error = "linear mixing needs multiplicities that are multiples of 16 (at most 4096)";
+    return E3_ERR_UNSUPPORTED;
+  }
+  if ((int)bi.size() > kLinMaxJobs || (int)bo.size() > kLinMaxJobs) {
+    g_last_error = "linear mixing supports at most 64 blocks per side";
+    return E3_ERR_UNSUPPORTED;
+  }
+  e3_linear* L = new (std::nothrow) e3_linear();
+  if (!L) return E3_ERR_ALLOC;
+  L->c_in = c_in, L->c_out = c_out;
+  std::vector<int> irow(bi.size()), orow(bo.size());
+  for (size_t i = 0; i < bi.size(); ++i) irow[i] = L->d_in, L->d_in += 2 * bi[i].l + 1;
+  for (size_t o = 0; o < bo.size(); ++o) orow[o] = L->d_out, L->d_out += 2 * bo[o].l + 1;
+  // forward: one job per output block, sources = input blocks of its type, in order
+  std::vector<std::vector<std::pair<int, int64_t>>> feeds(bi.size());  // input -> (output, W offset)
+  int64_t woff = 0;
+  for (size_t o = 0; o < bo.size(); ++o) {
+    LinJob j{2 * bo[o].l + 1, orow[o], (int)L->fs.size(), 0};
+    for (size_t i = 0; i < bi.size(); ++i)
+      if (bi[i].l == bo[o].l && bi[i].p == bo[o].p) {
+        L->fs.push_back(LinSrc{irow[i], 0, woff});
+        L->pairs.push_back(LinPair{j.R, irow[i], orow[o], 0, woff});
+        feeds[i].push_back({(int)o, woff});
+        woff += (int64_t)c_in * c_out;
+        ++j.nsrc;
+      }
+    L->fj.push_back(j);
+  }
+  L->nw = woff;
+  // dx: one job per input block, sources = the output blocks it feeds (W read transposed)
+  for (size_t i = 0; i < bi.size(); ++i) {
+    LinJob j{2 * bi[i].l + 1, irow[i], (int)L->bs.size(), (int)feeds[i].size()};
+    for (auto& f : feeds[i]) L->bs.push_back(LinSrc{orow[f.first], 0, f.second});
+    L->bj.push_back(j);
+  }
+  *out = L;
+  return E3_OK;
+}
+
+e3_status e3_linear_query(const e3_linear* L, int64_t* n_weights, int* d_in, int* d_out, int* c_in, int* c_out) {
+  if (!L) return E3_ERR_INVALID_ARG;
+  if (n_weights) *n_weights = L->nw;
+  if (d_in) *d_in = L->d_in;
+  if (d_out) *d_out = L->d_out;
+  if (c_in) *c_in = L->c_in;
+  if (c_out) *c_out = L->c_out;
+  return E3_OK;
+}
+
+e3_status e3_linear_destroy(e3_linear* L) {
+  if (!L) return E3_OK;
+  if (L->dev) (void)hipFree(L->dev);
+  delete L;
+  return E3_OK;
+}
+
+e3_status e3_linear_fwd(e3_linear* L, const float* x, const float* W, float* out, int64_t n, e3_stream stream) {
+  if (!L || n < 0) return E3_ERR_INVALID_ARG;
+  if (n == 0) return E3_OK;
+  if (!x || !W || !out || !aligned16(x) || !aligned16(out)) return E3_ERR_INVALID_ARG;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  e3_status s = lin_upload(L, st);
+  if (s != E3_OK) return s;
+  return lin_gemm(L->fj, reinterpret_cast<const LinJob*>(L->dev + L->off_fj),
+                  reinterpret_cast<const LinSrc*>(L->dev + L->off_fs), x, W, out, n, L->d_in, L->c_in, L->d_out,
+                  L->c_out, L->c_out, 1, "linear_fwd", st);
+}
+
+e3_status e3_linear_workspace_size(const e3_linear* L, size_t* bwd_bytes) {
+  if (!L || !bwd_bytes) return E3_ERR_INVALID_ARG;
+  *bwd_bytes = lin_ws(L);
+  return E3_OK;
+}
+
+e3_status e3_linear_bwd(e3_linear* L, const float* x, const float* W, const float* dout, float* dx, float* dW,
+                        void* ws, size_t ws_bytes, int64_t n, e3_stream stream) {
+  if (!L || n < 0) return E3_ERR_INVALID_ARG;
+  if (!W || !dW || (n > 0 && (!x || !dout || !dx || !aligned16(x) || !aligned16(dout) || !aligned16(dx))))
+    return E3_ERR_INVALID_ARG;
+  if (ws_bytes < lin_ws(L)) return E3_ERR_WORKSPACE_TOO_SMALL;
+  if (lin_ws(L) > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  e3_status s = lin_upload(L, st);
+  if (s != E3_OK) return s;
+  const LinPair* dp = reinterpret_cast<const LinPair*>(L->dev + L->off_pairs);
+  if (n > 0) {
+    // slices of Wt sit at the same offsets as those of W (pair order)
+    float* Wt = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + lin_ws_dwp(L));
+    if (!L->pairs.empty()) {
+      TimedLaunch t_("linear_bwd_transpose", st);
+      hipLaunchKernelGGL(k_lin_transpose, dim3(blocks_for(L->nw, 256)), dim3(256), 0, st, W, dp, Wt,
+                         (int)L->pairs.size(), L->c_in, L->c_out);
+      E3_HIP(hipGetLastError());
+    }
+    s = lin_gemm(L->bj, reinterpret_cast<const LinJob*>(L->dev + L->off_bj),
+                 reinterpret_cast<const LinSrc*>(L->dev + L->off_bs), dout, Wt, dx, n, L->d_out, L->c_out, L->d_in,
+                 L->c_in, L->c_in, 1, "linear_bwd_dx", st);
+    if (s != E3_OK) return s;
+  }
+  if (L->pairs.empty()) return E3_OK;
+  float* dWp = reinterpret_cast<float*>(ws);
+  LinDwArgs a{};
+  a.x = x, a.dout = dout, a.dWp = dWp, a.pairs = dp, a.n = n;
+  a.D_in = L->d_in, a.C_in = L->c_in, a.D_out = L->d_out, a.C_out = L->c_out;
+  a.ktiles = (L->c_in + 63) / 64, a.jtiles = (L->c_out + 63) / 64;
+  {
+    TimedLaunch t_("linear_bwd_dw", st);
+    const int64_t units = (int64_t)L->pairs.size() * kLinChunks * a.ktiles * a.jtiles;
+    hipLaunchKernelGGL(k_lin_dw, dim3((unsigned)units), dim3(kWave), 0, st, a);
+    E3_HIP(hipGetLastError());
+  }
+  {
+    TimedLaunch t_("linear_bwd_dw_sum", st);
+    const int64_t per = (int64_t)L->c_in * L->c_out;
+    hipLaunchKernelGGL(k_lin_dw_sum, dim3(blocks_for(per * (int64_t)L->pairs.size(), 256)), dim3(256), 0, st, dWp, dp,
+                       dW, (int)L->pairs.size(), per);
+    E3_HIP(hipGetLastError());
+  }
+  return E3_OK;
 }
 
 }  // extern "C"

@@ -58,6 +58,13 @@ SIGNATURES = {
     "e3_tp_workspace_size": (_I, [_P, _I64, ct.POINTER(ct.c_size_t)]),
     "e3_tp_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, _P]),
     "e3_conv_workspace_size": (_I, [_P, _P, ct.POINTER(ct.c_size_t), ct.POINTER(ct.c_size_t)]),
+    "e3_linear_create": (_I, [ct.c_char_p, ct.c_char_p, ct.POINTER(ct.c_void_p)]),
+    "e3_linear_query": (_I, [_P, ct.POINTER(ct.c_int64), ct.POINTER(ct.c_int), ct.POINTER(ct.c_int),
+                             ct.POINTER(ct.c_int), ct.POINTER(ct.c_int)]),
+    "e3_linear_destroy": (_I, [_P]),
+    "e3_linear_fwd": (_I, [_P, _P, _P, _P, _I64, _P]),
+    "e3_linear_workspace_size": (_I, [_P, ct.POINTER(ct.c_size_t)]),
+    "e3_linear_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, _P]),
     "e3_conv_fwd_y": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P]),
     "e3_conv_bwd_y": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_int, _P, ct.c_size_t, _P]),
     "e3_conv_bwd2": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
@@ -370,6 +377,55 @@ def conv_bwd2(plan: Plan, graph: Graph, x, y, s, dm, ddx, ddy, dds, ws=None, str
                               _ptr(gs, "gs", (E, plan.P, plan.C)), _ptr(gdm, "gdm", (N, plan.D_out, plan.C)),
                               ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd2")
     return gx, gy, gs, gdm
+
+
+class Linear:
+    """Equivariant linear mixing between two irreps layouts (weights shared over m)."""
+
+    def __init__(self, irreps_in: str, irreps_out: str):
+        h = ct.c_void_p()
+        _check(lib().e3_linear_create(irreps_in.encode(), irreps_out.encode(), ct.byref(h)), "e3_linear_create")
+        self.handle = h
+        nw, di, do, ci, co = ct.c_int64(), ct.c_int(), ct.c_int(), ct.c_int(), ct.c_int()
+        _check(lib().e3_linear_query(h, ct.byref(nw), ct.byref(di), ct.byref(do), ct.byref(ci), ct.byref(co)),
+               "e3_linear_query")
+        self.n_weights, self.D_in, self.D_out, self.C_in, self.C_out = nw.value, di.value, do.value, ci.value, co.value
+
+    def close(self):
+        if getattr(self, "handle", None) and self.handle.value:
+            lib().e3_linear_destroy(self.handle)
+            self.handle = ct.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def forward(self, x, W, out=None, stream=None):
+        n = x.shape[0]
+        out = _empty((n, self.D_out, self.C_out)) if out is None else out
+        _check(lib().e3_linear_fwd(self.handle, _ptr(x, "x", (n, self.D_in, self.C_in)),
+                                   _ptr(W, "W", (self.n_weights,)), _ptr(out, "out", (n, self.D_out, self.C_out)),
+                                   n, _stream(stream)), "e3_linear_fwd")
+        return out
+
+    def workspace_size(self) -> int:
+        b = ct.c_size_t()
+        _check(lib().e3_linear_workspace_size(self.handle, ct.byref(b)), "e3_linear_workspace_size")
+        return b.value
+
+    def backward(self, x, W, dout, dx=None, dW=None, ws=None, stream=None):
+        n = x.shape[0]
+        dx = _empty((n, self.D_in, self.C_in)) if dx is None else dx
+        dW = _empty((self.n_weights,)) if dW is None else dW
+        if ws is None:
+            ws = workspace(self.workspace_size())
+        _check(lib().e3_linear_bwd(self.handle, _ptr(x, "x", (n, self.D_in, self.C_in)),
+                                   _ptr(W, "W", (self.n_weights,)), _ptr(dout, "dout", (n, self.D_out, self.C_out)),
+                                   _ptr(dx, "dx", (n, self.D_in, self.C_in)), _ptr(dW, "dW", (self.n_weights,)),
+                                   ct.c_void_p(ws.data_ptr()), ws.numel(), n, _stream(stream)), "e3_linear_bwd")
+        return dx, dW
 
 
 def conv_radial_workspace_size(plan: Plan, graph: Graph, K: int) -> int:

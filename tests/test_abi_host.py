@@ -137,3 +137,25 @@ def test_null_and_negative_arguments_rejected_before_device_work():
     assert L.e3_conv_bwd_radial(plan.handle, None, None, None, None, None, 8, None, None, None, None, None,
                                 None, 0, None) == 1
     assert L.e3_conv_fwd_radial(None, None, None, None, None, None, 8, None, None) == 1
+
+
+def test_linear_descriptor_matches_oracle_plan():
+    """Weight count and layout sizes of the linear-mixing descriptor (host only)."""
+    from oracle import linear as olin
+    for ins, outs in [("16x0e+16x1o+16x1o+16x2e", "32x0e+32x1o+32x1e+32x2e"),
+                      ("128x0e+128x1o+128x2e+128x3o", "128x0e+128x1o+128x2e+128x3o")]:
+        L = e3mi.Linear(ins, outs)
+        jobs, d_in, d_out, c_in, c_out, nw = olin.plan(ins, outs)
+        assert (L.n_weights, L.D_in, L.D_out, L.C_in, L.C_out) == (nw, d_in, d_out, c_in, c_out)
+        L.close()
+    for bad in [("8x0e", "16x0e"), ("16x0e+8x1o", "16x0e"), ("", "16x0e")]:
+        with pytest.raises(e3mi.E3Error):
+            e3mi.Linear(*bad)
+    L = e3mi.Linear("16x0e", "16x0e")
+    Ll = e3mi.lib()
+    assert Ll.e3_linear_fwd(L.handle, None, None, None, -1, None) == 1
+    assert Ll.e3_linear_fwd(L.handle, None, None, None, 0, None) == 0
+    assert Ll.e3_linear_fwd(L.handle, None, None, None, 5, None) == 1
+    n = ct.c_size_t()
+    assert Ll.e3_linear_workspace_size(L.handle, ct.byref(n)) == 0 and n.value > 0
+    assert Ll.e3_linear_bwd(L.handle, None, None, None, None, None, None, 0, 5, None) == 1

@@ -650,3 +650,91 @@ def test_conv_bwd2_config4_sampled(e3):
     print("rel-L2", errs, f"(sub-problem: {sel.shape[0]} edges, {nodes.shape[0]} nodes)", flush=True)
     for k, v in errs.items():
         assert v < TOL, (k, v)
+
+
+# ---------------------------------------------------------------- linear mixing
+from oracle import linear as olinear  # noqa: E402
+
+
+@pytest.mark.parametrize("ins,outs,n", [
+    ("16x0e+16x1o+16x1o+16x2e", "32x0e+32x1o+32x1e+32x2e", 37),      # two 1o inputs; 1e has none
+    ("128x0e+128x1o+128x2e+128x3o", "128x0e+128x1o+128x2e+128x3o", 101),
+    ("64x0e+64x1o", "192x0e+192x1o", 9),                              # 3 column slabs
+    ("48x1o+48x0e+48x1o+48x1o", "16x1o+16x0e", 23),
+])
+def test_linear_small_full(e3, ins, outs, n):
+    import torch
+    _say("linear", ins, "->", outs, n)
+    L = e3.Linear(ins, outs)
+    rng = np.random.default_rng(18)
+    x = rng.standard_normal((n, L.D_in, L.C_in)).astype(np.float32)
+    W = (rng.standard_normal(L.n_weights) / 8).astype(np.float32)
+    dout = rng.standard_normal((n, L.D_out, L.C_out)).astype(np.float32)
+    xs, Ws, ds = to_dev(x), to_dev(W), to_dev(dout)
+    y = L.forward(xs, Ws)
+    dx, dW = L.backward(xs, Ws, ds)
+    y2 = L.forward(xs, Ws)
+    dx2, dW2 = L.backward(xs, Ws, ds)
+    assert torch.equal(y, y2) and torch.equal(dx, dx2) and torch.equal(dW, dW2)
+    ref_y = olinear.forward(ins, outs, x, W).numpy()
+    ref_dx, ref_dW = (t.numpy() for t in olinear.backward(ins, outs, x, W, dout))
+    errs = dict(y=rel_l2(to_np(y), ref_y), dx=rel_l2(to_np(dx), ref_dx), dW=rel_l2(to_np(dW), ref_dW))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+
+
+def _path_irreps(plan):
+    """Irreps string of the convolution's output blocks (one block per path)."""
+    names = []
+    for l1, l2, l3, p3, x_off, y_off, out_off in plan.paths():
+        names.append(f"{plan.C}x{l3}{'e' if p3 > 0 else 'o'}")
+    return "+".join(names)
+
+
+@pytest.mark.parametrize("which", ["nodes", "messages"])
+def test_linear_config4_sampled(e3, which):
+    """Full-size mixing at config 4 (24,000 atoms, 128 channels): node features
+    (x blocks 0e,1o,2e,3o), or the convolution output (34 path blocks mixed per
+    degree and parity).  Outputs on sampled nodes; dW on sampled pairs, each from
+    an oracle sub-problem holding only that pair's two blocks over all nodes."""
+    import torch
+    cfg = synth.CONFIGS[4]
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    N = 24000
+    ins = cfg.irreps if which == "nodes" else _path_irreps(plan)
+    outs = "128x0e+128x1o+128x2e+128x3o" if which == "nodes" else \
+        "128x0e+128x0o+128x1o+128x1e+128x2e+128x2o+128x3o+128x3e"
+    _say("linear config 4", which, ins[:40], "->", outs)
+    L = e3.Linear(ins, outs)
+    dev = torch.device("cuda")
+    xs = synth.normal_device(4, 20, (N, L.D_in, L.C_in), dev)
+    Ws = synth.normal_device(4, 21, (L.n_weights,), dev) / 16
+    ds = synth.normal_device(4, 22, (N, L.D_out, L.C_out), dev)
+    y = L.forward(xs, Ws)
+    dx, dW = L.backward(xs, Ws, ds)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(19)
+    rows = np.concatenate([[0, N - 1], rng.choice(N, 30, replace=False)])
+    ri = torch.as_tensor(rows, device=dev)
+    x_r, d_r, W_h = to_np(xs[ri]), to_np(ds[ri]), to_np(Ws)
+    errs = dict(y=rel_l2(to_np(y[ri]), olinear.forward(ins, outs, x_r, W_h).numpy()),
+                dx=rel_l2(to_np(dx[ri]), olinear.backward(ins, outs, x_r, W_h, d_r)[0].numpy()))
+    jobs = olinear.plan(ins, outs)[0]
+    bi = olinear.blocks(ins)[0]
+    bo = olinear.blocks(outs)[0]
+    pairs = [(o, t) for o, job in enumerate(jobs) for t in range(len(job[2]))]
+    for o, t in [pairs[i] for i in rng.choice(len(pairs), 3, replace=False)]:
+        l, orow, src, off, n = jobs[o]
+        irow = src[t]
+        R = 2 * l + 1
+        sub_in = f"{L.C_in}x{l}{'e' if bo[o][1] > 0 else 'o'}"
+        sub_out = f"{L.C_out}x{l}{'e' if bo[o][1] > 0 else 'o'}"
+        xb = to_np(xs[:, irow:irow + R])
+        db = to_np(ds[:, orow:orow + R])
+        ref = olinear.backward(sub_in, sub_out, xb, np.zeros(L.C_in * L.C_out), db)[1].numpy()
+        got = to_np(dW[off + t * L.C_in * L.C_out: off + (t + 1) * L.C_in * L.C_out])
+        errs[f"dW[{o},{t}]"] = rel_l2(got, ref)
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
