@@ -451,3 +451,63 @@ def test_linear_equivariance_and_backward():
     fd = (f(h) - f(-h)) / (2 * h)     # the loss is quadratic in t: exact up to rounding
     an = float((dx * torch.as_tensor(u)).sum() + (dW * torch.as_tensor(v)).sum())
     assert abs(fd - an) < 1e-8 * max(1.0, abs(an))
+
+
+# ---------------------------------------------------------------- generic records
+@pytest.mark.parametrize("spec", [("2x0e+2x1o+2x2e", 3, 3), ("3x0e+3x1o+3x2e+3x3o", 3, 3)])
+def test_generic_records_equal_path_tp_and_backward(spec):
+    """With the layout's own records and a shared y, the generic product equals
+    the path-by-path product; with per-channel y equal to the shared one in every
+    channel it equals it too; the backward equals float64 autograd of the forward
+    (shared and per-channel y) and its dy sums over channels when y is shared."""
+    from oracle import generic
+    rng = np.random.default_rng(51)
+    lay = irreps.layout(*spec)
+    recs = cg.coo_records(lay)
+    i0, i1, i2, v = (np.array([r[k] for r in recs]) for k in range(4))
+    R, C = 5, lay.channels
+    x = rng.standard_normal((R, lay.d_in, C))
+    y = sh.sh_unit(lay.lmax_sh, _unit(rng, R))
+    ref = tp.tp_unweighted(lay, x, y).numpy()
+    assert np.allclose(generic.tp(i0, i1, i2, v, x, y, lay.d_out), ref, atol=1e-12)
+    ypc = np.repeat(y[:, :, None], C, axis=2)
+    assert np.allclose(generic.tp(i0, i1, i2, v, x, ypc, lay.d_out), ref, atol=1e-12)
+    dz = rng.standard_normal(ref.shape)
+    for yy in (y, ypc + rng.standard_normal(ypc.shape)):
+        dx, dy = generic.tp_bwd(i0, i1, i2, v, x, yy, dz)
+        xt = torch.tensor(x, requires_grad=True)
+        yt = torch.tensor(yy, requires_grad=True)
+        ye = yt if yy.ndim == 3 else yt[:, :, None]
+        z = torch.zeros((R, lay.d_out, C), dtype=torch.float64)
+        z = z.index_add(1, torch.as_tensor(i0), torch.as_tensor(v)[None, :, None] * xt[:, i1, :] * ye[:, i2, :])
+        gx, gy = torch.autograd.grad((z * torch.as_tensor(dz)).sum(), [xt, yt])
+        assert np.allclose(dx, gx.numpy(), atol=1e-11) and np.allclose(dy, gy.numpy(), atol=1e-11)
+
+
+def test_generic_collapsed_output_block():
+    """Records of two paths with the same output degree sent to one output block
+    give the sum of the two paths' outputs (a collapsed output multiplicity)."""
+    from oracle import generic
+    rng = np.random.default_rng(52)
+    lay = irreps.layout("2x0e+2x1o", 2, 1)
+    recs = cg.coo_records(lay)
+    blocks = [(p.out_off, p.l3) for p in lay.paths]
+    # map every l3 = 1 block onto the first l3 = 1 block
+    first1 = min(off for off, l3 in blocks if l3 == 1)
+    remap = {}
+    for off, l3 in blocks:
+        for mm in range(2 * l3 + 1):
+            remap[off + mm] = (first1 + mm) if l3 == 1 else off + mm
+    i0 = np.array([remap[r[0]] for r in recs])
+    i1, i2, v = (np.array([r[k] for r in recs]) for k in (1, 2, 3))
+    x = rng.standard_normal((3, lay.d_in, lay.channels))
+    y = sh.sh_unit(lay.lmax_sh, _unit(rng, 3))
+    full = tp.tp_unweighted(lay, x, y).numpy()
+    got = generic.tp(i0, i1, i2, v, x, y, lay.d_out)
+    want = np.zeros_like(full)
+    for off, l3 in blocks:
+        if l3 == 1:
+            want[:, first1:first1 + 3] += full[:, off:off + 3]
+        else:
+            want[:, off:off + 2 * l3 + 1] = full[:, off:off + 2 * l3 + 1]
+    assert np.allclose(got, want, atol=1e-12)
