@@ -438,6 +438,28 @@ def main():
                          "frac": round(nb / (tb_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "alg_bytes": nb,
                          "event_ms": round(a0.elapsed_time(a1) / args.steps, 4)}
         log(f"tp_bwd: {tb_ms:.3f} ms, {out['tp_bwd']['alg_GBps']} GB/s")
+        # the same product through the caller-supplied record path (the plan's records, unweighted)
+        i0, i1, i2, rv = tplan.records()
+        rtp = e3mi.RecordTP(tplan.D_in, tplan.D_sh, tplan.D_out, i0, i1, i2, rv.astype(np.float32), False)
+        tz = torch.empty((R, tplan.D_out, tplan.C), dtype=torch.float32, device=dev)
+        for _ in range(args.warmup):
+            rtp.forward(txd, ty, out=tz)
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        for _ in range(args.steps):
+            rtp.forward(txd, ty, out=tz)
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        tt = e3mi.timing_read()
+        tg_ms = tt["tpg_fwd"][0] / tt["tpg_fwd"][1]
+        nb = R * (tplan.D_in * tplan.C + tplan.D_sh + tplan.D_out * tplan.C) * 4
+        out["tp_records"] = {"workload": out["tp"]["workload"] + ", unweighted, records streamed at run time",
+                             "nnz": int(i0.shape[0]), "ms": round(tg_ms, 4),
+                             "alg_GBps": round(nb / (tg_ms * 1e-3) / 1e9, 1)}
+        log(f"tp_records: {tg_ms:.3f} ms, {out['tp_records']['alg_GBps']} GB/s")
+        rtp.close()
+        del tz
         del tdz, tdx, tdw, tdy, tws, txd, twd, ty
 
     if args.copy_probe:

@@ -245,6 +245,27 @@ e3_status e3_linear_workspace_size(const e3_linear* lin, size_t* bwd_bytes);
 e3_status e3_linear_bwd(e3_linear* lin, const float* x, const float* W, const float* dout, float* dx, float* dW,
                         void* ws, size_t ws_bytes, int64_t n, e3_stream stream);
 
+/* Tensor product with caller-supplied coefficient records (App. E.2's
+ * unfolded COO form): z[r, i0, q] = sum over records (i0, i1, i2, v) of
+ * v x[r, i1, q] y[r, i2, q] (y_per_channel != 0) or v x[r, i1, q] y[r, i2]
+ * (y shared by the channels).  Any record set is allowed, e.g. several paths
+ * sent to one output block (collapsed output multiplicities).  Layouts:
+ * x [rows, d_x, C], y [rows, d_y, C] or [rows, d_y], z [rows, d_z, C]; any
+ * C >= 1.  Records are copied at create (index errors: E3_ERR_INDEX_OUT_OF_RANGE);
+ * operand rows must fit 64 KiB of staging per 64 channels (else
+ * E3_ERR_UNSUPPORTED).  Tables are uploaded to the device on first use.
+ * e3_tpg_bwd (eq. tp-bwd): dx = tensor_product(C^{i1}_{i2 i0}, y, dz) and
+ *   dy = tensor_product(C^{i2}_{i1 i0}, x, dz), summed over the channels when y
+ *   is shared (then ws holds per-slab partials, e3_tpg_workspace_size bytes). */
+typedef struct e3_tpg e3_tpg;
+e3_status e3_tpg_create(int d_x, int d_y, int d_z, int64_t nnz, const int32_t* i0, const int32_t* i1,
+                        const int32_t* i2, const float* val, int y_per_channel, e3_tpg** out);
+e3_status e3_tpg_destroy(e3_tpg* tpg);
+e3_status e3_tpg_fwd(e3_tpg* tpg, const float* x, const float* y, float* z, int64_t rows, int C, e3_stream stream);
+e3_status e3_tpg_workspace_size(const e3_tpg* tpg, int64_t rows, int C, size_t* bwd_bytes);
+e3_status e3_tpg_bwd(e3_tpg* tpg, const float* x, const float* y, const float* dz, float* dx, float* dy, void* ws,
+                     size_t ws_bytes, int64_t rows, int C, e3_stream stream);
+
 /* Per-kernel timing (instrumentation).  While enabled, every kernel the
  * library launches is bracketed by two HIP events on the caller's stream.
  * e3_timing_read waits for the recorded events and returns, per kernel name

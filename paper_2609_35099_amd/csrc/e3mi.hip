@@ -22,6 +22,7 @@
 #include <hipcub/hipcub.hpp>
 
 #include <algorithm>
+#include <array>
 #include <cstdint>
 #include <cstring>
 #include <map>
@@ -694,12 +695,18 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
         // an absent output has row size 0: its stores are dropped by the
         // buffer range check, with no branch in the contraction code
         const RowBuf dsb = row_buf(a.ds + e * V::NP * C, a.ds_row, q, C);
+        // accumulating: the old ds of this edge is loaded before the contraction
+        // starts, so that its latency is hidden behind the arithmetic
+        float old[ACC ? B::NPATH : 1][CPL];
+        if constexpr (ACC) {
+#pragma unroll
+          for (int i = 0; i < B::NPATH; ++i) bld<CPL>(dsb, B::PATH[i], old[i]);
+        }
         auto st = [&](int pl, const float (&v)[CPL]) {
           if constexpr (ACC) {
             float o[CPL];
-            bld<CPL>(dsb, B::PATH[pl], o);
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) o[c] += v[c];
+            for (int c = 0; c < CPL; ++c) o[c] = old[pl][c] + v[c];
             bst<CPL, kNT>(dsb, B::PATH[pl], o);
           } else {
             bst<CPL, kNT>(dsb, B::PATH[pl], v);
@@ -1480,6 +1487,82 @@ __global__ __launch_bounds__(256) void k_lin_dw_sum(const float* __restrict__ dW
   float s = 0.0f;
   for (int c = 0; c < kLinChunks; ++c) s += dWp[((int64_t)p * kLinChunks + c) * per + e];
   dW[pairs[p].w_off + e] = s;
+}
+
+
+// ------------------------------------------------------------ generic records
+// Tensor product with caller-supplied records (App. E.2's unfolded form):
+//   out[r, o, q] = sum over the records of segment o of v A[r, a, q] B[r, b, (q)]
+// Records are streamed through the scalar unit (uniform loads), segment by
+// segment; the two operand rows of the wave's (row, 64-channel slab) are staged
+// in LDS.  The backward is the same kernel on permuted record tables (eq.
+// tp-bwd); with RED the outputs are summed over the channels (a shared y's
+// cotangent): per-slab partials in fixed lane order, then k_tpg_sum.
+struct TpgRec {
+  int a, b;
+  float v;
+  int pad;
+};
+struct TpgArgs {
+  const float* A;
+  const float* B;
+  float* out;
+  float* part;  // RED: [rows][nslab][dout]
+  const int* seg;
+  const TpgRec* recs;
+  int64_t rows;
+  int C, nslab, dA, dB, dout;
+};
+
+template <bool BSH, bool RED>
+__global__ __launch_bounds__(kWave) void k_tpg(TpgArgs a) {
+  extern __shared__ float lds[];
+  const int sl = blockIdx.x % a.nslab;
+  const int64_t r = blockIdx.x / a.nslab;
+  const int lane = threadIdx.x, q = sl * kWave + lane;
+  const bool act = q < a.C;
+  float* sA = lds;
+  float* sB = sA + a.dA * kWave;
+  float* sP = sB + (BSH ? ((a.dB + 3) & ~3) : a.dB * kWave);
+  for (int i = 0; i < a.dA; ++i) sA[i * kWave + lane] = act ? a.A[(r * a.dA + i) * a.C + q] : 0.0f;
+  if constexpr (BSH) {
+    for (int i = lane; i < a.dB; i += kWave) sB[i] = a.B[r * a.dB + i];
+  } else {
+    for (int i = 0; i < a.dB; ++i) sB[i * kWave + lane] = act ? a.B[(r * a.dB + i) * a.C + q] : 0.0f;
+  }
+  __syncthreads();
+  for (int o = 0; o < a.dout; ++o) {
+    float acc = 0.0f;
+    const int k1 = a.seg[o + 1];
+    for (int k = a.seg[o]; k < k1; ++k) {
+      const TpgRec rc = a.recs[k];
+      const float bv = BSH ? sB[rc.b] : sB[rc.b * kWave + lane];
+      acc = fmaf(rc.v * sA[rc.a * kWave + lane], bv, acc);
+    }
+    if constexpr (RED)
+      sP[o * kWave + lane] = acc;
+    else if (act)
+      a.out[(r * a.dout + o) * a.C + q] = acc;
+  }
+  if constexpr (RED) {
+    __syncthreads();
+    for (int o = lane; o < a.dout; o += kWave) {
+      float t = 0.0f;
+      for (int l = 0; l < kWave; ++l) t += sP[o * kWave + l];
+      a.part[(r * a.nslab + sl) * a.dout + o] = t;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_tpg_sum(const float* __restrict__ part, float* __restrict__ out,
+                                                  int64_t rows, int nslab, int dout) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * dout) return;
+  const int64_t r = i / dout;
+  const int o = (int)(i % dout);
+  float t = 0.0f;
+  for (int sl = 0; sl < nslab; ++sl) t += part[(r * nslab + sl) * dout + o];
+  out[i] = t;
 }
 
 // ------------------------------------------------------------ graph
@@ -2594,6 +2677,182 @@ e3_status e3_linear_bwd(e3_linear* L, const float* x, const float* W, const floa
                        dW, (int)L->pairs.size(), per);
     E3_HIP(hipGetLastError());
   }
+  return E3_OK;
+}
+
+}  // extern "C"
+
+// ============================================================ generic records (host)
+struct e3_tpg {
+  int d_x = 0, d_y = 0, d_z = 0, ypc = 0;
+  // record tables: forward (out z, A x, B y), dx (out x, A dz, B y), dy (out y, A x, B dz)
+  struct Table {
+    std::vector<int> seg;
+    std::vector<TpgRec> recs;
+    size_t off_seg = 0, off_recs = 0;
+  } t[3];
+  std::mutex mu;
+  char* dev = nullptr;
+};
+
+namespace {
+e3_tpg::Table tpg_table(int d_out, const std::vector<std::array<int, 3>>& key, const std::vector<float>& val) {
+  // key = (out, a, b); stable order by (out, a, b)
+  std::vector<size_t> ord(key.size());
+  for (size_t i = 0; i < ord.size(); ++i) ord[i] = i;
+  std::stable_sort(ord.begin(), ord.end(), [&](size_t u, size_t v) { return key[u] < key[v]; });
+  e3_tpg::Table T;
+  T.seg.assign(d_out + 1, 0);
+  for (size_t i : ord) {
+    T.recs.push_back(TpgRec{key[i][1], key[i][2], val[i], 0});
+    ++T.seg[key[i][0] + 1];
+  }
+  for (int o = 0; o < d_out; ++o) T.seg[o + 1] += T.seg[o];
+  return T;
+}
+
+e3_status tpg_upload(e3_tpg* G, hipStream_t st) {
+  std::lock_guard<std::mutex> lk(G->mu);
+  if (G->dev) return E3_OK;
+  size_t off = 0;
+  for (auto& T : G->t) {
+    T.off_seg = off;
+    off = align256(off + T.seg.size() * sizeof(int));
+    T.off_recs = off;
+    off = align256(off + T.recs.size() * sizeof(TpgRec) + 1);
+  }
+  std::vector<char> host(off, 0);
+  for (auto& T : G->t) {
+    std::memcpy(host.data() + T.off_seg, T.seg.data(), T.seg.size() * sizeof(int));
+    if (!T.recs.empty()) std::memcpy(host.data() + T.off_recs, T.recs.data(), T.recs.size() * sizeof(TpgRec));
+  }
+  char* d = nullptr;
+  E3_HIP(hipMalloc(&d, off));
+  hipError_t e = hipMemcpyAsync(d, host.data(), off, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    g_last_error = std::string("record tables upload: ") + hipGetErrorString(e);
+    (void)hipFree(d);
+    return E3_ERR_HIP;
+  }
+  G->dev = d;
+  return E3_OK;
+}
+
+size_t tpg_lds(int dA, int dB, int dout, bool bsh, bool red) {
+  return ((size_t)dA * kWave + (bsh ? ((dB + 3) & ~3) : (size_t)dB * kWave) + (red ? (size_t)dout * kWave : 0)) *
+         sizeof(float);
+}
+constexpr size_t kTpgMaxLds = 64 * 1024;
+
+e3_status tpg_run(const e3_tpg* G, int which, const float* A, int dA, const float* B, int dB, bool bsh, float* out,
+                  float* part, bool red, int64_t rows, int C, const char* name, hipStream_t st) {
+  const e3_tpg::Table& T = G->t[which];
+  TpgArgs a{};
+  a.A = A, a.B = B, a.out = out, a.part = part;
+  a.seg = reinterpret_cast<const int*>(G->dev + T.off_seg);
+  a.recs = reinterpret_cast<const TpgRec*>(G->dev + T.off_recs);
+  a.rows = rows, a.C = C, a.nslab = (C + kWave - 1) / kWave, a.dA = dA, a.dB = dB;
+  a.dout = (int)T.seg.size() - 1;
+  const size_t lds = tpg_lds(dA, dB, a.dout, bsh, red);
+  const int64_t grid = rows * a.nslab;
+  if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
+  TimedLaunch t_(name, st);
+  if (bsh && red)
+    hipLaunchKernelGGL((k_tpg<true, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+  else if (bsh)
+    hipLaunchKernelGGL((k_tpg<true, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+  else if (red)
+    hipLaunchKernelGGL((k_tpg<false, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+  else
+    hipLaunchKernelGGL((k_tpg<false, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+}  // namespace
+
+extern "C" {
+
+e3_status e3_tpg_create(int d_x, int d_y, int d_z, int64_t nnz, const int32_t* i0, const int32_t* i1,
+                        const int32_t* i2, const float* val, int y_per_channel, e3_tpg** out) {
+  if (!out) return E3_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (d_x < 1 || d_y < 1 || d_z < 1 || nnz < 0 || nnz > (1 << 24) || (nnz > 0 && (!i0 || !i1 || !i2 || !val)))
+    return E3_ERR_INVALID_ARG;
+  for (int64_t k = 0; k < nnz; ++k)
+    if (i0[k] < 0 || i0[k] >= d_z || i1[k] < 0 || i1[k] >= d_x || i2[k] < 0 || i2[k] >= d_y)
+      return E3_ERR_INDEX_OUT_OF_RANGE;
+  const bool bsh = !y_per_channel;
+  if (tpg_lds(d_x, d_y, d_z, bsh, false) > kTpgMaxLds || tpg_lds(d_z, d_y, d_x, bsh, false) > kTpgMaxLds ||
+      tpg_lds(d_x, d_z, d_y, false, bsh) > kTpgMaxLds) {
+    g_last_error = "record tensor product: operand rows do not fit the 64 KiB staging limit";
+    return E3_ERR_UNSUPPORTED;
+  }
+  e3_tpg* G = new (std::nothrow) e3_tpg();
+  if (!G) return E3_ERR_ALLOC;
+  G->d_x = d_x, G->d_y = d_y, G->d_z = d_z, G->ypc = y_per_channel ? 1 : 0;
+  std::vector<std::array<int, 3>> kf(nnz), kx(nnz), ky(nnz);
+  std::vector<float> v(val, val + nnz);
+  for (int64_t k = 0; k < nnz; ++k) {
+    kf[k] = {i0[k], i1[k], i2[k]};  // z[i0] from x[i1], y[i2]
+    kx[k] = {i1[k], i0[k], i2[k]};  // dx[i1] from dz[i0], y[i2]   (records (i1, i2, i0) of eq. tp-bwd)
+    ky[k] = {i2[k], i1[k], i0[k]};  // dy[i2] from x[i1], dz[i0]   (records (i2, i1, i0))
+  }
+  G->t[0] = tpg_table(d_z, kf, v);
+  G->t[1] = tpg_table(d_x, kx, v);
+  G->t[2] = tpg_table(d_y, ky, v);
+  *out = G;
+  return E3_OK;
+}
+
+e3_status e3_tpg_destroy(e3_tpg* G) {
+  if (!G) return E3_OK;
+  if (G->dev) (void)hipFree(G->dev);
+  delete G;
+  return E3_OK;
+}
+
+e3_status e3_tpg_fwd(e3_tpg* G, const float* x, const float* y, float* z, int64_t rows, int C, e3_stream stream) {
+  if (!G || rows < 0 || C < 1) return E3_ERR_INVALID_ARG;
+  if (rows == 0) return E3_OK;
+  if (!x || !y || !z) return E3_ERR_INVALID_ARG;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  e3_status s = tpg_upload(G, st);
+  if (s != E3_OK) return s;
+  return tpg_run(G, 0, x, G->d_x, y, G->d_y, !G->ypc, z, nullptr, false, rows, C, "tpg_fwd", st);
+}
+
+e3_status e3_tpg_workspace_size(const e3_tpg* G, int64_t rows, int C, size_t* bwd_bytes) {
+  if (!G || rows < 0 || C < 1 || !bwd_bytes) return E3_ERR_INVALID_ARG;
+  *bwd_bytes = G->ypc ? 0 : align256((size_t)rows * ((C + kWave - 1) / kWave) * G->d_y * sizeof(float));
+  return E3_OK;
+}
+
+e3_status e3_tpg_bwd(e3_tpg* G, const float* x, const float* y, const float* dz, float* dx, float* dy, void* ws,
+                     size_t ws_bytes, int64_t rows, int C, e3_stream stream) {
+  if (!G || rows < 0 || C < 1) return E3_ERR_INVALID_ARG;
+  if (rows == 0) return E3_OK;
+  if (!x || !y || !dz || !dx || !dy) return E3_ERR_INVALID_ARG;
+  size_t need = 0;
+  e3_status s = e3_tpg_workspace_size(G, rows, C, &need);
+  if (s != E3_OK) return s;
+  if (ws_bytes < need) return E3_ERR_WORKSPACE_TOO_SMALL;
+  if (need > 0 && !ws) return E3_ERR_INVALID_ARG;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if ((s = tpg_upload(G, st)) != E3_OK) return s;
+  // dx = tensor_product(C^{i1}_{i2 i0}, y, dz)
+  if ((s = tpg_run(G, 1, dz, G->d_z, y, G->d_y, !G->ypc, dx, nullptr, false, rows, C, "tpg_bwd_dx", st)) != E3_OK)
+    return s;
+  // dy = tensor_product(C^{i2}_{i1 i0}, x, dz), summed over channels when y is shared
+  if (G->ypc)
+    return tpg_run(G, 2, x, G->d_x, dz, G->d_z, false, dy, nullptr, false, rows, C, "tpg_bwd_dy", st);
+  float* part = reinterpret_cast<float*>(ws);
+  if ((s = tpg_run(G, 2, x, G->d_x, dz, G->d_z, false, nullptr, part, true, rows, C, "tpg_bwd_dy", st)) != E3_OK)
+    return s;
+  TimedLaunch t_("tpg_bwd_dy_sum", st);
+  hipLaunchKernelGGL(k_tpg_sum, dim3(blocks_for(rows * G->d_y, 256)), dim3(256), 0, st, part, dy, rows,
+                     (C + kWave - 1) / kWave, G->d_y);
+  E3_HIP(hipGetLastError());
   return E3_OK;
 }
 

@@ -65,6 +65,11 @@ SIGNATURES = {
     "e3_linear_fwd": (_I, [_P, _P, _P, _P, _I64, _P]),
     "e3_linear_workspace_size": (_I, [_P, ct.POINTER(ct.c_size_t)]),
     "e3_linear_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, _P]),
+    "e3_tpg_create": (_I, [ct.c_int, ct.c_int, ct.c_int, _I64, _P, _P, _P, _P, ct.c_int, ct.POINTER(ct.c_void_p)]),
+    "e3_tpg_destroy": (_I, [_P]),
+    "e3_tpg_fwd": (_I, [_P, _P, _P, _P, _I64, ct.c_int, _P]),
+    "e3_tpg_workspace_size": (_I, [_P, _I64, ct.c_int, ct.POINTER(ct.c_size_t)]),
+    "e3_tpg_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, ct.c_int, _P]),
     "e3_conv_fwd_y": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P]),
     "e3_conv_bwd_y": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_int, _P, ct.c_size_t, _P]),
     "e3_conv_bwd2": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
@@ -377,6 +382,54 @@ def conv_bwd2(plan: Plan, graph: Graph, x, y, s, dm, ddx, ddy, dds, ws=None, str
                               _ptr(gs, "gs", (E, plan.P, plan.C)), _ptr(gdm, "gdm", (N, plan.D_out, plan.C)),
                               ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd2")
     return gx, gy, gs, gdm
+
+
+class RecordTP:
+    """Tensor product with caller-supplied records (i0, i1, i2, value)."""
+
+    def __init__(self, d_x: int, d_y: int, d_z: int, i0, i1, i2, val, y_per_channel: bool):
+        i0, i1, i2 = (np.ascontiguousarray(a, dtype=np.int32) for a in (i0, i1, i2))
+        val = np.ascontiguousarray(val, dtype=np.float32)
+        h = ct.c_void_p()
+        _check(lib().e3_tpg_create(d_x, d_y, d_z, val.shape[0], i0.ctypes.data_as(ct.c_void_p),
+                                   i1.ctypes.data_as(ct.c_void_p), i2.ctypes.data_as(ct.c_void_p),
+                                   val.ctypes.data_as(ct.c_void_p), 1 if y_per_channel else 0, ct.byref(h)),
+               "e3_tpg_create")
+        self.handle = h
+        self.d_x, self.d_y, self.d_z, self.ypc = d_x, d_y, d_z, bool(y_per_channel)
+
+    def close(self):
+        if getattr(self, "handle", None) and self.handle.value:
+            lib().e3_tpg_destroy(self.handle)
+            self.handle = ct.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _yshape(self, R, C):
+        return (R, self.d_y, C) if self.ypc else (R, self.d_y)
+
+    def forward(self, x, y, out=None, stream=None):
+        R, _, C = x.shape
+        out = _empty((R, self.d_z, C)) if out is None else out
+        _check(lib().e3_tpg_fwd(self.handle, _ptr(x, "x", (R, self.d_x, C)), _ptr(y, "y", self._yshape(R, C)),
+                                _ptr(out, "z", (R, self.d_z, C)), R, C, _stream(stream)), "e3_tpg_fwd")
+        return out
+
+    def backward(self, x, y, dz, stream=None):
+        R, _, C = x.shape
+        dx, dy = _empty((R, self.d_x, C)), _empty(self._yshape(R, C))
+        b = ct.c_size_t()
+        _check(lib().e3_tpg_workspace_size(self.handle, R, C, ct.byref(b)), "e3_tpg_workspace_size")
+        ws = workspace(b.value)
+        _check(lib().e3_tpg_bwd(self.handle, _ptr(x, "x", (R, self.d_x, C)), _ptr(y, "y", self._yshape(R, C)),
+                                _ptr(dz, "dz", (R, self.d_z, C)), _ptr(dx, "dx", (R, self.d_x, C)),
+                                _ptr(dy, "dy", self._yshape(R, C)), ct.c_void_p(ws.data_ptr()), ws.numel(), R, C,
+                                _stream(stream)), "e3_tpg_bwd")
+        return dx, dy
 
 
 class Linear:

@@ -159,3 +159,24 @@ def test_linear_descriptor_matches_oracle_plan():
     n = ct.c_size_t()
     assert Ll.e3_linear_workspace_size(L.handle, ct.byref(n)) == 0 and n.value > 0
     assert Ll.e3_linear_bwd(L.handle, None, None, None, None, None, None, 0, 5, None) == 1
+
+
+def test_record_tp_create_checks():
+    """Record tensor product descriptor: index, size and staging-limit checks (host only)."""
+    L = e3mi.lib()
+    h = ct.c_void_p()
+    i = (ct.c_int32 * 2)(0, 1)
+    v = (ct.c_float * 2)(1.0, 2.0)
+    assert L.e3_tpg_create(4, 4, 4, 2, i, i, i, v, 1, ct.byref(h)) == 0
+    assert L.e3_tpg_destroy(h) == 0
+    bad = (ct.c_int32 * 2)(0, 4)
+    assert L.e3_tpg_create(4, 4, 4, 2, bad, i, i, v, 1, ct.byref(h)) == 3
+    assert L.e3_tpg_create(0, 4, 4, 2, i, i, i, v, 1, ct.byref(h)) == 1
+    assert L.e3_tpg_create(4, 4, 4, 2, None, i, i, v, 1, ct.byref(h)) == 1
+    assert L.e3_tpg_create(4, 4, 400, 2, i, i, i, v, 1, ct.byref(h)) == 2     # 400 rows x 64 lanes > 64 KiB
+    assert L.e3_tpg_create(4, 4, 4, 0, None, None, None, None, 0, ct.byref(h)) == 0
+    n = ct.c_size_t()
+    assert L.e3_tpg_workspace_size(h, 10, 128, ct.byref(n)) == 0 and n.value >= 10 * 2 * 4 * 4
+    assert L.e3_tpg_fwd(h, None, None, None, 0, 8, None) == 0
+    assert L.e3_tpg_fwd(h, None, None, None, 3, 8, None) == 1
+    assert L.e3_tpg_destroy(h) == 0

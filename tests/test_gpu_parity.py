@@ -738,3 +738,77 @@ def test_linear_config4_sampled(e3, which):
     print("rel-L2", errs, flush=True)
     for k, v in errs.items():
         assert v < TOL, (k, v)
+
+
+# ---------------------------------------------------------------- caller-supplied records
+from oracle import cg as ocg  # noqa: E402
+from oracle import generic as ogeneric  # noqa: E402
+
+
+def _layout_records(lay):
+    recs = ocg.coo_records(lay)
+    return tuple(np.array([r[k] for r in recs]) for k in range(4))
+
+
+@pytest.mark.parametrize("case", ["layout-shared", "layout-perchannel", "random-shared", "random-perchannel",
+                                  "collapsed", "C7"])
+def test_record_tp_parity(e3, case):
+    import torch
+    _say("record tp", case)
+    rng = np.random.default_rng(61)
+    if case in ("layout-shared", "layout-perchannel", "C7"):
+        lay = oirreps.layout("8x0e+8x1o+8x2e+8x3o", 3, 3)
+        i0, i1, i2, v = _layout_records(lay)
+        dx_, dy_, dz_ = lay.d_in, lay.d_sh, lay.d_out
+        C = 7 if case == "C7" else 100
+    elif case == "collapsed":
+        lay = oirreps.layout("4x0e+4x1o", 2, 1)
+        i0, i1, i2, v = _layout_records(lay)
+        i0 = np.minimum(i0, 3)   # fold every output row past 3 onto row 3
+        dx_, dy_, dz_ = lay.d_in, lay.d_sh, 4
+        C = 64
+    else:
+        dx_, dy_, dz_, nnz = 11, 9, 23, 300
+        i0, i1, i2 = rng.integers(0, dz_, nnz), rng.integers(0, dx_, nnz), rng.integers(0, dy_, nnz)
+        v = rng.standard_normal(nnz)
+        C = 130
+    ypc = case.endswith("perchannel") or case == "C7"
+    R = 57
+    T = e3.RecordTP(dx_, dy_, dz_, i0, i1, i2, v.astype(np.float32), ypc)
+    x = rng.standard_normal((R, dx_, C)).astype(np.float32)
+    y = rng.standard_normal((R, dy_, C) if ypc else (R, dy_)).astype(np.float32)
+    dz = rng.standard_normal((R, dz_, C)).astype(np.float32)
+    vf = v.astype(np.float32).astype(np.float64)
+    z = to_np(T.forward(to_dev(x), to_dev(y)))
+    gdx, gdy = (to_np(t) for t in T.backward(to_dev(x), to_dev(y), to_dev(dz)))
+    rz = ogeneric.tp(i0, i1, i2, vf, x, y, dz_)
+    rdx, rdy = ogeneric.tp_bwd(i0, i1, i2, vf, x, y, dz)
+    errs = dict(z=rel_l2(z, rz), dx=rel_l2(gdx, rdx), dy=rel_l2(gdy, rdy))
+    print("rel-L2", errs, flush=True)
+    for k, e in errs.items():
+        assert e < TOL, (k, e)
+
+
+def test_record_tp_config2_matches_specialised(e3):
+    """Config 2 (200,000 rows, 128 channels, l <= 3) with the plan's own records:
+    the record kernel against the oracle on sampled rows, and against the
+    specialised tensor product on all rows."""
+    import torch
+    _say("record tp config 2")
+    cfg = synth.CONFIGS[2]
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    lay = layout_of(cfg)
+    i0, i1, i2, v = _layout_records(lay)
+    T = e3.RecordTP(lay.d_in, lay.d_sh, lay.d_out, i0, i1, i2, v.astype(np.float32), False)
+    x, u, w = synth.tp_inputs(cfg)
+    y = osh.sh_unit(3, u.astype(np.float64)).astype(np.float32)
+    xs, ys = to_dev(x), to_dev(y)
+    z = T.forward(xs, ys)
+    ones = torch.ones((x.shape[0], plan.P, plan.C), device="cuda")
+    zs = e3.tp_fwd(plan, xs, ys, ones)
+    torch.cuda.synchronize()
+    assert rel_l2(to_np(z), to_np(zs)) < TOL
+    rows = np.concatenate([[0, x.shape[0] - 1], np.random.default_rng(62).integers(0, x.shape[0], 30)])
+    ri = torch.as_tensor(rows, device="cuda")
+    ref = ogeneric.tp(i0, i1, i2, v.astype(np.float32).astype(np.float64), x[rows], y[rows], lay.d_out)
+    assert rel_l2(to_np(z[ri]), ref) < TOL
