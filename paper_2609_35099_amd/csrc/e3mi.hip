@@ -194,7 +194,14 @@ __device__ __forceinline__ RowBuf row_buf(const float* base, int64_t nbytes, int
   return b;
 }
 
-constexpr int kNT = 2;  // non-temporal (streamed once)
+constexpr int kNT = 2;  // non-temporal loads of data streamed once
+// Stores of streamed outputs: non-temporal.  A pure write stream runs faster
+// with plain stores on MI355X, but in these mixed read/write kernels plain
+// stores were measured equal or slower (TP backward 3.86 ms against 3.44 ms).
+#ifndef E3_STORE_AUX
+#define E3_STORE_AUX 2
+#endif
+constexpr int kST = E3_STORE_AUX;
 
 template <int CPL, int AUX = 0>
 __device__ __forceinline__ void bld(const RowBuf& b, int row, float (&v)[CPL]) {
@@ -365,7 +372,7 @@ __global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const
     for (int i = 0; i < T::NXR; ++i) bld<CPL, kNT>(xb, T::XROW[i], xv[i]);
 #pragma unroll
     for (int i = 0; i < T::NPATH; ++i) bld<CPL, kNT>(wb, T::PATH[i], wv[i]);
-    auto st = [&](int row, const float (&v)[CPL]) { bst<CPL, kNT>(zb, row, v); };
+    auto st = [&](int row, const float (&v)[CPL]) { bst<CPL, kST>(zb, row, v); };
     T::template rows<CPL>(sA + j * T::NA, xv, wv, st);
   }
 }
@@ -429,7 +436,7 @@ __device__ __forceinline__ void tpb_task(const TpbArgs& a, int64_t r0, int sl, f
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
       const RowBuf dwb = row_buf(a.dw + r * V::NP * C, (int64_t)V::NP * C * 4, q, C);
-      auto st = [&](int pl, const float (&v)[CPL]) { bst<CPL, kNT>(dwb, B::PATH[pl], v); };
+      auto st = [&](int pl, const float (&v)[CPL]) { bst<CPL, kST>(dwb, B::PATH[pl], v); };
       float dyl[V::D_SH];
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0f;
@@ -438,7 +445,7 @@ __device__ __forceinline__ void tpb_task(const TpbArgs& a, int64_t r0, int sl, f
       for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
       const RowBuf dxb = row_buf(a.dx + r * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
-      for (int i = 0; i < B::NXR; ++i) bst<CPL, kNT>(dxb, B::XROW[i], t[i]);
+      for (int i = 0; i < B::NXR; ++i) bst<CPL, kST>(dxb, B::XROW[i], t[i]);
     }
     const float tot = wave_reduce16(dy, lane);
     if ((lane & 3) == 0) a.DY[((r * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
@@ -605,7 +612,7 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
       }
     }
 #pragma unroll
-    for (int i = 0; i < F::NROW; ++i) bst<CPL, kNT>(mb, F::OROW[i], acc[i]);
+    for (int i = 0; i < F::NROW; ++i) bst<CPL, kST>(mb, F::OROW[i], acc[i]);
   }
 }
 
@@ -707,9 +714,9 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
             float o[CPL];
 #pragma unroll
             for (int c = 0; c < CPL; ++c) o[c] = old[pl][c] + v[c];
-            bst<CPL, kNT>(dsb, B::PATH[pl], o);
+            bst<CPL, kST>(dsb, B::PATH[pl], o);
           } else {
-            bst<CPL, kNT>(dsb, B::PATH[pl], v);
+            bst<CPL, kST>(dsb, B::PATH[pl], v);
           }
         };
         float dyl[V::D_SH];
@@ -808,7 +815,7 @@ __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__
   }
 #pragma unroll
   for (int k = 0; k < kDxVec; ++k)
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, acc[k]), o, off, k * kWave * 16, kNT);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, acc[k]), o, off, k * kWave * 16, kST);
 }
 
 // dvec of each live edge from its harmonic cotangent (summed over groups).
@@ -984,7 +991,7 @@ __device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, f
   if (act) {
     const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
-    for (int i = 0; i < F::NROW; ++i) bst<1, kNT>(mb, F::OROW[i], acc[i]);
+    for (int i = 0; i < F::NROW; ++i) bst<1, kST>(mb, F::OROW[i], acc[i]);
   }
 }
 
@@ -1066,7 +1073,7 @@ __device__ __forceinline__ void bwd_rad_task(const ConvArgs& a, int b, int sl, f
         for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
         const int64_t e = __builtin_amdgcn_readlane(my_e, j);
         const RowBuf dsb = row_buf(a.ds + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
-        auto st = [&](int pl, const float (&v)[1]) { bst<1, kNT>(dsb, B::PATH[pl], v); };
+        auto st = [&](int pl, const float (&v)[1]) { bst<1, kST>(dsb, B::PATH[pl], v); };
         float dyl[V::D_SH];
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0f;
