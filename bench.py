@@ -102,6 +102,66 @@ def tp_bwd_bytes(R, C, D_in, D_sh, D_out, P):
     return R * (2 * D_in * C + 2 * D_sh + 2 * P * C + D_out * C) * 4
 
 
+# The paper's e3j numbers for its channel sweep on an H100 (GB/s, channels 64..1024;
+# None where the kernel does not run).  Context only: other hardware, other graphs.
+PAPER_H100_GBPS = {
+    "lmax2": {"fwd_cuda": [625, 955, 913, 956, 880], "fwd_pallas": [None, 1621, 1669, 1716, 1871],
+              "bwd_cuda": [446, 709, 638, 560, 623], "bwd_pallas": [None, 1267, 1292, 1319, 1328]},
+    "lmax3": {"fwd_cuda": [389, 569, 573, 562, 538], "fwd_pallas": [None, 1818, 1859, 2074, 2067],
+              "bwd_cuda": [310, 423, 402, 317, 183], "bwd_pallas": [None, 1407, 1432, 1483, 1599]},
+}
+
+
+def sweep(args, dev):
+    """Forward and backward throughput (GB/s of inputs + outputs, the paper's
+    definition) over C = 64..1024 with N*C = 2^22 (l_max 2) or 2^21 (l_max 3)."""
+    import torch
+    from paper_2609_35099_amd import e3mi
+    rows = []
+    for lmax in (2, 3):
+        for C in (64, 128, 256, 512, 1024):
+            scfg = synth.sweep_config(lmax, C)
+            g = synth.graph(scfg)
+            N, E = g.n_nodes, g.sender.shape[0]
+            plan = e3mi.Plan(scfg.irreps, scfg.lmax_sh, scfg.lmax_out)
+            G = e3mi.Graph(torch.from_numpy(g.sender).to(dev), torch.from_numpy(g.receiver).to(dev), N)
+            x = synth.normal_device(scfg.cid, 1, (N, plan.D_in, C), dev)
+            s = synth.normal_device(scfg.cid, 2, (E, plan.P, C), dev)
+            dm = synth.normal_device(scfg.cid, 3, (N, plan.D_out, C), dev)
+            vs = torch.from_numpy(g.vec).to(dev)
+            m = torch.empty((N, plan.D_out, C), dtype=torch.float32, device=dev)
+            dx = torch.empty_like(x)
+            dvec = torch.empty_like(vs)
+            ds = torch.empty_like(s)
+            ws = e3mi.workspace(e3mi.conv_workspace_size(plan, G)[1])
+            for _ in range(2):
+                e3mi.conv_fwd(plan, G, x, vs, s, out=m)
+                e3mi.conv_bwd(plan, G, x, vs, s, dm, dx=dx, dvec=dvec, ds=ds, ws=ws)
+            torch.cuda.synchronize()
+            f0, f1, b1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            tf = tb = 0.0
+            for _ in range(5):
+                f0.record()
+                e3mi.conv_fwd(plan, G, x, vs, s, out=m)
+                f1.record()
+                e3mi.conv_bwd(plan, G, x, vs, s, dm, dx=dx, dvec=dvec, ds=ds, ws=ws)
+                b1.record()
+                torch.cuda.synchronize()
+                tf += f0.elapsed_time(f1) / 5
+                tb += f1.elapsed_time(b1) / 5
+            _, fb, bb = conv_bytes(N, E, C, plan.D_in, plan.D_out, plan.P)
+            rows.append({"lmax": lmax, "channels": C, "n_nodes": N, "n_edges": E,
+                         "avg_neighbours": round(E / N, 1), "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4),
+                         "fwd_GBps": round(fb / (tf * 1e-3) / 1e9, 1), "bwd_GBps": round(bb / (tb * 1e-3) / 1e9, 1)})
+            log(f"sweep l_max {lmax} C {C}: N {N} E {E}: fwd {rows[-1]['fwd_GBps']} GB/s, "
+                f"bwd {rows[-1]['bwd_GBps']} GB/s")
+            del x, s, dm, m, dx, dvec, ds, ws, G
+            torch.cuda.empty_cache()
+    return {"definition": "GB/s = (inputs + outputs) / time, per pass; water boxes with ~45 neighbours; "
+                          "N*C = 2^22 at l_max 2, 2^21 at l_max 3; x = C x (0e+1o+..); N(0,1) weights",
+            "rows": rows, "paper_h100_GBps_context": PAPER_H100_GBPS}
+
+
 def cpu_baseline(cfg, g, x, dm, seconds=12.0):
     """The fp64 oracle on the host cores, on a bounded sample of the same workload:
     forward for sampled receivers and backward for sampled senders and edges."""
@@ -153,6 +213,9 @@ def main():
     ap.add_argument("--only", choices=["all", "conv", "radial", "bwd2", "linear", "tp"], default="all")
     ap.add_argument("--order", choices=["generated", "cell"], default="generated",
                     help="atom order of the water box: as generated (spatially random) or cell-sorted")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also run the channel sweep at fixed node x channel count (the shape of the paper's "
+                         "convolution throughput table); generates ten water boxes first")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one plain 2 GiB device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -461,6 +524,9 @@ def main():
         rtp.close()
         del tz
         del tdz, tdx, tdw, tdy, tws, txd, twd, ty
+
+    if args.sweep:
+        out["sweep"] = sweep(args, dev)
 
     if args.copy_probe:
         n = (2 << 30) // 4

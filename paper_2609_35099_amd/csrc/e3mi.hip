@@ -916,9 +916,12 @@ __device__ __forceinline__ void stage_h(const ConvArgs& a, int lane, int n, int 
     for (int j = 0; j < a.K; ++j) sH[lane * kRadKMax + j] = lane < n ? a.h[(int64_t)my_e * a.K + j] : 0.0f;
 }
 
-template <class V, int G, int KR>
+template <class V, int G, int KR0>
 __device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, float* sA, float* sH) {
   using F = typename V::template FG<G>;
+  // W stays in registers only where the group's estimated footprint (sums,
+  // W, four edges of s, two x buffers) leaves room; otherwise it is re-read
+  constexpr int KR = (KR0 > 0 && F::NROW + F::NPATH * (KR0 + 4) + 2 * F::NXR <= 230) ? KR0 : 0;
   const int lane = threadIdx.x;
   int ch0, lanes;
   slab_of<1>(a.C, sl, ch0, lanes);

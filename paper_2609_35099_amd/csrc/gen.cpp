@@ -455,6 +455,7 @@ int main(int argc, char** argv) {
       {{0, 1, 2}, 3, 3, false},
       {{0, 1}, 3, 3, false},
       {{0, 1, 2, 3}, 3, 3, false},
+      {{0, 1, 2}, 2, 2, false},
   };
   // Forward groups: contiguous paths balanced on per-channel FMA work, each
   // within a register budget (per channel of a lane: accumulators + two

@@ -55,6 +55,18 @@ class Config:
     rows: int = 0      # tensor product rows (config 2)
     weights: str = "normal"   # "normal" or "bessel"
     edge_order: str = "receiver"
+    r_cut: float = R_CUT
+
+
+def sweep_config(lmax: int, channels: int) -> Config:
+    """Channel sweep at a fixed product of node count and channel count (2^21 at
+    l_max 3, 2^22 at l_max 2) on water boxes with ~45 neighbours per atom
+    (r_c = 4.75 A at liquid density): x = C x (0e+1o+...+l_max), harmonics and
+    outputs up to l_max, N(0,1) edge weights."""
+    n_atoms = (1 << (21 if lmax == 3 else 22)) // channels
+    irreps = "+".join(f"{channels}x{l}{'e' if l % 2 == 0 else 'o'}" for l in range(lmax + 1))
+    return Config(100 + 10 * lmax + channels.bit_length(), "conv", irreps, lmax, lmax, channels,
+                  n_mol=n_atoms // 3, r_cut=4.75)
 
 
 CONFIGS = {
@@ -259,7 +271,7 @@ def graph(cfg: Config, order: str = "generated") -> Graph:
         pos, L = water_box(cfg.cid, cfg.n_mol)
         if order == "cell":
             pos = pos[cell_order(pos, L, cfg.n_mol)]
-        i, j, d = _pairs_within(pos, L, R_CUT)
+        i, j, d = _pairs_within(pos, L, cfg.r_cut)
         box = L
         n = pos.shape[0]
     # both directions: edge (i -> j) carries pos[j]-pos[i]; (j -> i) the negative

@@ -235,6 +235,9 @@ def test_conv_config1_full(e3):
     ("128x0e+128x1o", 3, 3, 200, 4000, -1),
     ("16x0e+16x1o+16x2e", 3, 3, 40, 600, 3),
     ("128x0e+128x1o+128x2e", 3, 3, 50, 900, -1),
+    ("32x0e+32x1o+32x2e", 2, 2, 60, 900, -1),          # l_max 2 variant
+    ("256x0e+256x1o+256x2e", 2, 2, 30, 300, 4),
+    ("1024x0e+1024x1o+1024x2e+1024x3o", 3, 3, 12, 60, -1),   # the largest channel count
 ])
 def test_conv_random_graphs_full(e3, irreps, lsh, lout, n, e, pad):
     _say("conv random", irreps, n, e, pad)
