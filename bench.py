@@ -30,6 +30,11 @@ import synth  # noqa: E402
 
 METRIC = "edges/sec conv fwd+bwd (fp32, lmax=3, 128ch) + achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
+# fp32 vector peak without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2 flop (FMA) x 2.4 GHz.
+# The kernels are built with packed fp32 disabled, so this is the attainable VALU peak;
+# the published 157.3 TFLOP/s counts the packed FMA.
+VALU_PEAK_TFLOPS = 78.6
+VALU_PEAK_PACKED_TFLOPS = 157.3
 
 
 def log(*a):
@@ -76,6 +81,37 @@ def source_hash() -> str:
     for f in KERNEL_SOURCES:
         h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()[:16]
+
+
+UTIL = os.path.join(ROOT, "profiles", "util_config4.txt")
+
+
+def counter_util(kernel: str, metric: str):
+    """A per-kernel utilisation figure (percent) from the committed rocprofv3
+    summary, or None if missing or taken on a different kernel source."""
+    try:
+        lines = open(UTIL).read().splitlines()
+    except OSError:
+        return None
+    want = source_hash()
+    for ln in lines:
+        p = ln.split()
+        if len(p) == 5 and p[0] == "util" and p[1] == kernel and p[2] == metric and p[3] == want:
+            return float(p[4])
+    return None
+
+
+def fma_counts(plan):
+    """FMA-equivalent VALU operations per edge and channel of the forward and
+    backward sweeps, counted as the kernel generator's cost model counts them:
+    forward: one per (output, x) pre-contraction entry plus the path-weight
+    product per output row; backward: two per entry (dm x product and x
+    cotangent), one per coupling coefficient, two per output row (s dm and its
+    use) and two per harmonic row of each path (ds and dy)."""
+    i0, i1, _, val = plan.records()
+    pairs = len(set(zip(i0.tolist(), i1.tolist())))
+    s2 = sum(2 * int(l2) + 1 for (_, l2, _, _, _, _, _) in plan.paths())
+    return pairs + plan.D_out, 2 * pairs + len(val) + 2 * plan.D_out + 2 * s2
 
 
 def counter_traffic(kernel: str):
@@ -299,6 +335,16 @@ def main():
             kernels[name] = entry
         dom = max((k for k in kernels if k in kb), key=lambda k: kernels[k]["ms"])
         ach = kb[dom] / (kernels[dom]["ms"] * 1e-3) / 1e9
+        f_fwd, f_bwd = fma_counts(plan)
+        kflops = {"conv_fwd": 2.0 * f_fwd * C * E, "conv_bwd_edges": 2.0 * f_bwd * C * E}
+        for name in kflops:
+            if name in kernels:
+                tf = kflops[name] / (kernels[name]["ms"] * 1e-3) / 1e12
+                kernels[name].update({"fma_per_edge_channel": f_fwd if name == "conv_fwd" else f_bwd,
+                                      "TFLOPs": round(tf, 2), "valu_frac": round(tf / VALU_PEAK_TFLOPS, 4),
+                                      "valu_busy_pct": counter_util(name, "VALUBusy")})
+        dom_tf = kflops[dom] / (kernels[dom]["ms"] * 1e-3) / 1e12
+        traffic = counter_traffic(dom)
         out.update({
             "value": E / (ms_step * 1e-3),
             "ms_per_step": ms_step,
@@ -308,9 +354,18 @@ def main():
                                    + ("" if args.order == "generated" else "; atoms cell-sorted"),
                        "n_nodes": N, "n_edges": E, "channels": C, "paths": plan.P,
                        "D_in": plan.D_in, "D_out": plan.D_out},
-            "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                         "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                         "traffic": counter_traffic(dom), "alg_bytes": kb[dom]},
+            # the dominant sweep is bound by VALU issue (packed fp32 is disabled in this build):
+            # its FMA-equivalent work against the unpacked vector peak, with the HBM view beside it
+            "roofline": {"bound": "alu", "kernel": dom, "achieved": round(dom_tf, 2), "peak": VALU_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(dom_tf / VALU_PEAK_TFLOPS, 4),
+                         "traffic": traffic, "flops": kflops[dom],
+                         "peak_packed_fp32": VALU_PEAK_PACKED_TFLOPS,
+                         "frac_of_packed": round(dom_tf / VALU_PEAK_PACKED_TFLOPS, 4),
+                         "valu_busy_pct": counter_util(dom, "VALUBusy"),
+                         "hbm": {"achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                 "frac": round(ach / HBM_PEAK_GBS, 4), "alg_bytes": kb[dom],
+                                 "counter_GBps": None if traffic is None else
+                                 round(traffic / (kernels[dom]["ms"] * 1e-3) / 1e9, 1)}},
             "step_alg_GBps": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9, 1),
             "step_alg_frac": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "fwd_alg_bytes": fwd_b, "bwd_alg_bytes": bwd_b,
