@@ -558,7 +558,7 @@ def main():
         log(f"tp_bwd: {tb_ms:.3f} ms, {out['tp_bwd']['alg_GBps']} GB/s")
         # the same product through the caller-supplied record path (the plan's records, unweighted)
         i0, i1, i2, rv = tplan.records()
-        rtp = e3mi.RecordTP(tplan.D_in, tplan.D_sh, tplan.D_out, i0, i1, i2, rv.astype(np.float32), False)
+        rtp = e3mi.RecordTP(tplan.D_in, tplan.D_sh, tplan.D_out, i0, i1, i2, rv, False)
         tz = torch.empty((R, tplan.D_out, tplan.C), dtype=torch.float32, device=dev)
         for _ in range(args.warmup):
             rtp.forward(txd, ty, out=tz)

@@ -256,15 +256,23 @@ e3_status e3_linear_bwd(e3_linear* lin, const float* x, const float* W, const fl
  * E3_ERR_UNSUPPORTED).  Tables are uploaded to the device on first use.
  * e3_tpg_bwd (eq. tp-bwd): dx = tensor_product(C^{i1}_{i2 i0}, y, dz) and
  *   dy = tensor_product(C^{i2}_{i1 i0}, x, dz), summed over the channels when y
- *   is shared (then ws holds per-slab partials, e3_tpg_workspace_size bytes). */
+ *   is shared (then ws holds per-slab partials, e3_tpg_workspace_size bytes,
+ *   enough for either precision).
+ * Record values are given in float64; the _f64 entry points compute in float64
+ * throughout (operand rows then fit half the staging limit), the others in
+ * float32 with the values rounded once. */
 typedef struct e3_tpg e3_tpg;
 e3_status e3_tpg_create(int d_x, int d_y, int d_z, int64_t nnz, const int32_t* i0, const int32_t* i1,
-                        const int32_t* i2, const float* val, int y_per_channel, e3_tpg** out);
+                        const int32_t* i2, const double* val, int y_per_channel, e3_tpg** out);
 e3_status e3_tpg_destroy(e3_tpg* tpg);
 e3_status e3_tpg_fwd(e3_tpg* tpg, const float* x, const float* y, float* z, int64_t rows, int C, e3_stream stream);
 e3_status e3_tpg_workspace_size(const e3_tpg* tpg, int64_t rows, int C, size_t* bwd_bytes);
 e3_status e3_tpg_bwd(e3_tpg* tpg, const float* x, const float* y, const float* dz, float* dx, float* dy, void* ws,
                      size_t ws_bytes, int64_t rows, int C, e3_stream stream);
+e3_status e3_tpg_fwd_f64(e3_tpg* tpg, const double* x, const double* y, double* z, int64_t rows, int C,
+                         e3_stream stream);
+e3_status e3_tpg_bwd_f64(e3_tpg* tpg, const double* x, const double* y, const double* dz, double* dx, double* dy,
+                         void* ws, size_t ws_bytes, int64_t rows, int C, e3_stream stream);
 
 /* Per-kernel timing (instrumentation).  While enabled, every kernel the
  * library launches is bracketed by two HIP events on the caller's stream.

@@ -28,6 +28,7 @@
 #include <map>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/e3mi.h"
@@ -1513,41 +1514,47 @@ struct TpgRec {
   float v;
   int pad;
 };
+struct TpgRec64 {
+  int a, b;
+  double v;
+};
+template <class T>
 struct TpgArgs {
-  const float* A;
-  const float* B;
-  float* out;
-  float* part;  // RED: [rows][nslab][dout]
+  const T* A;
+  const T* B;
+  T* out;
+  T* part;  // RED: [rows][nslab][dout]
   const int* seg;
-  const TpgRec* recs;
+  const typename std::conditional<sizeof(T) == 8, TpgRec64, TpgRec>::type* recs;
   int64_t rows;
   int C, nslab, dA, dB, dout;
 };
 
-template <bool BSH, bool RED>
-__global__ __launch_bounds__(kWave) void k_tpg(TpgArgs a) {
-  extern __shared__ float lds[];
+template <class T, bool BSH, bool RED>
+__global__ __launch_bounds__(kWave) void k_tpg(TpgArgs<T> a) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  T* lds = reinterpret_cast<T*>(lds_raw);
   const int sl = blockIdx.x % a.nslab;
   const int64_t r = blockIdx.x / a.nslab;
   const int lane = threadIdx.x, q = sl * kWave + lane;
   const bool act = q < a.C;
-  float* sA = lds;
-  float* sB = sA + a.dA * kWave;
-  float* sP = sB + (BSH ? ((a.dB + 3) & ~3) : a.dB * kWave);
-  for (int i = 0; i < a.dA; ++i) sA[i * kWave + lane] = act ? a.A[(r * a.dA + i) * a.C + q] : 0.0f;
+  T* sA = lds;
+  T* sB = sA + a.dA * kWave;
+  T* sP = sB + (BSH ? ((a.dB + 3) & ~3) : a.dB * kWave);
+  for (int i = 0; i < a.dA; ++i) sA[i * kWave + lane] = act ? a.A[(r * a.dA + i) * a.C + q] : T(0);
   if constexpr (BSH) {
     for (int i = lane; i < a.dB; i += kWave) sB[i] = a.B[r * a.dB + i];
   } else {
-    for (int i = 0; i < a.dB; ++i) sB[i * kWave + lane] = act ? a.B[(r * a.dB + i) * a.C + q] : 0.0f;
+    for (int i = 0; i < a.dB; ++i) sB[i * kWave + lane] = act ? a.B[(r * a.dB + i) * a.C + q] : T(0);
   }
   __syncthreads();
   for (int o = 0; o < a.dout; ++o) {
-    float acc = 0.0f;
+    T acc = T(0);
     const int k1 = a.seg[o + 1];
     for (int k = a.seg[o]; k < k1; ++k) {
-      const TpgRec rc = a.recs[k];
-      const float bv = BSH ? sB[rc.b] : sB[rc.b * kWave + lane];
-      acc = fmaf(rc.v * sA[rc.a * kWave + lane], bv, acc);
+      const auto rc = a.recs[k];
+      const T bv = BSH ? sB[rc.b] : sB[rc.b * kWave + lane];
+      acc = fma(T(rc.v) * sA[rc.a * kWave + lane], bv, acc);
     }
     if constexpr (RED)
       sP[o * kWave + lane] = acc;
@@ -1557,20 +1564,21 @@ __global__ __launch_bounds__(kWave) void k_tpg(TpgArgs a) {
   if constexpr (RED) {
     __syncthreads();
     for (int o = lane; o < a.dout; o += kWave) {
-      float t = 0.0f;
+      T t = T(0);
       for (int l = 0; l < kWave; ++l) t += sP[o * kWave + l];
       a.part[(r * a.nslab + sl) * a.dout + o] = t;
     }
   }
 }
 
-__global__ __launch_bounds__(256) void k_tpg_sum(const float* __restrict__ part, float* __restrict__ out,
-                                                  int64_t rows, int nslab, int dout) {
+template <class T>
+__global__ __launch_bounds__(256) void k_tpg_sum(const T* __restrict__ part, T* __restrict__ out, int64_t rows,
+                                                  int nslab, int dout) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= rows * dout) return;
   const int64_t r = i / dout;
   const int o = (int)(i % dout);
-  float t = 0.0f;
+  T t = T(0);
   for (int sl = 0; sl < nslab; ++sl) t += part[(r * nslab + sl) * dout + o];
   out[i] = t;
 }
@@ -2699,14 +2707,15 @@ struct e3_tpg {
   struct Table {
     std::vector<int> seg;
     std::vector<TpgRec> recs;
-    size_t off_seg = 0, off_recs = 0;
+    std::vector<TpgRec64> recs64;
+    size_t off_seg = 0, off_recs = 0, off_recs64 = 0;
   } t[3];
   std::mutex mu;
   char* dev = nullptr;
 };
 
 namespace {
-e3_tpg::Table tpg_table(int d_out, const std::vector<std::array<int, 3>>& key, const std::vector<float>& val) {
+e3_tpg::Table tpg_table(int d_out, const std::vector<std::array<int, 3>>& key, const std::vector<double>& val) {
   // key = (out, a, b); stable order by (out, a, b)
   std::vector<size_t> ord(key.size());
   for (size_t i = 0; i < ord.size(); ++i) ord[i] = i;
@@ -2714,7 +2723,8 @@ e3_tpg::Table tpg_table(int d_out, const std::vector<std::array<int, 3>>& key, c
   e3_tpg::Table T;
   T.seg.assign(d_out + 1, 0);
   for (size_t i : ord) {
-    T.recs.push_back(TpgRec{key[i][1], key[i][2], val[i], 0});
+    T.recs.push_back(TpgRec{key[i][1], key[i][2], (float)val[i], 0});
+    T.recs64.push_back(TpgRec64{key[i][1], key[i][2], val[i]});
     ++T.seg[key[i][0] + 1];
   }
   for (int o = 0; o < d_out; ++o) T.seg[o + 1] += T.seg[o];
@@ -2730,11 +2740,15 @@ e3_status tpg_upload(e3_tpg* G, hipStream_t st) {
     off = align256(off + T.seg.size() * sizeof(int));
     T.off_recs = off;
     off = align256(off + T.recs.size() * sizeof(TpgRec) + 1);
+    T.off_recs64 = off;
+    off = align256(off + T.recs64.size() * sizeof(TpgRec64) + 1);
   }
   std::vector<char> host(off, 0);
   for (auto& T : G->t) {
     std::memcpy(host.data() + T.off_seg, T.seg.data(), T.seg.size() * sizeof(int));
     if (!T.recs.empty()) std::memcpy(host.data() + T.off_recs, T.recs.data(), T.recs.size() * sizeof(TpgRec));
+    if (!T.recs64.empty())
+      std::memcpy(host.data() + T.off_recs64, T.recs64.data(), T.recs64.size() * sizeof(TpgRec64));
   }
   char* d = nullptr;
   E3_HIP(hipMalloc(&d, off));
@@ -2749,33 +2763,35 @@ e3_status tpg_upload(e3_tpg* G, hipStream_t st) {
   return E3_OK;
 }
 
-size_t tpg_lds(int dA, int dB, int dout, bool bsh, bool red) {
+size_t tpg_lds(int dA, int dB, int dout, bool bsh, bool red, size_t elem = sizeof(float)) {
   return ((size_t)dA * kWave + (bsh ? ((dB + 3) & ~3) : (size_t)dB * kWave) + (red ? (size_t)dout * kWave : 0)) *
-         sizeof(float);
+         elem;
 }
 constexpr size_t kTpgMaxLds = 64 * 1024;
 
-e3_status tpg_run(const e3_tpg* G, int which, const float* A, int dA, const float* B, int dB, bool bsh, float* out,
-                  float* part, bool red, int64_t rows, int C, const char* name, hipStream_t st) {
-  const e3_tpg::Table& T = G->t[which];
-  TpgArgs a{};
+template <class T>
+e3_status tpg_run(const e3_tpg* G, int which, const T* A, int dA, const T* B, int dB, bool bsh, T* out, T* part,
+                  bool red, int64_t rows, int C, const char* name, hipStream_t st) {
+  const e3_tpg::Table& Tb = G->t[which];
+  TpgArgs<T> a{};
   a.A = A, a.B = B, a.out = out, a.part = part;
-  a.seg = reinterpret_cast<const int*>(G->dev + T.off_seg);
-  a.recs = reinterpret_cast<const TpgRec*>(G->dev + T.off_recs);
+  a.seg = reinterpret_cast<const int*>(G->dev + Tb.off_seg);
+  a.recs = reinterpret_cast<decltype(a.recs)>(G->dev + (sizeof(T) == 8 ? Tb.off_recs64 : Tb.off_recs));
   a.rows = rows, a.C = C, a.nslab = (C + kWave - 1) / kWave, a.dA = dA, a.dB = dB;
-  a.dout = (int)T.seg.size() - 1;
-  const size_t lds = tpg_lds(dA, dB, a.dout, bsh, red);
+  a.dout = (int)Tb.seg.size() - 1;
+  const size_t lds = tpg_lds(dA, dB, a.dout, bsh, red, sizeof(T));
+  if (lds > kTpgMaxLds) return E3_ERR_UNSUPPORTED;
   const int64_t grid = rows * a.nslab;
   if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
   TimedLaunch t_(name, st);
   if (bsh && red)
-    hipLaunchKernelGGL((k_tpg<true, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    hipLaunchKernelGGL((k_tpg<T, true, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
   else if (bsh)
-    hipLaunchKernelGGL((k_tpg<true, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    hipLaunchKernelGGL((k_tpg<T, true, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
   else if (red)
-    hipLaunchKernelGGL((k_tpg<false, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    hipLaunchKernelGGL((k_tpg<T, false, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
   else
-    hipLaunchKernelGGL((k_tpg<false, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    hipLaunchKernelGGL((k_tpg<T, false, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
   E3_HIP(hipGetLastError());
   return E3_OK;
 }
@@ -2784,7 +2800,7 @@ e3_status tpg_run(const e3_tpg* G, int which, const float* A, int dA, const floa
 extern "C" {
 
 e3_status e3_tpg_create(int d_x, int d_y, int d_z, int64_t nnz, const int32_t* i0, const int32_t* i1,
-                        const int32_t* i2, const float* val, int y_per_channel, e3_tpg** out) {
+                        const int32_t* i2, const double* val, int y_per_channel, e3_tpg** out) {
   if (!out) return E3_ERR_INVALID_ARG;
   *out = nullptr;
   if (d_x < 1 || d_y < 1 || d_z < 1 || nnz < 0 || nnz > (1 << 24) || (nnz > 0 && (!i0 || !i1 || !i2 || !val)))
@@ -2802,7 +2818,7 @@ e3_status e3_tpg_create(int d_x, int d_y, int d_z, int64_t nnz, const int32_t* i
   if (!G) return E3_ERR_ALLOC;
   G->d_x = d_x, G->d_y = d_y, G->d_z = d_z, G->ypc = y_per_channel ? 1 : 0;
   std::vector<std::array<int, 3>> kf(nnz), kx(nnz), ky(nnz);
-  std::vector<float> v(val, val + nnz);
+  std::vector<double> v(val, val + nnz);
   for (int64_t k = 0; k < nnz; ++k) {
     kf[k] = {i0[k], i1[k], i2[k]};  // z[i0] from x[i1], y[i2]
     kx[k] = {i1[k], i0[k], i2[k]};  // dx[i1] from dz[i0], y[i2]   (records (i1, i2, i0) of eq. tp-bwd)
@@ -2822,48 +2838,81 @@ e3_status e3_tpg_destroy(e3_tpg* G) {
   return E3_OK;
 }
 
-e3_status e3_tpg_fwd(e3_tpg* G, const float* x, const float* y, float* z, int64_t rows, int C, e3_stream stream) {
+}  // extern "C"
+
+namespace {
+template <class T>
+e3_status tpg_fwd(e3_tpg* G, const T* x, const T* y, T* z, int64_t rows, int C, hipStream_t st) {
   if (!G || rows < 0 || C < 1) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
   if (!x || !y || !z) return E3_ERR_INVALID_ARG;
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   e3_status s = tpg_upload(G, st);
   if (s != E3_OK) return s;
-  return tpg_run(G, 0, x, G->d_x, y, G->d_y, !G->ypc, z, nullptr, false, rows, C, "tpg_fwd", st);
+  return tpg_run<T>(G, 0, x, G->d_x, y, G->d_y, !G->ypc, z, nullptr, false, rows, C,
+                    sizeof(T) == 8 ? "tpg_fwd_f64" : "tpg_fwd", st);
+}
+
+size_t tpg_ws(const e3_tpg* G, int64_t rows, int C, size_t elem) {
+  return G->ypc ? 0 : align256((size_t)rows * ((C + kWave - 1) / kWave) * G->d_y * elem);
+}
+
+template <class T>
+e3_status tpg_bwd(e3_tpg* G, const T* x, const T* y, const T* dz, T* dx, T* dy, void* ws, size_t ws_bytes,
+                  int64_t rows, int C, hipStream_t st) {
+  if (!G || rows < 0 || C < 1) return E3_ERR_INVALID_ARG;
+  if (rows == 0) return E3_OK;
+  if (!x || !y || !dz || !dx || !dy) return E3_ERR_INVALID_ARG;
+  const size_t need = tpg_ws(G, rows, C, sizeof(T));
+  if (ws_bytes < need) return E3_ERR_WORKSPACE_TOO_SMALL;
+  if (need > 0 && !ws) return E3_ERR_INVALID_ARG;
+  e3_status s = tpg_upload(G, st);
+  if (s != E3_OK) return s;
+  const bool f64 = sizeof(T) == 8;
+  // dx = tensor_product(C^{i1}_{i2 i0}, y, dz)
+  if ((s = tpg_run<T>(G, 1, dz, G->d_z, y, G->d_y, !G->ypc, dx, nullptr, false, rows, C,
+                      f64 ? "tpg_bwd_dx_f64" : "tpg_bwd_dx", st)) != E3_OK)
+    return s;
+  // dy = tensor_product(C^{i2}_{i1 i0}, x, dz), summed over the channels when y is shared
+  if (G->ypc)
+    return tpg_run<T>(G, 2, x, G->d_x, dz, G->d_z, false, dy, nullptr, false, rows, C,
+                      f64 ? "tpg_bwd_dy_f64" : "tpg_bwd_dy", st);
+  T* part = reinterpret_cast<T*>(ws);
+  if ((s = tpg_run<T>(G, 2, x, G->d_x, dz, G->d_z, false, nullptr, part, true, rows, C,
+                      f64 ? "tpg_bwd_dy_f64" : "tpg_bwd_dy", st)) != E3_OK)
+    return s;
+  TimedLaunch t_(f64 ? "tpg_bwd_dy_sum_f64" : "tpg_bwd_dy_sum", st);
+  hipLaunchKernelGGL(k_tpg_sum<T>, dim3(blocks_for(rows * G->d_y, 256)), dim3(256), 0, st, part, dy, rows,
+                     (C + kWave - 1) / kWave, G->d_y);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+}  // namespace
+
+extern "C" {
+
+e3_status e3_tpg_fwd(e3_tpg* G, const float* x, const float* y, float* z, int64_t rows, int C, e3_stream stream) {
+  return tpg_fwd<float>(G, x, y, z, rows, C, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_tpg_fwd_f64(e3_tpg* G, const double* x, const double* y, double* z, int64_t rows, int C,
+                         e3_stream stream) {
+  return tpg_fwd<double>(G, x, y, z, rows, C, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_tpg_workspace_size(const e3_tpg* G, int64_t rows, int C, size_t* bwd_bytes) {
   if (!G || rows < 0 || C < 1 || !bwd_bytes) return E3_ERR_INVALID_ARG;
-  *bwd_bytes = G->ypc ? 0 : align256((size_t)rows * ((C + kWave - 1) / kWave) * G->d_y * sizeof(float));
+  *bwd_bytes = tpg_ws(G, rows, C, sizeof(double));  // enough for either precision
   return E3_OK;
 }
 
 e3_status e3_tpg_bwd(e3_tpg* G, const float* x, const float* y, const float* dz, float* dx, float* dy, void* ws,
                      size_t ws_bytes, int64_t rows, int C, e3_stream stream) {
-  if (!G || rows < 0 || C < 1) return E3_ERR_INVALID_ARG;
-  if (rows == 0) return E3_OK;
-  if (!x || !y || !dz || !dx || !dy) return E3_ERR_INVALID_ARG;
-  size_t need = 0;
-  e3_status s = e3_tpg_workspace_size(G, rows, C, &need);
-  if (s != E3_OK) return s;
-  if (ws_bytes < need) return E3_ERR_WORKSPACE_TOO_SMALL;
-  if (need > 0 && !ws) return E3_ERR_INVALID_ARG;
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if ((s = tpg_upload(G, st)) != E3_OK) return s;
-  // dx = tensor_product(C^{i1}_{i2 i0}, y, dz)
-  if ((s = tpg_run(G, 1, dz, G->d_z, y, G->d_y, !G->ypc, dx, nullptr, false, rows, C, "tpg_bwd_dx", st)) != E3_OK)
-    return s;
-  // dy = tensor_product(C^{i2}_{i1 i0}, x, dz), summed over channels when y is shared
-  if (G->ypc)
-    return tpg_run(G, 2, x, G->d_x, dz, G->d_z, false, dy, nullptr, false, rows, C, "tpg_bwd_dy", st);
-  float* part = reinterpret_cast<float*>(ws);
-  if ((s = tpg_run(G, 2, x, G->d_x, dz, G->d_z, false, nullptr, part, true, rows, C, "tpg_bwd_dy", st)) != E3_OK)
-    return s;
-  TimedLaunch t_("tpg_bwd_dy_sum", st);
-  hipLaunchKernelGGL(k_tpg_sum, dim3(blocks_for(rows * G->d_y, 256)), dim3(256), 0, st, part, dy, rows,
-                     (C + kWave - 1) / kWave, G->d_y);
-  E3_HIP(hipGetLastError());
-  return E3_OK;
+  return tpg_bwd<float>(G, x, y, dz, dx, dy, ws, ws_bytes, rows, C, reinterpret_cast<hipStream_t>(stream));
+}
+
+e3_status e3_tpg_bwd_f64(e3_tpg* G, const double* x, const double* y, const double* dz, double* dx, double* dy,
+                         void* ws, size_t ws_bytes, int64_t rows, int C, e3_stream stream) {
+  return tpg_bwd<double>(G, x, y, dz, dx, dy, ws, ws_bytes, rows, C, reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

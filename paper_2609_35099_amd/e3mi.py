@@ -70,6 +70,8 @@ SIGNATURES = {
     "e3_tpg_fwd": (_I, [_P, _P, _P, _P, _I64, ct.c_int, _P]),
     "e3_tpg_workspace_size": (_I, [_P, _I64, ct.c_int, ct.POINTER(ct.c_size_t)]),
     "e3_tpg_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, ct.c_int, _P]),
+    "e3_tpg_fwd_f64": (_I, [_P, _P, _P, _P, _I64, ct.c_int, _P]),
+    "e3_tpg_bwd_f64": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, ct.c_int, _P]),
     "e3_conv_fwd_y": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P]),
     "e3_conv_bwd_y": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_int, _P, ct.c_size_t, _P]),
     "e3_conv_bwd2": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
@@ -115,7 +117,7 @@ def _torch():
 
 def _ptr(t, name, shape=None, dtype="float32"):
     torch = _torch()
-    want = {"float32": torch.float32, "int32": torch.int32}[dtype]
+    want = {"float32": torch.float32, "float64": torch.float64, "int32": torch.int32}[dtype]
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch tensor")
     if t.dtype != want:
@@ -389,7 +391,7 @@ class RecordTP:
 
     def __init__(self, d_x: int, d_y: int, d_z: int, i0, i1, i2, val, y_per_channel: bool):
         i0, i1, i2 = (np.ascontiguousarray(a, dtype=np.int32) for a in (i0, i1, i2))
-        val = np.ascontiguousarray(val, dtype=np.float32)
+        val = np.ascontiguousarray(val, dtype=np.float64)
         h = ct.c_void_p()
         _check(lib().e3_tpg_create(d_x, d_y, d_z, val.shape[0], i0.ctypes.data_as(ct.c_void_p),
                                    i1.ctypes.data_as(ct.c_void_p), i2.ctypes.data_as(ct.c_void_p),
@@ -412,23 +414,35 @@ class RecordTP:
     def _yshape(self, R, C):
         return (R, self.d_y, C) if self.ypc else (R, self.d_y)
 
+    @staticmethod
+    def _kind(x):
+        torch = _torch()
+        return ("float64", "_f64") if x.dtype == torch.float64 else ("float32", "")
+
     def forward(self, x, y, out=None, stream=None):
+        """z in the precision of x (float32 or float64)."""
         R, _, C = x.shape
-        out = _empty((R, self.d_z, C)) if out is None else out
-        _check(lib().e3_tpg_fwd(self.handle, _ptr(x, "x", (R, self.d_x, C)), _ptr(y, "y", self._yshape(R, C)),
-                                _ptr(out, "z", (R, self.d_z, C)), R, C, _stream(stream)), "e3_tpg_fwd")
+        dt, sfx = self._kind(x)
+        out = _torch().empty((R, self.d_z, C), dtype=x.dtype, device="cuda") if out is None else out
+        _check(getattr(lib(), "e3_tpg_fwd" + sfx)(
+            self.handle, _ptr(x, "x", (R, self.d_x, C), dt), _ptr(y, "y", self._yshape(R, C), dt),
+            _ptr(out, "z", (R, self.d_z, C), dt), R, C, _stream(stream)), "e3_tpg_fwd" + sfx)
         return out
 
     def backward(self, x, y, dz, stream=None):
         R, _, C = x.shape
-        dx, dy = _empty((R, self.d_x, C)), _empty(self._yshape(R, C))
+        dt, sfx = self._kind(x)
+        torch = _torch()
+        dx = torch.empty((R, self.d_x, C), dtype=x.dtype, device="cuda")
+        dy = torch.empty(self._yshape(R, C), dtype=x.dtype, device="cuda")
         b = ct.c_size_t()
         _check(lib().e3_tpg_workspace_size(self.handle, R, C, ct.byref(b)), "e3_tpg_workspace_size")
         ws = workspace(b.value)
-        _check(lib().e3_tpg_bwd(self.handle, _ptr(x, "x", (R, self.d_x, C)), _ptr(y, "y", self._yshape(R, C)),
-                                _ptr(dz, "dz", (R, self.d_z, C)), _ptr(dx, "dx", (R, self.d_x, C)),
-                                _ptr(dy, "dy", self._yshape(R, C)), ct.c_void_p(ws.data_ptr()), ws.numel(), R, C,
-                                _stream(stream)), "e3_tpg_bwd")
+        _check(getattr(lib(), "e3_tpg_bwd" + sfx)(
+            self.handle, _ptr(x, "x", (R, self.d_x, C), dt), _ptr(y, "y", self._yshape(R, C), dt),
+            _ptr(dz, "dz", (R, self.d_z, C), dt), _ptr(dx, "dx", (R, self.d_x, C), dt),
+            _ptr(dy, "dy", self._yshape(R, C), dt), ct.c_void_p(ws.data_ptr()), ws.numel(), R, C,
+            _stream(stream)), "e3_tpg_bwd" + sfx)
         return dx, dy
 
 

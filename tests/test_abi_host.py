@@ -166,7 +166,7 @@ def test_record_tp_create_checks():
     L = e3mi.lib()
     h = ct.c_void_p()
     i = (ct.c_int32 * 2)(0, 1)
-    v = (ct.c_float * 2)(1.0, 2.0)
+    v = (ct.c_double * 2)(1.0, 2.0)
     assert L.e3_tpg_create(4, 4, 4, 2, i, i, i, v, 1, ct.byref(h)) == 0
     assert L.e3_tpg_destroy(h) == 0
     bad = (ct.c_int32 * 2)(0, 4)

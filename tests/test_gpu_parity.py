@@ -777,7 +777,7 @@ def test_record_tp_parity(e3, case):
         C = 130
     ypc = case.endswith("perchannel") or case == "C7"
     R = 57
-    T = e3.RecordTP(dx_, dy_, dz_, i0, i1, i2, v.astype(np.float32), ypc)
+    T = e3.RecordTP(dx_, dy_, dz_, i0, i1, i2, v, ypc)
     x = rng.standard_normal((R, dx_, C)).astype(np.float32)
     y = rng.standard_normal((R, dy_, C) if ypc else (R, dy_)).astype(np.float32)
     dz = rng.standard_normal((R, dz_, C)).astype(np.float32)
@@ -802,7 +802,7 @@ def test_record_tp_config2_matches_specialised(e3):
     plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
     lay = layout_of(cfg)
     i0, i1, i2, v = _layout_records(lay)
-    T = e3.RecordTP(lay.d_in, lay.d_sh, lay.d_out, i0, i1, i2, v.astype(np.float32), False)
+    T = e3.RecordTP(lay.d_in, lay.d_sh, lay.d_out, i0, i1, i2, v, False)
     x, u, w = synth.tp_inputs(cfg)
     y = osh.sh_unit(3, u.astype(np.float64)).astype(np.float32)
     xs, ys = to_dev(x), to_dev(y)
@@ -815,3 +815,32 @@ def test_record_tp_config2_matches_specialised(e3):
     ri = torch.as_tensor(rows, device="cuda")
     ref = ogeneric.tp(i0, i1, i2, v.astype(np.float32).astype(np.float64), x[rows], y[rows], lay.d_out)
     assert rel_l2(to_np(z[ri]), ref) < TOL
+
+
+@pytest.mark.parametrize("ypc", [False, True])
+def test_record_tp_float64(e3, ypc):
+    """The float64 record path against the oracle at float64 accuracy (operand
+    rows of up to 64 KiB of doubles per 64 channels; larger ones are refused)."""
+    _say("record tp f64", ypc)
+    rng = np.random.default_rng(63)
+    big = oirreps.layout("4x0e+4x1o+4x2e+4x3o", 3, 3)      # dz rows of 156 doubles: over the limit
+    Tb = e3.RecordTP(big.d_in, big.d_sh, big.d_out, *_layout_records(big), ypc)
+    with pytest.raises(e3.E3Error) as ei:
+        Tb.backward(*(to_dev(np.zeros(sh)) for sh in ((2, big.d_in, 8), (2, big.d_sh, 8) if ypc else (2, big.d_sh),
+                                                       (2, big.d_out, 8))))
+    assert ei.value.status == 2
+    lay = oirreps.layout("4x0e+4x1o+4x2e", 3, 2)
+    i0, i1, i2, v = _layout_records(lay)
+    R, C = 41, 70
+    T = e3.RecordTP(lay.d_in, lay.d_sh, lay.d_out, i0, i1, i2, v, ypc)
+    x = rng.standard_normal((R, lay.d_in, C))
+    y = rng.standard_normal((R, lay.d_sh, C) if ypc else (R, lay.d_sh))
+    dz = rng.standard_normal((R, lay.d_out, C))
+    z = to_np(T.forward(to_dev(x), to_dev(y)))
+    gdx, gdy = (to_np(t) for t in T.backward(to_dev(x), to_dev(y), to_dev(dz)))
+    rz = ogeneric.tp(i0, i1, i2, v, x, y, lay.d_out)
+    rdx, rdy = ogeneric.tp_bwd(i0, i1, i2, v, x, y, dz)
+    errs = dict(z=rel_l2(z, rz), dx=rel_l2(gdx, rdx), dy=rel_l2(gdy, rdy))
+    print("rel-L2", errs, flush=True)
+    for k, e in errs.items():
+        assert e < 1e-12, (k, e)
