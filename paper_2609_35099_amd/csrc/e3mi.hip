@@ -113,6 +113,9 @@ constexpr int kXcd = 8;
 #define E3_FWD_CPL 2
 #endif
 // 1: the backward sweep double-buffers the path weights as well as the x rows.
+#ifndef E3_FWD_PREFETCH3
+#define E3_FWD_PREFETCH3 1
+#endif
 #ifndef E3_RAD_WREG
 #define E3_RAD_WREG 1
 #endif
@@ -589,6 +592,24 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
 #pragma unroll
         for (int i = 0; i < F::NPATH; ++i) bld<CPL, kNT>(sb_, F::PATH[i], sv[i]);
       };
+#if E3_FWD_PREFETCH3
+      // three register buffers: the rows of edges j+1 and j+2 are in flight while j computes
+      float xc[F::NXR][CPL], sc[F::NPATH][CPL];
+      load(0, xa, sa);
+      if (1 < n) load(1, xb, sb);
+      for (int j = 0; j < n; j += 3) {
+        if (j + 2 < n) load(j + 2, xc, sc);
+        F::template edge<CPL>(sA + j * F::NA, xa, sa, acc);
+        if (j + 1 < n) {
+          if (j + 3 < n) load(j + 3, xa, sa);
+          F::template edge<CPL>(sA + (j + 1) * F::NA, xb, sb, acc);
+        }
+        if (j + 2 < n) {
+          if (j + 4 < n) load(j + 4, xb, sb);
+          F::template edge<CPL>(sA + (j + 2) * F::NA, xc, sc, acc);
+        }
+      }
+#else
       load(0, xa, sa);
       for (int j = 0; j < n; j += 2) {
         if (j + 1 < n) load(j + 1, xb, sb);
@@ -598,6 +619,7 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
           F::template edge<CPL>(sA + (j + 1) * F::NA, xb, sb, acc);
         }
       }
+#endif
     }
     __syncthreads();
   }
