@@ -72,7 +72,7 @@ def radial_bytes(N, E, C, D_in, D_out, P, K):
 
 KERNEL_SOURCES = ["paper_2609_35099_amd/csrc/e3mi.hip", "paper_2609_35099_amd/csrc/gen.cpp",
                   "paper_2609_35099_amd/csrc/builder.cpp", "paper_2609_35099_amd/csrc/builder.h"]
-COUNTERS = os.path.join(ROOT, "profiles", "conv_tp_config4_hbm_bytes.txt")
+COUNTERS = os.path.join(ROOT, "profiles", "conv_water8k_tp200k_hbm_bytes.txt")
 
 
 def source_hash() -> str:
@@ -83,7 +83,7 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-UTIL = os.path.join(ROOT, "profiles", "util_config4.txt")
+UTIL = os.path.join(ROOT, "profiles", "util_water8k_tp200k.txt")
 
 
 def counter_util(kernel: str, metric: str):
@@ -266,8 +266,8 @@ def main():
                     help="also run one plain 2 GiB device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              f"(the per-GPU kernel is the unit; see the sharding notes in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              f"(the per-GPU kernel on its share is the unit measured)", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -282,7 +282,7 @@ def main():
            "data": "synthetic"}
 
     # ---------------------------------------------------------------- conv
-    cfg = synth.CONFIGS[4]
+    cfg = synth.CONFIGS["water8k"]
     t0 = time.perf_counter()
     g = synth.graph(cfg, order=args.order)
     x = synth.node_features(cfg, g.n_nodes)
@@ -370,7 +370,7 @@ def main():
                                    + ("" if args.order == "generated" else "; atoms cell-sorted"),
                        "n_nodes": N, "n_edges": E, "channels": C, "paths": plan.P,
                        "D_in": plan.D_in, "D_out": plan.D_out},
-            # the dominant sweep is bound by VALU issue (packed fp32 is disabled in this build):
+            # the dominant sweep is bound by VALU issue (the kernels are compiled without packed fp32):
             # its FMA-equivalent work against the unpacked vector peak, with the HBM view beside it
             "roofline": {"bound": "alu", "kernel": dom, "achieved": round(dom_tf, 2), "peak": VALU_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(dom_tf / VALU_PEAK_TFLOPS, 4),
@@ -521,7 +521,7 @@ def main():
 
     # ---------------------------------------------------------------- tp
     if not args.no_tp and args.only in ("all", "tp"):
-        tcfg = synth.CONFIGS[2]
+        tcfg = synth.CONFIGS["tp200k"]
         tplan = e3mi.Plan(tcfg.irreps, tcfg.lmax_sh, tcfg.lmax_out)
         tx, tu, tw = synth.tp_inputs(tcfg)
         txd, twd = torch.from_numpy(tx).to(dev), torch.from_numpy(tw).to(dev)

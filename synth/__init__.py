@@ -7,22 +7,22 @@ contraction).  The per-edge weights of the water boxes are built from a random
 radial basis (a Bessel basis of the edge length times a fixed random matrix),
 which is input synthesis, not part of the operation under test.
 
-Every random stream is ``numpy.random.default_rng(SeedSequence([cfg, stream,
+Every random stream is ``numpy.random.default_rng(SeedSequence([seed, stream,
 chunk]))`` so that any chunk of any array can be regenerated on its own (the
-oracle checks large configurations on sampled rows).  Values are drawn in
-float64 and rounded to float32, the precision both sides consume.
+oracle checks large workloads on sampled rows).  Values are drawn in float64
+and rounded to float32, the precision both sides consume.
 
-Configurations (shapes of the workloads the method is benchmarked on):
+Workloads (shapes of those the method is benchmarked on), by name:
 
-  1  tiny conv: 64 atoms uniform in a non-periodic cube at 0.1 atoms/A^3,
-     all ordered pairs closer than 4 A; x 8x0e+8x1o, harmonics l<=2, output
-     l<=2; x, s, dm ~ N(0,1).  Edges in sender-major order.
-  2  standalone tensor product: 200,000 rows of x 128x0e+128x1o+128x2e,
-     random unit vectors (harmonics l<=3), per-row path weights ~ N(0,1).
-  3  water box, 1,000 rigid H2O at 1 g/cm^3, periodic, r_c = 5 A; x
-     128x0e+128x1o; s = Bessel_8(|r|) @ W.  Edges in receiver-major order.
-  4  same construction, 8,000 H2O (24,000 atoms); x 128x0e+128x1o+128x2e+128x3o.
-  5  70,000 H2O (210,000 atoms), 64 channels, s ~ N(0,1).
+  cube64    tiny conv: 64 atoms uniform in a non-periodic cube at 0.1 atoms/A^3,
+            all ordered pairs closer than 4 A; x 8x0e+8x1o, harmonics l<=2,
+            output l<=2; x, s, dm ~ N(0,1).  Edges in sender-major order.
+  tp200k    standalone tensor product: 200,000 rows of x 128x0e+128x1o+128x2e,
+            random unit vectors (harmonics l<=3), per-row path weights ~ N(0,1).
+  water1k   water box, 1,000 rigid H2O at 1 g/cm^3, periodic, r_c = 5 A; x
+            128x0e+128x1o; s = Bessel_8(|r|) @ W.  Edges in receiver-major order.
+  water8k   same construction, 8,000 H2O (24,000 atoms); x 128x0e+...+128x3o.
+  water70k  70,000 H2O (210,000 atoms), 64 channels, s ~ N(0,1).
 """
 from __future__ import annotations
 
@@ -51,8 +51,8 @@ class Config:
     lmax_out: int
     channels: int
     n_mol: int = 0     # water boxes
-    n_atoms: int = 0   # uniform cube (config 1)
-    rows: int = 0      # tensor product rows (config 2)
+    n_atoms: int = 0   # uniform cube of atoms
+    rows: int = 0      # tensor product rows
     weights: str = "normal"   # "normal" or "bessel"
     edge_order: str = "receiver"
     r_cut: float = R_CUT
@@ -69,13 +69,14 @@ def sweep_config(lmax: int, channels: int) -> Config:
                   n_mol=n_atoms // 3, r_cut=4.75)
 
 
+# Workloads by name (the number is the seed of each one's random streams).
 CONFIGS = {
-    1: Config(1, "conv", "8x0e+8x1o", 2, 2, 8, n_atoms=64, edge_order="sender"),
-    2: Config(2, "tp", "128x0e+128x1o+128x2e", 3, 3, 128, rows=200_000),
-    3: Config(3, "conv", "128x0e+128x1o", 3, 3, 128, n_mol=1000, weights="bessel"),
-    4: Config(4, "conv", "128x0e+128x1o+128x2e+128x3o", 3, 3, 128, n_mol=8000,
+    "cube64": Config(1, "conv", "8x0e+8x1o", 2, 2, 8, n_atoms=64, edge_order="sender"),
+    "tp200k": Config(2, "tp", "128x0e+128x1o+128x2e", 3, 3, 128, rows=200_000),
+    "water1k": Config(3, "conv", "128x0e+128x1o", 3, 3, 128, n_mol=1000, weights="bessel"),
+    "water8k": Config(4, "conv", "128x0e+128x1o+128x2e+128x3o", 3, 3, 128, n_mol=8000,
               weights="bessel"),
-    5: Config(5, "conv", "64x0e+64x1o+64x2e+64x3o", 3, 3, 64, n_mol=70_000),
+    "water70k": Config(5, "conv", "64x0e+64x1o+64x2e+64x3o", 3, 3, 64, n_mol=70_000),
 }
 
 
@@ -259,7 +260,7 @@ def cell_order(pos: np.ndarray, L: float, n_mol: int, cell: float = R_CUT) -> np
 
 
 def graph(cfg: Config, order: str = "generated") -> Graph:
-    """Edge list of a configuration.  order="cell" renumbers the atoms of a water
+    """Edge list of a workload.  order="cell" renumbers the atoms of a water
     box so that molecules are sorted by spatial cell (the as-generated order is
     spatially random)."""
     if cfg.n_atoms:
@@ -356,7 +357,7 @@ def edge_weights_rows(cfg: Config, vec: np.ndarray, rows: np.ndarray, W=None) ->
 
 def radial_inputs(cfg: Config, vec: np.ndarray):
     """(h [E, 8], W [8, P, C]) float32 with h = the Bessel basis of |r| and W the
-    config's fixed random matrix: h @ W is the config's per-edge weight recipe."""
+    workload's fixed random matrix: h @ W is its per-edge weight recipe."""
     P, _ = n_paths_dout(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
     r = np.linalg.norm(vec.astype(np.float64), axis=1)
     h = bessel_basis(r).astype(np.float32)

@@ -52,7 +52,7 @@ def test_graph_csr_bit_exact(e3, case):
     rng = np.random.default_rng(1)
     pad = -1
     if case == "cfg1":
-        g = synth.graph(synth.CONFIGS[1])
+        g = synth.graph(synth.CONFIGS["cube64"])
         snd, rcv, n = g.sender, g.receiver, g.n_nodes
     elif case == "random_pad":
         n = 300
@@ -105,7 +105,7 @@ def test_sh_and_sh_bwd(e3, lmax):
 
 # ---------------------------------------------------------------- tensor product
 @pytest.mark.parametrize("irreps,lsh,lout,rows", [
-    ("128x0e+128x1o+128x2e", 3, 3, 1001),   # config 2 layout, ragged batch tail
+    ("128x0e+128x1o+128x2e", 3, 3, 1001),   # the 200k-row layout, ragged batch tail
     ("64x0e+64x1o+64x2e", 3, 3, 77),
     ("8x0e+8x1o", 2, 2, 5),
     ("12x0e+12x1o+12x2e+12x3o", 3, 3, 33),    # C not a power of two
@@ -127,11 +127,12 @@ def test_tp_parity(e3, irreps, lsh, lout, rows):
     assert np.array_equal(z, z2)
 
 
-def test_tp_config2_full_size_sampled(e3):
-    """Config 2 at full size (200,000 rows), checked on sampled rows."""
+def test_tp_200k_rows_full_size_sampled(e3):
+    """The weighted TP at full size (200,000 rows, 128x0e+128x1o+128x2e, l <= 3),
+    checked on sampled rows."""
     import torch
-    _say("tp config 2 full")
-    cfg = synth.CONFIGS[2]
+    _say("tp 200k rows full")
+    cfg = synth.CONFIGS["tp200k"]
     plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
     lay = layout_of(cfg)
     x, u, w = synth.tp_inputs(cfg)
@@ -174,11 +175,11 @@ def test_tp_bwd_parity(e3, irreps, lsh, lout, rows):
         assert np.array_equal(u, v)
 
 
-def test_tp_bwd_config2_full_size_sampled(e3):
-    """TP backward at config 2's full size, checked on sampled rows."""
+def test_tp_bwd_200k_rows_full_size_sampled(e3):
+    """TP backward at full size (200,000 rows), checked on sampled rows."""
     import torch
-    _say("tp bwd config 2 full")
-    cfg = synth.CONFIGS[2]
+    _say("tp bwd 200k rows full")
+    cfg = synth.CONFIGS["tp200k"]
     plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
     lay = layout_of(cfg)
     x, u, w = synth.tp_inputs(cfg)
@@ -216,9 +217,10 @@ def _check_full(lay, snd, rcv, n, vec, x, s, dm, m, dx, dvec, ds, pad=-1):
     return ref_m, ref
 
 
-def test_conv_config1_full(e3):
-    _say("conv config 1")
-    cfg = synth.CONFIGS[1]
+def test_conv_cube64_full(e3):
+    """64 atoms in a cube, 8x0e+8x1o, harmonics and outputs to l = 2: full oracle."""
+    _say("conv cube64")
+    cfg = synth.CONFIGS["cube64"]
     g = synth.graph(cfg)
     x = synth.node_features(cfg, g.n_nodes)
     s = synth.edge_weights(cfg, g.vec, 0, g.sender.shape[0])
@@ -282,8 +284,8 @@ def test_conv_degenerate_graphs(e3):
 def test_conv_deterministic_and_invariants(e3):
     """Bitwise-identical repeats; trilinear identity and dvec . r = 0 on GPU outputs."""
     import torch
-    _say("conv determinism config 3")
-    cfg = synth.CONFIGS[3]
+    _say("conv determinism water1k")
+    cfg = synth.CONFIGS["water1k"]
     g = synth.graph(cfg)
     x = synth.node_features(cfg, g.n_nodes)
     dm = synth.out_cotangent(cfg, g.n_nodes)
@@ -324,13 +326,13 @@ def test_conv_deterministic_and_invariants(e3):
     assert rel_l2(to_np(dvec)[es], ref_dv) < TOL
 
 
-@pytest.mark.parametrize("cid", [4])
-def test_conv_full_size_sampled(e3, cid):
+@pytest.mark.parametrize("name", ["water8k"])
+def test_conv_full_size_sampled(e3, name):
     """The benchmark workload (24,000-atom water box, l<=3, 128 channels) at full
     size, in the launch configuration the benchmark times, on sampled rows."""
     import torch
-    _say("conv full size config", cid)
-    cfg = synth.CONFIGS[cid]
+    _say("conv full size", name)
+    cfg = synth.CONFIGS[name]
     g = synth.graph(cfg)
     x = synth.node_features(cfg, g.n_nodes)
     dm = synth.out_cotangent(cfg, g.n_nodes)
@@ -361,12 +363,12 @@ def test_conv_full_size_sampled(e3, cid):
 
 @pytest.mark.skipif(os.environ.get("E3MI_STRESS") != "1",
                     reason="capacity stress (~265 GB of HBM, several minutes): set E3MI_STRESS=1")
-def test_conv_stress_config5_sampled(e3):
+def test_conv_stress_water70k_sampled(e3):
     """70,000 H2O (210,000 atoms, ~11M edges), 64 channels: forward + backward at
     full size on one GPU, checked on sampled rows."""
     import torch
-    _say("conv stress config 5")
-    cfg = synth.CONFIGS[5]
+    _say("conv stress water70k")
+    cfg = synth.CONFIGS["water70k"]
     g = synth.graph(cfg)
     N, E = g.n_nodes, g.sender.shape[0]
     print(f"N={N} E={E}", flush=True)
@@ -477,16 +479,16 @@ def test_conv_radial_degenerate_graphs(e3):
             assert np.all(m[1:] == 0)
 
 
-def test_conv_radial_config4_sampled(e3):
-    """Config 4 (24,000-atom water box) with its own radial recipe fused: h = the
-    8-function Bessel basis of |r|, W = the config's fixed matrix.  m, dx, dvec
+def test_conv_radial_water8k_sampled(e3):
+    """The 24,000-atom water box with its own radial recipe fused: h = the
+    8-function Bessel basis of |r|, W = the workload's fixed matrix.  m, dx, dvec
     and dh are checked against the oracle on sampled rows.  dW sums over all
     1.27M edges, which the oracle cannot do in seconds: it is checked against a
     float64 sum of h_e ds_e with ds from the plain backward (itself checked
     against the oracle in test_conv_full_size_sampled)."""
     import torch
-    _say("conv radial config 4 full")
-    cfg = synth.CONFIGS[4]
+    _say("conv radial water8k full")
+    cfg = synth.CONFIGS["water8k"]
     g = synth.graph(cfg)
     x = synth.node_features(cfg, g.n_nodes)
     dm = synth.out_cotangent(cfg, g.n_nodes)
@@ -610,13 +612,13 @@ def test_conv_bwd2_random_graphs_full(e3, irreps, lsh, lout, n, e, pad):
         assert np.all(to_np(outs[0][1])[dead] == 0) and np.all(to_np(outs[0][2])[dead] == 0)
 
 
-def test_conv_bwd2_config4_sampled(e3):
-    """Double backward on config 4 (24,000-atom water box, y its harmonics) at full
+def test_conv_bwd2_water8k_sampled(e3):
+    """Double backward on the 24,000-atom water box (y its harmonics) at full
     size; checked on a compact sub-problem holding every in-edge of the sampled
     receivers, every out-edge of the sampled senders and the sampled edges."""
     import torch
-    _say("conv bwd2 config 4 full")
-    cfg = synth.CONFIGS[4]
+    _say("conv bwd2 water8k full")
+    cfg = synth.CONFIGS["water8k"]
     g = synth.graph(cfg)
     N, E = g.n_nodes, g.sender.shape[0]
     plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
@@ -696,19 +698,19 @@ def _path_irreps(plan):
 
 
 @pytest.mark.parametrize("which", ["nodes", "messages"])
-def test_linear_config4_sampled(e3, which):
-    """Full-size mixing at config 4 (24,000 atoms, 128 channels): node features
+def test_linear_water8k_sampled(e3, which):
+    """Full-size mixing on 24,000 nodes, 128 channels: node features
     (x blocks 0e,1o,2e,3o), or the convolution output (34 path blocks mixed per
     degree and parity).  Outputs on sampled nodes; dW on sampled pairs, each from
     an oracle sub-problem holding only that pair's two blocks over all nodes."""
     import torch
-    cfg = synth.CONFIGS[4]
+    cfg = synth.CONFIGS["water8k"]
     plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
     N = 24000
     ins = cfg.irreps if which == "nodes" else _path_irreps(plan)
     outs = "128x0e+128x1o+128x2e+128x3o" if which == "nodes" else \
         "128x0e+128x0o+128x1o+128x1e+128x2e+128x2o+128x3o+128x3e"
-    _say("linear config 4", which, ins[:40], "->", outs)
+    _say("linear water8k", which, ins[:40], "->", outs)
     L = e3.Linear(ins, outs)
     dev = torch.device("cuda")
     xs = synth.normal_device(4, 20, (N, L.D_in, L.C_in), dev)
@@ -792,13 +794,13 @@ def test_record_tp_parity(e3, case):
         assert e < TOL, (k, e)
 
 
-def test_record_tp_config2_matches_specialised(e3):
-    """Config 2 (200,000 rows, 128 channels, l <= 3) with the plan's own records:
+def test_record_tp_200k_rows_matches_specialised(e3):
+    """200,000 rows, 128x0e+128x1o+128x2e, l <= 3, with the plan's own records:
     the record kernel against the oracle on sampled rows, and against the
     specialised tensor product on all rows."""
     import torch
-    _say("record tp config 2")
-    cfg = synth.CONFIGS[2]
+    _say("record tp 200k rows")
+    cfg = synth.CONFIGS["tp200k"]
     plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
     lay = layout_of(cfg)
     i0, i1, i2, v = _layout_records(lay)
