@@ -113,6 +113,14 @@ constexpr int kXcd = 8;
 #define E3_FWD_CPL 2
 #endif
 // 1: the backward sweep double-buffers the path weights as well as the x rows.
+#ifndef E3_DX_VEC
+#define E3_DX_VEC 8
+#endif
+#ifndef E3_DX_UNROLL
+#define E3_DX_UNROLL 2
+#endif
+#define E3_PRAGMA(x) _Pragma(#x)
+#define E3_UNROLL(n) E3_PRAGMA(unroll n)
 #ifndef E3_FWD_PREFETCH3
 #define E3_FWD_PREFETCH3 1
 #endif
@@ -803,7 +811,7 @@ __global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd_edges(Conv
 // node's partials are one contiguous block of (out-degree) x D_in x C floats;
 // the wave reads each slot's D_in x C floats as float4s (lane l takes float4
 // l, l+64, ... of its slab) and keeps kDxVec float4 sums per lane.
-constexpr int kDxVec = 8;
+constexpr int kDxVec = E3_DX_VEC;
 
 __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__ T, float* __restrict__ dx,
                                                        const int* __restrict__ rowptr_s, int n_nodes, int chunk,
@@ -822,7 +830,7 @@ __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__
   const int64_t slot_bytes = (int64_t)flat4 * 16;
   __amdgpu_buffer_rsrc_t o = __builtin_amdgcn_make_buffer_rsrc(dx + (int64_t)node * flat4 * 4, (short)0,
                                                                (int)slot_bytes, 0x00020000);
-#pragma unroll 2
+  E3_UNROLL(E3_DX_UNROLL)
   for (int t = s0; t < s1; ++t) {
     // out-of-range float4s (past D_in x C) read as zero
     __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(

@@ -110,6 +110,7 @@ def test_sh_and_sh_bwd(e3, lmax):
     ("8x0e+8x1o", 2, 2, 5),
     ("12x0e+12x1o+12x2e+12x3o", 3, 3, 33),    # C not a power of two
     ("100x0e+100x1o", 3, 3, 19),              # 50 lanes x 2 channels
+    ("1024x0e+1024x1o+1024x2e", 3, 3, 9),     # the largest channel count
 ])
 def test_tp_parity(e3, irreps, lsh, lout, rows):
     _say("tp", irreps, rows)
@@ -152,6 +153,7 @@ def test_tp_200k_rows_full_size_sampled(e3):
     ("12x0e+12x1o+12x2e+12x3o", 3, 3, 33),
     ("100x0e+100x1o", 3, 3, 19),
     ("4x0e+4x1o", 3, 3, 1),
+    ("1024x0e+1024x1o+1024x2e", 3, 3, 5),
 ])
 def test_tp_bwd_parity(e3, irreps, lsh, lout, rows):
     _say("tp bwd", irreps, rows)
@@ -666,6 +668,7 @@ from oracle import linear as olinear  # noqa: E402
     ("128x0e+128x1o+128x2e+128x3o", "128x0e+128x1o+128x2e+128x3o", 101),
     ("64x0e+64x1o", "192x0e+192x1o", 9),                              # 3 column slabs
     ("48x1o+48x0e+48x1o+48x1o", "16x1o+16x0e", 23),
+    ("512x0e+512x1o", "1024x0e+1024x1o", 13),                       # large multiplicities
 ])
 def test_linear_small_full(e3, ins, outs, n):
     import torch
