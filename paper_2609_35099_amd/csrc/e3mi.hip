@@ -263,33 +263,57 @@ __device__ __forceinline__ void unit_of(const float* __restrict__ vec, int64_t e
   ux = vx * inv, uy = vy * inv, uz = vz * inv;
 }
 
+// Lane exchanges of gfx950 behind the wave reductions.  swap32(a, b) leaves
+// a = [a of lanes 0..31, b of lanes 0..31] and b = [a of lanes 32..63, b of
+// lanes 32..63]; swap16 does the same between the odd 16-lane rows of a and
+// the even rows of b, within each half.  dpp<CTRL>(v) reads v of another lane
+// of the same 16-lane row (quad permutes, rotate by 8 = lane ^ 8, mirror of
+// each 8-lane half = lane ^ 7).
+__device__ __forceinline__ void swap32(float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void swap16(float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppXor8 = 0x128, kDppXor7 = 0x141;
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+
 // Sum of v[16] over the 64 lanes of the wave by a fixed tree (transposed
-// halving: each stage keeps half of the values and exchanges the other half);
-// lane l with l % 4 == 0 ends with the total of index l / 4.
+// halving: each stage keeps half of the values and exchanges the other half,
+// on lane bits 5, 4, 3, then 2 paired by the half-row mirror, then a quad
+// sum; bk below is bit k of the lane); lane l ends with the total of index
+// l / 4.
 __device__ __forceinline__ float wave_reduce16(const float (&v)[16], int lane) {
   float w8[8], w4[4], w2[2];
-  const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8, b2 = lane & 4;
+  const bool b3 = lane & 8, b2 = lane & 4;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const float send = b5 ? v[i] : v[i + 8];
-    const float keep = b5 ? v[i + 8] : v[i];
-    w8[i] = keep + __shfl_xor(send, 32);
+  for (int i = 0; i < 8; ++i) {  // index i + 8 b5, summed over lane bit 5
+    float a = v[i], b = v[i + 8];
+    swap32(a, b);
+    w8[i] = a + b;
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float send = b4 ? w8[i] : w8[i + 4];
-    const float keep = b4 ? w8[i + 4] : w8[i];
-    w4[i] = keep + __shfl_xor(send, 16);
+  for (int i = 0; i < 4; ++i) {  // index i + 4 b4 + 8 b5, summed over bits 4, 5
+    float a = w8[i], b = w8[i + 4];
+    swap16(a, b);
+    w4[i] = a + b;
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < 2; ++i) {  // index i + 2 b3 + 4 b4 + 8 b5, summed over bits 3..5
     const float send = b3 ? w4[i] : w4[i + 2];
     const float keep = b3 ? w4[i + 2] : w4[i];
-    w2[i] = keep + __shfl_xor(send, 8);
+    w2[i] = keep + dpp<kDppXor8>(send);
   }
-  float w1 = (b2 ? w2[1] : w2[0]) + __shfl_xor(b2 ? w2[0] : w2[1], 4);
-  w1 += __shfl_xor(w1, 2);
-  w1 += __shfl_xor(w1, 1);
+  // index l / 4; the partner l ^ 7 has the same bits 3..5 and the other bit 2,
+  // and the quad sum then covers all eight values of the low three bits
+  float w1 = (b2 ? w2[1] : w2[0]) + dpp<kDppXor7>(b2 ? w2[0] : w2[1]);
+  w1 += dpp<kDppXor1>(w1);
+  w1 += dpp<kDppXor2>(w1);
   return w1;
 }
 
@@ -1167,27 +1191,28 @@ __global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd_rad(ConvAr
   bwd_rad_dispatch<V, 0>(a, b, g, sl, sA, sY, sY + kEdgeBatch * V::D_SH);
 }
 
-// Sum of v[8] over the wave by the same fixed tree as wave_reduce16; lane l
-// with l % 8 == 0 ends with the total of index l / 8.
+// Sum of v[8] over the wave by the same kind of tree as wave_reduce16
+// (exchanges on lane bits 5, 4, 3, then a sum over the low three bits); lane l
+// ends with the total of index l / 8.
 __device__ __forceinline__ float wave_reduce8(const float (&v)[8], int lane) {
   float w4[4], w2[2];
-  const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+  const bool b3 = lane & 8;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float send = b5 ? v[i] : v[i + 4];
-    const float keep = b5 ? v[i + 4] : v[i];
-    w4[i] = keep + __shfl_xor(send, 32);
+    float a = v[i], b = v[i + 4];
+    swap32(a, b);
+    w4[i] = a + b;
   }
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const float send = b4 ? w4[i] : w4[i + 2];
-    const float keep = b4 ? w4[i + 2] : w4[i];
-    w2[i] = keep + __shfl_xor(send, 16);
+    float a = w4[i], b = w4[i + 2];
+    swap16(a, b);
+    w2[i] = a + b;
   }
-  float w1 = (b3 ? w2[1] : w2[0]) + __shfl_xor(b3 ? w2[0] : w2[1], 8);
-  w1 += __shfl_xor(w1, 4);
-  w1 += __shfl_xor(w1, 2);
-  w1 += __shfl_xor(w1, 1);
+  float w1 = (b3 ? w2[1] : w2[0]) + dpp<kDppXor8>(b3 ? w2[0] : w2[1]);
+  w1 += dpp<kDppXor1>(w1);
+  w1 += dpp<kDppXor2>(w1);
+  w1 += dpp<kDppXor7>(w1);
   return w1;
 }
 
@@ -1201,8 +1226,14 @@ __device__ __forceinline__ float wave_reduce8(const float (&v)[8], int lane) {
 // gives dW[4 kq + i][col] in accumulator register i of the lane owning col.
 // Both partial sets are added up afterwards in a fixed order, so the result
 // does not depend on scheduling.
+#ifndef E3_GRAD_ROWS
+#define E3_GRAD_ROWS 4
+#endif
+#ifndef E3_GRAD_DB
+#define E3_GRAD_DB 1
+#endif
 constexpr int kGradF = 1;
-constexpr int kGradRows = 4;  // rows whose loads are issued before their arithmetic
+constexpr int kGradRows = E3_GRAD_ROWS;  // rows whose loads are issued together
 
 template <int KQ>
 __global__ __launch_bounds__(kWave) void k_rad_grad(const float* __restrict__ DS, const float* __restrict__ h,
@@ -1238,58 +1269,81 @@ __global__ __launch_bounds__(kWave) void k_rad_grad(const float* __restrict__ DS
     for (int u = 0; u < 4; ++u)
 #pragma unroll
       for (int k = 0; k < KQ; ++k) acc[f][u][k] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
-  for (int64_t rb = r0; rb < r1; rb += kGradRows) {
-    const int nr = (int)(r1 - rb < kGradRows ? r1 - rb : kGradRows);
-    f4v d[kGradRows][kGradF];
-    float hA[kGradRows][KQ];
+  // Row loads through descriptors bounded by the row: lanes past the last
+  // column slab read zero ds, and j >= K reads zero h.
+  auto load_row = [&](int64_t r, f4v(&d)[kGradF], float(&hA)[KQ]) {
+    const __amdgpu_buffer_rsrc_t rr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(DS) + r * PC4 * 4, (short)0, PC4 * 16, 0x00020000);
 #pragma unroll
-    for (int u = 0; u < kGradRows; ++u) {
+    for (int f = 0; f < kGradF; ++f)
+      d[f] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(rr, col4[f] * 16, 0, kNT));
+    const __amdgpu_buffer_rsrc_t hr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(h) + r * K, (short)0, K * 4, 0x00020000);
 #pragma unroll
-      for (int f = 0; f < kGradF; ++f) d[u][f] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int k = 0; k < KQ; ++k)
+      hA[k] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(hr, (4 * k + (lane & 3)) * 4, 0, 0));
+  };
+  auto row = [&](int64_t r, const f4v(&d)[kGradF], const float(&hA)[KQ]) {
+    float dh[NV];
 #pragma unroll
-      for (int k = 0; k < KQ; ++k) hA[u][k] = 0.0f;
-      if (u < nr) {
-        const int64_t r = rb + u;
-        const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<float*>(DS) + r * PC4 * 4, (short)0, PC4 * 16, 0x00020000);
+    for (int f = 0; f < kGradF; ++f) {
 #pragma unroll
-        for (int f = 0; f < kGradF; ++f)
-          if (col4[f] < PC4)
-            d[u][f] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(rr, col4[f] * 16, 0, kNT));
+      for (int c4 = 0; c4 < 4; ++c4)
 #pragma unroll
-        for (int k = 0; k < KQ; ++k) {
-          const int j = 4 * k + (lane & 3);
-          hA[u][k] = j < K ? h[r * K + j] : 0.0f;
-        }
+        for (int k = 0; k < KQ; ++k)
+          acc[f][c4][k] = __builtin_amdgcn_mfma_f32_4x4x1f32(hA[k], d[f][c4], acc[f][c4][k], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        const float t = d[f][0] * wv[f][j][0] + d[f][1] * wv[f][j][1] + d[f][2] * wv[f][j][2] + d[f][3] * wv[f][j][3];
+        dh[j] = f == 0 ? t : dh[j] + t;
       }
     }
+    float tot;
+    if constexpr (NV == 8)
+      tot = wave_reduce8(dh, lane);
+    else
+      tot = wave_reduce16(dh, lane);
+    if ((lane & (kWave / NV - 1)) == 0) DHp[((int64_t)sl * n_rows + r) * NV + lane / (kWave / NV)] = tot;
+  };
+  int64_t rb = r0;
+  if constexpr (E3_GRAD_DB) {
+    // two batches of rows in flight: the next batch loads while this one computes
+    const int64_t nb = (r1 - r0) / kGradRows;
+    f4v dA[kGradRows][kGradF], dB[kGradRows][kGradF];
+    float hA[kGradRows][KQ], hB[kGradRows][KQ];
+    auto load_batch = [&](int64_t b, f4v(&d)[kGradRows][kGradF], float(&hh)[kGradRows][KQ]) {
 #pragma unroll
-    for (int u = 0; u < kGradRows; ++u) {
-      if (u < nr) {
-        float dh[NV];
+      for (int u = 0; u < kGradRows; ++u) load_row(r0 + b * kGradRows + u, d[u], hh[u]);
+    };
+    auto run_batch = [&](int64_t b, const f4v(&d)[kGradRows][kGradF], const float(&hh)[kGradRows][KQ]) {
 #pragma unroll
-        for (int j = 0; j < NV; ++j) dh[j] = 0.0f;
-#pragma unroll
-        for (int f = 0; f < kGradF; ++f) {
-#pragma unroll
-          for (int c4 = 0; c4 < 4; ++c4)
-#pragma unroll
-            for (int k = 0; k < KQ; ++k)
-              acc[f][c4][k] = __builtin_amdgcn_mfma_f32_4x4x1f32(hA[u][k], d[u][f][c4], acc[f][c4][k], 0, 0, 0);
-#pragma unroll
-          for (int j = 0; j < NV; ++j)
-            dh[j] += d[u][f][0] * wv[f][j][0] + d[u][f][1] * wv[f][j][1] + d[u][f][2] * wv[f][j][2] +
-                     d[u][f][3] * wv[f][j][3];
-        }
-        float tot;
-        if constexpr (NV == 8)
-          tot = wave_reduce8(dh, lane);
-        else
-          tot = wave_reduce16(dh, lane);
-        if ((lane & (kWave / NV - 1)) == 0)
-          DHp[((int64_t)sl * n_rows + rb + u) * NV + lane / (kWave / NV)] = tot;
+      for (int u = 0; u < kGradRows; ++u) row(r0 + b * kGradRows + u, d[u], hh[u]);
+    };
+    if (nb > 0) load_batch(0, dA, hA);
+    for (int64_t b = 0; b < nb; b += 2) {
+      if (b + 1 < nb) load_batch(b + 1, dB, hB);
+      run_batch(b, dA, hA);
+      if (b + 1 < nb) {
+        if (b + 2 < nb) load_batch(b + 2, dA, hA);
+        run_batch(b + 1, dB, hB);
       }
     }
+    rb = r0 + nb * kGradRows;
+  } else {
+    for (; rb + kGradRows <= r1; rb += kGradRows) {
+      f4v d[kGradRows][kGradF];
+      float hA[kGradRows][KQ];
+#pragma unroll
+      for (int u = 0; u < kGradRows; ++u) load_row(rb + u, d[u], hA[u]);
+#pragma unroll
+      for (int u = 0; u < kGradRows; ++u) row(rb + u, d[u], hA[u]);
+    }
+  }
+  for (; rb < r1; ++rb) {
+    f4v d[kGradF];
+    float hA[KQ];
+    load_row(rb, d, hA);
+    row(rb, d, hA);
   }
   // dWp[c][j][col]: register i of acc[f][c4][k] is j = 4k + i, column 4 col4[f] + c4
   float* out = dWp + (int64_t)c * K * PC4 * 4;
@@ -1534,11 +1588,13 @@ __global__ __launch_bounds__(256) void k_lin_dw_sum(const float* __restrict__ dW
 // ------------------------------------------------------------ generic records
 // Tensor product with caller-supplied records (App. E.2's unfolded form):
 //   out[r, o, q] = sum over the records of segment o of v A[r, a, q] B[r, b, (q)]
-// Records are streamed through the scalar unit (uniform loads), segment by
-// segment; the two operand rows of the wave's (row, 64-channel slab) are staged
-// in LDS.  The backward is the same kernel on permuted record tables (eq.
-// tp-bwd); with RED the outputs are summed over the channels (a shared y's
-// cotangent): per-slab partials in fixed lane order, then k_tpg_sum.
+// A wave takes RB rows of one 64-channel slab.  The operand rows are staged in
+// LDS as [a][row][lane] (so one address serves the RB rows of a record), the
+// records and segment offsets are read-only for the launch and come through
+// the scalar cache, and each record feeds RB fused multiply-adds.  The
+// backward is the same kernel on permuted record tables (eq. tp-bwd); with RED
+// the outputs are summed over the channels (a shared y's cotangent): per-slab
+// partials in fixed lane order, then k_tpg_sum.
 struct TpgRec {
   int a, b;
   float v;
@@ -1560,43 +1616,93 @@ struct TpgArgs {
   int C, nslab, dA, dB, dout;
 };
 
-template <class T, bool BSH, bool RED>
+template <class T>
+using ConstPtr = const __attribute__((address_space(4))) T*;
+
+template <class T>
+__device__ __forceinline__ T buf_ld(__amdgpu_buffer_rsrc_t r, int off) {
+  if constexpr (sizeof(T) == 8)
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+  else
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
+template <class T, bool BSH, bool RED, int RB>
 __global__ __launch_bounds__(kWave) void k_tpg(TpgArgs<T> a) {
+  using Rec = typename std::conditional<sizeof(T) == 8, TpgRec64, TpgRec>::type;
+  const ConstPtr<Rec> recs = (ConstPtr<Rec>)a.recs;
+  const ConstPtr<int> seg = (ConstPtr<int>)a.seg;
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* lds = reinterpret_cast<T*>(lds_raw);
   const int sl = blockIdx.x % a.nslab;
-  const int64_t r = blockIdx.x / a.nslab;
+  const int64_t r0 = (int64_t)(blockIdx.x / a.nslab) * RB;
+  const int nr = a.rows - r0 < RB ? (int)(a.rows - r0) : RB;
   const int lane = threadIdx.x, q = sl * kWave + lane;
   const bool act = q < a.C;
-  T* sA = lds;
-  T* sB = sA + a.dA * kWave;
-  T* sP = sB + (BSH ? ((a.dB + 3) & ~3) : a.dB * kWave);
-  for (int i = 0; i < a.dA; ++i) sA[i * kWave + lane] = act ? a.A[(r * a.dA + i) * a.C + q] : T(0);
+  T* sA = lds;                                                        // [dA][RB][64]
+  T* sB = sA + a.dA * RB * kWave;                                     // BSH: [dB][RB], else [dB][RB][64]
+  T* sP = sB + (BSH ? ((a.dB * RB + 3) & ~3) : a.dB * RB * kWave);    // RED: [dout][RB][64]
+  // Operand loads through descriptors bounded by the block's rows: rows past
+  // the end read zero; lanes past C are zeroed (their sums enter RED's total).
+  const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>(a.A) + r0 * a.dA * a.C, (short)0, (int)((int64_t)nr * a.dA * a.C * sizeof(T)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>(a.B) + r0 * a.dB * (BSH ? 1 : a.C), (short)0,
+      (int)((int64_t)nr * a.dB * (BSH ? 1 : a.C) * sizeof(T)), 0x00020000);
+#pragma unroll 8
+  for (int i = 0; i < a.dA * RB; ++i) {
+    const int ai = i / RB, u = i % RB;
+    const T v = buf_ld<T>(ar, (int)(((u * a.dA + ai) * a.C + q) * sizeof(T)));
+    sA[i * kWave + lane] = act ? v : T(0);
+  }
   if constexpr (BSH) {
-    for (int i = lane; i < a.dB; i += kWave) sB[i] = a.B[r * a.dB + i];
+    for (int i = lane; i < a.dB * RB; i += kWave) {
+      const int bi = i / RB, u = i % RB;
+      sB[i] = buf_ld<T>(br, (int)((u * a.dB + bi) * sizeof(T)));
+    }
   } else {
-    for (int i = 0; i < a.dB; ++i) sB[i * kWave + lane] = act ? a.B[(r * a.dB + i) * a.C + q] : T(0);
+#pragma unroll 8
+    for (int i = 0; i < a.dB * RB; ++i) {
+      const int bi = i / RB, u = i % RB;
+      const T v = buf_ld<T>(br, (int)(((u * a.dB + bi) * a.C + q) * sizeof(T)));
+      sB[i * kWave + lane] = act ? v : T(0);
+    }
   }
   __syncthreads();
+  int k = seg[0];
   for (int o = 0; o < a.dout; ++o) {
-    T acc = T(0);
-    const int k1 = a.seg[o + 1];
-    for (int k = a.seg[o]; k < k1; ++k) {
-      const auto rc = a.recs[k];
-      const T bv = BSH ? sB[rc.b] : sB[rc.b * kWave + lane];
-      acc = fma(T(rc.v) * sA[rc.a * kWave + lane], bv, acc);
+    const int k1 = seg[o + 1];
+    T acc[RB];
+#pragma unroll
+    for (int u = 0; u < RB; ++u) acc[u] = T(0);
+#pragma unroll 2
+    for (; k < k1; ++k) {
+      const int ra = recs[k].a, rbi = recs[k].b;
+      const T rv = T(recs[k].v);
+      const T* pa = sA + ra * RB * kWave + lane;
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const T bv = BSH ? sB[rbi * RB + u] : sB[(rbi * RB + u) * kWave + lane];
+        acc[u] = fma(rv * pa[u * kWave], bv, acc[u]);
+      }
     }
-    if constexpr (RED)
-      sP[o * kWave + lane] = acc;
-    else if (act)
-      a.out[(r * a.dout + o) * a.C + q] = acc;
+    if constexpr (RED) {
+#pragma unroll
+      for (int u = 0; u < RB; ++u) sP[(o * RB + u) * kWave + lane] = acc[u];
+    } else if (act) {
+#pragma unroll
+      for (int u = 0; u < RB; ++u)
+        if (u < nr) a.out[((r0 + u) * a.dout + o) * a.C + q] = acc[u];
+    }
   }
   if constexpr (RED) {
     __syncthreads();
-    for (int o = lane; o < a.dout; o += kWave) {
+    for (int i = lane; i < a.dout * RB; i += kWave) {
+      const int o = i / RB, u = i % RB;
+      if (u >= nr) continue;
       T t = T(0);
-      for (int l = 0; l < kWave; ++l) t += sP[o * kWave + l];
-      a.part[(r * a.nslab + sl) * a.dout + o] = t;
+      for (int l = 0; l < kWave; ++l) t += sP[i * kWave + l];
+      a.part[((r0 + u) * a.nslab + sl) * a.dout + o] = t;
     }
   }
 }
@@ -2793,8 +2899,9 @@ e3_status tpg_upload(e3_tpg* G, hipStream_t st) {
   return E3_OK;
 }
 
-size_t tpg_lds(int dA, int dB, int dout, bool bsh, bool red, size_t elem = sizeof(float)) {
-  return ((size_t)dA * kWave + (bsh ? ((dB + 3) & ~3) : (size_t)dB * kWave) + (red ? (size_t)dout * kWave : 0)) *
+size_t tpg_lds(int dA, int dB, int dout, bool bsh, bool red, size_t elem = sizeof(float), int rb = 1) {
+  return ((size_t)dA * rb * kWave + (bsh ? (((size_t)dB * rb + 3) & ~3) : (size_t)dB * rb * kWave) +
+          (red ? (size_t)dout * rb * kWave : 0)) *
          elem;
 }
 constexpr size_t kTpgMaxLds = 64 * 1024;
@@ -2809,19 +2916,33 @@ e3_status tpg_run(const e3_tpg* G, int which, const T* A, int dA, const T* B, in
   a.recs = reinterpret_cast<decltype(a.recs)>(G->dev + (sizeof(T) == 8 ? Tb.off_recs64 : Tb.off_recs));
   a.rows = rows, a.C = C, a.nslab = (C + kWave - 1) / kWave, a.dA = dA, a.dB = dB;
   a.dout = (int)Tb.seg.size() - 1;
-  const size_t lds = tpg_lds(dA, dB, a.dout, bsh, red, sizeof(T));
+  // rows per wave: the most of 4, 2, 1 whose staging fits the LDS limit
+  int rb = 4;
+  while (rb > 1 && tpg_lds(dA, dB, a.dout, bsh, red, sizeof(T), rb) > kTpgMaxLds) rb /= 2;
+  const size_t lds = tpg_lds(dA, dB, a.dout, bsh, red, sizeof(T), rb);
   if (lds > kTpgMaxLds) return E3_ERR_UNSUPPORTED;
-  const int64_t grid = rows * a.nslab;
+  // operand blocks are addressed with 32-bit byte offsets
+  if ((int64_t)rb * std::max(dA, dB) * C * (int64_t)sizeof(T) > 0x7fffffff) return E3_ERR_INVALID_ARG;
+  const int64_t grid = (rows + rb - 1) / rb * a.nslab;
   if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
   TimedLaunch t_(name, st);
-  if (bsh && red)
-    hipLaunchKernelGGL((k_tpg<T, true, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
-  else if (bsh)
-    hipLaunchKernelGGL((k_tpg<T, true, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
-  else if (red)
-    hipLaunchKernelGGL((k_tpg<T, false, true>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+  auto go = [&](auto RBc) {
+    constexpr int R = decltype(RBc)::value;
+    if (bsh && red)
+      hipLaunchKernelGGL((k_tpg<T, true, true, R>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    else if (bsh)
+      hipLaunchKernelGGL((k_tpg<T, true, false, R>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    else if (red)
+      hipLaunchKernelGGL((k_tpg<T, false, true, R>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    else
+      hipLaunchKernelGGL((k_tpg<T, false, false, R>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+  };
+  if (rb == 4)
+    go(std::integral_constant<int, 4>{});
+  else if (rb == 2)
+    go(std::integral_constant<int, 2>{});
   else
-    hipLaunchKernelGGL((k_tpg<T, false, false>), dim3((unsigned)grid), dim3(kWave), lds, st, a);
+    go(std::integral_constant<int, 1>{});
   E3_HIP(hipGetLastError());
   return E3_OK;
 }
