@@ -525,7 +525,10 @@ __global__ __launch_bounds__(256) void k_tp_bwd_dy(const float* __restrict__ DY,
 }
 
 // ------------------------------------------------------------ convolution
-constexpr int kEdgeBatch = 16;  // edges whose pre-contraction is staged per LDS batch
+#ifndef E3_EDGE_BATCH
+#define E3_EDGE_BATCH 16
+#endif
+constexpr int kEdgeBatch = E3_EDGE_BATCH;  // edges whose pre-contraction is staged per LDS batch
 
 struct ConvArgs {
   const float* x;

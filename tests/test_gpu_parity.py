@@ -759,12 +759,21 @@ def _layout_records(lay):
 
 
 @pytest.mark.parametrize("case", ["layout-shared", "layout-perchannel", "random-shared", "random-perchannel",
-                                  "collapsed", "C7"])
+                                  "collapsed", "C7", "layout-l2in"])
 def test_record_tp_parity(e3, case):
+    """Records against the oracle.  The operand staging decides the rows per
+    wave (4, 2 or 1 within 64 KiB of LDS): the l <= 3 input layout runs its
+    forward at 4 and its backward at 1, the l <= 2 input layout (106 output
+    rows) its dx at 2; R = 57 leaves a ragged last block for each."""
     import torch
     _say("record tp", case)
     rng = np.random.default_rng(61)
-    if case in ("layout-shared", "layout-perchannel", "C7"):
+    if case == "layout-l2in":
+        lay = oirreps.layout("8x0e+8x1o+8x2e", 3, 3)
+        i0, i1, i2, v = _layout_records(lay)
+        dx_, dy_, dz_ = lay.d_in, lay.d_sh, lay.d_out
+        C = 100
+    elif case in ("layout-shared", "layout-perchannel", "C7"):
         lay = oirreps.layout("8x0e+8x1o+8x2e+8x3o", 3, 3)
         i0, i1, i2, v = _layout_records(lay)
         dx_, dy_, dz_ = lay.d_in, lay.d_sh, lay.d_out
