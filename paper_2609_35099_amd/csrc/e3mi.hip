@@ -206,6 +206,11 @@ __device__ __forceinline__ RowBuf row_buf(const float* base, int64_t nbytes, int
   return b;
 }
 
+// Read-only tables (records, job lists) through the constant address space,
+// so that uniform reads become scalar loads.
+template <class T>
+using ConstPtr = const __attribute__((address_space(4))) T*;
+
 constexpr int kNT = 2;  // non-temporal loads of data streamed once
 // Stores of streamed outputs: non-temporal.  A pure write stream runs faster
 // with plain stores on MI355X, but in these mixed read/write kernels plain
@@ -1408,6 +1413,9 @@ __global__ __launch_bounds__(256) void k_rad_dh_sum(const float* __restrict__ DH
 constexpr int kLinMaxJobs = 64;
 constexpr int kLinChunks = 64;  // row chunks of the dW reduction (fixed: deterministic)
 constexpr int kLinRT = 4;       // 16-row subtiles per wave in the gather-GEMM
+#ifndef E3_LIN_V4
+#define E3_LIN_V4 1
+#endif
 
 struct LinJob {
   int R, dst_row, src_first, nsrc;
@@ -1432,7 +1440,10 @@ struct LinArgs {
   int first[kLinMaxJobs + 1];
 };
 
-template <int RT>  // RT subtiles of 16 rows per wave
+// V4 (unit column stride, 16-byte aligned W, C_dst a multiple of 4): lane l
+// owns the four consecutive columns col0 + 4 (l % 16) .. +3, so one float4 of
+// a W row gives B of all four column blocks, and the results leave as float4s.
+template <int RT, bool V4>  // RT subtiles of 16 rows per wave
 __global__ __launch_bounds__(kWave) void k_lin_gemm(LinArgs a) {
   const int unit = blockIdx.x;
   int lo = 0, hi = a.njobs - 1;
@@ -1459,6 +1470,64 @@ __global__ __launch_bounds__(kWave) void k_lin_gemm(LinArgs a) {
     aval[s] = r < NR;
     const int64_t nd = aval[s] ? r / jb.R : 0, m = aval[s] ? r % jb.R : 0;
     abase[s] = (nd * a.D_src + m) * a.C_src + 4 * g;
+  }
+  if constexpr (V4) {
+    // Rows past NR and columns past C_dst load in-bounds data of other rows or
+    // read zero; the instruction keeps rows and columns apart and those results
+    // are not stored, so no masking is needed.  The A rows of the next
+    // (source, k-step) load while this one runs.
+    const int colv = col0 + 4 * li;
+    const bool cv = colv < a.C_dst;
+    const ConstPtr<LinSrc> srcs = (ConstPtr<LinSrc>)a.srcs;
+    const int ksteps = a.C_src / 16, nsteps = jb.nsrc * ksteps;
+    const int bvoff = ((4 * g) * a.ldk + colv) * 4;
+    auto load_a = [&](int i, f4v(&v)[RT]) {
+      const int t = i / ksteps;
+      const float* sp = a.src + (int64_t)srcs[jb.src_first + t].row * a.C_src + (i - t * ksteps) * 16;
+#pragma unroll
+      for (int s = 0; s < RT; ++s) v[s] = *reinterpret_cast<const f4v*>(sp + abase[s]);
+    };
+    // one (source, k-step): W (cache-resident) first, then the A rows of step
+    // i + 1 (clamped, so the loads are unconditional and the waits count
+    // exactly; loads complete in issue order), then the 64 instructions
+    auto step = [&](int i, const f4v(&av)[RT], f4v(&an)[RT]) {
+      const int t = i / ksteps, k0 = (i - t * ksteps) * 16;
+      const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(a.W + srcs[jb.src_first + t].w_off), (short)0, a.C_src * a.C_dst * 4, 0x00020000);
+      f4v bq[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        bq[c] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(wr, bvoff, (k0 + c) * a.ldk * 4, 0));
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(i + 1 < nsteps ? i + 1 : i, an);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+          for (int s = 0; s < RT; ++s)
+            acc[s][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s][c], bq[c][cb], acc[s][cb], 0, 0, 0);
+    };
+    f4v a0[RT], a1[RT];
+    if (nsteps > 0) load_a(0, a0);
+    for (int i = 0; i < nsteps; i += 2) {
+      step(i, a0, a1);
+      if (i + 1 < nsteps) step(i + 1, a1, a0);
+    }
+    // register r of acc[s][cb] in lane l: row 16 s + 4 (l / 16) + r, column col0 + 4 (l % 16) + cb
+    if (!cv) return;
+#pragma unroll
+    for (int s = 0; s < RT; ++s)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = r0 + 16 * s + 4 * g + r;
+        if (row >= NR) continue;
+        const int64_t nd = row / jb.R, m = row % jb.R;
+        float* dp = a.dst + (nd * a.D_dst + jb.dst_row + m) * a.C_dst;
+        *reinterpret_cast<f4v*>(dp + colv) = f4v{acc[s][0][r], acc[s][1][r], acc[s][2][r], acc[s][3][r]};
+      }
+    return;
   }
   // B[k][col] = W[w_off + k ldk + col ldc]: per-lane part in the vector offset,
   // the k step and column block in the (uniform) scalar offset; columns past
@@ -1538,8 +1607,8 @@ __global__ __launch_bounds__(kWave) void k_lin_dw(LinDwArgs a) {
   const int chunk = u / (a.ktiles * a.jtiles), kt = (u / a.jtiles) % a.ktiles, jt = u % a.jtiles;
   const LinPair pr = a.pairs[p];
   const int64_t NR = a.n * pr.R;
-  const int64_t rpc = (NR + kLinChunks - 1) / kLinChunks;
-  const int64_t rb = chunk * rpc, re = rb + rpc < NR ? rb + rpc : NR;
+  const int64_t rpc = ((NR + kLinChunks - 1) / kLinChunks + 15) / 16 * 16;  // rows per chunk, a multiple of 16
+  const int64_t rb = chunk * rpc < NR ? chunk * rpc : NR, re = rb + rpc < NR ? rb + rpc : NR;
   const int lane = threadIdx.x, g = lane >> 4, li = lane & 15;
   f4v acc[4][4];
 #pragma unroll
@@ -1548,18 +1617,71 @@ __global__ __launch_bounds__(kWave) void k_lin_dw(LinDwArgs a) {
     for (int j = 0; j < 4; ++j) acc[i][j] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
   const int kc = kt * 64 + 4 * li, jc = jt * 64 + 4 * li;  // multiples of 4; C_in, C_out are of 16
   const bool kv = kc < a.C_in, jv = jc < a.C_out;
-  for (int64_t r = rb; r < re; r += 4) {
-    const int64_t row = r + g;
-    const bool ok = row < re;
-    const int64_t nd = ok ? row / pr.R : 0, m = ok ? row % pr.R : 0;
-    const f4v xa = ok && kv ? *reinterpret_cast<const f4v*>(a.x + (nd * a.D_in + pr.src_row + m) * a.C_in + kc)
-                            : f4v{0.0f, 0.0f, 0.0f, 0.0f};
-    const f4v db = ok && jv ? *reinterpret_cast<const f4v*>(a.dout + (nd * a.D_out + pr.dst_row + m) * a.C_out + jc)
-                            : f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  // Lane rows rb + g, rb + g + 4, ...: the (node, m) position steps by four
+  // rows without a division.  Columns past C_in / C_out read column 0; their
+  // results are not stored.
+  const int R = pr.R, dq = 4 / R, dr = 4 % R;
+  int64_t row = rb + g;
+  int m = (int)(row % R);
+  int64_t ox = ((row / R) * a.D_in + pr.src_row + m) * a.C_in + (kv ? kc : 0);
+  int64_t od = ((row / R) * a.D_out + pr.dst_row + m) * a.C_out + (jv ? jc : 0);
+  const int64_t sx = ((int64_t)dq * a.D_in + dr) * a.C_in, wx = (int64_t)(a.D_in - R) * a.C_in;
+  const int64_t sd = ((int64_t)dq * a.D_out + dr) * a.C_out, wd = (int64_t)(a.D_out - R) * a.C_out;
+  auto advance = [&]() {
+    const bool w = m + dr >= R;
+    row += 4;
+    m += w ? dr - R : dr;
+    ox += w ? sx + wx : sx;
+    od += w ? sd + wd : sd;
+  };
+  auto group = [&](const f4v& xa, const f4v& db) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i], db[j], acc[i][j], 0, 0, 0);
+  };
+  // Whole fetches of 16 rows (chunks are sized in multiples of 16 rows, so
+  // only the last chunk has a tail): no masking, the next fetch in flight.
+  // Every fetch is unconditional so that the waits count exactly; the one
+  // past the last whole fetch reads row rb again and is not used.
+  constexpr int S = 4;
+  const int64_t nf = (re - rb) / (4 * S), rfull = rb + nf * 4 * S;
+  const int64_t ox0 = ((rb / R) * a.D_in + pr.src_row + rb % R) * a.C_in + (kv ? kc : 0);
+  const int64_t od0 = ((rb / R) * a.D_out + pr.dst_row + rb % R) * a.C_out + (jv ? jc : 0);
+  auto fetch = [&](f4v(&xs)[S], f4v(&ds)[S]) {
+#pragma unroll
+    for (int q = 0; q < S; ++q) {
+      const bool ok = row < rfull;
+      xs[q] = *reinterpret_cast<const f4v*>(a.x + (ok ? ox : ox0));
+      ds[q] = *reinterpret_cast<const f4v*>(a.dout + (ok ? od : od0));
+      advance();
+    }
+  };
+  if (nf > 0) {
+    f4v xA[S], dA[S], xB[S], dB[S];
+    fetch(xA, dA);
+    for (int64_t f = 0; f < nf; ++f) {
+      fetch(xB, dB);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < S; ++q) group(xA[q], dA[q]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < S; ++q) xA[q] = xB[q], dA[q] = dB[q];
+    }
+    // the state ran one fetch ahead: step back to the first row after the whole fetches
+    row = rb + g + nf * 4 * S;
+    m = (int)(row % R);
+    ox = ((row / R) * a.D_in + pr.src_row + m) * a.C_in + (kv ? kc : 0);
+    od = ((row / R) * a.D_out + pr.dst_row + m) * a.C_out + (jv ? jc : 0);
+  }
+  // the last chunk's tail: four-row groups, rows past re read as zero
+  for (int64_t r = rb + nf * 4 * S; r < re; r += 4) {
+    const bool ok = row < re;
+    const f4v xa = ok ? *reinterpret_cast<const f4v*>(a.x + ox) : f4v{0.0f, 0.0f, 0.0f, 0.0f};
+    const f4v db = ok ? *reinterpret_cast<const f4v*>(a.dout + od) : f4v{0.0f, 0.0f, 0.0f, 0.0f};
+    group(xa, db);
+    advance();
   }
   // register r of acc[a][b] in lane l: k = k-tile + 4 (4 (l / 16) + r) + a, j = j-tile + 4 (l % 16) + b
   float* out = a.dWp + ((int64_t)p * kLinChunks + chunk) * a.C_in * a.C_out;
@@ -1619,8 +1741,6 @@ struct TpgArgs {
   int C, nslab, dA, dB, dout;
 };
 
-template <class T>
-using ConstPtr = const __attribute__((address_space(4))) T*;
 
 template <class T>
 __device__ __forceinline__ T buf_ld(__amdgpu_buffer_rsrc_t r, int off) {
@@ -2687,7 +2807,10 @@ e3_status lin_gemm(const std::vector<LinJob>& jobs, const LinJob* djobs, const L
   if (u == 0) return E3_OK;
   if (u > 0x7fffffff) return E3_ERR_INVALID_ARG;
   TimedLaunch t_(name, st);
-  hipLaunchKernelGGL(k_lin_gemm<kLinRT>, dim3((unsigned)u), dim3(kWave), 0, st, a);
+  if (ldc == 1 && C_dst % 4 == 0 && aligned16(W) && E3_LIN_V4)
+    hipLaunchKernelGGL((k_lin_gemm<kLinRT, true>), dim3((unsigned)u), dim3(kWave), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_lin_gemm<kLinRT, false>), dim3((unsigned)u), dim3(kWave), 0, st, a);
   E3_HIP(hipGetLastError());
   return E3_OK;
 }
