@@ -253,7 +253,10 @@ e3_status e3_linear_bwd(e3_linear* lin, const float* x, const float* W, const fl
  * x [rows, d_x, C], y [rows, d_y, C] or [rows, d_y], z [rows, d_z, C]; any
  * C >= 1.  Records are copied at create (index errors: E3_ERR_INDEX_OUT_OF_RANGE);
  * operand rows must fit 64 KiB of staging per 64 channels (else
- * E3_ERR_UNSUPPORTED).  Tables are uploaded to the device on first use.
+ * E3_ERR_UNSUPPORTED).  A wave stages up to four rows (as many as fit the
+ * limit); an operand block of those rows, d C element bytes per row, must stay
+ * under 2 GiB (else E3_ERR_INVALID_ARG).  Tables are uploaded to the device
+ * on first use.
  * e3_tpg_bwd (eq. tp-bwd): dx = tensor_product(C^{i1}_{i2 i0}, y, dz) and
  *   dy = tensor_product(C^{i2}_{i1 i0}, x, dz), summed over the channels when y
  *   is shared (then ws holds per-slab partials, e3_tpg_workspace_size bytes,
