@@ -249,6 +249,62 @@ def cpu_baseline(cfg, g, x, dm, seconds=12.0):
             "cpu": cpu_model(), "numpy": np.__version__, "torch_threads": torch.get_num_threads()}
 
 
+def oracle_configs():
+    """The fp64 oracle on whole workloads of the three small configurations, on
+    the host cores (a reported baseline): convolution forward + backward of the
+    64-atom cube and the 1,000-molecule water box, and the weighted tensor
+    product of 200,000 rows (in chunks of 8,192 rows).  Best of three where one
+    run takes under 30 s, else one run."""
+    import torch
+    from oracle import conv as oconv
+    from oracle import irreps as oirreps
+    from oracle import sh as osh
+    from oracle import tp as otp
+    res = {}
+
+    def timed(fn):
+        best, n = float("inf"), 0
+        while n < 3:
+            t0 = time.perf_counter()
+            fn()
+            dt = time.perf_counter() - t0
+            best, n = min(best, dt), n + 1
+            if dt >= 30.0:
+                break
+        return best, n
+
+    for name in ("cube64", "water1k"):
+        cfg = synth.CONFIGS[name]
+        g = synth.graph(cfg)
+        lay = oirreps.layout(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+        E = int(g.sender.shape[0])
+        x = synth.node_features(cfg, g.n_nodes)
+        s = synth.edge_weights(cfg, g.vec, 0, E)
+        dm = synth.out_cotangent(cfg, g.n_nodes)
+        tf, nf = timed(lambda: oconv.conv_fwd(lay, x, g.vec, s, g.sender, g.receiver, g.n_nodes))
+        tb, nb = timed(lambda: oconv.conv_bwd(lay, x, g.vec, s, dm, g.sender, g.receiver, g.n_nodes))
+        res[name] = {"edges": E, "fwd_s": round(tf, 3), "bwd_s": round(tb, 3), "runs": [nf, nb],
+                     "edges_per_s": round(E / (tf + tb), 1)}
+        log(f"oracle {name}: {res[name]}")
+    cfg = synth.CONFIGS["tp200k"]
+    lay = oirreps.layout(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    x, u, w = synth.tp_inputs(cfg)
+    y = osh.sh_unit(cfg.lmax_sh, u.astype(np.float64))
+    R, chunk = x.shape[0], 8192
+
+    def tp_all():
+        for r0 in range(0, R, chunk):
+            otp.tp(lay, x[r0:r0 + chunk], y[r0:r0 + chunk], w[r0:r0 + chunk])
+
+    tt, nt = timed(tp_all)
+    res["tp200k"] = {"rows": R, "fwd_s": round(tt, 3), "runs": nt, "rows_per_s": round(R / tt, 1)}
+    log(f"oracle tp200k: {res['tp200k']}")
+    return {"kind": "oracle", "dtype": "f64", "configs": res, "cpu": cpu_model(), "numpy": np.__version__,
+            "torch_threads": torch.get_num_threads(), "affinity_cores": len(os.sched_getaffinity(0)),
+            "blas_env": {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS",
+                                                        "MKL_NUM_THREADS") if os.environ.get(k)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -264,7 +320,13 @@ def main():
                          "convolution throughput table); generates ten water boxes first")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one plain 2 GiB device copy (calibrates HBM byte counters)")
+    ap.add_argument("--oracle-configs", action="store_true",
+                    help="only time the fp64 oracle on the whole small workloads (64-atom cube, 1,000-molecule "
+                         "water box, 200,000-row tensor product) on the host cores, print one JSON line, exit")
     args = ap.parse_args()
+    if args.oracle_configs:
+        print(json.dumps(oracle_configs()), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               f"(the per-GPU kernel on its share is the unit measured)", file=sys.stderr)
