@@ -97,6 +97,33 @@ struct TimedLaunch {
 constexpr int kWave = 64;
 constexpr int kXcd = 8;
 
+// Row-tile kernels (tensor product, its backward, the record path): block ->
+// (tile, part).  With XCD, the `per` parts (groups, channel slabs) of tile T
+// run on XCD T % 8 in consecutive dispatch rounds, so that the parts of one
+// row, which read the neighbouring pieces of its rows, run on one XCD
+// together; otherwise the parts of a tile are consecutive blocks.  The grid
+// is tile_grid(...) blocks; blocks past the last tile return false.
+#ifndef E3_TP_XCD
+#define E3_TP_XCD 1
+#endif
+template <bool XCD>
+__device__ __forceinline__ bool tile_of(int64_t rows, int rows_per_tile, int per, int64_t& tile, int& part) {
+  const int64_t ntiles = (rows + rows_per_tile - 1) / rows_per_tile;
+  if constexpr (XCD) {
+    const int64_t u = blockIdx.x / kXcd;
+    part = (int)(u % per);
+    tile = (u / per) * kXcd + blockIdx.x % kXcd;
+  } else {
+    part = (int)(blockIdx.x % per);
+    tile = blockIdx.x / per;
+  }
+  return tile < ntiles;
+}
+inline int64_t tile_grid(bool xcd, int64_t rows, int rows_per_tile, int per) {
+  const int64_t ntiles = (rows + rows_per_tile - 1) / rows_per_tile;
+  return (xcd ? (ntiles + kXcd - 1) / kXcd * kXcd : ntiles) * per;
+}
+
 // Build-time tuning knobs: minimum resident waves per SIMD requested from the
 // compiler for the forward and backward sweeps, and channels per lane of the
 // backward sweep when C > 64.
@@ -214,7 +241,8 @@ using ConstPtr = const __attribute__((address_space(4))) T*;
 constexpr int kNT = 2;  // non-temporal loads of data streamed once
 // Stores of streamed outputs: non-temporal.  A pure write stream runs faster
 // with plain stores on MI355X, but in these mixed read/write kernels plain
-// stores were measured equal or slower (TP backward 3.86 ms against 3.44 ms).
+// stores were measured equal or slower (TP forward equal, TP backward 3.85 ms
+// against 3.43 ms, convolution step 21.3 ms against 20.8 ms).
 #ifndef E3_STORE_AUX
 #define E3_STORE_AUX 2
 #endif
@@ -389,10 +417,12 @@ __global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const
   __shared__ f4v smem[(kTpRows * T::NA + 3) / 4];
   float* sA = reinterpret_cast<float*>(smem);
   const int lane = threadIdx.x;
-  const int sl = blockIdx.x % nslab;
+  int sl;
+  int64_t tile;
+  if (!tile_of<false>(rows, kTpRows, nslab, tile, sl)) return;
   int ch0, lanes;
   slab_of<CPL>(C, sl, ch0, lanes);
-  const int64_t r0 = (int64_t)(blockIdx.x / nslab) * kTpRows;
+  const int64_t r0 = tile * kTpRows;
   const int n = (int)((rows - r0) < kTpRows ? (rows - r0) : kTpRows);
   if (lane < n) {
     float Y[V::D_SH];
@@ -506,9 +536,10 @@ __device__ __forceinline__ void tpb_dispatch(const TpbArgs& a, int64_t r0, int g
 template <class V, int CPL>
 __global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_tp_bwd(TpbArgs a) {
   __shared__ f4v smem[(kTpRows * (V::MAX_NA_B + V::D_SH) + 3) / 4];
-  const int per = V::NBG * a.nslab;
-  const int t = blockIdx.x % per;
-  const int64_t r0 = (int64_t)(blockIdx.x / per) * kTpRows;
+  int t;
+  int64_t tile;
+  if (!tile_of<E3_TP_XCD>(a.rows, kTpRows, V::NBG * a.nslab, tile, t)) return;
+  const int64_t r0 = tile * kTpRows;
   float* sA = reinterpret_cast<float*>(smem);
   tpb_dispatch<V, 0, CPL>(a, r0, t / a.nslab, t % a.nslab, sA, sA + kTpRows * V::MAX_NA_B);
 }
@@ -1757,8 +1788,10 @@ __global__ __launch_bounds__(kWave) void k_tpg(TpgArgs<T> a) {
   const ConstPtr<int> seg = (ConstPtr<int>)a.seg;
   extern __shared__ __align__(16) unsigned char lds_raw[];
   T* lds = reinterpret_cast<T*>(lds_raw);
-  const int sl = blockIdx.x % a.nslab;
-  const int64_t r0 = (int64_t)(blockIdx.x / a.nslab) * RB;
+  int sl;
+  int64_t tile;
+  if (!tile_of<false>(a.rows, RB, a.nslab, tile, sl)) return;
+  const int64_t r0 = tile * RB;
   const int nr = a.rows - r0 < RB ? (int)(a.rows - r0) : RB;
   const int lane = threadIdx.x, q = sl * kWave + lane;
   const bool act = q < a.C;
@@ -2039,9 +2072,8 @@ e3_status run_tp(const e3_plan* p, const float* x, const float* y, const float* 
   if (rows == 0) return E3_OK;
   {
     TimedLaunch t_("tp_fwd", st);
-    const int64_t tiles = (rows + kTpRows - 1) / kTpRows;
-    hipLaunchKernelGGL((k_tp<V, CPL>), dim3((unsigned)(tiles * p->nslab_f)), dim3(kWave), 0, st, x, y, w, z, rows,
-                       p->lay.C, p->nslab_f);
+    const dim3 grid((unsigned)tile_grid(false, rows, kTpRows, p->nslab_f));
+    hipLaunchKernelGGL((k_tp<V, CPL>), grid, dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, p->nslab_f);
   }
   E3_HIP(hipGetLastError());
   return E3_OK;
@@ -2057,10 +2089,11 @@ e3_status run_tp_bwd(const e3_plan* p, const float* x, const float* y, const flo
   a.rows = rows;
   a.C = p->lay.C;
   a.nslab = p->nslab_b;
-  const int64_t tiles = (rows + kTpRows - 1) / kTpRows;
   {
     TimedLaunch t_("tp_bwd", st);
-    hipLaunchKernelGGL((k_tp_bwd<V, CPL>), dim3((unsigned)(tiles * V::NBG * a.nslab)), dim3(kWave), 0, st, a);
+    // the (group, slab) waves of a row tile on one XCD: 3.42 -> 3.33 ms at 200,000 rows, l <= 3
+    const dim3 grid((unsigned)tile_grid(E3_TP_XCD, rows, kTpRows, V::NBG * a.nslab));
+    hipLaunchKernelGGL((k_tp_bwd<V, CPL>), grid, dim3(kWave), 0, st, a);
   }
   E3_HIP(hipGetLastError());
   {
@@ -3049,7 +3082,7 @@ e3_status tpg_run(const e3_tpg* G, int which, const T* A, int dA, const T* B, in
   if (lds > kTpgMaxLds) return E3_ERR_UNSUPPORTED;
   // operand blocks are addressed with 32-bit byte offsets
   if ((int64_t)rb * std::max(dA, dB) * C * (int64_t)sizeof(T) > 0x7fffffff) return E3_ERR_INVALID_ARG;
-  const int64_t grid = (rows + rb - 1) / rb * a.nslab;
+  const int64_t grid = tile_grid(false, rows, rb, a.nslab);
   if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
   TimedLaunch t_(name, st);
   auto go = [&](auto RBc) {
