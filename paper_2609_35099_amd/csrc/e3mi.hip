@@ -1443,7 +1443,10 @@ __global__ __launch_bounds__(256) void k_rad_dh_sum(const float* __restrict__ DH
 // transpose of the rows is needed.
 constexpr int kLinMaxJobs = 64;
 constexpr int kLinChunks = 64;  // row chunks of the dW reduction (fixed: deterministic)
-constexpr int kLinRT = 4;       // 16-row subtiles per wave in the gather-GEMM
+#ifndef E3_LIN_RT
+#define E3_LIN_RT 4
+#endif
+constexpr int kLinRT = E3_LIN_RT;  // 16-row subtiles per wave in the gather-GEMM
 #ifndef E3_LIN_V4
 #define E3_LIN_V4 1
 #endif
