@@ -663,34 +663,37 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
 #pragma unroll
         for (int i = 0; i < F::NPATH; ++i) bld<CPL, kNT>(sb_, F::PATH[i], sv[i]);
       };
-#if E3_FWD_PREFETCH3
-      // three register buffers: the rows of edges j+1 and j+2 are in flight while j computes
-      float xc[F::NXR][CPL], sc[F::NPATH][CPL];
-      load(0, xa, sa);
-      if (1 < n) load(1, xb, sb);
-      for (int j = 0; j < n; j += 3) {
-        if (j + 2 < n) load(j + 2, xc, sc);
-        F::template edge<CPL>(sA + j * F::NA, xa, sa, acc);
-        if (j + 1 < n) {
-          if (j + 3 < n) load(j + 3, xa, sa);
-          F::template edge<CPL>(sA + (j + 1) * F::NA, xb, sb, acc);
+      // a third register buffer where the group's footprint (sums and three
+      // x, s buffers) leaves room: above about 220 registers it spilled (the
+      // l <= 2 single-group layout, 25% slower than with two buffers)
+      if constexpr (E3_FWD_PREFETCH3 && (F::NROW + 3 * (F::NXR + F::NPATH)) * CPL <= 220) {
+        // the rows of edges j+1 and j+2 are in flight while j computes
+        float xc[F::NXR][CPL], sc[F::NPATH][CPL];
+        load(0, xa, sa);
+        if (1 < n) load(1, xb, sb);
+        for (int j = 0; j < n; j += 3) {
+          if (j + 2 < n) load(j + 2, xc, sc);
+          F::template edge<CPL>(sA + j * F::NA, xa, sa, acc);
+          if (j + 1 < n) {
+            if (j + 3 < n) load(j + 3, xa, sa);
+            F::template edge<CPL>(sA + (j + 1) * F::NA, xb, sb, acc);
+          }
+          if (j + 2 < n) {
+            if (j + 4 < n) load(j + 4, xb, sb);
+            F::template edge<CPL>(sA + (j + 2) * F::NA, xc, sc, acc);
+          }
         }
-        if (j + 2 < n) {
-          if (j + 4 < n) load(j + 4, xb, sb);
-          F::template edge<CPL>(sA + (j + 2) * F::NA, xc, sc, acc);
+      } else {
+        load(0, xa, sa);
+        for (int j = 0; j < n; j += 2) {
+          if (j + 1 < n) load(j + 1, xb, sb);
+          F::template edge<CPL>(sA + j * F::NA, xa, sa, acc);
+          if (j + 1 < n) {
+            if (j + 2 < n) load(j + 2, xa, sa);
+            F::template edge<CPL>(sA + (j + 1) * F::NA, xb, sb, acc);
+          }
         }
       }
-#else
-      load(0, xa, sa);
-      for (int j = 0; j < n; j += 2) {
-        if (j + 1 < n) load(j + 1, xb, sb);
-        F::template edge<CPL>(sA + j * F::NA, xa, sa, acc);
-        if (j + 1 < n) {
-          if (j + 2 < n) load(j + 2, xa, sa);
-          F::template edge<CPL>(sA + (j + 1) * F::NA, xb, sb, acc);
-        }
-      }
-#endif
     }
     __syncthreads();
   }
