@@ -103,15 +103,29 @@ def counter_util(kernel: str, metric: str):
 
 def fma_counts(plan):
     """FMA-equivalent VALU operations per edge and channel of the forward and
-    backward sweeps, counted as the kernel generator's cost model counts them:
-    forward: one per (output, x) pre-contraction entry plus the path-weight
-    product per output row; backward: two per entry (dm x product and x
-    cotangent), one per coupling coefficient, two per output row (s dm and its
-    use) and two per harmonic row of each path (ds and dy)."""
-    i0, i1, _, val = plan.records()
+    backward sweeps, counted as the kernel generator counts them.
+
+    Forward: one per (output, x) pre-contraction entry plus the path-weight
+    product per output row.  Backward, per path, the cheapest of three orders
+    of the same sums (the one the generated code uses), each with two per
+    harmonic row (ds = y . B and dy += s B):
+      A: two per entry (dm x product, x cotangent), one per coupling
+         coefficient, plus min(d1, d3) for the path weight;
+      B: one per entry, one per coefficient, one per (M, m2) pair, min(d1, d3);
+      C: one per coefficient, two per (m1, m2) pair, d1."""
+    i0, i1, i2, val = plan.records()
+    paths = plan.paths()
     pairs = len(set(zip(i0.tolist(), i1.tolist())))
-    s2 = sum(2 * int(l2) + 1 for (_, l2, _, _, _, _, _) in plan.paths())
-    return pairs + plan.D_out, 2 * pairs + len(val) + 2 * plan.D_out + 2 * s2
+    bwd = 0
+    for (l1, l2, l3, _, x_off, y_off, out_off) in paths.tolist():
+        d1, d2, d3 = 2 * l1 + 1, 2 * l2 + 1, 2 * l3 + 1
+        sel = (i0 >= out_off) & (i0 < out_off + d3) & (i1 >= x_off) & (i1 < x_off + d1) \
+            & (i2 >= y_off) & (i2 < y_off + d2)
+        a, b, c = i0[sel].tolist(), i1[sel].tolist(), i2[sel].tolist()
+        nnz, nE = len(a), len(set(zip(a, b)))
+        nMm2, nm1m2 = len(set(zip(a, c))), len(set(zip(b, c)))
+        bwd += min(2 * nE + nnz + min(d1, d3), nE + nnz + nMm2 + min(d1, d3), nnz + 2 * nm1m2 + d1) + 2 * d2
+    return pairs + plan.D_out, bwd
 
 
 def counter_traffic(kernel: str):

@@ -96,10 +96,40 @@ std::vector<PathInfo> path_infos(const Layout& lay) {
 
 int fwd_cost(const PathInfo& pi) { return (int)pi.entries.size() + 2 * pi.p.l3 + 1; }
 
-int bwd_cost(const PathInfo& pi) {
+// Backward contraction routes of one path, per edge and channel.  Every route
+// forms B[m2] = sum_{M,m1} C[M,m1,m2] dm[M] x[m1] (then ds = y . B and
+// dy += s B) and adds the path's share of the x cotangent,
+// t[m1] += s sum_M A[M,m1] dm[M]; they differ in the order of the sums:
+//   kRouteA: B through the products dm[M] x[m1] of the path's A entries;
+//   kRouteB: B through U[M,m2] = sum_{m1} C x[m1], then dm[M] U[M,m2];
+//   kRouteC: per m1, V[m2] = sum_M C dm[M], then B[m2] += x[m1] V[m2] and the
+//            unweighted cotangent sum_{m2} y[m2] V[m2]: no A entry is used.
+// Routes A and B take t through A: s dm[M] first when the output block is no
+// larger than the x block, the sum over M first otherwise.
+enum Route { kRouteA, kRouteB, kRouteC };
+
+struct RouteCost {
+  Route r;
+  int cost;  // multiply-adds per edge and channel, ds and dy included
+};
+
+RouteCost bwd_route(const PathInfo& pi) {
   const Path& p = pi.p;
-  return 2 * (int)pi.entries.size() + pi.nnz + 2 * (2 * p.l3 + 1) + 2 * (2 * p.l2 + 1);
+  const int d1 = 2 * p.l1 + 1, d2 = 2 * p.l2 + 1, d3 = 2 * p.l3 + 1;
+  const int nE = (int)pi.entries.size();
+  std::set<std::pair<int, int>> Mm2, m1m2;
+  for (const Entry& en : pi.entries)
+    for (const Rec& r : en.recs) Mm2.insert({en.M, r.m2}), m1m2.insert({en.m1, r.m2});
+  const int common = 2 * d2;
+  const int ca = 2 * nE + pi.nnz + std::min(d1, d3) + common;
+  const int cb = nE + pi.nnz + (int)Mm2.size() + std::min(d1, d3) + common;
+  const int cc = pi.nnz + 2 * (int)m1m2.size() + d1 + common;
+  if (ca <= cb && ca <= cc) return {kRouteA, ca};
+  if (cb <= cc) return {kRouteB, cb};
+  return {kRouteC, cc};
 }
+
+int bwd_cost(const PathInfo& pi) { return bwd_route(pi).cost; }
 
 // Contiguous partition of [0, n) into g parts minimising the largest cost,
 // each part [s, i) satisfying fits(s, i).
@@ -141,7 +171,9 @@ struct Group {
   int na_pad = 0;
 };
 
-Group make_group(const Layout& lay, const std::vector<PathInfo>& pis, int b, int e) {
+// with_A(k): whether path k's A entries are staged for the group
+template <class WithA>
+Group make_group(const Layout& lay, const std::vector<PathInfo>& pis, int b, int e, WithA with_A) {
   Group g;
   std::set<int> xs, ys;
   for (int k = b; k < e; ++k) {
@@ -150,7 +182,8 @@ Group make_group(const Layout& lay, const std::vector<PathInfo>& pis, int b, int
     for (int a = 0; a < 2 * pi.p.l1 + 1; ++a) xs.insert(pi.p.x_off + a);
     for (int M = 0; M < 2 * pi.p.l3 + 1; ++M) g.orows.push_back(pi.p.out_off + M);
     for (int m2 = 0; m2 < 2 * pi.p.l2 + 1; ++m2) ys.insert(pi.p.y_off + m2);
-    for (const Entry& en : pi.entries) g.entries.push_back(en);
+    if (with_A(k))
+      for (const Entry& en : pi.entries) g.entries.push_back(en);
   }
   g.xrows.assign(xs.begin(), xs.end());
   g.yrows.assign(ys.begin(), ys.end());
@@ -159,6 +192,10 @@ Group make_group(const Layout& lay, const std::vector<PathInfo>& pis, int b, int
   if (g.na_pad % 32 == 0) g.na_pad += 4;  // stagger LDS rows across banks
   (void)lay;
   return g;
+}
+
+Group make_group(const Layout& lay, const std::vector<PathInfo>& pis, int b, int e) {
+  return make_group(lay, pis, b, e, [](int) { return true; });
 }
 
 int index_of(const std::vector<int>& v, int x) {
@@ -320,47 +357,117 @@ void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
 }
 
 void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
-  o << "  // Per edge and channel, path by path: w = s dm (the mixed cotangent), t += A^T w\n"
-       "  // (the x cotangent before the sender reduction), B[m2] = sum C dm x, ds = y . B,\n"
-       "  // dy += s B (summed over this lane's channels).\n";
+  o << "  // Per edge and channel, path by path: B[m2] = sum C dm x, ds = y . B, dy += s B\n"
+       "  // (summed over this lane's channels), and t, the x cotangent before the sender\n"
+       "  // reduction, += s sum_M A dm; the order of each path's sums is its cheapest route.\n";
   o << "  template <int CPL, class DS>\n";
   o << "  __device__ __forceinline__ static void edge(const float* __restrict__ A, const float (&Y)[D_SH],\n"
        "      const float (&x)[NXR][CPL], const float (&s)[NPATH][CPL], const float (&dm)[NROW][CPL],\n"
        "      float (&t)[NXR][CPL], float (&dy)[D_SH], DS& st_ds) {\n";
   o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  o << "    (void)A4;\n";
   std::vector<bool> loaded(g.na_pad / 4, false);
   int ei = 0, orow0 = 0;
   for (size_t pl = 0; pl < g.paths.size(); ++pl) {
     const PathInfo& pi = pis[g.paths[pl]];
     const Path& p = pi.p;
-    const int d2 = 2 * p.l2 + 1, d3 = 2 * p.l3 + 1;
+    const int d1 = 2 * p.l1 + 1, d2 = 2 * p.l2 + 1, d3 = 2 * p.l3 + 1;
+    const Route route = bwd_route(pi).r;
+    const std::string S = "s[" + std::to_string(pl) + "][c]";
+    auto DM = [&](int M) { return "dm[" + std::to_string(orow0 + M) + "][c]"; };
+    auto X = [&](int m1) { return "x[" + std::to_string(index_of(g.xrows, p.x_off + m1)) + "][c]"; };
+    auto Tt = [&](int m1) { return "t[" + std::to_string(index_of(g.xrows, p.x_off + m1)) + "][c]"; };
     int lo = ei;
-    while (ei < (int)g.entries.size() && g.entries[ei].k == p.k) ++ei;
-    if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
-    o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << ")\n";
+    if (route != kRouteC) {
+      while (ei < (int)g.entries.size() && g.entries[ei].k == p.k) ++ei;
+      if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
+    }
+    static const char* rname[3] = {"A", "B", "C"};
+    o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << "), route " << rname[route] << "\n";
     o << "      float dsv[CPL];\n";
     o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
-    for (int M = 0; M < d3; ++M)
-      o << "        const float w" << M << " = s[" << pl << "][c] * dm[" << orow0 + M << "][c];\n";
     std::vector<bool> binit(d2, false);
     std::string decl;
     for (int b = 0; b < d2; ++b) decl += (b ? ", b" : "b") + std::to_string(b);
     o << "        float " << decl << ";\n";
-    for (int i = lo; i < ei; ++i) {
-      const Entry& en = g.entries[i];
-      int xl = index_of(g.xrows, p.x_off + en.m1);
-      o << "        t[" << xl << "][c] = fmaf(" << aval(i) << ", w" << en.M << ", t[" << xl << "][c]);\n";
-      o << "        {\n          const float pr = dm[" << orow0 + en.M << "][c] * x[" << xl << "][c];\n";
-      for (const Rec& r : en.recs) {
-        int b = r.m2 - p.y_off;
-        if (!binit[b]) {
-          o << "          b" << b << " = " << flit(r.c) << " * pr;\n";
-          binit[b] = true;
-        } else {
-          o << "          b" << b << " = fmaf(" << flit(r.c) << ", pr, b" << b << ");\n";
+    auto acc_b = [&](int b, const std::string& term_a, const std::string& term_b) {
+      // b_b += term_a * term_b
+      if (!binit[b]) {
+        o << "          b" << b << " = " << term_a << " * " << term_b << ";\n";
+        binit[b] = true;
+      } else {
+        o << "          b" << b << " = fmaf(" << term_a << ", " << term_b << ", b" << b << ");\n";
+      }
+    };
+    if (route != kRouteC) {
+      // x cotangent through the A entries [lo, ei)
+      if (d3 <= d1) {
+        std::set<int> Ms;
+        for (int i = lo; i < ei; ++i) Ms.insert(g.entries[i].M);
+        for (int M : Ms) o << "        const float w" << M << " = " << S << " * " << DM(M) << ";\n";
+        for (int i = lo; i < ei; ++i)
+          o << "        " << Tt(g.entries[i].m1) << " = fmaf(" << aval(i) << ", w" << g.entries[i].M << ", "
+            << Tt(g.entries[i].m1) << ");\n";
+      } else {
+        for (int m1 = 0; m1 < d1; ++m1) {
+          bool first = true;
+          for (int i = lo; i < ei; ++i) {
+            if (g.entries[i].m1 != m1) continue;
+            if (first)
+              o << "        {\n          float u = " << aval(i) << " * " << DM(g.entries[i].M) << ";\n";
+            else
+              o << "          u = fmaf(" << aval(i) << ", " << DM(g.entries[i].M) << ", u);\n";
+            first = false;
+          }
+          if (!first) o << "          " << Tt(m1) << " = fmaf(" << S << ", u, " << Tt(m1) << ");\n        }\n";
         }
       }
-      o << "        }\n";
+    }
+    if (route == kRouteA) {
+      for (int i = lo; i < ei; ++i) {
+        const Entry& en = g.entries[i];
+        o << "        {\n          const float pr = " << DM(en.M) << " * " << X(en.m1) << ";\n";
+        for (const Rec& r : en.recs) acc_b(r.m2 - p.y_off, flit(r.c), "pr");
+        o << "        }\n";
+      }
+    } else if (route == kRouteB) {
+      // U[M, m2] = sum_m1 C x[m1], then b[m2] += dm[M] U[M, m2]
+      for (int M = 0; M < d3; ++M) {
+        std::map<int, std::vector<std::pair<int, double>>> u;  // m2 -> (m1, c)
+        for (const Entry& en : pi.entries)
+          if (en.M == M)
+            for (const Rec& r : en.recs) u[r.m2 - p.y_off].push_back({en.m1, r.c});
+        for (const auto& [b, lst] : u) {
+          o << "        {\n          float u = " << flit(lst[0].second) << " * " << X(lst[0].first) << ";\n";
+          for (size_t j = 1; j < lst.size(); ++j)
+            o << "          u = fmaf(" << flit(lst[j].second) << ", " << X(lst[j].first) << ", u);\n";
+          acc_b(b, DM(M), "u");
+          o << "        }\n";
+        }
+      }
+    } else {
+      // per m1: V[m2] = sum_M C dm[M]; b[m2] += x[m1] V[m2]; t[m1] += s sum_m2 y[m2] V[m2]
+      for (int m1 = 0; m1 < d1; ++m1) {
+        std::map<int, std::vector<std::pair<int, double>>> v;  // m2 -> (M, c)
+        for (const Entry& en : pi.entries)
+          if (en.m1 == m1)
+            for (const Rec& r : en.recs) v[r.m2 - p.y_off].push_back({en.M, r.c});
+        if (v.empty()) continue;
+        o << "        {\n";
+        std::string ty;
+        for (const auto& [b, lst] : v) {
+          const std::string vn = "v" + std::to_string(b);
+          o << "          float " << vn << " = " << flit(lst[0].second) << " * " << DM(lst[0].first) << ";\n";
+          for (size_t j = 1; j < lst.size(); ++j)
+            o << "          " << vn << " = fmaf(" << flit(lst[j].second) << ", " << DM(lst[j].first) << ", " << vn
+              << ");\n";
+          acc_b(b, X(m1), vn);
+          const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]";
+          ty = ty.empty() ? yb + " * " + vn : "fmaf(" + yb + ", " + vn + ", " + ty + ")";
+        }
+        o << "          " << Tt(m1) << " = fmaf(" << S << ", " << ty << ", " << Tt(m1) << ");\n";
+        o << "        }\n";
+      }
     }
     std::string ds;
     for (int b = 0; b < d2; ++b) {
@@ -371,7 +478,7 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
     o << "        dsv[c] = " << (ds.empty() ? std::string("0.0f") : ds) << ";\n";
     for (int b = 0; b < d2; ++b) {
       if (!binit[b]) continue;
-      o << "        dy[" << p.y_off + b << "] = fmaf(s[" << pl << "][c], b" << b << ", dy[" << p.y_off + b << "]);\n";
+      o << "        dy[" << p.y_off + b << "] = fmaf(" << S << ", b" << b << ", dy[" << p.y_off + b << "]);\n";
     }
     for (int b = 0; b < d2; ++b)
       if (!binit[b]) o << "        (void)b" << b << ";\n";
@@ -529,7 +636,8 @@ int main(int argc, char** argv) {
     }
     std::vector<Group> fg, bg;
     for (auto [b, e] : fparts) fg.push_back(make_group(lay, pis, b, e));
-    for (auto [b, e] : bparts) bg.push_back(make_group(lay, pis, b, e));
+    for (auto [b, e] : bparts)
+      bg.push_back(make_group(lay, pis, b, e, [&](int k) { return bwd_route(pis[k]).r != kRouteC; }));
     Group tpg = make_group(lay, pis, 0, np);
 
     const std::string tag = tag_of(v);
