@@ -112,7 +112,10 @@ def fma_counts(plan):
       A: two per entry (dm x product, x cotangent), one per coupling
          coefficient, plus min(d1, d3) for the path weight;
       B: one per entry, one per coefficient, one per (M, m2) pair, min(d1, d3);
-      C: one per coefficient, two per (m1, m2) pair, d1."""
+      C: one per coefficient, two per (m1, m2) pair, d1;
+    and the paths whose coupling is the identity between the output block and
+    the x block or the harmonic block (the (0, l, l) and (l, 0, l) paths) take
+    2 d3 + 3 in all."""
     i0, i1, i2, val = plan.records()
     paths = plan.paths()
     pairs = len(set(zip(i0.tolist(), i1.tolist())))
@@ -124,6 +127,11 @@ def fma_counts(plan):
         a, b, c = i0[sel].tolist(), i1[sel].tolist(), i2[sel].tolist()
         nnz, nE = len(a), len(set(zip(a, b)))
         nMm2, nm1m2 = len(set(zip(a, c))), len(set(zip(b, c)))
+        v = val[sel]
+        unit = nE == d3 and nnz == nE and bool(np.all(np.abs(v - 1.0) <= 1e-12))
+        if unit and ((d1 == 1 and len(set(c)) == d3) or (d2 == 1 and len(set(b)) == d3)):
+            bwd += 2 * d3 + 3  # identity coupling with the x or the harmonic block
+            continue
         bwd += min(2 * nE + nnz + min(d1, d3), nE + nnz + nMm2 + min(d1, d3), nnz + 2 * nm1m2 + d1) + 2 * d2
     return pairs + plan.D_out, bwd
 

@@ -105,8 +105,33 @@ int fwd_cost(const PathInfo& pi) { return (int)pi.entries.size() + 2 * pi.p.l3 +
 //   kRouteC: per m1, V[m2] = sum_M C dm[M], then B[m2] += x[m1] V[m2] and the
 //            unweighted cotangent sum_{m2} y[m2] V[m2]: no A entry is used.
 // Routes A and B take t through A: s dm[M] first when the output block is no
-// larger than the x block, the sum over M first otherwise.
-enum Route { kRouteA, kRouteB, kRouteC };
+// larger than the x block, the sum over M first otherwise.  Two shortcuts
+// cover the paths whose coupling is the identity between two of the three
+// blocks (unit coefficients, one per entry, a one-to-one map), that is the
+// (0, l, l) and (l, 0, l) paths:
+//   kRouteX0: a scalar x block (d1 = 1): with T = sum_M y[m2(M)] dm[M],
+//             t += s T, ds = x T and dy[m2(M)] += (s x) dm[M];
+//   kRouteY0: a scalar harmonic (d2 = 1): with B = sum_M dm[M] x[m1(M)],
+//             ds = y B, dy += s B and t[m1(M)] += (s y) dm[M].
+// Neither uses A entries.
+enum Route { kRouteA, kRouteB, kRouteC, kRouteX0, kRouteY0 };
+
+// The path's coupling as a one-to-one map with unit coefficients between the
+// output rows and the rows of the x block (want_x) or of the harmonic block:
+// map[M] = partner row, empty if the path has no such structure.
+std::vector<int> unit_map(const PathInfo& pi, bool want_x) {
+  const int d3 = 2 * pi.p.l3 + 1;
+  std::vector<int> map(d3, -1);
+  std::set<int> seen;
+  if ((int)pi.entries.size() != d3) return {};
+  for (const Entry& en : pi.entries) {
+    if (en.recs.size() != 1 || std::fabs(en.recs[0].c - 1.0) > 1e-12) return {};
+    const int partner = want_x ? en.m1 : en.recs[0].m2 - pi.p.y_off;
+    if (map[en.M] != -1 || !seen.insert(partner).second) return {};
+    map[en.M] = partner;
+  }
+  return map;
+}
 
 struct RouteCost {
   Route r;
@@ -124,6 +149,8 @@ RouteCost bwd_route(const PathInfo& pi) {
   const int ca = 2 * nE + pi.nnz + std::min(d1, d3) + common;
   const int cb = nE + pi.nnz + (int)Mm2.size() + std::min(d1, d3) + common;
   const int cc = pi.nnz + 2 * (int)m1m2.size() + d1 + common;
+  if (d1 == 1 && !unit_map(pi, false).empty()) return {kRouteX0, 2 * d3 + 3};
+  if (d2 == 1 && !unit_map(pi, true).empty()) return {kRouteY0, 2 * d3 + 3};
   if (ca <= cb && ca <= cc) return {kRouteA, ca};
   if (cb <= cc) return {kRouteB, cb};
   return {kRouteC, cc};
@@ -378,11 +405,45 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
     auto X = [&](int m1) { return "x[" + std::to_string(index_of(g.xrows, p.x_off + m1)) + "][c]"; };
     auto Tt = [&](int m1) { return "t[" + std::to_string(index_of(g.xrows, p.x_off + m1)) + "][c]"; };
     int lo = ei;
-    if (route != kRouteC) {
+    const bool uses_A = route == kRouteA || route == kRouteB;
+    if (uses_A) {
       while (ei < (int)g.entries.size() && g.entries[ei].k == p.k) ++ei;
       if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
     }
-    static const char* rname[3] = {"A", "B", "C"};
+    static const char* rname[5] = {"A", "B", "C", "X0", "Y0"};
+    if (route == kRouteX0 || route == kRouteY0) {
+      // identity coupling between the output block and the harmonic (X0) or x (Y0) block
+      const std::vector<int> map = unit_map(pi, route == kRouteY0);
+      o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << "), route " << rname[route] << "\n";
+      o << "      float dsv[CPL];\n";
+      o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+      if (route == kRouteX0) {
+        auto Yr = [&](int b) { return "Y[" + std::to_string(p.y_off + b) + "]"; };
+        std::string tt = Yr(map[0]) + " * " + DM(0);
+        for (int M = 1; M < d3; ++M) tt = "fmaf(" + Yr(map[M]) + ", " + DM(M) + ", " + tt + ")";
+        o << "        const float T = " << tt << ";\n";
+        o << "        " << Tt(0) << " = fmaf(" << S << ", T, " << Tt(0) << ");\n";
+        o << "        dsv[c] = " << X(0) << " * T;\n";
+        o << "        const float sx = " << S << " * " << X(0) << ";\n";
+        for (int M = 0; M < d3; ++M)
+          o << "        dy[" << p.y_off + map[M] << "] = fmaf(sx, " << DM(M) << ", dy[" << p.y_off + map[M] << "]);\n";
+      } else {
+        std::string bb = DM(0) + " * " + X(map[0]);
+        for (int M = 1; M < d3; ++M) bb = "fmaf(" + DM(M) + ", " + X(map[M]) + ", " + bb + ")";
+        const std::string y0 = "Y[" + std::to_string(p.y_off) + "]";
+        o << "        const float B = " << bb << ";\n";
+        o << "        dsv[c] = " << y0 << " * B;\n";
+        o << "        dy[" << p.y_off << "] = fmaf(" << S << ", B, dy[" << p.y_off << "]);\n";
+        o << "        const float sy = " << S << " * " << y0 << ";\n";
+        for (int M = 0; M < d3; ++M)
+          o << "        " << Tt(map[M]) << " = fmaf(sy, " << DM(M) << ", " << Tt(map[M]) << ");\n";
+      }
+      o << "      }\n";
+      o << "      st_ds(" << pl << ", dsv);\n";
+      o << "    }\n";
+      orow0 += d3;
+      continue;
+    }
     o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << "), route " << rname[route] << "\n";
     o << "      float dsv[CPL];\n";
     o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
@@ -399,7 +460,7 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
         o << "          b" << b << " = fmaf(" << term_a << ", " << term_b << ", b" << b << ");\n";
       }
     };
-    if (route != kRouteC) {
+    if (uses_A) {
       // x cotangent through the A entries [lo, ei)
       if (d3 <= d1) {
         std::set<int> Ms;
@@ -637,7 +698,10 @@ int main(int argc, char** argv) {
     std::vector<Group> fg, bg;
     for (auto [b, e] : fparts) fg.push_back(make_group(lay, pis, b, e));
     for (auto [b, e] : bparts)
-      bg.push_back(make_group(lay, pis, b, e, [&](int k) { return bwd_route(pis[k]).r != kRouteC; }));
+      bg.push_back(make_group(lay, pis, b, e, [&](int k) {
+        const Route r = bwd_route(pis[k]).r;
+        return r == kRouteA || r == kRouteB;
+      }));
     Group tpg = make_group(lay, pis, 0, np);
 
     const std::string tag = tag_of(v);
