@@ -1459,6 +1459,18 @@ constexpr int kLinRT = E3_LIN_RT;  // 16-row subtiles per wave in the gather-GEM
 #ifndef E3_LIN_V4
 #define E3_LIN_V4 1
 #endif
+// Row fetches of the dW kernel in flight while one fetch runs (1 or 2; two
+// measured 1.29 -> 1.23 ms).
+#ifndef E3_LIN_DW_AHEAD
+#define E3_LIN_DW_AHEAD 2
+#endif
+// 1: the gather-GEMM requests the W operands of the next k step with its A
+// rows, instead of at the start of the step that uses them (forward 1.147 ->
+// 1.110 ms, dx 1.39 -> 1.356 ms; the A rows two steps ahead as well measured
+// no better for the forward and 6% slower for dx).
+#ifndef E3_LIN_BPF
+#define E3_LIN_BPF 1
+#endif
 
 struct LinJob {
   int R, dst_row, src_first, nsrc;
@@ -1530,20 +1542,15 @@ __global__ __launch_bounds__(kWave) void k_lin_gemm(LinArgs a) {
 #pragma unroll
       for (int s = 0; s < RT; ++s) v[s] = *reinterpret_cast<const f4v*>(sp + abase[s]);
     };
-    // one (source, k-step): W (cache-resident) first, then the A rows of step
-    // i + 1 (clamped, so the loads are unconditional and the waits count
-    // exactly; loads complete in issue order), then the 64 instructions
-    auto step = [&](int i, const f4v(&av)[RT], f4v(&an)[RT]) {
+    auto load_b = [&](int i, f4v(&bq)[4]) {
       const int t = i / ksteps, k0 = (i - t * ksteps) * 16;
       const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<float*>(a.W + srcs[jb.src_first + t].w_off), (short)0, a.C_src * a.C_dst * 4, 0x00020000);
-      f4v bq[4];
 #pragma unroll
       for (int c = 0; c < 4; ++c)
         bq[c] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(wr, bvoff, (k0 + c) * a.ldk * 4, 0));
-      __builtin_amdgcn_sched_barrier(0);
-      load_a(i + 1 < nsteps ? i + 1 : i, an);
-      __builtin_amdgcn_sched_barrier(0);
+    };
+    auto mfmas = [&](const f4v(&av)[RT], const f4v(&bq)[4]) {
 #pragma unroll
       for (int c = 0; c < 4; ++c)
 #pragma unroll
@@ -1552,11 +1559,41 @@ __global__ __launch_bounds__(kWave) void k_lin_gemm(LinArgs a) {
           for (int s = 0; s < RT; ++s)
             acc[s][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s][c], bq[c][cb], acc[s][cb], 0, 0, 0);
     };
-    f4v a0[RT], a1[RT];
-    if (nsteps > 0) load_a(0, a0);
-    for (int i = 0; i < nsteps; i += 2) {
-      step(i, a0, a1);
-      if (i + 1 < nsteps) step(i + 1, a1, a0);
+    if constexpr (E3_LIN_BPF) {
+      // one (source, k-step): the W and A operands of step i + 1 (clamped, so
+      // the loads are unconditional and the waits count exactly; loads
+      // complete in issue order) are requested, then the 64 instructions run
+      // on the operands of step i, requested one step earlier
+      auto step = [&](int i, const f4v(&av)[RT], const f4v(&bv)[4], f4v(&an)[RT], f4v(&bn)[4]) {
+        const int ni = i + 1 < nsteps ? i + 1 : i;
+        load_b(ni, bn);
+        load_a(ni, an);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(av, bv);
+      };
+      f4v a0[RT], a1[RT], b0[4], b1[4];
+      if (nsteps > 0) load_b(0, b0), load_a(0, a0);
+      for (int i = 0; i < nsteps; i += 2) {
+        step(i, a0, b0, a1, b1);
+        if (i + 1 < nsteps) step(i + 1, a1, b1, a0, b0);
+      }
+    } else {
+      // one (source, k-step): W (cache-resident) first, then the A rows of step
+      // i + 1, then the 64 instructions
+      auto step = [&](int i, const f4v(&av)[RT], f4v(&an)[RT]) {
+        f4v bq[4];
+        load_b(i, bq);
+        __builtin_amdgcn_sched_barrier(0);
+        load_a(i + 1 < nsteps ? i + 1 : i, an);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(av, bq);
+      };
+      f4v a0[RT], a1[RT];
+      if (nsteps > 0) load_a(0, a0);
+      for (int i = 0; i < nsteps; i += 2) {
+        step(i, a0, a1);
+        if (i + 1 < nsteps) step(i + 1, a1, a0);
+      }
     }
     // register r of acc[s][cb] in lane l: row 16 s + 4 (l / 16) + r, column col0 + 4 (l % 16) + cb
     if (!cv) return;
@@ -1700,7 +1737,26 @@ __global__ __launch_bounds__(kWave) void k_lin_dw(LinDwArgs a) {
       advance();
     }
   };
-  if (nf > 0) {
+  if (nf > 0 && E3_LIN_DW_AHEAD == 2) {
+    // two fetches in flight while one runs
+    f4v xA[S], dA[S], xB[S], dB[S], xC[S], dC[S];
+    fetch(xA, dA);
+    fetch(xB, dB);
+    for (int64_t f = 0; f < nf; ++f) {
+      fetch(xC, dC);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < S; ++q) group(xA[q], dA[q]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < S; ++q) xA[q] = xB[q], dA[q] = dB[q], xB[q] = xC[q], dB[q] = dC[q];
+    }
+    // the state ran two fetches ahead: step back to the first row after the whole fetches
+    row = rb + g + nf * 4 * S;
+    m = (int)(row % R);
+    ox = ((row / R) * a.D_in + pr.src_row + m) * a.C_in + (kv ? kc : 0);
+    od = ((row / R) * a.D_out + pr.dst_row + m) * a.C_out + (jv ? jc : 0);
+  } else if (nf > 0) {
     f4v xA[S], dA[S], xB[S], dB[S];
     fetch(xA, dA);
     for (int64_t f = 0; f < nf; ++f) {
