@@ -348,36 +348,50 @@ void emit_A_loads(std::ostream& o, int lo, int hi, std::vector<bool>& loaded, co
   }
 }
 
+// kFwdLead: float4 chunks of A values requested beyond the last one the
+// current row reads (emitted before its products; E3_FWD_PIN() between them
+// can keep the compiler from moving them).
+int kFwdLead = 4;
+
 void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
   o << "  template <int CPL>\n";
   o << "  __device__ __forceinline__ static void edge(const float* __restrict__ A, const float (&x)[NXR][CPL],\n"
        "      const float (&s)[NPATH][CPL], float (&acc)[NROW][CPL]) {\n";
   o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
-  std::vector<bool> loaded(g.na_pad / 4, false);
+  struct Row {
+    int pl, M, orow, lo, hi;
+  };
+  std::vector<Row> rows;
   int ei = 0, orow = 0;
   for (size_t pl = 0; pl < g.paths.size(); ++pl) {
     const PathInfo& pi = pis[g.paths[pl]];
-    const int d3 = 2 * pi.p.l3 + 1;
-    for (int M = 0; M < d3; ++M, ++orow) {
-      int lo = ei;
+    for (int M = 0; M < 2 * pi.p.l3 + 1; ++M, ++orow) {
+      const int lo = ei;
       while (ei < (int)g.entries.size() && g.entries[ei].k == pi.p.k && g.entries[ei].M == M) ++ei;
-      if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
-      o << "    {  // path " << pi.p.k << " (" << pi.p.l1 << "," << pi.p.l2 << "," << pi.p.l3 << ") row " << M << "\n";
-      o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
-      if (ei == lo) {
-        o << "        (void)c;\n      }\n    }\n";
-        continue;
-      }
-      for (int i = lo; i < ei; ++i) {
-        int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
-        if (i == lo)
-          o << "        float z = " << aval(i) << " * x[" << xl << "][c];\n";
-        else
-          o << "        z = fmaf(" << aval(i) << ", x[" << xl << "][c], z);\n";
-      }
-      o << "        acc[" << orow << "][c] = fmaf(s[" << pl << "][c], z, acc[" << orow << "][c]);\n";
-      o << "      }\n    }\n";
+      if (ei > lo) rows.push_back({(int)pl, M, orow, lo, ei});
     }
+  }
+  std::vector<bool> loaded(g.na_pad / 4, false);
+  const int nr = (int)rows.size();
+  const int nchunk = (int)g.entries.size() > 0 ? ((int)g.entries.size() - 1) / 4 + 1 : 0;
+  for (int r = 0; r < nr; ++r) {
+    // the chunks this row reads and kFwdLead more (within the entries in use)
+    const int last = std::min((rows[r].hi - 1) / 4 + kFwdLead, nchunk - 1);
+    emit_A_loads(o, 0, 4 * last + 1, loaded, "    ");
+    o << "    E3_FWD_PIN();\n";
+    const Row& rw = rows[r];
+    const PathInfo& pi = pis[g.paths[rw.pl]];
+    o << "    {  // path " << pi.p.k << " (" << pi.p.l1 << "," << pi.p.l2 << "," << pi.p.l3 << ") row " << rw.M << "\n";
+    o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+    for (int i = rw.lo; i < rw.hi; ++i) {
+      const int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
+      if (i == rw.lo)
+        o << "        float z = " << aval(i) << " * x[" << xl << "][c];\n";
+      else
+        o << "        z = fmaf(" << aval(i) << ", x[" << xl << "][c], z);\n";
+    }
+    o << "        acc[" << rw.orow << "][c] = fmaf(s[" << rw.pl << "][c], z, acc[" << rw.orow << "][c]);\n";
+    o << "      }\n    }\n";
   }
   o << "  }\n";
   (void)lay;
@@ -613,7 +627,7 @@ std::string tag_of(const VariantSpec& v) {
 
 int main(int argc, char** argv) {
   if (argc < 2) {
-    std::fprintf(stderr, "usage: gen <out.inc> [fwd_target fwd_regs fwd_rows]\n");
+    std::fprintf(stderr, "usage: gen <out.inc> [fwd_target fwd_regs fwd_rows fwd_lead]\n");
     return 2;
   }
   // Compiled variants: x blocks of degrees ls (any parities, all paths kept),
@@ -631,6 +645,7 @@ int main(int argc, char** argv) {
   const int FWD_TARGET = argc > 2 ? std::atoi(argv[2]) : 200;
   const int FWD_REGS = argc > 3 ? std::atoi(argv[3]) : 1000;
   const int FWD_RMAX = argc > 4 ? std::atoi(argv[4]) : 56;
+  if (argc > 5) kFwdLead = std::atoi(argv[5]);
   const int BWD_TARGET = 640;
   const int BWD_RMAX = 56;
 
