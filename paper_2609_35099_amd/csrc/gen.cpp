@@ -352,6 +352,9 @@ void emit_A_loads(std::ostream& o, int lo, int hi, std::vector<bool>& loaded, co
 // current row reads (emitted before its products; E3_FWD_PIN() between them
 // can keep the compiler from moving them).
 int kFwdLead = 4;
+// kBwdLead: float4 chunks of A values requested beyond a backward path's own,
+// before its code (held there by a scheduling barrier when PIN is set).
+int kBwdLead = 2;
 
 void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
   o << "  template <int CPL>\n";
@@ -401,7 +404,7 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
   o << "  // Per edge and channel, path by path: B[m2] = sum C dm x, ds = y . B, dy += s B\n"
        "  // (summed over this lane's channels), and t, the x cotangent before the sender\n"
        "  // reduction, += s sum_M A dm; the order of each path's sums is its cheapest route.\n";
-  o << "  template <int CPL, class DS>\n";
+  o << "  template <bool PIN, int CPL, class DS>\n";
   o << "  __device__ __forceinline__ static void edge(const float* __restrict__ A, const float (&Y)[D_SH],\n"
        "      const float (&x)[NXR][CPL], const float (&s)[NPATH][CPL], const float (&dm)[NROW][CPL],\n"
        "      float (&t)[NXR][CPL], float (&dy)[D_SH], DS& st_ds) {\n";
@@ -422,7 +425,12 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
     const bool uses_A = route == kRouteA || route == kRouteB;
     if (uses_A) {
       while (ei < (int)g.entries.size() && g.entries[ei].k == p.k) ++ei;
-      if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
+      if (ei > lo) {
+        // this path's chunks and kBwdLead more
+        const int nchunk = ((int)g.entries.size() - 1) / 4 + 1;
+        emit_A_loads(o, 0, 4 * std::min((ei - 1) / 4 + kBwdLead, nchunk - 1) + 1, loaded, "    ");
+        o << "    if constexpr (PIN) __builtin_amdgcn_sched_barrier(0);\n";
+      }
     }
     static const char* rname[5] = {"A", "B", "C", "X0", "Y0"};
     if (route == kRouteX0 || route == kRouteY0) {
@@ -646,6 +654,7 @@ int main(int argc, char** argv) {
   const int FWD_REGS = argc > 3 ? std::atoi(argv[3]) : 1000;
   const int FWD_RMAX = argc > 4 ? std::atoi(argv[4]) : 56;
   if (argc > 5) kFwdLead = std::atoi(argv[5]);
+  if (argc > 6) kBwdLead = std::atoi(argv[6]);
   const int BWD_TARGET = 640;
   const int BWD_RMAX = 56;
 
