@@ -246,7 +246,7 @@ def cpu_baseline(cfg, g, x, dm, seconds=12.0):
         k = sel.shape[0]
         return nodes, inv[:k].astype(np.int32), inv[k:].astype(np.int32)
 
-    while t_used < seconds and n_batches < 64:
+    while t_used < seconds and n_batches < 256:
         b = rng.choice(g.n_nodes, 4, replace=False)
         sel_r = np.nonzero(np.isin(g.receiver, b))[0]
         sel_s = np.nonzero(np.isin(g.sender, b))[0]
