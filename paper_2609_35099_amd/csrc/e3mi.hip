@@ -617,6 +617,10 @@ struct ConvArgs {
   const float* h;  // [E, K]
   const float* W;  // [K, P, C]
   int K;
+  // three-term forward of the double backward: the tangents of x, y and s
+  const float* x2;
+  const float* y2;
+  const float* s2;
 };
 
 // Receiver, group and channel slab of this wave: XCD k = blockIdx % 8 walks
@@ -755,6 +759,95 @@ __global__ __launch_bounds__(kWave, E3_FWD_MIN_WAVES) void k_conv_fwd(ConvArgs a
   int b, g, sl;
   if (!task_of<V::NFG>(a, b, g, sl)) return;
   fwd_dispatch<V, 0, CPL, ACC>(a, b, g, sl, reinterpret_cast<float*>(smem));
+}
+
+// The double backward's output cotangent in one pass over the receiver-sorted
+// edges (the sum of the three forward products of eq. conv-bwd-bwd-ddm):
+//   m[b] = sum_e s_e (A_e x2_src + A2_e x_src) + s2_e (A_e x_src),
+// A from the caller's harmonics y, A2 from their tangent y2; one channel per
+// lane, smaller edge batches (two pre-contractions per edge share the LDS).
+constexpr int kEdgeBatch3 = 8;
+
+template <class V, int G>
+__device__ __forceinline__ void fwd3_task(const ConvArgs& a, int b, int sl, float* sA, float* sA2) {
+  using F = typename V::template FG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<1>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  float acc[F::NROW][1];
+#pragma unroll
+  for (int i = 0; i < F::NROW; ++i) acc[i][0] = 0.0f;
+  for (int eb = e0; eb < e1; eb += kEdgeBatch3) {
+    const int n = imin(kEdgeBatch3, e1 - eb);
+    int my_e = 0, my_src = 0;
+    if (lane < n) {
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
+      float Y[V::D_SH], Yd[V::D_SH];
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) {
+        Y[i] = a.y[(int64_t)my_e * V::D_SH + i];
+        Yd[i] = a.y2[(int64_t)my_e * V::D_SH + i];
+      }
+      F::make_A(Y, sA + lane * F::NA);
+      F::make_A(Yd, sA2 + lane * F::NA);
+    }
+    __syncthreads();
+    if (act) {
+      float xa[F::NXR][1], xda[F::NXR][1], sa[F::NPATH][1], sda[F::NPATH][1];
+      float xb[F::NXR][1], xdb[F::NXR][1], sb[F::NPATH][1], sdb[F::NPATH][1];
+      auto load = [&](int j, float (&xv)[F::NXR][1], float (&xdv)[F::NXR][1], float (&sv)[F::NPATH][1],
+                      float (&sdv)[F::NPATH][1]) {
+        const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+        const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+        const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf x2r = row_buf(a.x2 + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf sr = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        const RowBuf s2r = row_buf(a.s2 + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+#pragma unroll
+        for (int i = 0; i < F::NXR; ++i) bld<1>(xr, F::XROW[i], xv[i]), bld<1>(x2r, F::XROW[i], xdv[i]);
+#pragma unroll
+        for (int i = 0; i < F::NPATH; ++i) bld<1, kNT>(sr, F::PATH[i], sv[i]), bld<1, kNT>(s2r, F::PATH[i], sdv[i]);
+      };
+      load(0, xa, xda, sa, sda);
+      for (int j = 0; j < n; j += 2) {
+        if (j + 1 < n) load(j + 1, xb, xdb, sb, sdb);
+        F::template edge3<1>(sA + j * F::NA, sA2 + j * F::NA, xa, xda, sa, sda, acc);
+        if (j + 1 < n) {
+          if (j + 2 < n) load(j + 2, xa, xda, sa, sda);
+          F::template edge3<1>(sA + (j + 1) * F::NA, sA2 + (j + 1) * F::NA, xb, xdb, sb, sdb, acc);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (act) {
+    const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+#pragma unroll
+    for (int i = 0; i < F::NROW; ++i) bst<1, kST>(mb, F::OROW[i], acc[i]);
+  }
+}
+
+template <class V, int G>
+__device__ __forceinline__ void fwd3_dispatch(const ConvArgs& a, int b, int g, int sl, float* sA, float* sA2) {
+  if constexpr (G < V::NFG) {
+    if (g == G)
+      fwd3_task<V, G>(a, b, sl, sA, sA2);
+    else
+      fwd3_dispatch<V, G + 1>(a, b, g, sl, sA, sA2);
+  }
+}
+
+template <class V>
+__global__ __launch_bounds__(kWave, E3_FWD_MIN_WAVES) void k_conv_fwd3(ConvArgs a) {
+  __shared__ f4v smem[(2 * kEdgeBatch3 * V::MAX_NA_F + 3) / 4];
+  int b, g, sl;
+  if (!task_of<V::NFG>(a, b, g, sl)) return;
+  float* sA = reinterpret_cast<float*>(smem);
+  fwd3_dispatch<V, 0>(a, b, g, sl, sA, sA + kEdgeBatch3 * V::MAX_NA_F);
 }
 
 template <class V, int G, int CPL, bool ACC>
@@ -2083,6 +2176,24 @@ e3_status run_fwd(const e3_plan* p, const e3_graph* g, const float* x, const flo
   return E3_OK;
 }
 
+// The double backward's three forward terms in one launch (k_conv_fwd3):
+// m = conv(x2, y, s) + conv(x, y2, s) + conv(x, y, s2), overwritten.
+template <class V>
+e3_status run_fwd3(const e3_plan* p, const e3_graph* g, const float* x, const float* x2, const float* y,
+                   const float* y2, const float* s, const float* s2, float* m, hipStream_t st) {
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.x2 = x2, a.y = y, a.y2 = y2, a.s = s, a.s2 = s2, a.m = m;
+  a.nslab = (a.C + kWave - 1) / kWave;  // one channel per lane
+  if (g->n_nodes == 0) return E3_OK;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
+  {
+    TimedLaunch t_("conv_fwd3", st);
+    hipLaunchKernelGGL((k_conv_fwd3<V>), dim3(grid), dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
 // One backward convolution.  Harmonics from y when given (then dy is the
 // harmonic cotangent output), else from vec (then dvec = J^T dy).  Any of
 // dx, dvec/dy, ds may be null: that cotangent is not stored.  accum is a mask
@@ -2337,6 +2448,8 @@ struct VariantOps {
   e3_status (*rbwd)(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*, int,
                     const float*, float*, float*, float*, float*, void*, hipStream_t);
   RadWs (*rws)(const e3_plan*, const e3_graph*, int);
+  e3_status (*fwd3)(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*,
+                    const float*, const float*, float*, hipStream_t);
 };
 
 #define E3_VARIANT(V)                                                                                    \
@@ -2355,7 +2468,8 @@ struct VariantOps {
              &tp_ws<e3gen::V>,                                                                           \
              &run_fwd_rad<e3gen::V>,                                                                     \
              &run_bwd_rad<e3gen::V>,                                                                     \
-             &rad_ws<e3gen::V>},
+             &rad_ws<e3gen::V>,                                                                          \
+             &run_fwd3<e3gen::V>},
 
 const VariantOps kVariants[] = {E3GEN_FOR_EACH_VARIANT(E3_VARIANT)};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
@@ -2853,10 +2967,8 @@ e3_status e3_conv_bwd2(const e3_plan* p, const e3_graph* g, const float* x, cons
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
   const int ci = cpl_index(cpl_of(p));
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  // ddm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds)
-  if ((st = v.fwd[ci](p, g, ddx, nullptr, y, s, gdm, 0, hs)) != E3_OK) return st;
-  if ((st = v.fwd[ci](p, g, x, nullptr, ddy, s, gdm, 1, hs)) != E3_OK) return st;
-  if ((st = v.fwd[ci](p, g, x, nullptr, y, dds, gdm, 1, hs)) != E3_OK) return st;
+  // ddm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds), in one pass
+  if ((st = v.fwd3(p, g, x, ddx, y, ddy, s, dds, gdm, hs)) != E3_OK) return st;
   // (-, d_x y, d_x s) = conv_bwd(ddx, y, s, dm)
   if ((st = v.bwd[ci](p, g, ddx, nullptr, y, s, dm, nullptr, nullptr, gy, gs, 0, ws, hs)) != E3_OK) return st;
   // (d_y x, -, d_y s) = conv_bwd(x, ddy, s, dm)

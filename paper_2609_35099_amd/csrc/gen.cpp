@@ -400,6 +400,52 @@ void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
   (void)lay;
 }
 
+// The three forward terms of the double backward's output cotangent in one
+// pass: acc += s (A xd + A2 x) + sd (A x), with A from the harmonics y and A2
+// from their tangent yd (same entry layout).
+void emit_fwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Group& g) {
+  o << "  template <int CPL>\n";
+  o << "  __device__ __forceinline__ static void edge3(const float* __restrict__ A, const float* __restrict__ A2,\n"
+       "      const float (&x)[NXR][CPL], const float (&xd)[NXR][CPL], const float (&s)[NPATH][CPL],\n"
+       "      const float (&sd)[NPATH][CPL], float (&acc)[NROW][CPL]) {\n";
+  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  o << "    const float4* __restrict__ B4 = reinterpret_cast<const float4*>(A2);\n";
+  std::vector<bool> loaded(g.na_pad / 4, false);
+  int ei = 0, orow = 0;
+  for (size_t pl = 0; pl < g.paths.size(); ++pl) {
+    const PathInfo& pi = pis[g.paths[pl]];
+    for (int M = 0; M < 2 * pi.p.l3 + 1; ++M, ++orow) {
+      const int lo = ei;
+      while (ei < (int)g.entries.size() && g.entries[ei].k == pi.p.k && g.entries[ei].M == M) ++ei;
+      if (ei == lo) continue;
+      for (int q = lo / 4; q <= (ei - 1) / 4; ++q)
+        if (!loaded[q]) {
+          o << "    const float4 a" << q << " = A4[" << q << "], b" << q << " = B4[" << q << "];\n";
+          loaded[q] = true;
+        }
+      o << "    {  // path " << pi.p.k << " (" << pi.p.l1 << "," << pi.p.l2 << "," << pi.p.l3 << ") row " << M << "\n";
+      o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+      for (int i = lo; i < ei; ++i) {
+        const int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
+        const std::string av = aval(i), bv = "b" + aval(i).substr(1);
+        if (i == lo) {
+          o << "        float z1 = " << av << " * xd[" << xl << "][c];\n";
+          o << "        float z2 = " << bv << " * x[" << xl << "][c];\n";
+          o << "        float z3 = " << av << " * x[" << xl << "][c];\n";
+        } else {
+          o << "        z1 = fmaf(" << av << ", xd[" << xl << "][c], z1);\n";
+          o << "        z2 = fmaf(" << bv << ", x[" << xl << "][c], z2);\n";
+          o << "        z3 = fmaf(" << av << ", x[" << xl << "][c], z3);\n";
+        }
+      }
+      o << "        acc[" << orow << "][c] = fmaf(s[" << pl << "][c], z1 + z2, fmaf(sd[" << pl << "][c], z3, acc["
+        << orow << "][c]));\n";
+      o << "      }\n    }\n";
+    }
+  }
+  o << "  }\n";
+}
+
 void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
   o << "  // Per edge and channel, path by path: B[m2] = sum C dm x, ds = y . B, dy += s B\n"
        "  // (summed over this lane's channels), and t, the x cotangent before the sender\n"
@@ -752,6 +798,7 @@ int main(int argc, char** argv) {
       emit_group_meta(o, fg[gi]);
       emit_make_A(o, fg[gi]);
       emit_fwd_group(o, lay, pis, fg[gi]);
+      emit_fwd3_group(o, pis, fg[gi]);
       o << "};\n\n";
     }
     for (size_t gi = 0; gi < bg.size(); ++gi) {

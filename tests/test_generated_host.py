@@ -61,6 +61,24 @@ void fwd_groups(const float* Y, const float* x, const float* s, float* m) {
 }
 
 template <class V, int G>
+void fwd3_groups(const float* Y, const float* Yd, const float* x, const float* xd, const float* s, const float* sd,
+                 float* m) {
+  if constexpr (G < V::NFG) {
+    using F = typename V::template FG<G>;
+    alignas(16) float A[F::NA], A2[F::NA];
+    F::make_A(Y, A);
+    F::make_A(Yd, A2);
+    float xv[F::NXR][1], xdv[F::NXR][1], sv[F::NPATH][1], sdv[F::NPATH][1], acc[F::NROW][1];
+    for (int i = 0; i < F::NXR; ++i) xv[i][0] = x[F::XROW[i]], xdv[i][0] = xd[F::XROW[i]];
+    for (int i = 0; i < F::NPATH; ++i) sv[i][0] = s[F::PATH[i]], sdv[i][0] = sd[F::PATH[i]];
+    for (int i = 0; i < F::NROW; ++i) acc[i][0] = 0.0f;
+    F::template edge3<1>(A, A2, xv, xdv, sv, sdv, acc);
+    for (int i = 0; i < F::NROW; ++i) m[F::OROW[i]] = acc[i][0];
+    fwd3_groups<V, G + 1>(Y, Yd, x, xd, s, sd, m);
+  }
+}
+
+template <class V, int G>
 void bwd_groups(const float* Y, const float* x, const float* s, const float* dm, float* dx, float* dy,
                 float* ds) {
   if constexpr (G < V::NBG) {
@@ -84,6 +102,10 @@ void bwd_groups(const float* Y, const float* x, const float* s, const float* dm,
 #define E3_HOST_ENTRY(V)                                                                        \
   extern "C" void V##_fwd(const float* Y, const float* x, const float* s, float* m) {          \
     fwd_groups<V, 0>(Y, x, s, m);                                                              \
+  }                                                                                            \
+  extern "C" void V##_fwd3(const float* Y, const float* Yd, const float* x, const float* xd, const float* s, \
+                           const float* sd, float* m) {                                        \
+    fwd3_groups<V, 0>(Y, Yd, x, xd, s, sd, m);                                                 \
   }                                                                                            \
   extern "C" void V##_bwd(const float* Y, const float* x, const float* s, const float* dm,      \
                           float* dx, float* dy, float* ds) {                                   \
@@ -152,3 +174,30 @@ def test_generated_edge_code_matches_oracle(hostlib, tag):
     assert _rel(dx, ref_dx.numpy()[:, :, 0]) < 1e-6
     assert _rel(ds, ref_dw.numpy()[:, :, 0]) < 1e-6
     assert _rel(dy, ref_dy.numpy()) < 1e-6
+
+
+@pytest.mark.parametrize("tag", sorted(VARIANTS))
+def test_generated_three_term_forward_matches_oracle(hostlib, tag):
+    """The double backward's output cotangent in one pass: the sum of three
+    forward products, with the x, harmonic and weight tangents in turn."""
+    ls, lsh, lout = VARIANTS[tag]
+    irreps = "+".join(f"1x{l}{'o' if l % 2 else 'e'}" for l in ls)
+    lay = oirreps.layout(irreps, lsh, lout)
+    rng = np.random.default_rng(12)
+    R = 16
+    u = rng.standard_normal((R, 3))
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    y = np.asarray(osh.sh_unit(lsh, u), dtype=np.float32)
+    yd = rng.standard_normal((R, lay.d_sh)).astype(np.float32)
+    x, xd = (rng.standard_normal((R, lay.d_in)).astype(np.float32) for _ in range(2))
+    s, sd = (rng.standard_normal((R, lay.n_paths)).astype(np.float32) for _ in range(2))
+    fwd3 = getattr(hostlib, f"{tag}_fwd3")
+    m = np.zeros((R, lay.d_out), np.float32)
+    for r in range(R):
+        rows = [np.ascontiguousarray(a[r]) for a in (y, yd, x, xd, s, sd)]
+        out = np.zeros(lay.d_out, np.float32)
+        fwd3(*[_ptr(a) for a in rows], _ptr(out))
+        m[r] = out
+    c = lambda a: a[:, :, None]
+    ref = (otp.tp(lay, c(xd), y, c(s)) + otp.tp(lay, c(x), yd, c(s)) + otp.tp(lay, c(x), y, c(sd))).numpy()[:, :, 0]
+    assert _rel(m, ref) < 1e-6
