@@ -192,9 +192,10 @@ e3_status e3_conv_bwd_y(const e3_plan* plan, const e3_graph* graph, const float*
  *   gx  = dx of conv_bwd(x, ddy, s, dm) + dx of conv_bwd(x, y, dds, dm)
  *   gy  = dy of conv_bwd(ddx, y, s, dm) + dy of conv_bwd(x, y, dds, dm)
  *   gs  = ds of conv_bwd(ddx, y, s, dm) + ds of conv_bwd(x, ddy, s, dm)
- * gdm by one sweep that forms the three forward terms together; the rest by
- * three backward sweeps that store only the cotangents used and add in place.
- * Deterministic.  ws as for e3_conv_bwd. */
+ * gdm by one sweep that forms the three forward terms together, and gx, gy,
+ * gs by one sweep that forms the three backward terms together (one channel
+ * per lane; a build with more runs three backward sweeps that store only the
+ * cotangents used and add in place).  Deterministic.  ws as for e3_conv_bwd. */
 e3_status e3_conv_bwd2(const e3_plan* plan, const e3_graph* graph, const float* x, const float* y,
                        const float* s, const float* dm, const float* ddx, const float* ddy, const float* dds,
                        float* gx, float* gy, float* gs, float* gdm, void* ws, size_t ws_bytes, e3_stream stream);

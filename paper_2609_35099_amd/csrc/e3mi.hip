@@ -991,6 +991,115 @@ __global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd_edges(Conv
   bwd_dispatch<V, 0, CPL, ACC>(a, b, g, sl, sA, sA + kEdgeBatch * V::MAX_NA_B);
 }
 
+// The double backward's three backward sweeps in one (generated BG::edge3):
+// per edge, with the harmonics y and their tangent y2 of the caller, x and its
+// tangent x2 (senders), s and its tangent s2 (edges) and dm (receiver), it
+// stores gs = ds(x2, y, s) + ds(x, y2, s), the x-cotangent partials of
+// (x, y2, s) and (x, y, s2) for the sender segment sum, and the per-wave
+// harmonic cotangent partials of (x2, y, s) and (x, y, s2).  One channel per
+// lane.
+template <class V, int G>
+__device__ __forceinline__ void bwd3_task(const ConvArgs& a, int b, int sl, float* sY, float* sY2) {
+  using B = typename V::template BG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<1>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  if (e0 == e1) return;
+  float dmv[B::NROW][1];
+  if (act) {
+    const RowBuf db = row_buf(a.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+#pragma unroll
+    for (int i = 0; i < B::NROW; ++i) bld<1>(db, B::OROW[i], dmv[i]);
+  }
+  for (int eb = e0; eb < e1; eb += kEdgeBatch) {
+    const int n = imin(kEdgeBatch, e1 - eb);
+    int my_e = 0, my_src = 0, my_slot = 0;
+    if (lane < n) {
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
+      my_slot = a.r2s[eb + lane];
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) {
+        sY[lane * V::D_SH + i] = a.y[(int64_t)my_e * V::D_SH + i];
+        sY2[lane * V::D_SH + i] = a.y2[(int64_t)my_e * V::D_SH + i];
+      }
+    }
+    __syncthreads();
+    float xa[B::NXR][1], xda[B::NXR][1], sa[B::NPATH][1], sda[B::NPATH][1];
+    float xb[B::NXR][1], xdb[B::NXR][1], sb[B::NPATH][1], sdb[B::NPATH][1];
+    auto load = [&](int j, float (&xv)[B::NXR][1], float (&xdv)[B::NXR][1], float (&sv)[B::NPATH][1],
+                    float (&sdv)[B::NPATH][1]) {
+      if (!act) return;
+      const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+      const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+      const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf x2r = row_buf(a.x2 + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf sr = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+      const RowBuf s2r = row_buf(a.s2 + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+#pragma unroll
+      for (int i = 0; i < B::NXR; ++i) bld<1>(xr, B::XROW[i], xv[i]), bld<1>(x2r, B::XROW[i], xdv[i]);
+#pragma unroll
+      for (int i = 0; i < B::NPATH; ++i) bld<1, kNT>(sr, B::PATH[i], sv[i]), bld<1, kNT>(s2r, B::PATH[i], sdv[i]);
+    };
+    auto compute = [&](int j, const float (&xv)[B::NXR][1], const float (&xdv)[B::NXR][1],
+                       const float (&sv)[B::NPATH][1], const float (&sdv)[B::NPATH][1]) {
+      const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+      const int64_t slot = __builtin_amdgcn_readlane(my_slot, j);
+      float dy[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dy[i] = 0.0f;
+      if (act) {
+        float t[B::NXR][1], Yv[V::D_SH], Y2v[V::D_SH], dyl[V::D_SH];
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) t[i][0] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i], Y2v[i] = sY2[j * V::D_SH + i], dyl[i] = 0.0f;
+        const RowBuf gsb = row_buf(a.ds + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        auto st = [&](int pl, const float (&v)[1]) { bst<1, kST>(gsb, B::PATH[pl], v); };
+        B::template edge3<1>(Yv, Y2v, xv, xdv, sv, sdv, dmv, t, dyl, st);
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
+        const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) bst<1, E3_T_STORE_AUX>(Tb, B::XROW[i], t[i]);
+      }
+      const float tot = wave_reduce16(dy, lane);
+      if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+    };
+    load(0, xa, xda, sa, sda);
+    for (int j = 0; j < n; j += 2) {
+      if (j + 1 < n) load(j + 1, xb, xdb, sb, sdb);
+      compute(j, xa, xda, sa, sda);
+      if (j + 1 < n) {
+        if (j + 2 < n) load(j + 2, xa, xda, sa, sda);
+        compute(j + 1, xb, xdb, sb, sdb);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <class V, int G>
+__device__ __forceinline__ void bwd3_dispatch(const ConvArgs& a, int b, int g, int sl, float* sY, float* sY2) {
+  if constexpr (G < V::NBG) {
+    if (g == G)
+      bwd3_task<V, G>(a, b, sl, sY, sY2);
+    else
+      bwd3_dispatch<V, G + 1>(a, b, g, sl, sY, sY2);
+  }
+}
+
+template <class V>
+__global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd3(ConvArgs a) {
+  __shared__ float smem[2 * kEdgeBatch * V::D_SH];
+  int b, g, sl;
+  if (!task_of<V::NBG>(a, b, g, sl)) return;
+  bwd3_dispatch<V, 0>(a, b, g, sl, smem, smem + kEdgeBatch * V::D_SH);
+}
+
 // dx[a] = sum of the partials of a's out-edges, in sender-CSR order.  A
 // node's partials are one contiguous block of (out-degree) x D_in x C floats;
 // the wave reads each slot's D_in x C floats as float4s (lane l takes float4
@@ -2264,6 +2373,51 @@ e3_status run_bwd(const e3_plan* p, const e3_graph* g, const float* x, const flo
   return E3_OK;
 }
 
+// The double backward's three backward terms in one sweep (k_conv_bwd3),
+// then the sender segment sum (gx) and the harmonic cotangent sum (gy); all
+// three outputs overwritten.  One channel per lane: the workspace layout of
+// e3_conv_bwd with one channel per lane (cpl_b == 1).
+template <class V>
+e3_status run_bwd3(const e3_plan* p, const e3_graph* g, const float* x, const float* x2, const float* y,
+                   const float* y2, const float* s, const float* s2, const float* dm, float* gx, float* gy,
+                   float* gs, void* ws, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  if (p->cpl_b != 1) return E3_ERR_UNSUPPORTED;
+  Ws w = bwd_ws<V>(p, g);
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.x2 = x2, a.y = y, a.y2 = y2, a.s = s, a.s2 = s2, a.dm = dm, a.ds = gs;
+  a.T = reinterpret_cast<float*>(ws);
+  a.DY = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.t_bytes);
+  a.nslab = p->nslab_b;
+  if (g->n_live > 0) {
+    const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
+    TimedLaunch t_("conv_bwd3", st);
+    hipLaunchKernelGGL((k_conv_bwd3<V>), dim3(grid), dim3(kWave), 0, st, a);
+    E3_HIP(hipGetLastError());
+  }
+  {
+    TimedLaunch t_("conv_bwd_dx", st);
+    const int flat4 = V::D_IN * a.C / 4;
+    const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
+    hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * a.chunk * nsl)), dim3(kWave), 0, st, a.T, gx,
+                       g->rowptr_s, a.n_nodes, a.chunk, flat4, nsl, 0);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_live > 0) {
+    TimedLaunch t_("conv_bwd_dy", st);
+    hipLaunchKernelGGL((k_conv_bwd_dy<V>), dim3(blocks_for(g->n_live * V::D_SH, 256)), dim3(256), 0, st, a.DY,
+                       g->eid_r, gy, g->n_live, p->nslab_b, 0);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_pad > 0) {  // padding edges: zero cotangents
+    TimedLaunch t_("conv_bwd_pad", st);
+    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, gs,
+                       (int64_t)V::NP * a.C, gy, (int64_t)V::D_SH);
+    E3_HIP(hipGetLastError());
+  }
+  return E3_OK;
+}
+
 template <class V, int CPL>
 e3_status run_tp(const e3_plan* p, const float* x, const float* y, const float* w, float* z, int64_t rows,
                  hipStream_t st) {
@@ -2450,6 +2604,8 @@ struct VariantOps {
   RadWs (*rws)(const e3_plan*, const e3_graph*, int);
   e3_status (*fwd3)(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*,
                     const float*, const float*, float*, hipStream_t);
+  e3_status (*bwd3)(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*,
+                    const float*, const float*, const float*, float*, float*, float*, void*, hipStream_t);
 };
 
 #define E3_VARIANT(V)                                                                                    \
@@ -2469,7 +2625,8 @@ struct VariantOps {
              &run_fwd_rad<e3gen::V>,                                                                     \
              &run_bwd_rad<e3gen::V>,                                                                     \
              &rad_ws<e3gen::V>,                                                                          \
-             &run_fwd3<e3gen::V>},
+             &run_fwd3<e3gen::V>,                                                                        \
+             &run_bwd3<e3gen::V>},
 
 const VariantOps kVariants[] = {E3GEN_FOR_EACH_VARIANT(E3_VARIANT)};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
@@ -2969,6 +3126,8 @@ e3_status e3_conv_bwd2(const e3_plan* p, const e3_graph* g, const float* x, cons
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   // ddm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds), in one pass
   if ((st = v.fwd3(p, g, x, ddx, y, ddy, s, dds, gdm, hs)) != E3_OK) return st;
+  // gx, gy, gs in one sweep where the backward runs one channel per lane
+  if (p->cpl_b == 1) return v.bwd3(p, g, x, ddx, y, ddy, s, dds, dm, gx, gy, gs, ws, hs);
   // (-, d_x y, d_x s) = conv_bwd(ddx, y, s, dm)
   if ((st = v.bwd[ci](p, g, ddx, nullptr, y, s, dm, nullptr, nullptr, gy, gs, 0, ws, hs)) != E3_OK) return st;
   // (d_y x, -, d_y s) = conv_bwd(x, ddy, s, dm)

@@ -620,6 +620,87 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
   (void)lay;
 }
 
+// The three backward sweeps of the double backward in one (per edge and
+// channel, every path through V = sum_M C dm, no A entry): with V[m1][m2],
+//   B1 = sum_m1 xd V, B2 = sum_m1 x V, T1 = sum_m2 y V, T2 = sum_m2 y2 V,
+//   gs = y . B1 + y2 . B2,  dy += s B1 + sd B2,  t += s T2 + sd T1,
+// i.e. ds of (xd, y, s) plus ds of (x, y2, s), dy of (xd, y, s) plus dy of
+// (x, y, sd), and the x cotangents of (x, y2, s) and (x, y, sd).
+void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Group& g) {
+  o << "  template <int CPL, class DS>\n";
+  o << "  __device__ __forceinline__ static void edge3(const float (&Y)[D_SH], const float (&Y2)[D_SH],\n"
+       "      const float (&x)[NXR][CPL], const float (&xd)[NXR][CPL], const float (&s)[NPATH][CPL],\n"
+       "      const float (&sd)[NPATH][CPL], const float (&dm)[NROW][CPL], float (&t)[NXR][CPL],\n"
+       "      float (&dy)[D_SH], DS& st_ds) {\n";
+  int orow0 = 0;
+  for (size_t pl = 0; pl < g.paths.size(); ++pl) {
+    const PathInfo& pi = pis[g.paths[pl]];
+    const Path& p = pi.p;
+    const int d1 = 2 * p.l1 + 1, d2 = 2 * p.l2 + 1, d3 = 2 * p.l3 + 1;
+    const std::string S = "s[" + std::to_string(pl) + "][c]", SD = "sd[" + std::to_string(pl) + "][c]";
+    auto DM = [&](int M) { return "dm[" + std::to_string(orow0 + M) + "][c]"; };
+    auto xi = [&](int m1) { return std::to_string(index_of(g.xrows, p.x_off + m1)); };
+    o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << ")\n";
+    o << "      float gsv[CPL];\n";
+    o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+    std::string decl;
+    for (int b = 0; b < d2; ++b) decl += (b ? ", p" : "p") + std::to_string(b) + ", q" + std::to_string(b);
+    o << "        float " << decl << ";\n";
+    std::vector<bool> binit(d2, false);
+    for (int m1 = 0; m1 < d1; ++m1) {
+      std::map<int, std::vector<std::pair<int, double>>> v;  // m2 -> (M, c)
+      for (const Entry& en : pi.entries)
+        if (en.m1 == m1)
+          for (const Rec& r : en.recs) v[r.m2 - p.y_off].push_back({en.M, r.c});
+      if (v.empty()) continue;
+      o << "        {\n";
+      std::string t1, t2;
+      for (const auto& [b, lst] : v) {
+        const std::string vn = "v" + std::to_string(b), bs = std::to_string(b);
+        o << "          float " << vn << " = " << flit(lst[0].second) << " * " << DM(lst[0].first) << ";\n";
+        for (size_t j = 1; j < lst.size(); ++j)
+          o << "          " << vn << " = fmaf(" << flit(lst[j].second) << ", " << DM(lst[j].first) << ", " << vn
+            << ");\n";
+        if (!binit[b]) {
+          o << "          p" << bs << " = xd[" << xi(m1) << "][c] * " << vn << ";\n";
+          o << "          q" << bs << " = x[" << xi(m1) << "][c] * " << vn << ";\n";
+          binit[b] = true;
+        } else {
+          o << "          p" << bs << " = fmaf(xd[" << xi(m1) << "][c], " << vn << ", p" << bs << ");\n";
+          o << "          q" << bs << " = fmaf(x[" << xi(m1) << "][c], " << vn << ", q" << bs << ");\n";
+        }
+        const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]", y2b = "Y2[" + std::to_string(p.y_off + b) + "]";
+        t1 = t1.empty() ? yb + " * " + vn : "fmaf(" + yb + ", " + vn + ", " + t1 + ")";
+        t2 = t2.empty() ? y2b + " * " + vn : "fmaf(" + y2b + ", " + vn + ", " + t2 + ")";
+      }
+      o << "          t[" << xi(m1) << "][c] = fmaf(" << S << ", " << t2 << ", fmaf(" << SD << ", " << t1 << ", t["
+        << xi(m1) << "][c]));\n";
+      o << "        }\n";
+    }
+    std::string gs;
+    for (int b = 0; b < d2; ++b) {
+      if (!binit[b]) continue;
+      const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]", y2b = "Y2[" + std::to_string(p.y_off + b) + "]";
+      const std::string bs = std::to_string(b);
+      gs = gs.empty() ? "fmaf(" + y2b + ", q" + bs + ", " + yb + " * p" + bs + ")"
+                      : "fmaf(" + y2b + ", q" + bs + ", fmaf(" + yb + ", p" + bs + ", " + gs + "))";
+    }
+    o << "        gsv[c] = " << (gs.empty() ? std::string("0.0f") : gs) << ";\n";
+    for (int b = 0; b < d2; ++b) {
+      if (!binit[b]) continue;
+      const std::string bs = std::to_string(b), dyi = "dy[" + std::to_string(p.y_off + b) + "]";
+      o << "        " << dyi << " = fmaf(" << S << ", p" << bs << ", fmaf(" << SD << ", q" << bs << ", " << dyi << "));\n";
+    }
+    for (int b = 0; b < d2; ++b)
+      if (!binit[b]) o << "        (void)p" << b << "; (void)q" << b << ";\n";
+    o << "      }\n";
+    o << "      st_ds(" << pl << ", gsv);\n";
+    o << "    }\n";
+    orow0 += d3;
+  }
+  o << "  }\n";
+}
+
 void emit_tp_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
   o << "  // Weighted tensor product rows: z[i0] = w[i3(i0)] * sum A x; each row handed to st.\n";
   o << "  template <int CPL, class ST>\n";
@@ -807,6 +888,7 @@ int main(int argc, char** argv) {
       emit_group_meta(o, bg[gi]);
       emit_make_A(o, bg[gi]);
       emit_bwd_group(o, lay, pis, bg[gi]);
+      emit_bwd3_group(o, pis, bg[gi]);
       o << "};\n\n";
     }
     o << "struct " << tag << "::TP {\n";

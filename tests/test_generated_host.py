@@ -99,6 +99,25 @@ void bwd_groups(const float* Y, const float* x, const float* s, const float* dm,
   }
 }
 
+template <class V, int G>
+void bwd3_groups(const float* Y, const float* Y2, const float* x, const float* xd, const float* s, const float* sd,
+                 const float* dm, float* gx, float* gy, float* gs) {
+  if constexpr (G < V::NBG) {
+    using B = typename V::template BG<G>;
+    float Yv[V::D_SH], Y2v[V::D_SH], dyl[V::D_SH];
+    for (int i = 0; i < V::D_SH; ++i) Yv[i] = Y[i], Y2v[i] = Y2[i], dyl[i] = 0.0f;
+    float xv[B::NXR][1], xdv[B::NXR][1], sv[B::NPATH][1], sdv[B::NPATH][1], dmv[B::NROW][1], t[B::NXR][1];
+    for (int i = 0; i < B::NXR; ++i) xv[i][0] = x[B::XROW[i]], xdv[i][0] = xd[B::XROW[i]], t[i][0] = 0.0f;
+    for (int i = 0; i < B::NPATH; ++i) sv[i][0] = s[B::PATH[i]], sdv[i][0] = sd[B::PATH[i]];
+    for (int i = 0; i < B::NROW; ++i) dmv[i][0] = dm[B::OROW[i]];
+    auto st = [&](int pl, const float (&v)[1]) { gs[B::PATH[pl]] = v[0]; };
+    B::template edge3<1>(Yv, Y2v, xv, xdv, sv, sdv, dmv, t, dyl, st);
+    for (int i = 0; i < B::NXR; ++i) gx[B::XROW[i]] += t[i][0];
+    for (int i = 0; i < V::D_SH; ++i) gy[i] += dyl[i];
+    bwd3_groups<V, G + 1>(Y, Y2, x, xd, s, sd, dm, gx, gy, gs);
+  }
+}
+
 #define E3_HOST_ENTRY(V)                                                                        \
   extern "C" void V##_fwd(const float* Y, const float* x, const float* s, float* m) {          \
     fwd_groups<V, 0>(Y, x, s, m);                                                              \
@@ -106,6 +125,13 @@ void bwd_groups(const float* Y, const float* x, const float* s, const float* dm,
   extern "C" void V##_fwd3(const float* Y, const float* Yd, const float* x, const float* xd, const float* s, \
                            const float* sd, float* m) {                                        \
     fwd3_groups<V, 0>(Y, Yd, x, xd, s, sd, m);                                                 \
+  }                                                                                            \
+  extern "C" void V##_bwd3(const float* Y, const float* Y2, const float* x, const float* xd,    \
+                           const float* s, const float* sd, const float* dm, float* gx, float* gy,  \
+                           float* gs) {                                                        \
+    for (int i = 0; i < V::D_IN; ++i) gx[i] = 0.0f;                                            \
+    for (int i = 0; i < V::D_SH; ++i) gy[i] = 0.0f;                                            \
+    bwd3_groups<V, 0>(Y, Y2, x, xd, s, sd, dm, gx, gy, gs);                                    \
   }                                                                                            \
   extern "C" void V##_bwd(const float* Y, const float* x, const float* s, const float* dm,      \
                           float* dx, float* dy, float* ds) {                                   \
@@ -201,3 +227,38 @@ def test_generated_three_term_forward_matches_oracle(hostlib, tag):
     c = lambda a: a[:, :, None]
     ref = (otp.tp(lay, c(xd), y, c(s)) + otp.tp(lay, c(x), yd, c(s)) + otp.tp(lay, c(x), y, c(sd))).numpy()[:, :, 0]
     assert _rel(m, ref) < 1e-6
+
+
+@pytest.mark.parametrize("tag", sorted(VARIANTS))
+def test_generated_three_term_backward_matches_oracle(hostlib, tag):
+    """The double backward's three backward products in one pass: ds of
+    (xd, y, s) and of (x, y2, s), dy of (xd, y, s) and of (x, y, sd), and the
+    x cotangents of (x, y2, s) and of (x, y, sd)."""
+    ls, lsh, lout = VARIANTS[tag]
+    irreps = "+".join(f"1x{l}{'o' if l % 2 else 'e'}" for l in ls)
+    lay = oirreps.layout(irreps, lsh, lout)
+    rng = np.random.default_rng(13)
+    R = 16
+    u = rng.standard_normal((R, 3))
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    y = np.asarray(osh.sh_unit(lsh, u), dtype=np.float32)
+    y2 = rng.standard_normal((R, lay.d_sh)).astype(np.float32)
+    x, xd = (rng.standard_normal((R, lay.d_in)).astype(np.float32) for _ in range(2))
+    s, sd = (rng.standard_normal((R, lay.n_paths)).astype(np.float32) for _ in range(2))
+    dm = rng.standard_normal((R, lay.d_out)).astype(np.float32)
+    bwd3 = getattr(hostlib, f"{tag}_bwd3")
+    gx = np.zeros((R, lay.d_in), np.float32)
+    gy = np.zeros((R, lay.d_sh), np.float32)
+    gs = np.zeros((R, lay.n_paths), np.float32)
+    for r in range(R):
+        rows = [np.ascontiguousarray(a[r]) for a in (y, y2, x, xd, s, sd, dm)]
+        outs = [np.zeros_like(a[r]) for a in (gx, gy, gs)]
+        bwd3(*[_ptr(a) for a in rows], *[_ptr(a) for a in outs])
+        gx[r], gy[r], gs[r] = outs
+    c = lambda a: a[:, :, None]
+    dx_a, dy_a, dw_a = otp.tp_bwd(lay, c(xd), y, c(s), c(dm))   # (xd, y, s)
+    dx_b, dy_b, dw_b = otp.tp_bwd(lay, c(x), y2, c(s), c(dm))   # (x, y2, s)
+    dx_c, dy_c, dw_c = otp.tp_bwd(lay, c(x), y, c(sd), c(dm))   # (x, y, sd)
+    assert _rel(gs, (dw_a + dw_b).numpy()[:, :, 0]) < 1e-6
+    assert _rel(gy, (dy_a + dy_c).numpy()) < 1e-6
+    assert _rel(gx, (dx_b + dx_c).numpy()[:, :, 0]) < 1e-6
