@@ -47,6 +47,8 @@ def _edge_ops(text, tag, kind):
         i = text.index(f"struct {tag}::{kind}<{g}>")
         body = text[i:text.index("\n};", i)]
         body = body[body.index("static void edge("):]
+        nxt = body.find("__device__", 1)  # the next member function (edge3) is not counted
+        body = body if nxt < 0 else body[:nxt]
         total += body.count("fmaf(") + body.count(" * ")
         g += 1
     assert g > 0, (tag, kind)
