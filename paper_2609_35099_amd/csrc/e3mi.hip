@@ -1093,7 +1093,12 @@ __device__ __forceinline__ void bwd3_dispatch(const ConvArgs& a, int b, int g, i
 }
 
 template <class V>
-__global__ __launch_bounds__(kWave, E3_BWD_MIN_WAVES) void k_conv_bwd3(ConvArgs a) {
+// One wave per SIMD: at two, the l <= 3 sweep spilled 136 bytes per lane and
+// ran 26.6 ms against 23.4 ms without the spill.
+#ifndef E3_BWD3_MIN_WAVES
+#define E3_BWD3_MIN_WAVES 1
+#endif
+__global__ __launch_bounds__(kWave, E3_BWD3_MIN_WAVES) void k_conv_bwd3(ConvArgs a) {
   __shared__ float smem[2 * kEdgeBatch * V::D_SH];
   int b, g, sl;
   if (!task_of<V::NBG>(a, b, g, sl)) return;
