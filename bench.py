@@ -263,12 +263,14 @@ def cpu_baseline(cfg, g, x, dm, seconds=12.0):
         t_used += time.perf_counter() - t0
         edges_done += (sel_r.shape[0] + sel_s.shape[0]) / 2.0
         n_batches += 1
-    return {"value": edges_done / t_used, "unit": "edges/s", "cores": torch.get_num_threads(),
-            "kind": "oracle",
+    return {"value": edges_done / t_used, "unit": "edges/s", "cores": len(os.sched_getaffinity(0)),
+            "kind": "oracle", "rate": "extrapolated from the sample",
             "sample": f"{n_batches} batches of 4 random atoms: forward of their {int(edges_done)} in-edges "
                       f"(avg of in/out counts) and full backward (dx of the atoms, ds/dvec of their "
-                      f"out-edges), float64, {t_used:.1f} s; rate = edges / (t_fwd + t_bwd)",
-            "cpu": cpu_model(), "numpy": np.__version__, "torch_threads": torch.get_num_threads()}
+                      f"out-edges), float64, {t_used:.1f} s; rate = edges / (t_fwd + t_bwd), extrapolated "
+                      f"to the whole workload",
+            "cpu": cpu_model(), "numpy": np.__version__, "torch_threads": torch.get_num_threads(),
+            "affinity_cores": len(os.sched_getaffinity(0))}
 
 
 def oracle_configs():

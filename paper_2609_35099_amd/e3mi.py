@@ -137,6 +137,22 @@ def _stream(stream):
     return ct.c_void_p(s.cuda_stream)
 
 
+def _on_stream(fn):
+    """Run a compute call with the caller's stream made current, so that the
+    outputs and the workspace it allocates belong to that stream in torch's
+    caching allocator (their memory is not handed out again while the kernels
+    launched on that stream may still use it)."""
+    import functools
+
+    @functools.wraps(fn)
+    def wrapped(*args, stream=None, **kw):
+        if stream is None:
+            return fn(*args, **kw)
+        with _torch().cuda.stream(stream):
+            return fn(*args, stream=stream, **kw)
+    return wrapped
+
+
 # ---------------------------------------------------------------- plan
 class Plan:
     """Paths, coupling tables and compiled kernel variant for an irreps layout."""
@@ -248,6 +264,7 @@ def _empty(shape, like=None):
     return torch.empty(shape, dtype=torch.float32, device="cuda")
 
 
+@_on_stream
 def sh(lmax: int, vec, out=None, stream=None):
     n = vec.shape[0]
     out = _empty((n, (lmax + 1) ** 2)) if out is None else out
@@ -256,6 +273,7 @@ def sh(lmax: int, vec, out=None, stream=None):
     return out
 
 
+@_on_stream
 def sh_bwd(lmax: int, vec, dy, out=None, stream=None):
     n = vec.shape[0]
     out = _empty((n, 3)) if out is None else out
@@ -264,6 +282,7 @@ def sh_bwd(lmax: int, vec, dy, out=None, stream=None):
     return out
 
 
+@_on_stream
 def tp_fwd(plan: Plan, x, y, w, out=None, stream=None):
     R = x.shape[0]
     out = _empty((R, plan.D_out, plan.C)) if out is None else out
@@ -279,6 +298,7 @@ def tp_workspace_size(plan: Plan, rows: int) -> int:
     return b.value
 
 
+@_on_stream
 def tp_bwd(plan: Plan, x, y, w, dz, dx=None, dy=None, dw=None, ws=None, stream=None):
     """(dx, dy, dw) of the weighted tensor product."""
     R = x.shape[0]
@@ -307,6 +327,7 @@ def workspace(nbytes: int):
     return torch.empty(max(nbytes, 1), dtype=torch.uint8, device="cuda")
 
 
+@_on_stream
 def conv_fwd(plan: Plan, graph: Graph, x, vec, s, out=None, stream=None):
     N, E = graph.n_nodes, graph.n_edges
     out = _empty((N, plan.D_out, plan.C)) if out is None else out
@@ -316,6 +337,7 @@ def conv_fwd(plan: Plan, graph: Graph, x, vec, s, out=None, stream=None):
     return out
 
 
+@_on_stream
 def conv_bwd(plan: Plan, graph: Graph, x, vec, s, dm, dx=None, dvec=None, ds=None, ws=None, stream=None):
     N, E = graph.n_nodes, graph.n_edges
     dx = _empty((N, plan.D_in, plan.C)) if dx is None else dx
@@ -335,6 +357,7 @@ def _optr(t, name, shape):
     return None if t is None else _ptr(t, name, shape)
 
 
+@_on_stream
 def conv_fwd_y(plan: Plan, graph: Graph, x, y, s, out=None, accumulate=False, stream=None):
     """m = conv(x, y, s) with the harmonics y [E, D_sh] given (m += ... when accumulate)."""
     N, E = graph.n_nodes, graph.n_edges
@@ -346,6 +369,7 @@ def conv_fwd_y(plan: Plan, graph: Graph, x, y, s, out=None, accumulate=False, st
     return out
 
 
+@_on_stream
 def conv_bwd_y(plan: Plan, graph: Graph, x, y, s, dm, dx=None, dy=None, ds=None, want=("dx", "dy", "ds"),
                accumulate=False, ws=None, stream=None):
     """(dx, dy, ds) of eq. (conv-bwd) with y given; cotangents not in `want` are neither
@@ -368,6 +392,7 @@ def conv_bwd_y(plan: Plan, graph: Graph, x, y, s, dm, dx=None, dy=None, ds=None,
     return dx, dy, ds
 
 
+@_on_stream
 def conv_bwd2(plan: Plan, graph: Graph, x, y, s, dm, ddx, ddy, dds, ws=None, stream=None):
     """Double backward: (gx, gy, gs, gdm), the variations of (x, y, s, dm) for
     variations (ddx, ddy, dds) of the backward's outputs."""
@@ -419,6 +444,7 @@ class RecordTP:
         torch = _torch()
         return ("float64", "_f64") if x.dtype == torch.float64 else ("float32", "")
 
+    @_on_stream
     def forward(self, x, y, out=None, stream=None):
         """z in the precision of x (float32 or float64)."""
         R, _, C = x.shape
@@ -429,6 +455,7 @@ class RecordTP:
             _ptr(out, "z", (R, self.d_z, C), dt), R, C, _stream(stream)), "e3_tpg_fwd" + sfx)
         return out
 
+    @_on_stream
     def backward(self, x, y, dz, stream=None):
         R, _, C = x.shape
         dt, sfx = self._kind(x)
@@ -469,6 +496,7 @@ class Linear:
         except Exception:
             pass
 
+    @_on_stream
     def forward(self, x, W, out=None, stream=None):
         n = x.shape[0]
         out = _empty((n, self.D_out, self.C_out)) if out is None else out
@@ -482,6 +510,7 @@ class Linear:
         _check(lib().e3_linear_workspace_size(self.handle, ct.byref(b)), "e3_linear_workspace_size")
         return b.value
 
+    @_on_stream
     def backward(self, x, W, dout, dx=None, dW=None, ws=None, stream=None):
         n = x.shape[0]
         dx = _empty((n, self.D_in, self.C_in)) if dx is None else dx
@@ -502,6 +531,7 @@ def conv_radial_workspace_size(plan: Plan, graph: Graph, K: int) -> int:
     return b.value
 
 
+@_on_stream
 def conv_fwd_radial(plan: Plan, graph: Graph, x, vec, h, W, out=None, stream=None):
     """m with per-edge weights s_e = h_e W formed inside the kernel (h [E, K], W [K, P, C])."""
     N, E = graph.n_nodes, graph.n_edges
@@ -515,6 +545,7 @@ def conv_fwd_radial(plan: Plan, graph: Graph, x, vec, h, W, out=None, stream=Non
     return out
 
 
+@_on_stream
 def conv_bwd_radial(plan: Plan, graph: Graph, x, vec, h, W, dm, dx=None, dvec=None, dh=None, dW=None, ws=None,
                     stream=None):
     """(dx, dvec, dh, dW) of the convolution with fused radial weights."""

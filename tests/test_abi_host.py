@@ -45,10 +45,11 @@ LAYOUTS = [("8x0e+8x1o", 2, 2), ("128x0e+128x1o+128x2e", 3, 3), ("128x0e+128x1o"
            ("4x1o+4x0e+4x2o", 2, 3)]
 
 
-@pytest.mark.parametrize("spec", LAYOUTS)
-def test_plan_tables_equal_oracle(spec):
-    plan = e3mi.Plan(*spec)
-    lay = oirreps.layout(*spec)
+@pytest.mark.parametrize("natural", [False, True])
+@pytest.mark.parametrize("spec", LAYOUTS + [("4x0o+4x1e", 2, 2), ("128x1o+128x0e+128x3o+128x2e", 3, 3)])
+def test_plan_tables_equal_oracle(spec, natural):
+    plan = e3mi.Plan(*spec, natural=natural)
+    lay = oirreps.layout(*spec, parity="natural" if natural else "all")
     assert (plan.P, plan.D_in, plan.D_sh, plan.D_out, plan.C) == \
         (lay.n_paths, lay.d_in, lay.d_sh, lay.d_out, lay.channels)
     paths = plan.paths()

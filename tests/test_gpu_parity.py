@@ -363,46 +363,6 @@ def test_conv_full_size_sampled(e3, name):
         assert v < TOL, (k, v)
 
 
-@pytest.mark.skipif(os.environ.get("E3MI_STRESS") != "1",
-                    reason="capacity stress (~265 GB of HBM, several minutes): set E3MI_STRESS=1")
-def test_conv_stress_water70k_sampled(e3):
-    """70,000 H2O (210,000 atoms, ~11M edges), 64 channels: forward + backward at
-    full size on one GPU, checked on sampled rows."""
-    import torch
-    _say("conv stress water70k")
-    cfg = synth.CONFIGS["water70k"]
-    g = synth.graph(cfg)
-    N, E = g.n_nodes, g.sender.shape[0]
-    print(f"N={N} E={E}", flush=True)
-    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
-    dev = torch.device("cuda")
-    x = synth.node_features(cfg, N)
-    s = synth.normal_device(cfg.cid, 2, (E, plan.P, plan.C), dev)
-    dm = synth.normal_device(cfg.cid, 3, (N, plan.D_out, plan.C), dev)
-    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), N)
-    xs, vs = to_dev(x), to_dev(g.vec)
-    m = e3.conv_fwd(plan, G, xs, vs, s)
-    torch.cuda.synchronize()
-    lay = layout_of(cfg)
-    rng = np.random.default_rng(9)
-    rs = np.concatenate([[0, N - 1], rng.choice(N, 14, replace=False)])
-    es = np.concatenate([[0, E - 1], rng.choice(E, 30, replace=False)])
-    sfn = lambda rows: s[torch.as_tensor(rows, device=dev)].cpu().numpy()
-    ref_m = oracle_fwd_rows(lay, x, g.vec, sfn, g.sender, g.receiver, N, rs)
-    err_m = rel_l2(to_np(m[torch.as_tensor(rs, device=dev)]), ref_m)
-    del m
-    torch.cuda.empty_cache()
-    dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, s, dm)
-    torch.cuda.synchronize()
-    ref_dx, ref_ds, ref_dv = oracle_bwd_rows(lay, x, g.vec, sfn, dm, g.sender, g.receiver, N, rs, es)
-    ri, ei = torch.as_tensor(rs, device=dev), torch.as_tensor(es, device=dev)
-    errs = dict(m=err_m, dx=rel_l2(to_np(dx[ri]), ref_dx), ds=rel_l2(to_np(ds[ei]), ref_ds),
-                dvec=rel_l2(to_np(dvec[ei]), ref_dv))
-    print("rel-L2", errs, flush=True)
-    for k, v in errs.items():
-        assert v < TOL, (k, v)
-
-
 # ---------------------------------------------------------------- fused radial weights
 def _radial_full(e3, plan, lay, snd, rcv, n, vec, x, h, W, dm, pad=-1, repeat=2):
     G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
@@ -910,3 +870,83 @@ def test_conv_step_in_captured_graph(e3):
         # eager work between replays, on the same buffers' inputs
         _ = e3.conv_fwd(plan, G, xs, vs, ss)
         torch.cuda.synchronize()
+
+
+
+def test_conv_on_side_stream(e3):
+    """Forward + backward launched on a stream other than torch's current one:
+    outputs and workspace are allocated for that stream, and the results equal
+    those of the current stream bit for bit, also with a large allocation made
+    on the current stream while the side stream's kernels may still run."""
+    import torch
+    _say("conv on a side stream")
+    rng = np.random.default_rng(72)
+    irreps = "128x0e+128x1o+128x2e+128x3o"
+    lay = oirreps.layout(irreps, 3, 3)
+    n, e = 400, 9000
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    plan = e3.Plan(irreps, 3, 3)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n)
+    xs = to_dev(rng.standard_normal((n, lay.d_in, C)).astype(np.float32))
+    vs = to_dev(vec)
+    ss = to_dev(rng.standard_normal((e, lay.n_paths, C)).astype(np.float32))
+    dms = to_dev(rng.standard_normal((n, lay.d_out, C)).astype(np.float32))
+    ref = [e3.conv_fwd(plan, G, xs, vs, ss), *e3.conv_bwd(plan, G, xs, vs, ss, dms)]
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        m = e3.conv_fwd(plan, G, xs, vs, ss, stream=side)
+        dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, ss, dms, stream=side)
+        junk = torch.full((64 << 20,), float("nan"), device="cuda")   # current stream
+        torch.cuda.current_stream().wait_stream(side)
+        for a, b in zip((m, dx, dvec, ds), ref):
+            assert torch.equal(a, b)
+        del junk
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- capacity (last: largest)
+def test_conv_stress_water70k_sampled(e3):
+    """70,000 H2O (210,000 atoms, ~11M edges), 64 channels: forward + backward at
+    full size on one GPU, checked on sampled rows.  Last in the file: it takes
+    most of the GPU's memory (about 250 GB) and the longest time."""
+    import torch
+    _say("conv stress water70k")
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    cfg = synth.CONFIGS["water70k"]
+    g = synth.graph(cfg)
+    N, E = g.n_nodes, g.sender.shape[0]
+    print(f"N={N} E={E}", flush=True)
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    dev = torch.device("cuda")
+    x = synth.node_features(cfg, N)
+    s = synth.normal_device(cfg.cid, 2, (E, plan.P, plan.C), dev)
+    dm = synth.normal_device(cfg.cid, 3, (N, plan.D_out, plan.C), dev)
+    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), N)
+    xs, vs = to_dev(x), to_dev(g.vec)
+    m = e3.conv_fwd(plan, G, xs, vs, s)
+    torch.cuda.synchronize()
+    lay = layout_of(cfg)
+    rng = np.random.default_rng(9)
+    rs = np.concatenate([[0, N - 1], rng.choice(N, 14, replace=False)])
+    es = np.concatenate([[0, E - 1], rng.choice(E, 30, replace=False)])
+    sfn = lambda rows: s[torch.as_tensor(rows, device=dev)].cpu().numpy()
+    ref_m = oracle_fwd_rows(lay, x, g.vec, sfn, g.sender, g.receiver, N, rs)
+    err_m = rel_l2(to_np(m[torch.as_tensor(rs, device=dev)]), ref_m)
+    del m
+    torch.cuda.empty_cache()
+    dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, s, dm)
+    torch.cuda.synchronize()
+    ref_dx, ref_ds, ref_dv = oracle_bwd_rows(lay, x, g.vec, sfn, dm, g.sender, g.receiver, N, rs, es)
+    ri, ei = torch.as_tensor(rs, device=dev), torch.as_tensor(es, device=dev)
+    errs = dict(m=err_m, dx=rel_l2(to_np(dx[ri]), ref_dx), ds=rel_l2(to_np(ds[ei]), ref_ds),
+                dvec=rel_l2(to_np(dvec[ei]), ref_dv))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    del dx, dvec, ds, s, dm, G
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
