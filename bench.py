@@ -220,6 +220,242 @@ def sweep(args, dev):
             "rows": rows, "paper_h100_GBps_context": PAPER_H100_GBPS}
 
 
+# Streaming probes of the library (e3_probe_stream): the bandwidth HBM sustains
+# for a read:write mix, with the sweeps' own load/store instructions.  Each
+# entry: name, read units, write units per step, bytes per lane, flags (1: non-
+# temporal loads, 2: non-temporal stores), and the kernels whose counter traffic
+# has that mix and instruction width (their ceiling).
+CEILING_PROBES = [
+    ("read_nt_b128", 16, 0, 16, 1, ["conv_bwd_dx"]),   # the dx segment sum reads T (98% reads)
+    ("read_nt_b64", 16, 0, 8, 1, []),
+    ("read_nt_b32", 16, 0, 4, 1, []),
+    ("read_b128", 16, 0, 16, 0, []),
+    ("write_nt_b128", 0, 16, 16, 2, []),
+    ("write_b128", 0, 16, 16, 0, []),
+    ("copy_nt_b128", 8, 8, 16, 3, []),
+    ("mix_14r1w_b64", 14, 1, 8, 3, ["conv_fwd"]),       # forward sweep: 93:7 by its counters, 8 bytes per lane
+    ("mix_14r16w_b32", 14, 16, 4, 3, ["conv_bwd_edges"]),  # backward sweep: 47:53, 4 bytes per lane
+    ("mix_2r6w_b64", 2, 6, 8, 3, ["tp_fwd"]),           # tensor product: 24:76
+    ("mix_8r2w_b64", 8, 2, 8, 3, ["tp_bwd"]),           # tensor-product backward: 81:19
+]
+
+
+def hbm_ceilings(dev, reps=10, gib=6):
+    """Run every streaming probe over `gib` GiB buffers: {name: GB/s and the mix}."""
+    import torch
+    from paper_2609_35099_amd import e3mi
+    n = (gib << 30) // 4
+    src = torch.zeros(n, dtype=torch.float32, device=dev)
+    dst = torch.empty(n, dtype=torch.float32, device=dev)
+    res = {}
+    for name, ru, wu, width, flags, _ in CEILING_PROBES:
+        for _ in range(2):
+            e3mi.probe_stream(src if ru else None, dst if wu else None, ru, wu, width, flags)
+        torch.cuda.synchronize()
+        e3mi.timing_reset()
+        e3mi.timing_enable(True)
+        for _ in range(reps):
+            br, bw = e3mi.probe_stream(src if ru else None, dst if wu else None, ru, wu, width, flags)
+        torch.cuda.synchronize()
+        e3mi.timing_enable(False)
+        ms_tot, cnt = e3mi.timing_read()["probe_stream"]
+        ms = ms_tot / cnt
+        res[name] = {"GBps": round((br + bw) / (ms * 1e-3) / 1e9, 1), "ms": round(ms, 4),
+                     "read_bytes": br, "write_bytes": bw, "bytes_per_lane": width,
+                     "nt_loads": bool(flags & 1), "nt_stores": bool(flags & 2)}
+        log(f"ceiling {name}: {res[name]['GBps']} GB/s")
+    del src, dst
+    torch.cuda.empty_cache()
+    return res
+
+
+def against_ceilings(kernels, ceil):
+    """Counter GB/s of each kernel with committed counter bytes, as a fraction of
+    the probe that matches its read:write mix."""
+    for name, _, _, _, _, users in CEILING_PROBES:
+        for k in users:
+            if k not in kernels or name not in ceil:
+                continue
+            t = counter_traffic(k)
+            if t is None:
+                continue
+            gbps = t / (kernels[k]["ms"] * 1e-3) / 1e9
+            kernels[k].update({"counter_GBps": round(gbps, 1), "ceiling": name,
+                               "frac_of_ceiling": round(gbps / ceil[name]["GBps"], 4)})
+
+
+# ---------------------------------------------------------------- profile summaries
+# rocprofv3 runs behind the files in profiles/ (on the GPU box, after
+# `cd /tmp && export TMPDIR=/tmp`; $REPO is the repository root, $OUT a results
+# directory): a kernel trace per bench section, one HBM byte counter per run,
+# and the utilisation counters.  `python bench.py --summarize-profiles $OUT`
+# reduces their CSV output to the committed summaries.
+PROF_TRACE = ("rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/trace_{s} -o trace "
+              "-- python -u $REPO/bench.py --only {s} --steps 10 --warmup 2 --no-cpu-baseline")
+PROF_PMC = ("rocprofv3 --pmc {c} --output-format csv -d $OUT/pmc_{s}_{c} -o p "
+            "-- python -u $REPO/bench.py --only {s} --steps 2 --warmup 1 --no-cpu-baseline --copy-probe")
+PROF_UTIL = ("rocprofv3 --pmc MfmaUtil VALUBusy LdsUtil SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_INSTS_VALU --output-format csv "
+             "-d $OUT/util_{s} -o u -- python -u $REPO/bench.py --only {s} --steps 2 --warmup 1 --no-cpu-baseline")
+PROF_FILES = [  # file, kind, sections, title
+    ("conv_water8k_tp200k_kernel_trace.txt", "trace", ["conv", "tp"],
+     "Kernel-time summary: convolution forward+backward (24,000-atom water box, 128 ch, l<=3) and weighted TP "
+     "forward+backward (200,000 rows)"),
+    ("bwd2_water8k_kernel_trace.txt", "trace", ["bwd2"],
+     "Kernel-time summary: double backward of the convolution (same water box)"),
+    ("linear_water8k_kernel_trace.txt", "trace", ["linear"],
+     "Kernel-time summary: linear mixing of the convolution output (24,000 nodes, 34 path blocks -> 8 irreps, 128 ch)"),
+    ("radial_water8k_kernel_trace.txt", "trace", ["radial"],
+     "Kernel-time summary: convolution with fused radial weights (same water box, K = 8 Bessel features)"),
+    ("conv_water8k_tp200k_hbm_bytes.txt", "hbm", ["conv", "tp"],
+     "HBM byte counters per dispatch (FETCH_SIZE, WRITE_SIZE in KiB), scaled by a plain 2 GiB device copy; "
+     "one counter per run"),
+    ("radial_water8k_hbm_bytes.txt", "hbm", ["radial"],
+     "HBM byte counters per dispatch (FETCH_SIZE, WRITE_SIZE in KiB), scaled by a plain 2 GiB device copy; "
+     "one counter per run"),
+    ("util_water8k_tp200k.txt", "util", ["conv", "linear", "radial", "tp"],
+     "Per-kernel utilisation (rocprofv3 derived metrics, per dispatch, mean over dispatches)"),
+]
+# kernel symbol -> short name used by the library's timing and the summaries
+PROF_NAMES = [("k_conv_bwd_edges", "conv_bwd_edges"), ("k_conv_bwd3", "conv_bwd3"), ("k_conv_fwd3", "conv_fwd3"),
+              ("k_conv_fwd_rad", "conv_fwd_rad"), ("k_conv_bwd_rad", "conv_bwd_rad_edges"),
+              ("k_conv_fwd", "conv_fwd"), ("k_conv_bwd_dx", "conv_bwd_dx"), ("k_conv_bwd_dvec", "conv_bwd_dvec"),
+              ("k_conv_bwd_dy", "conv_bwd_dy"), ("k_zero_pad", "zero_pad"), ("k_rad_grad", "rad_grad"),
+              ("k_rad_dw_sum", "rad_dw_sum"), ("k_rad_dh_sum", "rad_dh_sum"), ("k_lin_gemm", "linear_gemm(fwd+dx)"),
+              ("k_lin_dw_sum", "linear_dw_sum"), ("k_lin_dw", "linear_dw"), ("k_lin_transpose", "linear_transpose"),
+              ("k_tp_bwd_dy", "tp_bwd_dy"), ("k_tp_bwd", "tp_bwd"), ("k_tpg_sum", "tp_records_sum"),
+              ("k_tpg", "tp_records"), ("k_tp", "tp_fwd"), ("k_sh_bwd", "sh_bwd"), ("k_sh", "sh"),
+              ("k_graph_keys", "graph_keys"), ("k_graph_rowptr", "graph_rowptr"), ("k_graph_finish", "graph_finish"),
+              ("k_graph_r2s", "graph_r2s"), ("k_probe", "probe_stream")]
+COPY_PROBE = "copy_probe(__amd_rocclr_copyBuffer)"
+
+
+def _prof_short(name, cache={}):
+    import re
+    import subprocess
+    if name not in cache:
+        d = name
+        if name.startswith("_Z"):
+            d = subprocess.run(["c++filt", name], capture_output=True, text=True).stdout.strip() or name
+        short = None
+        if "__amd_rocclr_copyBuffer" in d:
+            short = COPY_PROBE
+        else:
+            for sym, nm in PROF_NAMES:
+                if re.search(r"(?<![A-Za-z0-9_])" + sym + r"(?=[<(]|$)", d):
+                    short = nm
+                    break
+        cache[name] = short
+    return cache[name]
+
+
+def _prof_rows(root, pattern):
+    import csv
+    import glob
+    out = []
+    for f in glob.glob(os.path.join(root, pattern), recursive=True):
+        out += list(csv.DictReader(open(f)))
+    return out
+
+
+def _prof_trace(root, sec):
+    d, tot = {}, 0.0
+    for r in _prof_rows(root, f"trace_{sec}/**/*kernel_trace.csv"):
+        dt = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6
+        tot += dt
+        k = _prof_short(r["Kernel_Name"])
+        if k is not None:
+            d.setdefault(k, []).append(dt)
+    lines = [f"## section {sec}"]
+    for k, v in sorted(d.items(), key=lambda kv: -sum(kv[1])):
+        lines.append(f"{k:<36s} {len(v):5d} {sum(v) / len(v):9.4f} {min(v):9.4f} {max(v):9.4f} "
+                     f"{100 * sum(v) / tot:6.2f}%")
+    return lines
+
+
+def _prof_counter(root, sec, ctr, rows_glob):
+    d = {}
+    rs = _prof_rows(root, rows_glob)
+    copies = [int(r["Grid_Size"]) for r in rs if "copyBuffer" in r["Kernel_Name"]]
+    big = max(copies) if copies else -1
+    for r in rs:
+        if r["Counter_Name"] != ctr:
+            continue
+        k = _prof_short(r["Kernel_Name"])
+        if k is None or (k == COPY_PROBE and int(r["Grid_Size"]) != big):
+            continue  # small runtime copies are not the 2 GiB calibration copy
+        slot = d.setdefault(k, {})
+        slot[r.get("Dispatch_Id")] = slot.get(r.get("Dispatch_Id"), 0.0) + float(r["Counter_Value"])
+    return {k: sum(v.values()) / len(v) for k, v in d.items()}
+
+
+def _prof_hbm(root, sec, h):
+    f = _prof_counter(root, sec, "FETCH_SIZE", f"pmc_{sec}_FETCH_SIZE/**/*counter_collection.csv")
+    w = _prof_counter(root, sec, "WRITE_SIZE", f"pmc_{sec}_WRITE_SIZE/**/*counter_collection.csv")
+    # scale: the counter bytes a plain copy of exactly 2 GiB each way reports
+    rs_, ws_ = 2097152.0 / f[COPY_PROBE], 2097152.0 / w[COPY_PROBE]
+    lines = [f"## section {sec}: the 2 GiB copy reads FETCH_SIZE {f[COPY_PROBE]:.1f} KiB -> read scale {rs_:.4f}; "
+             f"WRITE_SIZE {w[COPY_PROBE]:.1f} KiB -> write scale {ws_:.4f}",
+             "# kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | read bytes | write bytes | total bytes (scaled)"]
+    for k in sorted(f):
+        if k == COPY_PROBE or k not in w:
+            continue
+        rb, wb = int(f[k] * 1024 * rs_), int(w[k] * 1024 * ws_)
+        lines.append(f"{k:<24s} {f[k]:14.1f} {w[k]:14.1f} {rb:14d} {wb:14d} {rb + wb:14d}")
+        lines.append(f"traffic {k} {h} {rb + wb}")
+    return lines
+
+
+def _prof_util(root, sec, h):
+    mets = ["MfmaUtil", "VALUBusy", "LdsUtil", "SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_INSTS_VALU"]
+    d = {}
+    for r in _prof_rows(root, f"util_{sec}/**/*counter_collection.csv"):
+        k = _prof_short(r["Kernel_Name"])
+        if k is None or r["Counter_Name"] not in mets:
+            continue
+        slot = d.setdefault(k, {}).setdefault(r["Counter_Name"], {})
+        slot[r.get("Dispatch_Id")] = slot.get(r.get("Dispatch_Id"), 0.0) + float(r["Counter_Value"])
+    lines = [f"## section {sec}"]
+    for k in sorted(d, key=lambda k: -sum(d[k].get("SQ_INSTS_VALU", {0: 0}).values())):
+        m = {n: sum(v.values()) / len(v) for n, v in d[k].items()}
+        lines.append(f"{k:<24s} {m.get('MfmaUtil', 0):8.2f} {m.get('VALUBusy', 0):7.2f} {m.get('LdsUtil', 0):7.2f} "
+                     f"{m.get('SQ_INSTS_VALU_MFMA_MOPS_F32', 0):14.0f} {m.get('SQ_INSTS_VALU', 0):14.0f}")
+        for n in ("MfmaUtil", "VALUBusy", "LdsUtil"):
+            lines.append(f"util {k} {n} {h} {m.get(n, 0):.2f}")
+    return lines
+
+
+def summarize_profiles(root, only=None):
+    """Write the profiles/ summaries from rocprofv3 CSV output under root,
+    tagged with the hash of the kernel sources in this tree."""
+    h = source_hash()
+    for fname, kind, secs, title in PROF_FILES:
+        if only and fname not in only:
+            continue
+        if kind == "trace":
+            cmds = [PROF_TRACE.format(s=s) for s in secs]
+            body = ["# columns: kernel | calls | avg ms | min ms | max ms | share of the run's GPU time"]
+            for sec in secs:
+                body += _prof_trace(root, sec)
+        elif kind == "hbm":
+            cmds = [PROF_PMC.format(s=s, c=c) for s in secs for c in ("FETCH_SIZE", "WRITE_SIZE")]
+            body = []
+            for sec in secs:
+                body += _prof_hbm(root, sec, h)
+        else:
+            cmds = [PROF_UTIL.format(s=s) for s in secs]
+            body = ["# MfmaUtil, VALUBusy, LdsUtil in percent of the kernel's duration; MOPS_F32 in units of "
+                    "512 flop", "# kernel | MfmaUtil | VALUBusy | LdsUtil | SQ_INSTS_VALU_MFMA_MOPS_F32 | "
+                    "SQ_INSTS_VALU"]
+            for sec in secs:
+                body += _prof_util(root, sec, h)
+        head = [f"# {title}", f"# source hash (e3mi.hip, gen.cpp, builder.*): {h}",
+                "# on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`, with $REPO the repository root and "
+                "$OUT a results directory:"] + ["#   " + c for c in cmds]
+        with open(os.path.join(ROOT, "profiles", fname), "w") as fh:
+            fh.write("\n".join(head + body) + "\n")
+        log(f"wrote profiles/{fname}")
+
+
 def cpu_model() -> str:
     try:
         for ln in open("/proc/cpuinfo"):
@@ -336,18 +572,25 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tp", action="store_true")
-    ap.add_argument("--only", choices=["all", "conv", "radial", "bwd2", "linear", "tp"], default="all")
+    ap.add_argument("--only", choices=["all", "conv", "radial", "bwd2", "linear", "tp", "ceiling"], default="all")
     ap.add_argument("--order", choices=["generated", "cell"], default="generated",
                     help="atom order of the water box: as generated (spatially random) or cell-sorted")
     ap.add_argument("--sweep", action="store_true",
                     help="also run the channel sweep at fixed node x channel count (the shape of the paper's "
                          "convolution throughput table); generates ten water boxes first")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the streaming probes that measure the HBM ceilings of the kernels' read:write mixes")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one plain 2 GiB device copy (calibrates HBM byte counters)")
+    ap.add_argument("--summarize-profiles", metavar="DIR",
+                    help="only reduce the rocprofv3 CSV output under DIR to the profiles/ summaries, then exit")
     ap.add_argument("--oracle-configs", action="store_true",
                     help="only time the fp64 oracle on the whole small workloads (64-atom cube, 1,000-molecule "
                          "water box, 200,000-row tensor product) on the host cores, print one JSON line, exit")
     args = ap.parse_args()
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles)
+        return
     if args.oracle_configs:
         print(json.dumps(oracle_configs()), flush=True)
         return
@@ -366,6 +609,14 @@ def main():
     out = {"metric": METRIC, "unit": "edges/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic"}
+
+    ceil = None
+    if not args.no_ceiling and args.only in ("all", "ceiling"):
+        ceil = hbm_ceilings(dev)
+        out["ceiling"] = ceil
+        if args.only == "ceiling":
+            print(json.dumps(out), flush=True)
+            return
 
     # ---------------------------------------------------------------- conv
     cfg = synth.CONFIGS["water8k"]
@@ -445,6 +696,8 @@ def main():
                 kernels[name].update({"fma_per_edge_channel": f_fwd if name == "conv_fwd" else f_bwd,
                                       "TFLOPs": round(tf, 2), "valu_frac": round(tf / VALU_PEAK_TFLOPS, 4),
                                       "valu_busy_pct": counter_util(name, "VALUBusy")})
+        if ceil:
+            against_ceilings(kernels, ceil)
         dom_tf = kflops[dom] / (kernels[dom]["ms"] * 1e-3) / 1e12
         traffic = counter_traffic(dom)
         out.update({
@@ -634,6 +887,10 @@ def main():
                      "alg_GBps": round(nb / (t_ms * 1e-3) / 1e9, 1),
                      "frac": round(nb / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "alg_bytes": nb,
                      "event_ms": round(a0.elapsed_time(a1) / args.steps, 4)}
+        if ceil:
+            kk = {"tp_fwd": {"ms": t_ms}}
+            against_ceilings(kk, ceil)
+            out["tp"].update({k: v for k, v in kk["tp_fwd"].items() if k != "ms"})
         log(f"tp: {t_ms:.3f} ms, {out['tp']['alg_GBps']} GB/s")
         del tz
         tdz = synth.normal_device(tcfg.cid, synth._DM, (R, tplan.D_out, tplan.C), dev)
@@ -660,6 +917,10 @@ def main():
                          "alg_GBps": round(nb / (tb_ms * 1e-3) / 1e9, 1),
                          "frac": round(nb / (tb_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "alg_bytes": nb,
                          "event_ms": round(a0.elapsed_time(a1) / args.steps, 4)}
+        if ceil:
+            kk = {"tp_bwd": {"ms": tb_ms}}
+            against_ceilings(kk, ceil)
+            out["tp_bwd"].update({k: v for k, v in kk["tp_bwd"].items() if k != "ms"})
         log(f"tp_bwd: {tb_ms:.3f} ms, {out['tp_bwd']['alg_GBps']} GB/s")
         # the same product through the caller-supplied record path (the plan's records, unweighted)
         i0, i1, i2, rv = tplan.records()

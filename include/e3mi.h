@@ -233,8 +233,10 @@ e3_status e3_conv_bwd_radial(const e3_plan* plan, const e3_graph* graph, const f
  * gives its length.  irreps_in / irreps_out: irreps strings with one
  * multiplicity each (C_in, C_out multiples of 16; at most 64 blocks a side).
  * Layouts: x [n, D_in, C_in], out [n, D_out, C_out], both 16-byte aligned.
- * fp32 on the matrix cores.  The descriptor uploads its small block tables
- * to the current device on first use.
+ * fp32 on the matrix cores.  e3_linear_create uploads the descriptor's small
+ * block tables to the device current at creation (it allocates and waits for
+ * the copy; E3_ERR_HIP if that fails); the compute calls then only launch
+ * kernels, and return E3_ERR_INVALID_ARG when another device is current.
  * e3_linear_bwd: dx [n, D_in, C_in] and dW (same layout as W) from dout; dW is
  *   a fixed-order sum of fixed row-chunk partials kept in ws (at least
  *   e3_linear_workspace_size bytes), so it is deterministic. */
@@ -257,8 +259,10 @@ e3_status e3_linear_bwd(e3_linear* lin, const float* x, const float* W, const fl
  * operand rows must fit 64 KiB of staging per 64 channels (else
  * E3_ERR_UNSUPPORTED).  A wave stages up to four rows (as many as fit the
  * limit); an operand block of those rows, d C element bytes per row, must stay
- * under 2 GiB (else E3_ERR_INVALID_ARG).  Tables are uploaded to the device
- * on first use.
+ * under 2 GiB (else E3_ERR_INVALID_ARG).  e3_tpg_create uploads the tables
+ * to the device current at creation (it allocates and waits for the copy);
+ * the compute calls then only launch kernels, and return E3_ERR_INVALID_ARG
+ * when another device is current.
  * e3_tpg_bwd (eq. tp-bwd): dx = tensor_product(C^{i1}_{i2 i0}, y, dz) and
  *   dy = tensor_product(C^{i2}_{i1 i0}, x, dz), summed over the channels when y
  *   is shared (then ws holds per-slab partials, e3_tpg_workspace_size bytes,
@@ -289,6 +293,24 @@ e3_status e3_tpg_bwd_f64(e3_tpg* tpg, const double* x, const double* y, const do
 e3_status e3_timing_enable(int on);
 e3_status e3_timing_reset(void);
 e3_status e3_timing_read(int cap, char* names, double* ms, int64_t* count, int* n);
+
+/* Streaming probe (instrumentation): measures what HBM sustains for a given
+ * read:write mix, with the sweeps' own memory instructions -- buffer loads and
+ * stores of `width` bytes per lane (4, 8 or 16) at a per-lane offset, with the
+ * non-temporal bit on the loads (flags & E3_PROBE_NT_LOAD) and on the stores
+ * (flags & E3_PROBE_NT_STORE).  Throughput is defined as in App. D (bytes
+ * moved over run time).  Each step reads read_units and writes write_units
+ * contiguous units of 64 x width bytes (0..16 each, not both 0), so the mix
+ * is read_units:write_units; steps run until either buffer is exhausted.
+ * src (read) and dst (written, contents undefined afterwards) are device
+ * buffers of the caller, 16-byte aligned where used; *bytes_read and
+ * *bytes_written receive the bytes one call moves.  Asynchronous on stream;
+ * its launch is timed as "probe_stream" by e3_timing_*. */
+#define E3_PROBE_NT_LOAD 1u
+#define E3_PROBE_NT_STORE 2u
+e3_status e3_probe_stream(const void* src, size_t src_bytes, void* dst, size_t dst_bytes, int read_units,
+                          int write_units, int width, unsigned flags, size_t* bytes_read, size_t* bytes_written,
+                          e3_stream stream);
 
 const char* e3_status_str(e3_status s);
 /* Text of the last HIP error seen by this thread (empty if none). */

@@ -3150,15 +3150,15 @@ struct e3_linear {
   std::vector<LinJob> fj, bj;   // forward jobs (output blocks), dx jobs (input blocks)
   std::vector<LinSrc> fs, bs;
   std::vector<LinPair> pairs;
-  std::mutex mu;
-  char* dev = nullptr;  // device copy of the tables (uploaded on first use)
+  char* dev = nullptr;  // device copy of the tables (uploaded by e3_linear_create)
+  int device = -1;      // the device that holds it
   size_t off_fj = 0, off_fs = 0, off_bj = 0, off_bs = 0, off_pairs = 0;
 };
 
 namespace {
-e3_status lin_upload(e3_linear* L, hipStream_t st) {
-  std::lock_guard<std::mutex> lk(L->mu);
-  if (L->dev) return E3_OK;
+// Device copy of the job and pair tables, on the current device (synchronous:
+// called once, from e3_linear_create).
+e3_status lin_upload(e3_linear* L) {
   size_t off = 0;
   auto place = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
   L->off_fj = place(L->fj.size() * sizeof(LinJob) + 1);
@@ -3173,16 +3173,29 @@ e3_status lin_upload(e3_linear* L, hipStream_t st) {
   put(L->off_bj, L->bj.data(), L->bj.size() * sizeof(LinJob));
   put(L->off_bs, L->bs.data(), L->bs.size() * sizeof(LinSrc));
   put(L->off_pairs, L->pairs.data(), L->pairs.size() * sizeof(LinPair));
+  E3_HIP(hipGetDevice(&L->device));
   char* d = nullptr;
   E3_HIP(hipMalloc(&d, off));
-  hipError_t e = hipMemcpyAsync(d, host.data(), off, hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  const hipError_t e = hipMemcpy(d, host.data(), off, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     g_last_error = std::string("linear tables upload: ") + hipGetErrorString(e);
     (void)hipFree(d);
     return E3_ERR_HIP;
   }
   L->dev = d;
+  return E3_OK;
+}
+
+// The tables live on the device current at creation; a call made with another
+// device current is refused rather than reading another device's memory.
+e3_status check_device(int device, const char* what) {
+  int cur = -1;
+  E3_HIP(hipGetDevice(&cur));
+  if (cur != device) {
+    g_last_error = std::string(what) + " was created on device " + std::to_string(device) +
+                   ", called with device " + std::to_string(cur) + " current";
+    return E3_ERR_INVALID_ARG;
+  }
   return E3_OK;
 }
 
@@ -3270,6 +3283,11 @@ e3_status e3_linear_create(const char* irreps_in, const char* irreps_out, e3_lin
     for (auto& f : feeds[i]) L->bs.push_back(LinSrc{orow[f.first], 0, f.second});
     L->bj.push_back(j);
   }
+  const e3_status st = lin_upload(L);
+  if (st != E3_OK) {
+    delete L;
+    return st;
+  }
   *out = L;
   return E3_OK;
 }
@@ -3296,7 +3314,7 @@ e3_status e3_linear_fwd(e3_linear* L, const float* x, const float* W, float* out
   if (n == 0) return E3_OK;
   if (!x || !W || !out || !aligned16(x) || !aligned16(out)) return E3_ERR_INVALID_ARG;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  e3_status s = lin_upload(L, st);
+  e3_status s = check_device(L->device, "linear mixing handle");
   if (s != E3_OK) return s;
   return lin_gemm(L->fj, reinterpret_cast<const LinJob*>(L->dev + L->off_fj),
                   reinterpret_cast<const LinSrc*>(L->dev + L->off_fs), x, W, out, n, L->d_in, L->c_in, L->d_out,
@@ -3317,7 +3335,7 @@ e3_status e3_linear_bwd(e3_linear* L, const float* x, const float* W, const floa
   if (ws_bytes < lin_ws(L)) return E3_ERR_WORKSPACE_TOO_SMALL;
   if (lin_ws(L) > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  e3_status s = lin_upload(L, st);
+  e3_status s = check_device(L->device, "linear mixing handle");
   if (s != E3_OK) return s;
   const LinPair* dp = reinterpret_cast<const LinPair*>(L->dev + L->off_pairs);
   if (n > 0) {
@@ -3368,8 +3386,8 @@ struct e3_tpg {
     std::vector<TpgRec64> recs64;
     size_t off_seg = 0, off_recs = 0, off_recs64 = 0;
   } t[3];
-  std::mutex mu;
-  char* dev = nullptr;
+  char* dev = nullptr;  // device copy of the tables (uploaded by e3_tpg_create)
+  int device = -1;      // the device that holds it
 };
 
 namespace {
@@ -3389,9 +3407,9 @@ e3_tpg::Table tpg_table(int d_out, const std::vector<std::array<int, 3>>& key, c
   return T;
 }
 
-e3_status tpg_upload(e3_tpg* G, hipStream_t st) {
-  std::lock_guard<std::mutex> lk(G->mu);
-  if (G->dev) return E3_OK;
+// Device copy of the record tables, on the current device (synchronous:
+// called once, from e3_tpg_create).
+e3_status tpg_upload(e3_tpg* G) {
   size_t off = 0;
   for (auto& T : G->t) {
     T.off_seg = off;
@@ -3408,10 +3426,10 @@ e3_status tpg_upload(e3_tpg* G, hipStream_t st) {
     if (!T.recs64.empty())
       std::memcpy(host.data() + T.off_recs64, T.recs64.data(), T.recs64.size() * sizeof(TpgRec64));
   }
+  E3_HIP(hipGetDevice(&G->device));
   char* d = nullptr;
   E3_HIP(hipMalloc(&d, off));
-  hipError_t e = hipMemcpyAsync(d, host.data(), off, hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  const hipError_t e = hipMemcpy(d, host.data(), off, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     g_last_error = std::string("record tables upload: ") + hipGetErrorString(e);
     (void)hipFree(d);
@@ -3500,6 +3518,11 @@ e3_status e3_tpg_create(int d_x, int d_y, int d_z, int64_t nnz, const int32_t* i
   G->t[0] = tpg_table(d_z, kf, v);
   G->t[1] = tpg_table(d_x, kx, v);
   G->t[2] = tpg_table(d_y, ky, v);
+  const e3_status st = tpg_upload(G);
+  if (st != E3_OK) {
+    delete G;
+    return st;
+  }
   *out = G;
   return E3_OK;
 }
@@ -3519,7 +3542,7 @@ e3_status tpg_fwd(e3_tpg* G, const T* x, const T* y, T* z, int64_t rows, int C, 
   if (!G || rows < 0 || C < 1) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
   if (!x || !y || !z) return E3_ERR_INVALID_ARG;
-  e3_status s = tpg_upload(G, st);
+  e3_status s = check_device(G->device, "record tensor-product handle");
   if (s != E3_OK) return s;
   return tpg_run<T>(G, 0, x, G->d_x, y, G->d_y, !G->ypc, z, nullptr, false, rows, C,
                     sizeof(T) == 8 ? "tpg_fwd_f64" : "tpg_fwd", st);
@@ -3538,7 +3561,7 @@ e3_status tpg_bwd(e3_tpg* G, const T* x, const T* y, const T* dz, T* dx, T* dy, 
   const size_t need = tpg_ws(G, rows, C, sizeof(T));
   if (ws_bytes < need) return E3_ERR_WORKSPACE_TOO_SMALL;
   if (need > 0 && !ws) return E3_ERR_INVALID_ARG;
-  e3_status s = tpg_upload(G, st);
+  e3_status s = check_device(G->device, "record tensor-product handle");
   if (s != E3_OK) return s;
   const bool f64 = sizeof(T) == 8;
   // dx = tensor_product(C^{i1}_{i2 i0}, y, dz)
@@ -3589,3 +3612,158 @@ e3_status e3_tpg_bwd_f64(e3_tpg* G, const double* x, const double* y, const doub
 }
 
 }  // extern "C"
+
+// ============================================================ streaming probe
+// Instrumentation: the bandwidth HBM sustains for a given read:write mix, with
+// the load and store instructions of the sweeps (buffer loads and stores of
+// WB bytes per lane at a per-lane offset, with or without the non-temporal
+// bit).  Step s reads RU contiguous units of the source and writes WU
+// contiguous units of the destination (a unit is 64 lanes x WB bytes), so the
+// traffic mix is RU:WU; waves take steps in grid-stride order, so neighbouring
+// waves stream neighbouring memory.
+// Written only if a wave's sum of loaded values is 3e38, i.e. never for the
+// probe's data; its device address is a kernel argument, so that the compiler
+// cannot prove the loads feeding that sum unused.
+static __device__ __align__(256) float probe_sink[4096];
+
+namespace {
+
+template <int WB, int AUX>
+__device__ __forceinline__ float probe_load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  if constexpr (WB == 4) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX));
+  } else if constexpr (WB == 8) {
+    const f2v t = __builtin_bit_cast(f2v, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
+    return t.x + t.y;
+  } else {
+    const f4v t = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX));
+    return (t.x + t.y) + (t.z + t.w);
+  }
+}
+
+template <int WB, int AUX>
+__device__ __forceinline__ void probe_store(__amdgpu_buffer_rsrc_t r, int voff, int soff, float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  if constexpr (WB == 4) {
+    __builtin_amdgcn_raw_buffer_store_b32(u, r, voff, soff, AUX);
+  } else if constexpr (WB == 8) {
+    typedef unsigned u2v __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(u2v{u, u}, r, voff, soff, AUX);
+  } else {
+    typedef unsigned u4v __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(u4v{u, u, u, u}, r, voff, soff, AUX);
+  }
+}
+
+// Compiled probe shapes (read units, write units, bytes per lane): all loads
+// of a step are issued before any is used, as the sweeps issue a row's loads.
+#define E3_PROBE_SHAPES(X) \
+  X(16, 0, 16) X(16, 0, 8) X(16, 0, 4) X(0, 16, 16) X(0, 16, 8) X(0, 16, 4) X(8, 8, 16) X(14, 1, 8) \
+  X(14, 16, 4) X(2, 6, 8) X(8, 2, 8)
+
+template <int WB, int RU, int WU, int LA, int SA>
+__global__ __launch_bounds__(256) void k_probe(const char* __restrict__ src, char* __restrict__ dst,
+                                               int64_t n_steps, float* __restrict__ sink) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t nw = (int64_t)gridDim.x * (blockDim.x / kWave);
+  // wave index, uniform across the wave (buffer descriptors need scalar bases)
+  const int64_t w0 = (int64_t)blockIdx.x * (blockDim.x / kWave) + uniform((int)(threadIdx.x / kWave));
+  constexpr int unit = kWave * WB;
+  float acc = 0.0f;
+  for (int64_t s = w0; s < n_steps; s += nw) {
+    if constexpr (RU > 0) {
+      const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char*>(src) + s * RU * unit, (short)0, RU * unit, 0x00020000);
+      float v[RU];
+#pragma unroll
+      for (int u = 0; u < RU; ++u) v[u] = probe_load<WB, LA>(r, lane * WB, u * unit);
+#pragma unroll
+      for (int u = 0; u < RU; ++u) acc += v[u];
+    }
+    if constexpr (WU > 0) {
+      const __amdgpu_buffer_rsrc_t r =
+          __builtin_amdgcn_make_buffer_rsrc(dst + s * WU * unit, (short)0, WU * unit, 0x00020000);
+      const float val = (float)(s & 1023);
+#pragma unroll
+      for (int u = 0; u < WU; ++u) probe_store<WB, SA>(r, lane * WB, u * unit, val);
+    }
+  }
+  // keeps the loads: never true for finite data below 1e30
+  if (acc == 3.0e38f) sink[w0 & 4095] = acc;
+}
+
+template <int WB, int RU, int WU>
+void probe_launch(const char* src, char* dst, int64_t steps, unsigned flags, int blocks, float* sink,
+                  hipStream_t st) {
+  const bool nl = flags & 1u, ns = flags & 2u;
+  if (nl && ns)
+    hipLaunchKernelGGL((k_probe<WB, RU, WU, kNT, kST>), dim3(blocks), dim3(256), 0, st, src, dst, steps, sink);
+  else if (nl)
+    hipLaunchKernelGGL((k_probe<WB, RU, WU, kNT, 0>), dim3(blocks), dim3(256), 0, st, src, dst, steps, sink);
+  else if (ns)
+    hipLaunchKernelGGL((k_probe<WB, RU, WU, 0, kST>), dim3(blocks), dim3(256), 0, st, src, dst, steps, sink);
+  else
+    hipLaunchKernelGGL((k_probe<WB, RU, WU, 0, 0>), dim3(blocks), dim3(256), 0, st, src, dst, steps, sink);
+}
+
+bool probe_shape_supported(int ru, int wu, int width) {
+#define E3_PROBE_IS(R, W, B) if (ru == R && wu == W && width == B) return true;
+  E3_PROBE_SHAPES(E3_PROBE_IS)
+#undef E3_PROBE_IS
+  return false;
+}
+
+std::mutex g_sink_mu;
+float* g_sink_ptr[64] = {};
+
+// The current device's copy of probe_sink (looked up once per device).
+e3_status sink_of_current_device(float** out) {
+  int dev = -1;
+  E3_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return E3_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_sink_mu);
+  if (!g_sink_ptr[dev]) {
+    void* ptr = nullptr;
+    E3_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(probe_sink)));
+    g_sink_ptr[dev] = static_cast<float*>(ptr);
+  }
+  *out = g_sink_ptr[dev];
+  return *out ? E3_OK : E3_ERR_HIP;
+}
+}  // namespace
+
+extern "C" e3_status e3_probe_stream(const void* src, size_t src_bytes, void* dst, size_t dst_bytes,
+                                     int read_units, int write_units, int width, unsigned flags,
+                                     size_t* bytes_read, size_t* bytes_written, e3_stream stream) {
+  if (read_units < 0 || write_units < 0 || read_units + write_units == 0 ||
+      (width != 4 && width != 8 && width != 16) || flags > 3u || !bytes_read || !bytes_written)
+    return E3_ERR_INVALID_ARG;
+  if ((read_units > 0 && (!src || !aligned16(src))) || (write_units > 0 && (!dst || !aligned16(dst))))
+    return E3_ERR_INVALID_ARG;
+  if (!probe_shape_supported(read_units, write_units, width)) {
+    g_last_error = "probe shape not compiled (see E3_PROBE_SHAPES)";
+    return E3_ERR_UNSUPPORTED;
+  }
+  const int64_t unit = (int64_t)kWave * width;
+  int64_t steps = INT64_MAX;
+  if (read_units > 0) steps = std::min<int64_t>(steps, (int64_t)(src_bytes / (size_t)(unit * read_units)));
+  if (write_units > 0) steps = std::min<int64_t>(steps, (int64_t)(dst_bytes / (size_t)(unit * write_units)));
+  *bytes_read = (size_t)(steps * unit * read_units);
+  *bytes_written = (size_t)(steps * unit * write_units);
+  if (steps == 0) return E3_OK;
+  // eight waves per SIMD on every compute unit, or fewer when there is less work
+  const int blocks = (int)std::min<int64_t>((steps + 3) / 4, 2048);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const char* s = static_cast<const char*>(src);
+  char* d = static_cast<char*>(dst);
+  float* sink = nullptr;
+  const e3_status ss = sink_of_current_device(&sink);
+  if (ss != E3_OK) return ss;
+  TimedLaunch t_("probe_stream", st);
+#define E3_PROBE_GO(R, W, B) \
+  if (read_units == R && write_units == W && width == B) probe_launch<B, R, W>(s, d, steps, flags, blocks, sink, st);
+  E3_PROBE_SHAPES(E3_PROBE_GO)
+#undef E3_PROBE_GO
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}

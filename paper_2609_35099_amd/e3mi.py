@@ -80,6 +80,8 @@ SIGNATURES = {
     "e3_conv_bwd_radial": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_fwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
+    "e3_probe_stream": (_I, [_P, ct.c_size_t, _P, ct.c_size_t, _I, _I, _I, _U, ct.POINTER(ct.c_size_t),
+                             ct.POINTER(ct.c_size_t), _P]),
     "e3_timing_enable": (_I, [_I]),
     "e3_timing_reset": (_I, []),
     "e3_timing_read": (_I, [_I, _P, _P, _P, ct.POINTER(_I)]),
@@ -565,6 +567,23 @@ def conv_bwd_radial(plan: Plan, graph: Graph, x, vec, h, W, dm, dx=None, dvec=No
                                     _ptr(dW, "dW", (K, plan.P, plan.C)), ct.c_void_p(ws.data_ptr()), ws.numel(),
                                     _stream(stream)), "e3_conv_bwd_radial")
     return dx, dvec, dh, dW
+
+
+# ---------------------------------------------------------------- instrumentation
+PROBE_NT_LOAD, PROBE_NT_STORE = 1, 2
+
+
+@_on_stream
+def probe_stream(src, dst, read_units: int, write_units: int, width: int, flags: int, stream=None):
+    """One streaming probe launch; returns (bytes read, bytes written)."""
+    br, bw = ct.c_size_t(), ct.c_size_t()
+    sp = ct.c_void_p(src.data_ptr()) if src is not None else None
+    dp = ct.c_void_p(dst.data_ptr()) if dst is not None else None
+    sb = src.numel() * src.element_size() if src is not None else 0
+    db = dst.numel() * dst.element_size() if dst is not None else 0
+    _check(lib().e3_probe_stream(sp, sb, dp, db, read_units, write_units, width, flags, ct.byref(br),
+                                 ct.byref(bw), _stream(stream)), "e3_probe_stream")
+    return br.value, bw.value
 
 
 # ---------------------------------------------------------------- timing

@@ -140,44 +140,26 @@ def test_null_and_negative_arguments_rejected_before_device_work():
     assert L.e3_conv_fwd_radial(None, None, None, None, None, None, 8, None, None) == 1
 
 
-def test_linear_descriptor_matches_oracle_plan():
-    """Weight count and layout sizes of the linear-mixing descriptor (host only)."""
-    from oracle import linear as olin
-    for ins, outs in [("16x0e+16x1o+16x1o+16x2e", "32x0e+32x1o+32x1e+32x2e"),
-                      ("128x0e+128x1o+128x2e+128x3o", "128x0e+128x1o+128x2e+128x3o")]:
-        L = e3mi.Linear(ins, outs)
-        jobs, d_in, d_out, c_in, c_out, nw = olin.plan(ins, outs)
-        assert (L.n_weights, L.D_in, L.D_out, L.C_in, L.C_out) == (nw, d_in, d_out, c_in, c_out)
-        L.close()
+def test_linear_descriptor_rejects_bad_layouts():
+    """Linear-mixing descriptor: layouts it cannot take are refused before any
+    device work (host only; valid descriptors upload their tables to the
+    current device, so they are checked by the GPU tests)."""
     for bad in [("8x0e", "16x0e"), ("16x0e+8x1o", "16x0e"), ("", "16x0e")]:
-        with pytest.raises(e3mi.E3Error):
+        with pytest.raises(e3mi.E3Error) as ei:
             e3mi.Linear(*bad)
-    L = e3mi.Linear("16x0e", "16x0e")
-    Ll = e3mi.lib()
-    assert Ll.e3_linear_fwd(L.handle, None, None, None, -1, None) == 1
-    assert Ll.e3_linear_fwd(L.handle, None, None, None, 0, None) == 0
-    assert Ll.e3_linear_fwd(L.handle, None, None, None, 5, None) == 1
-    n = ct.c_size_t()
-    assert Ll.e3_linear_workspace_size(L.handle, ct.byref(n)) == 0 and n.value > 0
-    assert Ll.e3_linear_bwd(L.handle, None, None, None, None, None, None, 0, 5, None) == 1
+        assert ei.value.status in (1, 2)
 
 
 def test_record_tp_create_checks():
-    """Record tensor product descriptor: index, size and staging-limit checks (host only)."""
+    """Record tensor product descriptor: index, size and staging-limit checks,
+    all made before the tables are uploaded (host only)."""
     L = e3mi.lib()
     h = ct.c_void_p()
     i = (ct.c_int32 * 2)(0, 1)
     v = (ct.c_double * 2)(1.0, 2.0)
-    assert L.e3_tpg_create(4, 4, 4, 2, i, i, i, v, 1, ct.byref(h)) == 0
-    assert L.e3_tpg_destroy(h) == 0
     bad = (ct.c_int32 * 2)(0, 4)
     assert L.e3_tpg_create(4, 4, 4, 2, bad, i, i, v, 1, ct.byref(h)) == 3
     assert L.e3_tpg_create(0, 4, 4, 2, i, i, i, v, 1, ct.byref(h)) == 1
     assert L.e3_tpg_create(4, 4, 4, 2, None, i, i, v, 1, ct.byref(h)) == 1
     assert L.e3_tpg_create(4, 4, 400, 2, i, i, i, v, 1, ct.byref(h)) == 2     # 400 rows x 64 lanes > 64 KiB
-    assert L.e3_tpg_create(4, 4, 4, 0, None, None, None, None, 0, ct.byref(h)) == 0
-    n = ct.c_size_t()
-    assert L.e3_tpg_workspace_size(h, 10, 128, ct.byref(n)) == 0 and n.value >= 10 * 2 * 4 * 4
-    assert L.e3_tpg_fwd(h, None, None, None, 0, 8, None) == 0
-    assert L.e3_tpg_fwd(h, None, None, None, 3, 8, None) == 1
-    assert L.e3_tpg_destroy(h) == 0
+    assert L.e3_tpg_create(4, 4, 4, 2, i, i, i, v, 1, None) == 1

@@ -907,6 +907,85 @@ def test_conv_on_side_stream(e3):
     torch.cuda.synchronize()
 
 
+
+def test_linear_and_record_descriptors(e3):
+    """Descriptor sizes against the oracle's plan, and the argument checks of
+    the compute calls; a valid descriptor uploads its tables when created."""
+    import ctypes as ct
+    _say("linear and record descriptors")
+    for ins, outs in [("16x0e+16x1o+16x1o+16x2e", "32x0e+32x1o+32x1e+32x2e"),
+                      ("128x0e+128x1o+128x2e+128x3o", "128x0e+128x1o+128x2e+128x3o")]:
+        L = e3.Linear(ins, outs)
+        jobs, d_in, d_out, c_in, c_out, nw = olinear.plan(ins, outs)
+        assert (L.n_weights, L.D_in, L.D_out, L.C_in, L.C_out) == (nw, d_in, d_out, c_in, c_out)
+        L.close()
+    L = e3.Linear("16x0e", "16x0e")
+    Ll = e3.lib()
+    assert Ll.e3_linear_fwd(L.handle, None, None, None, -1, None) == 1
+    assert Ll.e3_linear_fwd(L.handle, None, None, None, 0, None) == 0
+    assert Ll.e3_linear_fwd(L.handle, None, None, None, 5, None) == 1
+    n = ct.c_size_t()
+    assert Ll.e3_linear_workspace_size(L.handle, ct.byref(n)) == 0 and n.value > 0
+    assert Ll.e3_linear_bwd(L.handle, None, None, None, None, None, None, 0, 5, None) == 1
+    L.close()
+    h = ct.c_void_p()
+    i = (ct.c_int32 * 2)(0, 1)
+    v = (ct.c_double * 2)(1.0, 2.0)
+    assert Ll.e3_tpg_create(4, 4, 4, 2, i, i, i, v, 1, ct.byref(h)) == 0
+    assert Ll.e3_tpg_destroy(h) == 0
+    assert Ll.e3_tpg_create(4, 4, 4, 0, None, None, None, None, 0, ct.byref(h)) == 0
+    assert Ll.e3_tpg_workspace_size(h, 10, 128, ct.byref(n)) == 0 and n.value >= 10 * 2 * 4 * 4
+    assert Ll.e3_tpg_fwd(h, None, None, None, 0, 8, None) == 0
+    assert Ll.e3_tpg_fwd(h, None, None, None, 3, 8, None) == 1
+    assert Ll.e3_tpg_destroy(h) == 0
+
+
+def test_first_linear_and_record_calls_in_captured_graph(e3):
+    """A linear mixing and a record tensor product whose very first forward
+    calls are made under HIP graph capture (their tables were uploaded when the
+    descriptors were created, so the calls only launch kernels): every replay
+    equals the eager result bit for bit and the oracle to the parity bar."""
+    import torch
+    _say("first linear / record calls in a captured graph")
+    rng = np.random.default_rng(73)
+    ins, outs, n = "32x0e+32x1o+32x1o", "32x0e+32x1o", 300
+    L = e3.Linear(ins, outs)
+    x = rng.standard_normal((n, L.D_in, L.C_in)).astype(np.float32)
+    W = (rng.standard_normal(L.n_weights) / 8).astype(np.float32)
+    xs, Ws = to_dev(x), to_dev(W)
+    lay = oirreps.layout("64x0e+64x1o", 2, 2)
+    recs = ocg.coo_records(lay)
+    i0, i1, i2, rv = (np.array([r[k] for r in recs]) for k in range(4))
+    R = e3.RecordTP(lay.d_in, lay.d_sh, lay.d_out, i0, i1, i2, rv, False)
+    rows = 500
+    xr = rng.standard_normal((rows, lay.d_in, lay.channels)).astype(np.float32)
+    yr = rng.standard_normal((rows, lay.d_sh)).astype(np.float32)
+    xrs, yrs = to_dev(xr), to_dev(yr)
+    out = torch.empty((n, L.D_out, L.C_out), device="cuda")
+    zr = torch.empty((rows, lay.d_out, lay.channels), device="cuda")
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        L.forward(xs, Ws, out=out)
+        R.forward(xrs, yrs, out=zr)
+    torch.cuda.synchronize()
+    ref_out = L.forward(xs, Ws)
+    ref_z = R.forward(xrs, yrs)
+    torch.cuda.synchronize()
+    assert rel_l2(to_np(ref_out), olinear.forward(ins, outs, x, W).numpy()) < TOL
+    assert rel_l2(to_np(ref_z), ogeneric.tp(i0, i1, i2, rv, xr, yr, lay.d_out)) < TOL
+    for it in range(3):
+        out.fill_(float("nan"))
+        zr.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref_out) and torch.equal(zr, ref_z), it
+        _ = L.forward(xs, Ws)
+        torch.cuda.synchronize()
+    L.close()
+    R.close()
+
+
 # ---------------------------------------------------------------- capacity (last: largest)
 def test_conv_stress_water70k_sampled(e3):
     """70,000 H2O (210,000 atoms, ~11M edges), 64 channels: forward + backward at
