@@ -169,6 +169,24 @@ e3_status e3_conv_bwd(const e3_plan* plan, const e3_graph* graph, const float* x
                       const float* s, const float* dm, float* dx, float* dvec, float* ds, void* ws,
                       size_t ws_bytes, e3_stream stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): e3_conv_bwd
+ * with its scratch -- the per-edge x-cotangent partials and the harmonic-
+ * cotangent partials -- in a fixed array of the library instead of a caller
+ * workspace.  Same arguments, outputs and results as e3_conv_bwd, bit for
+ * bit.  The array holds E3_NOALLOC_SCRATCH_BYTES (64 MiB) on each device the
+ * library runs on, kept until the process ends; a graph whose scratch
+ * (e3_conv_workspace_size's bwd_bytes) exceeds it is refused with
+ * E3_ERR_WORKSPACE_TOO_SMALL -- about 7,800 live edges with 16 feature rows
+ * of 128 channels.  The call allocates nothing (its first call on a device
+ * looks up that device's copy of the array once).  Every call on one device
+ * shares that device's array, which keeps the last call's contents: calls that
+ * overlap on one device (other streams, other threads) race, and the caller
+ * must order them. */
+#define E3_NOALLOC_SCRATCH_BYTES (64u << 20)
+e3_status e3_conv_bwd_noalloc(const e3_plan* plan, const e3_graph* graph, const float* x, const float* vec,
+                              const float* s, const float* dm, float* dx, float* dvec, float* ds, e3_stream stream);
+
 /* The convolution with the harmonics y [E, D_sh] given by the caller instead of
  * computed from edge vectors: eq. message_passing_convolution and eq. conv-bwd
  * exactly as stated (y is an input of both, dy an output of the backward).

@@ -3047,6 +3047,72 @@ e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const
                                      reinterpret_cast<hipStream_t>(stream));
 }
 
+}  // extern "C"
+
+// ------------------------------------------------------------ no-allocation backward
+// Scratch of e3_conv_bwd_noalloc: the per-edge x-cotangent partials and the
+// per-wave harmonic-cotangent partials of the backward sweep, in a fixed
+// array instead of a caller workspace.  Each device holds its own copy for the
+// life of the process.  Host code never uses the array's name as an address:
+// the device address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up on the first call made
+// with that device current.
+e3_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  E3_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) {
+    g_last_error = "device ordinal beyond the no-allocation scratch table";
+    return E3_ERR_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    E3_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) {
+      g_last_error = "hipGetSymbolAddress returned no address for the scratch array";
+      return E3_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return E3_OK;
+}
+}  // namespace
+
+extern "C" {
+
+e3_status e3_conv_bwd_noalloc(const e3_plan* p, const e3_graph* g, const float* x, const float* vec,
+                              const float* s, const float* dm, float* dx, float* dvec, float* ds, e3_stream stream) {
+  e3_status st = check_plan(p);
+  if (st != E3_OK) return st;
+  if (!g) return E3_ERR_INVALID_ARG;
+  if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
+    return E3_ERR_INVALID_ARG;
+  if (g->n_edges > 0 && (!vec || !s || !ds || !dvec || !aligned16(s) || !aligned16(ds))) return E3_ERR_INVALID_ARG;
+  const VariantOps& v = kVariants[p->variant];
+  const Ws w = v.ws(p, g);
+  if (w.t_bytes + w.dy_bytes > kNoAllocScratchBytes) {
+    g_last_error = "the backward needs " + std::to_string(w.t_bytes + w.dy_bytes) +
+                   " bytes of scratch; the no-allocation entry point has " + std::to_string(kNoAllocScratchBytes);
+    return E3_ERR_WORKSPACE_TOO_SMALL;
+  }
+  void* ptr = nullptr;
+  if ((st = scratch_of_current_device(&ptr)) != E3_OK) return st;
+  // every scratch byte the kernels read is written earlier in the same call
+  // (each live edge's partial rows and each wave's harmonic partials), so the
+  // previous call's contents need no clearing
+  return v.bwd[cpl_index(cpl_of(p))](p, g, x, vec, nullptr, s, dm, dx, dvec, nullptr, ds, 0, ptr,
+                                     reinterpret_cast<hipStream_t>(stream));
+}
+
 e3_status e3_conv_radial_workspace_size(const e3_plan* p, const e3_graph* g, int K, size_t* bwd_bytes) {
   e3_status st = check_plan(p);
   if (st != E3_OK) return st;

@@ -80,6 +80,7 @@ SIGNATURES = {
     "e3_conv_bwd_radial": (_I, [_P, _P, _P, _P, _P, _P, ct.c_int, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_fwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
+    "e3_conv_bwd_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "e3_probe_stream": (_I, [_P, ct.c_size_t, _P, ct.c_size_t, _I, _I, _I, _U, ct.POINTER(ct.c_size_t),
                              ct.POINTER(ct.c_size_t), _P]),
     "e3_timing_enable": (_I, [_I]),
@@ -352,6 +353,21 @@ def conv_bwd(plan: Plan, graph: Graph, x, vec, s, dm, dx=None, dvec=None, ds=Non
                              _ptr(dm, "dm", (N, plan.D_out, plan.C)), _ptr(dx, "dx", (N, plan.D_in, plan.C)),
                              _ptr(dvec, "dvec", (E, 3)), _ptr(ds, "ds", (E, plan.P, plan.C)),
                              ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd")
+    return dx, dvec, ds
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def conv_bwd_noalloc(plan: Plan, graph: Graph, x, vec, s, dm, dx, dvec, ds, stream=None):
+    """conv_bwd into the caller's outputs with the library's fixed scratch
+    (no allocation by the library or here; outputs must be given)."""
+    N, E = graph.n_nodes, graph.n_edges
+    _check(lib().e3_conv_bwd_noalloc(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C)),
+                                     _ptr(vec, "vec", (E, 3)), _ptr(s, "s", (E, plan.P, plan.C)),
+                                     _ptr(dm, "dm", (N, plan.D_out, plan.C)), _ptr(dx, "dx", (N, plan.D_in, plan.C)),
+                                     _ptr(dvec, "dvec", (E, 3)), _ptr(ds, "ds", (E, plan.P, plan.C)),
+                                     _stream(stream)), "e3_conv_bwd_noalloc")
     return dx, dvec, ds
 
 
