@@ -1,14 +1,23 @@
 """Build step: generate the per-variant device code, then compile libe3mi.so.
 
 1. g++ builds the table generator (csrc/gen.cpp + csrc/builder.cpp) and runs
-   it, writing csrc/generated/variants.inc (coupling constants as literals).
-2. hipcc compiles the HIP kernels, the C ABI and the builder into
-   libe3mi.so for gfx950, next to this file.
+   it, writing csrc/generated/: variants.inc (the coupling constants of every
+   compiled irreps layout as literals), one unit v_<tag>.hip per layout and
+   the core unit's table of them.
+2. hipcc compiles the core unit (csrc/e3mi.hip: C ABI, graph, linear mixing,
+   record path, probes), every layout unit and the builder for gfx950, in
+   parallel, and links libe3mi.so next to this file.
+
+Layouts beyond the defaults compiled into the generator (the benchmark and
+test layouts, natural-parity versions and one reordered block list) are
+added with E3MI_LAYOUTS, a ';'-separated list of irreps/lmax_sh/lmax_out/parity
+entries, e.g. E3MI_LAYOUTS="2e+0e+1o/3/3/all;0e+1o+1e/2/2/natural".
 
 Run: python -m paper_2609_35099_amd.build  (or __graft_entry__.build()).
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import os
 import shutil
 import subprocess
@@ -16,6 +25,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
+GEN = os.path.join(CSRC, "generated")
 ROOT = os.path.dirname(HERE)
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libe3mi.so")
@@ -38,22 +48,60 @@ def _run(cmd, verbose):
     return res
 
 
-def build(verbose: bool = True) -> str:
+def _jobs() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 4
+    return max(1, min(n, int(os.environ.get("MAX_JOBS", "16")), 16))
+
+
+def layouts_from_env() -> list[str]:
+    return [t.strip() for t in os.environ.get("E3MI_LAYOUTS", "").split(";") if t.strip()]
+
+
+def generate(verbose: bool = True, extra=None) -> list[str]:
+    """Run the generator into csrc/generated; returns the layout units."""
     os.makedirs(BUILD, exist_ok=True)
-    os.makedirs(os.path.join(CSRC, "generated"), exist_ok=True)
+    os.makedirs(GEN, exist_ok=True)
     gen = os.path.join(BUILD, "e3gen")
     _run(["g++", "-O2", "-std=c++17", "-o", gen,
           os.path.join(CSRC, "gen.cpp"), os.path.join(CSRC, "builder.cpp")], verbose)
-    inc = os.path.join(CSRC, "generated", "variants.inc")
-    tmp = inc + ".tmp"
-    _run([gen, tmp], verbose)
-    if not os.path.exists(inc) or open(inc).read() != open(tmp).read():
-        shutil.move(tmp, inc)
-    else:
-        os.remove(tmp)
+    tmp = os.path.join(BUILD, "generated.tmp")
+    shutil.rmtree(tmp, ignore_errors=True)
+    os.makedirs(tmp)
+    _run([gen, tmp, *(layouts_from_env() if extra is None else extra)], verbose)
+    units = open(os.path.join(tmp, "units.txt")).read().split()
+    # replace the generated directory's contents (unchanged files keep their times)
+    keep = set(os.listdir(tmp))
+    for f in os.listdir(GEN):
+        if f not in keep:
+            os.remove(os.path.join(GEN, f))
+    for f in keep:
+        src, dst = os.path.join(tmp, f), os.path.join(GEN, f)
+        if not os.path.exists(dst) or open(dst, "rb").read() != open(src, "rb").read():
+            shutil.copyfile(src, dst)
+    shutil.rmtree(tmp, ignore_errors=True)
+    return units
+
+
+def build(verbose: bool = True, extra=None) -> str:
+    units = generate(verbose, extra)
+    objdir = os.path.join(BUILD, "obj")
+    os.makedirs(objdir, exist_ok=True)
+    sources = [os.path.join(CSRC, "e3mi.hip"), os.path.join(CSRC, "builder.cpp")] + \
+              [os.path.join(GEN, u) for u in units]
+    objs = []
+    cmds = []
+    for src in sources:
+        obj = os.path.join(objdir, os.path.basename(src) + ".o")
+        objs.append(obj)
+        cmds.append([HIPCC, *HIP_FLAGS, "-c", "-o", obj, src])
+    with cf.ThreadPoolExecutor(max_workers=_jobs()) as ex:
+        for fut in [ex.submit(_run, c, verbose) for c in cmds]:
+            fut.result()
     out_tmp = LIB + ".tmp"
-    _run([HIPCC, *HIP_FLAGS, "-shared", "-o", out_tmp,
-          os.path.join(CSRC, "e3mi.hip"), os.path.join(CSRC, "builder.cpp")], verbose)
+    _run([HIPCC, *HIP_FLAGS, "-shared", "-o", out_tmp, *objs], verbose)
     os.replace(out_tmp, LIB)
     return LIB
 

@@ -99,12 +99,16 @@ bool make_layout(const std::string& irreps, int lmax_sh, int lmax_out, bool natu
   return true;
 }
 
+// Everything the generated kernels depend on: the x axis length and, per path
+// in order, its degrees and the first x row it reads (parities only select
+// which paths exist; the coefficients do not depend on them).
 std::string path_signature(const Layout& lay) {
-  std::string s;
+  std::string s = "D" + std::to_string(lay.d_in) + ":";
   for (size_t i = 0; i < lay.paths.size(); ++i) {
     const Path& p = lay.paths[i];
     if (i) s += ",";
-    s += std::to_string(p.l1) + "." + std::to_string(p.l2) + "." + std::to_string(p.l3);
+    s += std::to_string(p.l1) + "." + std::to_string(p.l2) + "." + std::to_string(p.l3) + "@" +
+         std::to_string(p.x_off);
   }
   return s;
 }

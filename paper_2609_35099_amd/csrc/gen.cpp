@@ -15,6 +15,7 @@
 //
 // usage: gen <out.inc>
 #include <algorithm>
+#include <cctype>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -49,18 +50,31 @@ struct Entry {     // one non-zero A[(path, M), m1]
 };
 
 struct VariantSpec {
-  std::vector<int> ls;  // degrees of the x blocks
+  std::string blocks;  // x blocks without multiplicities, e.g. "0e+1o+2e+3o"
   int lmax_sh, lmax_out;
   bool natural;
 };
 
-std::string irreps_of(const std::vector<int>& ls) {
-  std::string s;
-  for (size_t i = 0; i < ls.size(); ++i) {
-    if (i) s += "+";
-    s += "1x" + std::to_string(ls[i]) + ((ls[i] % 2) ? "o" : "e");
-  }
+// "0e+1o" -> "1x0e+1x1o" (the multiplicity does not change the kernels)
+std::string irreps_of(const std::string& blocks) {
+  std::string s, tok;
+  std::stringstream in(blocks);
+  while (std::getline(in, tok, '+')) s += (s.empty() ? "1x" : "+1x") + tok;
   return s;
+}
+
+// "irreps/lmax_sh/lmax_out/parity", parity "all" or "natural"
+bool parse_spec(const std::string& t, VariantSpec& v) {
+  std::vector<std::string> f;
+  std::string tok;
+  std::stringstream in(t);
+  while (std::getline(in, tok, '/')) f.push_back(tok);
+  if (f.size() != 4 || (f[3] != "all" && f[3] != "natural")) return false;
+  v.blocks = f[0];
+  v.lmax_sh = std::atoi(f[1].c_str());
+  v.lmax_out = std::atoi(f[2].c_str());
+  v.natural = f[3] == "natural";
+  return v.lmax_sh >= 0 && v.lmax_sh <= 3 && v.lmax_out >= 0 && v.lmax_out <= 3;
 }
 
 struct PathInfo {
@@ -750,9 +764,11 @@ void emit_group_meta(std::ostream& o, const Group& g) {
   o << "  static constexpr int OROW[" << std::max<size_t>(1, g.orows.size()) << "] = " << int_list(g.orows) << ";\n";
 }
 
+// Degrees of the blocks, with their parities when they select paths.
 std::string tag_of(const VariantSpec& v) {
   std::string t = "V_x";
-  for (int l : v.ls) t += std::to_string(l);
+  for (char c : v.blocks)
+    if (std::isdigit((unsigned char)c) || (v.natural && (c == 'e' || c == 'o'))) t += c;
   t += "_s" + std::to_string(v.lmax_sh) + "_o" + std::to_string(v.lmax_out);
   if (v.natural) t += "_n";
   return t;
@@ -762,26 +778,49 @@ std::string tag_of(const VariantSpec& v) {
 
 int main(int argc, char** argv) {
   if (argc < 2) {
-    std::fprintf(stderr, "usage: gen <out.inc> [fwd_target fwd_regs fwd_rows fwd_lead]\n");
+    std::fprintf(stderr,
+                 "usage: gen <out_dir> [irreps/lmax_sh/lmax_out/parity ...]\n"
+                 "writes <out_dir>/variants.inc (the code of every variant), variant_table.inc and one\n"
+                 "v_<tag>.hip unit per variant; the listed layouts are compiled besides the defaults\n");
     return 2;
   }
-  // Compiled variants: x blocks of degrees ls (any parities, all paths kept),
-  // harmonics up to lmax_sh, outputs up to lmax_out.
-  const std::vector<VariantSpec> specs = {
-      {{0, 1}, 2, 2, false},
-      {{0, 1, 2}, 3, 3, false},
-      {{0, 1}, 3, 3, false},
-      {{0, 1, 2, 3}, 3, 3, false},
-      {{0, 1, 2}, 2, 2, false},
+  const std::string out_dir = argv[1];
+  // Compiled variants: x blocks (all paths kept, or the natural-parity ones),
+  // harmonics up to lmax_sh, outputs up to lmax_out.  Layouts with the same
+  // kernels (same path signature and harmonics) are compiled once.
+  std::vector<VariantSpec> specs = {
+      {"0e+1o", 2, 2, false},
+      {"0e+1o+2e", 3, 3, false},
+      {"0e+1o", 3, 3, false},
+      {"0e+1o+2e+3o", 3, 3, false},
+      {"0e+1o+2e", 2, 2, false},
+      {"0e+1o", 2, 2, true},
+      {"0e+1o", 3, 3, true},
+      {"0e+1o+2e", 3, 3, true},
+      {"0e+1o+2e+3o", 3, 3, true},
+      {"1o+0e+3o+2e", 3, 3, false},
   };
+  for (int i = 2; i < argc; ++i) {
+    VariantSpec v;
+    if (!parse_spec(argv[i], v)) {
+      std::fprintf(stderr, "gen: bad layout '%s' (want irreps/lmax_sh/lmax_out/all|natural, l <= 3)\n", argv[i]);
+      return 2;
+    }
+    specs.push_back(v);
+  }
   // Forward groups: contiguous paths balanced on per-channel FMA work, each
   // within a register budget (per channel of a lane: accumulators + two
-  // buffered copies of its x rows and path weights).
-  const int FWD_TARGET = argc > 2 ? std::atoi(argv[2]) : 200;
-  const int FWD_REGS = argc > 3 ? std::atoi(argv[3]) : 1000;
-  const int FWD_RMAX = argc > 4 ? std::atoi(argv[4]) : 56;
-  if (argc > 5) kFwdLead = std::atoi(argv[5]);
-  if (argc > 6) kBwdLead = std::atoi(argv[6]);
+  // buffered copies of its x rows and path weights).  Tuning knobs from the
+  // environment (experiments only).
+  auto knob = [](const char* name, int def) {
+    const char* e = std::getenv(name);
+    return e ? std::atoi(e) : def;
+  };
+  const int FWD_TARGET = knob("E3GEN_FWD_TARGET", 200);
+  const int FWD_REGS = knob("E3GEN_FWD_REGS", 1000);
+  const int FWD_RMAX = knob("E3GEN_FWD_RMAX", 56);
+  kFwdLead = knob("E3GEN_FWD_LEAD", kFwdLead);
+  kBwdLead = knob("E3GEN_BWD_LEAD", kBwdLead);
   const int BWD_TARGET = 640;
   const int BWD_RMAX = 56;
 
@@ -791,13 +830,19 @@ int main(int argc, char** argv) {
   for (int l = 0; l <= 3; ++l) emit_sh(o, l);
 
   std::vector<std::string> tags;
+  std::set<std::string> seen;
   for (const auto& v : specs) {
     Layout lay;
     std::string err;
-    if (!make_layout(irreps_of(v.ls), v.lmax_sh, v.lmax_out, v.natural, lay, err)) {
+    if (!make_layout(irreps_of(v.blocks), v.lmax_sh, v.lmax_out, v.natural, lay, err)) {
       std::fprintf(stderr, "gen: %s\n", err.c_str());
       return 1;
     }
+    if (lay.paths.empty()) {
+      std::fprintf(stderr, "gen: layout %s has no paths\n", v.blocks.c_str());
+      return 1;
+    }
+    if (!seen.insert(path_signature(lay) + "/" + std::to_string(lay.d_sh)).second) continue;
     std::vector<PathInfo> pis = path_infos(lay);
     const int np = (int)pis.size();
     std::vector<int> fc(np), bc(np), rows(np);
@@ -902,13 +947,37 @@ int main(int argc, char** argv) {
   for (const auto& t : tags) o << " X(" << t << ")";
   o << "\n\n}  // namespace e3gen\n";
 
-  FILE* f = std::fopen(argv[1], "w");
-  if (!f) {
-    std::perror("gen");
-    return 1;
+  auto write = [&](const std::string& name, const std::string& text) {
+    const std::string path = out_dir + "/" + name;
+    FILE* f = std::fopen(path.c_str(), "w");
+    if (!f) {
+      std::perror(path.c_str());
+      return false;
+    }
+    std::fwrite(text.data(), 1, text.size(), f);
+    std::fclose(f);
+    return true;
+  };
+  if (!write("variants.inc", o.str())) return 1;
+  // the core unit's table of the variant units' entries
+  std::ostringstream t;
+  t << "// GENERATED by gen.cpp -- do not edit.\n";
+  for (const auto& tag : tags) t << "const VariantOps* e3_variant_" << tag << "();\n";
+  t << "namespace {\nconst VariantOps* (*const kVariants[])() = {";
+  for (size_t i = 0; i < tags.size(); ++i) t << (i ? ", " : "") << "&e3_variant_" << tags[i];
+  t << "};\nconstexpr int kNumVariants = " << tags.size() << ";\n}  // namespace\n";
+  if (!write("variant_table.inc", t.str())) return 1;
+  // one unit per variant: its launchers and kernels
+  for (const auto& tag : tags) {
+    std::ostringstream u;
+    u << "// GENERATED by gen.cpp -- do not edit.  Kernels and launchers of variant " << tag << ".\n";
+    u << "#include \"../e3mi_impl.h\"\n\n";
+    u << "const VariantOps* e3_variant_" << tag << "() {\n  static const VariantOps ops = E3_VARIANT_OPS(" << tag
+      << ");\n  return &ops;\n}\n";
+    if (!write("v_" + tag + ".hip", u.str())) return 1;
   }
-  std::string s = o.str();
-  std::fwrite(s.data(), 1, s.size(), f);
-  std::fclose(f);
-  return 0;
+  // the unit list, one per line, for the build
+  std::string units;
+  for (const auto& tag : tags) units += "v_" + tag + ".hip\n";
+  return write("units.txt", units) ? 0 : 1;
 }

@@ -65,6 +65,13 @@ def test_plan_tables_equal_oracle(spec, natural):
 def test_plan_supported_variants():
     for spec in LAYOUTS[:5]:
         assert e3mi.Plan(*spec).supported, spec
+        assert e3mi.Plan(*spec, natural=True).supported, spec
+    # any parities select the same kernels when every path is kept; a reordered
+    # block list has its own compiled kernels
+    assert e3mi.Plan("128x0o+128x1e+128x2o+128x3e", 3, 3).supported
+    assert e3mi.Plan("128x1o+128x0e+128x3o+128x2e", 3, 3).supported
+    # natural parities of other x parities select other paths: not compiled
+    assert not e3mi.Plan("128x0o+128x1e", 2, 2, natural=True).supported
     # a layout without a compiled kernel is still a valid plan
     p = e3mi.Plan("4x1o+4x0e+4x2o", 2, 3)
     assert not p.supported

@@ -23,6 +23,7 @@ VARIANTS = [
     ("64x0e+64x1o", 3, 3, "V_x01_s3_o3"),
     ("128x0e+128x1o+128x2e", 3, 3, "V_x012_s3_o3"),
     ("128x0e+128x1o+128x2e+128x3o", 3, 3, "V_x0123_s3_o3"),
+    ("128x1o+128x0e+128x3o+128x2e", 3, 3, "V_x1032_s3_o3"),
 ]
 
 
@@ -34,9 +35,8 @@ def generated(tmp_path_factory):
     exe = str(d / "e3gen")
     subprocess.run(["g++", "-O1", "-std=c++17", "-o", exe, os.path.join(CSRC, "gen.cpp"),
                     os.path.join(CSRC, "builder.cpp")], check=True)
-    out = d / "variants.inc"
-    subprocess.run([exe, str(out)], check=True)
-    return out.read_text()
+    subprocess.run([exe, str(d)], check=True)
+    return (d / "variants.inc").read_text()
 
 
 def _edge_ops(text, tag, kind):

@@ -24,14 +24,25 @@ from oracle import tp as otp
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_35099_amd", "csrc")
 
-# tag of the generated variant -> (x degrees, lmax_sh, lmax_out)
+# tag of the generated variant -> (x blocks, lmax_sh, lmax_out, parity)
 VARIANTS = {
-    "V_x01_s2_o2": ([0, 1], 2, 2),
-    "V_x012_s2_o2": ([0, 1, 2], 2, 2),
-    "V_x01_s3_o3": ([0, 1], 3, 3),
-    "V_x012_s3_o3": ([0, 1, 2], 3, 3),
-    "V_x0123_s3_o3": ([0, 1, 2, 3], 3, 3),
+    "V_x01_s2_o2": ("0e+1o", 2, 2, "all"),
+    "V_x012_s2_o2": ("0e+1o+2e", 2, 2, "all"),
+    "V_x01_s3_o3": ("0e+1o", 3, 3, "all"),
+    "V_x012_s3_o3": ("0e+1o+2e", 3, 3, "all"),
+    "V_x0123_s3_o3": ("0e+1o+2e+3o", 3, 3, "all"),
+    "V_x0e1o_s2_o2_n": ("0e+1o", 2, 2, "natural"),
+    "V_x0e1o_s3_o3_n": ("0e+1o", 3, 3, "natural"),
+    "V_x0e1o2e_s3_o3_n": ("0e+1o+2e", 3, 3, "natural"),
+    "V_x0e1o2e3o_s3_o3_n": ("0e+1o+2e+3o", 3, 3, "natural"),
+    "V_x1032_s3_o3": ("1o+0e+3o+2e", 3, 3, "all"),
 }
+
+
+def _layout(tag):
+    blocks, lsh, lout, parity = VARIANTS[tag]
+    irreps = "+".join("1x" + b for b in blocks.split("+"))
+    return oirreps.layout(irreps, lsh, lout, parity=parity), lsh
 
 DRIVER = r"""
 #include <cmath>
@@ -151,7 +162,7 @@ def hostlib(tmp_path_factory):
     exe = str(d / "e3gen")
     subprocess.run(["g++", "-O1", "-std=c++17", "-o", exe, os.path.join(CSRC, "gen.cpp"),
                     os.path.join(CSRC, "builder.cpp")], check=True)
-    subprocess.run([exe, str(d / "variants.inc")], check=True)
+    subprocess.run([exe, str(d)], check=True)
     (d / "driver.cpp").write_text(DRIVER)
     so = str(d / "libgenhost.so")
     subprocess.run(["g++", "-O1", "-std=c++17", "-ffp-contract=off", "-shared", "-fPIC", "-I", str(d), "-o", so,
@@ -170,9 +181,7 @@ def _rel(a, b):
 
 @pytest.mark.parametrize("tag", sorted(VARIANTS))
 def test_generated_edge_code_matches_oracle(hostlib, tag):
-    ls, lsh, lout = VARIANTS[tag]
-    irreps = "+".join(f"1x{l}{'o' if l % 2 else 'e'}" for l in ls)
-    lay = oirreps.layout(irreps, lsh, lout)
+    lay, lsh = _layout(tag)
     rng = np.random.default_rng(11)
     R = 24
     u = rng.standard_normal((R, 3))
@@ -206,9 +215,7 @@ def test_generated_edge_code_matches_oracle(hostlib, tag):
 def test_generated_three_term_forward_matches_oracle(hostlib, tag):
     """The double backward's output cotangent in one pass: the sum of three
     forward products, with the x, harmonic and weight tangents in turn."""
-    ls, lsh, lout = VARIANTS[tag]
-    irreps = "+".join(f"1x{l}{'o' if l % 2 else 'e'}" for l in ls)
-    lay = oirreps.layout(irreps, lsh, lout)
+    lay, lsh = _layout(tag)
     rng = np.random.default_rng(12)
     R = 16
     u = rng.standard_normal((R, 3))
@@ -234,9 +241,7 @@ def test_generated_three_term_backward_matches_oracle(hostlib, tag):
     """The double backward's three backward products in one pass: ds of
     (xd, y, s) and of (x, y2, s), dy of (xd, y, s) and of (x, y, sd), and the
     x cotangents of (x, y2, s) and of (x, y, sd)."""
-    ls, lsh, lout = VARIANTS[tag]
-    irreps = "+".join(f"1x{l}{'o' if l % 2 else 'e'}" for l in ls)
-    lay = oirreps.layout(irreps, lsh, lout)
+    lay, lsh = _layout(tag)
     rng = np.random.default_rng(13)
     R = 16
     u = rng.standard_normal((R, 3))

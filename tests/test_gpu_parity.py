@@ -261,6 +261,43 @@ def test_conv_random_graphs_full(e3, irreps, lsh, lout, n, e, pad):
         assert np.all(to_np(m)[pad] == 0) and np.all(to_np(dx)[pad] == 0)
 
 
+@pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad", [
+    ("8x0e+8x1o", 2, 2, "natural", 64, 900, -1),                         # the 64-atom cube's blocks
+    ("128x0e+128x1o", 3, 3, "natural", 120, 2500, 9),
+    ("32x0e+32x1o+32x2e", 3, 3, "natural", 80, 1300, -1),
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, "natural", 90, 1800, 7),      # the benchmark's blocks
+    ("128x0o+128x1e+128x2o+128x3e", 3, 3, "all", 60, 1100, -1),         # other parities, same kernels
+    ("128x1o+128x0e+128x3o+128x2e", 3, 3, "all", 100, 2100, 4),         # blocks out of degree order
+])
+def test_layout_variants_conv_and_tp(e3, irreps, lsh, lout, parity, n, e, pad):
+    """Natural-parity path sets and a reordered block list: convolution forward
+    and backward and the tensor product forward and backward, against the
+    oracle's layout of the same parity reading."""
+    _say("layout variant", irreps, parity, n, e, pad)
+    rng = np.random.default_rng(15)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = e3.Plan(irreps, lsh, lout, natural=parity == "natural")
+    assert plan.supported and (plan.P, plan.D_out) == (lay.n_paths, lay.d_out)
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    s = rng.standard_normal((e, lay.n_paths, C)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    G, m, dx, dvec, ds = _run_conv(e3, plan, snd, rcv, n, vec, x, s, dm, pad)
+    _check_full(lay, snd, rcv, n, vec, x, s, dm, m, dx, dvec, ds, pad)
+    rows = 37
+    g = rng.standard_normal((rows, 3))
+    y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
+    xt = rng.standard_normal((rows, lay.d_in, C)).astype(np.float32)
+    w = rng.standard_normal((rows, lay.n_paths, C)).astype(np.float32)
+    dz = rng.standard_normal((rows, lay.d_out, C)).astype(np.float32)
+    z = to_np(e3.tp_fwd(plan, to_dev(xt), to_dev(y), to_dev(w)))
+    assert rel_l2(z, otp.tp(lay, xt, y, w).numpy()) < TOL
+    got = [to_np(t) for t in e3.tp_bwd(plan, to_dev(xt), to_dev(y), to_dev(w), to_dev(dz))]
+    for a, r in zip(got, otp.tp_bwd(lay, xt, y, w, dz)):
+        assert rel_l2(a, r.numpy()) < TOL
+
+
 def test_conv_degenerate_graphs(e3):
     """No edges; a single edge; nodes without in-edges."""
     irreps = "128x0e+128x1o+128x2e+128x3o"
