@@ -70,7 +70,8 @@ def radial_bytes(N, E, C, D_in, D_out, P, K):
     return fwd, bwd
 
 
-KERNEL_SOURCES = ["paper_2609_35099_amd/csrc/e3mi.hip", "paper_2609_35099_amd/csrc/gen.cpp",
+KERNEL_SOURCES = ["paper_2609_35099_amd/csrc/e3mi.hip", "paper_2609_35099_amd/csrc/e3mi_impl.h",
+                  "paper_2609_35099_amd/csrc/gen.cpp",
                   "paper_2609_35099_amd/csrc/builder.cpp", "paper_2609_35099_amd/csrc/builder.h"]
 COUNTERS = os.path.join(ROOT, "profiles", "conv_water8k_tp200k_hbm_bytes.txt")
 

@@ -169,6 +169,28 @@ e3_status e3_conv_bwd(const e3_plan* plan, const e3_graph* graph, const float* x
                       const float* s, const float* dm, float* dx, float* dvec, float* ds, void* ws,
                       size_t ws_bytes, e3_stream stream);
 
+/* float64 builds of the tensor product and the convolution: the operations,
+ * layouts, index spaces and semantics of e3_tp_fwd / e3_tp_bwd / e3_conv_fwd /
+ * e3_conv_bwd with every floating-point array (x, y, w, z, dz, dx, dy, dw, vec,
+ * s, m, dm, ds, dvec) in float64 -- the precision App. D measures the float32
+ * kernels against ("Precision").  The same generated per-edge code runs in
+ * simpler kernels (one channel per lane); deterministic, atomics-free.
+ * Workspaces: e3_tp_workspace_size_f64 / e3_conv_workspace_size_f64 bytes
+ * (the x-cotangent and harmonic-cotangent partials, in float64).  Arrays with
+ * a channel axis and ws must be 16-byte aligned. */
+e3_status e3_tp_fwd_f64(const e3_plan* plan, const double* x, const double* y, const double* w, double* z,
+                        int64_t rows, e3_stream stream);
+e3_status e3_tp_workspace_size_f64(const e3_plan* plan, int64_t rows, size_t* bwd_bytes);
+e3_status e3_tp_bwd_f64(const e3_plan* plan, const double* x, const double* y, const double* w, const double* dz,
+                        double* dx, double* dy, double* dw, void* ws, size_t ws_bytes, int64_t rows,
+                        e3_stream stream);
+e3_status e3_conv_workspace_size_f64(const e3_plan* plan, const e3_graph* graph, size_t* bwd_bytes);
+e3_status e3_conv_fwd_f64(const e3_plan* plan, const e3_graph* graph, const double* x, const double* vec,
+                          const double* s, double* m, e3_stream stream);
+e3_status e3_conv_bwd_f64(const e3_plan* plan, const e3_graph* graph, const double* x, const double* vec,
+                          const double* s, const double* dm, double* dx, double* dvec, double* ds, void* ws,
+                          size_t ws_bytes, e3_stream stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): e3_conv_bwd
  * with its scratch -- the per-edge x-cotangent partials and the harmonic-

@@ -1187,6 +1187,402 @@ __global__ __launch_bounds__(256) void k_conv_bwd_dy(const float* __restrict__ D
 }
 
 
+// ------------------------------------------------------------ float64 builds
+// The tensor product and the convolution in float64, the precision the paper
+// measures its float32 kernels against (App. D, "Precision").  They run the
+// same generated per-edge code (generic in the scalar type) in simpler
+// skeletons than the float32 sweeps: one channel per lane, one 64-channel slab
+// per wave, rows through 8-byte buffer loads, harmonic cotangents summed
+// across the wave by a fixed butterfly.  Accuracy, not throughput, is their use.
+struct RowBuf64 {
+  __amdgpu_buffer_rsrc_t r;
+  int voff;      // lane's channel, bytes
+  int rowbytes;  // C * 8
+};
+
+__device__ __forceinline__ RowBuf64 row_buf64(const double* base, int64_t nbytes, int q, int C) {
+  RowBuf64 b;
+  b.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<double*>(base), (short)0,
+                                          (int)(nbytes < 0x7fffffff ? nbytes : 0x7fffffff), 0x00020000);
+  b.voff = q * 8;
+  b.rowbytes = C * 8;
+  return b;
+}
+
+__device__ __forceinline__ void bld64(const RowBuf64& b, int row, double (&v)[1]) {
+  typedef unsigned u2v __attribute__((ext_vector_type(2)));
+  v[0] = __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(b.r, b.voff, row * b.rowbytes, 0));
+  (void)sizeof(u2v);
+}
+
+__device__ __forceinline__ void bst64(const RowBuf64& b, int row, const double (&v)[1]) {
+  typedef unsigned u2v __attribute__((ext_vector_type(2)));
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u2v, v[0]), b.r, b.voff, row * b.rowbytes, 0);
+}
+
+// Sum over the 64 lanes, the same fixed butterfly on every lane.
+__device__ __forceinline__ double wave_sum64(double v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+__device__ __forceinline__ void unit_of64(const double* __restrict__ vec, int64_t e, double& ux, double& uy,
+                                          double& uz, double& inv) {
+  const double vx = vec[3 * e], vy = vec[3 * e + 1], vz = vec[3 * e + 2];
+  const double r2 = vx * vx + vy * vy + vz * vz;
+  inv = r2 > 0.0 ? 1.0 / sqrt(r2) : 0.0;
+  ux = vx * inv, uy = vy * inv, uz = vz * inv;
+}
+
+constexpr int kBatch64 = 8;  // rows / edges whose pre-contraction is staged per LDS batch
+
+template <class V>
+__global__ __launch_bounds__(kWave) void k_tp64(const double* __restrict__ x, const double* __restrict__ y,
+                                                const double* __restrict__ w, double* __restrict__ z, int64_t rows,
+                                                int C, int nslab) {
+  using F = typename V::TP;
+  __shared__ __align__(32) double sA[kBatch64 * F::NA];
+  const int lane = threadIdx.x;
+  int sl;
+  int64_t tile;
+  if (!tile_of<false>(rows, kBatch64, nslab, tile, sl)) return;
+  int ch0, lanes;
+  slab_of<1>(C, sl, ch0, lanes);
+  const int64_t r0 = tile * kBatch64;
+  const int n = (int)((rows - r0) < kBatch64 ? (rows - r0) : kBatch64);
+  if (lane < n) {
+    double Y[V::D_SH];
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) Y[i] = y[(r0 + lane) * V::D_SH + i];
+    F::make_A(Y, sA + lane * F::NA);
+  }
+  __syncthreads();
+  if (lane >= lanes) return;
+  const int q = ch0 + lane;
+  for (int j = 0; j < n; ++j) {
+    const int64_t r = r0 + j;
+    double xv[F::NXR][1], wv[F::NPATH][1];
+    const RowBuf64 xb = row_buf64(x + r * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+    const RowBuf64 wb = row_buf64(w + r * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+    const RowBuf64 zb = row_buf64(z + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+#pragma unroll
+    for (int i = 0; i < F::NXR; ++i) bld64(xb, F::XROW[i], xv[i]);
+#pragma unroll
+    for (int i = 0; i < F::NPATH; ++i) bld64(wb, F::PATH[i], wv[i]);
+    auto st = [&](int row, const double (&v)[1]) { bst64(zb, row, v); };
+    F::template rows<1>(sA + j * F::NA, xv, wv, st);
+  }
+}
+
+// Backward of one row group: dx, dw rows stored directly, dy summed over the
+// wave's channels into a per-(row, group, slab) slot of DY.
+struct Tpb64Args {
+  const double* x;
+  const double* y;
+  const double* w;
+  const double* dz;
+  double* dx;
+  double* dw;
+  double* DY;  // [rows, NBG * nslab, 16]
+  int64_t rows;
+  int C;
+  int nslab;
+};
+
+template <class V, int G>
+__device__ __forceinline__ void tpb64_task(const Tpb64Args& a, int64_t r0, int sl, double* sA, double* sY) {
+  using B = typename V::template BG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<1>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane;
+  const int n = (int)((a.rows - r0) < kBatch64 ? (a.rows - r0) : kBatch64);
+  if (lane < n) {
+    double Y[V::D_SH];
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) Y[i] = a.y[(r0 + lane) * V::D_SH + i];
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) sY[lane * V::D_SH + i] = Y[i];
+    B::make_A(Y, sA + lane * B::NA);
+  }
+  __syncthreads();
+  for (int j = 0; j < n; ++j) {
+    const int64_t r = r0 + j;
+    double dyl[V::D_SH];
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0;
+    if (act) {
+      const RowBuf64 xb = row_buf64(a.x + r * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+      const RowBuf64 wb = row_buf64(a.w + r * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+      const RowBuf64 zb = row_buf64(a.dz + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+      double xv[B::NXR][1], wv[B::NPATH][1], dzv[B::NROW][1], t[B::NXR][1], Yv[V::D_SH];
+#pragma unroll
+      for (int i = 0; i < B::NXR; ++i) bld64(xb, B::XROW[i], xv[i]), t[i][0] = 0.0;
+#pragma unroll
+      for (int i = 0; i < B::NPATH; ++i) bld64(wb, B::PATH[i], wv[i]);
+#pragma unroll
+      for (int i = 0; i < B::NROW; ++i) bld64(zb, B::OROW[i], dzv[i]);
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
+      const RowBuf64 dwb = row_buf64(a.dw + r * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+      auto st = [&](int pl, const double (&v)[1]) { bst64(dwb, B::PATH[pl], v); };
+      B::template edge<false, 1>(sA + j * B::NA, Yv, xv, wv, dzv, t, dyl, st);
+      const RowBuf64 dxb = row_buf64(a.dx + r * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+#pragma unroll
+      for (int i = 0; i < B::NXR; ++i) bst64(dxb, B::XROW[i], t[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) {
+      const double tot = wave_sum64(dyl[i]);
+      if (lane == 0) a.DY[((r * V::NBG + G) * a.nslab + sl) * 16 + i] = tot;
+    }
+  }
+}
+
+template <class V, int G>
+__device__ __forceinline__ void tpb64_dispatch(const Tpb64Args& a, int64_t r0, int g, int sl, double* sA,
+                                               double* sY) {
+  if constexpr (G < V::NBG) {
+    if (g == G)
+      tpb64_task<V, G>(a, r0, sl, sA, sY);
+    else
+      tpb64_dispatch<V, G + 1>(a, r0, g, sl, sA, sY);
+  }
+}
+
+template <class V>
+__global__ __launch_bounds__(kWave, 1) void k_tp_bwd64(Tpb64Args a) {
+  __shared__ __align__(32) double smem[kBatch64 * (V::MAX_NA_B + V::D_SH)];
+  int t;
+  int64_t tile;
+  if (!tile_of<false>(a.rows, kBatch64, V::NBG * a.nslab, tile, t)) return;
+  tpb64_dispatch<V, 0>(a, tile * kBatch64, t / a.nslab, t % a.nslab, smem, smem + kBatch64 * V::MAX_NA_B);
+}
+
+// dy of each row (or live edge): the sum of its per-(group, slab) partials, in order.
+template <class V>
+__global__ __launch_bounds__(256) void k_dy_sum64(const double* __restrict__ DY, const int* __restrict__ eid,
+                                                  double* __restrict__ dy, int64_t n, int nslab) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = i / V::D_SH;
+  const int c = (int)(i % V::D_SH);
+  if (r >= n) return;
+  double v = 0.0;
+  for (int g = 0; g < V::NBG * nslab; ++g) v += DY[(r * V::NBG * nslab + g) * 16 + c];
+  dy[(eid ? (int64_t)eid[r] : r) * V::D_SH + c] = v;
+}
+
+// Convolution forward: one wave per (receiver, forward group, slab); the
+// receiver's sums in registers, stored once.
+template <class V, int G>
+__device__ __forceinline__ void fwd64_task(const ConvArgs& a, const double* x, const double* vec, const double* s,
+                                           double* m, int b, int sl, double* sA) {
+  using F = typename V::template FG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<1>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  double acc[F::NROW][1];
+#pragma unroll
+  for (int i = 0; i < F::NROW; ++i) acc[i][0] = 0.0;
+  for (int eb = e0; eb < e1; eb += kBatch64) {
+    const int n = imin(kBatch64, e1 - eb);
+    int my_e = 0, my_src = 0;
+    if (lane < n) {
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
+      double ux, uy, uz, inv, Y[V::D_SH];
+      unit_of64(vec, my_e, ux, uy, uz, inv);
+      V::sh(ux, uy, uz, Y);
+      F::make_A(Y, sA + lane * F::NA);
+    }
+    __syncthreads();
+    if (act) {
+      for (int j = 0; j < n; ++j) {
+        const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+        const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+        const RowBuf64 xb = row_buf64(x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+        const RowBuf64 sb = row_buf64(s + e * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+        double xv[F::NXR][1], sv[F::NPATH][1];
+#pragma unroll
+        for (int i = 0; i < F::NXR; ++i) bld64(xb, F::XROW[i], xv[i]);
+#pragma unroll
+        for (int i = 0; i < F::NPATH; ++i) bld64(sb, F::PATH[i], sv[i]);
+        F::template edge<1>(sA + j * F::NA, xv, sv, acc);
+      }
+    }
+    __syncthreads();
+  }
+  if (act) {
+    const RowBuf64 mb = row_buf64(m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+#pragma unroll
+    for (int i = 0; i < F::NROW; ++i) bst64(mb, F::OROW[i], acc[i]);
+  }
+}
+
+template <class V, int G>
+__device__ __forceinline__ void fwd64_dispatch(const ConvArgs& a, const double* x, const double* vec,
+                                               const double* s, double* m, int b, int g, int sl, double* sA) {
+  if constexpr (G < V::NFG) {
+    if (g == G)
+      fwd64_task<V, G>(a, x, vec, s, m, b, sl, sA);
+    else
+      fwd64_dispatch<V, G + 1>(a, x, vec, s, m, b, g, sl, sA);
+  }
+}
+
+template <class V>
+__global__ __launch_bounds__(kWave, 1) void k_conv_fwd64(ConvArgs a, const double* __restrict__ x,
+                                                         const double* __restrict__ vec,
+                                                         const double* __restrict__ s, double* __restrict__ m) {
+  __shared__ __align__(32) double sA[kBatch64 * V::MAX_NA_F];
+  int b, g, sl;
+  if (!task_of<V::NFG>(a, b, g, sl)) return;
+  fwd64_dispatch<V, 0>(a, x, vec, s, m, b, g, sl, sA);
+}
+
+// Convolution backward sweep in receiver order: ds per edge, the x-cotangent
+// partials T at the edge's sender-CSR slot, the per-wave harmonic cotangents.
+struct Conv64Out {
+  const double* x;
+  const double* vec;
+  const double* s;
+  const double* dm;
+  double* ds;
+  double* T;   // [n_live, D_in, C]
+  double* DY;  // [n_live, NBG * nslab, 16]
+};
+
+template <class V, int G>
+__device__ __forceinline__ void bwd64_task(const ConvArgs& a, const Conv64Out& o, int b, int sl, double* sA,
+                                           double* sY) {
+  using B = typename V::template BG<G>;
+  const int lane = threadIdx.x;
+  int ch0, lanes;
+  slab_of<1>(a.C, sl, ch0, lanes);
+  const bool act = lane < lanes;
+  const int C = a.C, q = ch0 + lane;
+  const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
+  if (e0 == e1) return;
+  double dmv[B::NROW][1];
+  if (act) {
+    const RowBuf64 db = row_buf64(o.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+#pragma unroll
+    for (int i = 0; i < B::NROW; ++i) bld64(db, B::OROW[i], dmv[i]);
+  }
+  for (int eb = e0; eb < e1; eb += kBatch64) {
+    const int n = imin(kBatch64, e1 - eb);
+    int my_e = 0, my_src = 0, my_slot = 0;
+    if (lane < n) {
+      my_e = a.eid[eb + lane];
+      my_src = a.src[eb + lane];
+      my_slot = a.r2s[eb + lane];
+      double ux, uy, uz, inv, Y[V::D_SH];
+      unit_of64(o.vec, my_e, ux, uy, uz, inv);
+      V::sh(ux, uy, uz, Y);
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) sY[lane * V::D_SH + i] = Y[i];
+      B::make_A(Y, sA + lane * B::NA);
+    }
+    __syncthreads();
+    for (int j = 0; j < n; ++j) {
+      const int64_t e = __builtin_amdgcn_readlane(my_e, j);
+      const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
+      const int64_t slot = __builtin_amdgcn_readlane(my_slot, j);
+      double dyl[V::D_SH];
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0;
+      if (act) {
+        const RowBuf64 xb = row_buf64(o.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+        const RowBuf64 sb = row_buf64(o.s + e * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+        double xv[B::NXR][1], sv[B::NPATH][1], t[B::NXR][1], Yv[V::D_SH];
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) bld64(xb, B::XROW[i], xv[i]), t[i][0] = 0.0;
+#pragma unroll
+        for (int i = 0; i < B::NPATH; ++i) bld64(sb, B::PATH[i], sv[i]);
+#pragma unroll
+        for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
+        const RowBuf64 dsb = row_buf64(o.ds + e * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+        auto st = [&](int pl, const double (&v)[1]) { bst64(dsb, B::PATH[pl], v); };
+        B::template edge<false, 1>(sA + j * B::NA, Yv, xv, sv, dmv, t, dyl, st);
+        const RowBuf64 Tb = row_buf64(o.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+#pragma unroll
+        for (int i = 0; i < B::NXR; ++i) bst64(Tb, B::XROW[i], t[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < V::D_SH; ++i) {
+        const double tot = wave_sum64(dyl[i]);
+        if (lane == 0) o.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + i] = tot;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <class V, int G>
+__device__ __forceinline__ void bwd64_dispatch(const ConvArgs& a, const Conv64Out& o, int b, int g, int sl,
+                                               double* sA, double* sY) {
+  if constexpr (G < V::NBG) {
+    if (g == G)
+      bwd64_task<V, G>(a, o, b, sl, sA, sY);
+    else
+      bwd64_dispatch<V, G + 1>(a, o, b, g, sl, sA, sY);
+  }
+}
+
+template <class V>
+__global__ __launch_bounds__(kWave, 1) void k_conv_bwd64(ConvArgs a, Conv64Out o) {
+  __shared__ __align__(32) double smem[kBatch64 * (V::MAX_NA_B + V::D_SH)];
+  int b, g, sl;
+  if (!task_of<V::NBG>(a, b, g, sl)) return;
+  bwd64_dispatch<V, 0>(a, o, b, g, sl, smem, smem + kBatch64 * V::MAX_NA_B);
+}
+
+// dx[node] = sum of its partial rows in sender-CSR order (one wave per node
+// and 64-channel slab, rows walked in registers).
+__global__ __launch_bounds__(kWave) void k_conv_bwd_dx64(const double* __restrict__ T, double* __restrict__ dx,
+                                                         const int* __restrict__ rowptr_s, int n_nodes, int D_in,
+                                                         int C, int nslab) {
+  const int64_t bid = blockIdx.x;
+  const int node = (int)(bid / nslab), sl = (int)(bid % nslab);
+  if (node >= n_nodes) return;
+  const int q = sl * kWave + threadIdx.x;
+  if (q >= C) return;
+  const int s0 = uniform(rowptr_s[node]), s1 = uniform(rowptr_s[node + 1]);
+  for (int i = 0; i < D_in; ++i) {
+    double acc = 0.0;
+    for (int t = s0; t < s1; ++t) acc += T[((int64_t)t * D_in + i) * C + q];
+    dx[((int64_t)node * D_in + i) * C + q] = acc;
+  }
+}
+
+// dvec of each live edge from its harmonic cotangent (summed over groups).
+template <class V>
+__global__ __launch_bounds__(256) void k_conv_bwd_dvec64(const double* __restrict__ vec,
+                                                         const double* __restrict__ DY, const int* __restrict__ eid,
+                                                         double* __restrict__ dvec, int64_t n_live, int nslab) {
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (pos >= n_live) return;
+  const int64_t e = eid[pos];
+  double dY[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) dY[i] = 0.0;
+  for (int g = 0; g < V::NBG * nslab; ++g)
+#pragma unroll
+    for (int i = 0; i < V::D_SH; ++i) dY[i] += DY[(pos * V::NBG * nslab + g) * 16 + i];
+  double ux, uy, uz, inv, gx, gy, gz;
+  unit_of64(vec, e, ux, uy, uz, inv);
+  V::sh_grad(ux, uy, uz, dY, gx, gy, gz);
+  const double ug = ux * gx + uy * gy + uz * gz;
+  dvec[3 * e] = (gx - ux * ug) * inv;
+  dvec[3 * e + 1] = (gy - uy * ug) * inv;
+  dvec[3 * e + 2] = (gz - uz * ug) * inv;
+}
+
 // ------------------------------------------------------------ fused radial weights
 // The per-edge weights s_e = h_e W (K radial features times a K x (P C)
 // matrix) are formed in the sweep kernels on the matrix cores and never
@@ -1709,6 +2105,16 @@ struct VariantOps {
                     const float*, const float*, float*, hipStream_t);
   e3_status (*bwd3)(const e3_plan*, const e3_graph*, const float*, const float*, const float*, const float*,
                     const float*, const float*, const float*, float*, float*, float*, void*, hipStream_t);
+  // float64 builds
+  e3_status (*tp64)(const e3_plan*, const double*, const double*, const double*, double*, int64_t, hipStream_t);
+  e3_status (*tpb64)(const e3_plan*, const double*, const double*, const double*, const double*, double*, double*,
+                     double*, void*, int64_t, hipStream_t);
+  size_t (*tpws64)(const e3_plan*, int64_t);
+  e3_status (*fwd64)(const e3_plan*, const e3_graph*, const double*, const double*, const double*, double*,
+                     hipStream_t);
+  e3_status (*bwd64)(const e3_plan*, const e3_graph*, const double*, const double*, const double*, const double*,
+                     double*, double*, double*, void*, hipStream_t);
+  Ws (*ws64)(const e3_plan*, const e3_graph*);
 };
 
 namespace {
@@ -2052,6 +2458,103 @@ size_t tp_ws(const e3_plan* p, int64_t rows) {
 
 
 
+// ---- float64 builds (one channel per lane)
+inline int nslab64(const e3_plan* p) { return (p->lay.C + kWave - 1) / kWave; }
+
+template <class V>
+Ws bwd_ws64(const e3_plan* p, const e3_graph* g) {
+  Ws w;
+  w.t_bytes = align256((size_t)g->n_live * V::D_IN * p->lay.C * sizeof(double));
+  w.dy_bytes = align256((size_t)g->n_live * V::NBG * nslab64(p) * 16 * sizeof(double));
+  return w;
+}
+
+template <class V>
+size_t tp_ws64(const e3_plan* p, int64_t rows) {
+  return align256((size_t)rows * V::NBG * nslab64(p) * 16 * sizeof(double));
+}
+
+template <class V>
+e3_status run_tp64(const e3_plan* p, const double* x, const double* y, const double* w, double* z, int64_t rows,
+                   hipStream_t st) {
+  const int nsl = nslab64(p);
+  const int64_t grid = tile_grid(false, rows, kBatch64, nsl);
+  if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
+  TimedLaunch t_("tp_fwd_f64", st);
+  hipLaunchKernelGGL((k_tp64<V>), dim3((unsigned)grid), dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, nsl);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status run_tp_bwd64(const e3_plan* p, const double* x, const double* y, const double* w, const double* dz,
+                       double* dx, double* dy, double* dw, void* ws, int64_t rows, hipStream_t st) {
+  const int nsl = nslab64(p);
+  Tpb64Args a{x, y, w, dz, dx, dw, reinterpret_cast<double*>(ws), rows, p->lay.C, nsl};
+  const int64_t grid = tile_grid(false, rows, kBatch64, V::NBG * nsl);
+  if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
+  {
+    TimedLaunch t_("tp_bwd_f64", st);
+    hipLaunchKernelGGL((k_tp_bwd64<V>), dim3((unsigned)grid), dim3(kWave), 0, st, a);
+    E3_HIP(hipGetLastError());
+  }
+  TimedLaunch t_("tp_bwd_dy_f64", st);
+  hipLaunchKernelGGL((k_dy_sum64<V>), dim3(blocks_for(rows * V::D_SH, 256)), dim3(256), 0, st, a.DY,
+                     (const int*)nullptr, dy, rows, nsl);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status run_fwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                    double* m, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.nslab = nslab64(p);
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
+  TimedLaunch t_("conv_fwd_f64", st);
+  hipLaunchKernelGGL((k_conv_fwd64<V>), dim3(grid), dim3(kWave), 0, st, a, x, vec, s, m);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status run_bwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                    const double* dm, double* dx, double* dvec, double* ds, void* ws, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  const Ws w = bwd_ws64<V>(p, g);
+  ConvArgs a = base_args(p, g);
+  a.nslab = nslab64(p);
+  Conv64Out o{x, vec, s, dm, ds, reinterpret_cast<double*>(ws),
+              reinterpret_cast<double*>(reinterpret_cast<char*>(ws) + w.t_bytes)};
+  if (g->n_live > 0) {
+    const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
+    TimedLaunch t_("conv_bwd_edges_f64", st);
+    hipLaunchKernelGGL((k_conv_bwd64<V>), dim3(grid), dim3(kWave), 0, st, a, o);
+    E3_HIP(hipGetLastError());
+  }
+  {
+    TimedLaunch t_("conv_bwd_dx_f64", st);
+    hipLaunchKernelGGL(k_conv_bwd_dx64, dim3((unsigned)(g->n_nodes * a.nslab)), dim3(kWave), 0, st, o.T, dx,
+                       g->rowptr_s, a.n_nodes, V::D_IN, a.C, a.nslab);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_live > 0) {
+    TimedLaunch t_("conv_bwd_dvec_f64", st);
+    hipLaunchKernelGGL((k_conv_bwd_dvec64<V>), dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, vec, o.DY,
+                       g->eid_r, dvec, g->n_live, a.nslab);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_pad > 0) {  // padding edges: zero ds and dvec rows (as pairs of 32-bit zeros)
+    TimedLaunch t_("conv_bwd_pad", st);
+    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad,
+                       reinterpret_cast<float*>(ds), (int64_t)2 * V::NP * a.C, reinterpret_cast<float*>(dvec),
+                       (int64_t)6);
+    E3_HIP(hipGetLastError());
+  }
+  return E3_OK;
+}
+
 }  // namespace
 
 // One variant's entry in the core unit's table (constant-initialised).
@@ -2073,4 +2576,10 @@ size_t tp_ws(const e3_plan* p, int64_t rows) {
              &run_bwd_rad<e3gen::V>,                                                                     \
              &rad_ws<e3gen::V>,                                                                          \
              &run_fwd3<e3gen::V>,                                                                        \
-             &run_bwd3<e3gen::V>}
+             &run_bwd3<e3gen::V>,                                                                        \
+             &run_tp64<e3gen::V>,                                                                        \
+             &run_tp_bwd64<e3gen::V>,                                                                    \
+             &tp_ws64<e3gen::V>,                                                                         \
+             &run_fwd64<e3gen::V>,                                                                       \
+             &run_bwd64<e3gen::V>,                                                                       \
+             &bwd_ws64<e3gen::V>}

@@ -33,7 +33,7 @@ namespace {
 
 std::string flit(double v) {
   char buf[64];
-  std::snprintf(buf, sizeof(buf), "%.9ef", v);
+  std::snprintf(buf, sizeof(buf), "T(%.17e)", v);
   return buf;
 }
 
@@ -258,30 +258,30 @@ void emit_sh(std::ostream& o, int lmax) {
   const size_t nm = t.mono.size();
   auto powname = [](int axis, int e) {
     const char* a = axis == 0 ? "x" : (axis == 1 ? "y" : "z");
-    return e == 0 ? std::string("1.0f") : std::string(a) + std::to_string(e);
+    return e == 0 ? std::string("T(1)") : std::string(a) + std::to_string(e);
   };
   auto emit_pows = [&](int upto) {
     for (int e = 2; e <= upto; ++e)
       for (int a = 0; a < 3; ++a) {
         const char* n = a == 0 ? "x" : (a == 1 ? "y" : "z");
-        o << "  const float " << n << e << " = " << n << (e - 1 == 1 ? std::string("") : std::to_string(e - 1))
+        o << "  const T " << n << e << " = " << n << (e - 1 == 1 ? std::string("") : std::to_string(e - 1))
           << " * " << n << ";\n";
       }
-    o << "  const float x1 = x, y1 = y, z1 = z; (void)x1; (void)y1; (void)z1;\n";
+    o << "  const T x1 = x, y1 = y, z1 = z; (void)x1; (void)y1; (void)z1;\n";
   };
   auto mono_expr = [&](const std::array<int, 3>& m) {
     std::vector<std::string> f;
     for (int a = 0; a < 3; ++a)
       if (m[a]) f.push_back(powname(a, m[a]));
-    if (f.empty()) return std::string("1.0f");
+    if (f.empty()) return std::string("T(1)");
     std::string s;
     for (size_t i = 0; i < f.size(); ++i) s += (i ? " * " : "") + f[i];
     return s;
   };
   // values
   o << "// Real harmonics l <= " << lmax << " of a unit vector (x, y, z); rows l-major, m = -l..l.\n";
-  o << "__device__ __forceinline__ void sh_l" << lmax
-    << "(const float x, const float y, const float z, float* __restrict__ Y) {\n";
+  o << "template <class T>\n__device__ __forceinline__ void sh_l" << lmax
+    << "(const T x, const T y, const T z, T* __restrict__ Y) {\n";
   emit_pows(lmax);
   for (int r = 0; r < nrow; ++r) {
     std::string acc;
@@ -291,14 +291,14 @@ void emit_sh(std::ostream& o, int lmax) {
       std::string term = flit(c) + " * (" + mono_expr(t.mono[j]) + ")";
       acc += acc.empty() ? term : " + " + term;
     }
-    if (acc.empty()) acc = "0.0f";
+    if (acc.empty()) acc = "T(0)";
     o << "  Y[" << r << "] = " << acc << ";\n";
   }
   o << "}\n\n";
   // gradient of sum_r dY[r] P_r(u) with respect to u (polynomial gradient)
   o << "// g = sum_r dY[r] grad P_r(x, y, z), P_r the harmonic polynomials above.\n";
-  o << "__device__ __forceinline__ void sh_grad_l" << lmax
-    << "(const float x, const float y, const float z, const float* __restrict__ dY, float& gx, float& gy, float& gz) {\n";
+  o << "template <class T>\n__device__ __forceinline__ void sh_grad_l" << lmax
+    << "(const T x, const T y, const T z, const T* __restrict__ dY, T& gx, T& gy, T& gz) {\n";
   emit_pows(std::max(lmax - 1, 1));
   const char* gn[3] = {"gx", "gy", "gz"};
   for (int a = 0; a < 3; ++a) {
@@ -313,11 +313,11 @@ void emit_sh(std::ostream& o, int lmax) {
         d[a] -= 1;
         terms[d].push_back({r, f});
       }
-    o << "  " << gn[a] << " = 0.0f;\n";
+    o << "  " << gn[a] << " = T(0);\n";
     for (const auto& [m, lst] : terms) {
       std::string w;
       for (const auto& [r, f] : lst) w += (w.empty() ? "" : " + ") + flit(f) + " * dY[" + std::to_string(r) + "]";
-      o << "  " << gn[a] << " = fmaf(" << mono_expr(m) << ", " << w << ", " << gn[a] << ");\n";
+      o << "  " << gn[a] << " = e3fma(" << mono_expr(m) << ", " << w << ", " << gn[a] << ");\n";
     }
   }
   o << "}\n\n";
@@ -326,23 +326,24 @@ void emit_sh(std::ostream& o, int lmax) {
 // ------------------------------------------------------------------ groups
 void emit_make_A(std::ostream& o, const Group& g) {
   o << "  // A[entry] = sum_m2 C[M, m1, m2] y[m2] for entries (path, M, m1) of this group\n";
-  o << "  __device__ __forceinline__ static void make_A(const float* __restrict__ y, float* __restrict__ A) {\n";
+  o << "  template <class T>\n  __device__ __forceinline__ static void make_A(const T* __restrict__ y, T* __restrict__ A) {\n";
+  o << "    using T4 = typename Vec4<T>::type;\n";
   const int na = (int)g.entries.size();
   for (int q = 0; q < g.na_pad / 4; ++q) {
-    o << "    { float4 v;\n";
+    o << "    { T4 v;\n";
     const char* comp[4] = {"x", "y", "z", "w"};
     for (int c = 0; c < 4; ++c) {
       int i = 4 * q + c;
-      std::string expr = "0.0f";
+      std::string expr = "T(0)";
       if (i < na) {
         const Entry& e = g.entries[i];
         expr = flit(e.recs[0].c) + " * y[" + std::to_string(e.recs[0].m2) + "]";
         for (size_t r = 1; r < e.recs.size(); ++r)
-          expr = "fmaf(" + flit(e.recs[r].c) + ", y[" + std::to_string(e.recs[r].m2) + "], " + expr + ")";
+          expr = "e3fma(" + flit(e.recs[r].c) + ", y[" + std::to_string(e.recs[r].m2) + "], " + expr + ")";
       }
       o << "      v." << comp[c] << " = " << expr << ";\n";
     }
-    o << "      reinterpret_cast<float4*>(A)[" << q << "] = v; }\n";
+    o << "      reinterpret_cast<T4*>(A)[" << q << "] = v; }\n";
   }
   o << "  }\n";
 }
@@ -356,7 +357,7 @@ std::string aval(int i) {
 void emit_A_loads(std::ostream& o, int lo, int hi, std::vector<bool>& loaded, const char* ind) {
   for (int q = lo / 4; q <= (hi - 1) / 4; ++q) {
     if (q < (int)loaded.size() && !loaded[q]) {
-      o << ind << "const float4 a" << q << " = A4[" << q << "];\n";
+      o << ind << "const T4 a" << q << " = A4[" << q << "];\n";
       loaded[q] = true;
     }
   }
@@ -371,10 +372,11 @@ int kFwdLead = 4;
 int kBwdLead = 2;
 
 void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
-  o << "  template <int CPL>\n";
-  o << "  __device__ __forceinline__ static void edge(const float* __restrict__ A, const float (&x)[NXR][CPL],\n"
-       "      const float (&s)[NPATH][CPL], float (&acc)[NROW][CPL]) {\n";
-  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  o << "  template <int CPL, class T>\n";
+  o << "  __device__ __forceinline__ static void edge(const T* __restrict__ A, const T (&x)[NXR][CPL],\n"
+       "      const T (&s)[NPATH][CPL], T (&acc)[NROW][CPL]) {\n";
+  o << "    using T4 = typename Vec4<T>::type;\n";
+  o << "    const T4* __restrict__ A4 = reinterpret_cast<const T4*>(A);\n";
   struct Row {
     int pl, M, orow, lo, hi;
   };
@@ -403,11 +405,11 @@ void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
     for (int i = rw.lo; i < rw.hi; ++i) {
       const int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
       if (i == rw.lo)
-        o << "        float z = " << aval(i) << " * x[" << xl << "][c];\n";
+        o << "        T z = " << aval(i) << " * x[" << xl << "][c];\n";
       else
-        o << "        z = fmaf(" << aval(i) << ", x[" << xl << "][c], z);\n";
+        o << "        z = e3fma(" << aval(i) << ", x[" << xl << "][c], z);\n";
     }
-    o << "        acc[" << rw.orow << "][c] = fmaf(s[" << rw.pl << "][c], z, acc[" << rw.orow << "][c]);\n";
+    o << "        acc[" << rw.orow << "][c] = e3fma(s[" << rw.pl << "][c], z, acc[" << rw.orow << "][c]);\n";
     o << "      }\n    }\n";
   }
   o << "  }\n";
@@ -418,12 +420,13 @@ void emit_fwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
 // pass: acc += s (A xd + A2 x) + sd (A x), with A from the harmonics y and A2
 // from their tangent yd (same entry layout).
 void emit_fwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Group& g) {
-  o << "  template <int CPL>\n";
-  o << "  __device__ __forceinline__ static void edge3(const float* __restrict__ A, const float* __restrict__ A2,\n"
-       "      const float (&x)[NXR][CPL], const float (&xd)[NXR][CPL], const float (&s)[NPATH][CPL],\n"
-       "      const float (&sd)[NPATH][CPL], float (&acc)[NROW][CPL]) {\n";
-  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
-  o << "    const float4* __restrict__ B4 = reinterpret_cast<const float4*>(A2);\n";
+  o << "  template <int CPL, class T>\n";
+  o << "  __device__ __forceinline__ static void edge3(const T* __restrict__ A, const T* __restrict__ A2,\n"
+       "      const T (&x)[NXR][CPL], const T (&xd)[NXR][CPL], const T (&s)[NPATH][CPL],\n"
+       "      const T (&sd)[NPATH][CPL], T (&acc)[NROW][CPL]) {\n";
+  o << "    using T4 = typename Vec4<T>::type;\n";
+  o << "    const T4* __restrict__ A4 = reinterpret_cast<const T4*>(A);\n";
+  o << "    const T4* __restrict__ B4 = reinterpret_cast<const T4*>(A2);\n";
   std::vector<bool> loaded(g.na_pad / 4, false);
   int ei = 0, orow = 0;
   for (size_t pl = 0; pl < g.paths.size(); ++pl) {
@@ -434,7 +437,7 @@ void emit_fwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
       if (ei == lo) continue;
       for (int q = lo / 4; q <= (ei - 1) / 4; ++q)
         if (!loaded[q]) {
-          o << "    const float4 a" << q << " = A4[" << q << "], b" << q << " = B4[" << q << "];\n";
+          o << "    const T4 a" << q << " = A4[" << q << "], b" << q << " = B4[" << q << "];\n";
           loaded[q] = true;
         }
       o << "    {  // path " << pi.p.k << " (" << pi.p.l1 << "," << pi.p.l2 << "," << pi.p.l3 << ") row " << M << "\n";
@@ -443,16 +446,16 @@ void emit_fwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
         const int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
         const std::string av = aval(i), bv = "b" + aval(i).substr(1);
         if (i == lo) {
-          o << "        float z1 = " << av << " * xd[" << xl << "][c];\n";
-          o << "        float z2 = " << bv << " * x[" << xl << "][c];\n";
-          o << "        float z3 = " << av << " * x[" << xl << "][c];\n";
+          o << "        T z1 = " << av << " * xd[" << xl << "][c];\n";
+          o << "        T z2 = " << bv << " * x[" << xl << "][c];\n";
+          o << "        T z3 = " << av << " * x[" << xl << "][c];\n";
         } else {
-          o << "        z1 = fmaf(" << av << ", xd[" << xl << "][c], z1);\n";
-          o << "        z2 = fmaf(" << bv << ", x[" << xl << "][c], z2);\n";
-          o << "        z3 = fmaf(" << av << ", x[" << xl << "][c], z3);\n";
+          o << "        z1 = e3fma(" << av << ", xd[" << xl << "][c], z1);\n";
+          o << "        z2 = e3fma(" << bv << ", x[" << xl << "][c], z2);\n";
+          o << "        z3 = e3fma(" << av << ", x[" << xl << "][c], z3);\n";
         }
       }
-      o << "        acc[" << orow << "][c] = fmaf(s[" << pl << "][c], z1 + z2, fmaf(sd[" << pl << "][c], z3, acc["
+      o << "        acc[" << orow << "][c] = e3fma(s[" << pl << "][c], z1 + z2, e3fma(sd[" << pl << "][c], z3, acc["
         << orow << "][c]));\n";
       o << "      }\n    }\n";
     }
@@ -464,11 +467,12 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
   o << "  // Per edge and channel, path by path: B[m2] = sum C dm x, ds = y . B, dy += s B\n"
        "  // (summed over this lane's channels), and t, the x cotangent before the sender\n"
        "  // reduction, += s sum_M A dm; the order of each path's sums is its cheapest route.\n";
-  o << "  template <bool PIN, int CPL, class DS>\n";
-  o << "  __device__ __forceinline__ static void edge(const float* __restrict__ A, const float (&Y)[D_SH],\n"
-       "      const float (&x)[NXR][CPL], const float (&s)[NPATH][CPL], const float (&dm)[NROW][CPL],\n"
-       "      float (&t)[NXR][CPL], float (&dy)[D_SH], DS& st_ds) {\n";
-  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  o << "  template <bool PIN, int CPL, class DS, class T>\n";
+  o << "  __device__ __forceinline__ static void edge(const T* __restrict__ A, const T (&Y)[D_SH],\n"
+       "      const T (&x)[NXR][CPL], const T (&s)[NPATH][CPL], const T (&dm)[NROW][CPL],\n"
+       "      T (&t)[NXR][CPL], T (&dy)[D_SH], DS& st_ds) {\n";
+  o << "    using T4 = typename Vec4<T>::type;\n";
+  o << "    const T4* __restrict__ A4 = reinterpret_cast<const T4*>(A);\n";
   o << "    (void)A4;\n";
   std::vector<bool> loaded(g.na_pad / 4, false);
   int ei = 0, orow0 = 0;
@@ -497,28 +501,28 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
       // identity coupling between the output block and the harmonic (X0) or x (Y0) block
       const std::vector<int> map = unit_map(pi, route == kRouteY0);
       o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << "), route " << rname[route] << "\n";
-      o << "      float dsv[CPL];\n";
+      o << "      T dsv[CPL];\n";
       o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
       if (route == kRouteX0) {
         auto Yr = [&](int b) { return "Y[" + std::to_string(p.y_off + b) + "]"; };
         std::string tt = Yr(map[0]) + " * " + DM(0);
-        for (int M = 1; M < d3; ++M) tt = "fmaf(" + Yr(map[M]) + ", " + DM(M) + ", " + tt + ")";
-        o << "        const float T = " << tt << ";\n";
-        o << "        " << Tt(0) << " = fmaf(" << S << ", T, " << Tt(0) << ");\n";
-        o << "        dsv[c] = " << X(0) << " * T;\n";
-        o << "        const float sx = " << S << " * " << X(0) << ";\n";
+        for (int M = 1; M < d3; ++M) tt = "e3fma(" + Yr(map[M]) + ", " + DM(M) + ", " + tt + ")";
+        o << "        const T Tv = " << tt << ";\n";
+        o << "        " << Tt(0) << " = e3fma(" << S << ", Tv, " << Tt(0) << ");\n";
+        o << "        dsv[c] = " << X(0) << " * Tv;\n";
+        o << "        const T sx = " << S << " * " << X(0) << ";\n";
         for (int M = 0; M < d3; ++M)
-          o << "        dy[" << p.y_off + map[M] << "] = fmaf(sx, " << DM(M) << ", dy[" << p.y_off + map[M] << "]);\n";
+          o << "        dy[" << p.y_off + map[M] << "] = e3fma(sx, " << DM(M) << ", dy[" << p.y_off + map[M] << "]);\n";
       } else {
         std::string bb = DM(0) + " * " + X(map[0]);
-        for (int M = 1; M < d3; ++M) bb = "fmaf(" + DM(M) + ", " + X(map[M]) + ", " + bb + ")";
+        for (int M = 1; M < d3; ++M) bb = "e3fma(" + DM(M) + ", " + X(map[M]) + ", " + bb + ")";
         const std::string y0 = "Y[" + std::to_string(p.y_off) + "]";
-        o << "        const float B = " << bb << ";\n";
+        o << "        const T B = " << bb << ";\n";
         o << "        dsv[c] = " << y0 << " * B;\n";
-        o << "        dy[" << p.y_off << "] = fmaf(" << S << ", B, dy[" << p.y_off << "]);\n";
-        o << "        const float sy = " << S << " * " << y0 << ";\n";
+        o << "        dy[" << p.y_off << "] = e3fma(" << S << ", B, dy[" << p.y_off << "]);\n";
+        o << "        const T sy = " << S << " * " << y0 << ";\n";
         for (int M = 0; M < d3; ++M)
-          o << "        " << Tt(map[M]) << " = fmaf(sy, " << DM(M) << ", " << Tt(map[M]) << ");\n";
+          o << "        " << Tt(map[M]) << " = e3fma(sy, " << DM(M) << ", " << Tt(map[M]) << ");\n";
       }
       o << "      }\n";
       o << "      st_ds(" << pl << ", dsv);\n";
@@ -527,19 +531,19 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
       continue;
     }
     o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << "), route " << rname[route] << "\n";
-    o << "      float dsv[CPL];\n";
+    o << "      T dsv[CPL];\n";
     o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
     std::vector<bool> binit(d2, false);
     std::string decl;
     for (int b = 0; b < d2; ++b) decl += (b ? ", b" : "b") + std::to_string(b);
-    o << "        float " << decl << ";\n";
+    o << "        T " << decl << ";\n";
     auto acc_b = [&](int b, const std::string& term_a, const std::string& term_b) {
       // b_b += term_a * term_b
       if (!binit[b]) {
         o << "          b" << b << " = " << term_a << " * " << term_b << ";\n";
         binit[b] = true;
       } else {
-        o << "          b" << b << " = fmaf(" << term_a << ", " << term_b << ", b" << b << ");\n";
+        o << "          b" << b << " = e3fma(" << term_a << ", " << term_b << ", b" << b << ");\n";
       }
     };
     if (uses_A) {
@@ -547,9 +551,9 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
       if (d3 <= d1) {
         std::set<int> Ms;
         for (int i = lo; i < ei; ++i) Ms.insert(g.entries[i].M);
-        for (int M : Ms) o << "        const float w" << M << " = " << S << " * " << DM(M) << ";\n";
+        for (int M : Ms) o << "        const T w" << M << " = " << S << " * " << DM(M) << ";\n";
         for (int i = lo; i < ei; ++i)
-          o << "        " << Tt(g.entries[i].m1) << " = fmaf(" << aval(i) << ", w" << g.entries[i].M << ", "
+          o << "        " << Tt(g.entries[i].m1) << " = e3fma(" << aval(i) << ", w" << g.entries[i].M << ", "
             << Tt(g.entries[i].m1) << ");\n";
       } else {
         for (int m1 = 0; m1 < d1; ++m1) {
@@ -557,19 +561,19 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
           for (int i = lo; i < ei; ++i) {
             if (g.entries[i].m1 != m1) continue;
             if (first)
-              o << "        {\n          float u = " << aval(i) << " * " << DM(g.entries[i].M) << ";\n";
+              o << "        {\n          T u = " << aval(i) << " * " << DM(g.entries[i].M) << ";\n";
             else
-              o << "          u = fmaf(" << aval(i) << ", " << DM(g.entries[i].M) << ", u);\n";
+              o << "          u = e3fma(" << aval(i) << ", " << DM(g.entries[i].M) << ", u);\n";
             first = false;
           }
-          if (!first) o << "          " << Tt(m1) << " = fmaf(" << S << ", u, " << Tt(m1) << ");\n        }\n";
+          if (!first) o << "          " << Tt(m1) << " = e3fma(" << S << ", u, " << Tt(m1) << ");\n        }\n";
         }
       }
     }
     if (route == kRouteA) {
       for (int i = lo; i < ei; ++i) {
         const Entry& en = g.entries[i];
-        o << "        {\n          const float pr = " << DM(en.M) << " * " << X(en.m1) << ";\n";
+        o << "        {\n          const T pr = " << DM(en.M) << " * " << X(en.m1) << ";\n";
         for (const Rec& r : en.recs) acc_b(r.m2 - p.y_off, flit(r.c), "pr");
         o << "        }\n";
       }
@@ -581,9 +585,9 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
           if (en.M == M)
             for (const Rec& r : en.recs) u[r.m2 - p.y_off].push_back({en.m1, r.c});
         for (const auto& [b, lst] : u) {
-          o << "        {\n          float u = " << flit(lst[0].second) << " * " << X(lst[0].first) << ";\n";
+          o << "        {\n          T u = " << flit(lst[0].second) << " * " << X(lst[0].first) << ";\n";
           for (size_t j = 1; j < lst.size(); ++j)
-            o << "          u = fmaf(" << flit(lst[j].second) << ", " << X(lst[j].first) << ", u);\n";
+            o << "          u = e3fma(" << flit(lst[j].second) << ", " << X(lst[j].first) << ", u);\n";
           acc_b(b, DM(M), "u");
           o << "        }\n";
         }
@@ -600,15 +604,15 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
         std::string ty;
         for (const auto& [b, lst] : v) {
           const std::string vn = "v" + std::to_string(b);
-          o << "          float " << vn << " = " << flit(lst[0].second) << " * " << DM(lst[0].first) << ";\n";
+          o << "          T " << vn << " = " << flit(lst[0].second) << " * " << DM(lst[0].first) << ";\n";
           for (size_t j = 1; j < lst.size(); ++j)
-            o << "          " << vn << " = fmaf(" << flit(lst[j].second) << ", " << DM(lst[j].first) << ", " << vn
+            o << "          " << vn << " = e3fma(" << flit(lst[j].second) << ", " << DM(lst[j].first) << ", " << vn
               << ");\n";
           acc_b(b, X(m1), vn);
           const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]";
-          ty = ty.empty() ? yb + " * " + vn : "fmaf(" + yb + ", " + vn + ", " + ty + ")";
+          ty = ty.empty() ? yb + " * " + vn : "e3fma(" + yb + ", " + vn + ", " + ty + ")";
         }
-        o << "          " << Tt(m1) << " = fmaf(" << S << ", " << ty << ", " << Tt(m1) << ");\n";
+        o << "          " << Tt(m1) << " = e3fma(" << S << ", " << ty << ", " << Tt(m1) << ");\n";
         o << "        }\n";
       }
     }
@@ -616,12 +620,12 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
     for (int b = 0; b < d2; ++b) {
       if (!binit[b]) continue;
       std::string yb = "Y[" + std::to_string(p.y_off + b) + "]";
-      ds = ds.empty() ? yb + " * b" + std::to_string(b) : "fmaf(" + yb + ", b" + std::to_string(b) + ", " + ds + ")";
+      ds = ds.empty() ? yb + " * b" + std::to_string(b) : "e3fma(" + yb + ", b" + std::to_string(b) + ", " + ds + ")";
     }
-    o << "        dsv[c] = " << (ds.empty() ? std::string("0.0f") : ds) << ";\n";
+    o << "        dsv[c] = " << (ds.empty() ? std::string("T(0)") : ds) << ";\n";
     for (int b = 0; b < d2; ++b) {
       if (!binit[b]) continue;
-      o << "        dy[" << p.y_off + b << "] = fmaf(" << S << ", b" << b << ", dy[" << p.y_off + b << "]);\n";
+      o << "        dy[" << p.y_off + b << "] = e3fma(" << S << ", b" << b << ", dy[" << p.y_off + b << "]);\n";
     }
     for (int b = 0; b < d2; ++b)
       if (!binit[b]) o << "        (void)b" << b << ";\n";
@@ -641,11 +645,11 @@ void emit_bwd_group(std::ostream& o, const Layout& lay, const std::vector<PathIn
 // i.e. ds of (xd, y, s) plus ds of (x, y2, s), dy of (xd, y, s) plus dy of
 // (x, y, sd), and the x cotangents of (x, y2, s) and (x, y, sd).
 void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Group& g) {
-  o << "  template <int CPL, class DS>\n";
-  o << "  __device__ __forceinline__ static void edge3(const float (&Y)[D_SH], const float (&Y2)[D_SH],\n"
-       "      const float (&x)[NXR][CPL], const float (&xd)[NXR][CPL], const float (&s)[NPATH][CPL],\n"
-       "      const float (&sd)[NPATH][CPL], const float (&dm)[NROW][CPL], float (&t)[NXR][CPL],\n"
-       "      float (&dy)[D_SH], DS& st_ds) {\n";
+  o << "  template <int CPL, class DS, class T>\n";
+  o << "  __device__ __forceinline__ static void edge3(const T (&Y)[D_SH], const T (&Y2)[D_SH],\n"
+       "      const T (&x)[NXR][CPL], const T (&xd)[NXR][CPL], const T (&s)[NPATH][CPL],\n"
+       "      const T (&sd)[NPATH][CPL], const T (&dm)[NROW][CPL], T (&t)[NXR][CPL],\n"
+       "      T (&dy)[D_SH], DS& st_ds) {\n";
   int orow0 = 0;
   for (size_t pl = 0; pl < g.paths.size(); ++pl) {
     const PathInfo& pi = pis[g.paths[pl]];
@@ -655,11 +659,11 @@ void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
     auto DM = [&](int M) { return "dm[" + std::to_string(orow0 + M) + "][c]"; };
     auto xi = [&](int m1) { return std::to_string(index_of(g.xrows, p.x_off + m1)); };
     o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << ")\n";
-    o << "      float gsv[CPL];\n";
+    o << "      T gsv[CPL];\n";
     o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
     std::string decl;
     for (int b = 0; b < d2; ++b) decl += (b ? ", p" : "p") + std::to_string(b) + ", q" + std::to_string(b);
-    o << "        float " << decl << ";\n";
+    o << "        T " << decl << ";\n";
     std::vector<bool> binit(d2, false);
     for (int m1 = 0; m1 < d1; ++m1) {
       std::map<int, std::vector<std::pair<int, double>>> v;  // m2 -> (M, c)
@@ -671,23 +675,23 @@ void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
       std::string t1, t2;
       for (const auto& [b, lst] : v) {
         const std::string vn = "v" + std::to_string(b), bs = std::to_string(b);
-        o << "          float " << vn << " = " << flit(lst[0].second) << " * " << DM(lst[0].first) << ";\n";
+        o << "          T " << vn << " = " << flit(lst[0].second) << " * " << DM(lst[0].first) << ";\n";
         for (size_t j = 1; j < lst.size(); ++j)
-          o << "          " << vn << " = fmaf(" << flit(lst[j].second) << ", " << DM(lst[j].first) << ", " << vn
+          o << "          " << vn << " = e3fma(" << flit(lst[j].second) << ", " << DM(lst[j].first) << ", " << vn
             << ");\n";
         if (!binit[b]) {
           o << "          p" << bs << " = xd[" << xi(m1) << "][c] * " << vn << ";\n";
           o << "          q" << bs << " = x[" << xi(m1) << "][c] * " << vn << ";\n";
           binit[b] = true;
         } else {
-          o << "          p" << bs << " = fmaf(xd[" << xi(m1) << "][c], " << vn << ", p" << bs << ");\n";
-          o << "          q" << bs << " = fmaf(x[" << xi(m1) << "][c], " << vn << ", q" << bs << ");\n";
+          o << "          p" << bs << " = e3fma(xd[" << xi(m1) << "][c], " << vn << ", p" << bs << ");\n";
+          o << "          q" << bs << " = e3fma(x[" << xi(m1) << "][c], " << vn << ", q" << bs << ");\n";
         }
         const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]", y2b = "Y2[" + std::to_string(p.y_off + b) + "]";
-        t1 = t1.empty() ? yb + " * " + vn : "fmaf(" + yb + ", " + vn + ", " + t1 + ")";
-        t2 = t2.empty() ? y2b + " * " + vn : "fmaf(" + y2b + ", " + vn + ", " + t2 + ")";
+        t1 = t1.empty() ? yb + " * " + vn : "e3fma(" + yb + ", " + vn + ", " + t1 + ")";
+        t2 = t2.empty() ? y2b + " * " + vn : "e3fma(" + y2b + ", " + vn + ", " + t2 + ")";
       }
-      o << "          t[" << xi(m1) << "][c] = fmaf(" << S << ", " << t2 << ", fmaf(" << SD << ", " << t1 << ", t["
+      o << "          t[" << xi(m1) << "][c] = e3fma(" << S << ", " << t2 << ", e3fma(" << SD << ", " << t1 << ", t["
         << xi(m1) << "][c]));\n";
       o << "        }\n";
     }
@@ -696,14 +700,14 @@ void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
       if (!binit[b]) continue;
       const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]", y2b = "Y2[" + std::to_string(p.y_off + b) + "]";
       const std::string bs = std::to_string(b);
-      gs = gs.empty() ? "fmaf(" + y2b + ", q" + bs + ", " + yb + " * p" + bs + ")"
-                      : "fmaf(" + y2b + ", q" + bs + ", fmaf(" + yb + ", p" + bs + ", " + gs + "))";
+      gs = gs.empty() ? "e3fma(" + y2b + ", q" + bs + ", " + yb + " * p" + bs + ")"
+                      : "e3fma(" + y2b + ", q" + bs + ", e3fma(" + yb + ", p" + bs + ", " + gs + "))";
     }
-    o << "        gsv[c] = " << (gs.empty() ? std::string("0.0f") : gs) << ";\n";
+    o << "        gsv[c] = " << (gs.empty() ? std::string("T(0)") : gs) << ";\n";
     for (int b = 0; b < d2; ++b) {
       if (!binit[b]) continue;
       const std::string bs = std::to_string(b), dyi = "dy[" + std::to_string(p.y_off + b) + "]";
-      o << "        " << dyi << " = fmaf(" << S << ", p" << bs << ", fmaf(" << SD << ", q" << bs << ", " << dyi << "));\n";
+      o << "        " << dyi << " = e3fma(" << S << ", p" << bs << ", e3fma(" << SD << ", q" << bs << ", " << dyi << "));\n";
     }
     for (int b = 0; b < d2; ++b)
       if (!binit[b]) o << "        (void)p" << b << "; (void)q" << b << ";\n";
@@ -717,10 +721,11 @@ void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
 
 void emit_tp_group(std::ostream& o, const Layout& lay, const std::vector<PathInfo>& pis, const Group& g) {
   o << "  // Weighted tensor product rows: z[i0] = w[i3(i0)] * sum A x; each row handed to st.\n";
-  o << "  template <int CPL, class ST>\n";
-  o << "  __device__ __forceinline__ static void rows(const float* __restrict__ A, const float (&x)[NXR][CPL],\n"
-       "      const float (&w)[NPATH][CPL], ST& st) {\n";
-  o << "    const float4* __restrict__ A4 = reinterpret_cast<const float4*>(A);\n";
+  o << "  template <int CPL, class ST, class T>\n";
+  o << "  __device__ __forceinline__ static void rows(const T* __restrict__ A, const T (&x)[NXR][CPL],\n"
+       "      const T (&w)[NPATH][CPL], ST& st) {\n";
+  o << "    using T4 = typename Vec4<T>::type;\n";
+  o << "    const T4* __restrict__ A4 = reinterpret_cast<const T4*>(A);\n";
   std::vector<bool> loaded(g.na_pad / 4, false);
   int ei = 0;
   for (size_t pl = 0; pl < g.paths.size(); ++pl) {
@@ -731,17 +736,17 @@ void emit_tp_group(std::ostream& o, const Layout& lay, const std::vector<PathInf
       while (ei < (int)g.entries.size() && g.entries[ei].k == pi.p.k && g.entries[ei].M == M) ++ei;
       if (ei > lo) emit_A_loads(o, lo, ei, loaded, "    ");
       o << "    {  // path " << pi.p.k << " row " << M << "\n";
-      o << "      float v[CPL];\n";
+      o << "      T v[CPL];\n";
       o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
       if (ei == lo) {
-        o << "        v[c] = 0.0f;\n";
+        o << "        v[c] = T(0);\n";
       } else {
         for (int i = lo; i < ei; ++i) {
           int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
           if (i == lo)
-            o << "        float z = " << aval(i) << " * x[" << xl << "][c];\n";
+            o << "        T z = " << aval(i) << " * x[" << xl << "][c];\n";
           else
-            o << "        z = fmaf(" << aval(i) << ", x[" << xl << "][c], z);\n";
+            o << "        z = e3fma(" << aval(i) << ", x[" << xl << "][c], z);\n";
         }
         o << "        v[c] = w[" << pl << "][c] * z;\n";
       }
@@ -827,6 +832,12 @@ int main(int argc, char** argv) {
   std::ostringstream o;
   o << "// GENERATED by gen.cpp from the host table builder -- do not edit.\n";
   o << "#pragma once\n\nnamespace e3gen {\n\n";
+  // the code below is generic in the scalar type T (float or double)
+  o << "template <class T> struct Vec4;\n"
+       "template <> struct Vec4<float> { using type = float4; };\n"
+       "template <> struct Vec4<double> { using type = double4; };\n"
+       "__device__ __forceinline__ float e3fma(float a, float b, float c) { return fmaf(a, b, c); }\n"
+       "__device__ __forceinline__ double e3fma(double a, double b, double c) { return fma(a, b, c); }\n\n";
   for (int l = 0; l <= 3; ++l) emit_sh(o, l);
 
   std::vector<std::string> tags;
@@ -913,9 +924,9 @@ int main(int argc, char** argv) {
     o << "  static constexpr const char* SIG = \"" << path_signature(lay) << "\";\n";
     o << "  static constexpr int NFG = " << fg.size() << ", NBG = " << bg.size() << ";\n";
     o << "  static constexpr int MAX_NA_F = " << maxf << ", MAX_NA_B = " << maxb << ", NA_TP = " << tpg.na_pad << ";\n";
-    o << "  __device__ __forceinline__ static void sh(float x, float y, float z, float* Y) { sh_l" << v.lmax_sh
+    o << "  template <class T>\n  __device__ __forceinline__ static void sh(T x, T y, T z, T* Y) { sh_l" << v.lmax_sh
       << "(x, y, z, Y); }\n";
-    o << "  __device__ __forceinline__ static void sh_grad(float x, float y, float z, const float* dY, float& gx, float& gy, float& gz) { sh_grad_l"
+    o << "  template <class T>\n  __device__ __forceinline__ static void sh_grad(T x, T y, T z, const T* dY, T& gx, T& gy, T& gz) { sh_grad_l"
       << v.lmax_sh << "(x, y, z, dY, gx, gy, gz); }\n";
     o << "  template <int G> struct FG;\n  template <int G> struct BG;\n  struct TP;\n};\n\n";
     for (size_t gi = 0; gi < fg.size(); ++gi) {

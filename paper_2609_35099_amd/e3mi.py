@@ -81,6 +81,12 @@ SIGNATURES = {
     "e3_conv_fwd": (_I, [_P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_conv_bwd_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "e3_tp_fwd_f64": (_I, [_P, _P, _P, _P, _P, _I64, _P]),
+    "e3_tp_workspace_size_f64": (_I, [_P, _I64, ct.POINTER(ct.c_size_t)]),
+    "e3_tp_bwd_f64": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _I64, _P]),
+    "e3_conv_workspace_size_f64": (_I, [_P, _P, ct.POINTER(ct.c_size_t)]),
+    "e3_conv_fwd_f64": (_I, [_P, _P, _P, _P, _P, _P, _P]),
+    "e3_conv_bwd_f64": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ct.c_size_t, _P]),
     "e3_probe_stream": (_I, [_P, ct.c_size_t, _P, ct.c_size_t, _I, _I, _I, _U, ct.POINTER(ct.c_size_t),
                              ct.POINTER(ct.c_size_t), _P]),
     "e3_timing_enable": (_I, [_I]),
@@ -353,6 +359,66 @@ def conv_bwd(plan: Plan, graph: Graph, x, vec, s, dm, dx=None, dvec=None, ds=Non
                              _ptr(dm, "dm", (N, plan.D_out, plan.C)), _ptr(dx, "dx", (N, plan.D_in, plan.C)),
                              _ptr(dvec, "dvec", (E, 3)), _ptr(ds, "ds", (E, plan.P, plan.C)),
                              ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd")
+    return dx, dvec, ds
+
+
+# ---------------------------------------------------------------- float64 builds
+def _empty64(shape):
+    torch = _torch()
+    return torch.empty(shape, dtype=torch.float64, device="cuda")
+
+
+@_on_stream
+def tp_fwd_f64(plan: Plan, x, y, w, out=None, stream=None):
+    R = x.shape[0]
+    out = _empty64((R, plan.D_out, plan.C)) if out is None else out
+    f = "float64"
+    _check(lib().e3_tp_fwd_f64(plan.handle, _ptr(x, "x", (R, plan.D_in, plan.C), f), _ptr(y, "y", (R, plan.D_sh), f),
+                               _ptr(w, "w", (R, plan.P, plan.C), f), _ptr(out, "z", (R, plan.D_out, plan.C), f), R,
+                               _stream(stream)), "e3_tp_fwd_f64")
+    return out
+
+
+@_on_stream
+def tp_bwd_f64(plan: Plan, x, y, w, dz, stream=None):
+    R = x.shape[0]
+    f = "float64"
+    dx, dy, dw = _empty64((R, plan.D_in, plan.C)), _empty64((R, plan.D_sh)), _empty64((R, plan.P, plan.C))
+    b = ct.c_size_t()
+    _check(lib().e3_tp_workspace_size_f64(plan.handle, R, ct.byref(b)), "e3_tp_workspace_size_f64")
+    ws = workspace(b.value)
+    _check(lib().e3_tp_bwd_f64(plan.handle, _ptr(x, "x", (R, plan.D_in, plan.C), f), _ptr(y, "y", (R, plan.D_sh), f),
+                               _ptr(w, "w", (R, plan.P, plan.C), f), _ptr(dz, "dz", (R, plan.D_out, plan.C), f),
+                               _ptr(dx, "dx", (R, plan.D_in, plan.C), f), _ptr(dy, "dy", (R, plan.D_sh), f),
+                               _ptr(dw, "dw", (R, plan.P, plan.C), f), ct.c_void_p(ws.data_ptr()), ws.numel(), R,
+                               _stream(stream)), "e3_tp_bwd_f64")
+    return dx, dy, dw
+
+
+@_on_stream
+def conv_fwd_f64(plan: Plan, graph: Graph, x, vec, s, out=None, stream=None):
+    N, E = graph.n_nodes, graph.n_edges
+    f = "float64"
+    out = _empty64((N, plan.D_out, plan.C)) if out is None else out
+    _check(lib().e3_conv_fwd_f64(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C), f),
+                                 _ptr(vec, "vec", (E, 3), f), _ptr(s, "s", (E, plan.P, plan.C), f),
+                                 _ptr(out, "m", (N, plan.D_out, plan.C), f), _stream(stream)), "e3_conv_fwd_f64")
+    return out
+
+
+@_on_stream
+def conv_bwd_f64(plan: Plan, graph: Graph, x, vec, s, dm, stream=None):
+    N, E = graph.n_nodes, graph.n_edges
+    f = "float64"
+    dx, dvec, ds = _empty64((N, plan.D_in, plan.C)), _empty64((E, 3)), _empty64((E, plan.P, plan.C))
+    b = ct.c_size_t()
+    _check(lib().e3_conv_workspace_size_f64(plan.handle, graph.handle, ct.byref(b)), "e3_conv_workspace_size_f64")
+    ws = workspace(b.value)
+    _check(lib().e3_conv_bwd_f64(plan.handle, graph.handle, _ptr(x, "x", (N, plan.D_in, plan.C), f),
+                                 _ptr(vec, "vec", (E, 3), f), _ptr(s, "s", (E, plan.P, plan.C), f),
+                                 _ptr(dm, "dm", (N, plan.D_out, plan.C), f), _ptr(dx, "dx", (N, plan.D_in, plan.C), f),
+                                 _ptr(dvec, "dvec", (E, 3), f), _ptr(ds, "ds", (E, plan.P, plan.C), f),
+                                 ct.c_void_p(ws.data_ptr()), ws.numel(), _stream(stream)), "e3_conv_bwd_f64")
     return dx, dvec, ds
 
 

@@ -2,7 +2,7 @@
 the multiply-adds that the generated sweep code performs per edge and channel.
 
 The table generator is built and run here (g++, no GPU); the operations of
-each group's per-edge contraction are counted in its output (every fmaf and
+each group's per-edge contraction are counted in its output (every fused multiply-add and
 every plain product) and compared with bench.fma_counts, which derives the
 same figures from the plan's coupling records."""
 import os
@@ -49,7 +49,7 @@ def _edge_ops(text, tag, kind):
         body = body[body.index("static void edge("):]
         nxt = body.find("__device__", 1)  # the next member function (edge3) is not counted
         body = body if nxt < 0 else body[:nxt]
-        total += body.count("fmaf(") + body.count(" * ")
+        total += body.count("e3fma(") + body.count(" * ")
         g += 1
     assert g > 0, (tag, kind)
     return total

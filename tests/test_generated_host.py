@@ -50,6 +50,7 @@ DRIVER = r"""
 #define __forceinline__ inline
 #define __restrict__
 struct alignas(16) float4 { float x, y, z, w; };
+struct alignas(32) double4 { double x, y, z, w; };
 #define E3_FWD_PIN() ((void)0)
 #define __builtin_amdgcn_sched_barrier(x) ((void)0)
 #include "variants.inc"

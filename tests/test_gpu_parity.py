@@ -1023,6 +1023,100 @@ def test_first_linear_and_record_calls_in_captured_graph(e3):
     R.close()
 
 
+
+# ---------------------------------------------------------------- float64 builds
+# Bar for the float64 kernels, derived from the arithmetic: one float64 rounding
+# per term (about 1.1e-16) grown by the square root of the terms summed (a few
+# hundred per output here, so about 3e-15) and by the cancellation a random-sign
+# sum can add; 1e-12 leaves ample margin.
+TOL64 = 1e-12
+
+
+@pytest.mark.parametrize("case", ["cube64", "random_l3_pad", "natural_l3", "reordered_l3"])
+def test_conv_float64(e3, case):
+    """The float64 build of the convolution (forward, dx, ds, dvec) against the
+    fp64 oracle on the same float64 inputs, and the float32 build's error
+    measured against it, as the paper compares its kernels' precisions."""
+    import torch
+    _say("conv float64", case)
+    rng = np.random.default_rng(21)
+    if case == "cube64":
+        cfg = synth.CONFIGS["cube64"]
+        g = synth.graph(cfg)
+        snd, rcv, n, vec = g.sender, g.receiver, g.n_nodes, g.vec.astype(np.float64)
+        irreps, lsh, lout, parity, pad = cfg.irreps, cfg.lmax_sh, cfg.lmax_out, "all", -1
+    else:
+        irreps = {"random_l3_pad": "64x0e+64x1o+64x2e+64x3o", "natural_l3": "32x0e+32x1o+32x2e+32x3o",
+                  "reordered_l3": "16x1o+16x0e+16x3o+16x2e"}[case]
+        parity = "natural" if case == "natural_l3" else "all"
+        lsh = lout = 3
+        n, e = 70, 1300
+        pad = 5 if case == "random_l3_pad" else -1
+        snd, rcv, vec32 = _random_graph(rng, n, e)
+        vec = rng.standard_normal((e, 3)) * 2.0
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = e3.Plan(irreps, lsh, lout, natural=parity == "natural")
+    E, C = snd.shape[0], lay.channels
+    x = rng.standard_normal((n, lay.d_in, C))
+    s = rng.standard_normal((E, lay.n_paths, C))
+    dm = rng.standard_normal((n, lay.d_out, C))
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    d64 = [torch.from_numpy(a).to("cuda") for a in (x, vec, s, dm)]
+    m = e3.conv_fwd_f64(plan, G, *d64[:3])
+    dx, dvec, ds = e3.conv_bwd_f64(plan, G, *d64)
+    torch.cuda.synchronize()
+    ref_m = oconv.conv_fwd(lay, x, vec, s, snd, rcv, n, pad_node=pad).numpy()
+    ref = oconv.conv_bwd(lay, x, vec, s, dm, snd, rcv, n, pad_node=pad)
+    refs = dict(m=ref_m, dx=ref["dx"].numpy(), ds=ref["ds"].numpy(), dvec=ref["dvec"].numpy())
+    got = dict(m=m, dx=dx, ds=ds, dvec=dvec)
+    errs = {k: rel_l2(to_np(got[k]), refs[k]) for k in refs}
+    print("float64 rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL64, (k, v)
+    # the float32 build on the same inputs rounded to float32, against float64
+    d32 = [t.float() for t in d64]
+    m32 = e3.conv_fwd(plan, G, *d32[:3])
+    dx32, dvec32, ds32 = e3.conv_bwd(plan, G, *d32)
+    e32 = dict(m=rel_l2(to_np(m32), refs["m"]), dx=rel_l2(to_np(dx32), refs["dx"]),
+               ds=rel_l2(to_np(ds32), refs["ds"]), dvec=rel_l2(to_np(dvec32), refs["dvec"]))
+    print("float32 rel-L2 against float64", e32, flush=True)
+    for k, v in e32.items():
+        assert v < TOL, (k, v)
+    again = e3.conv_bwd_f64(plan, G, *d64)
+    for a, b in zip((dx, dvec, ds), again):
+        assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity,rows", [
+    ("128x0e+128x1o+128x2e", 3, 3, "all", 61),     # the 200k-row layout
+    ("8x0e+8x1o", 2, 2, "all", 5),
+    ("96x0e+96x1o+96x2e+96x3o", 3, 3, "natural", 17),
+])
+def test_tp_float64(e3, irreps, lsh, lout, parity, rows):
+    """The float64 build of the weighted tensor product and its backward."""
+    import torch
+    _say("tp float64", irreps, parity, rows)
+    rng = np.random.default_rng(22)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = e3.Plan(irreps, lsh, lout, natural=parity == "natural")
+    C = lay.channels
+    x = rng.standard_normal((rows, lay.d_in, C))
+    g = rng.standard_normal((rows, 3))
+    y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True))
+    w = rng.standard_normal((rows, lay.n_paths, C))
+    dz = rng.standard_normal((rows, lay.d_out, C))
+    dev = [torch.from_numpy(np.ascontiguousarray(a)).to("cuda") for a in (x, y, w, dz)]
+    z = e3.tp_fwd_f64(plan, *dev[:3])
+    dx, dy, dw = e3.tp_bwd_f64(plan, *dev)
+    torch.cuda.synchronize()
+    errs = dict(z=rel_l2(to_np(z), otp.tp(lay, x, y, w).numpy()))
+    for k, a, r in zip(("dx", "dy", "dw"), (dx, dy, dw), otp.tp_bwd(lay, x, y, w, dz)):
+        errs[k] = rel_l2(to_np(a), r.numpy())
+    print("float64 rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL64, (k, v)
+
+
 # ---------------------------------------------------------------- capacity (last: largest)
 def test_conv_stress_water70k_sampled(e3):
     """70,000 H2O (210,000 atoms, ~11M edges), 64 channels: forward + backward at
