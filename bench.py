@@ -152,6 +152,20 @@ def counter_traffic(kernel: str):
     return None
 
 
+def step_counter_bytes(kernels):
+    """Sum of the committed counter bytes of the convolution step's kernels
+    (None if any is missing or stale)."""
+    tot = 0
+    for k in ("conv_fwd", "conv_bwd_edges", "conv_bwd_dx", "conv_bwd_dvec"):
+        if k not in kernels:
+            continue
+        t = counter_traffic(k)
+        if t is None:
+            return None
+        tot += t
+    return tot
+
+
 def tp_bytes(R, C, D_in, D_sh, D_out, P):
     return R * (D_in * C + D_sh + P * C + D_out * C) * 4
 
@@ -723,6 +737,12 @@ def main():
                                  "counter_GBps": None if traffic is None else
                                  round(traffic / (kernels[dom]["ms"] * 1e-3) / 1e9, 1)}},
             "step_alg_GBps": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9, 1),
+            # the step's kernels' committed counter bytes (HBM and fabric reads, all writes),
+            # beside the algorithmic bytes: the difference is the dx partials' round trip and
+            # the sender feature re-gathers
+            "step_counter_bytes": step_counter_bytes(kernels),
+            "step_counter_GBps": None if step_counter_bytes(kernels) is None else
+            round(step_counter_bytes(kernels) / (ms_step * 1e-3) / 1e9, 1),
             "step_alg_frac": round((fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "fwd_alg_bytes": fwd_b, "bwd_alg_bytes": bwd_b,
             "kernels": kernels,
