@@ -1880,7 +1880,7 @@ __device__ __forceinline__ float wave_reduce8(const float (&v)[8], int lane) {
 //   dW[j][col] = sum_e h[e][j] ds[e][col]   (split over fixed chunks of rows),
 //   dh[e][j]   = sum_col ds[e][col] W[j][col] (split over column slabs).
 // One wave per (row chunk, column slab); a slab is kGradF float4s per lane,
-// lane l owning float4 columns (kGradF sl + f) 64 + l.  The dW outer products
+// lane l owning float4 columns (kGradF sl + f) 64 + l (f < kGradF).  The dW outer products
 // run on the matrix cores: h[e][4 kq + i] from lane 4b + i times ds[e][col]
 // gives dW[4 kq + i][col] in accumulator register i of the lane owning col.
 // Both partial sets are added up afterwards in a fixed order, so the result
@@ -1891,7 +1891,15 @@ __device__ __forceinline__ float wave_reduce8(const float (&v)[8], int lane) {
 #ifndef E3_GRAD_DB
 #define E3_GRAD_DB 1
 #endif
-constexpr int kGradF = 1;
+#ifndef E3_GRAD_F
+#define E3_GRAD_F 2
+#endif
+#ifndef E3_GRAD_WAVES
+#define E3_GRAD_WAVES 8192
+#endif
+// float4 columns per lane: E3_GRAD_F for K <= 8; one for K <= 16, whose
+// accumulators would otherwise leave one wave per SIMD
+constexpr int grad_f(int KQ) { return KQ == 2 ? E3_GRAD_F : 1; }
 constexpr int kGradRows = E3_GRAD_ROWS;  // rows whose loads are issued together
 
 template <int KQ>
@@ -1901,6 +1909,7 @@ __global__ __launch_bounds__(kWave) void k_rad_grad(const float* __restrict__ DS
                                                     int nsl4, int rows_per) {
   static_assert(KQ == 2 || KQ == 4, "K <= 8 or K <= 16");
   constexpr int NV = 4 * KQ;
+  constexpr int kGradF = grad_f(KQ);
   const int lane = threadIdx.x;
   const int c = blockIdx.x / nsl4, sl = blockIdx.x % nsl4;
   int col4[kGradF];
@@ -2022,13 +2031,27 @@ __global__ __launch_bounds__(kWave) void k_rad_grad(const float* __restrict__ DS
 }
 
 // dW = sum over row chunks of the partials, in chunk order.
-__global__ __launch_bounds__(256) void k_rad_dw_sum(const float* __restrict__ dWp, float* __restrict__ dW,
-                                                     int64_t n, int nchunk) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+// A block takes 64 consecutive entries; its kDwSplit waves each add every
+// kDwSplit-th chunk (in chunk order) and the first wave adds their sums in
+// wave order, so the order of every addition is fixed.
+constexpr int kDwSplit = 8;
+
+__global__ __launch_bounds__(kWave* kDwSplit) void k_rad_dw_sum(const float* __restrict__ dWp,
+                                                                float* __restrict__ dW, int64_t n, int nchunk) {
+  __shared__ float part[kDwSplit][kWave];
+  const int o = threadIdx.x % kWave, g = threadIdx.x / kWave;
+  const int64_t i = (int64_t)blockIdx.x * kWave + o;
   float s = 0.0f;
-  for (int c = 0; c < nchunk; ++c) s += dWp[(int64_t)c * n + i];
-  dW[i] = s;
+  if (i < n)
+    for (int c = g; c < nchunk; c += kDwSplit) s += dWp[(int64_t)c * n + i];
+  part[g][o] = s;
+  __syncthreads();
+  if (g == 0 && i < n) {
+    float t = part[0][o];
+#pragma unroll
+    for (int k = 1; k < kDwSplit; ++k) t += part[k][o];
+    dW[i] = t;
+  }
 }
 
 // dh[e] = sum over column slabs of the partials (laid out [slab][edge][NV]),
@@ -2342,10 +2365,11 @@ RadWs rad_ws(const e3_plan* p, const e3_graph* g, int K) {
   w.t = b.t_bytes, w.dy = b.dy_bytes;
   const int64_t pc = (int64_t)V::NP * p->lay.C, nl = g->n_live > 0 ? g->n_edges : 0;
   w.pc4 = (int)(pc / 4);
-  w.nsl4 = (w.pc4 + kWave * kGradF - 1) / (kWave * kGradF);
+  const int f = grad_f(K <= 8 ? 2 : 4);
+  w.nsl4 = (w.pc4 + kWave * f - 1) / (kWave * f);
   w.nv = K <= 8 ? 8 : 16;
-  // about 8k waves in the gradient kernel, at least 256 rows each
-  const int64_t want = std::max<int64_t>(1, 8192 / w.nsl4);
+  // about E3_GRAD_WAVES waves in the gradient kernel, at least 256 rows each
+  const int64_t want = std::max<int64_t>(1, E3_GRAD_WAVES / w.nsl4);
   const int64_t nch = std::min<int64_t>(want, std::max<int64_t>(1, (nl + 255) / 256));
   w.rows_per = (int)std::max<int64_t>(1, (nl + nch - 1) / nch);
   w.nchunk = (int)((nl + w.rows_per - 1) / w.rows_per);
@@ -2438,7 +2462,8 @@ e3_status run_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const
   {
     const int64_t n = (int64_t)K * w.pc4 * 4;
     TimedLaunch t_("rad_dw_sum", st);
-    hipLaunchKernelGGL(k_rad_dw_sum, dim3(blocks_for(n, 256)), dim3(256), 0, st, dWp, dW, n, w.nchunk);
+    hipLaunchKernelGGL(k_rad_dw_sum, dim3(blocks_for(n, kWave)), dim3(kWave * kDwSplit), 0, st, dWp, dW, n,
+                       w.nchunk);
     E3_HIP(hipGetLastError());
   }
   if (g->n_pad > 0) {
