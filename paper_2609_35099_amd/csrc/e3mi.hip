@@ -18,7 +18,6 @@
 //   * workgroups are single waves; block ids are mapped so that each XCD
 //     walks a contiguous range of receivers and the groups of one receiver run
 //     back to back on the same XCD (shared L2 for the sender gathers).
-#include <hipcub/hipcub.hpp>
 
 #include "e3mi_impl.h"
 
@@ -542,15 +541,145 @@ __global__ __launch_bounds__(256) void k_tpg_sum(const T* __restrict__ part, T* 
 // ------------------------------------------------------------ graph
 __global__ void k_graph_keys(const int32_t* __restrict__ snd, const int32_t* __restrict__ rcv, int64_t n_edges,
                              int32_t n_nodes, int32_t pad, uint32_t* __restrict__ key_r, uint32_t* __restrict__ key_s,
-                             int32_t* __restrict__ ids, int* __restrict__ bad) {
+                             int* __restrict__ bad) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= n_edges) return;
   const int32_t s = snd[e], r = rcv[e];
-  if (s < 0 || s >= n_nodes || r < 0 || r >= n_nodes) *bad = 1;  // every writer stores the same value
-  const bool is_pad = pad >= 0 && (s == pad || r == pad);
+  const bool out_of_range = s < 0 || s >= n_nodes || r < 0 || r >= n_nodes;
+  if (out_of_range) *bad = 1;  // every writer stores the same value
+  // an out-of-range index becomes the padding key (the build fails anyway),
+  // so that the sort's digits stay below 2^bits
+  const bool is_pad = out_of_range || (pad >= 0 && (s == pad || r == pad));
   key_r[e] = is_pad ? (uint32_t)n_nodes : (uint32_t)r;
   key_s[e] = is_pad ? (uint32_t)n_nodes : (uint32_t)s;
-  ids[e] = (int32_t)e;
+}
+
+// Stable LSD radix sort of (key, edge id) pairs, 8 bits of the key per pass.
+// A tile is kSortRounds rounds of one 256-thread block over consecutive
+// elements.  Per pass: k_sort_hist counts each tile's digits, k_sort_scan turns
+// each digit's tile counts into exclusive offsets and a digit total, and
+// k_sort_scatter places every element at
+//   (elements of smaller digits) + offset[digit][tile]
+//   + (same-digit elements of earlier rounds of its tile)
+//   + (same-digit elements of earlier waves of its round)
+//   + (same-digit elements of lower lanes of its wave),
+// so equal digits keep their input order and every pass is stable.  Integer
+// counts only: the result does not depend on scheduling.
+constexpr int kSortBlock = 256, kSortRounds = 16, kSortTile = kSortBlock * kSortRounds;
+constexpr int kSortWaves = kSortBlock / kWave;
+static_assert(kSortBlock == 256, "one thread per digit");
+
+__global__ __launch_bounds__(kSortBlock) void k_sort_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
+                                                          int64_t n_tiles, int32_t* __restrict__ count) {
+  __shared__ int hist[256];
+  const int tid = threadIdx.x;
+  hist[tid] = 0;
+  __syncthreads();
+  const int64_t t = blockIdx.x;
+  for (int j = 0; j < kSortRounds; ++j) {
+    const int64_t i = t * kSortTile + (int64_t)j * kSortBlock + tid;
+    if (i < n) atomicAdd(&hist[(keys[i] >> shift) & 255u], 1);
+  }
+  __syncthreads();
+  count[(int64_t)tid * n_tiles + t] = hist[tid];
+}
+
+// Inclusive scan of v over the block (Hillis-Steele in LDS); total = the sum
+// over the block.  Ends with a barrier after the last reads of buf.
+__device__ __forceinline__ int32_t block_incl_scan(int32_t v, int32_t (&buf)[2][kSortBlock], int tid,
+                                                   int32_t& total) {
+  buf[0][tid] = v;
+  __syncthreads();
+  int cur = 0;
+  for (int d = 1; d < kSortBlock; d <<= 1) {
+    const int32_t u = buf[cur][tid] + (tid >= d ? buf[cur][tid - d] : 0);
+    buf[cur ^ 1][tid] = u;
+    cur ^= 1;
+    __syncthreads();
+  }
+  const int32_t incl = buf[cur][tid];
+  total = buf[cur][kSortBlock - 1];
+  __syncthreads();
+  return incl;
+}
+
+// Per digit (one block each): exclusive scan of its tiles' counts in place
+// (row d of count) and the digit's total.
+__global__ __launch_bounds__(kSortBlock) void k_sort_scan(int32_t* __restrict__ count, int64_t n_tiles,
+                                                          int32_t* __restrict__ total) {
+  __shared__ int32_t buf[2][kSortBlock];
+  const int tid = threadIdx.x;
+  int32_t* row = count + (int64_t)blockIdx.x * n_tiles;
+  int32_t carry = 0;
+  for (int64_t c0 = 0; c0 < n_tiles; c0 += kSortBlock) {
+    const int64_t i = c0 + tid;
+    const int32_t v = i < n_tiles ? row[i] : 0;
+    int32_t chunk = 0;
+    const int32_t incl = block_incl_scan(v, buf, tid, chunk);
+    if (i < n_tiles) row[i] = carry + incl - v;
+    carry += chunk;
+  }
+  if (tid == 0) total[blockIdx.x] = carry;
+}
+
+// ids_in == nullptr: the ids are the element indices.  Positions outside
+// [0, n) cannot arise from consistent offsets; they are refused (bad = 1)
+// rather than written.
+__global__ __launch_bounds__(kSortBlock) void k_sort_scatter(const uint32_t* __restrict__ keys_in,
+                                                             const int32_t* __restrict__ ids_in, int64_t n, int shift,
+                                                             int64_t n_tiles, const int32_t* __restrict__ off,
+                                                             const int32_t* __restrict__ total,
+                                                             uint32_t* __restrict__ keys_out,
+                                                             int32_t* __restrict__ ids_out, int* __restrict__ bad) {
+  __shared__ int running[256];
+  __shared__ int cnt[kSortWaves][256];
+  __shared__ int32_t buf[2][kSortBlock];
+  const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+  {
+    // running starts at the digit's base: the elements of all smaller digits
+    int32_t all = 0;
+    const int32_t v = total[tid];
+    running[tid] = block_incl_scan(v, buf, tid, all) - v;
+  }
+#pragma unroll
+  for (int k = 0; k < kSortWaves; ++k) cnt[k][tid] = 0;
+  __syncthreads();
+  const int64_t t = blockIdx.x;
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (kWave - lane));
+  for (int j = 0; j < kSortRounds; ++j) {
+    const int64_t i = t * kSortTile + (int64_t)j * kSortBlock + tid;
+    const bool valid = i < n;
+    const uint32_t key = valid ? keys_in[i] : 0u;
+    const int32_t id = valid ? (ids_in ? ids_in[i] : (int32_t)i) : 0;
+    const int d = (int)((key >> shift) & 255u);
+    // lanes of this wave holding the same digit
+    uint64_t same = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t set = __ballot(valid && ((d >> bit) & 1));
+      same &= ((d >> bit) & 1) ? set : ~set;
+    }
+    const int rank = __popcll(same & below);
+    if (valid && (same & below) == 0) cnt[w][d] = __popcll(same);  // the digit's lowest lane
+    __syncthreads();
+    if (valid) {
+      int prefix = 0;
+      for (int k = 0; k < w; ++k) prefix += cnt[k][d];
+      const int64_t pos = (int64_t)off[(int64_t)d * n_tiles + t] + running[d] + prefix + rank;
+      if (pos >= 0 && pos < n) {
+        keys_out[pos] = key;
+        ids_out[pos] = id;
+      } else {
+        *bad = 1;
+      }
+    }
+    __syncthreads();
+    int add = 0;
+#pragma unroll
+    for (int k = 0; k < kSortWaves; ++k) add += cnt[k][tid], cnt[k][tid] = 0;
+    running[tid] += add;
+    __syncthreads();
+  }
 }
 
 // rowptr[b] = first position with key >= b (binary search; keys sorted).
@@ -757,6 +886,33 @@ e3_status e3_sh_host(int lmax, const double* u, double* y, int64_t n) {
   return E3_OK;
 }
 
+namespace {
+// Stable sort of keys[0, n) < 2^nbits with their element indices as ids:
+// ceil(nbits / 8) passes ping-ponging between (tk, ti) and the outputs, so that
+// the last lands in (keys_out, ids_out).  count holds 256 * (tiles + 1) ints
+// (the tile counts, then the digit totals).
+hipError_t sort_pairs(const uint32_t* keys, int64_t n, int nbits, uint32_t* keys_out, int32_t* ids_out,
+                      uint32_t* tk, int32_t* ti, int32_t* count, int* bad, hipStream_t st) {
+  const int64_t tiles = (n + kSortTile - 1) / kSortTile;
+  const int passes = (nbits + 7) / 8;
+  const uint32_t* kin = keys;
+  const int32_t* iin = nullptr;
+  for (int p = 0; p < passes; ++p) {
+    const bool to_out = ((passes - 1 - p) % 2) == 0;
+    uint32_t* kout = to_out ? keys_out : tk;
+    int32_t* iout = to_out ? ids_out : ti;
+    hipLaunchKernelGGL(k_sort_hist, dim3((unsigned)tiles), dim3(kSortBlock), 0, st, kin, n, 8 * p, tiles, count);
+    hipLaunchKernelGGL(k_sort_scan, dim3(256), dim3(kSortBlock), 0, st, count, tiles, count + 256 * tiles);
+    hipLaunchKernelGGL(k_sort_scatter, dim3((unsigned)tiles), dim3(kSortBlock), 0, st, kin, iin, n, 8 * p, tiles,
+                       count, count + 256 * tiles, kout, iout, bad);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    kin = kout, iin = iout;
+  }
+  return hipSuccess;
+}
+}  // namespace
+
 e3_status e3_graph_create(const int32_t* sender, const int32_t* receiver, int64_t n_nodes, int64_t n_edges,
                           int32_t pad_node, e3_stream stream, e3_graph** out) {
   if (!out) return E3_ERR_INVALID_ARG;
@@ -784,46 +940,38 @@ e3_status e3_graph_create(const int32_t* sender, const int32_t* receiver, int64_
       !alloc((void**)&g->eid_r, E * 4) || !alloc((void**)&g->eid_s, E * 4) || !alloc((void**)&g->src_r, E * 4) ||
       !alloc((void**)&g->r2s, E * 4) || !alloc((void**)&g->pos_s, E * 4))
     return fail(E3_ERR_ALLOC);
-  uint32_t *key_r = nullptr, *key_s = nullptr, *key_sorted = nullptr;
-  int32_t* ids = nullptr;
+  uint32_t *key_r = nullptr, *key_s = nullptr, *key_sorted = nullptr, *tk = nullptr;
+  int32_t *ti = nullptr, *count = nullptr;
   int* flag = nullptr;
-  void* tmp = nullptr;
   auto cleanup = [&]() {
-    (void)hipFree(key_r), (void)hipFree(key_s), (void)hipFree(key_sorted), (void)hipFree(ids), (void)hipFree(flag),
-        (void)hipFree(tmp);
+    (void)hipFree(key_r), (void)hipFree(key_s), (void)hipFree(key_sorted), (void)hipFree(tk), (void)hipFree(ti),
+        (void)hipFree(count), (void)hipFree(flag);
   };
+  const int64_t tiles = (E + kSortTile - 1) / kSortTile;
   if (!alloc((void**)&key_r, E * 4) || !alloc((void**)&key_s, E * 4) || !alloc((void**)&key_sorted, E * 4) ||
-      !alloc((void**)&ids, E * 4) || !alloc((void**)&flag, 2 * sizeof(int))) {
+      !alloc((void**)&tk, E * 4) || !alloc((void**)&ti, E * 4) || !alloc((void**)&count, 256 * (tiles + 1) * 4) ||
+      !alloc((void**)&flag, 2 * sizeof(int))) {
     cleanup();
     return fail(E3_ERR_ALLOC);
   }
+  // keys are receivers (senders) in [0, N), padding edges N
   int end_bit = 1;
   while (end_bit < 32 && ((int64_t)1 << end_bit) <= N) ++end_bit;
-  size_t tmp_bytes = 0;
   hipError_t herr = hipSuccess;
   herr = hipMemsetAsync(flag, 0, 2 * sizeof(int), st);
   if (herr == hipSuccess && E > 0) {
     hipLaunchKernelGGL(k_graph_keys, dim3(blocks_for(E, 256)), dim3(256), 0, st, sender, receiver, E, (int32_t)N,
-                       pad_node, key_r, key_s, ids, flag);
+                       pad_node, key_r, key_s, flag);
     herr = hipGetLastError();
     if (herr == hipSuccess)
-      herr = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_bytes, key_r, key_sorted, ids, g->eid_r, (int)E, 0,
-                                                end_bit, st);
-    if (herr == hipSuccess && !alloc(&tmp, tmp_bytes)) {
-      cleanup();
-      return fail(E3_ERR_ALLOC);
-    }
-    if (herr == hipSuccess)
-      herr = hipcub::DeviceRadixSort::SortPairs(tmp, tmp_bytes, key_r, key_sorted, ids, g->eid_r, (int)E, 0, end_bit,
-                                                st);
+      herr = sort_pairs(key_r, E, end_bit, key_sorted, g->eid_r, tk, ti, count, flag + 1, st);
     if (herr == hipSuccess) {
       hipLaunchKernelGGL(k_graph_rowptr, dim3(blocks_for(N + 1, 256)), dim3(256), 0, st, key_sorted, E, (int32_t)N,
                          g->rowptr_r);
       herr = hipGetLastError();
     }
     if (herr == hipSuccess)
-      herr = hipcub::DeviceRadixSort::SortPairs(tmp, tmp_bytes, key_s, key_sorted, ids, g->eid_s, (int)E, 0, end_bit,
-                                                st);
+      herr = sort_pairs(key_s, E, end_bit, key_sorted, g->eid_s, tk, ti, count, flag + 1, st);
     if (herr == hipSuccess) {
       hipLaunchKernelGGL(k_graph_rowptr, dim3(blocks_for(N + 1, 256)), dim3(256), 0, st, key_sorted, E, (int32_t)N,
                          g->rowptr_s);
@@ -833,9 +981,9 @@ e3_status e3_graph_create(const int32_t* sender, const int32_t* receiver, int64_
     herr = hipMemsetAsync(g->rowptr_r, 0, (N + 1) * 4, st);
     if (herr == hipSuccess) herr = hipMemsetAsync(g->rowptr_s, 0, (N + 1) * 4, st);
   }
-  int host[2] = {0, 0};
-  if (herr == hipSuccess) herr = hipMemcpyAsync(&host[0], flag, sizeof(int), hipMemcpyDeviceToHost, st);
-  if (herr == hipSuccess) herr = hipMemcpyAsync(&host[1], g->rowptr_r + N, sizeof(int), hipMemcpyDeviceToHost, st);
+  int host[3] = {0, 0, 0};
+  if (herr == hipSuccess) herr = hipMemcpyAsync(&host[0], flag, 2 * sizeof(int), hipMemcpyDeviceToHost, st);
+  if (herr == hipSuccess) herr = hipMemcpyAsync(&host[2], g->rowptr_r + N, sizeof(int), hipMemcpyDeviceToHost, st);
   if (herr == hipSuccess) herr = hipStreamSynchronize(st);
   if (herr != hipSuccess) {
     g_last_error = std::string("e3_graph_create: ") + hipGetErrorString(herr);
@@ -846,7 +994,12 @@ e3_status e3_graph_create(const int32_t* sender, const int32_t* receiver, int64_
     cleanup();
     return fail(E3_ERR_INDEX_OUT_OF_RANGE);
   }
-  g->n_live = host[1];
+  if (host[1]) {
+    g_last_error = "e3_graph_create: inconsistent sort offsets";
+    cleanup();
+    return fail(E3_ERR_HIP);
+  }
+  g->n_live = host[2];
   g->n_pad = E - g->n_live;
   if (g->n_live > 0) {
     hipLaunchKernelGGL(k_graph_finish, dim3(blocks_for(g->n_live, 256)), dim3(256), 0, st, sender, g->eid_r, g->eid_s,

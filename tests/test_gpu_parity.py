@@ -46,18 +46,38 @@ def _random_graph(rng, n, e, pad=-1):
 
 
 # ---------------------------------------------------------------- graph
-@pytest.mark.parametrize("case", ["cfg1", "random_pad", "empty", "isolated"])
+@pytest.mark.parametrize("case", ["cfg1", "random_pad", "empty", "isolated", "water8k", "three_passes",
+                                  "whole_tiles", "two_nodes"])
 def test_graph_csr_bit_exact(e3, case):
+    """The CSR arrays equal the oracle's stable argsort bit for bit: one radix
+    pass (N < 256), two (the 24,000-atom box) and three (N = 300,000, with
+    padding), edge counts that fill whole sort tiles and one more, the
+    smallest graphs."""
     _say("graph", case)
     rng = np.random.default_rng(1)
     pad = -1
     if case == "cfg1":
         g = synth.graph(synth.CONFIGS["cube64"])
         snd, rcv, n = g.sender, g.receiver, g.n_nodes
+    elif case == "water8k":
+        g = synth.graph(synth.CONFIGS["water8k"])
+        snd, rcv, n = g.sender, g.receiver, g.n_nodes
     elif case == "random_pad":
         n = 300
         snd, rcv, _ = _random_graph(rng, n, 5000)
         pad = 17
+    elif case == "three_passes":
+        n = 300_000
+        snd, rcv, _ = _random_graph(rng, n, 2_000_000)
+        pad = 123_456
+    elif case == "whole_tiles":
+        n = 700
+        snd, rcv, _ = _random_graph(rng, n, 3 * 4096 + 1)
+        snd, rcv = snd[:3 * 4096], rcv[:3 * 4096]
+    elif case == "two_nodes":
+        n = 2
+        snd = np.array([0, 1, 1, 0, 1], np.int32)
+        rcv = np.array([1, 0, 0, 1, 0], np.int32)
     elif case == "empty":
         n = 5
         snd = rcv = np.zeros(0, np.int32)
