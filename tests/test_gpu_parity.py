@@ -47,12 +47,12 @@ def _random_graph(rng, n, e, pad=-1):
 
 # ---------------------------------------------------------------- graph
 @pytest.mark.parametrize("case", ["cfg1", "random_pad", "empty", "isolated", "water8k", "three_passes",
-                                  "whole_tiles", "two_nodes"])
+                                  "four_passes", "whole_tiles", "two_nodes"])
 def test_graph_csr_bit_exact(e3, case):
     """The CSR arrays equal the oracle's stable argsort bit for bit: one radix
-    pass (N < 256), two (the 24,000-atom box) and three (N = 300,000, with
-    padding), edge counts that fill whole sort tiles and one more, the
-    smallest graphs."""
+    pass (N < 256), two (the 24,000-atom box), three (N = 300,000, with
+    padding) and four (N above 2^24, edges on a few hundred nodes, so most keys
+    repeat), edge counts that fill whole sort tiles, the smallest graphs."""
     _say("graph", case)
     rng = np.random.default_rng(1)
     pad = -1
@@ -70,6 +70,11 @@ def test_graph_csr_bit_exact(e3, case):
         n = 300_000
         snd, rcv, _ = _random_graph(rng, n, 2_000_000)
         pad = 123_456
+    elif case == "four_passes":
+        n = (1 << 24) + 5
+        hubs = rng.choice(n, 300, replace=False).astype(np.int32)
+        snd = hubs[rng.integers(0, 300, 50_000)]
+        rcv = hubs[rng.integers(0, 300, 50_000)]
     elif case == "whole_tiles":
         n = 700
         snd, rcv, _ = _random_graph(rng, n, 3 * 4096 + 1)
