@@ -1117,23 +1117,25 @@ __global__ __launch_bounds__(kWave) void k_conv_bwd_dx(const float* __restrict__
   const int64_t slot_bytes = (int64_t)flat4 * 16;
   __amdgpu_buffer_rsrc_t o = __builtin_amdgcn_make_buffer_rsrc(dx + (int64_t)node * flat4 * 4, (short)0,
                                                                (int)slot_bytes, 0x00020000);
+  // float4 k of the lane at byte offset off + k * 64 * 16, all of it in the
+  // lane offset (which the descriptor's range check covers): float4s past
+  // D_in x C read as zero and are not stored
   E3_UNROLL(E3_DX_UNROLL)
   for (int t = s0; t < s1; ++t) {
-    // out-of-range float4s (past D_in x C) read as zero
     __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(T) + (int64_t)t * flat4 * 4, (short)0, (int)slot_bytes, 0x00020000);
 #pragma unroll
     for (int k = 0; k < kDxVec; ++k)
-      acc[k] += __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(r, off, k * kWave * 16, kNT));
+      acc[k] += __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(r, off + k * kWave * 16, 0, kNT));
   }
   if (accum) {  // old + this sum, so that accumulating equals adding a separate result
 #pragma unroll
     for (int k = 0; k < kDxVec; ++k)
-      acc[k] += __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(o, off, k * kWave * 16, 0));
+      acc[k] += __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(o, off + k * kWave * 16, 0, 0));
   }
 #pragma unroll
   for (int k = 0; k < kDxVec; ++k)
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, acc[k]), o, off, k * kWave * 16, kST);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, acc[k]), o, off + k * kWave * 16, 0, kST);
 }
 
 // dvec of each live edge from its harmonic cotangent (summed over groups).
