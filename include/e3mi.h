@@ -39,8 +39,10 @@
  * take a stream are asynchronous on it; the *_fwd / *_bwd / e3_sh* entry
  * points never allocate, never synchronise, and fully overwrite their
  * outputs.  Results are bitwise reproducible for identical inputs on one
- * device and build: every sum runs in a fixed order (receiver-sorted or
- * sender-sorted CSR order and a fixed reduction tree) and no atomics are used.
+ * device and build: every floating-point sum runs in a fixed order
+ * (receiver-sorted or sender-sorted CSR order and a fixed reduction tree) and
+ * no floating-point atomics are used (the graph build counts keys with
+ * integer atomics, whose result does not depend on their order).
  *
  * Errors: every call returns an e3_status; nothing is thrown across the ABI.
  * Arguments are validated before any device work is enqueued.
