@@ -1058,6 +1058,16 @@ __device__ __forceinline__ void bwd3_task(const ConvArgs& a, int b, int sl, floa
       const float tot = wave_reduce16(dy, lane);
       if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
     };
+#ifndef E3_BWD3_SINGLE
+#define E3_BWD3_SINGLE 1
+#endif
+#if E3_BWD3_SINGLE
+    for (int j = 0; j < n; ++j) {
+      load(j, xa, xda, sa, sda);
+      compute(j, xa, xda, sa, sda);
+    }
+    (void)xb, (void)xdb, (void)sb, (void)sdb;
+#else
     load(0, xa, xda, sa, sda);
     for (int j = 0; j < n; j += 2) {
       if (j + 1 < n) load(j + 1, xb, xdb, sb, sdb);
@@ -1067,6 +1077,7 @@ __device__ __forceinline__ void bwd3_task(const ConvArgs& a, int b, int sl, floa
         compute(j + 1, xb, xdb, sb, sdb);
       }
     }
+#endif
     __syncthreads();
   }
 }
@@ -1081,12 +1092,15 @@ __device__ __forceinline__ void bwd3_dispatch(const ConvArgs& a, int b, int g, i
   }
 }
 
-template <class V>
-// One wave per SIMD: at two, the l <= 3 sweep spilled 136 bytes per lane and
-// ran 26.6 ms against 23.4 ms without the spill.
+// Two waves per SIMD with each edge's rows loaded just before its contraction
+// (E3_BWD3_SINGLE): 255 registers, no spill, 17.9 ms at the 24,000-atom box.
+// Loading the next edge's rows during the contraction needs about 30 more
+// registers: at two waves per SIMD it spilled 136 bytes per lane (26.6 ms), at
+// one it ran 23.4 ms.
 #ifndef E3_BWD3_MIN_WAVES
-#define E3_BWD3_MIN_WAVES 1
+#define E3_BWD3_MIN_WAVES 2
 #endif
+template <class V>
 __global__ __launch_bounds__(kWave, E3_BWD3_MIN_WAVES) void k_conv_bwd3(ConvArgs a) {
   __shared__ float smem[2 * kEdgeBatch * V::D_SH];
   int b, g, sl;
