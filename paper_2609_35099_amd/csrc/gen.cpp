@@ -427,38 +427,49 @@ void emit_fwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
   o << "    using T4 = typename Vec4<T>::type;\n";
   o << "    const T4* __restrict__ A4 = reinterpret_cast<const T4*>(A);\n";
   o << "    const T4* __restrict__ B4 = reinterpret_cast<const T4*>(A2);\n";
-  std::vector<bool> loaded(g.na_pad / 4, false);
+  // The path weights are folded into the x rows first: with
+  // u = s xd + sd x and v = s x (per channel, per x row of the path),
+  // acc[M] += sum A[M,m1] u[m1] + sum A2[M,m1] v[m1].  Each path is a block
+  // of its own, which loads the A chunks it reads (a chunk shared by two
+  // paths is read twice).
   int ei = 0, orow = 0;
   for (size_t pl = 0; pl < g.paths.size(); ++pl) {
     const PathInfo& pi = pis[g.paths[pl]];
+    const int d1 = 2 * pi.p.l1 + 1;
+    std::vector<bool> loaded(g.na_pad / 4, false);
+    o << "    {  // path " << pi.p.k << " (" << pi.p.l1 << "," << pi.p.l2 << "," << pi.p.l3 << ")\n";
+    o << "      T u[" << d1 << "][CPL], v[" << d1 << "][CPL];\n";
+    o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+    for (int m1 = 0; m1 < d1; ++m1) {
+      const int xl = index_of(g.xrows, pi.p.x_off + m1);
+      o << "        u[" << m1 << "][c] = e3fma(sd[" << pl << "][c], x[" << xl << "][c], s[" << pl << "][c] * xd[" << xl
+        << "][c]);\n";
+      o << "        v[" << m1 << "][c] = s[" << pl << "][c] * x[" << xl << "][c];\n";
+    }
+    o << "      }\n";
     for (int M = 0; M < 2 * pi.p.l3 + 1; ++M, ++orow) {
       const int lo = ei;
       while (ei < (int)g.entries.size() && g.entries[ei].k == pi.p.k && g.entries[ei].M == M) ++ei;
       if (ei == lo) continue;
       for (int q = lo / 4; q <= (ei - 1) / 4; ++q)
         if (!loaded[q]) {
-          o << "    const T4 a" << q << " = A4[" << q << "], b" << q << " = B4[" << q << "];\n";
+          o << "      const T4 a" << q << " = A4[" << q << "], b" << q << " = B4[" << q << "];\n";
           loaded[q] = true;
         }
-      o << "    {  // path " << pi.p.k << " (" << pi.p.l1 << "," << pi.p.l2 << "," << pi.p.l3 << ") row " << M << "\n";
-      o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
+      o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {  // row " << M << "\n";
+      o << "        T r = acc[" << orow << "][c];\n";
       for (int i = lo; i < ei; ++i) {
-        const int xl = index_of(g.xrows, pi.p.x_off + g.entries[i].m1);
-        const std::string av = aval(i), bv = "b" + aval(i).substr(1);
-        if (i == lo) {
-          o << "        T z1 = " << av << " * xd[" << xl << "][c];\n";
-          o << "        T z2 = " << bv << " * x[" << xl << "][c];\n";
-          o << "        T z3 = " << av << " * x[" << xl << "][c];\n";
-        } else {
-          o << "        z1 = e3fma(" << av << ", xd[" << xl << "][c], z1);\n";
-          o << "        z2 = e3fma(" << bv << ", x[" << xl << "][c], z2);\n";
-          o << "        z3 = e3fma(" << av << ", x[" << xl << "][c], z3);\n";
-        }
+        const int m1 = g.entries[i].m1;
+        o << "        r = e3fma(" << aval(i) << ", u[" << m1 << "][c], r);\n";
       }
-      o << "        acc[" << orow << "][c] = e3fma(s[" << pl << "][c], z1 + z2, e3fma(sd[" << pl << "][c], z3, acc["
-        << orow << "][c]));\n";
-      o << "      }\n    }\n";
+      for (int i = lo; i < ei; ++i) {
+        const int m1 = g.entries[i].m1;
+        o << "        r = e3fma(b" << aval(i).substr(1) << ", v[" << m1 << "][c], r);\n";
+      }
+      o << "        acc[" << orow << "][c] = r;\n";
+      o << "      }\n";
     }
+    o << "    }\n";
   }
   o << "  }\n";
 }
@@ -650,21 +661,22 @@ void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
        "      const T (&x)[NXR][CPL], const T (&xd)[NXR][CPL], const T (&s)[NPATH][CPL],\n"
        "      const T (&sd)[NPATH][CPL], const T (&dm)[NROW][CPL], T (&t)[NXR][CPL],\n"
        "      T (&dy)[D_SH], DS& st_ds) {\n";
+  // Per path and x row m1, with V[m2] = sum_M C dm[M], T1 = y . V and T2 = y2 . V:
+  //   gs += xd[m1] T1 + x[m1] T2          (= y . B1 + y2 . B2 summed over m1),
+  //   dy[m2] += z[m1] V[m2], z = s xd + sd x  (= s B1 + sd B2),
+  //   t[m1] += s T2 + sd T1.
   int orow0 = 0;
   for (size_t pl = 0; pl < g.paths.size(); ++pl) {
     const PathInfo& pi = pis[g.paths[pl]];
     const Path& p = pi.p;
-    const int d1 = 2 * p.l1 + 1, d2 = 2 * p.l2 + 1, d3 = 2 * p.l3 + 1;
+    const int d1 = 2 * p.l1 + 1, d3 = 2 * p.l3 + 1;
     const std::string S = "s[" + std::to_string(pl) + "][c]", SD = "sd[" + std::to_string(pl) + "][c]";
     auto DM = [&](int M) { return "dm[" + std::to_string(orow0 + M) + "][c]"; };
     auto xi = [&](int m1) { return std::to_string(index_of(g.xrows, p.x_off + m1)); };
     o << "    {  // path " << p.k << " (" << p.l1 << "," << p.l2 << "," << p.l3 << ")\n";
     o << "      T gsv[CPL];\n";
     o << "#pragma unroll\n      for (int c = 0; c < CPL; ++c) {\n";
-    std::string decl;
-    for (int b = 0; b < d2; ++b) decl += (b ? ", p" : "p") + std::to_string(b) + ", q" + std::to_string(b);
-    o << "        T " << decl << ";\n";
-    std::vector<bool> binit(d2, false);
+    o << "        T gs = T(0);\n";
     for (int m1 = 0; m1 < d1; ++m1) {
       std::map<int, std::vector<std::pair<int, double>>> v;  // m2 -> (M, c)
       for (const Entry& en : pi.entries)
@@ -672,45 +684,26 @@ void emit_bwd3_group(std::ostream& o, const std::vector<PathInfo>& pis, const Gr
           for (const Rec& r : en.recs) v[r.m2 - p.y_off].push_back({en.M, r.c});
       if (v.empty()) continue;
       o << "        {\n";
+      o << "          const T z = e3fma(" << SD << ", x[" << xi(m1) << "][c], " << S << " * xd[" << xi(m1) << "][c]);\n";
       std::string t1, t2;
       for (const auto& [b, lst] : v) {
-        const std::string vn = "v" + std::to_string(b), bs = std::to_string(b);
+        const std::string vn = "v" + std::to_string(b);
         o << "          T " << vn << " = " << flit(lst[0].second) << " * " << DM(lst[0].first) << ";\n";
         for (size_t j = 1; j < lst.size(); ++j)
           o << "          " << vn << " = e3fma(" << flit(lst[j].second) << ", " << DM(lst[j].first) << ", " << vn
             << ");\n";
-        if (!binit[b]) {
-          o << "          p" << bs << " = xd[" << xi(m1) << "][c] * " << vn << ";\n";
-          o << "          q" << bs << " = x[" << xi(m1) << "][c] * " << vn << ";\n";
-          binit[b] = true;
-        } else {
-          o << "          p" << bs << " = e3fma(xd[" << xi(m1) << "][c], " << vn << ", p" << bs << ");\n";
-          o << "          q" << bs << " = e3fma(x[" << xi(m1) << "][c], " << vn << ", q" << bs << ");\n";
-        }
+        const std::string dyi = "dy[" + std::to_string(p.y_off + b) + "]";
+        o << "          " << dyi << " = e3fma(z, " << vn << ", " << dyi << ");\n";
         const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]", y2b = "Y2[" + std::to_string(p.y_off + b) + "]";
         t1 = t1.empty() ? yb + " * " + vn : "e3fma(" + yb + ", " + vn + ", " + t1 + ")";
         t2 = t2.empty() ? y2b + " * " + vn : "e3fma(" + y2b + ", " + vn + ", " + t2 + ")";
       }
-      o << "          t[" << xi(m1) << "][c] = e3fma(" << S << ", " << t2 << ", e3fma(" << SD << ", " << t1 << ", t["
-        << xi(m1) << "][c]));\n";
+      o << "          const T t1 = " << t1 << ", t2 = " << t2 << ";\n";
+      o << "          t[" << xi(m1) << "][c] = e3fma(" << S << ", t2, e3fma(" << SD << ", t1, t[" << xi(m1) << "][c]));\n";
+      o << "          gs = e3fma(xd[" << xi(m1) << "][c], t1, e3fma(x[" << xi(m1) << "][c], t2, gs));\n";
       o << "        }\n";
     }
-    std::string gs;
-    for (int b = 0; b < d2; ++b) {
-      if (!binit[b]) continue;
-      const std::string yb = "Y[" + std::to_string(p.y_off + b) + "]", y2b = "Y2[" + std::to_string(p.y_off + b) + "]";
-      const std::string bs = std::to_string(b);
-      gs = gs.empty() ? "e3fma(" + y2b + ", q" + bs + ", " + yb + " * p" + bs + ")"
-                      : "e3fma(" + y2b + ", q" + bs + ", e3fma(" + yb + ", p" + bs + ", " + gs + "))";
-    }
-    o << "        gsv[c] = " << (gs.empty() ? std::string("T(0)") : gs) << ";\n";
-    for (int b = 0; b < d2; ++b) {
-      if (!binit[b]) continue;
-      const std::string bs = std::to_string(b), dyi = "dy[" + std::to_string(p.y_off + b) + "]";
-      o << "        " << dyi << " = e3fma(" << S << ", p" << bs << ", e3fma(" << SD << ", q" << bs << ", " << dyi << "));\n";
-    }
-    for (int b = 0; b < d2; ++b)
-      if (!binit[b]) o << "        (void)p" << b << "; (void)q" << b << ";\n";
+    o << "        gsv[c] = gs;\n";
     o << "      }\n";
     o << "      st_ds(" << pl << ", gsv);\n";
     o << "    }\n";
