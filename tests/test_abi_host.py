@@ -170,3 +170,19 @@ def test_record_tp_create_checks():
     assert L.e3_tpg_create(4, 4, 4, 2, None, i, i, v, 1, ct.byref(h)) == 1
     assert L.e3_tpg_create(4, 4, 400, 2, i, i, i, v, 1, ct.byref(h)) == 2     # 400 rows x 64 lanes > 64 KiB
     assert L.e3_tpg_create(4, 4, 4, 2, i, i, i, v, 1, None) == 1
+
+
+def test_probe_stream_argument_checks():
+    """Streaming probe: argument and shape checks, all before device work."""
+    L = e3mi.lib()
+    br, bw = ct.c_size_t(), ct.c_size_t()
+    fake = ct.c_void_p(256)
+    assert L.e3_probe_stream(fake, 1024, fake, 1024, 0, 0, 16, 0, ct.byref(br), ct.byref(bw), None) == 1
+    assert L.e3_probe_stream(fake, 1024, fake, 1024, 16, 0, 12, 0, ct.byref(br), ct.byref(bw), None) == 1
+    assert L.e3_probe_stream(fake, 1024, fake, 1024, 16, 0, 16, 4, ct.byref(br), ct.byref(bw), None) == 1
+    assert L.e3_probe_stream(None, 1024, fake, 1024, 16, 0, 16, 0, ct.byref(br), ct.byref(bw), None) == 1
+    assert L.e3_probe_stream(ct.c_void_p(4), 1024, fake, 1024, 16, 0, 16, 0, ct.byref(br), ct.byref(bw),
+                             None) == 1
+    assert L.e3_probe_stream(fake, 1024, fake, 1024, 16, 0, 16, 0, None, ct.byref(bw), None) == 1
+    # a read:write shape that is not compiled
+    assert L.e3_probe_stream(fake, 1024, fake, 1024, 3, 5, 4, 0, ct.byref(br), ct.byref(bw), None) == 2

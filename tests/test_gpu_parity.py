@@ -1142,6 +1142,34 @@ def test_tp_float64(e3, irreps, lsh, lout, parity, rows):
         assert v < TOL64, (k, v)
 
 
+def test_probe_stream_bytes_and_writes(e3):
+    """The streaming probe moves exactly the bytes it reports, writes every
+    unit of the destination it covers (the step index mod 1024, one value per
+    unit) and leaves the rest alone; its launch is timed."""
+    import torch
+    _say("probe stream")
+    dev = torch.device("cuda")
+    src = torch.ones(1 << 18, dtype=torch.float32, device=dev)          # 1 MiB
+    dst = torch.full((1 << 18,), -1.0, dtype=torch.float32, device=dev)
+    e3.timing_reset()
+    e3.timing_enable(True)
+    br, bw = e3.probe_stream(src, dst, 2, 6, 8, 3)
+    torch.cuda.synchronize()
+    e3.timing_enable(False)
+    unit = 64 * 8
+    steps = min((1 << 20) // (2 * unit), (1 << 20) // (6 * unit))
+    assert (br, bw) == (steps * 2 * unit, steps * 6 * unit)
+    got = to_np(dst).reshape(-1)
+    per_step = 6 * unit // 4
+    for st in (0, 1, steps // 2, steps - 1):
+        assert np.all(got[st * per_step:(st + 1) * per_step] == float(st & 1023)), st
+    assert np.all(got[steps * per_step:] == -1.0)
+    assert "probe_stream" in e3.timing_read()
+    br, bw = e3.probe_stream(src, None, 16, 0, 16, 1)
+    torch.cuda.synchronize()
+    assert bw == 0 and br == (1 << 20) // (16 * 64 * 16) * 16 * 64 * 16
+
+
 # ---------------------------------------------------------------- capacity (last: largest)
 def test_conv_stress_water70k_sampled(e3):
     """70,000 H2O (210,000 atoms, ~11M edges), 64 channels: forward + backward at
