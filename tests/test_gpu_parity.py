@@ -935,6 +935,63 @@ def test_conv_step_in_captured_graph(e3):
 
 
 
+def test_extensions_in_captured_graph(e3):
+    """The double backward, the fused-radial forward and backward and the
+    tensor product forward and backward captured in one HIP graph and replayed
+    several times, with eager work between replays: every replay equals the
+    eager result bit for bit."""
+    import torch
+    _say("extensions in captured graph")
+    rng = np.random.default_rng(72)
+    irreps = "128x0e+128x1o+128x2e+128x3o"
+    lay = oirreps.layout(irreps, 3, 3)
+    n, e, K, R = 200, 3000, 8, 500
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    plan = e3.Plan(irreps, 3, 3)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=5)
+    f = lambda *shape: to_dev(rng.standard_normal(shape).astype(np.float32))
+    x, vs, s, dm = f(n, lay.d_in, C), to_dev(vec), f(e, lay.n_paths, C), f(n, lay.d_out, C)
+    y, ddx, ddy, dds = f(e, lay.d_sh), f(n, lay.d_in, C), f(e, lay.d_sh), f(e, lay.n_paths, C)
+    h, W = f(e, K), f(K, lay.n_paths, C)
+    tx, ty, tw, tdz = f(R, lay.d_in, C), f(R, lay.d_sh), f(R, lay.n_paths, C), f(R, lay.d_out, C)
+    ws2 = e3.workspace(e3.conv_workspace_size(plan, G)[1])
+    wsr = e3.workspace(e3.conv_radial_workspace_size(plan, G, K))
+    wst = e3.workspace(e3.tp_workspace_size(plan, R))
+    m = torch.empty((n, lay.d_out, C), device="cuda")
+    rdx, rdvec, rdh, rdW = (torch.empty_like(t) for t in (x, vs, h, W))
+    tz = torch.empty_like(tdz)
+    tdx, tdy, tdw = torch.empty_like(tx), torch.empty_like(ty), torch.empty_like(tw)
+    outs = {}
+
+    def step():
+        outs["bwd2"] = e3.conv_bwd2(plan, G, x, y, s, dm, ddx, ddy, dds, ws=ws2)
+        e3.conv_fwd_radial(plan, G, x, vs, h, W, out=m)
+        e3.conv_bwd_radial(plan, G, x, vs, h, W, dm, dx=rdx, dvec=rdvec, dh=rdh, dW=rdW, ws=wsr)
+        e3.tp_fwd(plan, tx, ty, tw, out=tz)
+        e3.tp_bwd(plan, tx, ty, tw, tdz, tdx, tdy, tdw, wst)
+
+    def results():
+        return list(outs["bwd2"]) + [m, rdx, rdvec, rdh, rdW, tz, tdx, tdy, tdw]
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in results()]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for it in range(3):
+        for t in results():
+            t.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(results(), ref):
+            assert torch.equal(a, b), it
+        _ = e3.conv_fwd(plan, G, x, vs, s)   # eager work between replays
+        torch.cuda.synchronize()
+
+
 def test_conv_on_side_stream(e3):
     """Forward + backward launched on a stream other than torch's current one:
     outputs and workspace are allocated for that stream, and the results equal
