@@ -1,7 +1,8 @@
 """The no-allocation backward (e3_conv_bwd_noalloc), called through the C ABI:
 its outputs equal those of the workspace entry point (e3_conv_bwd) bit for bit
 and the fp64 oracle to the parity bar, on two calls in a row, the second on a
-smaller graph, and a graph whose scratch exceeds the fixed array is refused.
+smaller graph; a graph whose scratch exceeds the fixed array is refused; and a
+captured call replays to the eager result.
 """
 import numpy as np
 import pytest
@@ -85,3 +86,46 @@ def test_noalloc_backward_refuses_a_graph_beyond_its_scratch(e3):
         e3.conv_bwd_noalloc(plan, G, xs, to_dev(vec), ss, dms, torch.empty_like(xs),
                             torch.empty((e, 3), device="cuda"), torch.empty_like(ss))
     assert ei.value.status == 4
+
+
+def test_noalloc_backward_in_captured_graph(e3):
+    """The callers it is for: captured in a HIP graph with preallocated outputs
+    (no workspace), every replay equals the eager call bit for bit, with eager
+    work on the same scratch between replays."""
+    import torch
+    irreps = "128x0e+128x1o+128x2e+128x3o"
+    lay = oirreps.layout(irreps, 3, 3)
+    plan = e3.Plan(irreps, 3, 3)
+    C = lay.channels
+    rng = np.random.default_rng(76)
+    n, e = 300, 4000
+    print(f"[case] no-allocation backward in a captured graph, n={n} e={e}", flush=True)
+    snd, rcv, vec = _graph(rng, n, e)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n)
+    xs = to_dev(rng.standard_normal((n, lay.d_in, C)).astype(np.float32))
+    ss = to_dev(rng.standard_normal((e, lay.n_paths, C)).astype(np.float32))
+    dms = to_dev(rng.standard_normal((n, lay.d_out, C)).astype(np.float32))
+    vs = to_dev(vec)
+    dx, dvec, ds = torch.empty_like(xs), torch.empty((e, 3), device="cuda"), torch.empty_like(ss)
+    e3.conv_bwd_noalloc(plan, G, xs, vs, ss, dms, dx, dvec, ds)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (dx, dvec, ds)]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        e3.conv_bwd_noalloc(plan, G, xs, vs, ss, dms, dx, dvec, ds)
+    torch.cuda.synchronize()
+    # another call on a smaller graph between replays overwrites part of the scratch
+    m = 100
+    G2 = e3.Graph(to_dev(snd[:1000] % m), to_dev(rcv[:1000] % m), m)
+    x2, dm2 = xs[:m].contiguous(), dms[:m].contiguous()
+    for it in range(3):
+        for t in (dx, dvec, ds):
+            t.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip((dx, dvec, ds), ref):
+            assert torch.equal(a, b), it
+        e3.conv_bwd_noalloc(plan, G2, x2, vs[:1000].contiguous(), ss[:1000].contiguous(), dm2,
+                            torch.empty_like(x2), torch.empty((1000, 3), device="cuda"),
+                            torch.empty((1000, lay.n_paths, C), device="cuda"))
+        torch.cuda.synchronize()
