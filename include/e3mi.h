@@ -117,8 +117,10 @@ e3_status e3_sh_host(int lmax, const double* u, double* y, int64_t n);
  * their edge-id order (stable).  Edges with sender or receiver equal to
  * pad_node (pad_node >= 0) are padding: they are skipped by every kernel and
  * get zero cotangents; pad_node = -1 means no padding node.
- * Validates every index (E3_ERR_INDEX_OUT_OF_RANGE) and synchronises the
- * stream once.  n_edges may be 0.  The graph allocates its own device memory. */
+ * Validates every index (E3_ERR_INDEX_OUT_OF_RANGE); it synchronises the
+ * stream to read the validation result and again before it frees its
+ * temporaries (the sort's key and count buffers).  n_edges may be 0.  The
+ * graph allocates its own device memory. */
 e3_status e3_graph_create(const int32_t* sender, const int32_t* receiver, int64_t n_nodes,
                           int64_t n_edges, int32_t pad_node, e3_stream stream, e3_graph** out);
 /* Number of non-padding edges. */
