@@ -5,8 +5,9 @@
    compiled irreps layout as literals), one unit v_<tag>.hip per layout and
    the core unit's table of them.
 2. hipcc compiles the core unit (csrc/e3mi.hip: C ABI, graph, linear mixing,
-   record path, probes), every layout unit and the builder for gfx950, in
-   parallel, and links libe3mi.so next to this file.
+   record tensor product, probes), the record convolution (csrc/convr.hip:
+   layouts without a compiled unit), every layout unit and the builder for
+   gfx950, in parallel, and links libe3mi.so next to this file.
 
 Layouts beyond the defaults compiled into the generator (the benchmark and
 test layouts, natural-parity versions and one reordered block list) are
@@ -89,7 +90,8 @@ def build(verbose: bool = True, extra=None) -> str:
     units = generate(verbose, extra)
     objdir = os.path.join(BUILD, "obj")
     os.makedirs(objdir, exist_ok=True)
-    sources = [os.path.join(CSRC, "e3mi.hip"), os.path.join(CSRC, "builder.cpp")] + \
+    sources = [os.path.join(CSRC, "e3mi.hip"), os.path.join(CSRC, "convr.hip"),
+               os.path.join(CSRC, "builder.cpp")] + \
               [os.path.join(GEN, u) for u in units]
     objs = []
     cmds = []

@@ -719,10 +719,26 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int cpl_index(int cpl) { return cpl == 1 ? 0 : 1; }
 int cpl_of(const e3_plan* p) { return p->cpl_f; }
 
+// A compiled variant (every entry point).
 e3_status check_plan(const e3_plan* p) {
   if (!p) return E3_ERR_INVALID_ARG;
-  if (p->variant < 0) return E3_ERR_UNSUPPORTED;
+  if (p->variant < 0) {
+    g_last_error = p->rec ? "this entry point needs a compiled kernel variant for the layout"
+                          : p->no_rec_reason;
+    return E3_ERR_UNSUPPORTED;
+  }
   return E3_OK;
+}
+
+// A compiled variant, or the record path with its tables on the current
+// device (the convolution and tensor-product forward and backward).
+e3_status check_any(const e3_plan* p) {
+  if (!p) return E3_ERR_INVALID_ARG;
+  return p->variant >= 0 ? E3_OK : rec_check(p);
+}
+
+Ws conv_ws(const e3_plan* p, const e3_graph* g) {
+  return p->variant >= 0 ? (*kVariants[p->variant]()).ws(p, g) : rec_ws(p, g);
 }
 }  // namespace
 
@@ -794,7 +810,8 @@ e3_status e3_timing_read(int cap, char* names, double* ms, int64_t* count, int* 
 e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsigned flags, e3_plan** out) {
   if (!irreps_x || !out) return E3_ERR_INVALID_ARG;
   *out = nullptr;
-  if (lmax_sh < 0 || lmax_sh > 3 || lmax_out < 0 || lmax_out > 16 || flags > 1u) return E3_ERR_INVALID_ARG;
+  if (lmax_sh < 0 || lmax_sh > 3 || lmax_out < 0 || lmax_out > 16 || (flags & ~(E3_PARITY_NATURAL | E3_PLAN_RECORDS)))
+    return E3_ERR_INVALID_ARG;
   std::vector<e3b::Block> blocks;
   std::string err;
   if (!e3b::parse_irreps(irreps_x, blocks, err)) {
@@ -805,7 +822,7 @@ e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsign
     if (b.l > 16) return E3_ERR_INVALID_ARG;
   e3_plan* p = new (std::nothrow) e3_plan();
   if (!p) return E3_ERR_ALLOC;
-  if (!e3b::make_layout(irreps_x, lmax_sh, lmax_out, flags == E3_PARITY_NATURAL, p->lay, err)) {
+  if (!e3b::make_layout(irreps_x, lmax_sh, lmax_out, (flags & E3_PARITY_NATURAL) != 0, p->lay, err)) {
     g_last_error = err;
     delete p;
     return E3_ERR_UNSUPPORTED;
@@ -823,7 +840,7 @@ e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsign
   // per channel otherwise); the backward sweep gives each lane 1.  Channels
   // beyond one wave are covered by further 64-lane slabs.
   const int C = p->lay.C;
-  if (C >= 4 && C % 4 == 0 && C <= kMaxChannels) {
+  if (C >= 4 && C % 4 == 0 && C <= kMaxChannels && !(flags & E3_PLAN_RECORDS)) {
     for (int i = 0; i < kNumVariants; ++i)
       if (sig == kVariants[i]()->sig && p->lay.d_sh == kVariants[i]()->d_sh) p->variant = i;
   }
@@ -832,6 +849,9 @@ e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsign
     p->nslab_f = (C + kWave * p->cpl_f - 1) / (kWave * p->cpl_f);
     p->cpl_b = C <= kWave ? 1 : E3_BWD_CPL;
     p->nslab_b = (C + kWave * p->cpl_b - 1) / (kWave * p->cpl_b);
+  } else if (rec_create(p) != E3_OK) {
+    // still a valid plan (its tables can be queried); compute calls report this
+    p->no_rec_reason = g_last_error;
   }
   *out = p;
   return E3_OK;
@@ -847,7 +867,7 @@ e3_status e3_plan_query(const e3_plan* p, e3_plan_info* info) {
   info->nnz = (int)p->recs.size();
   info->lmax_sh = p->lay.lmax_sh;
   info->lmax_out = p->lay.lmax_out;
-  info->supported = p->variant >= 0 ? 1 : 0;
+  info->supported = p->variant >= 0 ? 1 : (rec_ready(p) ? 2 : 0);
   return E3_OK;
 }
 
@@ -1079,42 +1099,48 @@ e3_status e3_sh_bwd(int lmax, const float* vec, const float* dy, float* dvec, in
 
 e3_status e3_tp_fwd(const e3_plan* p, const float* x, const float* y, const float* w, float* z, int64_t rows,
                     e3_stream stream) {
-  e3_status s = check_plan(p);
+  e3_status s = check_any(p);
   if (s != E3_OK) return s;
   if (rows < 0) return E3_ERR_INVALID_ARG;
   if (rows > 0 && (!x || !y || !w || !z || !aligned16(x) || !aligned16(w) || !aligned16(z))) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
+  if (p->variant < 0) return rec_fwd(p, nullptr, rows, x, nullptr, y, w, z, 0, reinterpret_cast<hipStream_t>(stream));
   const VariantOps& v = (*kVariants[p->variant]());
   return v.tp[cpl_index(cpl_of(p))](p, x, y, w, z, rows, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_tp_workspace_size(const e3_plan* p, int64_t rows, size_t* bwd_bytes) {
-  e3_status s = check_plan(p);
+  e3_status s = check_any(p);
   if (s != E3_OK) return s;
   if (rows < 0 || !bwd_bytes) return E3_ERR_INVALID_ARG;
-  *bwd_bytes = (*kVariants[p->variant]()).tpws(p, rows);
+  *bwd_bytes = p->variant >= 0 ? (*kVariants[p->variant]()).tpws(p, rows) : rec_tp_ws(p, rows);
   return E3_OK;
 }
 
 e3_status e3_tp_bwd(const e3_plan* p, const float* x, const float* y, const float* w, const float* dz, float* dx,
                     float* dy, float* dw, void* ws, size_t ws_bytes, int64_t rows, e3_stream stream) {
-  e3_status s = check_plan(p);
+  e3_status s = check_any(p);
   if (s != E3_OK) return s;
   if (rows < 0) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
   if (!x || !y || !w || !dz || !dx || !dy || !dw || !ws || !aligned16(x) || !aligned16(w) || !aligned16(dz) ||
       !aligned16(dx) || !aligned16(dw) || !aligned16(ws))
     return E3_ERR_INVALID_ARG;
+  if (p->variant < 0) {
+    if (ws_bytes < rec_tp_ws(p, rows)) return E3_ERR_WORKSPACE_TOO_SMALL;
+    return rec_bwd(p, nullptr, rows, x, nullptr, y, w, dz, dx, nullptr, dy, dw, 0, ws,
+                   reinterpret_cast<hipStream_t>(stream));
+  }
   const VariantOps& v = (*kVariants[p->variant]());
   if (ws_bytes < v.tpws(p, rows)) return E3_ERR_WORKSPACE_TOO_SMALL;
   return v.tpb(p, x, y, w, dz, dx, dy, dw, ws, rows, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_workspace_size(const e3_plan* p, const e3_graph* g, size_t* fwd_bytes, size_t* bwd_bytes) {
-  e3_status s = check_plan(p);
+  e3_status s = check_any(p);
   if (s != E3_OK) return s;
   if (!g) return E3_ERR_INVALID_ARG;
-  Ws w = (*kVariants[p->variant]()).ws(p, g);
+  Ws w = conv_ws(p, g);
   if (fwd_bytes) *fwd_bytes = 0;
   if (bwd_bytes) *bwd_bytes = w.t_bytes + w.dy_bytes;
   return E3_OK;
@@ -1123,11 +1149,12 @@ e3_status e3_conv_workspace_size(const e3_plan* p, const e3_graph* g, size_t* fw
 e3_status e3_conv_fwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
                       float* m, void* ws, size_t ws_bytes, e3_stream stream) {
   (void)ws, (void)ws_bytes;
-  e3_status st = check_plan(p);
+  e3_status st = check_any(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x))) return E3_ERR_INVALID_ARG;
   if (g->n_live > 0 && (!vec || !s || !aligned16(s))) return E3_ERR_INVALID_ARG;
+  if (p->variant < 0) return rec_fwd(p, g, 0, x, vec, nullptr, s, m, 0, reinterpret_cast<hipStream_t>(stream));
   const VariantOps& v = (*kVariants[p->variant]());
   return v.fwd[cpl_index(cpl_of(p))](p, g, x, vec, nullptr, s, m, 0, reinterpret_cast<hipStream_t>(stream));
 }
@@ -1135,16 +1162,19 @@ e3_status e3_conv_fwd(const e3_plan* p, const e3_graph* g, const float* x, const
 e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* s,
                       const float* dm, float* dx, float* dvec, float* ds, void* ws, size_t ws_bytes,
                       e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_any(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
     return E3_ERR_INVALID_ARG;
   if (g->n_edges > 0 && (!vec || !s || !ds || !dvec || !aligned16(s) || !aligned16(ds))) return E3_ERR_INVALID_ARG;
-  const VariantOps& v = (*kVariants[p->variant]());
-  Ws w = v.ws(p, g);
+  Ws w = conv_ws(p, g);
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
+  if (p->variant < 0)
+    return rec_bwd(p, g, 0, x, vec, nullptr, s, dm, dx, dvec, nullptr, ds, 0, ws,
+                   reinterpret_cast<hipStream_t>(stream));
+  const VariantOps& v = (*kVariants[p->variant]());
   return v.bwd[cpl_index(cpl_of(p))](p, g, x, vec, nullptr, s, dm, dx, dvec, nullptr, ds, 0, ws,
                                      reinterpret_cast<hipStream_t>(stream));
 }
@@ -1262,14 +1292,13 @@ extern "C" {
 
 e3_status e3_conv_bwd_noalloc(const e3_plan* p, const e3_graph* g, const float* x, const float* vec,
                               const float* s, const float* dm, float* dx, float* dvec, float* ds, e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_any(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
     return E3_ERR_INVALID_ARG;
   if (g->n_edges > 0 && (!vec || !s || !ds || !dvec || !aligned16(s) || !aligned16(ds))) return E3_ERR_INVALID_ARG;
-  const VariantOps& v = (*kVariants[p->variant]());
-  const Ws w = v.ws(p, g);
+  const Ws w = conv_ws(p, g);
   if (w.t_bytes + w.dy_bytes > kNoAllocScratchBytes) {
     g_last_error = "the backward needs " + std::to_string(w.t_bytes + w.dy_bytes) +
                    " bytes of scratch; the no-allocation entry point has " + std::to_string(kNoAllocScratchBytes);
@@ -1280,6 +1309,10 @@ e3_status e3_conv_bwd_noalloc(const e3_plan* p, const e3_graph* g, const float* 
   // every scratch byte the kernels read is written earlier in the same call
   // (each live edge's partial rows and each wave's harmonic partials), so the
   // previous call's contents need no clearing
+  if (p->variant < 0)
+    return rec_bwd(p, g, 0, x, vec, nullptr, s, dm, dx, dvec, nullptr, ds, 0, ptr,
+                   reinterpret_cast<hipStream_t>(stream));
+  const VariantOps& v = (*kVariants[p->variant]());
   return v.bwd[cpl_index(cpl_of(p))](p, g, x, vec, nullptr, s, dm, dx, dvec, nullptr, ds, 0, ptr,
                                      reinterpret_cast<hipStream_t>(stream));
 }
@@ -1320,11 +1353,13 @@ e3_status e3_conv_bwd_radial(const e3_plan* p, const e3_graph* g, const float* x
 
 e3_status e3_conv_fwd_y(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
                         float* m, int accumulate, e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_any(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x))) return E3_ERR_INVALID_ARG;
   if (g->n_live > 0 && (!y || !s || !aligned16(s))) return E3_ERR_INVALID_ARG;
+  if (p->variant < 0)
+    return rec_fwd(p, g, 0, x, nullptr, y, s, m, accumulate != 0, reinterpret_cast<hipStream_t>(stream));
   const VariantOps& v = (*kVariants[p->variant]());
   return v.fwd[cpl_index(cpl_of(p))](p, g, x, nullptr, y, s, m, accumulate != 0,
                                      reinterpret_cast<hipStream_t>(stream));
@@ -1333,16 +1368,19 @@ e3_status e3_conv_fwd_y(const e3_plan* p, const e3_graph* g, const float* x, con
 e3_status e3_conv_bwd_y(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
                         const float* dm, float* dx, float* dy, float* ds, int accumulate, void* ws, size_t ws_bytes,
                         e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_any(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !dm || !aligned16(x) || !aligned16(dm) || (dx && !aligned16(dx))))
     return E3_ERR_INVALID_ARG;
   if (g->n_edges > 0 && (!y || !s || !aligned16(s) || (ds && !aligned16(ds)))) return E3_ERR_INVALID_ARG;
-  const VariantOps& v = (*kVariants[p->variant]());
-  Ws w = v.ws(p, g);
+  Ws w = conv_ws(p, g);
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
+  if (p->variant < 0)
+    return rec_bwd(p, g, 0, x, nullptr, y, s, dm, dx, nullptr, dy, ds, accumulate ? (kAccDx | kAccDy | kAccDs) : 0,
+                   ws, reinterpret_cast<hipStream_t>(stream));
+  const VariantOps& v = (*kVariants[p->variant]());
   return v.bwd[cpl_index(cpl_of(p))](p, g, x, nullptr, y, s, dm, dx, nullptr, dy, ds,
                                      accumulate ? (kAccDx | kAccDy | kAccDs) : 0, ws,
                                      reinterpret_cast<hipStream_t>(stream));
@@ -1351,7 +1389,7 @@ e3_status e3_conv_bwd_y(const e3_plan* p, const e3_graph* g, const float* x, con
 e3_status e3_conv_bwd2(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
                        const float* dm, const float* ddx, const float* ddy, const float* dds, float* gx, float* gy,
                        float* gs, float* gdm, void* ws, size_t ws_bytes, e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_any(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !dm || !ddx || !gx || !gdm || !aligned16(x) || !aligned16(dm) || !aligned16(ddx) ||
@@ -1360,12 +1398,21 @@ e3_status e3_conv_bwd2(const e3_plan* p, const e3_graph* g, const float* x, cons
   if (g->n_edges > 0 && (!y || !s || !ddy || !dds || !gy || !gs || !aligned16(s) || !aligned16(dds) ||
                          !aligned16(gs)))
     return E3_ERR_INVALID_ARG;
-  const VariantOps& v = (*kVariants[p->variant]());
-  Ws w = v.ws(p, g);
+  Ws w = conv_ws(p, g);
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
-  const int ci = cpl_index(cpl_of(p));
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (p->variant < 0) {  // the record path: three forward and three backward calls
+    if ((st = rec_fwd(p, g, 0, ddx, nullptr, y, s, gdm, 0, hs)) != E3_OK) return st;
+    if ((st = rec_fwd(p, g, 0, x, nullptr, ddy, s, gdm, 1, hs)) != E3_OK) return st;
+    if ((st = rec_fwd(p, g, 0, x, nullptr, y, dds, gdm, 1, hs)) != E3_OK) return st;
+    if ((st = rec_bwd(p, g, 0, ddx, nullptr, y, s, dm, nullptr, nullptr, gy, gs, 0, ws, hs)) != E3_OK) return st;
+    if ((st = rec_bwd(p, g, 0, x, nullptr, ddy, s, dm, gx, nullptr, nullptr, gs, kAccDs, ws, hs)) != E3_OK)
+      return st;
+    return rec_bwd(p, g, 0, x, nullptr, y, dds, dm, gx, nullptr, gy, nullptr, kAccDx | kAccDy, ws, hs);
+  }
+  const VariantOps& v = (*kVariants[p->variant]());
+  const int ci = cpl_index(cpl_of(p));
   // ddm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds), in one pass
   if ((st = v.fwd3(p, g, x, ddx, y, ddy, s, dds, gdm, hs)) != E3_OK) return st;
   // gx, gy, gs in one sweep where the backward runs one channel per lane

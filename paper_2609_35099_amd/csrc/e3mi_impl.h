@@ -2089,6 +2089,8 @@ unsigned blocks_for(int64_t n, int t) { return (unsigned)std::max<int64_t>(1, (n
 }  // namespace
 
 // ============================================================ handles
+struct RecPlan;  // device tables of the record path (convr.hip)
+
 struct e3_plan {
   e3b::Layout lay;
   std::vector<e3b::Record> recs;
@@ -2096,6 +2098,14 @@ struct e3_plan {
   // Channels per lane of the forward / tensor-product / dx kernels (the
   // backward sweep always uses 1) and the number of 64-lane channel slabs.
   int cpl_f = 0, cpl_b = 0, nslab_f = 0, nslab_b = 0;
+  // A layout without a compiled variant runs on the record path, whose
+  // tables are uploaded at plan creation (null when that was not possible).
+  RecPlan* rec = nullptr;
+  std::string no_rec_reason;  // why not, when rec is null
+  e3_plan() = default;
+  e3_plan(const e3_plan&) = delete;
+  e3_plan& operator=(const e3_plan&) = delete;
+  ~e3_plan();
 };
 
 struct e3_graph {
@@ -2113,6 +2123,22 @@ struct e3_graph {
 struct Ws {
   size_t t_bytes, dy_bytes;
 };
+
+// ---- the record path (convr.hip): convolution and tensor product of any
+// channelwise layout with degrees <= 3 from the plan's coupling records.
+// rec_fwd / rec_bwd take the receiver graph g, or g == null for the identity
+// graph over `rows` rows (the tensor product: s is w, m is z, ds is dw, and
+// dx is written directly, with no workspace share for it).
+e3_status rec_create(e3_plan* p);          // builds and uploads the tables
+bool rec_ready(const e3_plan* p);          // tables on a device
+e3_status rec_check(const e3_plan* p);     // ready, and their device is current
+Ws rec_ws(const e3_plan* p, const e3_graph* g);
+size_t rec_tp_ws(const e3_plan* p, int64_t rows);
+e3_status rec_fwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float* x, const float* vec,
+                  const float* y, const float* s, float* m, int accum, hipStream_t st);
+e3_status rec_bwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float* x, const float* vec,
+                  const float* y, const float* s, const float* dm, float* dx, float* dvec, float* dy, float* ds,
+                  int accum, void* ws, hipStream_t st);
 
 // Scratch of the radial backward: T and DY as in the plain backward, then ds
 // by edge id (all E rows when any edge is live), the dW partials of each row

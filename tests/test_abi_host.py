@@ -64,22 +64,57 @@ def test_plan_tables_equal_oracle(spec, natural):
 
 def test_plan_supported_variants():
     for spec in LAYOUTS[:5]:
-        assert e3mi.Plan(*spec).supported, spec
-        assert e3mi.Plan(*spec, natural=True).supported, spec
+        assert e3mi.Plan(*spec).kernels == "compiled", spec
+        assert e3mi.Plan(*spec, natural=True).kernels == "compiled", spec
     # any parities select the same kernels when every path is kept; a reordered
     # block list has its own compiled kernels
-    assert e3mi.Plan("128x0o+128x1e+128x2o+128x3e", 3, 3).supported
-    assert e3mi.Plan("128x1o+128x0e+128x3o+128x2e", 3, 3).supported
+    assert e3mi.Plan("128x0o+128x1e+128x2o+128x3e", 3, 3).kernels == "compiled"
+    assert e3mi.Plan("128x1o+128x0e+128x3o+128x2e", 3, 3).kernels == "compiled"
     # natural parities of other x parities select other paths: not compiled
-    assert not e3mi.Plan("128x0o+128x1e", 2, 2, natural=True).supported
-    # a layout without a compiled kernel is still a valid plan
-    p = e3mi.Plan("4x1o+4x0e+4x2o", 2, 3)
-    assert not p.supported
+    assert e3mi.Plan("128x0o+128x1e", 2, 2, natural=True).kernels != "compiled"
+
+
+def test_plan_without_kernels_is_valid_and_refuses_compute():
+    """A layout the record path does not take (an x block of degree 4) is
+    still a plan with queryable tables; its compute calls report
+    E3_ERR_UNSUPPORTED.  Without a device, every layout without a compiled
+    variant is in that state (the record path's tables live on a device)."""
+    p = e3mi.Plan("4x1o+4x0e+4x4o", 2, 3)
+    assert not p.supported and p.kernels is None and p.info.nnz > 0
     with pytest.raises(e3mi.E3Error) as ei:
-        e3mi.lib()  # noqa
         st = e3mi.lib().e3_tp_fwd(p.handle, None, None, None, None, 1, None)
         e3mi._check(st, "e3_tp_fwd")
     assert ei.value.status == 2
+    q = e3mi.Plan("4x1o+4x0e+4x2o", 2, 3)
+    assert q.kernels in (None, "records")
+
+
+@pytest.mark.parametrize("spec", [("16x0e+16x0o+16x1o+16x1e", 2, 2, False), ("32x2e+32x0e+32x1o", 3, 3, False),
+                                  ("8x3o+8x1e", 1, 3, True), ("68x1o+68x2o", 3, 2, False), ("4x0e", 0, 0, False),
+                                  ("8x0o+8x1o", 1, 1, True), ("1024x1o+1024x1e", 1, 1, False),
+                                  ("64x0e+64x1o+64x1e+64x2e+64x3o", 3, 3, True),
+                                  ("4x0e+4x1o+4x2e+4x3o+4x0o+4x1e+4x2o+4x3e", 3, 3, False)])
+def test_record_tables_pass_their_bounds_check(spec):
+    """The record path's tables of layouts without compiled kernels are built
+    and pass the bounds check of every index the kernels read, before the
+    device upload: here, without a device, creation stops only at the upload."""
+    irreps, lsh, lout, natural = spec
+    p = e3mi.Plan(irreps, lsh, lout, natural=natural)
+    if p.kernels == "records":
+        return
+    assert p.kernels is None
+    with pytest.raises(e3mi.E3Error) as ei:
+        e3mi._check(e3mi.lib().e3_tp_fwd(p.handle, None, None, None, None, 1, None), "e3_tp_fwd")
+    assert ei.value.status == 2 and "no device" in str(ei.value), str(ei.value)
+
+
+def test_record_path_refuses_degree_4_and_unknown_flags():
+    p = e3mi.Plan("4x0e+4x4o", 2, 3)
+    with pytest.raises(e3mi.E3Error) as ei:
+        e3mi._check(e3mi.lib().e3_tp_fwd(p.handle, None, None, None, None, 1, None), "e3_tp_fwd")
+    assert ei.value.status == 2 and "degree up to 3" in str(ei.value), str(ei.value)
+    h = ct.c_void_p()
+    assert e3mi.lib().e3_plan_create(b"4x0e", 0, 0, 4, ct.byref(h)) == 1
 
 
 def test_natural_parity_filter():

@@ -1,0 +1,280 @@
+"""GPU parity of the record path: the convolution and tensor product of
+layouts without compiled kernels (and of compiled ones forced onto it),
+driven by the plan's coupling records at run time, against the fp64 oracle.
+
+Bar: relative L2 <= 1e-5 per output tensor; padding rows exactly zero;
+bitwise-identical repeats.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import conv as oconv
+from oracle import irreps as oirreps
+from oracle import sh as osh
+from oracle import tp as otp
+
+from gpu_util import TOL, layout_of, oracle_bwd_rows, oracle_fwd_rows, rel_l2, to_dev, to_np, upload_weights
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def e3():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2609_35099_amd import e3mi
+    e3mi.lib()
+    return e3mi
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _random_graph(rng, n, e):
+    snd = rng.integers(0, n, e).astype(np.int32)
+    rcv = rng.integers(0, n, e).astype(np.int32)
+    rcv = np.where(rcv == snd, (rcv + 1) % n, rcv).astype(np.int32)
+    vec = (rng.standard_normal((e, 3)) * 2.0).astype(np.float32)
+    return snd, rcv, vec
+
+
+def _plan(e3, irreps, lsh, lout, parity, records=False):
+    plan = e3.Plan(irreps, lsh, lout, natural=parity == "natural", records=records)
+    assert plan.kernels == "records", (irreps, plan.kernels)
+    return plan
+
+
+# (irreps, lmax_sh, lmax_out, parity, force, n, e, pad)
+CASES = [
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", False, 50, 700, -1),   # two blocks of each degree
+    ("32x2e+32x0e+32x1o", 3, 3, "all", False, 60, 900, 5),          # blocks out of degree order
+    ("8x3o+8x1e", 1, 3, "natural", False, 40, 500, -1),             # natural parities, l_sh 1
+    ("68x1o+68x2o", 3, 2, "all", False, 45, 600, 3),                # a ragged second channel slab
+    ("4x0e", 0, 0, "all", False, 30, 200, -1),                      # the smallest layout
+    ("8x0o+8x1o", 1, 1, "natural", False, 40, 500, 2),              # a block with no path
+    ("1024x1o+1024x1e", 1, 1, "all", False, 10, 60, -1),            # 16 channel slabs
+    ("128x0e+128x1o+128x2e+128x3o", 2, 3, "all", False, 60, 1200, -1),
+    ("64x0e+64x1o+64x1e+64x2e+64x3o", 3, 3, "natural", False, 40, 600, 4),
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, "all", True, 80, 1500, 7),   # the benchmark layout, forced
+]
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity,force,n,e,pad", CASES)
+def test_record_conv_full(e3, irreps, lsh, lout, parity, force, n, e, pad):
+    import torch
+    _say("record conv", irreps, lsh, lout, parity, force, n, e, pad)
+    rng = np.random.default_rng(41)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = _plan(e3, irreps, lsh, lout, parity, force)
+    assert (plan.P, plan.D_out) == (lay.n_paths, lay.d_out)
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    s = rng.standard_normal((e, lay.n_paths, C)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    xs, vs, ss, dms = to_dev(x), to_dev(vec), to_dev(s), to_dev(dm)
+    outs = []
+    for _ in range(2):
+        m = e3.conv_fwd(plan, G, xs, vs, ss)
+        dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, ss, dms)
+        outs.append((m, dx, dvec, ds))
+    torch.cuda.synchronize()
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+    m, dx, dvec, ds = outs[0]
+    ref_m = oconv.conv_fwd(lay, x, vec, s, snd, rcv, n, pad_node=pad).numpy()
+    ref = oconv.conv_bwd(lay, x, vec, s, dm, snd, rcv, n, pad_node=pad)
+    errs = dict(m=rel_l2(to_np(m), ref_m), dx=rel_l2(to_np(dx), ref["dx"].numpy()),
+                ds=rel_l2(to_np(ds), ref["ds"].numpy()), dvec=rel_l2(to_np(dvec), ref["dvec"].numpy()))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    if pad >= 0:
+        dead = (snd == pad) | (rcv == pad)
+        assert np.all(to_np(ds)[dead] == 0) and np.all(to_np(dvec)[dead] == 0)
+        assert np.all(to_np(m)[pad] == 0) and np.all(to_np(dx)[pad] == 0)
+    if force:  # the compiled kernels of the same layout agree to rounding
+        cp = e3.Plan(irreps, lsh, lout, natural=parity == "natural")
+        assert cp.kernels == "compiled"
+        mc = e3.conv_fwd(cp, G, xs, vs, ss)
+        dxc, dvc, dsc = e3.conv_bwd(cp, G, xs, vs, ss, dms)
+        for a, b in ((m, mc), (dx, dxc), (dvec, dvc), (ds, dsc)):
+            assert rel_l2(to_np(a), to_np(b)) < 1e-6
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity,force,rows", [
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", False, 37),
+    ("68x1o+68x2o", 3, 2, "all", False, 300),
+    ("8x0o+8x1o", 1, 1, "natural", False, 50),
+    ("32x0e+32x1o+32x2e", 2, 2, "all", True, 257),
+])
+def test_record_tp_fwd_bwd(e3, irreps, lsh, lout, parity, force, rows):
+    """The weighted tensor product on the record path (the convolution code on
+    the identity graph) forward and backward against the oracle."""
+    _say("record tp", irreps, lsh, lout, parity, force, rows)
+    rng = np.random.default_rng(42)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = _plan(e3, irreps, lsh, lout, parity, force)
+    C = lay.channels
+    g = rng.standard_normal((rows, 3))
+    y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
+    x = rng.standard_normal((rows, lay.d_in, C)).astype(np.float32)
+    w = rng.standard_normal((rows, lay.n_paths, C)).astype(np.float32)
+    dz = rng.standard_normal((rows, lay.d_out, C)).astype(np.float32)
+    z = to_np(e3.tp_fwd(plan, to_dev(x), to_dev(y), to_dev(w)))
+    assert rel_l2(z, otp.tp(lay, x, y, w).numpy()) < TOL
+    got = [to_np(t) for t in e3.tp_bwd(plan, to_dev(x), to_dev(y), to_dev(w), to_dev(dz))]
+    for name, a, r in zip(("dx", "dy", "dw"), got, otp.tp_bwd(lay, x, y, w, dz)):
+        err = rel_l2(a, r.numpy())
+        print(name, err, flush=True)
+        assert err < TOL, name
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad", [
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 40, 600, -1),
+    ("68x1o+68x2o", 3, 2, "all", 30, 400, 4),
+])
+def test_record_conv_y_accumulate_optional(e3, irreps, lsh, lout, parity, n, e, pad):
+    """Caller harmonics y, accumulation and omitted cotangents on the record path."""
+    import torch
+    _say("record conv y-input", irreps, n, e, pad)
+    rng = np.random.default_rng(43)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = _plan(e3, irreps, lsh, lout, parity)
+    snd, rcv, _ = _random_graph(rng, n, e)
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    y = rng.standard_normal((e, lay.d_sh)).astype(np.float32)
+    s = rng.standard_normal((e, lay.n_paths, C)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    xs, ys, ss, dms = (to_dev(a) for a in (x, y, s, dm))
+    m = e3.conv_fwd_y(plan, G, xs, ys, ss)
+    dx, dy, ds = e3.conv_bwd_y(plan, G, xs, ys, ss, dms)
+    ref_m = oconv.conv_fwd_from_y(lay, x, y, s, snd, rcv, n, pad_node=pad).numpy()
+    ref = oconv.conv_bwd_from_y(lay, x, y, s, dm, snd, rcv, n, pad_node=pad)
+    errs = dict(m=rel_l2(to_np(m), ref_m), dx=rel_l2(to_np(dx), ref["dx"].numpy()),
+                dy=rel_l2(to_np(dy), ref["dy"].numpy()), ds=rel_l2(to_np(ds), ref["ds"].numpy()))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    m2 = m.clone()
+    e3.conv_fwd_y(plan, G, xs, ys, ss, out=m2, accumulate=True)
+    d2 = [t.clone() for t in (dx, dy, ds)]
+    e3.conv_bwd_y(plan, G, xs, ys, ss, dms, dx=d2[0], dy=d2[1], ds=d2[2], accumulate=True)
+    assert torch.equal(m2, 2 * m)
+    for a, b in zip(d2, (dx, dy, ds)):
+        assert torch.equal(a, 2 * b)
+    for want in (("dx",), ("dy",), ("ds",), ("dy", "ds")):
+        got = e3.conv_bwd_y(plan, G, xs, ys, ss, dms, want=want)
+        for name, full, part in zip(("dx", "dy", "ds"), (dx, dy, ds), got):
+            if name in want:
+                assert torch.equal(full, part), (want, name)
+            else:
+                assert part is None
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad", [
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 30, 400, -1),
+    ("32x2e+32x0e+32x1o", 3, 3, "all", 25, 300, 3),
+])
+def test_record_conv_bwd2(e3, irreps, lsh, lout, parity, n, e, pad):
+    """Double backward on the record path (three forward and three backward
+    passes) against the oracle."""
+    import torch
+    _say("record conv bwd2", irreps, n, e, pad)
+    rng = np.random.default_rng(44)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = _plan(e3, irreps, lsh, lout, parity)
+    snd, rcv, _ = _random_graph(rng, n, e)
+    C = lay.channels
+    arrs = dict(x=(n, lay.d_in, C), y=(e, lay.d_sh), s=(e, lay.n_paths, C), dm=(n, lay.d_out, C),
+                ddx=(n, lay.d_in, C), ddy=(e, lay.d_sh), dds=(e, lay.n_paths, C))
+    a = {k: rng.standard_normal(v).astype(np.float32) for k, v in arrs.items()}
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    d = {k: to_dev(v) for k, v in a.items()}
+    outs = [e3.conv_bwd2(plan, G, d["x"], d["y"], d["s"], d["dm"], d["ddx"], d["ddy"], d["dds"]) for _ in range(2)]
+    for u, v in zip(*outs):
+        assert torch.equal(u, v)
+    ref = oconv.conv_bwd2(lay, a["x"], a["y"], a["s"], a["dm"], a["ddx"], a["ddy"], a["dds"], snd, rcv, n,
+                          pad_node=pad)
+    errs = {k: rel_l2(to_np(g), ref[k].numpy()) for k, g in zip(("dx", "dy", "ds", "ddm"), outs[0])}
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+
+
+def test_record_conv_degenerate_graphs(e3):
+    """No edges; a single edge; nodes without in-edges; on the record path."""
+    irreps, lsh, lout = "16x0e+16x0o+16x1o+16x1e", 2, 2
+    lay = oirreps.layout(irreps, lsh, lout)
+    plan = _plan(e3, irreps, lsh, lout, "all")
+    C = lay.channels
+    rng = np.random.default_rng(45)
+    for snd, rcv, n in [(np.zeros(0, np.int32), np.zeros(0, np.int32), 4),
+                        (np.array([2], np.int32), np.array([0], np.int32), 3)]:
+        _say("record conv degenerate", len(snd))
+        e = len(snd)
+        vec = rng.standard_normal((e, 3)).astype(np.float32)
+        x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+        s = rng.standard_normal((e, lay.n_paths, C)).astype(np.float32)
+        dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+        G = e3.Graph(to_dev(snd), to_dev(rcv), n)
+        xs, vs, ss, dms = to_dev(x), to_dev(vec), to_dev(s), to_dev(dm)
+        m = e3.conv_fwd(plan, G, xs, vs, ss)
+        dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, ss, dms)
+        if e == 0:
+            assert np.all(to_np(m) == 0) and np.all(to_np(dx) == 0)
+        else:
+            ref_m = oconv.conv_fwd(lay, x, vec, s, snd, rcv, n).numpy()
+            ref = oconv.conv_bwd(lay, x, vec, s, dm, snd, rcv, n)
+            assert rel_l2(to_np(m), ref_m) < TOL
+            assert rel_l2(to_np(dx), ref["dx"].numpy()) < TOL
+            assert rel_l2(to_np(ds), ref["ds"].numpy()) < TOL
+            assert rel_l2(to_np(dvec), ref["dvec"].numpy()) < TOL
+            assert np.all(to_np(m)[1:] == 0)
+
+
+def test_record_conv_water8k_sampled(e3):
+    """The benchmark workload (24,000-atom water box, 128x0e+128x1o+128x2e+128x3o,
+    l <= 3) forced onto the record path at full size: sampled receivers,
+    senders and edges against the oracle, and the whole outputs against the
+    compiled kernels."""
+    _say("record conv water8k")
+    cfg = synth.CONFIGS["water8k"]
+    g = synth.graph(cfg)
+    x = synth.node_features(cfg, g.n_nodes)
+    dm = synth.out_cotangent(cfg, g.n_nodes)
+    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out, records=True)
+    assert plan.kernels == "records"
+    s = upload_weights(cfg, g.vec)
+    G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), g.n_nodes)
+    xs, vs, dms = to_dev(x), to_dev(g.vec), to_dev(dm)
+    m = e3.conv_fwd(plan, G, xs, vs, s)
+    dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, s, dms)
+    lay = layout_of(cfg)
+    rng = np.random.default_rng(46)
+    rs = rng.choice(g.n_nodes, 24, replace=False)
+    es = rng.choice(g.sender.shape[0], 64, replace=False)
+    W = synth.bessel_matrix(cfg)
+    sfn = lambda rows: synth.edge_weights_rows(cfg, g.vec, rows, W=W)
+    ref_m = oracle_fwd_rows(lay, x, g.vec, sfn, g.sender, g.receiver, g.n_nodes, rs)
+    ref_dx, ref_ds, ref_dv = oracle_bwd_rows(lay, x, g.vec, sfn, dm, g.sender, g.receiver, g.n_nodes, rs, es)
+    import torch
+    ri, ei = torch.as_tensor(rs, device="cuda"), torch.as_tensor(es, device="cuda")
+    errs = dict(m=rel_l2(to_np(m[ri]), ref_m), dx=rel_l2(to_np(dx[ri]), ref_dx),
+                ds=rel_l2(to_np(ds[ei]), ref_ds), dvec=rel_l2(to_np(dvec[ei]), ref_dv))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    cp = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out)
+    mc = e3.conv_fwd(cp, G, xs, vs, s)
+    dxc, dvc, dsc = e3.conv_bwd(cp, G, xs, vs, s, dms)
+    for a, b in ((m, mc), (dx, dxc), (dvec, dvc), (ds, dsc)):
+        num = float(torch.linalg.vector_norm((a - b).double()))
+        den = float(torch.linalg.vector_norm(b.double()))
+        assert num <= 1e-6 * den, (num, den)
