@@ -701,7 +701,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tp", action="store_true")
-    ap.add_argument("--only", choices=["all", "conv", "records", "radial", "bwd2", "linear", "tp", "ceiling",
+    ap.add_argument("--only", choices=["all", "conv", "generic", "radial", "bwd2", "linear", "tp", "ceiling",
                                        "capacity"],
                     default="all",
                     help="one section; 'capacity' (not part of 'all') times the 210,000-atom box at 64 channels, "
@@ -883,42 +883,47 @@ def main():
         })
         log(f"conv: {ms_step:.3f} ms/step, {E / ms_step / 1e3:.1f} M edges/s; kernels {kernels}")
 
-    # ---------------------------------------------------------------- record path
-    if args.only in ("all", "records"):
-        # the same step with the layout forced onto the record path (the generic
-        # kernels that walk the coupling records at run time)
-        rplan = e3mi.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out, records=True)
-        rws = e3mi.workspace(e3mi.conv_workspace_size(rplan, graph)[1])
+    # ---------------------------------------------------------------- generic paths
+    if args.only in ("all", "generic"):
+        # the same step with the layout forced onto the two paths that serve
+        # layouts without compiled kernels: generated single-block kinds run
+        # block by block (composed), and the coupling records walked at run
+        # time (records)
+        for path in ("composed", "records"):
+            gplan = e3mi.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out, records=path == "records",
+                              composed=path == "composed")
+            gws = e3mi.workspace(e3mi.conv_workspace_size(gplan, graph)[1])
 
-        def rec_step():
-            e3mi.conv_fwd(rplan, graph, xs, vs, s, out=m)
-            e3mi.conv_bwd(rplan, graph, xs, vs, s, dms, dx=dx, dvec=dvec, ds=ds, ws=rws)
+            def gen_step():
+                e3mi.conv_fwd(gplan, graph, xs, vs, s, out=m)
+                e3mi.conv_bwd(gplan, graph, xs, vs, s, dms, dx=dx, dvec=dvec, ds=ds, ws=gws)
 
-        for _ in range(args.warmup):
-            rec_step()
-        torch.cuda.synchronize()
-        e3mi.timing_reset()
-        e3mi.timing_enable(True)
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for _ in range(args.steps):
-            rec_step()
-        ev1.record()
-        torch.cuda.synchronize()
-        e3mi.timing_enable(False)
-        per = e3mi.timing_read()
-        rec_ms = ev0.elapsed_time(ev1) / args.steps
-        _, fwd_b, bwd_b = conv_bytes(N, E, C, plan.D_in, plan.D_out, plan.P)
-        out["records"] = {
-            "workload": "the convolution step above on the record path (kernels driven by the coupling "
-                        "records at run time, for layouts without compiled kernels)",
-            "ms_per_step": round(rec_ms, 4), "edges_per_s": E / (rec_ms * 1e-3),
-            "step_alg_GBps": round((fwd_b + bwd_b) / (rec_ms * 1e-3) / 1e9, 1),
-            "kernels": {k: {"ms": round(t / c, 4), "launches": c} for k, (t, c) in per.items()}}
-        if "ms_per_step" in out:
-            out["records"]["speed_vs_compiled"] = round(out["ms_per_step"] / rec_ms, 4)
-        log(f"records: {rec_ms:.3f} ms/step, {E / rec_ms / 1e3:.1f} M edges/s; kernels {out['records']['kernels']}")
-        del rws, rplan
+            for _ in range(args.warmup):
+                gen_step()
+            torch.cuda.synchronize()
+            e3mi.timing_reset()
+            e3mi.timing_enable(True)
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            nst = args.steps if path == "composed" else max(1, min(args.steps, 5))
+            ev0.record()
+            for _ in range(nst):
+                gen_step()
+            ev1.record()
+            torch.cuda.synchronize()
+            e3mi.timing_enable(False)
+            per = e3mi.timing_read()
+            g_ms = ev0.elapsed_time(ev1) / nst
+            _, fwd_b, bwd_b = conv_bytes(N, E, C, plan.D_in, plan.D_out, plan.P)
+            entry = {"ms_per_step": round(g_ms, 4), "edges_per_s": E / (g_ms * 1e-3), "steps": nst,
+                     "step_alg_GBps": round((fwd_b + bwd_b) / (g_ms * 1e-3) / 1e9, 1),
+                     "kernels": {k: {"ms_total_per_step": round(t / nst, 4), "launches": c}
+                                 for k, (t, c) in per.items()}}
+            if "ms_per_step" in out:
+                entry["speed_vs_compiled"] = round(out["ms_per_step"] / g_ms, 4)
+            out.setdefault("generic", {"workload": "the convolution step above with the layout forced onto the "
+                                                   "paths for layouts without compiled kernels"})[path] = entry
+            log(f"{path}: {g_ms:.3f} ms/step, {E / g_ms / 1e3:.1f} M edges/s; kernels {entry['kernels']}")
+            del gws, gplan
 
     del ws, ds, s
     torch.cuda.empty_cache()

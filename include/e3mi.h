@@ -77,6 +77,7 @@ typedef void* e3_stream;
 #define E3_PARITY_ALL 0u      /* keep every triangle-allowed path (default) */
 #define E3_PARITY_NATURAL 1u  /* keep only paths whose output parity is (-1)^l3 */
 #define E3_PLAN_RECORDS 2u    /* run on the record path even where a compiled variant exists */
+#define E3_PLAN_COMPOSED 4u   /* run on the composed path even where a compiled variant exists */
 
 typedef struct {
   int C;            /* channels (the common multiplicity) */
@@ -84,33 +85,40 @@ typedef struct {
   int D_in, D_sh, D_out;
   int nnz;          /* non-zero coupling records */
   int lmax_sh, lmax_out;
-  int supported;    /* 1: a compiled kernel variant; 2: the record path; 0: no compute */
+  int supported;    /* 1: a compiled kernel variant; 2: the record path; 3: the composed path; 0: none */
 } e3_plan_info;
 
 /* Builds the path list and the coupling tables on the host (float64).
  * irreps_x: e.g. "128x0e+128x1o+128x2e+128x3o".  lmax_sh in [0, 3],
  * lmax_out >= 0.  flags: E3_PARITY_ALL or E3_PARITY_NATURAL, optionally or-ed
- * with E3_PLAN_RECORDS.  INVALID_ARG for a malformed string, out-of-range
- * degree or unknown flag; UNSUPPORTED when the blocks have different
- * multiplicities.
+ * with one of E3_PLAN_RECORDS and E3_PLAN_COMPOSED.  INVALID_ARG for a
+ * malformed string, out-of-range degree or unknown flag (or both path
+ * flags); UNSUPPORTED when the blocks have different multiplicities.
  *
  * Kernels.  A layout whose path list was compiled into the library runs its
  * generated kernels (info.supported == 1).  Any other layout with x blocks
  * and outputs of degree <= 3 and C a multiple of 4 up to 1024 runs on the
- * record path (info.supported == 2; E3_PLAN_RECORDS selects it for any such
- * layout): the generic sparse kernel of App. E
- * ("CUDA kernels"), which walks the plan's unfolded records (i0, i1, i2, C) at
- * run time, lanes on the channels, each receiver's messages summed on chip.
- * Its tables are uploaded at creation to the device current then (the call
- * allocates and waits for the copy); its compute calls return
- * E3_ERR_INVALID_ARG when another device is current.  The record path serves
+ * composed path (info.supported == 3): the library also holds generated
+ * kernels for every single x block (degree, all or natural-parity paths,
+ * harmonics and output degrees), and runs them block by block with the
+ * layout's strides and offsets; each block writes its own output rows, ds
+ * rows, x-cotangent partial rows and harmonic partial sums, which the shared
+ * sender-order segment sum and the harmonic sum then complete.  Nothing is
+ * uploaded.  E3_PLAN_RECORDS selects instead the record path
+ * (info.supported == 2): the generic sparse kernel of App. E ("CUDA
+ * kernels"), which walks the plan's unfolded records (i0, i1, i2, C) at run
+ * time, lanes on the channels, each receiver's messages summed on chip; its
+ * tables are uploaded at creation to the device current then (the call
+ * allocates and waits for the copy), and its compute calls return
+ * E3_ERR_INVALID_ARG when another device is current.  E3_PLAN_COMPOSED
+ * selects the composed path even for a compiled layout.  Both paths serve
  * e3_tp_fwd / e3_tp_bwd / e3_tp_workspace_size, e3_conv_fwd / e3_conv_bwd /
- * e3_conv_workspace_size / e3_conv_bwd_noalloc, e3_conv_fwd_y / e3_conv_bwd_y
- * and e3_conv_bwd2, with the same semantics (deterministic, atomics-free);
- * the float64 and fused-radial entry points need a compiled variant.
- * Otherwise (no device at creation, a larger degree) the plan is still
- * created (info.supported == 0): its tables can be queried, and the compute
- * entry points return E3_ERR_UNSUPPORTED. */
+ * e3_conv_workspace_size / e3_conv_bwd_noalloc, e3_conv_fwd_y /
+ * e3_conv_bwd_y and e3_conv_bwd2, with the same semantics (deterministic,
+ * atomics-free); the float64 and fused-radial entry points need a compiled
+ * variant.  Otherwise (a larger degree; the record path without a device
+ * at creation) the plan is still created (info.supported == 0): its tables
+ * can be queried, and the compute entry points return E3_ERR_UNSUPPORTED. */
 e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsigned flags,
                          e3_plan** out);
 e3_status e3_plan_query(const e3_plan* plan, e3_plan_info* info);

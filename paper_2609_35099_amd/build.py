@@ -3,7 +3,9 @@
 1. g++ builds the table generator (csrc/gen.cpp + csrc/builder.cpp) and runs
    it, writing csrc/generated/: variants.inc (the coupling constants of every
    compiled irreps layout as literals), one unit v_<tag>.hip per layout and
-   the core unit's table of them.
+   the core unit's table of them; kinds.inc (every single x block kind of
+   degree <= 3, composed at run time into other layouts), its units k_<n>.hip
+   and their table.
 2. hipcc compiles the core unit (csrc/e3mi.hip: C ABI, graph, linear mixing,
    record tensor product, probes), the record convolution (csrc/convr.hip:
    layouts without a compiled unit), every layout unit and the builder for

@@ -1,7 +1,18 @@
-// e3mi record path: the convolution and the weighted tensor product for any
-// channelwise layout (blocks of degree <= 3, outputs to degree 3), driven at
-// run time by the plan's unfolded coupling records instead of code generated
-// for the layout.  This is the paper's generic sparse kernel (App. E, "CUDA
+// e3mi: the convolution and the weighted tensor product of layouts without a
+// compiled variant (x blocks of degree <= 3, outputs to degree 3).  Two paths.
+//
+// The composed path (the default).  The build generates the kernels of every
+// single x block kind -- degree, all or natural-parity paths, harmonics and
+// output degrees -- with strides and offsets left to run time.  A layout runs
+// block by block: each block's kernels read its x rows and path weights and
+// write its output rows, its ds rows, its rows of the per-edge x-cotangent
+// partials and its own harmonic partial groups; the sender-order segment sum
+// and the fixed-order harmonic sum then finish the backward once.  Blocks
+// without paths get zero cotangent rows.
+//
+// The record path (E3_PLAN_RECORDS): the same operations driven at run time
+// by the plan's unfolded coupling records instead of code generated for the
+// layout.  This is the paper's generic sparse kernel (App. E, "CUDA
 // kernels": records (i0, i1, i2, value) over the whole unfolded axes, lanes
 // on the trailing channels, one receiver's messages summed on chip over its
 // receiver-CSR segment; App. E.2's trilinear form for the messages), run in
@@ -28,6 +39,7 @@
 // code on the identity graph (row r is edge r from node r to node r), with
 // the x-cotangent partials stored straight into dx.
 #include "e3mi_impl.h"
+#include "generated/kind_table.inc"
 
 namespace {
 
@@ -385,6 +397,15 @@ __global__ __launch_bounds__(256) void k_convr_dy(const float* __restrict__ DY, 
   dy[o] = accum ? dy[o] + v : v;
 }
 
+// Zero `len` floats at offset `off` of each of n rows of `stride` floats (the
+// cotangent rows of x blocks without paths).
+__global__ __launch_bounds__(256) void k_zero_rows(float* __restrict__ base, int64_t n, int64_t stride,
+                                                   int64_t off, int64_t len) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n * len) return;
+  base[(i / len) * stride + off + i % len] = 0.0f;
+}
+
 }  // namespace
 
 // ============================================================ host
@@ -662,6 +683,7 @@ e3_status rec_create(e3_plan* p) {
 }
 
 e3_status rec_check(const e3_plan* p) {
+  if (p->composed) return E3_OK;
   if (!rec_ready(p)) {
     g_last_error = p->no_rec_reason;
     return E3_ERR_UNSUPPORTED;
@@ -726,7 +748,189 @@ e3_status rec_bwd_l(const RecArgs& a, size_t lds, hipStream_t st) {
 
 }  // namespace
 
+// ------------------------------------------------------------ composed path
+e3_status comp_create(e3_plan* p) {
+  const auto& L = p->lay;
+  const int C = L.C;
+  if (C < 4 || C % 4 != 0 || C > kMaxChannels || L.lmax_out > 3) return E3_ERR_UNSUPPORTED;
+  const int nb = (int)L.blocks.size();
+  std::vector<e3_plan::KindBlock> kb;
+  std::vector<std::pair<int, int>> pathless;
+  int x_off = 0, k = 0, g0 = 0;
+  for (int b = 0; b < nb; ++b) {
+    const auto& B = L.blocks[b];
+    if (B.l > 3) return E3_ERR_UNSUPPORTED;
+    const int d1 = 2 * B.l + 1;
+    const int k0 = k;
+    while (k < (int)L.paths.size() && L.paths[k].xb == b) ++k;
+    if (k == k0) {
+      pathless.push_back({x_off, d1});
+      x_off += d1;
+      continue;
+    }
+    // the same block alone: its path list selects the kind
+    e3b::Layout one;
+    std::string err;
+    const std::string irr = "1x" + std::to_string(B.l) + (B.p > 0 ? "e" : "o");
+    if (!e3b::make_layout(irr, L.lmax_sh, L.lmax_out, L.natural, one, err)) return E3_ERR_UNSUPPORTED;
+    if ((int)one.paths.size() != k - k0) return E3_ERR_UNSUPPORTED;
+    for (int j = 0; j < k - k0; ++j) {
+      const auto& a = L.paths[k0 + j];
+      const auto& o = one.paths[j];
+      if (a.l1 != o.l1 || a.l2 != o.l2 || a.l3 != o.l3 || a.x_off != x_off || a.out_off != L.paths[k0].out_off + o.out_off)
+        return E3_ERR_UNSUPPORTED;
+    }
+    const std::string sig = e3b::path_signature(one);
+    int kind = -1;
+    for (int i = 0; i < kNumKinds; ++i)
+      if (sig == kKinds[i]()->sig && one.d_sh == kKinds[i]()->d_sh) kind = i;
+    if (kind < 0) return E3_ERR_UNSUPPORTED;
+    const KindOps& K = *kKinds[kind]();
+    if (K.d_in != d1 || K.np != k - k0 || K.d_out != one.d_out) return E3_ERR_UNSUPPORTED;
+    kb.push_back({kind, x_off, k0, L.paths[k0].out_off, g0});
+    g0 += K.nbg;
+    x_off += d1;
+  }
+  if (x_off != L.d_in || k != (int)L.paths.size()) return E3_ERR_UNSUPPORTED;
+  p->kblocks = std::move(kb);
+  p->pathless = std::move(pathless);
+  p->kng = g0;
+  p->composed = true;
+  p->cpl_f = C <= kWave ? 1 : E3_FWD_CPL;
+  p->nslab_f = (C + kWave * p->cpl_f - 1) / (kWave * p->cpl_f);
+  p->cpl_b = 1;
+  p->nslab_b = (C + kWave - 1) / kWave;
+  return E3_OK;
+}
+
+namespace {
+
+KindCall comp_call(const e3_plan* p, int g0) {
+  return KindCall{p->lay.d_in, (int)p->lay.paths.size(), p->lay.d_out, p->kng, g0};
+}
+
+e3_status comp_zero_rows(float* base, int64_t n, int64_t stride, int64_t off, int64_t len, hipStream_t st) {
+  if (n == 0 || len == 0) return E3_OK;
+  TimedLaunch t_("kind_zero_rows", st);
+  hipLaunchKernelGGL(k_zero_rows, dim3(blocks_for(n * len, 256)), dim3(256), 0, st, base, n, stride, off, len);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+Ws comp_ws(const e3_plan* p, const e3_graph* g) {
+  Ws w{};
+  w.t_bytes = align256((size_t)g->n_live * p->lay.d_in * p->lay.C * sizeof(float));
+  w.dy_bytes = align256((size_t)g->n_live * p->kng * p->nslab_b * 16 * sizeof(float));
+  return w;
+}
+
+template <int L>
+e3_status launch_dvec(const float* vec, const float* DY, const int* eid, float* dvec, int64_t n, int nparts,
+                      hipStream_t st) {
+  hipLaunchKernelGGL(k_convr_dvec<L>, dim3(blocks_for(n, 256)), dim3(256), 0, st, vec, DY, eid, dvec, n, nparts);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+// dvec / dy from the harmonic partials, zero rows of padding edges.
+e3_status finish_bwd(const e3_plan* p, const e3_graph* g, int64_t n_live, const float* vec, const float* DY,
+                     float* dvec, float* dy, float* ds, int nparts, int accum, hipStream_t st) {
+  const int lsh = p->lay.lmax_sh, dsh = p->lay.d_sh;
+  const int* eid = g ? g->eid_r : nullptr;
+  if (n_live > 0 && dvec) {
+    if (!g) return E3_ERR_INVALID_ARG;
+    TimedLaunch t_("convr_dvec", st);
+    e3_status s2;
+    switch (lsh) {
+      case 0: s2 = launch_dvec<0>(vec, DY, eid, dvec, n_live, nparts, st); break;
+      case 1: s2 = launch_dvec<1>(vec, DY, eid, dvec, n_live, nparts, st); break;
+      case 2: s2 = launch_dvec<2>(vec, DY, eid, dvec, n_live, nparts, st); break;
+      default: s2 = launch_dvec<3>(vec, DY, eid, dvec, n_live, nparts, st); break;
+    }
+    if (s2 != E3_OK) return s2;
+  }
+  if (n_live > 0 && dy) {
+    TimedLaunch t_("convr_dy", st);
+    hipLaunchKernelGGL(k_convr_dy, dim3(blocks_for(n_live * dsh, 256)), dim3(256), 0, st, DY, eid, dy, n_live, dsh,
+                       nparts, (accum & kAccDy) != 0);
+    E3_HIP(hipGetLastError());
+  }
+  // padding edges: zero cotangents (left unchanged when accumulating)
+  if (g && g->n_pad > 0) {
+    float* z0 = (accum & kAccDs) ? nullptr : ds;
+    float* z1 = dvec ? dvec : ((accum & kAccDy) ? nullptr : dy);
+    const int64_t w1 = dvec ? 3 : dsh;
+    if (z0 || z1) {
+      TimedLaunch t_("conv_bwd_pad", st);
+      hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad,
+                         z0, (int64_t)p->lay.paths.size() * p->lay.C, z1, w1);
+      E3_HIP(hipGetLastError());
+    }
+  }
+  return E3_OK;
+}
+
+e3_status comp_fwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float* x, const float* vec,
+                   const float* y, const float* s, float* m, int accum, hipStream_t st) {
+  const int64_t C = p->lay.C;
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    const KindCall kc = comp_call(p, b.g0);
+    e3_status r = g ? K.fwd(p, g, x + b.x_off * C, vec, y, s + b.k0 * C, m + b.o_off * C, accum, kc, st)
+                    : K.tp(p, x + b.x_off * C, y, s + b.k0 * C, m + b.o_off * C, rows, kc, st);
+    if (r != E3_OK) return r;
+  }
+  return E3_OK;
+}
+
+e3_status comp_bwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float* x, const float* vec,
+                   const float* y, const float* s, const float* dm, float* dx, float* dvec, float* dy, float* ds,
+                   int accum, void* ws, hipStream_t st) {
+  const int64_t C = p->lay.C, D_in = p->lay.d_in, P = (int64_t)p->lay.paths.size();
+  const int nparts = p->kng * p->nslab_b;
+  e3_status r;
+  if (!g) {  // tensor product: dx and dw rows stored directly
+    float* DY = reinterpret_cast<float*>(ws);
+    for (const auto& b : p->kblocks) {
+      const KindOps& K = *kKinds[b.kind]();
+      if ((r = K.tpb(p, x + b.x_off * C, y, s + b.k0 * C, dm + b.o_off * C, dx + b.x_off * C, ds + b.k0 * C, DY,
+                     rows, comp_call(p, b.g0), st)) != E3_OK)
+        return r;
+    }
+    for (const auto& z : p->pathless)
+      if ((r = comp_zero_rows(dx, rows, D_in * C, z.first * C, z.second * C, st)) != E3_OK) return r;
+    return finish_bwd(p, nullptr, rows, nullptr, DY, nullptr, dy, nullptr, nparts, 0, st);
+  }
+  if (g->n_nodes == 0) return E3_OK;
+  const Ws w = comp_ws(p, g);
+  float* T = reinterpret_cast<float*>(ws);
+  float* DY = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.t_bytes);
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    const int64_t t_row = dx ? (int64_t)K.d_in * C * 4 : 0, ds_row = ds ? (int64_t)K.np * C * 4 : 0;
+    if ((r = K.bwd(p, g, x + b.x_off * C, vec, y, s + b.k0 * C, dm + b.o_off * C, T + b.x_off * C, t_row, DY,
+                   ds ? ds + b.k0 * C : DY, ds_row, (accum & kAccDs) != 0, comp_call(p, b.g0), st)) != E3_OK)
+      return r;
+  }
+  if (dx) {
+    for (const auto& z : p->pathless)
+      if ((r = comp_zero_rows(T, g->n_live, D_in * C, z.first * C, z.second * C, st)) != E3_OK) return r;
+    TimedLaunch t_("conv_bwd_dx", st);
+    const int flat4 = (int)(D_in * C / 4);
+    const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
+    const int chunk = (int)((g->n_nodes + kXcd - 1) / kXcd);
+    hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * chunk * nsl)), dim3(kWave), 0, st, T, dx, g->rowptr_s,
+                       (int)g->n_nodes, chunk, flat4, nsl, (accum & kAccDx) != 0);
+    E3_HIP(hipGetLastError());
+  }
+  (void)P;
+  return finish_bwd(p, g, g->n_live, vec, DY, dvec, dy, ds, nparts, accum, st);
+}
+
+}  // namespace
+
 Ws rec_ws(const e3_plan* p, const e3_graph* g) {
+  if (p->composed) return comp_ws(p, g);
   Ws w{};
   const RecPlan& R = *p->rec;
   w.t_bytes = align256((size_t)g->n_live * p->lay.d_in * p->lay.C * sizeof(float));
@@ -735,6 +939,7 @@ Ws rec_ws(const e3_plan* p, const e3_graph* g) {
 }
 
 size_t rec_tp_ws(const e3_plan* p, int64_t rows) {
+  if (p->composed) return align256((size_t)rows * p->kng * p->nslab_b * 16 * sizeof(float));
   const RecPlan& R = *p->rec;
   return align256((size_t)rows * R.groups.size() * R.nslab * 16 * sizeof(float));
 }
@@ -744,6 +949,7 @@ e3_status rec_fwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float
   const int64_t n = g ? g->n_nodes : rows;
   if (n == 0) return E3_OK;
   if (n > 0x7fffffff) return E3_ERR_UNSUPPORTED;
+  if (p->composed) return comp_fwd(p, g, rows, x, vec, y, s, m, accum, st);
   RecArgs a = rec_args(p, g, rows);
   a.x = x, a.vec = vec, a.y = y, a.s = s, a.m = m, a.accum = accum;
   const size_t lds = rec_lds_bytes(*p->rec, false);
@@ -761,6 +967,7 @@ e3_status rec_bwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float
   const int64_t n = g ? g->n_nodes : rows;
   if (n == 0) return E3_OK;
   if (n > 0x7fffffff) return E3_ERR_UNSUPPORTED;
+  if (p->composed) return comp_bwd(p, g, rows, x, vec, y, s, dm, dx, dvec, dy, ds, accum, ws, st);
   const RecPlan& R = *p->rec;
   const int64_t n_live = g ? g->n_live : rows;
   const int lsh = p->lay.lmax_sh, dsh = p->lay.d_sh, C = p->lay.C;

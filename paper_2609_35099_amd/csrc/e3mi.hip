@@ -810,7 +810,9 @@ e3_status e3_timing_read(int cap, char* names, double* ms, int64_t* count, int* 
 e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsigned flags, e3_plan** out) {
   if (!irreps_x || !out) return E3_ERR_INVALID_ARG;
   *out = nullptr;
-  if (lmax_sh < 0 || lmax_sh > 3 || lmax_out < 0 || lmax_out > 16 || (flags & ~(E3_PARITY_NATURAL | E3_PLAN_RECORDS)))
+  if (lmax_sh < 0 || lmax_sh > 3 || lmax_out < 0 || lmax_out > 16 ||
+      (flags & ~(E3_PARITY_NATURAL | E3_PLAN_RECORDS | E3_PLAN_COMPOSED)) ||
+      ((flags & E3_PLAN_RECORDS) && (flags & E3_PLAN_COMPOSED)))
     return E3_ERR_INVALID_ARG;
   std::vector<e3b::Block> blocks;
   std::string err;
@@ -840,7 +842,7 @@ e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsign
   // per channel otherwise); the backward sweep gives each lane 1.  Channels
   // beyond one wave are covered by further 64-lane slabs.
   const int C = p->lay.C;
-  if (C >= 4 && C % 4 == 0 && C <= kMaxChannels && !(flags & E3_PLAN_RECORDS)) {
+  if (C >= 4 && C % 4 == 0 && C <= kMaxChannels && !(flags & (E3_PLAN_RECORDS | E3_PLAN_COMPOSED))) {
     for (int i = 0; i < kNumVariants; ++i)
       if (sig == kVariants[i]()->sig && p->lay.d_sh == kVariants[i]()->d_sh) p->variant = i;
   }
@@ -849,9 +851,14 @@ e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsign
     p->nslab_f = (C + kWave * p->cpl_f - 1) / (kWave * p->cpl_f);
     p->cpl_b = C <= kWave ? 1 : E3_BWD_CPL;
     p->nslab_b = (C + kWave * p->cpl_b - 1) / (kWave * p->cpl_b);
-  } else if (rec_create(p) != E3_OK) {
-    // still a valid plan (its tables can be queried); compute calls report this
-    p->no_rec_reason = g_last_error;
+  } else if ((flags & E3_PLAN_RECORDS) || comp_create(p) != E3_OK) {
+    // still a valid plan (its tables can be queried) when neither path takes
+    // it: its compute calls report why
+    if (flags & E3_PLAN_COMPOSED)
+      p->no_rec_reason = "the composed path takes x blocks and outputs of degree <= 3 and C a multiple of 4 "
+                         "up to " + std::to_string(kMaxChannels);
+    else if (rec_create(p) != E3_OK)
+      p->no_rec_reason = g_last_error;
   }
   *out = p;
   return E3_OK;
@@ -867,7 +874,7 @@ e3_status e3_plan_query(const e3_plan* p, e3_plan_info* info) {
   info->nnz = (int)p->recs.size();
   info->lmax_sh = p->lay.lmax_sh;
   info->lmax_out = p->lay.lmax_out;
-  info->supported = p->variant >= 0 ? 1 : (rec_ready(p) ? 2 : 0);
+  info->supported = p->variant >= 0 ? 1 : p->composed ? 3 : (rec_ready(p) ? 2 : 0);
   return E3_OK;
 }
 

@@ -420,13 +420,42 @@ __global__ __launch_bounds__(256) void k_sh_bwd(const float* __restrict__ vec, c
   dvec[3 * e] = ox, dvec[3 * e + 1] = oy, dvec[3 * e + 2] = oz;
 }
 
+// Row strides and harmonic-partial slots: the variant's own for a compiled
+// layout, the whole layout's (given at run time) for a single-block kind.
+template <class V, class A>
+__device__ __forceinline__ int x_rows(const A& a) {
+  if constexpr (V::RT) return a.xr;
+  else return V::D_IN;
+}
+template <class V, class A>
+__device__ __forceinline__ int p_rows(const A& a) {
+  if constexpr (V::RT) return a.pr;
+  else return V::NP;
+}
+template <class V, class A>
+__device__ __forceinline__ int o_rows(const A& a) {
+  if constexpr (V::RT) return a.orr;
+  else return V::D_OUT;
+}
+template <class V, int G, class A>
+__device__ __forceinline__ int64_t dy_group(const A& a, int64_t pos) {
+  if constexpr (V::RT) return pos * a.ng + a.g0 + G;
+  else return pos * V::NBG + G;
+}
+
+// Row strides of a single-block kind's tensor product inside a larger layout
+// (unused by compiled layouts).
+struct TpStr {
+  int xr, pr, orr;
+};
+
 // ------------------------------------------------------------ tensor product
 constexpr int kTpRows = 8;  // rows whose pre-contraction is staged per LDS batch
 
 template <class V, int CPL>
 __global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const float* __restrict__ y,
                                               const float* __restrict__ w, float* __restrict__ z, int64_t rows,
-                                              int C, int nslab) {
+                                              int C, int nslab, TpStr ts) {
   using T = typename V::TP;
   __shared__ f4v smem[(kTpRows * T::NA + 3) / 4];
   float* sA = reinterpret_cast<float*>(smem);
@@ -450,9 +479,9 @@ __global__ __launch_bounds__(kWave) void k_tp(const float* __restrict__ x, const
   for (int j = 0; j < n; ++j) {
     const int64_t r = r0 + j;
     float xv[T::NXR][CPL], wv[T::NPATH][CPL];
-    const RowBuf xb = row_buf(x + r * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-    const RowBuf wb = row_buf(w + r * V::NP * C, (int64_t)V::NP * C * 4, q, C);
-    const RowBuf zb = row_buf(z + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+    const RowBuf xb = row_buf(x + r * x_rows<V>(ts) * C, (int64_t)V::D_IN * C * 4, q, C);
+    const RowBuf wb = row_buf(w + r * p_rows<V>(ts) * C, (int64_t)V::NP * C * 4, q, C);
+    const RowBuf zb = row_buf(z + r * o_rows<V>(ts) * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
     for (int i = 0; i < T::NXR; ++i) bld<CPL, kNT>(xb, T::XROW[i], xv[i]);
 #pragma unroll
@@ -478,6 +507,7 @@ struct TpbArgs {
   int64_t rows;
   int C;
   int nslab;
+  int xr, pr, orr, ng, g0;  // a single-block kind inside a larger layout (as in ConvArgs)
 };
 
 template <class V, int G, int CPL>
@@ -504,9 +534,9 @@ __device__ __forceinline__ void tpb_task(const TpbArgs& a, int64_t r0, int sl, f
 #pragma unroll
     for (int i = 0; i < 16; ++i) dy[i] = 0.0f;
     if (act) {
-      const RowBuf xb = row_buf(a.x + r * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-      const RowBuf wb = row_buf(a.w + r * V::NP * C, (int64_t)V::NP * C * 4, q, C);
-      const RowBuf zb = row_buf(a.dz + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+      const RowBuf xb = row_buf(a.x + r * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf wb = row_buf(a.w + r * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
+      const RowBuf zb = row_buf(a.dz + r * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 4, q, C);
       float xv[B::NXR][CPL], wv[B::NPATH][CPL], dzv[B::NROW][CPL], t[B::NXR][CPL], Yv[V::D_SH];
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) {
@@ -520,7 +550,7 @@ __device__ __forceinline__ void tpb_task(const TpbArgs& a, int64_t r0, int sl, f
       for (int i = 0; i < B::NROW; ++i) bld<CPL, kNT>(zb, B::OROW[i], dzv[i]);
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
-      const RowBuf dwb = row_buf(a.dw + r * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+      const RowBuf dwb = row_buf(a.dw + r * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
       auto st = [&](int pl, const float (&v)[CPL]) { bst<CPL, kST>(dwb, B::PATH[pl], v); };
       float dyl[V::D_SH];
 #pragma unroll
@@ -528,12 +558,12 @@ __device__ __forceinline__ void tpb_task(const TpbArgs& a, int64_t r0, int sl, f
       B::template edge<false, CPL>(sA + j * B::NA, Yv, xv, wv, dzv, t, dyl, st);
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
-      const RowBuf dxb = row_buf(a.dx + r * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf dxb = row_buf(a.dx + r * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) bst<CPL, kST>(dxb, B::XROW[i], t[i]);
     }
     const float tot = wave_reduce16(dy, lane);
-    if ((lane & 3) == 0) a.DY[((r * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+    if ((lane & 3) == 0) a.DY[(dy_group<V, G>(a, r) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
   }
 }
 
@@ -610,7 +640,12 @@ struct ConvArgs {
   const float* x2;
   const float* y2;
   const float* s2;
+  // a single-block kind (V::RT) inside a larger layout: rows of the whole
+  // layout per node of x / dx / T slot, per edge of s / ds, per node of m /
+  // dm, and its harmonic-partial groups (all of them, and this block's first)
+  int xr, pr, orr, ng, g0;
 };
+
 
 // Receiver, group and channel slab of this wave: XCD k = blockIdx % 8 walks
 // receivers [k*chunk, (k+1)*chunk); the (group, slab) waves of one receiver are
@@ -674,8 +709,8 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
       auto load = [&](int j, float (&xv)[F::NXR][CPL], float (&sv)[F::NPATH][CPL]) {
         const int64_t e = __builtin_amdgcn_readlane(my_e, j);
         const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
-        const RowBuf xb_ = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-        const RowBuf sb_ = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        const RowBuf xb_ = row_buf(a.x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf sb_ = row_buf(a.s + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
 #pragma unroll
         for (int i = 0; i < F::NXR; ++i) bld<CPL>(xb_, F::XROW[i], xv[i]);
 #pragma unroll
@@ -716,8 +751,9 @@ __device__ __forceinline__ void fwd_task(const ConvArgs& a, int b, int sl, float
     __syncthreads();
   }
   if (act) {
-    const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
-    if constexpr (ACC) {
+    const RowBuf mb = row_buf(a.m + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 4, q, C);
+    // a kind takes the accumulate flag at run time (one kernel for both)
+    if (ACC || (V::RT && a.accum)) {
 #pragma unroll
       for (int i = 0; i < F::NROW; ++i) {
         float o[CPL];
@@ -851,7 +887,7 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
   if (e0 == e1) return;
   float dmv[B::NROW][CPL];
   if (act) {
-    const RowBuf db = row_buf(a.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+    const RowBuf db = row_buf(a.dm + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
     for (int i = 0; i < B::NROW; ++i) bld<CPL>(db, B::OROW[i], dmv[i]);
   }
@@ -878,14 +914,14 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
     auto load_x = [&](int j, float (&xv)[B::NXR][CPL]) {
       if (!act) return;
       const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
-      const RowBuf xb_ = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf xb_ = row_buf(a.x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) bld<CPL>(xb_, B::XROW[i], xv[i]);
     };
     auto load_s = [&](int j, float (&sv)[B::NPATH][CPL]) {
       if (!act) return;
       const int64_t e = __builtin_amdgcn_readlane(my_e, j);
-      const RowBuf sb_ = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+      const RowBuf sb_ = row_buf(a.s + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < B::NPATH; ++i) bld<CPL, kNT>(sb_, B::PATH[i], sv[i]);
     };
@@ -905,23 +941,30 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
         for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
         // an absent output has row size 0: its stores are dropped by the
         // buffer range check, with no branch in the contraction code
-        const RowBuf dsb = row_buf(a.ds + e * V::NP * C, a.ds_row, q, C);
+        const RowBuf dsb = row_buf(a.ds + e * p_rows<V>(a) * C, a.ds_row, q, C);
         // accumulating: the old ds of this edge is loaded before the contraction
-        // starts, so that its latency is hidden behind the arithmetic
-        float old[ACC ? B::NPATH : 1][CPL];
-        if constexpr (ACC) {
+        // starts, so that its latency is hidden behind the arithmetic (a kind
+        // takes the flag at run time)
+        constexpr bool MAYACC = ACC || V::RT;
+        const bool acc_ds = ACC || (V::RT && a.accum);
+        float old[MAYACC ? B::NPATH : 1][CPL];
+        if constexpr (MAYACC) {
+          if (acc_ds) {
 #pragma unroll
-          for (int i = 0; i < B::NPATH; ++i) bld<CPL>(dsb, B::PATH[i], old[i]);
+            for (int i = 0; i < B::NPATH; ++i) bld<CPL>(dsb, B::PATH[i], old[i]);
+          }
         }
         auto st = [&](int pl, const float (&v)[CPL]) {
-          if constexpr (ACC) {
-            float o[CPL];
+          if constexpr (MAYACC) {
+            if (acc_ds) {
+              float o[CPL];
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) o[c] = old[pl][c] + v[c];
-            bst<CPL, kST>(dsb, B::PATH[pl], o);
-          } else {
-            bst<CPL, kST>(dsb, B::PATH[pl], v);
+              for (int c = 0; c < CPL; ++c) o[c] = old[pl][c] + v[c];
+              bst<CPL, kST>(dsb, B::PATH[pl], o);
+              return;
+            }
           }
+          bst<CPL, kST>(dsb, B::PATH[pl], v);
         };
         float dyl[V::D_SH];
 #pragma unroll
@@ -930,13 +973,13 @@ __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
         {
-          const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, a.t_row, q, C);
+          const RowBuf Tb = row_buf(a.T + slot * x_rows<V>(a) * C, a.t_row, q, C);
 #pragma unroll
           for (int i = 0; i < B::NXR; ++i) bst<CPL, E3_T_STORE_AUX>(Tb, B::XROW[i], t[i]);
         }
       }
       const float tot = wave_reduce16(dy, lane);
-      if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+      if ((lane & 3) == 0) a.DY[(dy_group<V, G>(a, eb + j) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
     };
     load_x(0, xa);
     if (E3_BWD_DB_S) load_s(0, sa);
@@ -2102,6 +2145,17 @@ struct e3_plan {
   // tables are uploaded at plan creation (null when that was not possible).
   RecPlan* rec = nullptr;
   std::string no_rec_reason;  // why not, when rec is null
+  // The composed path (a layout without a compiled variant, every x block of
+  // degree <= 3): per x block with paths, its kind and offsets; the x rows of
+  // blocks without paths (their cotangent rows are zero); the harmonic-partial
+  // groups over all blocks.
+  struct KindBlock {
+    int kind, x_off, k0, o_off, g0;
+  };
+  bool composed = false;
+  std::vector<KindBlock> kblocks;
+  std::vector<std::pair<int, int>> pathless;  // (first x row, rows)
+  int kng = 0;
   e3_plan() = default;
   e3_plan(const e3_plan&) = delete;
   e3_plan& operator=(const e3_plan&) = delete;
@@ -2124,11 +2178,13 @@ struct Ws {
   size_t t_bytes, dy_bytes;
 };
 
-// ---- the record path (convr.hip): convolution and tensor product of any
-// channelwise layout with degrees <= 3 from the plan's coupling records.
-// rec_fwd / rec_bwd take the receiver graph g, or g == null for the identity
-// graph over `rows` rows (the tensor product: s is w, m is z, ds is dw, and
-// dx is written directly, with no workspace share for it).
+// ---- layouts without a compiled variant (convr.hip): the composed path
+// (single-block kinds run block by block) or, when forced or when no kind
+// fits, the record path (the plan's coupling records walked at run time).
+// rec_fwd / rec_bwd take the receiver graph g, or g == null for the tensor
+// product over `rows` rows (s is w, m is z, ds is dw, dx written directly,
+// with no workspace share for it); they run whichever of the two the plan has.
+e3_status comp_create(e3_plan* p);         // matches every x block with a kind
 e3_status rec_create(e3_plan* p);          // builds and uploads the tables
 bool rec_ready(const e3_plan* p);          // tables on a device
 e3_status rec_check(const e3_plan* p);     // ready, and their device is current
@@ -2180,6 +2236,32 @@ struct VariantOps {
   e3_status (*bwd64)(const e3_plan*, const e3_graph*, const double*, const double*, const double*, const double*,
                      double*, double*, double*, void*, hipStream_t);
   Ws (*ws64)(const e3_plan*, const e3_graph*);
+};
+
+// ---- single-block kinds: the generated code of one x block (degree <= 3,
+// all its paths or its natural-parity ones) under given harmonics and output
+// degrees, run with the strides and offsets of a larger layout, block by
+// block, for layouts without a compiled variant (the composed path).
+struct KindCall {
+  int xr, pr, orr;  // rows of the whole layout: x / dx per node, s / ds per edge, m / dm per node
+  int ng, g0;       // harmonic-partial groups of the whole layout, and this block's first
+};
+
+struct KindOps {
+  const char* sig;
+  int d_in, d_sh, d_out, np, lsh, nbg;
+  // the forward sweep of the block's output rows (x, s, m offset to the block)
+  e3_status (*fwd)(const e3_plan*, const e3_graph*, const float* x, const float* vec, const float* y,
+                   const float* s, float* m, int accum, const KindCall&, hipStream_t);
+  // the backward edge sweep of the block: its ds rows, its rows of the
+  // x-cotangent partials T, its harmonic partial groups
+  e3_status (*bwd)(const e3_plan*, const e3_graph*, const float* x, const float* vec, const float* y,
+                   const float* s, const float* dm, float* T, int64_t t_row, float* DY, float* ds, int64_t ds_row,
+                   int accum_ds, const KindCall&, hipStream_t);
+  e3_status (*tp)(const e3_plan*, const float* x, const float* y, const float* w, float* z, int64_t rows,
+                  const KindCall&, hipStream_t);
+  e3_status (*tpb)(const e3_plan*, const float* x, const float* y, const float* w, const float* dz, float* dx,
+                   float* dw, float* DY, int64_t rows, const KindCall&, hipStream_t);
 };
 
 namespace {
@@ -2368,7 +2450,7 @@ e3_status run_tp(const e3_plan* p, const float* x, const float* y, const float* 
   {
     TimedLaunch t_("tp_fwd", st);
     const dim3 grid((unsigned)tile_grid(false, rows, kTpRows, p->nslab_f));
-    hipLaunchKernelGGL((k_tp<V, CPL>), grid, dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, p->nslab_f);
+    hipLaunchKernelGGL((k_tp<V, CPL>), grid, dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, p->nslab_f, TpStr{});
   }
   E3_HIP(hipGetLastError());
   return E3_OK;
@@ -2622,7 +2704,88 @@ e3_status run_bwd64(const e3_plan* p, const e3_graph* g, const double* x, const 
   return E3_OK;
 }
 
+// ---- launchers of a single-block kind (one channel per lane in the backward
+// and tensor-product kernels; the accumulate flag is taken at run time)
+template <class V>
+e3_status kind_fwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* y,
+                   const float* s, float* m, int accum, const KindCall& kc, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.y = y, a.s = s, a.m = m, a.accum = accum;
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr;
+  a.nslab = p->nslab_f;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
+  {
+    TimedLaunch t_("kind_fwd", st);
+    if (p->cpl_f == 1)
+      hipLaunchKernelGGL((k_conv_fwd<V, 1, false>), dim3(grid), dim3(kWave), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_conv_fwd<V, E3_FWD_CPL, false>), dim3(grid), dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_bwd(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* y,
+                   const float* s, const float* dm, float* T, int64_t t_row, float* DY, float* ds, int64_t ds_row,
+                   int accum_ds, const KindCall& kc, hipStream_t st) {
+  if (g->n_live == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.y = y, a.s = s, a.dm = dm, a.accum = accum_ds;
+  a.T = T, a.t_row = t_row, a.DY = DY, a.ds = ds, a.ds_row = ds_row;
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr, a.ng = kc.ng, a.g0 = kc.g0;
+  a.nslab = p->nslab_b;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
+  {
+    TimedLaunch t_("kind_bwd", st);
+    hipLaunchKernelGGL((k_conv_bwd_edges<V, 1, false>), dim3(grid), dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_tp(const e3_plan* p, const float* x, const float* y, const float* w, float* z, int64_t rows,
+                  const KindCall& kc, hipStream_t st) {
+  if (rows == 0) return E3_OK;
+  const int nslab = (p->lay.C + kWave - 1) / kWave;
+  {
+    TimedLaunch t_("kind_tp", st);
+    const dim3 grid((unsigned)tile_grid(false, rows, kTpRows, nslab));
+    hipLaunchKernelGGL((k_tp<V, 1>), grid, dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, nslab,
+                       TpStr{kc.xr, kc.pr, kc.orr});
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_tpb(const e3_plan* p, const float* x, const float* y, const float* w, const float* dz, float* dx,
+                   float* dw, float* DY, int64_t rows, const KindCall& kc, hipStream_t st) {
+  if (rows == 0) return E3_OK;
+  TpbArgs a{};
+  a.x = x, a.y = y, a.w = w, a.dz = dz, a.dx = dx, a.dw = dw, a.DY = DY;
+  a.rows = rows;
+  a.C = p->lay.C;
+  a.nslab = (a.C + kWave - 1) / kWave;
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr, a.ng = kc.ng, a.g0 = kc.g0;
+  {
+    TimedLaunch t_("kind_tp_bwd", st);
+    const dim3 grid((unsigned)tile_grid(E3_TP_XCD, rows, kTpRows, V::NBG * a.nslab));
+    hipLaunchKernelGGL((k_tp_bwd<V, 1>), grid, dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
 }  // namespace
+
+// One kind's entry in the composed path's table (constant-initialised).
+#define E3_KIND_OPS(V)                                                                                  \
+  KindOps{e3gen::V::SIG, e3gen::V::D_IN, e3gen::V::D_SH, e3gen::V::D_OUT, e3gen::V::NP, e3gen::V::LSH, \
+          e3gen::V::NBG, &kind_fwd<e3gen::V>, &kind_bwd<e3gen::V>, &kind_tp<e3gen::V>,                 \
+          &kind_tpb<e3gen::V>}
 
 // One variant's entry in the core unit's table (constant-initialised).
 #define E3_VARIANT_OPS(V)                                                                                    \

@@ -12,8 +12,11 @@
 //     (entries (path, M, m1), App. E.4's grouping of records by i0 then i1),
 //     the forward contraction z = A x with the path weight, the backward
 //     contraction (cotangents of x, s and y), and the tensor-product rows.
+// The same code is emitted for every single x block kind (degree <= 3, all
+// or natural-parity paths, harmonics and outputs to degree 3) with its row
+// strides left to run time, so that any other layout runs block by block.
 //
-// usage: gen <out.inc>
+// usage: gen <out_dir> [irreps/lmax_sh/lmax_out/parity ...]
 #include <algorithm>
 #include <cctype>
 #include <cmath>
@@ -833,20 +836,10 @@ int main(int argc, char** argv) {
        "__device__ __forceinline__ double e3fma(double a, double b, double c) { return fma(a, b, c); }\n\n";
   for (int l = 0; l <= 3; ++l) emit_sh(o, l);
 
-  std::vector<std::string> tags;
-  std::set<std::string> seen;
-  for (const auto& v : specs) {
-    Layout lay;
-    std::string err;
-    if (!make_layout(irreps_of(v.blocks), v.lmax_sh, v.lmax_out, v.natural, lay, err)) {
-      std::fprintf(stderr, "gen: %s\n", err.c_str());
-      return 1;
-    }
-    if (lay.paths.empty()) {
-      std::fprintf(stderr, "gen: layout %s has no paths\n", v.blocks.c_str());
-      return 1;
-    }
-    if (!seen.insert(path_signature(lay) + "/" + std::to_string(lay.d_sh)).second) continue;
+  // One layout's struct: its constants, forward groups, backward groups and
+  // the tensor product's single group.  rt: strides and group offsets come at
+  // run time (a single-block kind composed into larger layouts).
+  auto emit_layout = [&](std::ostream& os, const std::string& tag, const Layout& lay, int lmax_sh, bool rt) {
     std::vector<PathInfo> pis = path_infos(lay);
     const int np = (int)pis.size();
     std::vector<int> fc(np), bc(np), rows(np);
@@ -904,48 +897,67 @@ int main(int argc, char** argv) {
       }));
     Group tpg = make_group(lay, pis, 0, np);
 
-    const std::string tag = tag_of(v);
-    tags.push_back(tag);
     int maxf = 0, maxb = 0;
     for (auto& g : fg) maxf = std::max(maxf, g.na_pad);
     for (auto& g : bg) maxb = std::max(maxb, g.na_pad);
-    o << "// ============================================================ " << tag << "\n";
-    o << "// " << np << " paths, D_in " << lay.d_in << ", D_sh " << lay.d_sh << ", D_out " << lay.d_out << "\n";
-    o << "struct " << tag << " {\n";
-    o << "  static constexpr int D_IN = " << lay.d_in << ", D_SH = " << lay.d_sh << ", D_OUT = " << lay.d_out
-      << ", NP = " << np << ", LSH = " << v.lmax_sh << ";\n";
-    o << "  static constexpr const char* SIG = \"" << path_signature(lay) << "\";\n";
-    o << "  static constexpr int NFG = " << fg.size() << ", NBG = " << bg.size() << ";\n";
-    o << "  static constexpr int MAX_NA_F = " << maxf << ", MAX_NA_B = " << maxb << ", NA_TP = " << tpg.na_pad << ";\n";
-    o << "  template <class T>\n  __device__ __forceinline__ static void sh(T x, T y, T z, T* Y) { sh_l" << v.lmax_sh
-      << "(x, y, z, Y); }\n";
-    o << "  template <class T>\n  __device__ __forceinline__ static void sh_grad(T x, T y, T z, const T* dY, T& gx, T& gy, T& gz) { sh_grad_l"
-      << v.lmax_sh << "(x, y, z, dY, gx, gy, gz); }\n";
-    o << "  template <int G> struct FG;\n  template <int G> struct BG;\n  struct TP;\n};\n\n";
+    os << "// ============================================================ " << tag << "\n";
+    os << "// " << np << " paths, D_in " << lay.d_in << ", D_sh " << lay.d_sh << ", D_out " << lay.d_out << "\n";
+    os << "struct " << tag << " {\n";
+    os << "  static constexpr int D_IN = " << lay.d_in << ", D_SH = " << lay.d_sh << ", D_OUT = " << lay.d_out
+       << ", NP = " << np << ", LSH = " << lmax_sh << ";\n";
+    os << "  static constexpr bool RT = " << (rt ? "true" : "false") << ";\n";
+    os << "  static constexpr const char* SIG = \"" << path_signature(lay) << "\";\n";
+    os << "  static constexpr int NFG = " << fg.size() << ", NBG = " << bg.size() << ";\n";
+    os << "  static constexpr int MAX_NA_F = " << maxf << ", MAX_NA_B = " << maxb << ", NA_TP = " << tpg.na_pad
+       << ";\n";
+    os << "  template <class T>\n  __device__ __forceinline__ static void sh(T x, T y, T z, T* Y) { sh_l" << lmax_sh
+       << "(x, y, z, Y); }\n";
+    os << "  template <class T>\n  __device__ __forceinline__ static void sh_grad(T x, T y, T z, const T* dY, T& gx, T& gy, T& gz) { sh_grad_l"
+       << lmax_sh << "(x, y, z, dY, gx, gy, gz); }\n";
+    os << "  template <int G> struct FG;\n  template <int G> struct BG;\n  struct TP;\n};\n\n";
     for (size_t gi = 0; gi < fg.size(); ++gi) {
-      o << "template <> struct " << tag << "::FG<" << gi << "> {\n";
-      o << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
-      emit_group_meta(o, fg[gi]);
-      emit_make_A(o, fg[gi]);
-      emit_fwd_group(o, lay, pis, fg[gi]);
-      emit_fwd3_group(o, pis, fg[gi]);
-      o << "};\n\n";
+      os << "template <> struct " << tag << "::FG<" << gi << "> {\n";
+      os << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
+      emit_group_meta(os, fg[gi]);
+      emit_make_A(os, fg[gi]);
+      emit_fwd_group(os, lay, pis, fg[gi]);
+      if (!rt) emit_fwd3_group(os, pis, fg[gi]);
+      os << "};\n\n";
     }
     for (size_t gi = 0; gi < bg.size(); ++gi) {
-      o << "template <> struct " << tag << "::BG<" << gi << "> {\n";
-      o << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
-      emit_group_meta(o, bg[gi]);
-      emit_make_A(o, bg[gi]);
-      emit_bwd_group(o, lay, pis, bg[gi]);
-      emit_bwd3_group(o, pis, bg[gi]);
-      o << "};\n\n";
+      os << "template <> struct " << tag << "::BG<" << gi << "> {\n";
+      os << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
+      emit_group_meta(os, bg[gi]);
+      emit_make_A(os, bg[gi]);
+      emit_bwd_group(os, lay, pis, bg[gi]);
+      if (!rt) emit_bwd3_group(os, pis, bg[gi]);
+      os << "};\n\n";
     }
-    o << "struct " << tag << "::TP {\n";
-    o << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
-    emit_group_meta(o, tpg);
-    emit_make_A(o, tpg);
-    emit_tp_group(o, lay, pis, tpg);
-    o << "};\n\n";
+    os << "struct " << tag << "::TP {\n";
+    os << "  static constexpr int D_SH = " << lay.d_sh << ";\n";
+    emit_group_meta(os, tpg);
+    emit_make_A(os, tpg);
+    emit_tp_group(os, lay, pis, tpg);
+    os << "};\n\n";
+  };
+
+  std::vector<std::string> tags;
+  std::set<std::string> seen;
+  for (const auto& v : specs) {
+    Layout lay;
+    std::string err;
+    if (!make_layout(irreps_of(v.blocks), v.lmax_sh, v.lmax_out, v.natural, lay, err)) {
+      std::fprintf(stderr, "gen: %s\n", err.c_str());
+      return 1;
+    }
+    if (lay.paths.empty()) {
+      std::fprintf(stderr, "gen: layout %s has no paths\n", v.blocks.c_str());
+      return 1;
+    }
+    if (!seen.insert(path_signature(lay) + "/" + std::to_string(lay.d_sh)).second) continue;
+    const std::string tag = tag_of(v);
+    tags.push_back(tag);
+    emit_layout(o, tag, lay, v.lmax_sh, false);
   }
   o << "#define E3GEN_FOR_EACH_VARIANT(X)";
   for (const auto& t : tags) o << " X(" << t << ")";
@@ -980,8 +992,67 @@ int main(int argc, char** argv) {
       << ");\n  return &ops;\n}\n";
     if (!write("v_" + tag + ".hip", u.str())) return 1;
   }
+  // Kinds: every single x block (degree l1 <= 3, with all paths or with the
+  // natural-parity ones of either block parity) under every harmonics and
+  // output degree up to 3.  A layout without a compiled variant runs block by
+  // block on these, with its strides and offsets given at run time.  Blocks
+  // with the same path list and harmonics share one kind.
+  std::ostringstream ko, kt;
+  ko << "// GENERATED by gen.cpp from the host table builder -- do not edit.\n";
+  ko << "// Single-block kinds, composed at run time into layouts without a compiled variant.\n";
+  ko << "#pragma once\n\nnamespace e3gen {\n\n";
+  std::vector<std::vector<std::string>> unit_kinds;
+  std::vector<std::string> ktags;
+  std::set<std::string> kseen;
+  for (int l1 = 0; l1 <= 3; ++l1) {
+    for (int lsh = 0; lsh <= 3; ++lsh) {
+      std::vector<std::string> in_unit;
+      for (int lout = 0; lout <= 3; ++lout) {
+        for (int cls = 0; cls < 3; ++cls) {  // all paths; natural, block parity (-1)^l1; natural, the other
+          const bool natural = cls != 0;
+          const bool even = ((l1 % 2 == 0) == (cls != 2));
+          const std::string blk = std::to_string(l1) + (even ? "e" : "o");
+          Layout lay;
+          std::string err;
+          if (!make_layout("1x" + blk, lsh, lout, natural, lay, err)) {
+            std::fprintf(stderr, "gen: kind %s: %s\n", blk.c_str(), err.c_str());
+            return 1;
+          }
+          if (lay.paths.empty()) continue;
+          if (!kseen.insert(path_signature(lay) + "/" + std::to_string(lay.d_sh)).second) continue;
+          const std::string tag = "K_l" + std::to_string(l1) + "_s" + std::to_string(lsh) + "_o" +
+                                  std::to_string(lout) + (cls == 0 ? "_a" : cls == 1 ? "_n" : "_p");
+          emit_layout(ko, tag, lay, lsh, true);
+          ktags.push_back(tag);
+          in_unit.push_back(tag);
+        }
+      }
+      if (!in_unit.empty()) unit_kinds.push_back(in_unit);
+    }
+  }
+  ko << "}  // namespace e3gen\n";
+  if (!write("kinds.inc", ko.str())) return 1;
+  kt << "// GENERATED by gen.cpp -- do not edit.\n";
+  for (const auto& tag : ktags) kt << "const KindOps* e3_kind_" << tag << "();\n";
+  kt << "namespace {\nconst KindOps* (*const kKinds[])() = {";
+  for (size_t i = 0; i < ktags.size(); ++i) kt << (i ? ", " : "") << "&e3_kind_" << ktags[i];
+  kt << "};\nconstexpr int kNumKinds = " << ktags.size() << ";\n}  // namespace\n";
+  if (!write("kind_table.inc", kt.str())) return 1;
+  std::vector<std::string> kunits;
+  for (size_t u = 0; u < unit_kinds.size(); ++u) {
+    std::ostringstream k;
+    k << "// GENERATED by gen.cpp -- do not edit.  Kernels and launchers of single-block kinds.\n";
+    k << "#include \"../e3mi_impl.h\"\n#include \"kinds.inc\"\n\n";
+    for (const auto& tag : unit_kinds[u])
+      k << "const KindOps* e3_kind_" << tag << "() {\n  static const KindOps ops = E3_KIND_OPS(" << tag
+        << ");\n  return &ops;\n}\n";
+    const std::string name = "k_" + std::to_string(u) + ".hip";
+    if (!write(name, k.str())) return 1;
+    kunits.push_back(name);
+  }
   // the unit list, one per line, for the build
   std::string units;
   for (const auto& tag : tags) units += "v_" + tag + ".hip\n";
+  for (const auto& name : kunits) units += name + "\n";
   return write("units.txt", units) ? 0 : 1;
 }

@@ -23,6 +23,7 @@ _STATUS = {0: "E3_OK", 1: "E3_ERR_INVALID_ARG", 2: "E3_ERR_UNSUPPORTED",
 E3_PARITY_ALL = 0
 E3_PARITY_NATURAL = 1
 E3_PLAN_RECORDS = 2
+E3_PLAN_COMPOSED = 4
 
 
 class E3Error(RuntimeError):
@@ -168,14 +169,16 @@ class Plan:
     """Paths, coupling tables and kernels for an irreps layout.
 
     `kernels` is "compiled" when a kernel variant was generated for the layout,
-    "records" when the layout runs on the record path (its coupling records
-    uploaded to the current device at creation), else None (no compute).
+    "composed" when it runs block by block on generated single-block kernels,
+    "records" when it runs on the record path (its coupling records uploaded
+    to the current device at creation), else None (no compute).
     """
 
     def __init__(self, irreps: str, lmax_sh: int, lmax_out: int, natural: bool = False,
-                 records: bool = False):
+                 records: bool = False, composed: bool = False):
         h = ct.c_void_p()
-        flags = (E3_PARITY_NATURAL if natural else E3_PARITY_ALL) | (E3_PLAN_RECORDS if records else 0)
+        flags = ((E3_PARITY_NATURAL if natural else E3_PARITY_ALL) | (E3_PLAN_RECORDS if records else 0)
+                 | (E3_PLAN_COMPOSED if composed else 0))
         _check(lib().e3_plan_create(irreps.encode(), lmax_sh, lmax_out, flags, ct.byref(h)),
                "e3_plan_create")
         self._h = h
@@ -186,7 +189,7 @@ class Plan:
         self.C, self.P = info.C, info.P
         self.D_in, self.D_sh, self.D_out = info.D_in, info.D_sh, info.D_out
         self.supported = bool(info.supported)
-        self.kernels = {1: "compiled", 2: "records"}.get(info.supported)
+        self.kernels = {1: "compiled", 2: "records", 3: "composed"}.get(info.supported)
 
     @property
     def handle(self):

@@ -75,10 +75,10 @@ def test_plan_supported_variants():
 
 
 def test_plan_without_kernels_is_valid_and_refuses_compute():
-    """A layout the record path does not take (an x block of degree 4) is
-    still a plan with queryable tables; its compute calls report
-    E3_ERR_UNSUPPORTED.  Without a device, every layout without a compiled
-    variant is in that state (the record path's tables live on a device)."""
+    """A layout neither the composed nor the record path takes (an x block of
+    degree 4) is still a plan with queryable tables; its compute calls report
+    E3_ERR_UNSUPPORTED.  Any layout of degrees <= 3 is composed of
+    single-block kinds (no device tables needed)."""
     p = e3mi.Plan("4x1o+4x0e+4x4o", 2, 3)
     assert not p.supported and p.kernels is None and p.info.nnz > 0
     with pytest.raises(e3mi.E3Error) as ei:
@@ -86,7 +86,7 @@ def test_plan_without_kernels_is_valid_and_refuses_compute():
         e3mi._check(st, "e3_tp_fwd")
     assert ei.value.status == 2
     q = e3mi.Plan("4x1o+4x0e+4x2o", 2, 3)
-    assert q.kernels in (None, "records")
+    assert q.kernels == "composed"
 
 
 @pytest.mark.parametrize("spec", [("16x0e+16x0o+16x1o+16x1e", 2, 2, False), ("32x2e+32x0e+32x1o", 3, 3, False),
@@ -97,9 +97,11 @@ def test_plan_without_kernels_is_valid_and_refuses_compute():
 def test_record_tables_pass_their_bounds_check(spec):
     """The record path's tables of layouts without compiled kernels are built
     and pass the bounds check of every index the kernels read, before the
-    device upload: here, without a device, creation stops only at the upload."""
+    device upload: here, without a device, creation stops only at the upload.
+    Without the flag, the same layouts are composed of single-block kinds."""
     irreps, lsh, lout, natural = spec
-    p = e3mi.Plan(irreps, lsh, lout, natural=natural)
+    assert e3mi.Plan(irreps, lsh, lout, natural=natural).kernels == "composed"
+    p = e3mi.Plan(irreps, lsh, lout, natural=natural, records=True)
     if p.kernels == "records":
         return
     assert p.kernels is None
@@ -114,7 +116,15 @@ def test_record_path_refuses_degree_4_and_unknown_flags():
         e3mi._check(e3mi.lib().e3_tp_fwd(p.handle, None, None, None, None, 1, None), "e3_tp_fwd")
     assert ei.value.status == 2 and "degree up to 3" in str(ei.value), str(ei.value)
     h = ct.c_void_p()
-    assert e3mi.lib().e3_plan_create(b"4x0e", 0, 0, 4, ct.byref(h)) == 1
+    assert e3mi.lib().e3_plan_create(b"4x0e", 0, 0, 8, ct.byref(h)) == 1    # unknown flag
+    assert e3mi.lib().e3_plan_create(b"4x0e", 0, 0, 2 | 4, ct.byref(h)) == 1  # records and composed
+    c = e3mi.Plan("4x0e+4x4o", 2, 3, composed=True)
+    assert c.kernels is None
+    with pytest.raises(e3mi.E3Error) as ei:
+        e3mi._check(e3mi.lib().e3_tp_fwd(c.handle, None, None, None, None, 1, None), "e3_tp_fwd")
+    assert ei.value.status == 2 and "composed path" in str(ei.value), str(ei.value)
+    # a compiled layout forced onto the composed path
+    assert e3mi.Plan("128x0e+128x1o+128x2e+128x3o", 3, 3, composed=True).kernels == "composed"
 
 
 def test_natural_parity_filter():

@@ -1,6 +1,7 @@
-"""GPU parity of the record path: the convolution and tensor product of
-layouts without compiled kernels (and of compiled ones forced onto it),
-driven by the plan's coupling records at run time, against the fp64 oracle.
+"""GPU parity of the two paths for layouts without compiled kernels -- the
+composed path (generated single-block kinds run block by block) and the
+record path (the plan's coupling records walked at run time) -- on such
+layouts and on compiled ones forced onto them, against the fp64 oracle.
 
 Bar: relative L2 <= 1e-5 per output tensor; padding rows exactly zero;
 bitwise-identical repeats.
@@ -41,34 +42,39 @@ def _random_graph(rng, n, e):
     return snd, rcv, vec
 
 
-def _plan(e3, irreps, lsh, lout, parity, records=False):
-    plan = e3.Plan(irreps, lsh, lout, natural=parity == "natural", records=records)
-    assert plan.kernels == "records", (irreps, plan.kernels)
+PATHS = ["composed", "records"]
+
+
+def _plan(e3, irreps, lsh, lout, parity, path):
+    plan = e3.Plan(irreps, lsh, lout, natural=parity == "natural", records=path == "records",
+                   composed=path == "composed")
+    assert plan.kernels == path, (irreps, plan.kernels)
     return plan
 
 
-# (irreps, lmax_sh, lmax_out, parity, force, n, e, pad)
+# (irreps, lmax_sh, lmax_out, parity, n, e, pad)
 CASES = [
-    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", False, 50, 700, -1),   # two blocks of each degree
-    ("32x2e+32x0e+32x1o", 3, 3, "all", False, 60, 900, 5),          # blocks out of degree order
-    ("8x3o+8x1e", 1, 3, "natural", False, 40, 500, -1),             # natural parities, l_sh 1
-    ("68x1o+68x2o", 3, 2, "all", False, 45, 600, 3),                # a ragged second channel slab
-    ("4x0e", 0, 0, "all", False, 30, 200, -1),                      # the smallest layout
-    ("8x0o+8x1o", 1, 1, "natural", False, 40, 500, 2),              # a block with no path
-    ("1024x1o+1024x1e", 1, 1, "all", False, 10, 60, -1),            # 16 channel slabs
-    ("128x0e+128x1o+128x2e+128x3o", 2, 3, "all", False, 60, 1200, -1),
-    ("64x0e+64x1o+64x1e+64x2e+64x3o", 3, 3, "natural", False, 40, 600, 4),
-    ("128x0e+128x1o+128x2e+128x3o", 3, 3, "all", True, 80, 1500, 7),   # the benchmark layout, forced
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 50, 700, -1),   # two blocks of each degree
+    ("32x2e+32x0e+32x1o", 3, 3, "all", 60, 900, 5),          # blocks out of degree order
+    ("8x3o+8x1e", 1, 3, "natural", 40, 500, -1),             # natural parities, l_sh 1
+    ("68x1o+68x2o", 3, 2, "all", 45, 600, 3),                # a ragged second channel slab
+    ("4x0e", 0, 0, "all", 30, 200, -1),                      # the smallest layout
+    ("8x0o+8x1o", 1, 1, "natural", 40, 500, 2),              # a block with no path
+    ("1024x1o+1024x1e", 1, 1, "all", 10, 60, -1),            # 16 channel slabs
+    ("128x0e+128x1o+128x2e+128x3o", 2, 3, "all", 60, 1200, -1),
+    ("64x0e+64x1o+64x1e+64x2e+64x3o", 3, 3, "natural", 40, 600, 4),
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, "all", 80, 1500, 7),   # the benchmark layout (compiled too)
 ]
 
 
-@pytest.mark.parametrize("irreps,lsh,lout,parity,force,n,e,pad", CASES)
-def test_record_conv_full(e3, irreps, lsh, lout, parity, force, n, e, pad):
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad", CASES)
+def test_generic_conv_full(e3, irreps, lsh, lout, parity, n, e, pad, path):
     import torch
-    _say("record conv", irreps, lsh, lout, parity, force, n, e, pad)
+    _say("generic conv", path, irreps, lsh, lout, parity, n, e, pad)
     rng = np.random.default_rng(41)
     lay = oirreps.layout(irreps, lsh, lout, parity=parity)
-    plan = _plan(e3, irreps, lsh, lout, parity, force)
+    plan = _plan(e3, irreps, lsh, lout, parity, path)
     assert (plan.P, plan.D_out) == (lay.n_paths, lay.d_out)
     snd, rcv, vec = _random_graph(rng, n, e)
     C = lay.channels
@@ -97,28 +103,29 @@ def test_record_conv_full(e3, irreps, lsh, lout, parity, force, n, e, pad):
         dead = (snd == pad) | (rcv == pad)
         assert np.all(to_np(ds)[dead] == 0) and np.all(to_np(dvec)[dead] == 0)
         assert np.all(to_np(m)[pad] == 0) and np.all(to_np(dx)[pad] == 0)
-    if force:  # the compiled kernels of the same layout agree to rounding
-        cp = e3.Plan(irreps, lsh, lout, natural=parity == "natural")
-        assert cp.kernels == "compiled"
+    cp = e3.Plan(irreps, lsh, lout, natural=parity == "natural")
+    if cp.kernels == "compiled":  # the compiled kernels of the same layout agree to rounding
         mc = e3.conv_fwd(cp, G, xs, vs, ss)
         dxc, dvc, dsc = e3.conv_bwd(cp, G, xs, vs, ss, dms)
         for a, b in ((m, mc), (dx, dxc), (dvec, dvc), (ds, dsc)):
             assert rel_l2(to_np(a), to_np(b)) < 1e-6
 
 
-@pytest.mark.parametrize("irreps,lsh,lout,parity,force,rows", [
-    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", False, 37),
-    ("68x1o+68x2o", 3, 2, "all", False, 300),
-    ("8x0o+8x1o", 1, 1, "natural", False, 50),
-    ("32x0e+32x1o+32x2e", 2, 2, "all", True, 257),
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("irreps,lsh,lout,parity,rows", [
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 37),
+    ("68x1o+68x2o", 3, 2, "all", 300),
+    ("8x0o+8x1o", 1, 1, "natural", 50),
+    ("32x0e+32x1o+32x2e", 2, 2, "all", 257),
 ])
-def test_record_tp_fwd_bwd(e3, irreps, lsh, lout, parity, force, rows):
-    """The weighted tensor product on the record path (the convolution code on
-    the identity graph) forward and backward against the oracle."""
-    _say("record tp", irreps, lsh, lout, parity, force, rows)
+def test_generic_tp_fwd_bwd(e3, irreps, lsh, lout, parity, rows, path):
+    """The weighted tensor product on the composed path (single-block tensor
+    product kernels) and on the record path (the convolution code on the
+    identity graph), forward and backward, against the oracle."""
+    _say("generic tp", path, irreps, lsh, lout, parity, rows)
     rng = np.random.default_rng(42)
     lay = oirreps.layout(irreps, lsh, lout, parity=parity)
-    plan = _plan(e3, irreps, lsh, lout, parity, force)
+    plan = _plan(e3, irreps, lsh, lout, parity, path)
     C = lay.channels
     g = rng.standard_normal((rows, 3))
     y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
@@ -134,17 +141,19 @@ def test_record_tp_fwd_bwd(e3, irreps, lsh, lout, parity, force, rows):
         assert err < TOL, name
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad", [
     ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 40, 600, -1),
     ("68x1o+68x2o", 3, 2, "all", 30, 400, 4),
+    ("8x0o+8x1o", 1, 1, "natural", 30, 400, -1),
 ])
-def test_record_conv_y_accumulate_optional(e3, irreps, lsh, lout, parity, n, e, pad):
-    """Caller harmonics y, accumulation and omitted cotangents on the record path."""
+def test_generic_conv_y_accumulate_optional(e3, irreps, lsh, lout, parity, n, e, pad, path):
+    """Caller harmonics y, accumulation and omitted cotangents."""
     import torch
-    _say("record conv y-input", irreps, n, e, pad)
+    _say("generic conv y-input", path, irreps, n, e, pad)
     rng = np.random.default_rng(43)
     lay = oirreps.layout(irreps, lsh, lout, parity=parity)
-    plan = _plan(e3, irreps, lsh, lout, parity)
+    plan = _plan(e3, irreps, lsh, lout, parity, path)
     snd, rcv, _ = _random_graph(rng, n, e)
     C = lay.channels
     x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
@@ -178,18 +187,19 @@ def test_record_conv_y_accumulate_optional(e3, irreps, lsh, lout, parity, n, e, 
                 assert part is None
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad", [
     ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 30, 400, -1),
     ("32x2e+32x0e+32x1o", 3, 3, "all", 25, 300, 3),
 ])
-def test_record_conv_bwd2(e3, irreps, lsh, lout, parity, n, e, pad):
-    """Double backward on the record path (three forward and three backward
-    passes) against the oracle."""
+def test_generic_conv_bwd2(e3, irreps, lsh, lout, parity, n, e, pad, path):
+    """Double backward (three forward and three backward passes) against the
+    oracle."""
     import torch
-    _say("record conv bwd2", irreps, n, e, pad)
+    _say("generic conv bwd2", path, irreps, n, e, pad)
     rng = np.random.default_rng(44)
     lay = oirreps.layout(irreps, lsh, lout, parity=parity)
-    plan = _plan(e3, irreps, lsh, lout, parity)
+    plan = _plan(e3, irreps, lsh, lout, parity, path)
     snd, rcv, _ = _random_graph(rng, n, e)
     C = lay.channels
     arrs = dict(x=(n, lay.d_in, C), y=(e, lay.d_sh), s=(e, lay.n_paths, C), dm=(n, lay.d_out, C),
@@ -208,16 +218,17 @@ def test_record_conv_bwd2(e3, irreps, lsh, lout, parity, n, e, pad):
         assert v < TOL, (k, v)
 
 
-def test_record_conv_degenerate_graphs(e3):
-    """No edges; a single edge; nodes without in-edges; on the record path."""
+@pytest.mark.parametrize("path", PATHS)
+def test_generic_conv_degenerate_graphs(e3, path):
+    """No edges; a single edge; nodes without in-edges."""
     irreps, lsh, lout = "16x0e+16x0o+16x1o+16x1e", 2, 2
     lay = oirreps.layout(irreps, lsh, lout)
-    plan = _plan(e3, irreps, lsh, lout, "all")
+    plan = _plan(e3, irreps, lsh, lout, "all", path)
     C = lay.channels
     rng = np.random.default_rng(45)
     for snd, rcv, n in [(np.zeros(0, np.int32), np.zeros(0, np.int32), 4),
                         (np.array([2], np.int32), np.array([0], np.int32), 3)]:
-        _say("record conv degenerate", len(snd))
+        _say("generic conv degenerate", path, len(snd))
         e = len(snd)
         vec = rng.standard_normal((e, 3)).astype(np.float32)
         x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
@@ -239,18 +250,18 @@ def test_record_conv_degenerate_graphs(e3):
             assert np.all(to_np(m)[1:] == 0)
 
 
-def test_record_conv_water8k_sampled(e3):
+@pytest.mark.parametrize("path", PATHS)
+def test_generic_conv_water8k_sampled(e3, path):
     """The benchmark workload (24,000-atom water box, 128x0e+128x1o+128x2e+128x3o,
-    l <= 3) forced onto the record path at full size: sampled receivers,
-    senders and edges against the oracle, and the whole outputs against the
-    compiled kernels."""
-    _say("record conv water8k")
+    l <= 3) forced onto each path at full size: sampled receivers, senders and
+    edges against the oracle, and the whole outputs against the compiled
+    kernels."""
+    _say("generic conv water8k", path)
     cfg = synth.CONFIGS["water8k"]
     g = synth.graph(cfg)
     x = synth.node_features(cfg, g.n_nodes)
     dm = synth.out_cotangent(cfg, g.n_nodes)
-    plan = e3.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out, records=True)
-    assert plan.kernels == "records"
+    plan = _plan(e3, cfg.irreps, cfg.lmax_sh, cfg.lmax_out, "all", path)
     s = upload_weights(cfg, g.vec)
     G = e3.Graph(to_dev(g.sender), to_dev(g.receiver), g.n_nodes)
     xs, vs, dms = to_dev(x), to_dev(g.vec), to_dev(dm)
