@@ -71,7 +71,7 @@ def radial_bytes(N, E, C, D_in, D_out, P, K):
 
 
 KERNEL_SOURCES = ["paper_2609_35099_amd/csrc/e3mi.hip", "paper_2609_35099_amd/csrc/e3mi_impl.h",
-                  "paper_2609_35099_amd/csrc/gen.cpp",
+                  "paper_2609_35099_amd/csrc/convr.hip", "paper_2609_35099_amd/csrc/gen.cpp",
                   "paper_2609_35099_amd/csrc/builder.cpp", "paper_2609_35099_amd/csrc/builder.h"]
 COUNTERS = os.path.join(ROOT, "profiles", "conv_water8k_tp200k_hbm_bytes.txt")
 
@@ -317,6 +317,9 @@ PROF_FILES = [  # file, kind, sections, title
      "forward+backward (200,000 rows)"),
     ("bwd2_water8k_kernel_trace.txt", "trace", ["bwd2"],
      "Kernel-time summary: double backward of the convolution (same water box)"),
+    ("generic_water8k_kernel_trace.txt", "trace", ["generic"],
+     "Kernel-time summary: the convolution step (same water box) on the composed path (kind_*: generated "
+     "single-block kernels, block by block) and on the runtime-record path (convr_*)"),
     ("linear_water8k_kernel_trace.txt", "trace", ["linear"],
      "Kernel-time summary: linear mixing of the convolution output (24,000 nodes, 34 path blocks -> 8 irreps, 128 ch)"),
     ("radial_water8k_kernel_trace.txt", "trace", ["radial"],
@@ -340,7 +343,9 @@ PROF_NAMES = [("k_conv_bwd_edges", "conv_bwd_edges"), ("k_conv_bwd3", "conv_bwd3
               ("k_tp_bwd_dy", "tp_bwd_dy"), ("k_tp_bwd", "tp_bwd"), ("k_tpg_sum", "tp_records_sum"),
               ("k_tpg", "tp_records"), ("k_tp", "tp_fwd"), ("k_sh_bwd", "sh_bwd"), ("k_sh", "sh"),
               ("k_graph_keys", "graph_keys"), ("k_graph_rowptr", "graph_rowptr"), ("k_graph_finish", "graph_finish"),
-              ("k_graph_r2s", "graph_r2s"), ("k_probe", "probe_stream")]
+              ("k_graph_r2s", "graph_r2s"), ("k_probe", "probe_stream"), ("k_convr_fwd", "convr_fwd"),
+              ("k_convr_bwd", "convr_bwd"), ("k_convr_dvec", "convr_dvec"), ("k_convr_dy", "convr_dy"),
+              ("k_zero_rows", "zero_rows")]
 COPY_PROBE = "copy_probe(__amd_rocclr_copyBuffer)"
 
 
@@ -359,6 +364,8 @@ def _prof_short(name, cache={}):
                 if re.search(r"(?<![A-Za-z0-9_])" + sym + r"(?=[<(]|$)", d):
                     short = nm
                     break
+            if short and "e3gen::K_" in d:  # a single-block kind of the composed path
+                short = "kind_" + short
         cache[name] = short
     return cache[name]
 
@@ -463,7 +470,7 @@ def summarize_profiles(root, only=None):
                     "SQ_INSTS_VALU"]
             for sec in secs:
                 body += _prof_util(root, sec, h)
-        head = [f"# {title}", f"# source hash (e3mi.hip, gen.cpp, builder.*): {h}",
+        head = [f"# {title}", f"# source hash (e3mi.hip, e3mi_impl.h, convr.hip, gen.cpp, builder.*): {h}",
                 "# on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`, with $REPO the repository root and "
                 "$OUT a results directory:"] + ["#   " + c for c in cmds]
         with open(os.path.join(ROOT, "profiles", fname), "w") as fh:
