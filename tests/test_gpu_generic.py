@@ -289,3 +289,65 @@ def test_generic_conv_water8k_sampled(e3, path):
         num = float(torch.linalg.vector_norm((a - b).double()))
         den = float(torch.linalg.vector_norm(b.double()))
         assert num <= 1e-6 * den, (num, den)
+
+
+def test_generic_paths_in_captured_graph(e3):
+    """Both paths only launch kernels: the composed path's convolution forward,
+    backward and double backward and tensor product forward and backward, and
+    the record path's convolution forward and backward, captured in one HIP
+    graph and replayed several times with eager work between replays, equal
+    the eager results bit for bit."""
+    import torch
+    _say("generic paths in captured graph")
+    rng = np.random.default_rng(47)
+    irreps, lsh, lout = "32x2e+32x0e+32x1o", 3, 3
+    lay = oirreps.layout(irreps, lsh, lout)
+    cp = _plan(e3, irreps, lsh, lout, "all", "composed")
+    rp = _plan(e3, irreps, lsh, lout, "all", "records")
+    n, e, R = 150, 2000, 300
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=4)
+    f = lambda *shape: to_dev(rng.standard_normal(shape).astype(np.float32))
+    x, vs, s, dm = f(n, lay.d_in, C), to_dev(vec), f(e, lay.n_paths, C), f(n, lay.d_out, C)
+    y, ddx, ddy, dds = f(e, lay.d_sh), f(n, lay.d_in, C), f(e, lay.d_sh), f(e, lay.n_paths, C)
+    tx, ty, tw, tdz = f(R, lay.d_in, C), f(R, lay.d_sh), f(R, lay.n_paths, C), f(R, lay.d_out, C)
+    wsc = e3.workspace(e3.conv_workspace_size(cp, G)[1])
+    wsr = e3.workspace(e3.conv_workspace_size(rp, G)[1])
+    wst = e3.workspace(e3.tp_workspace_size(cp, R))
+    m, mr = (torch.empty((n, lay.d_out, C), device="cuda") for _ in range(2))
+    dx, dxr = torch.empty_like(x), torch.empty_like(x)
+    dvec, dvecr = torch.empty_like(vs), torch.empty_like(vs)
+    ds, dsr = torch.empty_like(s), torch.empty_like(s)
+    tz = torch.empty_like(tdz)
+    tdx, tdy, tdw = torch.empty_like(tx), torch.empty_like(ty), torch.empty_like(tw)
+    outs = {}
+
+    def step():
+        e3.conv_fwd(cp, G, x, vs, s, out=m)
+        e3.conv_bwd(cp, G, x, vs, s, dm, dx=dx, dvec=dvec, ds=ds, ws=wsc)
+        outs["bwd2"] = e3.conv_bwd2(cp, G, x, y, s, dm, ddx, ddy, dds, ws=wsc)
+        e3.tp_fwd(cp, tx, ty, tw, out=tz)
+        e3.tp_bwd(cp, tx, ty, tw, tdz, tdx, tdy, tdw, wst)
+        e3.conv_fwd(rp, G, x, vs, s, out=mr)
+        e3.conv_bwd(rp, G, x, vs, s, dm, dx=dxr, dvec=dvecr, ds=dsr, ws=wsr)
+
+    def results():
+        return [m, dx, dvec, ds] + list(outs["bwd2"]) + [tz, tdx, tdy, tdw, mr, dxr, dvecr, dsr]
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in results()]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for it in range(3):
+        for t in results():
+            t.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(results(), ref):
+            assert torch.equal(a, b), it
+        _ = e3.conv_fwd(cp, G, x, vs, s)   # eager work between replays
+        torch.cuda.synchronize()

@@ -32,17 +32,22 @@ def _graph(rng, n, e, pad=-1):
     return snd, rcv, vec
 
 
-def test_noalloc_backward_equals_workspace_backward(e3):
+@pytest.mark.parametrize("irreps,lsh,lout,force,kernels", [
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, False, "compiled"),
+    ("64x1o+64x0e+64x1e", 2, 2, False, "composed"),                 # a layout without compiled kernels
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, True, "composed"),        # forced onto the composed path
+])
+def test_noalloc_backward_equals_workspace_backward(e3, irreps, lsh, lout, force, kernels):
     import torch
-    irreps = "128x0e+128x1o+128x2e+128x3o"
-    lay = oirreps.layout(irreps, 3, 3)
-    plan = e3.Plan(irreps, 3, 3)
+    lay = oirreps.layout(irreps, lsh, lout)
+    plan = e3.Plan(irreps, lsh, lout, composed=force)
+    assert plan.kernels == kernels
     C = lay.channels
     rng = np.random.default_rng(74)
     # the second call is smaller, so it leaves the first call's partials in the
     # part of the scratch it does not use
     for n, e, pad in [(600, 7000, -1), (120, 1500, 5)]:
-        print(f"[case] no-allocation backward, n={n} e={e} pad={pad}", flush=True)
+        print(f"[case] no-allocation backward, {irreps} {kernels} n={n} e={e} pad={pad}", flush=True)
         snd, rcv, vec = _graph(rng, n, e)
         if pad >= 0:
             snd[::97] = pad
