@@ -406,6 +406,45 @@ __global__ __launch_bounds__(256) void k_zero_rows(float* __restrict__ base, int
   base[(i / len) * stride + off + i % len] = 0.0f;
 }
 
+// float64: dvec of each live edge from its harmonic partials (summed in
+// order), and dy (eid null: position == row).
+template <int LSH>
+__global__ __launch_bounds__(256) void k_convr_dvec64(const double* __restrict__ vec, const double* __restrict__ DY,
+                                                      const int* __restrict__ eid, double* __restrict__ dvec,
+                                                      int64_t n_live, int nparts) {
+  constexpr int DSH = (LSH + 1) * (LSH + 1);
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (pos >= n_live) return;
+  const int64_t e = eid[pos];
+  double dY[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) dY[i] = 0.0;
+  for (int g = 0; g < nparts; ++g)
+#pragma unroll
+    for (int i = 0; i < DSH; ++i) dY[i] += DY[(pos * nparts + g) * 16 + i];
+  double ux, uy, uz, inv, gx, gy, gz;
+  unit_of64(vec, e, ux, uy, uz, inv);
+  if constexpr (LSH == 0) e3gen::sh_grad_l0<double>(ux, uy, uz, dY, gx, gy, gz);
+  else if constexpr (LSH == 1) e3gen::sh_grad_l1<double>(ux, uy, uz, dY, gx, gy, gz);
+  else if constexpr (LSH == 2) e3gen::sh_grad_l2<double>(ux, uy, uz, dY, gx, gy, gz);
+  else e3gen::sh_grad_l3<double>(ux, uy, uz, dY, gx, gy, gz);
+  const double ug = ux * gx + uy * gy + uz * gz;
+  dvec[3 * e] = (gx - ux * ug) * inv;
+  dvec[3 * e + 1] = (gy - uy * ug) * inv;
+  dvec[3 * e + 2] = (gz - uz * ug) * inv;
+}
+
+__global__ __launch_bounds__(256) void k_convr_dy64(const double* __restrict__ DY, const int* __restrict__ eid,
+                                                    double* __restrict__ dy, int64_t n, int dsh, int nparts) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = i / dsh;
+  const int c = (int)(i % dsh);
+  if (r >= n) return;
+  double v = 0.0;
+  for (int g = 0; g < nparts; ++g) v += DY[(r * nparts + g) * 16 + c];
+  dy[(eid ? (int64_t)eid[r] : r) * dsh + c] = v;
+}
+
 }  // namespace
 
 // ============================================================ host
@@ -1036,5 +1075,120 @@ e3_status rec_bwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float
       E3_HIP(hipGetLastError());
     }
   }
+  return E3_OK;
+}
+
+// ------------------------------------------------------------ composed path, float64
+namespace {
+int nslab_c64(const e3_plan* p) { return (p->lay.C + kWave - 1) / kWave; }
+
+template <int L>
+e3_status launch_dvec64(const double* vec, const double* DY, const int* eid, double* dvec, int64_t n, int nparts,
+                        hipStream_t st) {
+  hipLaunchKernelGGL(k_convr_dvec64<L>, dim3(blocks_for(n, 256)), dim3(256), 0, st, vec, DY, eid, dvec, n, nparts);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+}  // namespace
+
+Ws comp_ws64(const e3_plan* p, const e3_graph* g) {
+  Ws w{};
+  w.t_bytes = align256((size_t)g->n_live * p->lay.d_in * p->lay.C * sizeof(double));
+  w.dy_bytes = align256((size_t)g->n_live * p->kng * nslab_c64(p) * 16 * sizeof(double));
+  return w;
+}
+
+size_t comp_tp_ws64(const e3_plan* p, int64_t rows) {
+  return align256((size_t)rows * p->kng * nslab_c64(p) * 16 * sizeof(double));
+}
+
+e3_status comp_fwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                     double* m, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  const int64_t C = p->lay.C;
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    e3_status r = K.fwd64(p, g, x + b.x_off * C, vec, s + b.k0 * C, m + b.o_off * C, comp_call(p, b.g0), st);
+    if (r != E3_OK) return r;
+  }
+  return E3_OK;
+}
+
+e3_status comp_bwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                     const double* dm, double* dx, double* dvec, double* ds, void* ws, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  const int64_t C = p->lay.C, D_in = p->lay.d_in, P = (int64_t)p->lay.paths.size();
+  const int nsl = nslab_c64(p), nparts = p->kng * nsl;
+  const Ws w = comp_ws64(p, g);
+  double* T = reinterpret_cast<double*>(ws);
+  double* DY = reinterpret_cast<double*>(reinterpret_cast<char*>(ws) + w.t_bytes);
+  e3_status r;
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    if ((r = K.bwd64(p, g, x + b.x_off * C, vec, s + b.k0 * C, dm + b.o_off * C, T + b.x_off * C, DY,
+                     ds + b.k0 * C, comp_call(p, b.g0), st)) != E3_OK)
+      return r;
+  }
+  // zero partial rows of blocks without paths, as pairs of 32-bit zeros
+  for (const auto& z : p->pathless)
+    if ((r = comp_zero_rows(reinterpret_cast<float*>(T), g->n_live, 2 * D_in * C, 2 * z.first * C, 2 * z.second * C,
+                            st)) != E3_OK)
+      return r;
+  {
+    TimedLaunch t_("conv_bwd_dx_f64", st);
+    hipLaunchKernelGGL(k_conv_bwd_dx64, dim3((unsigned)(g->n_nodes * nsl)), dim3(kWave), 0, st, T, dx, g->rowptr_s,
+                       (int)g->n_nodes, (int)D_in, (int)C, nsl);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_live > 0) {
+    TimedLaunch t_("convr_dvec_f64", st);
+    switch (p->lay.lmax_sh) {
+      case 0: r = launch_dvec64<0>(vec, DY, g->eid_r, dvec, g->n_live, nparts, st); break;
+      case 1: r = launch_dvec64<1>(vec, DY, g->eid_r, dvec, g->n_live, nparts, st); break;
+      case 2: r = launch_dvec64<2>(vec, DY, g->eid_r, dvec, g->n_live, nparts, st); break;
+      default: r = launch_dvec64<3>(vec, DY, g->eid_r, dvec, g->n_live, nparts, st); break;
+    }
+    if (r != E3_OK) return r;
+  }
+  if (g->n_pad > 0) {  // padding edges: zero ds and dvec rows (as pairs of 32-bit zeros)
+    TimedLaunch t_("conv_bwd_pad", st);
+    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad,
+                       reinterpret_cast<float*>(ds), (int64_t)2 * P * C, reinterpret_cast<float*>(dvec), (int64_t)6);
+    E3_HIP(hipGetLastError());
+  }
+  return E3_OK;
+}
+
+e3_status comp_tp64(const e3_plan* p, const double* x, const double* y, const double* w, double* z, int64_t rows,
+                    hipStream_t st) {
+  const int64_t C = p->lay.C;
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    e3_status r = K.tp64(p, x + b.x_off * C, y, w + b.k0 * C, z + b.o_off * C, rows, comp_call(p, b.g0), st);
+    if (r != E3_OK) return r;
+  }
+  return E3_OK;
+}
+
+e3_status comp_tpb64(const e3_plan* p, const double* x, const double* y, const double* w, const double* dz,
+                     double* dx, double* dy, double* dw, void* ws, int64_t rows, hipStream_t st) {
+  const int64_t C = p->lay.C, D_in = p->lay.d_in;
+  const int nparts = p->kng * nslab_c64(p);
+  double* DY = reinterpret_cast<double*>(ws);
+  e3_status r;
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    if ((r = K.tpb64(p, x + b.x_off * C, y, w + b.k0 * C, dz + b.o_off * C, dx + b.x_off * C, dw + b.k0 * C, DY,
+                     rows, comp_call(p, b.g0), st)) != E3_OK)
+      return r;
+  }
+  for (const auto& z : p->pathless)
+    if ((r = comp_zero_rows(reinterpret_cast<float*>(dx), rows, 2 * D_in * C, 2 * z.first * C, 2 * z.second * C,
+                            st)) != E3_OK)
+      return r;
+  TimedLaunch t_("convr_dy_f64", st);
+  hipLaunchKernelGGL(k_convr_dy64, dim3(blocks_for(rows * p->lay.d_sh, 256)), dim3(256), 0, st, DY,
+                     (const int*)nullptr, dy, rows, p->lay.d_sh, nparts);
+  E3_HIP(hipGetLastError());
   return E3_OK;
 }

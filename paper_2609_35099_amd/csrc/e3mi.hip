@@ -737,6 +737,14 @@ e3_status check_any(const e3_plan* p) {
   return p->variant >= 0 ? E3_OK : rec_check(p);
 }
 
+// A compiled variant or the composed path (the float64 builds).
+e3_status check_f64(const e3_plan* p) {
+  if (!p) return E3_ERR_INVALID_ARG;
+  if (p->variant >= 0 || p->composed) return E3_OK;
+  g_last_error = p->rec ? "the float64 builds need a compiled variant or the composed path" : p->no_rec_reason;
+  return E3_ERR_UNSUPPORTED;
+}
+
 Ws conv_ws(const e3_plan* p, const e3_graph* g) {
   return p->variant >= 0 ? (*kVariants[p->variant]()).ws(p, g) : rec_ws(p, g);
 }
@@ -1189,70 +1197,78 @@ e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const
 // ---- float64 builds
 e3_status e3_tp_fwd_f64(const e3_plan* p, const double* x, const double* y, const double* w, double* z,
                         int64_t rows, e3_stream stream) {
-  e3_status s = check_plan(p);
+  e3_status s = check_f64(p);
   if (s != E3_OK) return s;
   if (rows < 0) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
   if (!x || !y || !w || !z || !aligned16(x) || !aligned16(w) || !aligned16(z)) return E3_ERR_INVALID_ARG;
+  if (p->variant < 0) return comp_tp64(p, x, y, w, z, rows, reinterpret_cast<hipStream_t>(stream));
   return (*kVariants[p->variant]()).tp64(p, x, y, w, z, rows, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_tp_workspace_size_f64(const e3_plan* p, int64_t rows, size_t* bwd_bytes) {
-  e3_status s = check_plan(p);
+  e3_status s = check_f64(p);
   if (s != E3_OK) return s;
   if (rows < 0 || !bwd_bytes) return E3_ERR_INVALID_ARG;
-  *bwd_bytes = (*kVariants[p->variant]()).tpws64(p, rows);
+  *bwd_bytes = p->variant >= 0 ? (*kVariants[p->variant]()).tpws64(p, rows) : comp_tp_ws64(p, rows);
   return E3_OK;
 }
 
 e3_status e3_tp_bwd_f64(const e3_plan* p, const double* x, const double* y, const double* w, const double* dz,
                         double* dx, double* dy, double* dw, void* ws, size_t ws_bytes, int64_t rows,
                         e3_stream stream) {
-  e3_status s = check_plan(p);
+  e3_status s = check_f64(p);
   if (s != E3_OK) return s;
   if (rows < 0) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
   if (!x || !y || !w || !dz || !dx || !dy || !dw || !ws || !aligned16(x) || !aligned16(w) || !aligned16(dz) ||
       !aligned16(dx) || !aligned16(dw) || !aligned16(ws))
     return E3_ERR_INVALID_ARG;
+  if (p->variant < 0) {
+    if (ws_bytes < comp_tp_ws64(p, rows)) return E3_ERR_WORKSPACE_TOO_SMALL;
+    return comp_tpb64(p, x, y, w, dz, dx, dy, dw, ws, rows, reinterpret_cast<hipStream_t>(stream));
+  }
   const VariantOps& v = (*kVariants[p->variant]());
   if (ws_bytes < v.tpws64(p, rows)) return E3_ERR_WORKSPACE_TOO_SMALL;
   return v.tpb64(p, x, y, w, dz, dx, dy, dw, ws, rows, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_workspace_size_f64(const e3_plan* p, const e3_graph* g, size_t* bwd_bytes) {
-  e3_status s = check_plan(p);
+  e3_status s = check_f64(p);
   if (s != E3_OK) return s;
   if (!g || !bwd_bytes) return E3_ERR_INVALID_ARG;
-  const Ws w = (*kVariants[p->variant]()).ws64(p, g);
+  const Ws w = p->variant >= 0 ? (*kVariants[p->variant]()).ws64(p, g) : comp_ws64(p, g);
   *bwd_bytes = w.t_bytes + w.dy_bytes;
   return E3_OK;
 }
 
 e3_status e3_conv_fwd_f64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
                           double* m, e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_f64(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !m || !aligned16(x) || !aligned16(m))) return E3_ERR_INVALID_ARG;
   if (g->n_edges > 0 && (!vec || !s || !aligned16(s))) return E3_ERR_INVALID_ARG;
+  if (p->variant < 0) return comp_fwd64(p, g, x, vec, s, m, reinterpret_cast<hipStream_t>(stream));
   return (*kVariants[p->variant]()).fwd64(p, g, x, vec, s, m, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_bwd_f64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
                           const double* dm, double* dx, double* dvec, double* ds, void* ws, size_t ws_bytes,
                           e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_f64(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
     return E3_ERR_INVALID_ARG;
   if (g->n_edges > 0 && (!vec || !s || !ds || !dvec || !aligned16(s) || !aligned16(ds))) return E3_ERR_INVALID_ARG;
-  const VariantOps& v = (*kVariants[p->variant]());
-  const Ws w = v.ws64(p, g);
+  const Ws w = p->variant >= 0 ? (*kVariants[p->variant]()).ws64(p, g) : comp_ws64(p, g);
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
-  return v.bwd64(p, g, x, vec, s, dm, dx, dvec, ds, ws, reinterpret_cast<hipStream_t>(stream));
+  if (p->variant < 0)
+    return comp_bwd64(p, g, x, vec, s, dm, dx, dvec, ds, ws, reinterpret_cast<hipStream_t>(stream));
+  return (*kVariants[p->variant]()).bwd64(p, g, x, vec, s, dm, dx, dvec, ds, ws,
+                                          reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -1299,7 +1299,7 @@ constexpr int kBatch64 = 8;  // rows / edges whose pre-contraction is staged per
 template <class V>
 __global__ __launch_bounds__(kWave) void k_tp64(const double* __restrict__ x, const double* __restrict__ y,
                                                 const double* __restrict__ w, double* __restrict__ z, int64_t rows,
-                                                int C, int nslab) {
+                                                int C, int nslab, TpStr ts) {
   using F = typename V::TP;
   __shared__ __align__(32) double sA[kBatch64 * F::NA];
   const int lane = threadIdx.x;
@@ -1322,9 +1322,9 @@ __global__ __launch_bounds__(kWave) void k_tp64(const double* __restrict__ x, co
   for (int j = 0; j < n; ++j) {
     const int64_t r = r0 + j;
     double xv[F::NXR][1], wv[F::NPATH][1];
-    const RowBuf64 xb = row_buf64(x + r * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
-    const RowBuf64 wb = row_buf64(w + r * V::NP * C, (int64_t)V::NP * C * 8, q, C);
-    const RowBuf64 zb = row_buf64(z + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+    const RowBuf64 xb = row_buf64(x + r * x_rows<V>(ts) * C, (int64_t)V::D_IN * C * 8, q, C);
+    const RowBuf64 wb = row_buf64(w + r * p_rows<V>(ts) * C, (int64_t)V::NP * C * 8, q, C);
+    const RowBuf64 zb = row_buf64(z + r * o_rows<V>(ts) * C, (int64_t)V::D_OUT * C * 8, q, C);
 #pragma unroll
     for (int i = 0; i < F::NXR; ++i) bld64(xb, F::XROW[i], xv[i]);
 #pragma unroll
@@ -1347,6 +1347,7 @@ struct Tpb64Args {
   int64_t rows;
   int C;
   int nslab;
+  int xr, pr, orr, ng, g0;  // a single-block kind inside a larger layout (as in ConvArgs)
 };
 
 template <class V, int G>
@@ -1373,9 +1374,9 @@ __device__ __forceinline__ void tpb64_task(const Tpb64Args& a, int64_t r0, int s
 #pragma unroll
     for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0;
     if (act) {
-      const RowBuf64 xb = row_buf64(a.x + r * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
-      const RowBuf64 wb = row_buf64(a.w + r * V::NP * C, (int64_t)V::NP * C * 8, q, C);
-      const RowBuf64 zb = row_buf64(a.dz + r * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+      const RowBuf64 xb = row_buf64(a.x + r * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 8, q, C);
+      const RowBuf64 wb = row_buf64(a.w + r * p_rows<V>(a) * C, (int64_t)V::NP * C * 8, q, C);
+      const RowBuf64 zb = row_buf64(a.dz + r * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 8, q, C);
       double xv[B::NXR][1], wv[B::NPATH][1], dzv[B::NROW][1], t[B::NXR][1], Yv[V::D_SH];
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) bld64(xb, B::XROW[i], xv[i]), t[i][0] = 0.0;
@@ -1385,17 +1386,17 @@ __device__ __forceinline__ void tpb64_task(const Tpb64Args& a, int64_t r0, int s
       for (int i = 0; i < B::NROW; ++i) bld64(zb, B::OROW[i], dzv[i]);
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
-      const RowBuf64 dwb = row_buf64(a.dw + r * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+      const RowBuf64 dwb = row_buf64(a.dw + r * p_rows<V>(a) * C, (int64_t)V::NP * C * 8, q, C);
       auto st = [&](int pl, const double (&v)[1]) { bst64(dwb, B::PATH[pl], v); };
       B::template edge<false, 1>(sA + j * B::NA, Yv, xv, wv, dzv, t, dyl, st);
-      const RowBuf64 dxb = row_buf64(a.dx + r * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+      const RowBuf64 dxb = row_buf64(a.dx + r * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 8, q, C);
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) bst64(dxb, B::XROW[i], t[i]);
     }
 #pragma unroll
     for (int i = 0; i < V::D_SH; ++i) {
       const double tot = wave_sum64(dyl[i]);
-      if (lane == 0) a.DY[((r * V::NBG + G) * a.nslab + sl) * 16 + i] = tot;
+      if (lane == 0) a.DY[(dy_group<V, G>(a, r) * a.nslab + sl) * 16 + i] = tot;
     }
   }
 }
@@ -1464,8 +1465,8 @@ __device__ __forceinline__ void fwd64_task(const ConvArgs& a, const double* x, c
       for (int j = 0; j < n; ++j) {
         const int64_t e = __builtin_amdgcn_readlane(my_e, j);
         const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
-        const RowBuf64 xb = row_buf64(x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
-        const RowBuf64 sb = row_buf64(s + e * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+        const RowBuf64 xb = row_buf64(x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 8, q, C);
+        const RowBuf64 sb = row_buf64(s + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 8, q, C);
         double xv[F::NXR][1], sv[F::NPATH][1];
 #pragma unroll
         for (int i = 0; i < F::NXR; ++i) bld64(xb, F::XROW[i], xv[i]);
@@ -1477,7 +1478,7 @@ __device__ __forceinline__ void fwd64_task(const ConvArgs& a, const double* x, c
     __syncthreads();
   }
   if (act) {
-    const RowBuf64 mb = row_buf64(m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+    const RowBuf64 mb = row_buf64(m + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 8, q, C);
 #pragma unroll
     for (int i = 0; i < F::NROW; ++i) bst64(mb, F::OROW[i], acc[i]);
   }
@@ -1529,7 +1530,7 @@ __device__ __forceinline__ void bwd64_task(const ConvArgs& a, const Conv64Out& o
   if (e0 == e1) return;
   double dmv[B::NROW][1];
   if (act) {
-    const RowBuf64 db = row_buf64(o.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 8, q, C);
+    const RowBuf64 db = row_buf64(o.dm + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 8, q, C);
 #pragma unroll
     for (int i = 0; i < B::NROW; ++i) bld64(db, B::OROW[i], dmv[i]);
   }
@@ -1556,8 +1557,8 @@ __device__ __forceinline__ void bwd64_task(const ConvArgs& a, const Conv64Out& o
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) dyl[i] = 0.0;
       if (act) {
-        const RowBuf64 xb = row_buf64(o.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
-        const RowBuf64 sb = row_buf64(o.s + e * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+        const RowBuf64 xb = row_buf64(o.x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 8, q, C);
+        const RowBuf64 sb = row_buf64(o.s + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 8, q, C);
         double xv[B::NXR][1], sv[B::NPATH][1], t[B::NXR][1], Yv[V::D_SH];
 #pragma unroll
         for (int i = 0; i < B::NXR; ++i) bld64(xb, B::XROW[i], xv[i]), t[i][0] = 0.0;
@@ -1565,17 +1566,17 @@ __device__ __forceinline__ void bwd64_task(const ConvArgs& a, const Conv64Out& o
         for (int i = 0; i < B::NPATH; ++i) bld64(sb, B::PATH[i], sv[i]);
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
-        const RowBuf64 dsb = row_buf64(o.ds + e * V::NP * C, (int64_t)V::NP * C * 8, q, C);
+        const RowBuf64 dsb = row_buf64(o.ds + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 8, q, C);
         auto st = [&](int pl, const double (&v)[1]) { bst64(dsb, B::PATH[pl], v); };
         B::template edge<false, 1>(sA + j * B::NA, Yv, xv, sv, dmv, t, dyl, st);
-        const RowBuf64 Tb = row_buf64(o.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 8, q, C);
+        const RowBuf64 Tb = row_buf64(o.T + slot * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 8, q, C);
 #pragma unroll
         for (int i = 0; i < B::NXR; ++i) bst64(Tb, B::XROW[i], t[i]);
       }
 #pragma unroll
       for (int i = 0; i < V::D_SH; ++i) {
         const double tot = wave_sum64(dyl[i]);
-        if (lane == 0) o.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + i] = tot;
+        if (lane == 0) o.DY[(dy_group<V, G>(a, eb + j) * a.nslab + sl) * 16 + i] = tot;
       }
     }
     __syncthreads();
@@ -2195,6 +2196,17 @@ e3_status rec_fwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float
 e3_status rec_bwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float* x, const float* vec,
                   const float* y, const float* s, const float* dm, float* dx, float* dvec, float* dy, float* ds,
                   int accum, void* ws, hipStream_t st);
+// the composed path's float64 builds
+Ws comp_ws64(const e3_plan* p, const e3_graph* g);
+size_t comp_tp_ws64(const e3_plan* p, int64_t rows);
+e3_status comp_fwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                     double* m, hipStream_t st);
+e3_status comp_bwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                     const double* dm, double* dx, double* dvec, double* ds, void* ws, hipStream_t st);
+e3_status comp_tp64(const e3_plan* p, const double* x, const double* y, const double* w, double* z, int64_t rows,
+                    hipStream_t st);
+e3_status comp_tpb64(const e3_plan* p, const double* x, const double* y, const double* w, const double* dz,
+                     double* dx, double* dy, double* dw, void* ws, int64_t rows, hipStream_t st);
 
 // Scratch of the radial backward: T and DY as in the plain backward, then ds
 // by edge id (all E rows when any edge is live), the dW partials of each row
@@ -2262,6 +2274,15 @@ struct KindOps {
                   const KindCall&, hipStream_t);
   e3_status (*tpb)(const e3_plan*, const float* x, const float* y, const float* w, const float* dz, float* dx,
                    float* dw, float* DY, int64_t rows, const KindCall&, hipStream_t);
+  // float64 builds (one channel per lane)
+  e3_status (*fwd64)(const e3_plan*, const e3_graph*, const double* x, const double* vec, const double* s,
+                     double* m, const KindCall&, hipStream_t);
+  e3_status (*bwd64)(const e3_plan*, const e3_graph*, const double* x, const double* vec, const double* s,
+                     const double* dm, double* T, double* DY, double* ds, const KindCall&, hipStream_t);
+  e3_status (*tp64)(const e3_plan*, const double* x, const double* y, const double* w, double* z, int64_t rows,
+                    const KindCall&, hipStream_t);
+  e3_status (*tpb64)(const e3_plan*, const double* x, const double* y, const double* w, const double* dz,
+                     double* dx, double* dw, double* DY, int64_t rows, const KindCall&, hipStream_t);
 };
 
 namespace {
@@ -2630,7 +2651,8 @@ e3_status run_tp64(const e3_plan* p, const double* x, const double* y, const dou
   const int64_t grid = tile_grid(false, rows, kBatch64, nsl);
   if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
   TimedLaunch t_("tp_fwd_f64", st);
-  hipLaunchKernelGGL((k_tp64<V>), dim3((unsigned)grid), dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, nsl);
+  hipLaunchKernelGGL((k_tp64<V>), dim3((unsigned)grid), dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, nsl,
+                     TpStr{});
   E3_HIP(hipGetLastError());
   return E3_OK;
 }
@@ -2779,13 +2801,71 @@ e3_status kind_tpb(const e3_plan* p, const float* x, const float* y, const float
   return E3_OK;
 }
 
+template <class V>
+e3_status kind_fwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                     double* m, const KindCall& kc, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.nslab = nslab64(p);
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
+  TimedLaunch t_("kind_fwd_f64", st);
+  hipLaunchKernelGGL((k_conv_fwd64<V>), dim3(grid), dim3(kWave), 0, st, a, x, vec, s, m);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_bwd64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
+                     const double* dm, double* T, double* DY, double* ds, const KindCall& kc, hipStream_t st) {
+  if (g->n_live == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.nslab = nslab64(p);
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr, a.ng = kc.ng, a.g0 = kc.g0;
+  Conv64Out o{x, vec, s, dm, ds, T, DY};
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
+  TimedLaunch t_("kind_bwd_f64", st);
+  hipLaunchKernelGGL((k_conv_bwd64<V>), dim3(grid), dim3(kWave), 0, st, a, o);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_tp64(const e3_plan* p, const double* x, const double* y, const double* w, double* z, int64_t rows,
+                    const KindCall& kc, hipStream_t st) {
+  if (rows == 0) return E3_OK;
+  const int nsl = nslab64(p);
+  const int64_t grid = tile_grid(false, rows, kBatch64, nsl);
+  if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
+  TimedLaunch t_("kind_tp_f64", st);
+  hipLaunchKernelGGL((k_tp64<V>), dim3((unsigned)grid), dim3(kWave), 0, st, x, y, w, z, rows, p->lay.C, nsl,
+                     TpStr{kc.xr, kc.pr, kc.orr});
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_tpb64(const e3_plan* p, const double* x, const double* y, const double* w, const double* dz,
+                     double* dx, double* dw, double* DY, int64_t rows, const KindCall& kc, hipStream_t st) {
+  if (rows == 0) return E3_OK;
+  const int nsl = nslab64(p);
+  Tpb64Args a{x, y, w, dz, dx, dw, DY, rows, p->lay.C, nsl, kc.xr, kc.pr, kc.orr, kc.ng, kc.g0};
+  const int64_t grid = tile_grid(false, rows, kBatch64, V::NBG * nsl);
+  if (grid > 0x7fffffff) return E3_ERR_INVALID_ARG;
+  TimedLaunch t_("kind_tp_bwd_f64", st);
+  hipLaunchKernelGGL((k_tp_bwd64<V>), dim3((unsigned)grid), dim3(kWave), 0, st, a);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
 }  // namespace
 
 // One kind's entry in the composed path's table (constant-initialised).
 #define E3_KIND_OPS(V)                                                                                  \
   KindOps{e3gen::V::SIG, e3gen::V::D_IN, e3gen::V::D_SH, e3gen::V::D_OUT, e3gen::V::NP, e3gen::V::LSH, \
           e3gen::V::NBG, &kind_fwd<e3gen::V>, &kind_bwd<e3gen::V>, &kind_tp<e3gen::V>,                 \
-          &kind_tpb<e3gen::V>}
+          &kind_tpb<e3gen::V>, &kind_fwd64<e3gen::V>, &kind_bwd64<e3gen::V>, &kind_tp64<e3gen::V>,     \
+          &kind_tpb64<e3gen::V>}
 
 // One variant's entry in the core unit's table (constant-initialised).
 #define E3_VARIANT_OPS(V)                                                                                    \

@@ -19,6 +19,8 @@ from gpu_util import TOL, layout_of, oracle_bwd_rows, oracle_fwd_rows, rel_l2, t
 
 pytestmark = pytest.mark.gpu
 
+TOL64 = 1e-12   # float64 builds against the float64 oracle (the bar of the compiled float64 tests)
+
 
 @pytest.fixture(scope="module")
 def e3():
@@ -351,3 +353,59 @@ def test_generic_paths_in_captured_graph(e3):
             assert torch.equal(a, b), it
         _ = e3.conv_fwd(cp, G, x, vs, s)   # eager work between replays
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad,rows", [
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 50, 700, 3, 37),
+    ("8x0o+8x1o", 1, 1, "natural", 40, 500, -1, 20),                # a block with no path
+    ("68x1o+68x2o", 3, 2, "all", 30, 400, -1, 11),                  # a ragged second slab
+    ("64x0e+64x1o+64x2e+64x3o", 3, 3, "all", 40, 600, 4, 9),        # a compiled layout, forced
+])
+def test_composed_float64(e3, irreps, lsh, lout, parity, n, e, pad, rows):
+    """The float64 builds of the convolution and the tensor product on the
+    composed path against the oracle on the same float64 inputs (bar 1e-12),
+    with bitwise repeats."""
+    import torch
+    _say("composed float64", irreps, lsh, lout, parity, n, e, pad, rows)
+    rng = np.random.default_rng(48)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = _plan(e3, irreps, lsh, lout, parity, "composed")
+    snd, rcv, _ = _random_graph(rng, n, e)
+    vec = rng.standard_normal((e, 3)) * 2.0
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C))
+    s = rng.standard_normal((e, lay.n_paths, C))
+    dm = rng.standard_normal((n, lay.d_out, C))
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    d64 = [torch.from_numpy(a).to("cuda") for a in (x, vec, s, dm)]
+    m = e3.conv_fwd_f64(plan, G, *d64[:3])
+    dx, dvec, ds = e3.conv_bwd_f64(plan, G, *d64)
+    torch.cuda.synchronize()
+    ref_m = oconv.conv_fwd(lay, x, vec, s, snd, rcv, n, pad_node=pad).numpy()
+    ref = oconv.conv_bwd(lay, x, vec, s, dm, snd, rcv, n, pad_node=pad)
+    errs = dict(m=rel_l2(to_np(m), ref_m), dx=rel_l2(to_np(dx), ref["dx"].numpy()),
+                ds=rel_l2(to_np(ds), ref["ds"].numpy()), dvec=rel_l2(to_np(dvec), ref["dvec"].numpy()))
+    print("float64 conv rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL64, (k, v)
+    if pad >= 0:
+        dead = (snd == pad) | (rcv == pad)
+        assert np.all(to_np(ds)[dead] == 0) and np.all(to_np(dvec)[dead] == 0)
+    again = e3.conv_bwd_f64(plan, G, *d64)
+    for a, b in zip((dx, dvec, ds), again):
+        assert torch.equal(a, b)
+    g = rng.standard_normal((rows, 3))
+    y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True))
+    tx = rng.standard_normal((rows, lay.d_in, C))
+    tw = rng.standard_normal((rows, lay.n_paths, C))
+    tdz = rng.standard_normal((rows, lay.d_out, C))
+    dev = [torch.from_numpy(np.ascontiguousarray(a)).to("cuda") for a in (tx, y, tw, tdz)]
+    z = e3.tp_fwd_f64(plan, *dev[:3])
+    tdx, tdy, tdw = e3.tp_bwd_f64(plan, *dev)
+    torch.cuda.synchronize()
+    terrs = dict(z=rel_l2(to_np(z), otp.tp(lay, tx, y, tw).numpy()))
+    for k, a, r in zip(("dx", "dy", "dw"), (tdx, tdy, tdw), otp.tp_bwd(lay, tx, y, tw, tdz)):
+        terrs[k] = rel_l2(to_np(a), r.numpy())
+    print("float64 tp rel-L2", terrs, flush=True)
+    for k, v in terrs.items():
+        assert v < TOL64, (k, v)
