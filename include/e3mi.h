@@ -115,8 +115,8 @@ typedef struct {
  * e3_tp_fwd / e3_tp_bwd / e3_tp_workspace_size, e3_conv_fwd / e3_conv_bwd /
  * e3_conv_workspace_size / e3_conv_bwd_noalloc, e3_conv_fwd_y /
  * e3_conv_bwd_y and e3_conv_bwd2, with the same semantics (deterministic,
- * atomics-free); the composed path also serves the float64 builds; the
- * fused-radial entry points need a compiled variant.  Otherwise (a larger degree; the record path without a device
+ * atomics-free); the composed path also serves the float64 builds and the
+ * fused radial weights (the record path has neither).  Otherwise (a larger degree; the record path without a device
  * at creation) the plan is still created (info.supported == 0): its tables
  * can be queried, and the compute entry points return E3_ERR_UNSUPPORTED. */
 e3_status e3_plan_create(const char* irreps_x, int lmax_sh, int lmax_out, unsigned flags,

@@ -1192,3 +1192,94 @@ e3_status comp_tpb64(const e3_plan* p, const double* x, const double* y, const d
   E3_HIP(hipGetLastError());
   return E3_OK;
 }
+
+// ------------------------------------------------------------ composed path, fused radial weights
+RadWs comp_rad_ws(const e3_plan* p, const e3_graph* g, int K) {
+  return rad_ws_of(p, g, K, (int)p->lay.paths.size(), comp_ws(p, g));
+}
+
+e3_status comp_fwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                       const float* W, int K, float* m, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  const int64_t C = p->lay.C;
+  for (const auto& b : p->kblocks) {
+    const KindOps& Kd = *kKinds[b.kind]();
+    e3_status r = Kd.rfwd(p, g, x + b.x_off * C, vec, h, W + b.k0 * C, K, m + b.o_off * C, comp_call(p, b.g0), st);
+    if (r != E3_OK) return r;
+  }
+  return E3_OK;
+}
+
+e3_status comp_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                       const float* W, int K, const float* dm, float* dx, float* dvec, float* dh, float* dW,
+                       void* ws, hipStream_t st) {
+  const int64_t C = p->lay.C, D_in = p->lay.d_in;
+  const RadWs w = comp_rad_ws(p, g, K);
+  char* base = reinterpret_cast<char*>(ws);
+  float* T = reinterpret_cast<float*>(base);
+  float* DY = reinterpret_cast<float*>(base + w.t);
+  float* DS = reinterpret_cast<float*>(base + w.t + w.dy);
+  float* dWp = reinterpret_cast<float*>(base + w.t + w.dy + w.ds);
+  float* DHp = reinterpret_cast<float*>(base + w.t + w.dy + w.ds + w.dwp);
+  const int nparts = p->kng * p->nslab_b;
+  e3_status r;
+  for (const auto& b : p->kblocks) {
+    const KindOps& Kd = *kKinds[b.kind]();
+    if ((r = Kd.rbwd(p, g, x + b.x_off * C, vec, h, W + b.k0 * C, K, dm + b.o_off * C, T + b.x_off * C, DY,
+                     DS + b.k0 * C, comp_call(p, b.g0), st)) != E3_OK)
+      return r;
+  }
+  if (g->n_nodes > 0) {
+    for (const auto& z : p->pathless)
+      if ((r = comp_zero_rows(T, g->n_live, D_in * C, z.first * C, z.second * C, st)) != E3_OK) return r;
+    TimedLaunch t_("conv_bwd_dx", st);
+    const int flat4 = (int)(D_in * C / 4);
+    const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
+    const int chunk = (int)((g->n_nodes + kXcd - 1) / kXcd);
+    hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * chunk * nsl)), dim3(kWave), 0, st, T, dx, g->rowptr_s,
+                       (int)g->n_nodes, chunk, flat4, nsl, 0);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_live > 0) {
+    if ((r = finish_bwd(p, g, g->n_live, vec, DY, dvec, nullptr, nullptr, nparts, 0, st)) != E3_OK) return r;
+    if (g->n_pad > 0) {
+      // the ds rows of padding edges enter the gradient sums: clear them
+      TimedLaunch t_("rad_pad_ds", st);
+      hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, DS,
+                         (int64_t)w.pc4 * 4, dvec, (int64_t)3);
+      E3_HIP(hipGetLastError());
+    }
+    const int64_t E = g->n_edges;
+    {
+      TimedLaunch t_("rad_grad", st);
+      const dim3 grid((unsigned)((int64_t)w.nchunk * w.nsl4));
+      if (K <= 8)
+        hipLaunchKernelGGL(k_rad_grad<2>, grid, dim3(kWave), 0, st, DS, h, W, dWp, DHp, E, w.pc4, K, w.nsl4,
+                           w.rows_per);
+      else
+        hipLaunchKernelGGL(k_rad_grad<4>, grid, dim3(kWave), 0, st, DS, h, W, dWp, DHp, E, w.pc4, K, w.nsl4,
+                           w.rows_per);
+      E3_HIP(hipGetLastError());
+    }
+    {
+      TimedLaunch t_("rad_dh_sum", st);
+      hipLaunchKernelGGL(k_rad_dh_sum, dim3(blocks_for(E * w.nv, 256)), dim3(256), 0, st, DHp, dh, E, K, w.nsl4,
+                         w.nv);
+      E3_HIP(hipGetLastError());
+    }
+  }
+  {
+    const int64_t n = (int64_t)K * w.pc4 * 4;
+    TimedLaunch t_("rad_dw_sum", st);
+    hipLaunchKernelGGL(k_rad_dw_sum, dim3(blocks_for(n, kWave)), dim3(kWave * kDwSplit), 0, st, dWp, dW, n,
+                       w.nchunk);
+    E3_HIP(hipGetLastError());
+  }
+  if (g->n_pad > 0) {
+    TimedLaunch t_("conv_bwd_pad", st);
+    hipLaunchKernelGGL(k_zero_pad, dim3((unsigned)g->n_pad), dim3(256), 0, st, g->eid_r + g->n_live, g->n_pad, dh,
+                       (int64_t)K, dvec, (int64_t)3);
+    E3_HIP(hipGetLastError());
+  }
+  return E3_OK;
+}

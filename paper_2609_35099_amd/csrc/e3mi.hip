@@ -737,11 +737,12 @@ e3_status check_any(const e3_plan* p) {
   return p->variant >= 0 ? E3_OK : rec_check(p);
 }
 
-// A compiled variant or the composed path (the float64 builds).
-e3_status check_f64(const e3_plan* p) {
+// A compiled variant or the composed path (the float64 builds and the fused
+// radial weights, which the record path does not have).
+e3_status check_composable(const e3_plan* p) {
   if (!p) return E3_ERR_INVALID_ARG;
   if (p->variant >= 0 || p->composed) return E3_OK;
-  g_last_error = p->rec ? "the float64 builds need a compiled variant or the composed path" : p->no_rec_reason;
+  g_last_error = p->rec ? "this entry point needs a compiled variant or the composed path" : p->no_rec_reason;
   return E3_ERR_UNSUPPORTED;
 }
 
@@ -1197,7 +1198,7 @@ e3_status e3_conv_bwd(const e3_plan* p, const e3_graph* g, const float* x, const
 // ---- float64 builds
 e3_status e3_tp_fwd_f64(const e3_plan* p, const double* x, const double* y, const double* w, double* z,
                         int64_t rows, e3_stream stream) {
-  e3_status s = check_f64(p);
+  e3_status s = check_composable(p);
   if (s != E3_OK) return s;
   if (rows < 0) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
@@ -1207,7 +1208,7 @@ e3_status e3_tp_fwd_f64(const e3_plan* p, const double* x, const double* y, cons
 }
 
 e3_status e3_tp_workspace_size_f64(const e3_plan* p, int64_t rows, size_t* bwd_bytes) {
-  e3_status s = check_f64(p);
+  e3_status s = check_composable(p);
   if (s != E3_OK) return s;
   if (rows < 0 || !bwd_bytes) return E3_ERR_INVALID_ARG;
   *bwd_bytes = p->variant >= 0 ? (*kVariants[p->variant]()).tpws64(p, rows) : comp_tp_ws64(p, rows);
@@ -1217,7 +1218,7 @@ e3_status e3_tp_workspace_size_f64(const e3_plan* p, int64_t rows, size_t* bwd_b
 e3_status e3_tp_bwd_f64(const e3_plan* p, const double* x, const double* y, const double* w, const double* dz,
                         double* dx, double* dy, double* dw, void* ws, size_t ws_bytes, int64_t rows,
                         e3_stream stream) {
-  e3_status s = check_f64(p);
+  e3_status s = check_composable(p);
   if (s != E3_OK) return s;
   if (rows < 0) return E3_ERR_INVALID_ARG;
   if (rows == 0) return E3_OK;
@@ -1234,7 +1235,7 @@ e3_status e3_tp_bwd_f64(const e3_plan* p, const double* x, const double* y, cons
 }
 
 e3_status e3_conv_workspace_size_f64(const e3_plan* p, const e3_graph* g, size_t* bwd_bytes) {
-  e3_status s = check_f64(p);
+  e3_status s = check_composable(p);
   if (s != E3_OK) return s;
   if (!g || !bwd_bytes) return E3_ERR_INVALID_ARG;
   const Ws w = p->variant >= 0 ? (*kVariants[p->variant]()).ws64(p, g) : comp_ws64(p, g);
@@ -1244,7 +1245,7 @@ e3_status e3_conv_workspace_size_f64(const e3_plan* p, const e3_graph* g, size_t
 
 e3_status e3_conv_fwd_f64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
                           double* m, e3_stream stream) {
-  e3_status st = check_f64(p);
+  e3_status st = check_composable(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !m || !aligned16(x) || !aligned16(m))) return E3_ERR_INVALID_ARG;
@@ -1256,7 +1257,7 @@ e3_status e3_conv_fwd_f64(const e3_plan* p, const e3_graph* g, const double* x, 
 e3_status e3_conv_bwd_f64(const e3_plan* p, const e3_graph* g, const double* x, const double* vec, const double* s,
                           const double* dm, double* dx, double* dvec, double* ds, void* ws, size_t ws_bytes,
                           e3_stream stream) {
-  e3_status st = check_f64(p);
+  e3_status st = check_composable(p);
   if (st != E3_OK) return st;
   if (!g) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
@@ -1341,37 +1342,40 @@ e3_status e3_conv_bwd_noalloc(const e3_plan* p, const e3_graph* g, const float* 
 }
 
 e3_status e3_conv_radial_workspace_size(const e3_plan* p, const e3_graph* g, int K, size_t* bwd_bytes) {
-  e3_status st = check_plan(p);
+  e3_status st = check_composable(p);
   if (st != E3_OK) return st;
   if (!g || !bwd_bytes || K < 1 || K > kRadKMax) return E3_ERR_INVALID_ARG;
-  *bwd_bytes = (*kVariants[p->variant]()).rws(p, g, K).total();
+  *bwd_bytes = p->variant >= 0 ? (*kVariants[p->variant]()).rws(p, g, K).total() : comp_rad_ws(p, g, K).total();
   return E3_OK;
 }
 
 e3_status e3_conv_fwd_radial(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
                              const float* W, int K, float* m, e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_composable(p);
   if (st != E3_OK) return st;
   if (!g || K < 1 || K > kRadKMax) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!m || !aligned16(m) || !x || !aligned16(x) || !W || !aligned16(W))) return E3_ERR_INVALID_ARG;
   if (g->n_live > 0 && (!vec || !h)) return E3_ERR_INVALID_ARG;
+  if (p->variant < 0) return comp_fwd_rad(p, g, x, vec, h, W, K, m, reinterpret_cast<hipStream_t>(stream));
   return (*kVariants[p->variant]()).rfwd(p, g, x, vec, h, W, K, m, reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_bwd_radial(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
                              const float* W, int K, const float* dm, float* dx, float* dvec, float* dh, float* dW,
                              void* ws, size_t ws_bytes, e3_stream stream) {
-  e3_status st = check_plan(p);
+  e3_status st = check_composable(p);
   if (st != E3_OK) return st;
   if (!g || K < 1 || K > kRadKMax || !W || !aligned16(W) || !dW) return E3_ERR_INVALID_ARG;
   if (g->n_nodes > 0 && (!x || !dm || !dx || !aligned16(x) || !aligned16(dm) || !aligned16(dx)))
     return E3_ERR_INVALID_ARG;
   if (g->n_edges > 0 && (!vec || !h || !dh || !dvec)) return E3_ERR_INVALID_ARG;
-  const VariantOps& v = (*kVariants[p->variant]());
-  const RadWs w = v.rws(p, g, K);
+  const RadWs w = p->variant >= 0 ? (*kVariants[p->variant]()).rws(p, g, K) : comp_rad_ws(p, g, K);
   if (w.total() > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.total()) return E3_ERR_WORKSPACE_TOO_SMALL;
-  return v.rbwd(p, g, x, vec, h, W, K, dm, dx, dvec, dh, dW, ws, reinterpret_cast<hipStream_t>(stream));
+  if (p->variant < 0)
+    return comp_bwd_rad(p, g, x, vec, h, W, K, dm, dx, dvec, dh, dW, ws, reinterpret_cast<hipStream_t>(stream));
+  return (*kVariants[p->variant]()).rbwd(p, g, x, vec, h, W, K, dm, dx, dvec, dh, dW, ws,
+                                         reinterpret_cast<hipStream_t>(stream));
 }
 
 e3_status e3_conv_fwd_y(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,

@@ -1669,8 +1669,8 @@ __device__ __forceinline__ void radial_quad_reg(const float (&wr)[KR][NPATH], co
 }
 
 template <class V, int NPATH>
-__device__ __forceinline__ void radial_quad(const RowBuf& wb, const float* sH, int q4, int K, const int (&path)[NPATH],
-                                            f4v (&s4)[NPATH]) {
+__device__ __forceinline__ void radial_quad(const RowBuf& wb, int wrows, const float* sH, int q4, int K,
+                                            const int (&path)[NPATH], f4v (&s4)[NPATH]) {
   const int lane = threadIdx.x;
 #pragma unroll
   for (int p = 0; p < NPATH; ++p) s4[p] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
@@ -1678,10 +1678,19 @@ __device__ __forceinline__ void radial_quad(const RowBuf& wb, const float* sH, i
     const float hv = sH[(q4 + (lane & 3)) * kRadKMax + j];
     float wv[NPATH][1];
 #pragma unroll
-    for (int p = 0; p < NPATH; ++p) bld<1>(wb, j * V::NP + path[p], wv[p]);
+    for (int p = 0; p < NPATH; ++p) bld<1>(wb, j * wrows + path[p], wv[p]);
 #pragma unroll
     for (int p = 0; p < NPATH; ++p) s4[p] = __builtin_amdgcn_mfma_f32_4x4x1f32(hv, wv[p][0], s4[p], 0, 0, 0);
   }
+}
+
+// Bytes of W [K, P, C] a kernel may read from its base: all of it for a
+// compiled layout; for a single-block kind (base at its first path, row
+// stride P) the K row sets up to its own last path.
+template <class V>
+__device__ __forceinline__ int64_t w_bytes(const ConvArgs& a) {
+  if constexpr (V::RT) return ((int64_t)(a.K - 1) * a.pr + V::NP) * a.C * 4;
+  else return (int64_t)a.K * V::NP * a.C * 4;
 }
 
 // Lane j < n of the batch stages h of its edge (rows past n read as zero).
@@ -1705,7 +1714,7 @@ __device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, f
   float acc[F::NROW][1];
 #pragma unroll
   for (int i = 0; i < F::NROW; ++i) acc[i][0] = 0.0f;
-  const RowBuf wb = row_buf(a.W, (int64_t)a.K * V::NP * C * 4, q, C);
+  const RowBuf wb = row_buf(a.W, w_bytes<V>(a), q, C);
   float wr[KR > 0 ? KR : 1][F::NPATH];
   if constexpr (KR > 0) {
 #pragma unroll
@@ -1713,7 +1722,7 @@ __device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, f
 #pragma unroll
       for (int p = 0; p < F::NPATH; ++p) {
         float v[1] = {0.0f};
-        if (j < a.K) bld<1>(wb, j * V::NP + F::PATH[p], v);
+        if (j < a.K) bld<1>(wb, j * p_rows<V>(a) + F::PATH[p], v);
         wr[j][p] = v[0];
       }
   }
@@ -1735,7 +1744,7 @@ __device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, f
     auto load_x = [&](int j, float (&xv)[F::NXR][1]) {
       if (!act) return;
       const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
-      const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf xr = row_buf(a.x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < F::NXR; ++i) bld<1>(xr, F::XROW[i], xv[i]);
     };
@@ -1745,7 +1754,7 @@ __device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, f
       if constexpr (KR > 0)
         radial_quad_reg<V, F::NPATH, (KR > 0 ? KR : 1)>(wr, sH, q4, s4);
       else
-        radial_quad<V, F::NPATH>(wb, sH, q4, a.K, F::PATH, s4);
+        radial_quad<V, F::NPATH>(wb, p_rows<V>(a), sH, q4, a.K, F::PATH, s4);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int j = q4 + i;
@@ -1766,7 +1775,7 @@ __device__ __forceinline__ void fwd_rad_task(const ConvArgs& a, int b, int sl, f
     __syncthreads();
   }
   if (act) {
-    const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+    const RowBuf mb = row_buf(a.m + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
     for (int i = 0; i < F::NROW; ++i) bst<1, kST>(mb, F::OROW[i], acc[i]);
   }
@@ -1807,11 +1816,11 @@ __device__ __forceinline__ void bwd_rad_task(const ConvArgs& a, int b, int sl, f
   if (e0 == e1) return;
   float dmv[B::NROW][1];
   if (act) {
-    const RowBuf db = row_buf(a.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+    const RowBuf db = row_buf(a.dm + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
     for (int i = 0; i < B::NROW; ++i) bld<1>(db, B::OROW[i], dmv[i]);
   }
-  const RowBuf wb = row_buf(a.W, (int64_t)a.K * V::NP * C * 4, q, C);
+  const RowBuf wb = row_buf(a.W, w_bytes<V>(a), q, C);
   for (int eb = e0; eb < e1; eb += kEdgeBatch) {
     const int n = imin(kEdgeBatch, e1 - eb);
     int my_e = 0, my_src = 0, my_slot = 0;
@@ -1833,7 +1842,7 @@ __device__ __forceinline__ void bwd_rad_task(const ConvArgs& a, int b, int sl, f
     auto load_x = [&](int j, float (&xv)[B::NXR][1]) {
       if (!act) return;
       const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
-      const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf xr = row_buf(a.x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) bld<1>(xr, B::XROW[i], xv[i]);
     };
@@ -1849,7 +1858,7 @@ __device__ __forceinline__ void bwd_rad_task(const ConvArgs& a, int b, int sl, f
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i];
         const int64_t e = __builtin_amdgcn_readlane(my_e, j);
-        const RowBuf dsb = row_buf(a.ds + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        const RowBuf dsb = row_buf(a.ds + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
         auto st = [&](int pl, const float (&v)[1]) { bst<1, kST>(dsb, B::PATH[pl], v); };
         float dyl[V::D_SH];
 #pragma unroll
@@ -1857,17 +1866,17 @@ __device__ __forceinline__ void bwd_rad_task(const ConvArgs& a, int b, int sl, f
         B::template edge<false, 1>(sA + j * B::NA, Yv, xv, sv, dmv, t, dyl, st);
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
-        const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf Tb = row_buf(a.T + slot * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
         for (int i = 0; i < B::NXR; ++i) bst<1, E3_T_STORE_AUX>(Tb, B::XROW[i], t[i]);
       }
       const float tot = wave_reduce16(dy, lane);
-      if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+      if ((lane & 3) == 0) a.DY[(dy_group<V, G>(a, eb + j) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
     };
     load_x(0, xa);
     for (int q4 = 0; q4 < n; q4 += 4) {
       f4v s4[B::NPATH];
-      radial_quad<V, B::NPATH>(wb, sH, q4, a.K, B::PATH, s4);
+      radial_quad<V, B::NPATH>(wb, p_rows<V>(a), sH, q4, a.K, B::PATH, s4);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int j = q4 + i;
@@ -2179,6 +2188,15 @@ struct Ws {
   size_t t_bytes, dy_bytes;
 };
 
+// Scratch of the radial backward: T and DY as in the plain backward, then ds
+// by edge id (all E rows when any edge is live), the dW partials of each row
+// chunk and the dh partials of each column slab.
+struct RadWs {
+  size_t t, dy, ds, dwp, dhp;
+  int nchunk, rows_per, nsl4, nv, pc4;
+  size_t total() const { return t + dy + ds + dwp + dhp; }
+};
+
 // ---- layouts without a compiled variant (convr.hip): the composed path
 // (single-block kinds run block by block) or, when forced or when no kind
 // fits, the record path (the plan's coupling records walked at run time).
@@ -2196,6 +2214,13 @@ e3_status rec_fwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float
 e3_status rec_bwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float* x, const float* vec,
                   const float* y, const float* s, const float* dm, float* dx, float* dvec, float* dy, float* ds,
                   int accum, void* ws, hipStream_t st);
+// the composed path's fused radial weights
+RadWs comp_rad_ws(const e3_plan* p, const e3_graph* g, int K);
+e3_status comp_fwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                       const float* W, int K, float* m, hipStream_t st);
+e3_status comp_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                       const float* W, int K, const float* dm, float* dx, float* dvec, float* dh, float* dW,
+                       void* ws, hipStream_t st);
 // the composed path's float64 builds
 Ws comp_ws64(const e3_plan* p, const e3_graph* g);
 size_t comp_tp_ws64(const e3_plan* p, int64_t rows);
@@ -2208,14 +2233,6 @@ e3_status comp_tp64(const e3_plan* p, const double* x, const double* y, const do
 e3_status comp_tpb64(const e3_plan* p, const double* x, const double* y, const double* w, const double* dz,
                      double* dx, double* dy, double* dw, void* ws, int64_t rows, hipStream_t st);
 
-// Scratch of the radial backward: T and DY as in the plain backward, then ds
-// by edge id (all E rows when any edge is live), the dW partials of each row
-// chunk and the dh partials of each column slab.
-struct RadWs {
-  size_t t, dy, ds, dwp, dhp;
-  int nchunk, rows_per, nsl4, nv, pc4;
-  size_t total() const { return t + dy + ds + dwp + dhp; }
-};
 
 struct VariantOps {
   const char* sig;
@@ -2283,6 +2300,12 @@ struct KindOps {
                     const KindCall&, hipStream_t);
   e3_status (*tpb64)(const e3_plan*, const double* x, const double* y, const double* w, const double* dz,
                      double* dx, double* dw, double* DY, int64_t rows, const KindCall&, hipStream_t);
+  // fused radial weights: W offset to the block's first path, row stride P
+  e3_status (*rfwd)(const e3_plan*, const e3_graph*, const float* x, const float* vec, const float* h,
+                    const float* W, int K, float* m, const KindCall&, hipStream_t);
+  e3_status (*rbwd)(const e3_plan*, const e3_graph*, const float* x, const float* vec, const float* h,
+                    const float* W, int K, const float* dm, float* T, float* DY, float* DS, const KindCall&,
+                    hipStream_t);
 };
 
 namespace {
@@ -2503,12 +2526,11 @@ e3_status run_tp_bwd(const e3_plan* p, const float* x, const float* y, const flo
 }
 
 
-template <class V>
-RadWs rad_ws(const e3_plan* p, const e3_graph* g, int K) {
+// np: paths of the layout; b: the plain backward's scratch.
+inline RadWs rad_ws_of(const e3_plan* p, const e3_graph* g, int K, int np, Ws b) {
   RadWs w{};
-  const Ws b = bwd_ws<V>(p, g);
   w.t = b.t_bytes, w.dy = b.dy_bytes;
-  const int64_t pc = (int64_t)V::NP * p->lay.C, nl = g->n_live > 0 ? g->n_edges : 0;
+  const int64_t pc = (int64_t)np * p->lay.C, nl = g->n_live > 0 ? g->n_edges : 0;
   w.pc4 = (int)(pc / 4);
   const int f = grad_f(K <= 8 ? 2 : 4);
   w.nsl4 = (w.pc4 + kWave * f - 1) / (kWave * f);
@@ -2522,6 +2544,11 @@ RadWs rad_ws(const e3_plan* p, const e3_graph* g, int K) {
   w.dwp = align256((size_t)w.nchunk * K * pc * sizeof(float));
   w.dhp = align256((size_t)nl * w.nsl4 * w.nv * sizeof(float));
   return w;
+}
+
+template <class V>
+RadWs rad_ws(const e3_plan* p, const e3_graph* g, int K) {
+  return rad_ws_of(p, g, K, V::NP, bwd_ws<V>(p, g));
 }
 
 template <class V>
@@ -2858,6 +2885,42 @@ e3_status kind_tpb64(const e3_plan* p, const double* x, const double* y, const d
   return E3_OK;
 }
 
+template <class V>
+e3_status kind_fwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                       const float* W, int K, float* m, const KindCall& kc, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.h = h, a.W = W, a.K = K, a.m = m;
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr;
+  a.nslab = p->nslab_b;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
+  {
+    TimedLaunch t_("kind_fwd_rad", st);
+    if (K <= 8 && E3_RAD_WREG)
+      hipLaunchKernelGGL((k_conv_fwd_rad<V, 8>), dim3(grid), dim3(kWave), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_conv_fwd_rad<V, 0>), dim3(grid), dim3(kWave), 0, st, a);
+  }
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
+                       const float* W, int K, const float* dm, float* T, float* DY, float* DS, const KindCall& kc,
+                       hipStream_t st) {
+  if (g->n_live == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.vec = vec, a.h = h, a.W = W, a.K = K, a.dm = dm, a.T = T, a.DY = DY, a.ds = DS;
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr, a.ng = kc.ng, a.g0 = kc.g0;
+  a.nslab = p->nslab_b;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
+  TimedLaunch t_("kind_bwd_rad", st);
+  hipLaunchKernelGGL((k_conv_bwd_rad<V>), dim3(grid), dim3(kWave), 0, st, a);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
 }  // namespace
 
 // One kind's entry in the composed path's table (constant-initialised).
@@ -2865,7 +2928,7 @@ e3_status kind_tpb64(const e3_plan* p, const double* x, const double* y, const d
   KindOps{e3gen::V::SIG, e3gen::V::D_IN, e3gen::V::D_SH, e3gen::V::D_OUT, e3gen::V::NP, e3gen::V::LSH, \
           e3gen::V::NBG, &kind_fwd<e3gen::V>, &kind_bwd<e3gen::V>, &kind_tp<e3gen::V>,                 \
           &kind_tpb<e3gen::V>, &kind_fwd64<e3gen::V>, &kind_bwd64<e3gen::V>, &kind_tp64<e3gen::V>,     \
-          &kind_tpb64<e3gen::V>}
+          &kind_tpb64<e3gen::V>, &kind_fwd_rad<e3gen::V>, &kind_bwd_rad<e3gen::V>}
 
 // One variant's entry in the core unit's table (constant-initialised).
 #define E3_VARIANT_OPS(V)                                                                                    \

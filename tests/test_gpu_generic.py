@@ -12,6 +12,7 @@ import pytest
 import synth
 from oracle import conv as oconv
 from oracle import irreps as oirreps
+from oracle import radial as oradial
 from oracle import sh as osh
 from oracle import tp as otp
 
@@ -409,3 +410,45 @@ def test_composed_float64(e3, irreps, lsh, lout, parity, n, e, pad, rows):
     print("float64 tp rel-L2", terrs, flush=True)
     for k, v in terrs.items():
         assert v < TOL64, (k, v)
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,K,pad", [
+    ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 50, 700, 8, 3),
+    ("8x0o+8x1o", 1, 1, "natural", 40, 500, 5, -1),                 # a block with no path
+    ("68x1o+68x2o", 3, 2, "all", 30, 400, 12, -1),                  # a ragged slab, K > 8
+    ("128x0e+128x1o+128x2e+128x3o", 3, 3, "all", 60, 1200, 8, 5),   # the benchmark layout, forced
+])
+def test_composed_radial(e3, irreps, lsh, lout, parity, n, e, K, pad):
+    """The fused radial weights (s = h W on the matrix cores) on the composed
+    path: m, dx, dvec, dh, dW against the oracle, bitwise repeats, zero
+    cotangents of padding edges."""
+    _say("composed radial", irreps, lsh, lout, parity, n, e, K, pad)
+    rng = np.random.default_rng(49)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    plan = _plan(e3, irreps, lsh, lout, parity, "composed")
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    h = rng.standard_normal((e, K)).astype(np.float32)
+    W = (rng.standard_normal((K, lay.n_paths, C)) / np.sqrt(K)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    xs, vs, hs, Ws, dms = (to_dev(a) for a in (x, vec, h, W, dm))
+    outs = []
+    for _ in range(2):
+        m = e3.conv_fwd_radial(plan, G, xs, vs, hs, Ws)
+        outs.append([to_np(t) for t in (m,) + e3.conv_bwd_radial(plan, G, xs, vs, hs, Ws, dms)])
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b), "not deterministic"
+    m, dx, dvec, dh, dW = outs[0]
+    ref_m = oradial.conv_fwd(lay, x, vec, h, W, snd, rcv, n, pad_node=pad).numpy()
+    ref = oradial.conv_bwd(lay, x, vec, h, W, dm, snd, rcv, n, pad_node=pad)
+    errs = dict(m=rel_l2(m, ref_m), dx=rel_l2(dx, ref["dx"].numpy()), dvec=rel_l2(dvec, ref["dvec"].numpy()),
+                dh=rel_l2(dh, ref["dh"].numpy()), dW=rel_l2(dW, ref["dW"].numpy()))
+    print("rel-L2", errs, flush=True)
+    for k, v in errs.items():
+        assert v < TOL, (k, v)
+    if pad >= 0:
+        dead = (snd == pad) | (rcv == pad)
+        assert np.all(dh[dead] == 0) and np.all(dvec[dead] == 0)
+        assert np.all(m[pad] == 0) and np.all(dx[pad] == 0)
