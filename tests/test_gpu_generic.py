@@ -67,6 +67,7 @@ CASES = [
     ("128x0e+128x1o+128x2e+128x3o", 2, 3, "all", 60, 1200, -1),
     ("64x0e+64x1o+64x1e+64x2e+64x3o", 3, 3, "natural", 40, 600, 4),
     ("128x0e+128x1o+128x2e+128x3o", 3, 3, "all", 80, 1500, 7),   # the benchmark layout (compiled too)
+    ("12x0e+12x1o+12x2e+12x3o+12x0o+12x1e+12x2o+12x3e", 3, 3, "all", 30, 400, -1),   # eight blocks
 ]
 
 
