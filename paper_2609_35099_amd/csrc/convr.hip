@@ -466,12 +466,8 @@ e3_plan::~e3_plan() {
 
 namespace {
 
-int add_tab(std::vector<int>& t, int v) {
-  t.push_back(v);
-  return (int)t.size() - 1;
-}
-
-// The record path's tables of a layout, or an empty optional reason.
+// The record path's tables of a layout; false, with the reason in `why`, for
+// a layout it does not take.
 bool rec_tables(const e3_plan* p, RecPlan& R, std::string& why) {
   const auto& L = p->lay;
   if (L.C < 4 || L.C % 4 != 0 || L.C > kMaxChannels) {

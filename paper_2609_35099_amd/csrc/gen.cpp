@@ -1030,7 +1030,9 @@ int main(int argc, char** argv) {
       if (!in_unit.empty()) unit_kinds.push_back(in_unit);
     }
   }
-  ko << "}  // namespace e3gen\n";
+  ko << "#define E3GEN_FOR_EACH_KIND(X)";
+  for (const auto& t : ktags) ko << " X(" << t << ")";
+  ko << "\n\n}  // namespace e3gen\n";
   if (!write("kinds.inc", ko.str())) return 1;
   kt << "// GENERATED by gen.cpp -- do not edit.\n";
   for (const auto& tag : ktags) kt << "const KindOps* e3_kind_" << tag << "();\n";

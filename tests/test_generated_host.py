@@ -8,7 +8,8 @@ contraction order the generator picks) is plain C++ apart from a few device
 qualifiers.  Here it is built with g++ next to a small driver that runs the
 forward and backward groups of one edge and one channel, and the results are
 compared with the oracle's weighted tensor product and its backward
-(App. E.1, eq. tp-bwd) on random inputs, for every compiled variant."""
+(App. E.1, eq. tp-bwd) on random inputs, for every compiled variant and every
+single-block kind of the composed path."""
 import ctypes as ct
 import os
 import shutil
@@ -152,6 +153,27 @@ void bwd3_groups(const float* Y, const float* Y2, const float* x, const float* x
     bwd_groups<V, 0>(Y, x, s, dm, dx, dy, ds);                                                 \
   }
 E3GEN_FOR_EACH_VARIANT(E3_HOST_ENTRY)
+
+// single-block kinds (forward and backward groups; their strides are the
+// composed path's business, the per-edge code is the same)
+#include "kinds.inc"
+#define E3_KIND_ENTRY(V)                                                                        \
+  extern "C" void V##_fwd(const float* Y, const float* x, const float* s, float* m) {          \
+    fwd_groups<V, 0>(Y, x, s, m);                                                              \
+  }                                                                                            \
+  extern "C" void V##_bwd(const float* Y, const float* x, const float* s, const float* dm,      \
+                          float* dx, float* dy, float* ds) {                                   \
+    for (int i = 0; i < V::D_IN; ++i) dx[i] = 0.0f;                                            \
+    for (int i = 0; i < V::D_SH; ++i) dy[i] = 0.0f;                                            \
+    bwd_groups<V, 0>(Y, x, s, dm, dx, dy, ds);                                                 \
+  }                                                                                            \
+  extern "C" const char* V##_sig() { return V::SIG; }
+E3GEN_FOR_EACH_KIND(E3_KIND_ENTRY)
+extern "C" const char* e3_kind_list() {
+  return ""
+#define E3_KIND_NAME(V) #V " "
+  E3GEN_FOR_EACH_KIND(E3_KIND_NAME);
+}
 """
 
 
@@ -268,3 +290,66 @@ def test_generated_three_term_backward_matches_oracle(hostlib, tag):
     assert _rel(gs, (dw_a + dw_b).numpy()[:, :, 0]) < 1e-6
     assert _rel(gy, (dy_a + dy_c).numpy()) < 1e-6
     assert _rel(gx, (dx_b + dx_c).numpy()[:, :, 0]) < 1e-6
+
+
+def _kind_layout(tag):
+    """The single-block layout a kind tag names: K_l<l1>_s<lsh>_o<lout>_<a|n|p>
+    (all paths; natural-parity paths of a block of parity (-1)^l1; of the
+    other parity)."""
+    _, l, sh, o, cls = tag.split("_")
+    l1, lsh, lout = int(l[1:]), int(sh[1:]), int(o[1:])
+    even = (l1 % 2 == 0) == (cls != "p")
+    irreps = f"1x{l1}{'e' if even else 'o'}"
+    return oirreps.layout(irreps, lsh, lout, parity="all" if cls == "a" else "natural"), lsh
+
+
+def test_generated_kind_code_matches_oracle(hostlib):
+    """Every single-block kind the composed path runs: its per-edge forward and
+    backward code against the oracle's tensor product of that block alone, and
+    the set of kinds covers every block of degree <= 3 under harmonics and
+    outputs to degree 3 (each block's path list has a kind)."""
+    hostlib.e3_kind_list.restype = ct.c_char_p
+    tags = hostlib.e3_kind_list().decode().split()
+    assert len(tags) == len(set(tags)) > 0
+    have = set()
+    for tag in tags:
+        lay, lsh = _kind_layout(tag)
+        assert lay.n_paths > 0, tag
+        have.add((tuple((p.l1, p.l2, p.l3) for p in lay.paths), lsh))
+        rng = np.random.default_rng(17)
+        R = 6
+        u = rng.standard_normal((R, 3))
+        u /= np.linalg.norm(u, axis=1, keepdims=True)
+        y = np.asarray(osh.sh_unit(lsh, u), dtype=np.float32)
+        x = rng.standard_normal((R, lay.d_in)).astype(np.float32)
+        s = rng.standard_normal((R, lay.n_paths)).astype(np.float32)
+        dm = rng.standard_normal((R, lay.d_out)).astype(np.float32)
+        fwd, bwd = getattr(hostlib, f"{tag}_fwd"), getattr(hostlib, f"{tag}_bwd")
+        m = np.zeros((R, lay.d_out), np.float32)
+        dx = np.zeros((R, lay.d_in), np.float32)
+        dy = np.zeros((R, lay.d_sh), np.float32)
+        ds = np.zeros((R, lay.n_paths), np.float32)
+        for r in range(R):
+            rows = [np.ascontiguousarray(a[r]) for a in (y, x, s, dm)]
+            outs = [np.zeros_like(a[r]) for a in (m, dx, dy, ds)]
+            fwd(_ptr(rows[0]), _ptr(rows[1]), _ptr(rows[2]), _ptr(outs[0]))
+            bwd(_ptr(rows[0]), _ptr(rows[1]), _ptr(rows[2]), _ptr(rows[3]), _ptr(outs[1]), _ptr(outs[2]),
+                _ptr(outs[3]))
+            m[r], dx[r], dy[r], ds[r] = outs
+        ref_m = otp.tp(lay, x[:, :, None], y, s[:, :, None]).numpy()[:, :, 0]
+        ref_dx, ref_dy, ref_dw = otp.tp_bwd(lay, x[:, :, None], y, s[:, :, None], dm[:, :, None])
+        assert _rel(m, ref_m) < 1e-6, tag
+        assert _rel(dx, ref_dx.numpy()[:, :, 0]) < 1e-6, tag
+        assert _rel(ds, ref_dw.numpy()[:, :, 0]) < 1e-6, tag
+        assert _rel(dy, ref_dy.numpy()) < 1e-6, tag
+    # coverage: every block (degree, parity) of degree <= 3, each parity rule,
+    # harmonics and outputs to degree 3
+    for l1 in range(4):
+        for p in "eo":
+            for lsh in range(4):
+                for lout in range(4):
+                    for parity in ("all", "natural"):
+                        lay = oirreps.layout(f"1x{l1}{p}", lsh, lout, parity=parity)
+                        if lay.n_paths:
+                            key = (tuple((q.l1, q.l2, q.l3) for q in lay.paths), lsh)
+                            assert key in have, (l1, p, lsh, lout, parity)
