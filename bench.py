@@ -1011,7 +1011,22 @@ def main():
                        "kernels": {k: {"ms_total_per_call": round(t / args.steps, 4), "launches": c}
                                    for k, (t, c) in per.items()}}
         log(f"bwd2: {b2_ms:.3f} ms, {out['bwd2']['alg_GBps']} GB/s; kernels {out['bwd2']['kernels']}")
-        del outs, ws2, s2, dds, ddx, ddy, ys
+        del outs, ws2
+        # the same on the composed path (single-block kinds, fused sweeps per block)
+        cplan = e3mi.Plan(cfg.irreps, cfg.lmax_sh, cfg.lmax_out, composed=True)
+        wsc = e3mi.workspace(e3mi.conv_workspace_size(cplan, graph)[1])
+        for _ in range(args.warmup):
+            outs = e3mi.conv_bwd2(cplan, graph, xs, ys, s2, dms, ddx, ddy, dds, ws=wsc)
+        del outs
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(args.steps):
+            outs = e3mi.conv_bwd2(cplan, graph, xs, ys, s2, dms, ddx, ddy, dds, ws=wsc)
+        ev1.record()
+        torch.cuda.synchronize()
+        out["bwd2"]["composed_ms"] = round(ev0.elapsed_time(ev1) / args.steps, 4)
+        log(f"bwd2 composed: {out['bwd2']['composed_ms']:.3f} ms")
+        del outs, wsc, cplan, s2, dds, ddx, ddy, ys
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- linear mixing

@@ -1279,3 +1279,42 @@ e3_status comp_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, cons
   }
   return E3_OK;
 }
+
+// ------------------------------------------------------------ composed path, double backward
+e3_status comp_bwd2(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
+                    const float* dm, const float* ddx, const float* ddy, const float* dds, float* gx, float* gy,
+                    float* gs, float* gdm, void* ws, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  const int64_t C = p->lay.C, D_in = p->lay.d_in;
+  e3_status r;
+  // gdm = conv(ddx, y, s) + conv(x, ddy, s) + conv(x, y, dds): one sweep per block
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    if ((r = K.fwd3(p, g, x + b.x_off * C, ddx + b.x_off * C, y, ddy, s + b.k0 * C, dds + b.k0 * C,
+                    gdm + b.o_off * C, comp_call(p, b.g0), st)) != E3_OK)
+      return r;
+  }
+  // gx, gy, gs: the three backward terms in one sweep per block, then the
+  // shared sender-order sum and harmonic sum
+  const Ws w = comp_ws(p, g);
+  float* T = reinterpret_cast<float*>(ws);
+  float* DY = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.t_bytes);
+  for (const auto& b : p->kblocks) {
+    const KindOps& K = *kKinds[b.kind]();
+    if ((r = K.bwd3(p, g, x + b.x_off * C, ddx + b.x_off * C, y, ddy, s + b.k0 * C, dds + b.k0 * C,
+                    dm + b.o_off * C, T + b.x_off * C, DY, gs + b.k0 * C, comp_call(p, b.g0), st)) != E3_OK)
+      return r;
+  }
+  for (const auto& z : p->pathless)
+    if ((r = comp_zero_rows(T, g->n_live, D_in * C, z.first * C, z.second * C, st)) != E3_OK) return r;
+  {
+    TimedLaunch t_("conv_bwd_dx", st);
+    const int flat4 = (int)(D_in * C / 4);
+    const int nsl = (flat4 + kWave * kDxVec - 1) / (kWave * kDxVec);
+    const int chunk = (int)((g->n_nodes + kXcd - 1) / kXcd);
+    hipLaunchKernelGGL(k_conv_bwd_dx, dim3((unsigned)(kXcd * chunk * nsl)), dim3(kWave), 0, st, T, gx, g->rowptr_s,
+                       (int)g->n_nodes, chunk, flat4, nsl, 0);
+    E3_HIP(hipGetLastError());
+  }
+  return finish_bwd(p, g, g->n_live, nullptr, DY, nullptr, gy, gs, p->kng * p->nslab_b, 0, st);
+}

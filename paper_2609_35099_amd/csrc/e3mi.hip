@@ -1429,6 +1429,7 @@ e3_status e3_conv_bwd2(const e3_plan* p, const e3_graph* g, const float* x, cons
   if (w.t_bytes + w.dy_bytes > 0 && (!ws || !aligned16(ws))) return E3_ERR_INVALID_ARG;
   if (ws_bytes < w.t_bytes + w.dy_bytes) return E3_ERR_WORKSPACE_TOO_SMALL;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  if (p->composed) return comp_bwd2(p, g, x, y, s, dm, ddx, ddy, dds, gx, gy, gs, gdm, ws, hs);
   if (p->variant < 0) {  // the record path: three forward and three backward calls
     if ((st = rec_fwd(p, g, 0, ddx, nullptr, y, s, gdm, 0, hs)) != E3_OK) return st;
     if ((st = rec_fwd(p, g, 0, x, nullptr, ddy, s, gdm, 1, hs)) != E3_OK) return st;

@@ -828,10 +828,10 @@ __device__ __forceinline__ void fwd3_task(const ConvArgs& a, int b, int sl, floa
                       float (&sdv)[F::NPATH][1]) {
         const int64_t e = __builtin_amdgcn_readlane(my_e, j);
         const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
-        const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-        const RowBuf x2r = row_buf(a.x2 + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-        const RowBuf sr = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
-        const RowBuf s2r = row_buf(a.s2 + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        const RowBuf xr = row_buf(a.x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf x2r = row_buf(a.x2 + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf sr = row_buf(a.s + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
+        const RowBuf s2r = row_buf(a.s2 + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
 #pragma unroll
         for (int i = 0; i < F::NXR; ++i) bld<1>(xr, F::XROW[i], xv[i]), bld<1>(x2r, F::XROW[i], xdv[i]);
 #pragma unroll
@@ -850,7 +850,7 @@ __device__ __forceinline__ void fwd3_task(const ConvArgs& a, int b, int sl, floa
     __syncthreads();
   }
   if (act) {
-    const RowBuf mb = row_buf(a.m + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+    const RowBuf mb = row_buf(a.m + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
     for (int i = 0; i < F::NROW; ++i) bst<1, kST>(mb, F::OROW[i], acc[i]);
   }
@@ -1042,7 +1042,7 @@ __device__ __forceinline__ void bwd3_task(const ConvArgs& a, int b, int sl, floa
   if (e0 == e1) return;
   float dmv[B::NROW][1];
   if (act) {
-    const RowBuf db = row_buf(a.dm + (int64_t)b * V::D_OUT * C, (int64_t)V::D_OUT * C * 4, q, C);
+    const RowBuf db = row_buf(a.dm + (int64_t)b * o_rows<V>(a) * C, (int64_t)V::D_OUT * C * 4, q, C);
 #pragma unroll
     for (int i = 0; i < B::NROW; ++i) bld<1>(db, B::OROW[i], dmv[i]);
   }
@@ -1067,10 +1067,10 @@ __device__ __forceinline__ void bwd3_task(const ConvArgs& a, int b, int sl, floa
       if (!act) return;
       const int64_t e = __builtin_amdgcn_readlane(my_e, j);
       const int64_t snd = __builtin_amdgcn_readlane(my_src, j);
-      const RowBuf xr = row_buf(a.x + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-      const RowBuf x2r = row_buf(a.x2 + snd * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
-      const RowBuf sr = row_buf(a.s + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
-      const RowBuf s2r = row_buf(a.s2 + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+      const RowBuf xr = row_buf(a.x + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf x2r = row_buf(a.x2 + snd * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
+      const RowBuf sr = row_buf(a.s + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
+      const RowBuf s2r = row_buf(a.s2 + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
 #pragma unroll
       for (int i = 0; i < B::NXR; ++i) bld<1>(xr, B::XROW[i], xv[i]), bld<1>(x2r, B::XROW[i], xdv[i]);
 #pragma unroll
@@ -1089,17 +1089,17 @@ __device__ __forceinline__ void bwd3_task(const ConvArgs& a, int b, int sl, floa
         for (int i = 0; i < B::NXR; ++i) t[i][0] = 0.0f;
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) Yv[i] = sY[j * V::D_SH + i], Y2v[i] = sY2[j * V::D_SH + i], dyl[i] = 0.0f;
-        const RowBuf gsb = row_buf(a.ds + e * V::NP * C, (int64_t)V::NP * C * 4, q, C);
+        const RowBuf gsb = row_buf(a.ds + e * p_rows<V>(a) * C, (int64_t)V::NP * C * 4, q, C);
         auto st = [&](int pl, const float (&v)[1]) { bst<1, kST>(gsb, B::PATH[pl], v); };
         B::template edge3<1>(Yv, Y2v, xv, xdv, sv, sdv, dmv, t, dyl, st);
 #pragma unroll
         for (int i = 0; i < V::D_SH; ++i) dy[i] = dyl[i];
-        const RowBuf Tb = row_buf(a.T + slot * V::D_IN * C, (int64_t)V::D_IN * C * 4, q, C);
+        const RowBuf Tb = row_buf(a.T + slot * x_rows<V>(a) * C, (int64_t)V::D_IN * C * 4, q, C);
 #pragma unroll
         for (int i = 0; i < B::NXR; ++i) bst<1, E3_T_STORE_AUX>(Tb, B::XROW[i], t[i]);
       }
       const float tot = wave_reduce16(dy, lane);
-      if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * V::NBG + G) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
+      if ((lane & 3) == 0) a.DY[(dy_group<V, G>(a, eb + j) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
     };
 #ifndef E3_BWD3_SINGLE
 #define E3_BWD3_SINGLE 1
@@ -2214,6 +2214,10 @@ e3_status rec_fwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float
 e3_status rec_bwd(const e3_plan* p, const e3_graph* g, int64_t rows, const float* x, const float* vec,
                   const float* y, const float* s, const float* dm, float* dx, float* dvec, float* dy, float* ds,
                   int accum, void* ws, hipStream_t st);
+// the composed path's double backward (fused sweeps per block)
+e3_status comp_bwd2(const e3_plan* p, const e3_graph* g, const float* x, const float* y, const float* s,
+                    const float* dm, const float* ddx, const float* ddy, const float* dds, float* gx, float* gy,
+                    float* gs, float* gdm, void* ws, hipStream_t st);
 // the composed path's fused radial weights
 RadWs comp_rad_ws(const e3_plan* p, const e3_graph* g, int K);
 e3_status comp_fwd_rad(const e3_plan* p, const e3_graph* g, const float* x, const float* vec, const float* h,
@@ -2306,6 +2310,12 @@ struct KindOps {
   e3_status (*rbwd)(const e3_plan*, const e3_graph*, const float* x, const float* vec, const float* h,
                     const float* W, int K, const float* dm, float* T, float* DY, float* DS, const KindCall&,
                     hipStream_t);
+  // the double backward's three forward terms and three backward terms, each in one sweep
+  e3_status (*fwd3)(const e3_plan*, const e3_graph*, const float* x, const float* x2, const float* y,
+                    const float* y2, const float* s, const float* s2, float* m, const KindCall&, hipStream_t);
+  e3_status (*bwd3)(const e3_plan*, const e3_graph*, const float* x, const float* x2, const float* y,
+                    const float* y2, const float* s, const float* s2, const float* dm, float* T, float* DY,
+                    float* gs, const KindCall&, hipStream_t);
 };
 
 namespace {
@@ -2921,6 +2931,37 @@ e3_status kind_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, cons
   return E3_OK;
 }
 
+template <class V>
+e3_status kind_fwd3(const e3_plan* p, const e3_graph* g, const float* x, const float* x2, const float* y,
+                    const float* y2, const float* s, const float* s2, float* m, const KindCall& kc, hipStream_t st) {
+  if (g->n_nodes == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.x2 = x2, a.y = y, a.y2 = y2, a.s = s, a.s2 = s2, a.m = m;
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr;
+  a.nslab = (a.C + kWave - 1) / kWave;  // one channel per lane
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
+  TimedLaunch t_("kind_fwd3", st);
+  hipLaunchKernelGGL((k_conv_fwd3<V>), dim3(grid), dim3(kWave), 0, st, a);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
+template <class V>
+e3_status kind_bwd3(const e3_plan* p, const e3_graph* g, const float* x, const float* x2, const float* y,
+                    const float* y2, const float* s, const float* s2, const float* dm, float* T, float* DY,
+                    float* gs, const KindCall& kc, hipStream_t st) {
+  if (g->n_live == 0) return E3_OK;
+  ConvArgs a = base_args(p, g);
+  a.x = x, a.x2 = x2, a.y = y, a.y2 = y2, a.s = s, a.s2 = s2, a.dm = dm, a.ds = gs, a.T = T, a.DY = DY;
+  a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr, a.ng = kc.ng, a.g0 = kc.g0;
+  a.nslab = p->nslab_b;
+  const unsigned grid = (unsigned)(kXcd * a.chunk * V::NBG * a.nslab);
+  TimedLaunch t_("kind_bwd3", st);
+  hipLaunchKernelGGL((k_conv_bwd3<V>), dim3(grid), dim3(kWave), 0, st, a);
+  E3_HIP(hipGetLastError());
+  return E3_OK;
+}
+
 }  // namespace
 
 // One kind's entry in the composed path's table (constant-initialised).
@@ -2928,7 +2969,8 @@ e3_status kind_bwd_rad(const e3_plan* p, const e3_graph* g, const float* x, cons
   KindOps{e3gen::V::SIG, e3gen::V::D_IN, e3gen::V::D_SH, e3gen::V::D_OUT, e3gen::V::NP, e3gen::V::LSH, \
           e3gen::V::NBG, &kind_fwd<e3gen::V>, &kind_bwd<e3gen::V>, &kind_tp<e3gen::V>,                 \
           &kind_tpb<e3gen::V>, &kind_fwd64<e3gen::V>, &kind_bwd64<e3gen::V>, &kind_tp64<e3gen::V>,     \
-          &kind_tpb64<e3gen::V>, &kind_fwd_rad<e3gen::V>, &kind_bwd_rad<e3gen::V>}
+          &kind_tpb64<e3gen::V>, &kind_fwd_rad<e3gen::V>, &kind_bwd_rad<e3gen::V>, &kind_fwd3<e3gen::V>,  \
+          &kind_bwd3<e3gen::V>}
 
 // One variant's entry in the core unit's table (constant-initialised).
 #define E3_VARIANT_OPS(V)                                                                                    \

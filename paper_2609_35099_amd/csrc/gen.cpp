@@ -921,7 +921,7 @@ int main(int argc, char** argv) {
       emit_group_meta(os, fg[gi]);
       emit_make_A(os, fg[gi]);
       emit_fwd_group(os, lay, pis, fg[gi]);
-      if (!rt) emit_fwd3_group(os, pis, fg[gi]);
+      emit_fwd3_group(os, pis, fg[gi]);
       os << "};\n\n";
     }
     for (size_t gi = 0; gi < bg.size(); ++gi) {
@@ -930,7 +930,7 @@ int main(int argc, char** argv) {
       emit_group_meta(os, bg[gi]);
       emit_make_A(os, bg[gi]);
       emit_bwd_group(os, lay, pis, bg[gi]);
-      if (!rt) emit_bwd3_group(os, pis, bg[gi]);
+      emit_bwd3_group(os, pis, bg[gi]);
       os << "};\n\n";
     }
     os << "struct " << tag << "::TP {\n";
