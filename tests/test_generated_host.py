@@ -9,7 +9,8 @@ qualifiers.  Here it is built with g++ next to a small driver that runs the
 forward and backward groups of one edge and one channel, and the results are
 compared with the oracle's weighted tensor product and its backward
 (App. E.1, eq. tp-bwd) on random inputs, for every compiled variant and every
-single-block kind of the composed path."""
+single-block kind of the composed path (and the double backward's three-term
+sweeps of both)."""
 import ctypes as ct
 import os
 import shutil
@@ -40,7 +41,42 @@ VARIANTS = {
 }
 
 
+def _kind_layout(tag):
+    """The single-block layout a kind tag names: K_l<l1>_s<lsh>_o<lout>_<a|n|p>
+    (all paths; natural-parity paths of a block of parity (-1)^l1; of the
+    other parity)."""
+    _, l, sh, o, cls = tag.split("_")
+    l1, lsh, lout = int(l[1:]), int(sh[1:]), int(o[1:])
+    even = (l1 % 2 == 0) == (cls != "p")
+    irreps = f"1x{l1}{'e' if even else 'o'}"
+    return oirreps.layout(irreps, lsh, lout, parity="all" if cls == "a" else "natural"), lsh
+
+
+def _kind_tags():
+    """The kinds the generator should emit: every single x block of degree
+    <= 3 (all paths, or the natural-parity ones of either block parity) under
+    harmonics and outputs to degree 3, one per distinct (path list, harmonics
+    degree), in the generator's enumeration order."""
+    seen, tags = set(), []
+    for l1 in range(4):
+        for lsh in range(4):
+            for lout in range(4):
+                for cls in "anp":
+                    tag = f"K_l{l1}_s{lsh}_o{lout}_{cls}"
+                    lay, _ = _kind_layout(tag)
+                    key = (tuple((p.l1, p.l2, p.l3) for p in lay.paths), lsh)
+                    if lay.n_paths and key not in seen:
+                        seen.add(key)
+                        tags.append(tag)
+    return tags
+
+
+KINDS = _kind_tags()
+
+
 def _layout(tag):
+    if tag.startswith("K_"):
+        return _kind_layout(tag)
     blocks, lsh, lout, parity = VARIANTS[tag]
     irreps = "+".join("1x" + b for b in blocks.split("+"))
     return oirreps.layout(irreps, lsh, lout, parity=parity), lsh
@@ -154,21 +190,10 @@ void bwd3_groups(const float* Y, const float* Y2, const float* x, const float* x
   }
 E3GEN_FOR_EACH_VARIANT(E3_HOST_ENTRY)
 
-// single-block kinds (forward and backward groups; their strides are the
-// composed path's business, the per-edge code is the same)
+// single-block kinds (their strides are the composed path's business; the
+// per-edge code is the same)
 #include "kinds.inc"
-#define E3_KIND_ENTRY(V)                                                                        \
-  extern "C" void V##_fwd(const float* Y, const float* x, const float* s, float* m) {          \
-    fwd_groups<V, 0>(Y, x, s, m);                                                              \
-  }                                                                                            \
-  extern "C" void V##_bwd(const float* Y, const float* x, const float* s, const float* dm,      \
-                          float* dx, float* dy, float* ds) {                                   \
-    for (int i = 0; i < V::D_IN; ++i) dx[i] = 0.0f;                                            \
-    for (int i = 0; i < V::D_SH; ++i) dy[i] = 0.0f;                                            \
-    bwd_groups<V, 0>(Y, x, s, dm, dx, dy, ds);                                                 \
-  }                                                                                            \
-  extern "C" const char* V##_sig() { return V::SIG; }
-E3GEN_FOR_EACH_KIND(E3_KIND_ENTRY)
+E3GEN_FOR_EACH_KIND(E3_HOST_ENTRY)
 extern "C" const char* e3_kind_list() {
   return ""
 #define E3_KIND_NAME(V) #V " "
@@ -234,7 +259,7 @@ def test_generated_edge_code_matches_oracle(hostlib, tag):
     assert _rel(dy, ref_dy.numpy()) < 1e-6
 
 
-@pytest.mark.parametrize("tag", sorted(VARIANTS))
+@pytest.mark.parametrize("tag", sorted(VARIANTS) + KINDS)
 def test_generated_three_term_forward_matches_oracle(hostlib, tag):
     """The double backward's output cotangent in one pass: the sum of three
     forward products, with the x, harmonic and weight tangents in turn."""
@@ -259,7 +284,7 @@ def test_generated_three_term_forward_matches_oracle(hostlib, tag):
     assert _rel(m, ref) < 1e-6
 
 
-@pytest.mark.parametrize("tag", sorted(VARIANTS))
+@pytest.mark.parametrize("tag", sorted(VARIANTS) + KINDS)
 def test_generated_three_term_backward_matches_oracle(hostlib, tag):
     """The double backward's three backward products in one pass: ds of
     (xd, y, s) and of (x, y2, s), dy of (xd, y, s) and of (x, y, sd), and the
@@ -292,17 +317,6 @@ def test_generated_three_term_backward_matches_oracle(hostlib, tag):
     assert _rel(gx, (dx_b + dx_c).numpy()[:, :, 0]) < 1e-6
 
 
-def _kind_layout(tag):
-    """The single-block layout a kind tag names: K_l<l1>_s<lsh>_o<lout>_<a|n|p>
-    (all paths; natural-parity paths of a block of parity (-1)^l1; of the
-    other parity)."""
-    _, l, sh, o, cls = tag.split("_")
-    l1, lsh, lout = int(l[1:]), int(sh[1:]), int(o[1:])
-    even = (l1 % 2 == 0) == (cls != "p")
-    irreps = f"1x{l1}{'e' if even else 'o'}"
-    return oirreps.layout(irreps, lsh, lout, parity="all" if cls == "a" else "natural"), lsh
-
-
 def test_generated_kind_code_matches_oracle(hostlib):
     """Every single-block kind the composed path runs: its per-edge forward and
     backward code against the oracle's tensor product of that block alone, and
@@ -310,7 +324,7 @@ def test_generated_kind_code_matches_oracle(hostlib):
     outputs to degree 3 (each block's path list has a kind)."""
     hostlib.e3_kind_list.restype = ct.c_char_p
     tags = hostlib.e3_kind_list().decode().split()
-    assert len(tags) == len(set(tags)) > 0
+    assert tags == KINDS
     have = set()
     for tag in tags:
         lay, lsh = _kind_layout(tag)
