@@ -453,3 +453,61 @@ def test_composed_radial(e3, irreps, lsh, lout, parity, n, e, K, pad):
         dead = (snd == pad) | (rcv == pad)
         assert np.all(dh[dead] == 0) and np.all(dvec[dead] == 0)
         assert np.all(m[pad] == 0) and np.all(dx[pad] == 0)
+
+
+def _random_layout(rng):
+    """A random channelwise layout: 1-5 blocks of degree <= 3 with random
+    parities, harmonics and outputs to degree 3, all or natural paths, C a
+    multiple of 4 (re-drawn until it has a path)."""
+    while True:
+        nb = int(rng.integers(1, 6))
+        C = 4 * int(rng.integers(1, 50))
+        blocks = [f"{C}x{int(rng.integers(0, 4))}{'eo'[int(rng.integers(0, 2))]}" for _ in range(nb)]
+        irreps = "+".join(blocks)
+        lsh, lout = int(rng.integers(0, 4)), int(rng.integers(0, 4))
+        parity = "natural" if rng.random() < 0.4 else "all"
+        lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+        if lay.n_paths > 0:
+            return irreps, lsh, lout, parity, lay
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_generic_random_layouts(e3, seed):
+    """Seeded random layouts: the convolution forward and backward and the
+    tensor product forward and backward on the composed path (and, for even
+    seeds, the record path) against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    irreps, lsh, lout, parity, lay = _random_layout(rng)
+    n, e = int(rng.integers(10, 50)), int(rng.integers(50, 400))
+    pad = int(rng.integers(0, n)) if seed % 3 == 0 else -1
+    C = lay.channels
+    snd, rcv, vec = _random_graph(rng, n, e)
+    x = rng.standard_normal((n, lay.d_in, C)).astype(np.float32)
+    s = rng.standard_normal((e, lay.n_paths, C)).astype(np.float32)
+    dm = rng.standard_normal((n, lay.d_out, C)).astype(np.float32)
+    rows = int(rng.integers(1, 40))
+    g = rng.standard_normal((rows, 3))
+    y = osh.sh_unit(lsh, g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
+    tx = rng.standard_normal((rows, lay.d_in, C)).astype(np.float32)
+    tw = rng.standard_normal((rows, lay.n_paths, C)).astype(np.float32)
+    tdz = rng.standard_normal((rows, lay.d_out, C)).astype(np.float32)
+    ref_m = oconv.conv_fwd(lay, x, vec, s, snd, rcv, n, pad_node=pad).numpy()
+    ref = oconv.conv_bwd(lay, x, vec, s, dm, snd, rcv, n, pad_node=pad)
+    ref_z = otp.tp(lay, tx, y, tw).numpy()
+    ref_t = otp.tp_bwd(lay, tx, y, tw, tdz)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=pad)
+    for path in (("composed", "records") if seed % 2 == 0 else ("composed",)):
+        _say("random layout", seed, path, irreps, lsh, lout, parity, n, e, pad, rows)
+        plan = _plan(e3, irreps, lsh, lout, parity, path)
+        xs, vs, ss, dms = to_dev(x), to_dev(vec), to_dev(s), to_dev(dm)
+        m = e3.conv_fwd(plan, G, xs, vs, ss)
+        dx, dvec, ds = e3.conv_bwd(plan, G, xs, vs, ss, dms)
+        z = e3.tp_fwd(plan, to_dev(tx), to_dev(y), to_dev(tw))
+        tdx, tdy, tdw = e3.tp_bwd(plan, to_dev(tx), to_dev(y), to_dev(tw), to_dev(tdz))
+        errs = dict(m=rel_l2(to_np(m), ref_m), dx=rel_l2(to_np(dx), ref["dx"].numpy()),
+                    ds=rel_l2(to_np(ds), ref["ds"].numpy()), dvec=rel_l2(to_np(dvec), ref["dvec"].numpy()),
+                    z=rel_l2(to_np(z), ref_z), tdx=rel_l2(to_np(tdx), ref_t[0].numpy()),
+                    tdy=rel_l2(to_np(tdy), ref_t[1].numpy()), tdw=rel_l2(to_np(tdw), ref_t[2].numpy()))
+        print("rel-L2", errs, flush=True)
+        for k, v in errs.items():
+            assert v < TOL, (path, k, v)
