@@ -300,7 +300,7 @@ def against_ceilings(kernels, ceil):
 
 
 # ---------------------------------------------------------------- profile summaries
-# rocprofv3 runs behind the files in profiles/ (on the GPU machine, after
+# rocprofv3 runs behind the files in profiles/ (on an MI355X machine, after
 # `cd /tmp && export TMPDIR=/tmp`; $REPO is the repository root, $OUT a results
 # directory): a kernel trace per bench section, one HBM byte counter per run,
 # and the utilisation counters.  `python bench.py --summarize-profiles $OUT`
@@ -471,7 +471,7 @@ def summarize_profiles(root, only=None):
             for sec in secs:
                 body += _prof_util(root, sec, h)
         head = [f"# {title}", f"# source hash (e3mi.hip, e3mi_impl.h, convr.hip, gen.cpp, builder.*): {h}",
-                "# on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`, with $REPO the repository root and "
+                "# on an MI355X machine, after `cd /tmp && export TMPDIR=/tmp`, with $REPO the repository root and "
                 "$OUT a results directory:"] + ["#   " + c for c in cmds]
         with open(os.path.join(ROOT, "profiles", fname), "w") as fh:
             fh.write("\n".join(head + body) + "\n")
