@@ -179,10 +179,15 @@ __device__ __forceinline__ void rec_put(const RecStage& st, int nx, int npath, f
 __device__ __forceinline__ float rec_row(const RecArgs& a, ConstPtr<int> tab, int pair0, int p0, int p1,
                                          const float* Aj, const float* sX) {
   const int lane = threadIdx.x;
-  float z = 0.0f;
-#pragma unroll 2
-  for (int p = p0; p < p1; ++p) z = fmaf(Aj[p], sX[tab[a.o_pxl + pair0 + p] + lane], z);
-  return z;
+  // two independent partial sums, added in a fixed order
+  float z0 = 0.0f, z1 = 0.0f;
+  int p = p0;
+  for (; p + 2 <= p1; p += 2) {
+    z0 = fmaf(Aj[p], sX[tab[a.o_pxl + pair0 + p] + lane], z0);
+    z1 = fmaf(Aj[p + 1], sX[tab[a.o_pxl + pair0 + p + 1] + lane], z1);
+  }
+  if (p < p1) z0 = fmaf(Aj[p], sX[tab[a.o_pxl + pair0 + p] + lane], z0);
+  return z0 + z1;
 }
 
 template <int LSH>
@@ -324,13 +329,21 @@ __global__ __launch_bounds__(kWave) void k_convr_bwd(RecArgs a) {
         for (int xl = 0; xl < kRecX; ++xl) {
           if (xl < nx) {
             const int t0 = tab[ttab + xl], t1 = tab[ttab + xl + 1];
-            float t = 0.0f;
-#pragma unroll 2
-            for (int u = t0; u < t1; ++u) {
-              const int ent = tab[ttab + nx + 1 + u];
-              t = fmaf(Aj[ent & 0xffff], sW[(ent >> 16) * kWave + lane], t);
+            // four independent partial sums, added in a fixed order
+            float ta[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            int u = t0;
+            for (; u + 4 <= t1; u += 4) {
+#pragma unroll
+              for (int k = 0; k < 4; ++k) {
+                const int ent = tab[ttab + nx + 1 + u + k];
+                ta[k] = fmaf(Aj[ent & 0xffff], sW[(ent >> 16) * kWave + lane], ta[k]);
+              }
             }
-            float v[1] = {t};
+            for (; u < t1; ++u) {
+              const int ent = tab[ttab + nx + 1 + u];
+              ta[0] = fmaf(Aj[ent & 0xffff], sW[(ent >> 16) * kWave + lane], ta[0]);
+            }
+            float v[1] = {(ta[0] + ta[1]) + (ta[2] + ta[3])};
             if (act) bst<1, E3_T_STORE_AUX>(Tb, xl, v);
           }
         }
@@ -343,14 +356,22 @@ __global__ __launch_bounds__(kWave) void k_convr_bwd(RecArgs a) {
 #pragma unroll
       for (int i = 0; i < DSH; ++i) {
         const int u0 = tab[dytab + i], u1 = tab[dytab + i + 1];
-        float v = 0.0f;
-#pragma unroll 2
-        for (int u = u0; u < u1; ++u) {
+        float va[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        int u = u0;
+        for (; u + 4 <= u1; u += 4) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int ent = tab[dyent + 2 * (u + k)];
+            const float c = __int_as_float(tab[dyent + 2 * (u + k) + 1]);
+            va[k] = fmaf(c, sX[(ent & 0xff) * kWave + lane] * sW[(ent >> 8) * kWave + lane], va[k]);
+          }
+        }
+        for (; u < u1; ++u) {
           const int ent = tab[dyent + 2 * u];
           const float c = __int_as_float(tab[dyent + 2 * u + 1]);
-          v = fmaf(c, sX[(ent & 0xff) * kWave + lane] * sW[(ent >> 8) * kWave + lane], v);
+          va[0] = fmaf(c, sX[(ent & 0xff) * kWave + lane] * sW[(ent >> 8) * kWave + lane], va[0]);
         }
-        dyl[i] = v;
+        dyl[i] = (va[0] + va[1]) + (va[2] + va[3]);
       }
       const float tot = wave_reduce16(dyl, lane);
       if ((lane & 3) == 0) a.DY[(((int64_t)(eb + j) * a.ng + g) * a.nslab + sl) * 16 + (lane >> 2)] = tot;
