@@ -265,7 +265,9 @@ e3_status e3_conv_bwd_y(const e3_plan* plan, const e3_graph* graph, const float*
  * gdm by one sweep that forms the three forward terms together, and gx, gy,
  * gs by one sweep that forms the three backward terms together (one channel
  * per lane; a build with more runs three backward sweeps that store only the
- * cotangents used and add in place).  Deterministic.  ws as for e3_conv_bwd. */
+ * cotangents used and add in place).  The composed path runs both sweeps per
+ * x block, the record path three forward and three backward calls.
+ * Deterministic.  ws as for e3_conv_bwd. */
 e3_status e3_conv_bwd2(const e3_plan* plan, const e3_graph* graph, const float* x, const float* y,
                        const float* s, const float* dm, const float* ddx, const float* ddy, const float* dds,
                        float* gx, float* gy, float* gs, float* gdm, void* ws, size_t ws_bytes, e3_stream stream);
