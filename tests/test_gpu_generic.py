@@ -511,3 +511,46 @@ def test_generic_random_layouts(e3, seed):
         print("rel-L2", errs, flush=True)
         for k, v in errs.items():
             assert v < TOL, (path, k, v)
+
+
+@pytest.mark.parametrize("irreps,lsh,lout,parity", [
+    ("16x0e+16x1o", 2, 2, "all"), ("16x0e+16x1o+16x2e", 2, 2, "all"), ("16x0e+16x1o", 3, 3, "all"),
+    ("16x0e+16x1o+16x2e", 3, 3, "all"), ("16x0e+16x1o+16x2e+16x3o", 3, 3, "all"),
+    ("16x0e+16x1o", 2, 2, "natural"), ("16x0e+16x1o", 3, 3, "natural"), ("16x0e+16x1o+16x2e", 3, 3, "natural"),
+    ("16x0e+16x1o+16x2e+16x3o", 3, 3, "natural"), ("16x1o+16x0e+16x3o+16x2e", 3, 3, "all"),
+])
+def test_composed_equals_compiled_on_every_compiled_layout(e3, irreps, lsh, lout, parity):
+    """Every compiled layout forced onto the composed path: convolution forward,
+    backward and double backward, and the tensor product forward and backward,
+    agree with the compiled kernels to float32 rounding (the two sum in
+    different orders)."""
+    import torch
+    _say("composed vs compiled", irreps, lsh, lout, parity)
+    rng = np.random.default_rng(50)
+    lay = oirreps.layout(irreps, lsh, lout, parity=parity)
+    nat = parity == "natural"
+    cp = e3.Plan(irreps, lsh, lout, natural=nat)
+    kp = e3.Plan(irreps, lsh, lout, natural=nat, composed=True)
+    assert (cp.kernels, kp.kernels) == ("compiled", "composed")
+    n, e, R = 40, 500, 33
+    snd, rcv, vec = _random_graph(rng, n, e)
+    C = lay.channels
+    f = lambda *shape: to_dev(rng.standard_normal(shape).astype(np.float32))
+    x, vs, s, dm = f(n, lay.d_in, C), to_dev(vec), f(e, lay.n_paths, C), f(n, lay.d_out, C)
+    y, ddx, ddy, dds = f(e, lay.d_sh), f(n, lay.d_in, C), f(e, lay.d_sh), f(e, lay.n_paths, C)
+    tx, ty, tw, tdz = f(R, lay.d_in, C), f(R, lay.d_sh), f(R, lay.n_paths, C), f(R, lay.d_out, C)
+    G = e3.Graph(to_dev(snd), to_dev(rcv), n, pad_node=3)
+
+    def run(plan):
+        out = [e3.conv_fwd(plan, G, x, vs, s)]
+        out += list(e3.conv_bwd(plan, G, x, vs, s, dm))
+        out += list(e3.conv_bwd2(plan, G, x, y, s, dm, ddx, ddy, dds))
+        out += [e3.tp_fwd(plan, tx, ty, tw)]
+        out += list(e3.tp_bwd(plan, tx, ty, tw, tdz))
+        torch.cuda.synchronize()
+        return out
+
+    names = ["m", "dx", "dvec", "ds", "gx", "gy", "gs", "gdm", "z", "tdx", "tdy", "tdw"]
+    for name, a, b in zip(names, run(kp), run(cp)):
+        err = rel_l2(to_np(a), to_np(b))
+        assert err < 1e-6, (name, err)
