@@ -330,7 +330,7 @@ PROF_FILES = [  # file, kind, sections, title
     ("radial_water8k_hbm_bytes.txt", "hbm", ["radial"],
      "HBM byte counters per dispatch (FETCH_SIZE, WRITE_SIZE in KiB), scaled by a plain 2 GiB device copy; "
      "one counter per run"),
-    ("util_water8k_tp200k.txt", "util", ["conv", "linear", "radial", "tp"],
+    ("util_water8k_tp200k.txt", "util", ["conv", "linear", "radial", "tp", "bwd2", "generic"],
      "Per-kernel utilisation (rocprofv3 derived metrics, per dispatch, mean over dispatches)"),
 ]
 # kernel symbol -> short name used by the library's timing and the summaries
