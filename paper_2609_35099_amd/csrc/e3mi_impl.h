@@ -25,6 +25,19 @@
 #ifndef E3_FWD_ALOAD_PIN
 #define E3_FWD_ALOAD_PIN 1
 #endif
+// Three-term forward of the double backward: 1 runs the waves of two channel
+// slabs of one (receiver, group) in one workgroup, sharing the staged
+// pre-contractions (2.4% faster at equal batches); 0 gives every slab its own
+// workgroup.
+#ifndef E3_FWD3_PAIR
+#define E3_FWD3_PAIR 1
+#endif
+// Edges per staged batch of a slab pair (at most 64): 16 measured 3.7% faster
+// than 8 and 12, 24 and 32 slower (fewer workgroups fit the LDS).
+#ifndef E3_FWD3_BATCH2
+#define E3_FWD3_BATCH2 16
+#endif
+static_assert(E3_FWD3_BATCH2 >= 1 && E3_FWD3_BATCH2 <= 64, "one lane per edge of a batch");
 #if E3_FWD_ALOAD_PIN
 #define E3_FWD_PIN() __builtin_amdgcn_sched_barrier(0)
 #else
@@ -640,6 +653,8 @@ struct ConvArgs {
   const float* x2;
   const float* y2;
   const float* s2;
+  int sw;  // three-term forward: slab waves per workgroup (1, or 2 sharing the staged A and A2)
+  int fb;  // three-term forward: edges per staged batch
   // a single-block kind (V::RT) inside a larger layout: rows of the whole
   // layout per node of x / dx / T slot, per edge of s / ds, per node of m /
   // dm, and its harmonic-partial groups (all of them, and this block's first)
@@ -791,34 +806,39 @@ __global__ __launch_bounds__(kWave, E3_FWD_MIN_WAVES) void k_conv_fwd(ConvArgs a
 //   m[b] = sum_e s_e (A_e x2_src + A2_e x_src) + s2_e (A_e x_src),
 // A from the caller's harmonics y, A2 from their tangent y2; one channel per
 // lane, smaller edge batches (two pre-contractions per edge share the LDS).
+// With a.sw = 2 a workgroup holds the waves of two consecutive channel slabs of
+// one (receiver, group): they share the staged A and A2 of each batch, the
+// first wave forming A and the second A2.  A lone wave stages batches of
+// kEdgeBatch3 edges, a pair batches of E3_FWD3_BATCH2.
 constexpr int kEdgeBatch3 = 8;
 
 template <class V, int G>
 __device__ __forceinline__ void fwd3_task(const ConvArgs& a, int b, int sl, float* sA, float* sA2) {
   using F = typename V::template FG<G>;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   int ch0, lanes;
-  slab_of<1>(a.C, sl, ch0, lanes);
+  slab_of<1>(a.C, sl * a.sw + w, ch0, lanes);
   const bool act = lane < lanes;
   const int C = a.C, q = ch0 + lane;
   const int e0 = uniform(a.rowptr[b]), e1 = uniform(a.rowptr[b + 1]);
   float acc[F::NROW][1];
 #pragma unroll
   for (int i = 0; i < F::NROW; ++i) acc[i][0] = 0.0f;
-  for (int eb = e0; eb < e1; eb += kEdgeBatch3) {
-    const int n = imin(kEdgeBatch3, e1 - eb);
+  for (int eb = e0; eb < e1; eb += a.fb) {
+    const int n = imin(a.fb, e1 - eb);
     int my_e = 0, my_src = 0;
     if (lane < n) {
       my_e = a.eid[eb + lane];
       my_src = a.src[eb + lane];
-      float Y[V::D_SH], Yd[V::D_SH];
+      // a lone wave forms both pre-contractions; of a pair, wave w forms one
+      for (int k = a.sw == 1 ? 0 : w; k < 2; k += a.sw) {
+        const float* yk = k == 0 ? a.y : a.y2;
+        float Y[V::D_SH];
 #pragma unroll
-      for (int i = 0; i < V::D_SH; ++i) {
-        Y[i] = a.y[(int64_t)my_e * V::D_SH + i];
-        Yd[i] = a.y2[(int64_t)my_e * V::D_SH + i];
+        for (int i = 0; i < V::D_SH; ++i) Y[i] = yk[(int64_t)my_e * V::D_SH + i];
+        F::make_A(Y, (k == 0 ? sA : sA2) + lane * F::NA);
       }
-      F::make_A(Y, sA + lane * F::NA);
-      F::make_A(Yd, sA2 + lane * F::NA);
     }
     __syncthreads();
     if (act) {
@@ -866,14 +886,18 @@ __device__ __forceinline__ void fwd3_dispatch(const ConvArgs& a, int b, int g, i
   }
 }
 
+// a.nslab counts slab groups of a.sw slabs here; blockDim.x = a.sw * kWave;
+// dynamic LDS: fwd3_lds_bytes<V>(a)
 template <class V>
-__global__ __launch_bounds__(kWave, E3_FWD_MIN_WAVES) void k_conv_fwd3(ConvArgs a) {
-  __shared__ f4v smem[(2 * kEdgeBatch3 * V::MAX_NA_F + 3) / 4];
+__global__ __launch_bounds__(2 * kWave, E3_FWD_MIN_WAVES) void k_conv_fwd3(ConvArgs a) {
+  extern __shared__ __align__(16) float lds3[];
   int b, g, sl;
   if (!task_of<V::NFG>(a, b, g, sl)) return;
-  float* sA = reinterpret_cast<float*>(smem);
-  fwd3_dispatch<V, 0>(a, b, g, sl, sA, sA + kEdgeBatch3 * V::MAX_NA_F);
+  fwd3_dispatch<V, 0>(a, b, g, sl, lds3, lds3 + a.fb * V::MAX_NA_F);
 }
+
+template <class V>
+size_t fwd3_lds_bytes(const ConvArgs& a) { return (size_t)2 * a.fb * V::MAX_NA_F * sizeof(float); }
 
 template <class V, int G, int CPL, bool ACC>
 __device__ __forceinline__ void bwd_task(const ConvArgs& a, int b, int sl, float* sA, float* sY) {
@@ -2364,6 +2388,16 @@ e3_status run_fwd(const e3_plan* p, const e3_graph* g, const float* x, const flo
   return E3_OK;
 }
 
+// Slabs of the three-term forward: one channel per lane; the waves of two
+// consecutive slabs share a workgroup when there are two or more slabs (an odd
+// last slab's partner wave only forms A2).
+inline void fwd3_slabs(ConvArgs& a) {
+  const int nslab = (a.C + kWave - 1) / kWave;
+  a.sw = E3_FWD3_PAIR && nslab >= 2 ? 2 : 1;
+  a.nslab = (nslab + a.sw - 1) / a.sw;
+  a.fb = a.sw == 2 ? E3_FWD3_BATCH2 : kEdgeBatch3;
+}
+
 // The double backward's three forward terms in one launch (k_conv_fwd3):
 // m = conv(x2, y, s) + conv(x, y2, s) + conv(x, y, s2), overwritten.
 template <class V>
@@ -2371,12 +2405,12 @@ e3_status run_fwd3(const e3_plan* p, const e3_graph* g, const float* x, const fl
                    const float* y2, const float* s, const float* s2, float* m, hipStream_t st) {
   ConvArgs a = base_args(p, g);
   a.x = x, a.x2 = x2, a.y = y, a.y2 = y2, a.s = s, a.s2 = s2, a.m = m;
-  a.nslab = (a.C + kWave - 1) / kWave;  // one channel per lane
+  fwd3_slabs(a);
   if (g->n_nodes == 0) return E3_OK;
   const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
   {
     TimedLaunch t_("conv_fwd3", st);
-    hipLaunchKernelGGL((k_conv_fwd3<V>), dim3(grid), dim3(kWave), 0, st, a);
+    hipLaunchKernelGGL((k_conv_fwd3<V>), dim3(grid), dim3(a.sw * kWave), fwd3_lds_bytes<V>(a), st, a);
   }
   E3_HIP(hipGetLastError());
   return E3_OK;
@@ -2938,10 +2972,10 @@ e3_status kind_fwd3(const e3_plan* p, const e3_graph* g, const float* x, const f
   ConvArgs a = base_args(p, g);
   a.x = x, a.x2 = x2, a.y = y, a.y2 = y2, a.s = s, a.s2 = s2, a.m = m;
   a.xr = kc.xr, a.pr = kc.pr, a.orr = kc.orr;
-  a.nslab = (a.C + kWave - 1) / kWave;  // one channel per lane
+  fwd3_slabs(a);
   const unsigned grid = (unsigned)(kXcd * a.chunk * V::NFG * a.nslab);
   TimedLaunch t_("kind_fwd3", st);
-  hipLaunchKernelGGL((k_conv_fwd3<V>), dim3(grid), dim3(kWave), 0, st, a);
+  hipLaunchKernelGGL((k_conv_fwd3<V>), dim3(grid), dim3(a.sw * kWave), fwd3_lds_bytes<V>(a), st, a);
   E3_HIP(hipGetLastError());
   return E3_OK;
 }

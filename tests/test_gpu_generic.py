@@ -195,6 +195,7 @@ def test_generic_conv_y_accumulate_optional(e3, irreps, lsh, lout, parity, n, e,
 @pytest.mark.parametrize("irreps,lsh,lout,parity,n,e,pad", [
     ("16x0e+16x0o+16x1o+16x1e", 2, 2, "all", 30, 400, -1),
     ("32x2e+32x0e+32x1o", 3, 3, "all", 25, 300, 3),
+    ("132x1o+132x0e+132x2e", 2, 2, "all", 20, 250, -1),  # three channel slabs, the last of four channels
 ])
 def test_generic_conv_bwd2(e3, irreps, lsh, lout, parity, n, e, pad, path):
     """Double backward (three forward and three backward passes) against the

@@ -608,6 +608,7 @@ def test_conv_y_input_accumulate_and_optional_outputs(e3, irreps, lsh, lout, n, 
     ("128x0e+128x1o+128x2e+128x3o", 3, 3, 40, 700, 6),
     ("16x0e+16x1o+16x2e", 3, 3, 30, 400, -1),
     ("8x0e+8x1o", 2, 2, 20, 150, 2),
+    ("132x0e+132x1o", 2, 2, 25, 300, -1),  # three channel slabs, the last of four channels
 ])
 def test_conv_bwd2_random_graphs_full(e3, irreps, lsh, lout, n, e, pad):
     import torch
